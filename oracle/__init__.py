@@ -1,0 +1,45 @@
+"""Plain, slow fp64 CPU oracle of the SAS hot path.
+
+TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the benchmark's
+CPU-baseline leg may import or run anything here; the product path (the HIP
+library and its binding) never does, and this package imports nothing from
+the product package.  Every function computes the paper's definitions
+directly in float64 NumPy, rounding to the activation dtype only where the
+GPU path materialises a tensor in HBM.
+
+Sections and equations cited are those of the SAS paper (arXiv 2609.13141):
+standard attention (Eq. fula), block-sparse attention (Eq. spa), the Top-K
+block selection (Eq. selected_context), the normalized log gate
+(Eq. normalized_log_gate, Sec. 4.2.2), SAS attention (Eq. ours_train,
+Sec. 4.3), and the training/inference steps (Alg. 1, Alg. 2).
+
+Parity status of each part (how it is pinned by the oracle self-tests):
+
+* rounding ``rho``: pinned against torch's float32 -> bfloat16 conversion and
+  hand-derived ties (a direct fp64 -> bf16 rounding, not via float32).
+* RMSNorm, SiLU: pinned against torch.nn.functional.rms_norm / silu.
+* RoPE: pinned by invariants (pair norms, identity at position 0, scores
+  depending only on the relative position).
+* selector (block summaries, gate query, scores): the paper names the
+  selector but does not define its architecture; its arithmetic is pinned by
+  exact rational brute force and planted rankings.  The architecture itself
+  is "parity unpinned" by the paper (it is this build's reading).
+* normalized log gate, Top-K, attention: pinned by closed forms (q = 0),
+  V = const, reductions to textbook causal / block-local attention computed
+  by torch's scaled_dot_product_attention, causality, shift invariance and
+  the soft-reweighting identity of Eq. rank_unbounded.
+"""
+from .numerics import rho, round_bf16, round_f32, rmsnorm, rope, silu
+from .selector import (block_summaries, gate_query, selector_scores,
+                       normalized_log_gate, topk_blocks, select)
+from .attention import sas_attention
+from .layer import (Spec, layer_forward, mlp_forward, attention_prefill,
+                    DecodeCache, decode_step, embed_tokens, lm_head_argmax)
+
+__all__ = [
+    "rho", "round_bf16", "round_f32", "rmsnorm", "rope", "silu",
+    "block_summaries", "gate_query", "selector_scores", "normalized_log_gate",
+    "topk_blocks", "select", "sas_attention", "Spec", "layer_forward",
+    "mlp_forward", "attention_prefill", "DecodeCache", "decode_step",
+    "embed_tokens", "lm_head_argmax",
+]
