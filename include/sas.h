@@ -1,0 +1,237 @@
+/*
+ * sas.h -- C ABI of the SAS (Simple Attention Sparsification) hot path for
+ * AMD MI355X (gfx950).
+ *
+ * SAS (arXiv 2609.13141) splits the keys/values of every query into blocks of
+ * B tokens (Sec. 3, Eq. selected_context).  The block holding the query is
+ * the current block B_0 and is always attended with unit gate (Sec. 4.1).  A
+ * selector scores the earlier ("historical") blocks, the scores become
+ * normalized log gates log g = s - LSE(s) (Eq. normalized_log_gate), and the
+ * Top-K historical blocks are kept.  Training-time attention adds log g to
+ * the logits of the kept blocks (Eq. ours_train, Alg. 1); inference attends
+ * to the kept blocks without the gate (Alg. 2).  The paper's serving
+ * pipeline prefills densely and decodes block-sparsely (Sec. 5.1).
+ *
+ * Selector (the paper names one but does not define its architecture; this
+ * library's reading, shared with its checker): block summary = mean of the
+ * block's post-RoPE keys, gate query = sum of the group's query heads, both
+ * optionally projected by per-group [dh, dh] matrices, score = exact dot
+ * product (fp64) scaled by 1/(G*sqrt(dh)).  Top-K ranks the exact score,
+ * ties to the lower block index, so selected indices are exact integers.
+ *
+ * Conventions shared by every entry point:
+ *  - All tensor pointers are caller-owned DEVICE memory, row-major and
+ *    contiguous, 16-byte aligned; nothing is allocated by the library.
+ *    Scratch memory comes from `ws` (size from sas_workspace_size).
+ *  - Activations and weights share one dtype (SAS_F32 or SAS_BF16 storage);
+ *    statistics are fp32, indices int32.  Accumulation is fp32; selector
+ *    arithmetic is fp64.
+ *  - Linear weights use the nn.Linear layout [out, in]; no biases.  Query
+ *    head h reads KV head h / G with G = n_heads / n_kv_heads.
+ *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = default
+ *    stream).  SAS_OK means "enqueued"; device faults surface at the
+ *    caller's next synchronisation.
+ *  - On any error nothing is enqueued, outputs are untouched and
+ *    sas_last_error() returns a message (thread-local).
+ *  - Optional outputs may be NULL; their writes are skipped.
+ */
+#ifndef SAS_H
+#define SAS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SAS_OK = 0,
+  SAS_ERR_INVALID_ARGUMENT = -1, /* bad pointer, shape or config */
+  SAS_ERR_UNSUPPORTED = -2,      /* valid but not implemented (e.g. head_dim 96) */
+  SAS_ERR_WORKSPACE = -3,        /* ws NULL or smaller than sas_workspace_size */
+  SAS_ERR_HIP = -4               /* a HIP launch or runtime call failed */
+} sas_status;
+
+typedef enum { SAS_F32 = 0, SAS_BF16 = 1 } sas_dtype;
+
+/* Attention of the prefill entry points.
+ *  DENSE : causal softmax attention over all earlier tokens (Eq. fula).
+ *  SPARSE: current block + the Top-K historical blocks, no bias (Alg. 2).
+ *  GATED : same set; every token of a kept historical block m carries the
+ *          bias log g_m, the current block carries 0 (Eq. ours_train). */
+typedef enum { SAS_MODE_DENSE = 0, SAS_MODE_SPARSE = 1, SAS_MODE_GATED = 2 } sas_mode;
+
+/* Operation codes for sas_workspace_size. */
+typedef enum {
+  SAS_OP_ATTENTION = 0, /* sas_attention_prefill: batch, seq_len */
+  SAS_OP_MLP = 1,       /* sas_mlp_forward: batch = tokens, seq_len ignored */
+  SAS_OP_LAYER = 2,     /* sas_layer_forward: batch, seq_len */
+  SAS_OP_DECODE = 3,    /* sas_decode_step: batch, seq_len = max context */
+  SAS_OP_LM_HEAD = 4    /* sas_lm_head_argmax: batch, seq_len = vocab */
+} sas_op;
+
+typedef struct {
+  int32_t d_model;
+  int32_t n_heads;
+  int32_t n_kv_heads;  /* n_heads % n_kv_heads == 0 */
+  int32_t head_dim;    /* 64 or 128 */
+  int32_t d_ff;
+  int32_t block_size;  /* B, tokens per SAS block: 16, 32, 64 or 128 */
+  int32_t top_k;       /* K, historical blocks kept per query, 0..64 */
+  float rope_base;     /* rotary base (rotate-half pairing i, i + head_dim/2) */
+  float rms_eps;       /* RMSNorm epsilon */
+  float sm_scale;      /* attention scale; <= 0 selects 1/sqrt(head_dim) */
+  int32_t dtype;       /* sas_dtype */
+  int32_t mode;        /* sas_mode (prefill only; decode always uses SPARSE) */
+} sas_config;
+
+/* Attention inputs (post-RoPE), the paper's problem statement (Alg. 1/2):
+ * q [b, n, H, dh], k and v [b, n, Hkv, dh]; optional selector projections
+ * w_gq, w_gk [Hkv, dh, dh] ([out, in] per group; NULL = identity). */
+typedef struct {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* w_gq;
+  const void* w_gk;
+} sas_attn_in;
+
+/* Attention outputs.  NB = ceil(n / B).
+ *  o         [b, n, H, dh]   attention output (activation dtype)
+ *  lse       [b, H, n]       fp32 natural-log sum of exp of the biased,
+ *                            scaled logits over the attended set (optional)
+ *  k_summary [b, Hkv, NB, dh] selector key summary of every complete block
+ *                            (after w_gk); incomplete-block rows are zero
+ *                            (optional)
+ *  sel_idx   [b, Hkv, n, K]  int32 kept historical blocks, ascending, -1
+ *                            padded (optional)
+ *  log_gate  [b, Hkv, n, NB] fp32 log g of every historical block of every
+ *                            query, -inf where m >= floor(t / B) (optional)
+ *  tau       [b, Hkv, n]     fp32 log gate of the lowest-ranked kept block
+ *                            when floor(t/B) > K >= 1, +inf when K = 0 <
+ *                            floor(t/B), -inf otherwise (optional)
+ * The selector outputs are produced in every mode when requested; in DENSE
+ * mode they do not influence attention. */
+typedef struct {
+  void* o;
+  float* lse;
+  void* k_summary;
+  int32_t* sel_idx;
+  float* log_gate;
+  float* tau;
+} sas_attn_out;
+
+/* Decoder-layer weights (activation dtype).  rms1/rms2 [d]; wq [H*dh, d];
+ * wk, wv [Hkv*dh, d]; wo [d, H*dh]; w_gate, w_up [d_ff, d]; w_down [d, d_ff];
+ * w_gq, w_gk [Hkv, dh, dh] or NULL. */
+typedef struct {
+  const void* rms1;
+  const void* wq;
+  const void* wk;
+  const void* wv;
+  const void* wo;
+  const void* rms2;
+  const void* w_gate;
+  const void* w_up;
+  const void* w_down;
+  const void* w_gq;
+  const void* w_gk;
+} sas_layer_weights;
+
+/* Optional intermediate taps of sas_layer_forward (any field may be NULL):
+ * q [b,n,H,dh], k, v [b,n,Hkv,dh] after RoPE, h1 = x + attention [b,n,d]. */
+typedef struct {
+  void* q;
+  void* k;
+  void* v;
+  void* h1;
+} sas_layer_taps;
+
+/* Paged KV cache of one layer (Sec. 5.1's serving setting).
+ *  k_pages, v_pages [num_pages, Hkv, page_size, dh] (activation dtype)
+ *  block_table      [b, max_pages_per_seq] int32 page ids; logical
+ *                   position p of sequence i lives in page
+ *                   block_table[i][p / page_size], slot p % page_size
+ *  k_summary        [b, Hkv, max_blocks, dh] selector key summaries of the
+ *                   complete SAS blocks (after w_gk)
+ *  block_size must be a multiple of page_size. */
+typedef struct {
+  void* k_pages;
+  void* v_pages;
+  const int32_t* block_table;
+  void* k_summary;
+  int32_t num_pages;
+  int32_t page_size;
+  int32_t max_pages_per_seq;
+  int32_t max_blocks;
+} sas_paged_kv;
+
+/* Bytes of scratch memory an entry point needs (0 on invalid config). */
+size_t sas_workspace_size(const sas_config* cfg, int32_t op, int32_t batch, int32_t seq_len);
+
+/* Selector + SAS attention over given Q/K/V (Alg. 1 lines 1-4 / Alg. 2
+ * lines 1-4 applied to every query of a causal prefill; App. E forward).
+ * batch >= 1, seq_len >= 1. out->o is required. */
+sas_status sas_attention_prefill(const sas_config* cfg, int32_t batch, int32_t seq_len,
+                                 const sas_attn_in* in, sas_attn_out* out,
+                                 void* ws, size_t ws_bytes, void* stream);
+
+/* y = x + SwiGLU(RMSNorm(x)) for `tokens` rows of width d_model:
+ * u = RMSNorm(x) * rms2; a = silu(u W_gate^T) * (u W_up^T); y = x + a W_down^T.
+ * SAS defines nothing on the MLP; it is the layer's dense remainder. */
+sas_status sas_mlp_forward(const sas_config* cfg, int32_t tokens, const void* x,
+                           const sas_layer_weights* w, void* y,
+                           void* ws, size_t ws_bytes, void* stream);
+
+/* One pre-norm decoder layer over x [b, n, d] -> y [b, n, d]:
+ * u1 = RMSNorm(x); Q,K,V = RoPE(u1 W^T); SAS attention (cfg->mode);
+ * h1 = x + O W_o^T; y = h1 + SwiGLU(RMSNorm(h1)).
+ * stats: optional attention outputs (o, lse, selector outputs); taps:
+ * optional intermediates; cache: when non-NULL, K/V of positions 0..n-1 are
+ * written to the pages of every sequence and the summaries of the complete
+ * blocks to cache->k_summary (the dense-prefill half of Sec. 5.1). */
+sas_status sas_layer_forward(const sas_config* cfg, int32_t batch, int32_t seq_len,
+                             const void* x, const sas_layer_weights* w, void* y,
+                             sas_attn_out* stats, sas_layer_taps* taps,
+                             sas_paged_kv* cache, void* ws, size_t ws_bytes, void* stream);
+
+/* One SAS decode step of one layer (Alg. 2) for `batch` sequences:
+ * x [b, d] is the new token's hidden state at position pos[i] (DEVICE int32
+ * array; the cache must hold positions 0..pos[i]-1 and have room for
+ * pos[i]).  Appends K/V at pos[i]; when pos[i]+1 is a multiple of B the
+ * block's summary is written; scores the summaries of the floor(pos/B)
+ * complete blocks, keeps the Top-K per KV group and attends to them plus the
+ * current block without gate bias.  y [b, d]; sel_idx [b, Hkv, K] optional.
+ * Positions outside the cache are skipped by the kernels (no write). */
+sas_status sas_decode_step(const sas_config* cfg, int32_t batch, const void* x,
+                           const int32_t* pos, const sas_layer_weights* w,
+                           sas_paged_kv* cache, void* y, int32_t* sel_idx,
+                           void* ws, size_t ws_bytes, void* stream);
+
+/* Token embedding for the model ends: x [b, n, d] = table[ids] for ids >= 0;
+ * an id < 0 marks an image slot, filled with the next row of
+ * img_embed [b, n_img, d] (n_img = number of negative ids in each row;
+ * img_embed may be NULL only when there are none). ids is DEVICE memory. */
+sas_status sas_embed(const sas_config* cfg, int32_t batch, int32_t seq_len, const int32_t* ids,
+                     const void* table, int32_t vocab, const void* img_embed, int32_t n_img,
+                     void* x, void* stream);
+
+/* Greedy next token: logits = RMSNorm(h) W_lm^T (fp32 accumulation),
+ * tokens[i] = argmax, lowest id on ties.  h [b, d]; gamma [d];
+ * w_lm [vocab, d]; logits [b, vocab] fp32 optional; tokens [b] int32. */
+sas_status sas_lm_head_argmax(const sas_config* cfg, int32_t batch, const void* h,
+                              const void* gamma, const void* w_lm, int32_t vocab,
+                              float* logits, int32_t* tokens,
+                              void* ws, size_t ws_bytes, void* stream);
+
+/* Message describing the last non-OK status on this thread ("" if none). */
+const char* sas_last_error(void);
+
+/* Library version string. */
+const char* sas_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SAS_H */

@@ -1,0 +1,429 @@
+// C ABI of the SAS hot path: argument validation, workspace planning and the
+// kernel sequence of every entry point.  No allocation happens here; all
+// scratch comes from the caller's workspace.
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "../../include/sas.h"
+#include "kernels.h"
+
+using namespace sas;
+
+namespace {
+
+thread_local std::string g_err;
+
+sas_status fail(sas_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+sas_status hip_check(hipError_t e, const char* what) {
+  if (e == hipSuccess) return SAS_OK;
+  return fail(SAS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define SAS_TRY(expr)                         \
+  do {                                        \
+    sas_status _st = (expr);                  \
+    if (_st != SAS_OK) return _st;            \
+  } while (0)
+#define HIP_TRY(expr, what) SAS_TRY(hip_check((expr), (what)))
+
+size_t act_bytes(const sas_config* c) { return c->dtype == SAS_BF16 ? 2 : 4; }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+sas_status check_ptr(const void* p, const char* name, bool required) {
+  if (!p) return required ? fail(SAS_ERR_INVALID_ARGUMENT, "%s is NULL", name) : SAS_OK;
+  if (!aligned16(p)) return fail(SAS_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", name);
+  return SAS_OK;
+}
+
+sas_status check_config(const sas_config* c, bool need_mlp) {
+  if (!c) return fail(SAS_ERR_INVALID_ARGUMENT, "config is NULL");
+  if (c->dtype != SAS_F32 && c->dtype != SAS_BF16)
+    return fail(SAS_ERR_INVALID_ARGUMENT, "dtype %d is not SAS_F32 or SAS_BF16", c->dtype);
+  if (c->mode < SAS_MODE_DENSE || c->mode > SAS_MODE_GATED)
+    return fail(SAS_ERR_INVALID_ARGUMENT, "mode %d is not DENSE, SPARSE or GATED", c->mode);
+  if (c->n_heads <= 0 || c->n_kv_heads <= 0 || c->n_heads % c->n_kv_heads != 0)
+    return fail(SAS_ERR_INVALID_ARGUMENT, "n_heads %d must be a positive multiple of n_kv_heads %d",
+                c->n_heads, c->n_kv_heads);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(SAS_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", c->head_dim);
+  if (c->block_size != 16 && c->block_size != 32 && c->block_size != 64 && c->block_size != 128)
+    return fail(SAS_ERR_UNSUPPORTED, "block_size %d (supported: 16, 32, 64, 128)", c->block_size);
+  if (c->top_k < 0) return fail(SAS_ERR_INVALID_ARGUMENT, "top_k %d is negative", c->top_k);
+  if (c->top_k > 32) return fail(SAS_ERR_UNSUPPORTED, "top_k %d (supported: 0..32)", c->top_k);
+  if (need_mlp) {
+    if (c->d_model <= 0 || c->d_ff <= 0)
+      return fail(SAS_ERR_INVALID_ARGUMENT, "d_model %d and d_ff %d must be positive", c->d_model, c->d_ff);
+    if (c->d_model % 8 || c->d_ff % 8)
+      return fail(SAS_ERR_UNSUPPORTED, "d_model %d and d_ff %d must be multiples of 8", c->d_model, c->d_ff);
+    if (!(c->rms_eps >= 0.f)) return fail(SAS_ERR_INVALID_ARGUMENT, "rms_eps must be >= 0");
+    if (!(c->rope_base > 0.f)) return fail(SAS_ERR_INVALID_ARGUMENT, "rope_base must be > 0");
+  }
+  return SAS_OK;
+}
+
+float sm_scale_of(const sas_config* c) {
+  return c->sm_scale > 0.f ? c->sm_scale : 1.0f / sqrtf((float)c->head_dim);
+}
+
+// Bump allocator over the caller's workspace (offsets aligned to 256 bytes).
+struct Carve {
+  char* base;
+  size_t off = 0;
+  explicit Carve(void* b) : base((char*)b) {}
+  void* take(size_t bytes) {
+    void* p = base ? base + off : nullptr;
+    off += align_up(bytes, 256);
+    return p;
+  }
+};
+
+struct AttnWs {
+  void* kplain;
+  void* ksum;
+  int32_t* sel;
+  float* sel_bias;
+};
+
+AttnWs carve_attention(Carve& cv, const sas_config* c, int b, int n) {
+  const size_t ab = act_bytes(c);
+  const int NB = cdiv(n, c->block_size);
+  const size_t kb = (size_t)b * c->n_kv_heads * NB * c->head_dim * ab;
+  const size_t rows = (size_t)b * c->n_kv_heads * n * (size_t)(c->top_k > 0 ? c->top_k : 1);
+  AttnWs w;
+  w.kplain = cv.take(kb);
+  w.ksum = cv.take(kb);
+  w.sel = (int32_t*)cv.take(rows * 4);
+  w.sel_bias = (float*)cv.take(rows * 4);
+  return w;
+}
+
+struct MlpWs {
+  void* u2;
+  void* a;
+};
+
+MlpWs carve_mlp(Carve& cv, const sas_config* c, size_t T) {
+  const size_t ab = act_bytes(c);
+  MlpWs w;
+  w.u2 = cv.take(T * c->d_model * ab);
+  w.a = cv.take(T * c->d_ff * ab);
+  return w;
+}
+
+struct LayerWs {
+  void* u1;
+  float2* rope;
+  void* q;
+  void* k;
+  void* v;
+  void* o;
+  float* lse;
+  void* h1;
+  AttnWs att;
+  MlpWs mlp;
+};
+
+LayerWs carve_layer(Carve& cv, const sas_config* c, int b, int n) {
+  const size_t ab = act_bytes(c);
+  const size_t T = (size_t)b * n;
+  const size_t H = c->n_heads, Hkv = c->n_kv_heads, dh = c->head_dim;
+  LayerWs w;
+  w.u1 = cv.take(T * c->d_model * ab);
+  w.rope = (float2*)cv.take((size_t)n * (dh / 2) * sizeof(float2));
+  w.q = cv.take(T * H * dh * ab);
+  w.k = cv.take(T * Hkv * dh * ab);
+  w.v = cv.take(T * Hkv * dh * ab);
+  w.o = cv.take(T * H * dh * ab);
+  w.lse = (float*)cv.take(T * H * 4);
+  w.h1 = cv.take(T * c->d_model * ab);
+  w.att = carve_attention(cv, c, b, n);
+  w.mlp = carve_mlp(cv, c, T);
+  return w;
+}
+
+// Selector + attention given Q/K/V already in device memory.
+sas_status run_attention(const sas_config* c, int b, int n, const void* q, const void* k, const void* v,
+                         const void* w_gq, const void* w_gk, void* o, float* lse, void* k_summary,
+                         int32_t* sel_idx, float* log_gate, float* tau, const AttnWs& ws,
+                         hipStream_t s) {
+  const int NB = cdiv(n, c->block_size);
+  const int H = c->n_heads, Hkv = c->n_kv_heads, dh = c->head_dim;
+  const bool need_sel = c->mode != SAS_MODE_DENSE || sel_idx || log_gate || tau || k_summary;
+  void* ksum = k_summary ? k_summary : ws.ksum;
+  int32_t* sel = sel_idx ? sel_idx : ws.sel;
+  if (need_sel) {
+    HIP_TRY(launch_block_summaries(c->dtype, k, b, n, Hkv, dh, c->block_size, w_gk, ws.kplain, ksum, s),
+            "block summaries");
+    SelectArgs sa;
+    sa.b = b;
+    sa.n = n;
+    sa.H = H;
+    sa.Hkv = Hkv;
+    sa.dh = dh;
+    sa.B = c->block_size;
+    sa.K = c->top_k;
+    sa.NB = NB;
+    sa.Q = q;
+    sa.kbar = ksum;
+    sa.w_gq = w_gq;
+    sa.sel = sel;
+    sa.sel_bias = ws.sel_bias;
+    sa.log_gate = log_gate;
+    sa.tau = tau;
+    HIP_TRY(launch_select(c->dtype, sa, s), "select");
+  }
+  AttnArgs aa;
+  aa.b = b;
+  aa.n = n;
+  aa.H = H;
+  aa.Hkv = Hkv;
+  aa.dh = dh;
+  aa.B = c->block_size;
+  aa.K = c->top_k;
+  aa.mode = c->mode;
+  aa.sm_scale = sm_scale_of(c);
+  aa.Q = q;
+  aa.Kt = k;
+  aa.V = v;
+  aa.sel = sel;
+  aa.sel_bias = ws.sel_bias;
+  aa.O = o;
+  aa.lse = lse;
+  HIP_TRY(launch_attention(c->dtype, aa, s), "attention");
+  return SAS_OK;
+}
+
+sas_status run_mlp(const sas_config* c, size_t T, const void* x, const sas_layer_weights* w, void* y,
+                   const MlpWs& ws, hipStream_t s) {
+  HIP_TRY(launch_rmsnorm(c->dtype, x, w->rms2, ws.u2, (int)T, c->d_model, c->rms_eps, s), "rmsnorm");
+  GemmArgs g = {};
+  g.epi = EPI_SWIGLU;
+  g.M = (int)T;
+  g.K = c->d_model;
+  g.A = ws.u2;
+  g.B0 = w->w_gate;
+  g.B1 = w->w_up;
+  g.N = c->d_ff;
+  g.out = ws.a;
+  HIP_TRY(launch_gemm(c->dtype, g, s), "gate/up gemm");
+  GemmArgs d = {};
+  d.epi = EPI_RESID;
+  d.M = (int)T;
+  d.K = c->d_ff;
+  d.A = ws.a;
+  d.B0 = w->w_down;
+  d.N = c->d_model;
+  d.resid = x;
+  d.out = y;
+  HIP_TRY(launch_gemm(c->dtype, d, s), "down gemm");
+  return SAS_OK;
+}
+
+sas_status check_weights(const sas_layer_weights* w, bool attn, bool mlp) {
+  if (!w) return fail(SAS_ERR_INVALID_ARGUMENT, "weights is NULL");
+  if (attn) {
+    SAS_TRY(check_ptr(w->rms1, "w.rms1", true));
+    SAS_TRY(check_ptr(w->wq, "w.wq", true));
+    SAS_TRY(check_ptr(w->wk, "w.wk", true));
+    SAS_TRY(check_ptr(w->wv, "w.wv", true));
+    SAS_TRY(check_ptr(w->wo, "w.wo", true));
+    SAS_TRY(check_ptr(w->w_gq, "w.w_gq", false));
+    SAS_TRY(check_ptr(w->w_gk, "w.w_gk", false));
+  }
+  if (mlp) {
+    SAS_TRY(check_ptr(w->rms2, "w.rms2", true));
+    SAS_TRY(check_ptr(w->w_gate, "w.w_gate", true));
+    SAS_TRY(check_ptr(w->w_up, "w.w_up", true));
+    SAS_TRY(check_ptr(w->w_down, "w.w_down", true));
+  }
+  return SAS_OK;
+}
+
+sas_status check_ws(void* ws, size_t ws_bytes, size_t need) {
+  if (need == 0) return SAS_OK;
+  if (!ws) return fail(SAS_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if (ws_bytes < need) return fail(SAS_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, need);
+  if (!aligned16(ws)) return fail(SAS_ERR_INVALID_ARGUMENT, "workspace is not 16-byte aligned");
+  return SAS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sas_last_error(void) { return g_err.c_str(); }
+
+const char* sas_version(void) { return "sas-mi355x 0.1 (gfx950)"; }
+
+size_t sas_workspace_size(const sas_config* c, int32_t op, int32_t batch, int32_t seq_len) {
+  if (!c || batch <= 0) return 0;
+  Carve cv(nullptr);
+  switch (op) {
+    case SAS_OP_ATTENTION:
+      if (seq_len <= 0 || check_config(c, false) != SAS_OK) return 0;
+      carve_attention(cv, c, batch, seq_len);
+      break;
+    case SAS_OP_MLP:
+      if (check_config(c, true) != SAS_OK) return 0;
+      carve_mlp(cv, c, (size_t)batch);
+      break;
+    case SAS_OP_LAYER:
+      if (seq_len <= 0 || check_config(c, true) != SAS_OK) return 0;
+      carve_layer(cv, c, batch, seq_len);
+      break;
+    default:
+      return 0;
+  }
+  g_err.clear();
+  return cv.off;
+}
+
+sas_status sas_attention_prefill(const sas_config* c, int32_t batch, int32_t seq_len, const sas_attn_in* in,
+                                 sas_attn_out* out, void* ws, size_t ws_bytes, void* stream) {
+  SAS_TRY(check_config(c, false));
+  if (batch <= 0 || seq_len <= 0)
+    return fail(SAS_ERR_INVALID_ARGUMENT, "batch %d and seq_len %d must be positive", batch, seq_len);
+  if (!in || !out) return fail(SAS_ERR_INVALID_ARGUMENT, "in/out is NULL");
+  SAS_TRY(check_ptr(in->q, "in.q", true));
+  SAS_TRY(check_ptr(in->k, "in.k", true));
+  SAS_TRY(check_ptr(in->v, "in.v", true));
+  SAS_TRY(check_ptr(in->w_gq, "in.w_gq", false));
+  SAS_TRY(check_ptr(in->w_gk, "in.w_gk", false));
+  SAS_TRY(check_ptr(out->o, "out.o", true));
+  SAS_TRY(check_ptr(out->lse, "out.lse", false));
+  SAS_TRY(check_ptr(out->k_summary, "out.k_summary", false));
+  SAS_TRY(check_ptr(out->sel_idx, "out.sel_idx", false));
+  SAS_TRY(check_ptr(out->log_gate, "out.log_gate", false));
+  SAS_TRY(check_ptr(out->tau, "out.tau", false));
+  Carve cv(ws);
+  AttnWs aw = carve_attention(cv, c, batch, seq_len);
+  SAS_TRY(check_ws(ws, ws_bytes, cv.off));
+  SAS_TRY(run_attention(c, batch, seq_len, in->q, in->k, in->v, in->w_gq, in->w_gk, out->o, out->lse,
+                        out->k_summary, out->sel_idx, out->log_gate, out->tau, aw, (hipStream_t)stream));
+  return SAS_OK;
+}
+
+sas_status sas_mlp_forward(const sas_config* c, int32_t tokens, const void* x, const sas_layer_weights* w,
+                           void* y, void* ws, size_t ws_bytes, void* stream) {
+  SAS_TRY(check_config(c, true));
+  if (tokens <= 0) return fail(SAS_ERR_INVALID_ARGUMENT, "tokens %d must be positive", tokens);
+  SAS_TRY(check_ptr(x, "x", true));
+  SAS_TRY(check_ptr(y, "y", true));
+  SAS_TRY(check_weights(w, false, true));
+  Carve cv(ws);
+  MlpWs mw = carve_mlp(cv, c, (size_t)tokens);
+  SAS_TRY(check_ws(ws, ws_bytes, cv.off));
+  return run_mlp(c, (size_t)tokens, x, w, y, mw, (hipStream_t)stream);
+}
+
+sas_status sas_layer_forward(const sas_config* c, int32_t batch, int32_t seq_len, const void* x,
+                             const sas_layer_weights* w, void* y, sas_attn_out* stats, sas_layer_taps* taps,
+                             sas_paged_kv* cache, void* ws, size_t ws_bytes, void* stream) {
+  SAS_TRY(check_config(c, true));
+  if (batch <= 0 || seq_len <= 0)
+    return fail(SAS_ERR_INVALID_ARGUMENT, "batch %d and seq_len %d must be positive", batch, seq_len);
+  SAS_TRY(check_ptr(x, "x", true));
+  SAS_TRY(check_ptr(y, "y", true));
+  SAS_TRY(check_weights(w, true, true));
+  sas_attn_out st = {};
+  if (stats) {
+    st = *stats;
+    SAS_TRY(check_ptr(st.o, "stats.o", false));
+    SAS_TRY(check_ptr(st.lse, "stats.lse", false));
+    SAS_TRY(check_ptr(st.k_summary, "stats.k_summary", false));
+    SAS_TRY(check_ptr(st.sel_idx, "stats.sel_idx", false));
+    SAS_TRY(check_ptr(st.log_gate, "stats.log_gate", false));
+    SAS_TRY(check_ptr(st.tau, "stats.tau", false));
+  }
+  sas_layer_taps tp = {};
+  if (taps) {
+    tp = *taps;
+    SAS_TRY(check_ptr(tp.q, "taps.q", false));
+    SAS_TRY(check_ptr(tp.k, "taps.k", false));
+    SAS_TRY(check_ptr(tp.v, "taps.v", false));
+    SAS_TRY(check_ptr(tp.h1, "taps.h1", false));
+  }
+  if (cache) return fail(SAS_ERR_UNSUPPORTED, "paged cache fill is not available yet");
+  Carve cv(ws);
+  LayerWs lw = carve_layer(cv, c, batch, seq_len);
+  SAS_TRY(check_ws(ws, ws_bytes, cv.off));
+  hipStream_t s = (hipStream_t)stream;
+  const size_t T = (size_t)batch * seq_len;
+  void* q = tp.q ? tp.q : lw.q;
+  void* k = tp.k ? tp.k : lw.k;
+  void* v = tp.v ? tp.v : lw.v;
+  void* o = st.o ? st.o : lw.o;
+  void* h1 = tp.h1 ? tp.h1 : lw.h1;
+
+  HIP_TRY(launch_rope_table(lw.rope, seq_len, c->head_dim, c->rope_base, s), "rope table");
+  HIP_TRY(launch_rmsnorm(c->dtype, x, w->rms1, lw.u1, (int)T, c->d_model, c->rms_eps, s), "rmsnorm");
+  GemmArgs g = {};
+  g.epi = EPI_QKV_ROPE;
+  g.M = (int)T;
+  g.K = c->d_model;
+  g.A = lw.u1;
+  g.B0 = w->wq;
+  g.B1 = w->wk;
+  g.B2 = w->wv;
+  g.N = (c->n_heads + 2 * c->n_kv_heads) * c->head_dim;
+  g.out = q;
+  g.out1 = k;
+  g.out2 = v;
+  g.n_heads = c->n_heads;
+  g.n_kv_heads = c->n_kv_heads;
+  g.head_dim = c->head_dim;
+  g.seq_len = seq_len;
+  g.rope = lw.rope;
+  HIP_TRY(launch_gemm(c->dtype, g, s), "qkv gemm");
+  SAS_TRY(run_attention(c, batch, seq_len, q, k, v, w->w_gq, w->w_gk, o, st.lse, st.k_summary, st.sel_idx,
+                        st.log_gate, st.tau, lw.att, s));
+  GemmArgs og = {};
+  og.epi = EPI_RESID;
+  og.M = (int)T;
+  og.K = c->n_heads * c->head_dim;
+  og.A = o;
+  og.B0 = w->wo;
+  og.N = c->d_model;
+  og.resid = x;
+  og.out = h1;
+  HIP_TRY(launch_gemm(c->dtype, og, s), "o-proj gemm");
+  return run_mlp(c, T, h1, w, y, lw.mlp, s);
+}
+
+sas_status sas_decode_step(const sas_config* c, int32_t batch, const void* x, const int32_t* pos,
+                           const sas_layer_weights* w, sas_paged_kv* cache, void* y, int32_t* sel_idx, void* ws,
+                           size_t ws_bytes, void* stream) {
+  (void)c; (void)batch; (void)x; (void)pos; (void)w; (void)cache; (void)y; (void)sel_idx; (void)ws;
+  (void)ws_bytes; (void)stream;
+  return fail(SAS_ERR_UNSUPPORTED, "sas_decode_step is not available yet");
+}
+
+sas_status sas_embed(const sas_config* c, int32_t batch, int32_t seq_len, const int32_t* ids, const void* table,
+                     int32_t vocab, const void* img_embed, int32_t n_img, void* x, void* stream) {
+  (void)c; (void)batch; (void)seq_len; (void)ids; (void)table; (void)vocab; (void)img_embed; (void)n_img;
+  (void)x; (void)stream;
+  return fail(SAS_ERR_UNSUPPORTED, "sas_embed is not available yet");
+}
+
+sas_status sas_lm_head_argmax(const sas_config* c, int32_t batch, const void* h, const void* gamma,
+                              const void* w_lm, int32_t vocab, float* logits, int32_t* tokens, void* ws,
+                              size_t ws_bytes, void* stream) {
+  (void)c; (void)batch; (void)h; (void)gamma; (void)w_lm; (void)vocab; (void)logits; (void)tokens; (void)ws;
+  (void)ws_bytes; (void)stream;
+  return fail(SAS_ERR_UNSUPPORTED, "sas_lm_head_argmax is not available yet");
+}
+
+}  // extern "C"

@@ -1,0 +1,78 @@
+// Device helpers shared by the SAS kernels (gfx950, wave64).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/sas.h"
+
+namespace sas {
+
+typedef uint16_t bf16_t;  // bfloat16 storage
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float floatx4_t;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16_t;
+
+constexpr int WAVE = 64;
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t h) {
+  return __uint_as_float(((uint32_t)h) << 16);
+}
+
+// float -> bfloat16, round to nearest even (finite inputs; NaN stays NaN).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u) return (bf16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+// double -> bfloat16 directly (one rounding, ties to even), including
+// subnormal results and overflow to infinity.
+__device__ __forceinline__ bf16_t f64_to_bf16(double d) {
+  uint64_t u = (uint64_t)__double_as_longlong(d);
+  uint32_t sign = (uint32_t)(u >> 48) & 0x8000u;
+  uint64_t a = u & 0x7fffffffffffffffull;
+  if (a >= 0x7ff0000000000000ull) {  // inf / nan
+    return (bf16_t)(sign | 0x7f80u | (a > 0x7ff0000000000000ull ? 0x40u : 0u));
+  }
+  double ad = __longlong_as_double((long long)a);
+  if (ad < 0x1p-126) {  // bfloat16 subnormal range: spacing 2^-133
+    double r = rint(ad * 0x1p133);  // <= 128, exact; 128 is the smallest normal
+    return (bf16_t)(sign | (uint32_t)r);
+  }
+  // keep 7 mantissa bits of the double: round at bit 45 (ties to even); a
+  // carry propagates into the exponent naturally
+  uint64_t r = (a + 0x00000fffffffffffull + ((a >> 45) & 1ull)) >> 45;
+  // r = (biased_exp_d << 7) | mant7 ; rebias 1023 -> 127
+  int64_t e = (int64_t)(r >> 7) - 1023 + 127;
+  if (e >= 255) return (bf16_t)(sign | 0x7f80u);
+  return (bf16_t)(sign | ((uint32_t)e << 7) | (uint32_t)(r & 0x7f));
+}
+
+template <typename T> struct Act;
+template <> struct Act<float> {
+  static __device__ __forceinline__ float load(const float* p, size_t i) { return p[i]; }
+  static __device__ __forceinline__ float to_f32(float v) { return v; }
+  static __device__ __forceinline__ float from_f32(float v) { return v; }
+  static __device__ __forceinline__ float from_f64(double v) { return (float)v; }
+};
+template <> struct Act<bf16_t> {
+  static __device__ __forceinline__ float load(const bf16_t* p, size_t i) { return bf16_to_f32(p[i]); }
+  static __device__ __forceinline__ float to_f32(bf16_t v) { return bf16_to_f32(v); }
+  static __device__ __forceinline__ bf16_t from_f32(float v) { return f32_to_bf16(v); }
+  static __device__ __forceinline__ bf16_t from_f64(double v) { return f64_to_bf16(v); }
+};
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+}  // namespace sas

@@ -1,0 +1,115 @@
+// Host-side launchers of the SAS kernels (one translation unit each).
+// Every launcher enqueues on `stream` and returns hipGetLastError().
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sas {
+
+inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ---- elementwise.hip -------------------------------------------------------
+// out[r, :] = x[r, :] / sqrt(mean(x[r, :]^2) + eps) * gamma   (fp32 math)
+hipError_t launch_rmsnorm(int dtype, const void* x, const void* gamma, void* out, int rows, int d,
+                          float eps, hipStream_t s);
+// rope[p, i] = (cos(p * theta_i), sin(p * theta_i)), theta_i = base^(-2i/dh),
+// for p in [0, n), i in [0, dh/2); computed in fp64, stored as float2.
+hipError_t launch_rope_table(float2* rope, int n, int dh, float base, hipStream_t s);
+
+// ---- gemm.hip --------------------------------------------------------------
+// C = A[M, K] * B[N, K]^T with one of three fused epilogues.
+enum GemmEpi { EPI_QKV_ROPE = 0, EPI_SWIGLU = 1, EPI_RESID = 2 };
+struct GemmArgs {
+  int epi;
+  int M, K;
+  const void* A;          // [M, K]
+  // EPI_RESID: B0 = W [N, K]; out[M, N] = resid + A W^T
+  // EPI_SWIGLU: B0 = W_gate, B1 = W_up [F, K]; out[M, F] = silu(A Wg^T) * (A Wu^T)
+  // EPI_QKV_ROPE: B0 = Wq [H*dh, K], B1 = Wk, B2 = Wv [Hkv*dh, K];
+  //   out = Q [M, H, dh], out1 = K, out2 = V [M, Hkv, dh]; RoPE on Q and K at
+  //   position (row % seq_len) from rope table [seq_len, dh/2] float2.
+  const void* B0;
+  const void* B1;
+  const void* B2;
+  int N;                  // RESID: N; SWIGLU: F; QKV: (H + 2 Hkv) * dh
+  const void* resid;      // RESID
+  void* out;
+  void* out1;
+  void* out2;
+  int n_heads, n_kv_heads, head_dim, seq_len;
+  const float2* rope;
+  const int32_t* row_pos; // optional per-row positions (decode), else row % seq_len
+};
+hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s);
+
+// ---- selector.hip ----------------------------------------------------------
+// Block summaries kbar[b, Hkv, NB, dh] of the complete blocks of K[b, n, Hkv, dh]
+// (mean, fp64 ascending sum, rounded once); incomplete rows zeroed.  When
+// w_gk is given the projected summary is written to `ksum` and the plain one
+// to `kplain` (scratch), otherwise `ksum` holds the plain summary.
+hipError_t launch_block_summaries(int dtype, const void* K, int b, int n, int Hkv, int dh, int B,
+                                  const void* w_gk, void* kplain, void* ksum, hipStream_t s);
+// Per (b, group, query) selection (Top-K, gate, tau) against kbar.
+struct SelectArgs {
+  int b, n, H, Hkv, dh, B, K, NB;
+  const void* Q;          // [b, n, H, dh]
+  const void* kbar;       // [b, Hkv, NB, dh]
+  const void* w_gq;       // [Hkv, dh, dh] or null
+  int32_t* sel;           // [b, Hkv, n, K] (required, scratch or user)
+  float* sel_bias;        // [b, Hkv, n, K] log g of each kept block (required)
+  float* log_gate;        // [b, Hkv, n, NB] optional
+  float* tau;             // [b, Hkv, n] optional
+};
+hipError_t launch_select(int dtype, const SelectArgs& a, hipStream_t s);
+
+// ---- attention.hip ---------------------------------------------------------
+struct AttnArgs {
+  int b, n, H, Hkv, dh, B, K, mode;
+  float sm_scale;
+  const void* Q;          // [b, n, H, dh]
+  const void* Kt;         // [b, n, Hkv, dh]
+  const void* V;          // [b, n, Hkv, dh]
+  const int32_t* sel;     // [b, Hkv, n, K] (unused in DENSE)
+  const float* sel_bias;  // [b, Hkv, n, K] (GATED)
+  void* O;                // [b, n, H, dh]
+  float* lse;             // [b, H, n] optional
+};
+hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
+
+// ---- decode.hip ------------------------------------------------------------
+struct DecodeArgs {
+  int b, H, Hkv, dh, B, K, d, F;
+  float sm_scale, eps, rope_base;
+  const int32_t* pos;
+  // paged cache
+  void* k_pages;
+  void* v_pages;
+  const int32_t* block_table;
+  void* k_summary;
+  int num_pages, page_size, max_pages, max_blocks;
+  const void* w_gq;
+  const void* w_gk;
+};
+// Writes K/V of positions 0..n-1 of every sequence into the pages and copies
+// the complete-block summaries into the summary cache.
+hipError_t launch_cache_fill(int dtype, const void* K, const void* V, const void* ksum, int b, int n,
+                             int Hkv, int dh, int B, int NB, const DecodeArgs& c, hipStream_t s);
+// q [b, H, dh], k/v [b, Hkv, dh] of the new tokens -> append + summary.
+hipError_t launch_kv_append(int dtype, const void* k, const void* v, const DecodeArgs& c,
+                            void* kplain_scratch, hipStream_t s);
+// Top-K per (seq, group) against the cached summaries -> sel [b, Hkv, K].
+hipError_t launch_decode_select(int dtype, const void* q, const DecodeArgs& c, int32_t* sel,
+                                hipStream_t s);
+// Sparse attention of the new tokens over current block + selected blocks.
+hipError_t launch_decode_attention(int dtype, const void* q, const DecodeArgs& c, const int32_t* sel,
+                                   float* part_ml, float* part_o, void* O, hipStream_t s);
+
+// ---- model_ends.hip --------------------------------------------------------
+hipError_t launch_embed(int dtype, int b, int n, const int32_t* ids, const void* table, int vocab,
+                        const void* img, int n_img, void* x, int d, hipStream_t s);
+hipError_t launch_lm_head(int dtype, int b, int d, const void* u, const void* w_lm, int vocab,
+                          float* logits, int32_t* tokens, float* part_val, int32_t* part_idx,
+                          hipStream_t s);
+
+}  // namespace sas

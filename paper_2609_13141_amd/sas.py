@@ -1,0 +1,256 @@
+"""ctypes binding of ``libsas.so`` (the C ABI declared in ``include/sas.h``).
+
+Argument marshalling only: torch tensors provide device memory and the
+current HIP stream; every computation runs in the library's HIP kernels.
+The library is loaded on first use; if it is missing or was built without a
+GPU target the call raises instead of computing anything another way.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+
+import torch
+
+from .configs import Workload
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsas.so")
+
+SAS_OK, SAS_ERR_INVALID_ARGUMENT, SAS_ERR_UNSUPPORTED, SAS_ERR_WORKSPACE, SAS_ERR_HIP = 0, -1, -2, -3, -4
+SAS_F32, SAS_BF16 = 0, 1
+MODES = {"dense": 0, "sparse": 1, "gated": 2}
+OP_ATTENTION, OP_MLP, OP_LAYER, OP_DECODE, OP_LM_HEAD = 0, 1, 2, 3, 4
+TORCH_DTYPE = {"bf16": torch.bfloat16, "f32": torch.float32}
+
+EXPORTS = ("sas_workspace_size", "sas_attention_prefill", "sas_mlp_forward", "sas_layer_forward",
+           "sas_decode_step", "sas_embed", "sas_lm_head_argmax", "sas_last_error", "sas_version")
+
+
+class SasError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"sas status {status}: {msg}")
+        self.status = status
+
+
+class Config(C.Structure):
+    _fields_ = [("d_model", C.c_int32), ("n_heads", C.c_int32), ("n_kv_heads", C.c_int32),
+                ("head_dim", C.c_int32), ("d_ff", C.c_int32), ("block_size", C.c_int32),
+                ("top_k", C.c_int32), ("rope_base", C.c_float), ("rms_eps", C.c_float),
+                ("sm_scale", C.c_float), ("dtype", C.c_int32), ("mode", C.c_int32)]
+
+
+class AttnIn(C.Structure):
+    _fields_ = [("q", C.c_void_p), ("k", C.c_void_p), ("v", C.c_void_p), ("w_gq", C.c_void_p),
+                ("w_gk", C.c_void_p)]
+
+
+class AttnOut(C.Structure):
+    _fields_ = [("o", C.c_void_p), ("lse", C.c_void_p), ("k_summary", C.c_void_p),
+                ("sel_idx", C.c_void_p), ("log_gate", C.c_void_p), ("tau", C.c_void_p)]
+
+
+class LayerWeights(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in ("rms1", "wq", "wk", "wv", "wo", "rms2", "w_gate", "w_up",
+                                          "w_down", "w_gq", "w_gk")]
+
+
+class LayerTaps(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in ("q", "k", "v", "h1")]
+
+
+class PagedKV(C.Structure):
+    _fields_ = [("k_pages", C.c_void_p), ("v_pages", C.c_void_p), ("block_table", C.c_void_p),
+                ("k_summary", C.c_void_p), ("num_pages", C.c_int32), ("page_size", C.c_int32),
+                ("max_pages_per_seq", C.c_int32), ("max_blocks", C.c_int32)]
+
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    """Load libsas.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_13141_amd.build`")
+    L = C.CDLL(LIB_PATH)
+    vp, i32, sz = C.c_void_p, C.c_int32, C.c_size_t
+    L.sas_workspace_size.restype = sz
+    L.sas_workspace_size.argtypes = [C.POINTER(Config), i32, i32, i32]
+    L.sas_attention_prefill.restype = i32
+    L.sas_attention_prefill.argtypes = [C.POINTER(Config), i32, i32, C.POINTER(AttnIn), C.POINTER(AttnOut),
+                                        vp, sz, vp]
+    L.sas_mlp_forward.restype = i32
+    L.sas_mlp_forward.argtypes = [C.POINTER(Config), i32, vp, C.POINTER(LayerWeights), vp, vp, sz, vp]
+    L.sas_layer_forward.restype = i32
+    L.sas_layer_forward.argtypes = [C.POINTER(Config), i32, i32, vp, C.POINTER(LayerWeights), vp,
+                                    C.POINTER(AttnOut), C.POINTER(LayerTaps), C.POINTER(PagedKV), vp, sz, vp]
+    L.sas_decode_step.restype = i32
+    L.sas_decode_step.argtypes = [C.POINTER(Config), i32, vp, vp, C.POINTER(LayerWeights), C.POINTER(PagedKV),
+                                  vp, vp, vp, sz, vp]
+    L.sas_embed.restype = i32
+    L.sas_embed.argtypes = [C.POINTER(Config), i32, i32, vp, vp, i32, vp, i32, vp, vp]
+    L.sas_lm_head_argmax.restype = i32
+    L.sas_lm_head_argmax.argtypes = [C.POINTER(Config), i32, vp, vp, vp, i32, vp, vp, vp, sz, vp]
+    L.sas_last_error.restype = C.c_char_p
+    L.sas_last_error.argtypes = []
+    L.sas_version.restype = C.c_char_p
+    L.sas_version.argtypes = []
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != SAS_OK:
+        raise SasError(status, lib().sas_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def make_config(w: Workload, mode: str | None = None, sm_scale: float = 0.0) -> Config:
+    return Config(w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.d_ff, w.block_size, w.top_k,
+                  w.rope_base, w.rms_eps, sm_scale, SAS_BF16 if w.dtype == "bf16" else SAS_F32,
+                  MODES[mode or w.mode])
+
+
+def workspace_size(cfg: Config, op: int, batch: int, seq_len: int) -> int:
+    return int(lib().sas_workspace_size(C.byref(cfg), op, batch, seq_len))
+
+
+class Workspace:
+    """Grow-only device scratch buffer reused across calls."""
+
+    def __init__(self, device="cuda"):
+        self.device = device
+        self.buf = None
+
+    def get(self, nbytes: int):
+        if nbytes == 0:
+            return None, 0
+        if self.buf is None or self.buf.numel() < nbytes:
+            self.buf = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        return self.buf, self.buf.numel()
+
+
+_default_ws: dict = {}
+
+
+def _ws(ws: Workspace | None, nbytes: int):
+    if ws is None:
+        dev = torch.cuda.current_device()
+        ws = _default_ws.setdefault(dev, Workspace(f"cuda:{dev}"))
+    buf, n = ws.get(nbytes)
+    return _ptr(buf), n
+
+
+def weights_struct(W: dict) -> LayerWeights:
+    return LayerWeights(*[_ptr(W.get(k)) for k in ("rms1", "wq", "wk", "wv", "wo", "rms2", "w_gate",
+                                                   "w_up", "w_down", "w_gq", "w_gk")])
+
+
+def attention_prefill(cfg: Config, q, k, v, w_gq=None, w_gk=None, *, lse=True, k_summary=True,
+                      sel_idx=True, log_gate=False, tau=False, ws: Workspace | None = None) -> dict:
+    """Selector + SAS attention.  q [b,n,H,dh], k/v [b,n,Hkv,dh] on the GPU."""
+    b, n, H, dh = q.shape
+    Hkv = k.shape[2]
+    B, K = cfg.block_size, cfg.top_k
+    NB = -(-n // B)
+    dev = q.device
+    out = {"o": torch.empty_like(q)}
+    if lse:
+        out["lse"] = torch.empty(b, H, n, dtype=torch.float32, device=dev)
+    if k_summary:
+        out["k_summary"] = torch.empty(b, Hkv, NB, dh, dtype=q.dtype, device=dev)
+    if sel_idx:
+        out["sel_idx"] = torch.empty(b, Hkv, n, K, dtype=torch.int32, device=dev)
+    if log_gate:
+        out["log_gate"] = torch.empty(b, Hkv, n, NB, dtype=torch.float32, device=dev)
+    if tau:
+        out["tau"] = torch.empty(b, Hkv, n, dtype=torch.float32, device=dev)
+    ain = AttnIn(_ptr(q), _ptr(k), _ptr(v), _ptr(w_gq), _ptr(w_gk))
+    aout = AttnOut(*[_ptr(out.get(f)) for f in ("o", "lse", "k_summary", "sel_idx", "log_gate", "tau")])
+    wsp, wsn = _ws(ws, workspace_size(cfg, OP_ATTENTION, b, n))
+    _check(lib().sas_attention_prefill(C.byref(cfg), b, n, C.byref(ain), C.byref(aout), wsp, wsn, _stream()))
+    return out
+
+
+def mlp_forward(cfg: Config, x, W: dict, ws: Workspace | None = None):
+    """y = x + SwiGLU(RMSNorm(x)); x [..., d]."""
+    T = x.numel() // x.shape[-1]
+    y = torch.empty_like(x)
+    wsp, wsn = _ws(ws, workspace_size(cfg, OP_MLP, T, 0))
+    _check(lib().sas_mlp_forward(C.byref(cfg), T, _ptr(x), C.byref(weights_struct(W)), _ptr(y), wsp, wsn,
+                                 _stream()))
+    return y
+
+
+@dataclass
+class PagedCache:
+    """Paged KV cache of one layer (device tensors)."""
+    k_pages: torch.Tensor
+    v_pages: torch.Tensor
+    block_table: torch.Tensor
+    k_summary: torch.Tensor
+    page_size: int
+
+    def struct(self) -> PagedKV:
+        return PagedKV(_ptr(self.k_pages), _ptr(self.v_pages), _ptr(self.block_table), _ptr(self.k_summary),
+                       self.k_pages.shape[0], self.page_size, self.block_table.shape[1],
+                       self.k_summary.shape[2])
+
+
+def layer_forward(cfg: Config, x, W: dict, *, stats: bool = True, lse=True, sel_idx=True, log_gate=False,
+                  tau=False, k_summary=False, taps: bool = False, cache: PagedCache | None = None,
+                  ws: Workspace | None = None) -> dict:
+    """One decoder layer over x [b, n, d]."""
+    b, n, d = x.shape
+    H, Hkv, dh, B, K = cfg.n_heads, cfg.n_kv_heads, cfg.head_dim, cfg.block_size, cfg.top_k
+    NB = -(-n // B)
+    dev = x.device
+    out = {"y": torch.empty_like(x)}
+    st = None
+    if stats:
+        out["o"] = torch.empty(b, n, H, dh, dtype=x.dtype, device=dev)
+        if lse:
+            out["lse"] = torch.empty(b, H, n, dtype=torch.float32, device=dev)
+        if sel_idx:
+            out["sel_idx"] = torch.empty(b, Hkv, n, K, dtype=torch.int32, device=dev)
+        if log_gate:
+            out["log_gate"] = torch.empty(b, Hkv, n, NB, dtype=torch.float32, device=dev)
+        if tau:
+            out["tau"] = torch.empty(b, Hkv, n, dtype=torch.float32, device=dev)
+        if k_summary:
+            out["k_summary"] = torch.empty(b, Hkv, NB, dh, dtype=x.dtype, device=dev)
+        st = AttnOut(*[_ptr(out.get(f)) for f in ("o", "lse", "k_summary", "sel_idx", "log_gate", "tau")])
+    tp = None
+    if taps:
+        out["q"] = torch.empty(b, n, H, dh, dtype=x.dtype, device=dev)
+        out["k"] = torch.empty(b, n, Hkv, dh, dtype=x.dtype, device=dev)
+        out["v"] = torch.empty(b, n, Hkv, dh, dtype=x.dtype, device=dev)
+        out["h1"] = torch.empty_like(x)
+        tp = LayerTaps(*[_ptr(out[f]) for f in ("q", "k", "v", "h1")])
+    cs = cache.struct() if cache is not None else None
+    wsp, wsn = _ws(ws, workspace_size(cfg, OP_LAYER, b, n))
+    _check(lib().sas_layer_forward(C.byref(cfg), b, n, _ptr(x), C.byref(weights_struct(W)), _ptr(out["y"]),
+                                   C.byref(st) if st is not None else None,
+                                   C.byref(tp) if tp is not None else None,
+                                   C.byref(cs) if cs is not None else None, wsp, wsn, _stream()))
+    return out
+
+
+def to_device(arr, dtype: str, device="cuda"):
+    """float32 NumPy array (values exact in `dtype`) -> device tensor."""
+    t = torch.from_numpy(arr)
+    return t.to(TORCH_DTYPE[dtype]).to(device)
+
+
+def weights_to_device(W: dict, dtype: str, device="cuda") -> dict:
+    return {k: (None if v is None else to_device(v, dtype, device)) for k, v in W.items()}
