@@ -1,0 +1,152 @@
+#!/usr/bin/env python3
+"""Benchmark of the SAS hot path on one MI355X.
+
+A step is one decoder-layer forward of the 7B-shape workload (batch 1,
+1024 tokens: 576 image tokens then 448 text tokens, bf16, GATED SAS attention
+with B = 64, K = 8): RMSNorm, QKV GEMM + RoPE, block summaries, selector and
+Top-K, gated block-sparse attention, O-projection + residual, RMSNorm,
+gate/up GEMM + SwiGLU, down GEMM + residual -- all HIP kernels of libsas.so.
+Inputs are resident in HBM before the timed region.
+
+Prints one JSON line: tokens/s per layer (value), algorithmic TFLOP/s and
+its fraction of the bf16 MFMA peak, the roofline of the dominant kernel
+(timed with HIP events on its stream over a second pass of the same steps)
+and the fp64 CPU oracle timed on the host over one layer forward.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+HBM_PEAK_GBS = 8000.0
+
+METRIC = "prefill tokens/s per layer + % bf16 MFMA peak; decode % HBM GB/s"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="7b_layer_1k")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-threads", type=int, default=0, help="oracle BLAS threads (0: affinity, max 16)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the SAS hot path here is single-GPU "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    cores = args.cpu_threads or min(16, len(os.sched_getaffinity(0)))
+    for var in ("OPENBLAS_NUM_THREADS", "OMP_NUM_THREADS", "MKL_NUM_THREADS"):
+        os.environ[var] = str(cores)
+
+    import numpy as np
+    import torch
+
+    here = os.path.dirname(os.path.abspath(__file__))
+    sys.path.insert(0, here)
+    from paper_2609_13141_amd import configs, inputs, sas
+
+    w = configs.BY_NAME[args.workload]
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    x_np = inputs.embeddings(w)
+    W_np = inputs.layer_weights(w)
+    x = sas.to_device(x_np, w.dtype, dev)
+    W = sas.weights_to_device(W_np, w.dtype, dev)
+    cfg = sas.make_config(w)
+    ws = sas.Workspace(dev)
+
+    def step():
+        return sas.layer_forward(cfg, x, W, stats=False, ws=ws)["y"]
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms = (t1 - t0) * 1e3 / args.steps
+    T = w.tokens
+    tok_s = T / (ms * 1e-3)
+    flops = w.prefill_flops()
+    tflops = flops / (ms * 1e-3) / 1e12
+
+    # second pass of the same steps with an event pair around every kernel
+    sas.profiler_start(64 * args.steps + 64)
+    for _ in range(args.steps):
+        step()
+    recs = sas.profiler_stop()
+    fam = {}
+    for name, t in recs:
+        fam.setdefault(name, []).append(t)
+    kern_ms = {k: sum(v) / len(v) for k, v in fam.items()}
+    kern_calls = {k: len(v) // args.steps for k, v in fam.items()}
+    # dominant kernel: the gate/up GEMM (2 * T * d * 2 * d_ff algorithmic flops per launch)
+    dom = "gemm_gate_up"
+    dom_flops = 2.0 * T * w.d_model * 2 * w.d_ff
+    dom_tf = dom_flops / (kern_ms[dom] * 1e-3) / 1e12
+
+    line = {
+        "metric": METRIC,
+        "value": round(tok_s, 1),
+        "unit": "tokens/s/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded N(0,1) text / N(0,1)*2 image embeddings, N(0,0.02) weights)",
+        "config": {"workload": w.name, "batch": w.batch, "seq_len": w.seq_len, "d_model": w.d_model,
+                   "n_heads": w.n_heads, "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
+                   "d_ff": w.d_ff, "mode": w.mode, "block_size": w.block_size, "top_k": w.top_k},
+        "alg_tflops": round(tflops, 2),
+        "mfma_frac": round(tflops / BF16_PEAK_TFLOPS, 4),
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(dom_tf, 2),
+                     "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(dom_tf / BF16_PEAK_TFLOPS, 4),
+                     "traffic": None, "alg_gflop_per_launch": round(dom_flops / 1e9, 3),
+                     "avg_ms": round(kern_ms[dom], 4)},
+        "kernels_ms": {k: round(v, 4) for k, v in sorted(kern_ms.items(), key=lambda kv: -kv[1] * kern_calls[kv[0]])},
+    }
+
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, x_np, W_np, cores)
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(w, x_np, W_np, cores):
+    """The fp64 oracle, as it stands, over one full layer forward of the same
+    workload on the host cores."""
+    import numpy as np
+
+    import oracle
+    from oracle.layer import Spec
+    try:
+        from threadpoolctl import threadpool_info
+        used = max([p.get("num_threads", 1) for p in threadpool_info()] or [cores])
+    except Exception:
+        used = cores
+    spec = Spec(w.n_heads, w.n_kv_heads, w.head_dim, w.block_size, w.top_k, w.mode, w.dtype, w.rope_base,
+                w.rms_eps)
+    x = x_np.astype(np.float64)
+    Wd = {k: (None if a is None else a.astype(np.float64)) for k, a in W_np.items()}
+    t0 = time.perf_counter()
+    oracle.layer_forward(x, Wd, spec)
+    dt = time.perf_counter() - t0
+    return {"value": round(w.tokens / dt, 2), "unit": "tokens/s/layer", "cores": int(used), "kind": "oracle",
+            "sample": f"one full layer forward of {w.name} ({w.tokens} tokens), fp64 NumPy, {dt:.2f} s"}
+
+
+if __name__ == "__main__":
+    main()

@@ -78,7 +78,7 @@ typedef struct {
   int32_t head_dim;    /* 64 or 128 */
   int32_t d_ff;
   int32_t block_size;  /* B, tokens per SAS block: 16, 32, 64 or 128 */
-  int32_t top_k;       /* K, historical blocks kept per query, 0..64 */
+  int32_t top_k;       /* K, historical blocks kept per query, 0..32 */
   float rope_base;     /* rotary base (rotate-half pairing i, i + head_dim/2) */
   float rms_eps;       /* RMSNorm epsilon */
   float sm_scale;      /* attention scale; <= 0 selects 1/sqrt(head_dim) */
@@ -230,6 +230,19 @@ const char* sas_last_error(void);
 
 /* Library version string. */
 const char* sas_version(void);
+
+/* Kernel timing for measurement tools (not needed by the compute path).
+ * sas_profiler_start(capacity): every kernel launched afterwards by this
+ * library (up to `capacity` launches, on any stream) is bracketed by a pair
+ * of hipEvents recorded on its stream.  sas_profiler_stop() ends recording
+ * and returns the number of launches recorded.  After the caller has
+ * synchronised the streams, sas_profiler_record(i, &name, &ms) returns the
+ * kernel family name ("gemm_gate_up", "attention", ...) and the elapsed
+ * milliseconds of launch i.  Not thread-safe; the events live until the next
+ * sas_profiler_start. */
+int32_t sas_profiler_start(int32_t capacity);
+int32_t sas_profiler_stop(void);
+int32_t sas_profiler_record(int32_t i, const char** name, float* ms);
 
 #ifdef __cplusplus
 }

@@ -6,6 +6,7 @@
 #include <stdio.h>
 
 #include <string>
+#include <vector>
 
 #include "../../include/sas.h"
 #include "kernels.h"
@@ -37,6 +38,44 @@ sas_status hip_check(hipError_t e, const char* what) {
     if (_st != SAS_OK) return _st;            \
   } while (0)
 #define HIP_TRY(expr, what) SAS_TRY(hip_check((expr), (what)))
+
+// Opt-in kernel timing: a hipEvent pair around every launch on its stream.
+struct Profiler {
+  bool on = false;
+  std::vector<hipEvent_t> ev;
+  std::vector<const char*> names;
+  int used = 0;
+  int start(int capacity) {
+    for (auto e : ev) (void)hipEventDestroy(e);
+    ev.clear();
+    names.assign(capacity, nullptr);
+    for (int i = 0; i < 2 * capacity; ++i) {
+      hipEvent_t e;
+      if (hipEventCreate(&e) != hipSuccess) return -1;
+      ev.push_back(e);
+    }
+    used = 0;
+    on = true;
+    return 0;
+  }
+  int begin(const char* name, hipStream_t s) {
+    if (!on || used >= (int)names.size()) return -1;
+    names[used] = name;
+    (void)hipEventRecord(ev[2 * used], s);
+    return used++;
+  }
+  void end(int id, hipStream_t s) {
+    if (id >= 0) (void)hipEventRecord(ev[2 * id + 1], s);
+  }
+};
+Profiler g_prof;
+
+struct Timed {
+  int id;
+  hipStream_t s;
+  Timed(const char* name, hipStream_t st) : id(g_prof.begin(name, st)), s(st) {}
+  ~Timed() { g_prof.end(id, s); }
+};
 
 size_t act_bytes(const sas_config* c) { return c->dtype == SAS_BF16 ? 2 : 4; }
 
@@ -165,8 +204,11 @@ sas_status run_attention(const sas_config* c, int b, int n, const void* q, const
   void* ksum = k_summary ? k_summary : ws.ksum;
   int32_t* sel = sel_idx ? sel_idx : ws.sel;
   if (need_sel) {
-    HIP_TRY(launch_block_summaries(c->dtype, k, b, n, Hkv, dh, c->block_size, w_gk, ws.kplain, ksum, s),
-            "block summaries");
+    {
+      Timed tm("summaries", s);
+      HIP_TRY(launch_block_summaries(c->dtype, k, b, n, Hkv, dh, c->block_size, w_gk, ws.kplain, ksum, s),
+              "block summaries");
+    }
     SelectArgs sa;
     sa.b = b;
     sa.n = n;
@@ -183,7 +225,10 @@ sas_status run_attention(const sas_config* c, int b, int n, const void* q, const
     sa.sel_bias = ws.sel_bias;
     sa.log_gate = log_gate;
     sa.tau = tau;
-    HIP_TRY(launch_select(c->dtype, sa, s), "select");
+    {
+      Timed tm("select", s);
+      HIP_TRY(launch_select(c->dtype, sa, s), "select");
+    }
   }
   AttnArgs aa;
   aa.b = b;
@@ -202,13 +247,19 @@ sas_status run_attention(const sas_config* c, int b, int n, const void* q, const
   aa.sel_bias = ws.sel_bias;
   aa.O = o;
   aa.lse = lse;
-  HIP_TRY(launch_attention(c->dtype, aa, s), "attention");
+  {
+    Timed tm("attention", s);
+    HIP_TRY(launch_attention(c->dtype, aa, s), "attention");
+  }
   return SAS_OK;
 }
 
 sas_status run_mlp(const sas_config* c, size_t T, const void* x, const sas_layer_weights* w, void* y,
                    const MlpWs& ws, hipStream_t s) {
-  HIP_TRY(launch_rmsnorm(c->dtype, x, w->rms2, ws.u2, (int)T, c->d_model, c->rms_eps, s), "rmsnorm");
+  {
+    Timed tm("rmsnorm", s);
+    HIP_TRY(launch_rmsnorm(c->dtype, x, w->rms2, ws.u2, (int)T, c->d_model, c->rms_eps, s), "rmsnorm");
+  }
   GemmArgs g = {};
   g.epi = EPI_SWIGLU;
   g.M = (int)T;
@@ -218,7 +269,10 @@ sas_status run_mlp(const sas_config* c, size_t T, const void* x, const sas_layer
   g.B1 = w->w_up;
   g.N = c->d_ff;
   g.out = ws.a;
-  HIP_TRY(launch_gemm(c->dtype, g, s), "gate/up gemm");
+  {
+    Timed tm("gemm_gate_up", s);
+    HIP_TRY(launch_gemm(c->dtype, g, s), "gate/up gemm");
+  }
   GemmArgs d = {};
   d.epi = EPI_RESID;
   d.M = (int)T;
@@ -228,7 +282,10 @@ sas_status run_mlp(const sas_config* c, size_t T, const void* x, const sas_layer
   d.N = c->d_model;
   d.resid = x;
   d.out = y;
-  HIP_TRY(launch_gemm(c->dtype, d, s), "down gemm");
+  {
+    Timed tm("gemm_down", s);
+    HIP_TRY(launch_gemm(c->dtype, d, s), "down gemm");
+  }
   return SAS_OK;
 }
 
@@ -267,6 +324,22 @@ extern "C" {
 const char* sas_last_error(void) { return g_err.c_str(); }
 
 const char* sas_version(void) { return "sas-mi355x 0.1 (gfx950)"; }
+
+int32_t sas_profiler_start(int32_t capacity) {
+  if (capacity <= 0) return fail(SAS_ERR_INVALID_ARGUMENT, "capacity must be positive");
+  return g_prof.start(capacity) == 0 ? SAS_OK : fail(SAS_ERR_HIP, "hipEventCreate failed");
+}
+
+int32_t sas_profiler_stop(void) {
+  g_prof.on = false;
+  return g_prof.used;
+}
+
+int32_t sas_profiler_record(int32_t i, const char** name, float* ms) {
+  if (i < 0 || i >= g_prof.used) return fail(SAS_ERR_INVALID_ARGUMENT, "record %d out of range", i);
+  *name = g_prof.names[i];
+  return hip_check(hipEventElapsedTime(ms, g_prof.ev[2 * i], g_prof.ev[2 * i + 1]), "hipEventElapsedTime");
+}
 
 size_t sas_workspace_size(const sas_config* c, int32_t op, int32_t batch, int32_t seq_len) {
   if (!c || batch <= 0) return 0;
@@ -368,8 +441,14 @@ sas_status sas_layer_forward(const sas_config* c, int32_t batch, int32_t seq_len
   void* o = st.o ? st.o : lw.o;
   void* h1 = tp.h1 ? tp.h1 : lw.h1;
 
-  HIP_TRY(launch_rope_table(lw.rope, seq_len, c->head_dim, c->rope_base, s), "rope table");
-  HIP_TRY(launch_rmsnorm(c->dtype, x, w->rms1, lw.u1, (int)T, c->d_model, c->rms_eps, s), "rmsnorm");
+  {
+    Timed tm("rope_table", s);
+    HIP_TRY(launch_rope_table(lw.rope, seq_len, c->head_dim, c->rope_base, s), "rope table");
+  }
+  {
+    Timed tm("rmsnorm", s);
+    HIP_TRY(launch_rmsnorm(c->dtype, x, w->rms1, lw.u1, (int)T, c->d_model, c->rms_eps, s), "rmsnorm");
+  }
   GemmArgs g = {};
   g.epi = EPI_QKV_ROPE;
   g.M = (int)T;
@@ -387,7 +466,10 @@ sas_status sas_layer_forward(const sas_config* c, int32_t batch, int32_t seq_len
   g.head_dim = c->head_dim;
   g.seq_len = seq_len;
   g.rope = lw.rope;
-  HIP_TRY(launch_gemm(c->dtype, g, s), "qkv gemm");
+  {
+    Timed tm("gemm_qkv", s);
+    HIP_TRY(launch_gemm(c->dtype, g, s), "qkv gemm");
+  }
   SAS_TRY(run_attention(c, batch, seq_len, q, k, v, w->w_gq, w->w_gk, o, st.lse, st.k_summary, st.sel_idx,
                         st.log_gate, st.tau, lw.att, s));
   GemmArgs og = {};
@@ -399,7 +481,10 @@ sas_status sas_layer_forward(const sas_config* c, int32_t batch, int32_t seq_len
   og.N = c->d_model;
   og.resid = x;
   og.out = h1;
-  HIP_TRY(launch_gemm(c->dtype, og, s), "o-proj gemm");
+  {
+    Timed tm("gemm_o", s);
+    HIP_TRY(launch_gemm(c->dtype, og, s), "o-proj gemm");
+  }
   return run_mlp(c, T, h1, w, y, lw.mlp, s);
 }
 

@@ -24,7 +24,8 @@ OP_ATTENTION, OP_MLP, OP_LAYER, OP_DECODE, OP_LM_HEAD = 0, 1, 2, 3, 4
 TORCH_DTYPE = {"bf16": torch.bfloat16, "f32": torch.float32}
 
 EXPORTS = ("sas_workspace_size", "sas_attention_prefill", "sas_mlp_forward", "sas_layer_forward",
-           "sas_decode_step", "sas_embed", "sas_lm_head_argmax", "sas_last_error", "sas_version")
+           "sas_decode_step", "sas_embed", "sas_lm_head_argmax", "sas_last_error", "sas_version",
+           "sas_profiler_start", "sas_profiler_stop", "sas_profiler_record")
 
 
 class SasError(RuntimeError):
@@ -98,6 +99,12 @@ def lib() -> C.CDLL:
     L.sas_last_error.argtypes = []
     L.sas_version.restype = C.c_char_p
     L.sas_version.argtypes = []
+    L.sas_profiler_start.restype = i32
+    L.sas_profiler_start.argtypes = [i32]
+    L.sas_profiler_stop.restype = i32
+    L.sas_profiler_stop.argtypes = []
+    L.sas_profiler_record.restype = i32
+    L.sas_profiler_record.argtypes = [i32, C.POINTER(C.c_char_p), C.POINTER(C.c_float)]
     _lib = L
     return L
 
@@ -243,6 +250,22 @@ def layer_forward(cfg: Config, x, W: dict, *, stats: bool = True, lse=True, sel_
                                    C.byref(st) if st is not None else None,
                                    C.byref(tp) if tp is not None else None,
                                    C.byref(cs) if cs is not None else None, wsp, wsn, _stream()))
+    return out
+
+
+def profiler_start(capacity: int = 4096):
+    _check(lib().sas_profiler_start(capacity))
+
+
+def profiler_stop() -> list:
+    """Stop recording; synchronise; return [(kernel family, ms), ...]."""
+    n = lib().sas_profiler_stop()
+    torch.cuda.synchronize()
+    out = []
+    name, ms = C.c_char_p(), C.c_float()
+    for i in range(n):
+        _check(lib().sas_profiler_record(i, C.byref(name), C.byref(ms)))
+        out.append((name.value.decode(), float(ms.value)))
     return out
 
 
