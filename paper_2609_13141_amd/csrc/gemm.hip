@@ -53,6 +53,111 @@ __device__ __forceinline__ float silu_f(float x) { return x / (1.0f + __expf(-x)
 
 constexpr int BK = 64;
 
+// Epilogue shared by the GEMM kernels.  Lane (lr, lk) of wave (wm, wn) holds
+// column lr of every 32x32 subtile (i, j) of its TM x TN tile, at rows
+// 8*(v/4) + 4*lk + (v%4) of the subtile for accumulator element v.
+template <int EPI, int TM, int TN, int FM, int FN>
+__device__ __forceinline__ void gemm_epilogue_t(const GemmParams& P, floatx16_t (&acc)[FM][FN], int m0, int n0,
+                                                int wm, int wn, int lr, int lk) {
+  // The loads an element needs (residual, rotary table) are issued for a
+  // whole 32x32 subtile before any of them is used, from clamped addresses,
+  // so that their latencies overlap.
+  const int colbase = n0 + wn * TN;
+  const int rowbase = m0 + wm * TM + 4 * lk;
+  if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int col = colbase + j * 32 + lr;
+        const int colc = min(col, P.N - 1);
+        float r[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int rowc = min(rowbase + i * 32 + 8 * (v >> 2) + (v & 3), P.M - 1);
+          r[v] = bf16_to_f32(P.resid[(size_t)rowc * P.N + colc]);
+        }
+        if (col >= P.N) continue;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int row = rowbase + i * 32 + 8 * (v >> 2) + (v & 3);
+          if (row < P.M) P.out[(size_t)row * P.N + col] = f32_to_bf16(acc[i][j][v] + r[v]);
+        }
+      }
+    return;
+  }
+  const int hh = P.dh >> 1;
+#pragma unroll
+  for (int jp = 0; jp < FN / 2; ++jp) {
+    const int J = colbase + jp * 64 + lr;  // half-0 logical column
+    const int p = (J >> 6) * 32 + (J & 31);
+    const bool pvalid = p < P.npairs;
+    // per-column-pair destination (row stride ld, element offset base)
+    bf16_t* dst;
+    size_t ld;
+    int ir = 0;
+    bool rot = false;
+    if constexpr (EPI == EPI_SWIGLU) {
+      dst = P.out + p;
+      ld = (size_t)P.npairs;
+    } else {
+      const int hd = min(p, P.npairs - 1) / hh;
+      ir = min(p, P.npairs - 1) - hd * hh;
+      if (hd < P.H) {
+        dst = P.out + (size_t)hd * P.dh + ir;
+        ld = (size_t)P.H * P.dh;
+      } else if (hd < P.H + P.Hkv) {
+        dst = P.out1 + (size_t)(hd - P.H) * P.dh + ir;
+        ld = (size_t)P.Hkv * P.dh;
+      } else {
+        dst = P.out2 + (size_t)(hd - P.H - P.Hkv) * P.dh + ir;
+        ld = (size_t)P.Hkv * P.dh;
+      }
+      rot = hd < P.H + P.Hkv;
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      float2 cs[16];
+      if constexpr (EPI == EPI_QKV_ROPE) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int rowc = min(rowbase + i * 32 + 8 * (v >> 2) + (v & 3), P.M - 1);
+          const int pos = P.row_pos ? P.row_pos[rowc] : rowc % P.seq_len;
+          cs[v] = P.rope[(size_t)pos * hh + ir];
+        }
+      }
+      if (!pvalid) continue;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = rowbase + i * 32 + 8 * (v >> 2) + (v & 3);
+        if (row >= P.M) continue;
+        float x1 = acc[i][2 * jp][v], x2 = acc[i][2 * jp + 1][v];
+        if constexpr (EPI == EPI_SWIGLU) {
+          dst[(size_t)row * ld] = f32_to_bf16(silu_f(x1) * x2);
+        } else {
+          if (rot) {
+            const float o1 = x1 * cs[v].x - x2 * cs[v].y;
+            const float o2 = x2 * cs[v].x + x1 * cs[v].y;
+            x1 = o1;
+            x2 = o2;
+          }
+          dst[(size_t)row * ld] = f32_to_bf16(x1);
+          dst[(size_t)row * ld + hh] = f32_to_bf16(x2);
+        }
+      }
+    }
+  }
+}
+
+template <int TM, int TN, int FM, int FN>
+__device__ __forceinline__ void gemm_epilogue(const GemmParams& P, floatx16_t (&acc)[FM][FN], int m0, int n0,
+                                              int wm, int wn, int lr, int lk) {
+  if (P.epi == EPI_RESID) gemm_epilogue_t<EPI_RESID, TM, TN, FM, FN>(P, acc, m0, n0, wm, wn, lr, lk);
+  else if (P.epi == EPI_SWIGLU) gemm_epilogue_t<EPI_SWIGLU, TM, TN, FM, FN>(P, acc, m0, n0, wm, wn, lr, lk);
+  else gemm_epilogue_t<EPI_QKV_ROPE, TM, TN, FM, FN>(P, acc, m0, n0, wm, wn, lr, lk);
+}
+
+
 template <int BM, int BN, int WM, int WN>
 __global__ void __launch_bounds__(WM * WN * 64)
 gemm_bf16_kernel(GemmParams P) {
@@ -87,7 +192,7 @@ gemm_bf16_kernel(GemmParams P) {
     int row = c >> 3, c16 = c & 7;
     int gr = m0 + row;
     a_src[i] = (gr < P.M) ? P.A + (size_t)gr * P.K + c16 * 8 : nullptr;
-    a_lds[i] = row * BK + ((c16 ^ (row & 7)) << 3);
+    a_lds[i] = row * BK + ((c16 ^ ((row >> 1) & 7)) << 3);
   }
 #pragma unroll
   for (int i = 0; i < BCH; ++i) {
@@ -96,7 +201,7 @@ gemm_bf16_kernel(GemmParams P) {
     const bf16_t* r = b_row<bf16_t>(P.epi, n0 + row, P.N, P.npairs, P.K, P.B0, P.B1, P.B2, P.H,
                                     P.Hkv, P.dh);
     b_src[i] = r ? r + c16 * 8 : nullptr;
-    b_lds[i] = row * BK + ((c16 ^ (row & 7)) << 3);
+    b_lds[i] = row * BK + ((c16 ^ ((row >> 1) & 7)) << 3);
   }
 
   floatx16_t acc[FM][FN];
@@ -151,12 +256,12 @@ gemm_bf16_kernel(GemmParams P) {
 #pragma unroll
       for (int i = 0; i < FM; ++i) {
         int row = wm * TM + i * 32 + lr;
-        fa[i] = *(const bf16x8_t*)(a + row * BK + ((kc ^ (row & 7)) << 3));
+        fa[i] = *(const bf16x8_t*)(a + row * BK + ((kc ^ ((row >> 1) & 7)) << 3));
       }
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
         int row = wn * TN + j * 32 + lr;
-        fb[j] = *(const bf16x8_t*)(b + row * BK + ((kc ^ (row & 7)) << 3));
+        fb[j] = *(const bf16x8_t*)(b + row * BK + ((kc ^ ((row >> 1) & 7)) << 3));
       }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
@@ -168,65 +273,161 @@ gemm_bf16_kernel(GemmParams P) {
     __syncthreads();
   }
 
-  // ---- epilogue: lane holds column lr of each 32x32 subtile, rows
-  // 8*(v/4) + 4*lk + (v%4) ----
-  const int colbase = n0 + wn * TN;
-  if (P.epi == EPI_RESID) {
+  gemm_epilogue<TM, TN, FM, FN>(P, acc, m0, n0, wm, wn, lr, lk);
+}
+
+// ---- direct-to-LDS pipelined variant (K % BKT == 0) ---------------------
+// Global tiles are copied straight into LDS with global_load_lds_dwordx4
+// (each lane writes 16 bytes at M0 + 16*lane), so no VGPRs stage them.  The
+// XOR swizzle of the 16-byte chunks is applied by choosing which global chunk
+// each lane fetches: with CPR = BKT/8 chunks per row, LDS chunk c of a stage
+// holds row r = c / CPR and k-chunk (c % CPR) ^ ((r / (16/CPR)) % CPR).  A
+// 128-bit LDS read serves 16 lanes per pass; 16 consecutive rows then cover
+// 16 distinct 4-bank groups.  Out-of-range rows are clamped to a valid row
+// (their results are never stored), so the main loop has no predication.
+// STAGES LDS buffers: the loads of k-tile t + STAGES - 1 are issued right after
+// the barrier that ends the reads of k-tile t - 1, so STAGES - 1 tiles are in
+// flight while k-tile t is multiplied.
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+template <int EPI, int BM, int BN, int WM, int WN, int BKT, int STAGES, bool DB = false>
+__global__ void __launch_bounds__(WM * WN * 64)
+gemm_bf16_pipe_kernel(GemmParams P) {
+  constexpr int NW = WM * WN;
+  constexpr int TM = BM / WM, TN = BN / WN;
+  constexpr int FM = TM / 32, FN = TN / 32;
+  constexpr int CPR = BKT / 8;               // 16-byte chunks per row
+  constexpr int RPG = 16 / CPR;              // rows per 256-byte bank sweep
+  constexpr int AI = BM * CPR / (64 * NW);   // load instructions per wave per stage (A)
+  constexpr int BI = BN * CPR / (64 * NW);
+  static_assert(AI * 64 * NW == BM * CPR && BI * 64 * NW == BN * CPR, "tile/threads mismatch");
+  static_assert(TN % 64 == 0, "pair epilogues need 64-column wave tiles");
+  static_assert((STAGES - 2) * (AI + BI) <= 63, "vmcnt range");
+  constexpr int STAGE = (BM + BN) * BKT;  // elements per stage
+
+  extern __shared__ __align__(16) unsigned char smem[];
+  bf16_t* S = (bf16_t*)smem;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int Mt = (P.M + BM - 1) / BM;
+  const int tile = blockIdx.x;
+  const int mt = tile % Mt, nt = tile / Mt;
+  const int m0 = mt * BM, n0 = nt * BN;
+
+  // element offsets of this lane's chunks from the operand base (32-bit: the
+  // operands hold fewer than 2^31 elements); B rows may come from three
+  // matrices, so their base pointer is kept per chunk
+  uint32_t a_off[AI];
+  const bf16_t* b_src[BI];
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        int col = colbase + j * 32 + lr;
-        if (col >= P.N) continue;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          int row = m0 + wm * TM + i * 32 + 8 * (v >> 2) + 4 * lk + (v & 3);
-          if (row < P.M) {
-            size_t o = (size_t)row * P.N + col;
-            P.out[o] = f32_to_bf16(acc[i][j][v] + bf16_to_f32(P.resid[o]));
-          }
-        }
-      }
-    return;
+  for (int j = 0; j < AI; ++j) {
+    const int c = (wave * AI + j) * 64 + lane;
+    const int r = c / CPR, cc = (c % CPR) ^ ((r / RPG) % CPR);
+    const int gr = min(m0 + r, P.M - 1);
+    a_off[j] = (uint32_t)gr * (uint32_t)P.K + cc * 8;
   }
-  const int hh = P.dh >> 1;
+#pragma unroll
+  for (int j = 0; j < BI; ++j) {
+    const int c = (wave * BI + j) * 64 + lane;
+    const int r = c / CPR, cc = (c % CPR) ^ ((r / RPG) % CPR);
+    const bf16_t* row = b_row<bf16_t>(P.epi, n0 + r, P.N, P.npairs, P.K, P.B0, P.B1, P.B2, P.H, P.Hkv, P.dh);
+    b_src[j] = (row ? row : P.B0) + cc * 8;
+  }
+
+  auto issue = [&](int kt) {
+    const int k0 = kt * BKT;
+    bf16_t* st = S + (kt % STAGES) * STAGE;
+#pragma unroll
+    for (int j = 0; j < AI; ++j)
+      __builtin_amdgcn_global_load_lds((const void*)(P.A + a_off[j] + k0),
+                                       (lds_void_t*)(st + (wave * AI + j) * 64 * 8), 16, 0, 0);
+#pragma unroll
+    for (int j = 0; j < BI; ++j)
+      __builtin_amdgcn_global_load_lds((const void*)(b_src[j] + k0),
+                                       (lds_void_t*)(st + BM * BKT + (wave * BI + j) * 64 * 8), 16, 0, 0);
+  };
+
+  floatx16_t acc[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int jp = 0; jp < FN / 2; ++jp) {
-      int J = colbase + jp * 64 + lr;  // half-0 logical column
-      int p = (J >> 6) * 32 + (J & 31);
-      if (p >= P.npairs) continue;
+    for (int j = 0; j < FN; ++j)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        int row = m0 + wm * TM + i * 32 + 8 * (v >> 2) + 4 * lk + (v & 3);
-        if (row >= P.M) continue;
-        float x1 = acc[i][2 * jp][v], x2 = acc[i][2 * jp + 1][v];
-        if (P.epi == EPI_SWIGLU) {
-          P.out[(size_t)row * P.npairs + p] = f32_to_bf16(silu_f(x1) * x2);
-        } else {
-          int hd = p / hh, ir = p % hh;
-          bf16_t* dst;
-          if (hd < P.H) {
-            dst = P.out + ((size_t)row * P.H + hd) * P.dh;
-          } else if (hd < P.H + P.Hkv) {
-            dst = P.out1 + ((size_t)row * P.Hkv + (hd - P.H)) * P.dh;
-          } else {
-            dst = P.out2 + ((size_t)row * P.Hkv + (hd - P.H - P.Hkv)) * P.dh;
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  const int lr = lane & 31, lk = lane >> 5;
+  int aoff[FM], boff[FN];  // element offset of this lane's fragment row
+#pragma unroll
+  for (int i = 0; i < FM; ++i) aoff[i] = (wm * TM + i * 32 + lr) * BKT;
+#pragma unroll
+  for (int j = 0; j < FN; ++j) boff[j] = BM * BKT + (wn * TN + j * 32 + lr) * BKT;
+  const int sw = (lr / RPG) % CPR;  // fragment row bases are multiples of 32
+
+  const int nk = P.K / BKT;
+#pragma unroll
+  for (int t = 0; t < STAGES - 1; ++t)
+    if (t < nk) issue(t);
+  for (int kt = 0; kt < nk; ++kt) {
+    // tile kt has landed once at most (tiles issued after it) * (AI + BI) loads remain
+    if (kt + STAGES - 2 < nk) wait_vmcnt<(STAGES - 2) * (AI + BI)>();
+    else wait_vmcnt<0>();
+    __syncthreads();
+    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
+    const bf16_t* st = S + (kt % STAGES) * STAGE;
+    if constexpr (!DB) {
+#pragma unroll
+      for (int kk = 0; kk < BKT / 16; ++kk) {
+        const int kc = kk * 2 + lk;
+        bf16x8_t fa[FM], fb[FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) fa[i] = *(const bf16x8_t*)(st + aoff[i] + ((kc ^ sw) << 3));
+#pragma unroll
+        for (int j = 0; j < FN; ++j) fb[j] = *(const bf16x8_t*)(st + boff[j] + ((kc ^ sw) << 3));
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+      }
+    } else {
+      // The fragments of step kk+1 are read while the MFMAs of step kk run.
+      // sched_barrier(0) after every MFMA keeps this order: the compiler would
+      // otherwise chain MFMAs on one accumulator and wait on each read at once.
+      bf16x8_t fa[2][FM], fb[2][FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) fa[0][i] = *(const bf16x8_t*)(st + aoff[i] + ((lk ^ sw) << 3));
+#pragma unroll
+      for (int j = 0; j < FN; ++j) fb[0][j] = *(const bf16x8_t*)(st + boff[j] + ((lk ^ sw) << 3));
+#pragma unroll
+      for (int kk = 0; kk < BKT / 16; ++kk) {
+        const int cur = kk & 1, nxt = cur ^ 1;
+        const bool more = kk + 1 < BKT / 16;
+        const int kc = ((kk + 1) * 2 + lk) ^ sw;
+        int g = 0;  // next read to issue: fa[0], fb[0..FN-1], fa[1..FM-1] (use order of step kk+1)
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j) {
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j], 0, 0, 0);
+            if (more && g < FM + FN) {
+              if (g == 0) fa[nxt][0] = *(const bf16x8_t*)(st + aoff[0] + (kc << 3));
+              else if (g <= FN) fb[nxt][g - 1] = *(const bf16x8_t*)(st + boff[g - 1] + (kc << 3));
+              else fa[nxt][g - FN] = *(const bf16x8_t*)(st + aoff[g - FN] + (kc << 3));
+            }
+            ++g;
+            __builtin_amdgcn_sched_barrier(0);
           }
-          if (hd < P.H + P.Hkv) {
-            int pos = P.row_pos ? P.row_pos[row] : row % P.seq_len;
-            float2 cs = P.rope[(size_t)pos * hh + ir];
-            float o1 = x1 * cs.x - x2 * cs.y;
-            float o2 = x2 * cs.x + x1 * cs.y;
-            x1 = o1;
-            x2 = o2;
-          }
-          dst[ir] = f32_to_bf16(x1);
-          dst[ir + hh] = f32_to_bf16(x2);
-        }
       }
     }
+  }
+  gemm_epilogue_t<EPI, TM, TN, FM, FN>(P, acc, m0, n0, wm, wn, lr, lk);
 }
 
 // ---- fp32 path: one thread per (row, logical pair or column) ----------------
@@ -288,6 +489,29 @@ static hipError_t run_bf16(const GemmParams& P, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int EPI, int BM, int BN, int WM, int WN, int BKT, int STAGES, bool DB>
+static hipError_t run_pipe_t(const GemmParams& P, hipStream_t s) {
+  constexpr int NT = WM * WN * 64;
+  const int tiles = ((P.M + BM - 1) / BM) * ((P.N + BN - 1) / BN);
+  const size_t lds = (size_t)STAGES * (BM + BN) * BKT * sizeof(bf16_t);
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute((const void*)gemm_bf16_pipe_kernel<EPI, BM, BN, WM, WN, BKT, STAGES, DB>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    attr = true;
+  }
+  hipLaunchKernelGGL((gemm_bf16_pipe_kernel<EPI, BM, BN, WM, WN, BKT, STAGES, DB>), dim3(tiles), dim3(NT), lds,
+                     s, P);
+  return hipGetLastError();
+}
+
+template <int BM, int BN, int WM, int WN, int BKT, int STAGES, bool DB = false>
+static hipError_t run_pipe(const GemmParams& P, hipStream_t s) {
+  if (P.epi == EPI_RESID) return run_pipe_t<EPI_RESID, BM, BN, WM, WN, BKT, STAGES, DB>(P, s);
+  if (P.epi == EPI_SWIGLU) return run_pipe_t<EPI_SWIGLU, BM, BN, WM, WN, BKT, STAGES, DB>(P, s);
+  return run_pipe_t<EPI_QKV_ROPE, BM, BN, WM, WN, BKT, STAGES, DB>(P, s);
+}
+
 static bool attrs_done = false;
 
 hipError_t launch_gemm(int dtype, const GemmArgs& g, hipStream_t s) {
@@ -305,9 +529,9 @@ hipError_t launch_gemm(int dtype, const GemmArgs& g, hipStream_t s) {
     return hipGetLastError();
   }
   if (!attrs_done) {
-    hipFuncSetAttribute((const void*)gemm_bf16_kernel<256, 256, 2, 4>,
+    (void)hipFuncSetAttribute((const void*)gemm_bf16_kernel<256, 256, 2, 4>,
                         hipFuncAttributeMaxDynamicSharedMemorySize, 2 * (256 + 256) * BK * 2);
-    hipFuncSetAttribute((const void*)gemm_bf16_kernel<128, 128, 2, 2>,
+    (void)hipFuncSetAttribute((const void*)gemm_bf16_kernel<128, 128, 2, 2>,
                         hipFuncAttributeMaxDynamicSharedMemorySize, 2 * (128 + 128) * BK * 2);
     attrs_done = true;
   }
@@ -332,6 +556,14 @@ hipError_t launch_gemm(int dtype, const GemmArgs& g, hipStream_t s) {
   P.rope = g.rope;
   P.row_pos = g.row_pos;
   const long big_tiles = (long)((g.M + 255) / 256) * ((nlog + 255) / 256);
+  if (g.K % 64 == 0) {
+    // Tile choice from measurements on MI355X: 256x256 (8 waves) wherever
+    // there are enough tiles; for short M (one wave of tiles or less) the
+    // tile that best fills 256 CUs: 256x128 for wide N, 128x128 for N <= 8K.
+    if (g.M >= 4096 || (nlog >= 8192 && nlog < 16384)) return run_pipe<256, 256, 2, 4, 64, 2, true>(P, s);
+    if (nlog >= 16384) return run_pipe<256, 128, 4, 2, 64, 2, true>(P, s);
+    return run_pipe<128, 128, 2, 2, 64, 2, true>(P, s);
+  }
   if (big_tiles >= 256) return run_bf16<256, 256, 2, 4>(P, s);
   return run_bf16<128, 128, 2, 2>(P, s);
 }
