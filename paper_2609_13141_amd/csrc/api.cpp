@@ -132,6 +132,8 @@ struct Carve {
 struct AttnWs {
   void* kplain;
   void* ksum;
+  void* qplain;
+  void* qhat;
   int32_t* sel;
   float* sel_bias;
 };
@@ -144,6 +146,9 @@ AttnWs carve_attention(Carve& cv, const sas_config* c, int b, int n) {
   AttnWs w;
   w.kplain = cv.take(kb);
   w.ksum = cv.take(kb);
+  const size_t qb = (size_t)b * c->n_kv_heads * n * c->head_dim * ab;
+  w.qplain = cv.take(qb);
+  w.qhat = cv.take(qb);
   w.sel = (int32_t*)cv.take(rows * 4);
   w.sel_bias = (float*)cv.take(rows * 4);
   return w;
@@ -209,6 +214,10 @@ sas_status run_attention(const sas_config* c, int b, int n, const void* q, const
       HIP_TRY(launch_block_summaries(c->dtype, k, b, n, Hkv, dh, c->block_size, w_gk, ws.kplain, ksum, s),
               "block summaries");
     }
+    if (w_gq) {  // projected gate queries are computed first; otherwise the select kernel sums the heads
+      Timed tm("gate_query", s);
+      HIP_TRY(launch_gate_query(c->dtype, q, b, n, H, Hkv, dh, w_gq, ws.qplain, ws.qhat, s), "gate query");
+    }
     SelectArgs sa;
     sa.b = b;
     sa.n = n;
@@ -219,8 +228,8 @@ sas_status run_attention(const sas_config* c, int b, int n, const void* q, const
     sa.K = c->top_k;
     sa.NB = NB;
     sa.Q = q;
+    sa.qhat = w_gq ? ws.qhat : nullptr;
     sa.kbar = ksum;
-    sa.w_gq = w_gq;
     sa.sel = sel;
     sa.sel_bias = ws.sel_bias;
     sa.log_gate = log_gate;

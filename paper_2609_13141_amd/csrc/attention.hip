@@ -31,10 +31,11 @@ namespace sas {
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 
-template <int DH>
-__global__ void __launch_bounds__(256) attn_bf16_kernel(AttnArgs P) {
+template <int DH, bool SINGLE>
+__global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
   constexpr int KP = DH + 8;  // K tile row pitch (elements)
   constexpr int VP = 64 + 4;  // V^T tile row pitch (elements)
+  constexpr int KPG = DH / 32;  // keys per V-staging group (4 for DH=128, 2 for DH=64)
   __shared__ __align__(16) bf16_t Ks[64 * KP];
   __shared__ __align__(16) bf16_t Vt[DH * VP];
 
@@ -47,6 +48,7 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(AttnArgs P) {
   const int t = qtile * 128 + wave * 32 + lr;
   const bool qvalid = t < n;
   const int beta = qvalid ? t / B : -1;
+  const int bshift = 31 - __clz(B < 64 ? B : 64);  // log2 of keys per SAS block inside a tile
 
   // Q^T as the B operand: lane supplies Q[t][ks*16 + lk*8 + 0..7]
   bf16x8_t qb[DH / 16];
@@ -59,18 +61,19 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(AttnArgs P) {
     }
   }
 
-  // selection cursor
+  // selection cursor over the ascending list of kept blocks
   const int32_t* selp = nullptr;
   const float* biasp = nullptr;
   int cur = 0, next_sel = 0x7fffffff;
   if (P.mode != SAS_MODE_DENSE && qvalid && Kn > 0) {
-    size_t row = (((size_t)bi * P.Hkv + g) * n + t) * Kn;
+    const size_t row = (((size_t)bi * P.Hkv + g) * n + t) * Kn;
     selp = P.sel + row;
     biasp = P.sel_bias + row;
-    int s0 = selp[0];
+    const int s0 = selp[0];
     next_sel = s0 >= 0 ? s0 : 0x7fffffff;
   }
   const bool gated = P.mode == SAS_MODE_GATED;
+  const bool dense = P.mode == SAS_MODE_DENSE;
 
   floatx16_t o[DH / 32];
 #pragma unroll
@@ -82,57 +85,71 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(AttnArgs P) {
 
   const int t_hi = min(n, qtile * 128 + 128) - 1;  // last query of the workgroup
   const int last_tile = t_hi / 64;
-  const int bt = B < 64 ? B : 64;  // keys per SAS block inside a tile
-  const int nsub = 64 / bt;        // SAS blocks per tile (1, 2 or 4)
-
-  const bf16_t* Kg = (const bf16_t*)P.Kt;
-  const bf16_t* Vg = (const bf16_t*)P.V;
+  const bf16_t* Kg = (const bf16_t*)P.Kt + (size_t)g * DH;
+  const bf16_t* Vg = (const bf16_t*)P.V + (size_t)g * DH;
+  const size_t kstride = (size_t)P.Hkv * DH;  // elements between consecutive keys
+  const size_t kbase = (size_t)bi * n;
 
   for (int kt = 0; kt <= last_tile; ++kt) {
     const int k0 = kt * 64;
-    // per-lane status of the (up to 4) SAS blocks of this tile: bias in the
-    // base-2 domain or -inf when masked
-    float bsub[4];
+    // bias (base-2 domain) of each SAS block of this tile for this lane's
+    // query, -inf when masked; one block per tile when B >= 64
+    constexpr int NSUB = SINGLE ? 1 : 4;
+    float bsub[NSUB];
     bool need = false;
 #pragma unroll
-    for (int sb = 0; sb < 4; ++sb) {
+    for (int sb = 0; sb < NSUB; ++sb) {
       bsub[sb] = -INFINITY;
-      if (sb >= nsub || !qvalid) continue;
-      const int m = (k0 + sb * bt) / B;
-      if (k0 + sb * bt > t) continue;  // future keys only
-      if (m == beta) {
-        bsub[sb] = 0.f;
-      } else if (P.mode == SAS_MODE_DENSE) {
+      const int kstart = k0 + (sb << bshift);
+      if (!qvalid || kstart > t || (!SINGLE && (sb << bshift) >= 64)) continue;
+      const int m = kstart / B;
+      if (m == beta || dense) {
         bsub[sb] = 0.f;
       } else if (m == next_sel) {
         bsub[sb] = gated ? biasp[cur] * LOG2E : 0.f;
-        // a block spans several sub-blocks when B > 64: advance once, at its end
-        if (k0 + sb * bt + bt >= (m + 1) * B) {
+        // a block wider than a tile is consumed at its last tile
+        if (kstart + (1 << bshift) >= (m + 1) * B) {
           ++cur;
-          int s1 = cur < Kn ? selp[cur] : -1;
+          const int s1 = cur < Kn ? selp[cur] : -1;
           next_sel = s1 >= 0 ? s1 : 0x7fffffff;
         }
       }
       need |= bsub[sb] != -INFINITY;
     }
+    // also orders this tile's LDS writes after the previous tile's reads
     if (!__syncthreads_or(need)) continue;
 
-    // stage K (row-major) and V (transposed) tiles
+    // stage K row-major and V transposed; each lane transposes KPG keys x 8 dims
+    {
 #pragma unroll
-    for (int i = 0; i < (64 * DH / 8) / 256; ++i) {
-      const int c = tid + i * 256;
-      const int kr = c / (DH / 8), c8 = c % (DH / 8);
-      const int key = k0 + kr;
-      uint4 ku = make_uint4(0, 0, 0, 0), vu = make_uint4(0, 0, 0, 0);
-      if (key < n) {
-        const size_t off = (((size_t)bi * n + key) * P.Hkv + g) * DH + c8 * 8;
-        ku = *(const uint4*)(Kg + off);
-        vu = *(const uint4*)(Vg + off);
+      for (int i = 0; i < (64 * DH / 8) / 256; ++i) {
+        const int c = tid + i * 256;
+        const int kr = c / (DH / 8), c8 = c % (DH / 8);
+        const int key = k0 + kr;
+        uint4 ku = key < n ? *(const uint4*)(Kg + (kbase + key) * kstride + c8 * 8) : make_uint4(0, 0, 0, 0);
+        *(uint4*)(Ks + kr * KP + c8 * 8) = ku;
       }
-      *(uint4*)(Ks + kr * KP + c8 * 8) = ku;
-      const bf16_t* ve = (const bf16_t*)&vu;
+      const int c8 = tid % (DH / 8), kg = tid / (DH / 8);
+      uint32_t w[KPG][4];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) Vt[(c8 * 8 + e) * VP + kr] = ve[e];
+      for (int q = 0; q < KPG; ++q) {
+        const int key = k0 + kg * KPG + q;
+        uint4 vu = key < n ? *(const uint4*)(Vg + (kbase + key) * kstride + c8 * 8) : make_uint4(0, 0, 0, 0);
+        w[q][0] = vu.x; w[q][1] = vu.y; w[q][2] = vu.z; w[q][3] = vu.w;
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int sh = (e & 1) * 16;
+        bf16_t* dst = Vt + (c8 * 8 + e) * VP + kg * KPG;
+        if constexpr (KPG == 4) {
+          uint2 pk;
+          pk.x = ((w[0][e >> 1] >> sh) & 0xffffu) | (((w[1][e >> 1] >> sh) & 0xffffu) << 16);
+          pk.y = ((w[2][e >> 1] >> sh) & 0xffffu) | (((w[3][e >> 1] >> sh) & 0xffffu) << 16);
+          *(uint2*)dst = pk;
+        } else {
+          *(uint32_t*)dst = ((w[0][e >> 1] >> sh) & 0xffffu) | (((w[1][e >> 1] >> sh) & 0xffffu) << 16);
+        }
+      }
     }
     __syncthreads();
 
@@ -144,34 +161,39 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(AttnArgs P) {
       for (int v = 0; v < 16; ++v) s[st][v] = 0.f;
 #pragma unroll
       for (int ks = 0; ks < DH / 16; ++ks) {
-        bf16x8_t a = *(const bf16x8_t*)(Ks + (st * 32 + lr) * KP + ks * 16 + lk * 8);
+        const bf16x8_t a = *(const bf16x8_t*)(Ks + (st * 32 + lr) * KP + ks * 16 + lk * 8);
         s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qb[ks], s[st], 0, 0, 0);
       }
     }
     // scale, bias, mask; row max over this lane's 32 keys and the partner's
+    const int lim = t - k0;  // keys kl <= lim are causal for this lane
     float mx = -INFINITY;
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int kl = st * 32 + 8 * (v >> 2) + 4 * lk + (v & 3);
-        const int sb = kl / bt;
-        const float bb = sb == 0 ? bsub[0] : sb == 1 ? bsub[1] : sb == 2 ? bsub[2] : bsub[3];
-        const bool ok = (k0 + kl <= t) && bb != -INFINITY;
-        const float x = ok ? s[st][v] * qk_scale + bb : -INFINITY;
+        float bb;
+        if constexpr (SINGLE) {
+          bb = bsub[0];
+        } else {
+          const int sb = kl >> bshift;
+          bb = sb == 0 ? bsub[0] : sb == 1 ? bsub[1] : sb == 2 ? bsub[2] : bsub[3];
+        }
+        const float x = (kl <= lim) ? s[st][v] * qk_scale + bb : -INFINITY;
         s[st][v] = x;
         mx = fmaxf(mx, x);
       }
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float m_new = fmaxf(m_run, mx);
     const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = exp2f(m_run - m_use);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
     float rs = 0.f;
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const float p = exp2f(s[st][v] - m_use);
+        const float p = __builtin_amdgcn_exp2f(s[st][v] - m_use);
         s[st][v] = p;
         rs += p;
       }
@@ -195,13 +217,12 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(AttnArgs P) {
 #pragma unroll
       for (int dt = 0; dt < DH / 32; ++dt) {
         const bf16_t* vr = Vt + (dt * 32 + lr) * VP + 16 * ks + 4 * lk;
-        uint2 lo = *(const uint2*)vr;
-        uint2 hi = *(const uint2*)(vr + 8);
+        const uint2 lo = *(const uint2*)vr;
+        const uint2 hi = *(const uint2*)(vr + 8);
         uint4 u = make_uint4(lo.x, lo.y, hi.x, hi.y);
         o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(bf16x8_t*)&u, pb, o[dt], 0, 0, 0);
       }
     }
-    __syncthreads();
   }
 
   if (!qvalid) return;
@@ -212,10 +233,10 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(AttnArgs P) {
 #pragma unroll
     for (int v4 = 0; v4 < 4; ++v4) {
       const int d0 = dt * 32 + 8 * v4 + 4 * lk;
-      uint32_t w0 = (uint32_t)f32_to_bf16(o[dt][4 * v4 + 0] * inv_l) |
-                    ((uint32_t)f32_to_bf16(o[dt][4 * v4 + 1] * inv_l) << 16);
-      uint32_t w1 = (uint32_t)f32_to_bf16(o[dt][4 * v4 + 2] * inv_l) |
-                    ((uint32_t)f32_to_bf16(o[dt][4 * v4 + 3] * inv_l) << 16);
+      const uint32_t w0 = (uint32_t)f32_to_bf16(o[dt][4 * v4 + 0] * inv_l) |
+                          ((uint32_t)f32_to_bf16(o[dt][4 * v4 + 1] * inv_l) << 16);
+      const uint32_t w1 = (uint32_t)f32_to_bf16(o[dt][4 * v4 + 2] * inv_l) |
+                          ((uint32_t)f32_to_bf16(o[dt][4 * v4 + 3] * inv_l) << 16);
       *(uint2*)(op + d0) = make_uint2(w0, w1);
     }
   if (P.lse && lk == 0) P.lse[((size_t)bi * P.H + h) * n + t] = (m_run + log2f(l_run)) * LN2;
@@ -278,8 +299,14 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
   if (a.n <= 0 || a.b <= 0) return hipSuccess;
   if (dtype == SAS_BF16) {
     dim3 grid(cdiv(a.n, 128), a.H, a.b);
-    if (a.dh == 128) attn_bf16_kernel<128><<<grid, 256, 0, s>>>(a);
-    else attn_bf16_kernel<64><<<grid, 256, 0, s>>>(a);
+    const bool single = a.B >= 64;
+    if (a.dh == 128) {
+      if (single) attn_bf16_kernel<128, true><<<grid, 256, 0, s>>>(a);
+      else attn_bf16_kernel<128, false><<<grid, 256, 0, s>>>(a);
+    } else {
+      if (single) attn_bf16_kernel<64, true><<<grid, 256, 0, s>>>(a);
+      else attn_bf16_kernel<64, false><<<grid, 256, 0, s>>>(a);
+    }
   } else {
     size_t tot = (size_t)a.b * a.H * a.n;
     unsigned grid = (unsigned)((tot + 127) / 128);

@@ -4,38 +4,69 @@
 
 namespace sas {
 
-// One workgroup of 256 threads per row; the row is read twice (L2-resident),
-// sum of squares in fp32, output rounded once to the activation dtype.
-template <typename T>
+// One workgroup of 256 threads per row; each thread keeps its 16-byte
+// chunks of the row in registers between the sum of squares (fp32) and the
+// scaled write, rounded once to the activation dtype.
+template <typename T, int CPT>
 __global__ void __launch_bounds__(256) rmsnorm_kernel(const T* __restrict__ x, const T* __restrict__ gamma,
                                                       T* __restrict__ out, int d, float eps) {
+  constexpr int EPC = 16 / sizeof(T);  // elements per 16-byte chunk
   const size_t row = blockIdx.x;
   const T* xr = x + row * (size_t)d;
+  T* o = out + row * (size_t)d;
+  const int nch = d / EPC;
+  uint4 v[CPT];
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += 256) {
-    float v = Act<T>::to_f32(xr[i]);
-    ss += v * v;
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int c = threadIdx.x + i * 256;
+    v[i] = c < nch ? *(const uint4*)(xr + (size_t)c * EPC) : make_uint4(0, 0, 0, 0);
+    const T* e = (const T*)&v[i];
+#pragma unroll
+    for (int k = 0; k < EPC; ++k) {
+      const float f = Act<T>::to_f32(e[k]);
+      ss += f * f;
+    }
   }
   ss = wave_sum(ss);
   __shared__ float part[4];
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
   __syncthreads();
-  float tot = part[0] + part[1] + part[2] + part[3];
-  float inv = 1.0f / sqrtf(tot / (float)d + eps);
-  T* o = out + row * (size_t)d;
-  for (int i = threadIdx.x; i < d; i += 256) {
-    float v = Act<T>::to_f32(xr[i]) * inv * Act<T>::to_f32(gamma[i]);
-    o[i] = Act<T>::from_f32(v);
+  const float tot = part[0] + part[1] + part[2] + part[3];
+  const float inv = 1.0f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int c = threadIdx.x + i * 256;
+    if (c >= nch) continue;
+    const uint4 gv = *(const uint4*)(gamma + (size_t)c * EPC);
+    const T* e = (const T*)&v[i];
+    const T* ge = (const T*)&gv;
+    uint4 r;
+    T* re = (T*)&r;
+#pragma unroll
+    for (int k = 0; k < EPC; ++k) re[k] = Act<T>::from_f32(Act<T>::to_f32(e[k]) * inv * Act<T>::to_f32(ge[k]));
+    *(uint4*)(o + (size_t)c * EPC) = r;
   }
 }
 
 hipError_t launch_rmsnorm(int dtype, const void* x, const void* gamma, void* out, int rows, int d,
                           float eps, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  if (dtype == SAS_BF16)
-    rmsnorm_kernel<bf16_t><<<rows, 256, 0, s>>>((const bf16_t*)x, (const bf16_t*)gamma, (bf16_t*)out, d, eps);
-  else
-    rmsnorm_kernel<float><<<rows, 256, 0, s>>>((const float*)x, (const float*)gamma, (float*)out, d, eps);
+  // d is a multiple of 8 (validated); up to 16 chunks of 16 bytes per thread
+  const int epc = dtype == SAS_BF16 ? 8 : 4;
+  const int cpt = (d / epc + 255) / 256;
+  if (cpt > 16) return hipErrorInvalidValue;
+#define RMS_LAUNCH(T, C) rmsnorm_kernel<T, C><<<rows, 256, 0, s>>>((const T*)x, (const T*)gamma, (T*)out, d, eps)
+  if (dtype == SAS_BF16) {
+    if (cpt <= 2) RMS_LAUNCH(bf16_t, 2);
+    else if (cpt <= 4) RMS_LAUNCH(bf16_t, 4);
+    else RMS_LAUNCH(bf16_t, 16);
+  } else {
+    if (cpt <= 2) RMS_LAUNCH(float, 2);
+    else if (cpt <= 4) RMS_LAUNCH(float, 4);
+    else RMS_LAUNCH(float, 16);
+  }
+#undef RMS_LAUNCH
   return hipGetLastError();
 }
 

@@ -50,12 +50,17 @@ hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s);
 // to `kplain` (scratch), otherwise `ksum` holds the plain summary.
 hipError_t launch_block_summaries(int dtype, const void* K, int b, int n, int Hkv, int dh, int B,
                                   const void* w_gk, void* kplain, void* ksum, hipStream_t s);
+// Gate queries qhat[b, Hkv, n, dh]: the group's query heads summed (fp64,
+// ascending head index) and rounded once; projected by w_gq when given (the
+// unprojected query then goes to `qplain`, scratch).
+hipError_t launch_gate_query(int dtype, const void* Q, int b, int n, int H, int Hkv, int dh, const void* w_gq,
+                             void* qplain, void* qhat, hipStream_t s);
 // Per (b, group, query) selection (Top-K, gate, tau) against kbar.
 struct SelectArgs {
   int b, n, H, Hkv, dh, B, K, NB;
-  const void* Q;          // [b, n, H, dh]
+  const void* Q;          // [b, n, H, dh]: gate query = rounded sum of the group's heads
+  const void* qhat;       // [b, Hkv, n, dh] precomputed gate queries (projection) or null
   const void* kbar;       // [b, Hkv, NB, dh]
-  const void* w_gq;       // [Hkv, dh, dh] or null
   int32_t* sel;           // [b, Hkv, n, K] (required, scratch or user)
   float* sel_bias;        // [b, Hkv, n, K] log g of each kept block (required)
   float* log_gate;        // [b, Hkv, n, NB] optional

@@ -16,27 +16,66 @@
 namespace sas {
 
 // ---------------------------------------------------------------------------
-// Block summaries: thread per (b, g, m, j).
+// 8 consecutive activation values as floats (one 16-byte load for bf16).
+template <typename T> struct Vec8;
+template <> struct Vec8<bf16_t> {
+  uint4 u;
+  __device__ __forceinline__ void load(const bf16_t* p) { u = *(const uint4*)p; }
+  __device__ __forceinline__ float get(int e) const {
+    const uint32_t w = e < 2 ? u.x : e < 4 ? u.y : e < 6 ? u.z : u.w;
+    return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+  }
+};
+template <> struct Vec8<float> {
+  float4 a, b;
+  __device__ __forceinline__ void load(const float* p) {
+    a = *(const float4*)p;
+    b = *(const float4*)(p + 4);
+  }
+  __device__ __forceinline__ float get(int e) const {
+    const float4& v = e < 4 ? a : b;
+    const int k = e & 3;
+    return k == 0 ? v.x : k == 1 ? v.y : k == 2 ? v.z : v.w;
+  }
+};
+
+// Block summaries: thread per (b, g, m, 8-dim chunk); the B keys of the block
+// are read 8 at a time (independent 16-byte loads) and summed per dimension
+// in fp64 in ascending token order.
 template <typename T>
 __global__ void summaries_kernel(const T* __restrict__ K, T* __restrict__ out, int n, int Hkv, int dh,
                                  int B, int NB, size_t total) {
-  size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= total) return;
-  int j = (int)(idx % dh);
-  size_t r = idx / dh;
-  int m = (int)(r % NB);
+  const int nc = dh / 8;
+  const int c8 = (int)(idx % nc);
+  size_t r = idx / nc;
+  const int m = (int)(r % NB);
   r /= NB;
-  int g = (int)(r % Hkv);
-  int bi = (int)(r / Hkv);
+  const int g = (int)(r % Hkv);
+  const int bi = (int)(r / Hkv);
+  T* o = out + (((size_t)bi * Hkv + g) * NB + m) * dh + c8 * 8;
   if ((m + 1) * B > n) {  // incomplete block: no summary
-    out[idx] = Act<T>::from_f32(0.f);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = Act<T>::from_f32(0.f);
     return;
   }
-  const T* p = K + (((size_t)bi * n + (size_t)m * B) * Hkv + g) * dh + j;
+  const T* p = K + (((size_t)bi * n + (size_t)m * B) * Hkv + g) * dh + c8 * 8;
   const size_t stride = (size_t)Hkv * dh;
-  double acc = 0.0;
-  for (int i = 0; i < B; ++i) acc += (double)Act<T>::to_f32(p[(size_t)i * stride]);
-  out[idx] = Act<T>::from_f64(acc / (double)B);
+  double acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+  for (int i0 = 0; i0 < B; i0 += 8) {
+    Vec8<T> v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q].load(p + (size_t)(i0 + q) * stride);
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] += (double)v[q].get(e);
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = Act<T>::from_f64(acc[e] / (double)B);
 }
 
 // Per-group projection out[.., g, m, k] = rho(sum_j W[g, k, j] * in[.., g, m, j]).
@@ -56,17 +95,60 @@ __global__ void project_kernel(const T* __restrict__ in, const T* __restrict__ W
   out[idx] = Act<T>::from_f64(acc);
 }
 
+// Gate query qhat[b, g, t, j] = rho(sum over the group's heads of Q[b, t, h, j]),
+// fp64 sum in ascending head order: thread per (b, g, t, j).
+template <typename T>
+__global__ void gate_query_kernel(const T* __restrict__ Q, T* __restrict__ out, int n, int H, int Hkv, int dh,
+                                  size_t total) {
+  size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int j = (int)(idx % dh);
+  size_t r = idx / dh;
+  const int t = (int)(r % n);
+  r /= n;
+  const int g = (int)(r % Hkv);
+  const int bi = (int)(r / Hkv);
+  const int G = H / Hkv;
+  const T* q = Q + (((size_t)bi * n + t) * H + (size_t)g * G) * dh + j;
+  double acc = 0.0;
+  for (int h = 0; h < G; ++h) acc += (double)Act<T>::to_f32(q[(size_t)h * dh]);
+  out[idx] = Act<T>::from_f64(acc);
+}
+
+hipError_t launch_gate_query(int dtype, const void* Q, int b, int n, int H, int Hkv, int dh, const void* w_gq,
+                             void* qplain, void* qhat, hipStream_t s) {
+  const size_t total = (size_t)b * Hkv * n * dh;
+  if (total == 0) return hipSuccess;
+  const unsigned grid = (unsigned)((total + 255) / 256);
+  void* dst = w_gq ? qplain : qhat;
+  if (dtype == SAS_BF16)
+    gate_query_kernel<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)Q, (bf16_t*)dst, n, H, Hkv, dh, total);
+  else
+    gate_query_kernel<float><<<grid, 256, 0, s>>>((const float*)Q, (float*)dst, n, H, Hkv, dh, total);
+  if (w_gq) {
+    if (dtype == SAS_BF16)
+      project_kernel<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)qplain, (const bf16_t*)w_gq, (bf16_t*)qhat,
+                                                  Hkv, n, dh, total);
+    else
+      project_kernel<float><<<grid, 256, 0, s>>>((const float*)qplain, (const float*)w_gq, (float*)qhat, Hkv,
+                                                 n, dh, total);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_block_summaries(int dtype, const void* K, int b, int n, int Hkv, int dh, int B,
                                   const void* w_gk, void* kplain, void* ksum, hipStream_t s) {
   const int NB = cdiv(n, B);
   const size_t total = (size_t)b * Hkv * NB * dh;
   if (total == 0) return hipSuccess;
   const unsigned grid = (unsigned)((total + 255) / 256);
+  const size_t tchunks = total / 8;
+  const unsigned sgrid = (unsigned)((tchunks + 63) / 64);
   void* dst = w_gk ? kplain : ksum;
   if (dtype == SAS_BF16)
-    summaries_kernel<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)K, (bf16_t*)dst, n, Hkv, dh, B, NB, total);
+    summaries_kernel<bf16_t><<<sgrid, 64, 0, s>>>((const bf16_t*)K, (bf16_t*)dst, n, Hkv, dh, B, NB, tchunks);
   else
-    summaries_kernel<float><<<grid, 256, 0, s>>>((const float*)K, (float*)dst, n, Hkv, dh, B, NB, total);
+    summaries_kernel<float><<<sgrid, 64, 0, s>>>((const float*)K, (float*)dst, n, Hkv, dh, B, NB, tchunks);
   if (w_gk) {
     // rows of incomplete blocks are zero and project to zero
     if (dtype == SAS_BF16)
@@ -83,55 +165,50 @@ hipError_t launch_block_summaries(int dtype, const void* K, int b, int n, int Hk
 // Selection: one wave per 64 consecutive query rows of one (batch, group).
 constexpr int SEL_MC = 16;  // summaries staged in LDS per step
 
-template <typename T, int DH>
-__device__ __forceinline__ double dot_f64(const float (&q)[DH], const float* __restrict__ kb) {
-  double acc = 0.0;
-#pragma unroll
-  for (int j = 0; j < DH; j += 4) {
-    float4 k4 = *(const float4*)(kb + j);
-    acc = fma((double)q[j + 0], (double)k4.x, acc);
-    acc = fma((double)q[j + 1], (double)k4.y, acc);
-    acc = fma((double)q[j + 2], (double)k4.z, acc);
-    acc = fma((double)q[j + 3], (double)k4.w, acc);
-  }
-  return acc;
-}
-
 template <typename T, int DH, int KMAX>
 __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
-  __shared__ __align__(16) float kb[SEL_MC][DH];
-  extern __shared__ __align__(16) float qs_dyn[];  // [WAVE][DH + 4]: pre-projection gate query (W_gq only)
+  __shared__ __align__(16) float kb[SEL_MC][DH];       // summaries of the current chunk
+  __shared__ __align__(16) T qs[WAVE][DH + 8];         // this wave's 64 gate queries
   const int lane = threadIdx.x;
   const int g = blockIdx.y, bi = blockIdx.z;
-  const int t = blockIdx.x * WAVE + lane;
+  const int t0 = blockIdx.x * WAVE;
+  const int t = t0 + lane;
   const bool valid = t < P.n;
   const int G = P.H / P.Hkv;
   const int ct = valid ? t / P.B : 0;
-  const int t_last = min(P.n - 1, (int)blockIdx.x * WAVE + WAVE - 1);
+  const int t_last = min(P.n - 1, t0 + WAVE - 1);
   const int cmax = t_last / P.B;  // wave-uniform loop bound
   const double inv_scale = 1.0 / ((double)G * sqrt((double)DH));
 
-  // gate query: rho(sum of the group's query heads), optionally projected
-  float q[DH];
+  // stage the 64 gate queries: either the precomputed (projected) rows, or
+  // the group's query heads summed here in fp64 and rounded once
   {
-    const T* Qr = (const T*)P.Q + (((size_t)bi * P.n + (valid ? t : 0)) * P.H + (size_t)g * G) * DH;
+    constexpr int NC = DH / 8;  // 8-value chunks per row
+    const int rows = t_last - t0 + 1;
+#pragma unroll 4
+    for (int i = 0; i < NC; ++i) {
+      const int c = lane + i * WAVE;
+      const int r = c / NC, c8 = c % NC;
+      const int rr = min(r, rows - 1);
+      double acc[8];
+      if (P.qhat) {
+        Vec8<T> v;
+        v.load((const T*)P.qhat + (((size_t)bi * P.Hkv + g) * P.n + t0 + rr) * DH + c8 * 8);
 #pragma unroll
-    for (int j = 0; j < DH; ++j) {
-      double acc = 0.0;
-      for (int h = 0; h < G; ++h) acc += (double)Act<T>::to_f32(Qr[(size_t)h * DH + j]);
-      q[j] = Act<T>::to_f32(Act<T>::from_f64(acc));
-    }
-    if (P.w_gq) {
+        for (int e = 0; e < 8; ++e) acc[e] = v.get(e);
+      } else {
+        const T* qp = (const T*)P.Q + (((size_t)bi * P.n + t0 + rr) * P.H + (size_t)g * G) * DH + c8 * 8;
 #pragma unroll
-      for (int j = 0; j < DH; ++j) qs_dyn[lane * (DH + 4) + j] = q[j];
-      const T* W = (const T*)P.w_gq + (size_t)g * DH * DH;
+        for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+        for (int h = 0; h < G; ++h) {
+          Vec8<T> v;
+          v.load(qp + (size_t)h * DH);
 #pragma unroll
-      for (int k = 0; k < DH; ++k) {
-        double acc = 0.0;
-        for (int j = 0; j < DH; ++j)
-          acc = fma((double)Act<T>::to_f32(W[(size_t)k * DH + j]), (double)qs_dyn[lane * (DH + 4) + j], acc);
-        q[k] = Act<T>::to_f32(Act<T>::from_f64(acc));
+          for (int e = 0; e < 8; ++e) acc[e] += (double)v.get(e);
+        }
       }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qs[r][c8 * 8 + e] = r < rows ? Act<T>::from_f64(acc[e]) : Act<T>::from_f32(0.f);
     }
   }
 
@@ -149,27 +226,55 @@ __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
   for (int m0 = 0; m0 < cmax; m0 += SEL_MC) {
     const int mc = min(SEL_MC, cmax - m0);
     __syncthreads();
-    for (int e = lane; e < mc * DH; e += WAVE) kb[e / DH][e % DH] = Act<T>::load(kbar, (size_t)m0 * DH + e);
+    {
+      constexpr int NC = DH / 8;
+#pragma unroll
+      for (int i = 0; i < SEL_MC * NC / WAVE; ++i) {
+        const int c = lane + i * WAVE;
+        const int r = c / NC, c8 = c % NC;
+        Vec8<T> v;
+        v.load(kbar + (size_t)(m0 + min(r, mc - 1)) * DH + c8 * 8);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) kb[r][c8 * 8 + e] = r < mc ? v.get(e) : 0.f;
+      }
+    }
     __syncthreads();
-    for (int mm = 0; mm < mc; ++mm) {
+    // r[mm] = sum_j q_j kbar[m0+mm]_j: one fp64 FMA chain per block, j ascending
+    double r[SEL_MC];
+#pragma unroll
+    for (int mm = 0; mm < SEL_MC; ++mm) r[mm] = 0.0;
+    for (int j = 0; j < DH; j += 4) {
+      const double q0 = Act<T>::to_f32(qs[lane][j]), q1 = Act<T>::to_f32(qs[lane][j + 1]);
+      const double q2 = Act<T>::to_f32(qs[lane][j + 2]), q3 = Act<T>::to_f32(qs[lane][j + 3]);
+#pragma unroll
+      for (int mm = 0; mm < SEL_MC; ++mm) {
+        const float4 k4 = *(const float4*)&kb[mm][j];
+        r[mm] = fma(q0, (double)k4.x, r[mm]);
+        r[mm] = fma(q1, (double)k4.y, r[mm]);
+        r[mm] = fma(q2, (double)k4.z, r[mm]);
+        r[mm] = fma(q3, (double)k4.w, r[mm]);
+      }
+    }
+#pragma unroll
+    for (int mm = 0; mm < SEL_MC; ++mm) {
       const int m = m0 + mm;
-      if (m >= ct) continue;
-      double r = dot_f64<T, DH>(q, kb[mm]);
-      double sv = r * inv_scale;
+      if (mm >= mc || m >= ct) continue;
+      const double rv = r[mm];
+      const double sv = rv * inv_scale;
       if (sv > mrun) {
         lrun = lrun * expf((float)(mrun - sv)) + 1.f;
         mrun = sv;
       } else {
         lrun += expf((float)(sv - mrun));
       }
-      if (r > tr[KMAX - 1]) {
-        double cr = r;
+      if (rv > tr[KMAX - 1]) {
+        double cr = rv;
         int cm = m;
 #pragma unroll
         for (int i = 0; i < KMAX; ++i) {
-          bool better = cr > tr[i];  // strict: an equal key keeps the lower index ahead
-          double orr = tr[i];
-          int om = tm[i];
+          const bool better = cr > tr[i];  // strict: an equal key keeps the lower index ahead
+          const double orr = tr[i];
+          const int om = tm[i];
           tr[i] = better ? cr : orr;
           tm[i] = better ? cm : om;
           cr = better ? orr : cr;
@@ -201,14 +306,14 @@ __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
   // order the kept blocks by index (odd-even transposition; empty slots last)
 #pragma unroll
   for (int i = 0; i < KMAX; ++i)
-    if (i >= kk) { tm[i] = 0x7fffffff; }
+    if (i >= kk) tm[i] = 0x7fffffff;
 #pragma unroll
   for (int pass = 0; pass < KMAX; ++pass) {
 #pragma unroll
     for (int i = (pass & 1); i + 1 < KMAX; i += 2) {
-      bool sw = tm[i] > tm[i + 1];
-      int a = tm[i], c = tm[i + 1];
-      double ra = tr[i], rc = tr[i + 1];
+      const bool sw = tm[i] > tm[i + 1];
+      const int a = tm[i], c = tm[i + 1];
+      const double ra = tr[i], rc = tr[i + 1];
       tm[i] = sw ? c : a;
       tm[i + 1] = sw ? a : c;
       tr[i] = sw ? rc : ra;
@@ -226,14 +331,15 @@ __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
   }
 
   if (P.log_gate) {
+    // every historical block's log gate: the scores again, same summation order
     float* lg = P.log_gate + row * P.NB;
     for (int m = 0; m < P.NB; ++m) {
       float v = -INFINITY;
       if (m < ct) {
         const T* kr = kbar + (size_t)m * DH;
         double acc = 0.0;
-#pragma unroll
-        for (int j = 0; j < DH; ++j) acc = fma((double)q[j], (double)Act<T>::to_f32(kr[j]), acc);
+        for (int j = 0; j < DH; ++j)
+          acc = fma((double)Act<T>::to_f32(qs[lane][j]), (double)Act<T>::to_f32(kr[j]), acc);
         v = (float)(acc * inv_scale - lse);
       }
       lg[m] = v;
@@ -244,10 +350,9 @@ __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
 template <typename T, int DH>
 static void run_select(const SelectArgs& a, hipStream_t s) {
   dim3 grid(cdiv(a.n, WAVE), a.Hkv, a.b);
-  const size_t lds = a.w_gq ? (size_t)WAVE * (DH + 4) * sizeof(float) : 0;
-  if (a.K <= 8) select_kernel<T, DH, 8><<<grid, WAVE, lds, s>>>(a);
-  else if (a.K <= 16) select_kernel<T, DH, 16><<<grid, WAVE, lds, s>>>(a);
-  else select_kernel<T, DH, 32><<<grid, WAVE, lds, s>>>(a);
+  if (a.K <= 8) select_kernel<T, DH, 8><<<grid, WAVE, 0, s>>>(a);
+  else if (a.K <= 16) select_kernel<T, DH, 16><<<grid, WAVE, 0, s>>>(a);
+  else select_kernel<T, DH, 32><<<grid, WAVE, 0, s>>>(a);
 }
 
 hipError_t launch_select(int dtype, const SelectArgs& a, hipStream_t s) {
