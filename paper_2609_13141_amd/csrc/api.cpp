@@ -202,10 +202,10 @@ LayerWs carve_layer(Carve& cv, const sas_config* c, int b, int n) {
 sas_status run_attention(const sas_config* c, int b, int n, const void* q, const void* k, const void* v,
                          const void* w_gq, const void* w_gk, void* o, float* lse, void* k_summary,
                          int32_t* sel_idx, float* log_gate, float* tau, const AttnWs& ws,
-                         hipStream_t s) {
+                         hipStream_t s, bool need_summary = false) {
   const int NB = cdiv(n, c->block_size);
   const int H = c->n_heads, Hkv = c->n_kv_heads, dh = c->head_dim;
-  const bool need_sel = c->mode != SAS_MODE_DENSE || sel_idx || log_gate || tau || k_summary;
+  const bool need_sel = c->mode != SAS_MODE_DENSE || sel_idx || log_gate || tau || k_summary || need_summary;
   void* ksum = k_summary ? k_summary : ws.ksum;
   int32_t* sel = sel_idx ? sel_idx : ws.sel;
   if (need_sel) {
@@ -318,6 +318,112 @@ sas_status check_weights(const sas_layer_weights* w, bool attn, bool mlp) {
   return SAS_OK;
 }
 
+sas_status check_cache(const sas_config* c, const sas_paged_kv* kv) {
+  SAS_TRY(check_ptr(kv->k_pages, "cache.k_pages", true));
+  SAS_TRY(check_ptr(kv->v_pages, "cache.v_pages", true));
+  SAS_TRY(check_ptr(kv->block_table, "cache.block_table", true));
+  SAS_TRY(check_ptr(kv->k_summary, "cache.k_summary", true));
+  if (kv->page_size <= 0 || kv->num_pages <= 0 || kv->max_pages_per_seq <= 0 || kv->max_blocks <= 0)
+    return fail(SAS_ERR_INVALID_ARGUMENT, "cache geometry must be positive (page_size %d, num_pages %d, "
+                "max_pages_per_seq %d, max_blocks %d)", kv->page_size, kv->num_pages, kv->max_pages_per_seq,
+                kv->max_blocks);
+  if (c->block_size % kv->page_size != 0)
+    return fail(SAS_ERR_INVALID_ARGUMENT, "block_size %d is not a multiple of page_size %d", c->block_size,
+                kv->page_size);
+  if (kv->max_blocks > 2048)
+    return fail(SAS_ERR_UNSUPPORTED, "max_blocks %d (supported: <= 2048)", kv->max_blocks);
+  return SAS_OK;
+}
+
+DecodeArgs decode_args(const sas_config* c, int b, const int32_t* pos, const sas_paged_kv* kv,
+                       const sas_layer_weights* w) {
+  DecodeArgs d;
+  d.b = b;
+  d.H = c->n_heads;
+  d.Hkv = c->n_kv_heads;
+  d.dh = c->head_dim;
+  d.B = c->block_size;
+  d.K = c->top_k;
+  d.d = c->d_model;
+  d.F = c->d_ff;
+  d.sm_scale = sm_scale_of(c);
+  d.eps = c->rms_eps;
+  d.rope_base = c->rope_base;
+  d.pos = pos;
+  d.k_pages = kv->k_pages;
+  d.v_pages = kv->v_pages;
+  d.block_table = kv->block_table;
+  d.k_summary = kv->k_summary;
+  d.num_pages = kv->num_pages;
+  d.page_size = kv->page_size;
+  d.max_pages = kv->max_pages_per_seq;
+  d.max_blocks = kv->max_blocks;
+  d.w_gq = w ? w->w_gq : nullptr;
+  d.w_gk = w ? w->w_gk : nullptr;
+  return d;
+}
+
+// Linear layer of a few rows (decode): the streaming kernel when it applies,
+// else the tiled GEMM (rope table indexed by row).
+hipError_t small_gemm(int dtype, GemmArgs g, hipStream_t s) {
+  if (dtype == SAS_BF16 && g.M <= 16 && g.K % 128 == 0) return launch_gemv(g, s);
+  g.seq_len = g.M;
+  g.row_pos = nullptr;
+  return launch_gemm(dtype, g, s);
+}
+
+struct DecodeWs {
+  void* u1;
+  float2* rope;
+  void* q;
+  void* k;
+  void* v;
+  void* kplain;
+  int32_t* sel;
+  float* part_ml;
+  float* part_o;
+  void* o;
+  void* h1;
+  MlpWs mlp;
+};
+
+DecodeWs carve_decode(Carve& cv, const sas_config* c, int b) {
+  const size_t ab = act_bytes(c);
+  const size_t H = c->n_heads, Hkv = c->n_kv_heads, dh = c->head_dim, K = c->top_k;
+  DecodeWs w;
+  w.u1 = cv.take((size_t)b * c->d_model * ab);
+  w.rope = (float2*)cv.take((size_t)b * (dh / 2) * sizeof(float2));
+  w.q = cv.take((size_t)b * H * dh * ab);
+  w.k = cv.take((size_t)b * Hkv * dh * ab);
+  w.v = cv.take((size_t)b * Hkv * dh * ab);
+  w.kplain = cv.take((size_t)b * Hkv * dh * ab);
+  w.sel = (int32_t*)cv.take((size_t)b * Hkv * (K > 0 ? K : 1) * 4);
+  w.part_ml = (float*)cv.take((size_t)b * H * (K + 1) * 2 * 4);
+  w.part_o = (float*)cv.take((size_t)b * H * (K + 1) * dh * 4);
+  w.o = cv.take((size_t)b * H * dh * ab);
+  w.h1 = cv.take((size_t)b * c->d_model * ab);
+  w.mlp = carve_mlp(cv, c, (size_t)b);
+  return w;
+}
+
+constexpr int ARGMAX_SLICES = 64;
+
+struct LmWs {
+  void* u;
+  float* logits;
+  float* pv;
+  int32_t* pi;
+};
+
+LmWs carve_lm(Carve& cv, const sas_config* c, int b, int vocab) {
+  LmWs w;
+  w.u = cv.take((size_t)b * c->d_model * act_bytes(c));
+  w.logits = (float*)cv.take((size_t)b * vocab * 4);
+  w.pv = (float*)cv.take((size_t)b * ARGMAX_SLICES * 4);
+  w.pi = (int32_t*)cv.take((size_t)b * ARGMAX_SLICES * 4);
+  return w;
+}
+
 sas_status check_ws(void* ws, size_t ws_bytes, size_t need) {
   if (need == 0) return SAS_OK;
   if (!ws) return fail(SAS_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
@@ -365,6 +471,14 @@ size_t sas_workspace_size(const sas_config* c, int32_t op, int32_t batch, int32_
     case SAS_OP_LAYER:
       if (seq_len <= 0 || check_config(c, true) != SAS_OK) return 0;
       carve_layer(cv, c, batch, seq_len);
+      break;
+    case SAS_OP_DECODE:
+      if (check_config(c, true) != SAS_OK) return 0;
+      carve_decode(cv, c, batch);
+      break;
+    case SAS_OP_LM_HEAD:
+      if (seq_len <= 0 || !c || (c->dtype != SAS_F32 && c->dtype != SAS_BF16) || c->d_model <= 0) return 0;
+      carve_lm(cv, c, batch, seq_len);
       break;
     default:
       return 0;
@@ -438,7 +552,7 @@ sas_status sas_layer_forward(const sas_config* c, int32_t batch, int32_t seq_len
     SAS_TRY(check_ptr(tp.v, "taps.v", false));
     SAS_TRY(check_ptr(tp.h1, "taps.h1", false));
   }
-  if (cache) return fail(SAS_ERR_UNSUPPORTED, "paged cache fill is not available yet");
+  if (cache) SAS_TRY(check_cache(c, cache));
   Carve cv(ws);
   LayerWs lw = carve_layer(cv, c, batch, seq_len);
   SAS_TRY(check_ws(ws, ws_bytes, cv.off));
@@ -480,7 +594,14 @@ sas_status sas_layer_forward(const sas_config* c, int32_t batch, int32_t seq_len
     HIP_TRY(launch_gemm(c->dtype, g, s), "qkv gemm");
   }
   SAS_TRY(run_attention(c, batch, seq_len, q, k, v, w->w_gq, w->w_gk, o, st.lse, st.k_summary, st.sel_idx,
-                        st.log_gate, st.tau, lw.att, s));
+                        st.log_gate, st.tau, lw.att, s, cache != nullptr));
+  if (cache) {
+    Timed tm("cache_fill", s);
+    const DecodeArgs da = decode_args(c, batch, nullptr, cache, w);
+    HIP_TRY(launch_cache_fill(c->dtype, k, v, st.k_summary ? st.k_summary : lw.att.ksum, batch, seq_len,
+                              c->n_kv_heads, c->head_dim, c->block_size, cdiv(seq_len, c->block_size), da, s),
+            "cache fill");
+  }
   GemmArgs og = {};
   og.epi = EPI_RESID;
   og.M = (int)T;
@@ -500,24 +621,165 @@ sas_status sas_layer_forward(const sas_config* c, int32_t batch, int32_t seq_len
 sas_status sas_decode_step(const sas_config* c, int32_t batch, const void* x, const int32_t* pos,
                            const sas_layer_weights* w, sas_paged_kv* cache, void* y, int32_t* sel_idx, void* ws,
                            size_t ws_bytes, void* stream) {
-  (void)c; (void)batch; (void)x; (void)pos; (void)w; (void)cache; (void)y; (void)sel_idx; (void)ws;
-  (void)ws_bytes; (void)stream;
-  return fail(SAS_ERR_UNSUPPORTED, "sas_decode_step is not available yet");
+  SAS_TRY(check_config(c, true));
+  if (batch <= 0) return fail(SAS_ERR_INVALID_ARGUMENT, "batch %d must be positive", batch);
+  SAS_TRY(check_ptr(x, "x", true));
+  SAS_TRY(check_ptr(pos, "pos", true));
+  SAS_TRY(check_ptr(y, "y", true));
+  SAS_TRY(check_ptr(sel_idx, "sel_idx", false));
+  SAS_TRY(check_weights(w, true, true));
+  if (!cache) return fail(SAS_ERR_INVALID_ARGUMENT, "cache is NULL");
+  SAS_TRY(check_cache(c, cache));
+  Carve cv(ws);
+  DecodeWs dw = carve_decode(cv, c, batch);
+  SAS_TRY(check_ws(ws, ws_bytes, cv.off));
+  hipStream_t s = (hipStream_t)stream;
+  const DecodeArgs da = decode_args(c, batch, pos, cache, w);
+  const int H = c->n_heads, Hkv = c->n_kv_heads, dh = c->head_dim;
+  int32_t* sel = sel_idx ? sel_idx : dw.sel;
+  {
+    Timed tm("rope_rows", s);
+    HIP_TRY(launch_rope_rows(pos, dw.rope, batch, dh, c->rope_base, s), "rope rows");
+  }
+  {
+    Timed tm("rmsnorm", s);
+    HIP_TRY(launch_rmsnorm(c->dtype, x, w->rms1, dw.u1, batch, c->d_model, c->rms_eps, s), "rmsnorm");
+  }
+  GemmArgs g = {};
+  g.epi = EPI_QKV_ROPE;
+  g.M = batch;
+  g.K = c->d_model;
+  g.A = dw.u1;
+  g.B0 = w->wq;
+  g.B1 = w->wk;
+  g.B2 = w->wv;
+  g.N = (H + 2 * Hkv) * dh;
+  g.out = dw.q;
+  g.out1 = dw.k;
+  g.out2 = dw.v;
+  g.n_heads = H;
+  g.n_kv_heads = Hkv;
+  g.head_dim = dh;
+  g.rope = dw.rope;
+  {
+    Timed tm("dec_qkv", s);
+    HIP_TRY(small_gemm(c->dtype, g, s), "qkv gemm");
+  }
+  {
+    Timed tm("dec_append", s);
+    HIP_TRY(launch_kv_append(c->dtype, dw.k, dw.v, da, dw.kplain, s), "kv append");
+  }
+  {
+    Timed tm("dec_select", s);
+    HIP_TRY(launch_decode_select(c->dtype, dw.q, da, sel, s), "decode select");
+  }
+  {
+    Timed tm("dec_attention", s);
+    HIP_TRY(launch_decode_attention(c->dtype, dw.q, da, sel, dw.part_ml, dw.part_o, dw.o, s), "decode attention");
+  }
+  GemmArgs og = {};
+  og.epi = EPI_RESID;
+  og.M = batch;
+  og.K = H * dh;
+  og.A = dw.o;
+  og.B0 = w->wo;
+  og.N = c->d_model;
+  og.resid = x;
+  og.out = dw.h1;
+  {
+    Timed tm("dec_o", s);
+    HIP_TRY(small_gemm(c->dtype, og, s), "o-proj gemm");
+  }
+  {
+    Timed tm("rmsnorm", s);
+    HIP_TRY(launch_rmsnorm(c->dtype, dw.h1, w->rms2, dw.mlp.u2, batch, c->d_model, c->rms_eps, s), "rmsnorm");
+  }
+  GemmArgs gu = {};
+  gu.epi = EPI_SWIGLU;
+  gu.M = batch;
+  gu.K = c->d_model;
+  gu.A = dw.mlp.u2;
+  gu.B0 = w->w_gate;
+  gu.B1 = w->w_up;
+  gu.N = c->d_ff;
+  gu.out = dw.mlp.a;
+  {
+    Timed tm("dec_gate_up", s);
+    HIP_TRY(small_gemm(c->dtype, gu, s), "gate/up gemm");
+  }
+  GemmArgs dg = {};
+  dg.epi = EPI_RESID;
+  dg.M = batch;
+  dg.K = c->d_ff;
+  dg.A = dw.mlp.a;
+  dg.B0 = w->w_down;
+  dg.N = c->d_model;
+  dg.resid = dw.h1;
+  dg.out = y;
+  {
+    Timed tm("dec_down", s);
+    HIP_TRY(small_gemm(c->dtype, dg, s), "down gemm");
+  }
+  return SAS_OK;
 }
 
 sas_status sas_embed(const sas_config* c, int32_t batch, int32_t seq_len, const int32_t* ids, const void* table,
                      int32_t vocab, const void* img_embed, int32_t n_img, void* x, void* stream) {
-  (void)c; (void)batch; (void)seq_len; (void)ids; (void)table; (void)vocab; (void)img_embed; (void)n_img;
-  (void)x; (void)stream;
-  return fail(SAS_ERR_UNSUPPORTED, "sas_embed is not available yet");
+  if (!c || (c->dtype != SAS_F32 && c->dtype != SAS_BF16) || c->d_model <= 0)
+    return fail(SAS_ERR_INVALID_ARGUMENT, "config is NULL or invalid");
+  if (batch <= 0 || seq_len <= 0 || vocab <= 0 || n_img < 0)
+    return fail(SAS_ERR_INVALID_ARGUMENT, "batch %d, seq_len %d, vocab %d must be positive, n_img %d >= 0", batch,
+                seq_len, vocab, n_img);
+  SAS_TRY(check_ptr(ids, "ids", true));
+  SAS_TRY(check_ptr(table, "table", true));
+  SAS_TRY(check_ptr(img_embed, "img_embed", false));
+  SAS_TRY(check_ptr(x, "x", true));
+  hipStream_t s = (hipStream_t)stream;
+  Timed tm("embed", s);
+  HIP_TRY(launch_embed(c->dtype, batch, seq_len, ids, table, vocab, img_embed, n_img, x, c->d_model, s), "embed");
+  return SAS_OK;
 }
 
 sas_status sas_lm_head_argmax(const sas_config* c, int32_t batch, const void* h, const void* gamma,
                               const void* w_lm, int32_t vocab, float* logits, int32_t* tokens, void* ws,
                               size_t ws_bytes, void* stream) {
-  (void)c; (void)batch; (void)h; (void)gamma; (void)w_lm; (void)vocab; (void)logits; (void)tokens; (void)ws;
-  (void)ws_bytes; (void)stream;
-  return fail(SAS_ERR_UNSUPPORTED, "sas_lm_head_argmax is not available yet");
+  if (!c || (c->dtype != SAS_F32 && c->dtype != SAS_BF16) || c->d_model <= 0 || c->d_model % 8)
+    return fail(SAS_ERR_INVALID_ARGUMENT, "config is NULL or invalid");
+  if (batch <= 0 || vocab <= 0)
+    return fail(SAS_ERR_INVALID_ARGUMENT, "batch %d and vocab %d must be positive", batch, vocab);
+  if (c->dtype == SAS_BF16 && (batch > 16 || c->d_model % 128))
+    return fail(SAS_ERR_UNSUPPORTED, "bf16 LM head needs batch <= 16 and d_model %% 128 == 0");
+  SAS_TRY(check_ptr(h, "h", true));
+  SAS_TRY(check_ptr(gamma, "gamma", true));
+  SAS_TRY(check_ptr(w_lm, "w_lm", true));
+  SAS_TRY(check_ptr(logits, "logits", false));
+  SAS_TRY(check_ptr(tokens, "tokens", true));
+  Carve cv(ws);
+  LmWs lw = carve_lm(cv, c, batch, vocab);
+  SAS_TRY(check_ws(ws, ws_bytes, cv.off));
+  hipStream_t s = (hipStream_t)stream;
+  float* lg = logits ? logits : lw.logits;
+  {
+    Timed tm("rmsnorm", s);
+    HIP_TRY(launch_rmsnorm(c->dtype, h, gamma, lw.u, batch, c->d_model, c->rms_eps, s), "rmsnorm");
+  }
+  GemmArgs g = {};
+  g.epi = EPI_F32OUT;
+  g.M = batch;
+  g.K = c->d_model;
+  g.A = lw.u;
+  g.B0 = w_lm;
+  g.N = vocab;
+  g.out = lg;
+  {
+    Timed tm("lm_head", s);
+    HIP_TRY(small_gemm(c->dtype, g, s), "lm head");
+  }
+  {
+    Timed tm("argmax", s);
+    HIP_TRY(launch_argmax(lg, batch, vocab, lw.pv, lw.pi, ARGMAX_SLICES, tokens, s), "argmax");
+  }
+  return SAS_OK;
 }
 
 }  // extern "C"

@@ -437,16 +437,17 @@ __global__ void gemm_f32_kernel(int epi, int M, int K, int N, int npairs, const 
                                 float* out, float* out1, float* out2, int H, int Hkv, int dh,
                                 int seq_len, const float2* __restrict__ rope,
                                 const int32_t* __restrict__ row_pos) {
-  const int cols = (epi == EPI_RESID) ? N : npairs;  // columns or pairs
+  const bool plain = epi == EPI_RESID || epi == EPI_F32OUT;
+  const int cols = plain ? N : npairs;  // columns or pairs
   const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (size_t)M * cols) return;
   const int row = (int)(idx / cols), c = (int)(idx % cols);
   const float* a = A + (size_t)row * K;
-  if (epi == EPI_RESID) {
+  if (plain) {
     const float* b = B0 + (size_t)c * K;
     float s = 0.f;
     for (int k = 0; k < K; ++k) s = fmaf(a[k], b[k], s);
-    out[(size_t)row * N + c] = resid[(size_t)row * N + c] + s;
+    out[(size_t)row * N + c] = (epi == EPI_RESID ? resid[(size_t)row * N + c] : 0.f) + s;
     return;
   }
   // logical pair c -> the two logical columns of the tile mapping
@@ -518,9 +519,10 @@ hipError_t launch_gemm(int dtype, const GemmArgs& g, hipStream_t s) {
   if (g.M <= 0) return hipSuccess;
   // pair epilogues: SWIGLU has F pairs, QKV has (H + 2 Hkv) dh / 2 pairs
   const int npairs = g.epi == EPI_SWIGLU ? g.N : (g.epi == EPI_QKV_ROPE ? g.N / 2 : 0);
-  const int nlog = g.epi == EPI_RESID ? g.N : (npairs + 31) / 32 * 64;
+  const bool plain = g.epi == EPI_RESID || g.epi == EPI_F32OUT;
+  const int nlog = plain ? g.N : (npairs + 31) / 32 * 64;
   if (dtype == SAS_F32) {
-    const int cols = (g.epi == EPI_RESID) ? g.N : npairs;
+    const int cols = plain ? g.N : npairs;
     size_t tot = (size_t)g.M * cols;
     gemm_f32_kernel<<<(unsigned)((tot + 255) / 256), 256, 0, s>>>(
         g.epi, g.M, g.K, nlog, npairs, (const float*)g.A, (const float*)g.B0, (const float*)g.B1,
@@ -556,6 +558,7 @@ hipError_t launch_gemm(int dtype, const GemmArgs& g, hipStream_t s) {
   P.rope = g.rope;
   P.row_pos = g.row_pos;
   const long big_tiles = (long)((g.M + 255) / 256) * ((nlog + 255) / 256);
+  if (g.epi == EPI_F32OUT) return hipErrorInvalidValue;  // bf16 fp32-output products go through gemv
   if (g.K % 64 == 0) {
     // Tile choice from measurements on MI355X: 256x256 (8 waves) wherever
     // there are enough tiles; for short M (one wave of tiles or less) the

@@ -19,7 +19,7 @@ hipError_t launch_rope_table(float2* rope, int n, int dh, float base, hipStream_
 
 // ---- gemm.hip --------------------------------------------------------------
 // C = A[M, K] * B[N, K]^T with one of three fused epilogues.
-enum GemmEpi { EPI_QKV_ROPE = 0, EPI_SWIGLU = 1, EPI_RESID = 2 };
+enum GemmEpi { EPI_QKV_ROPE = 0, EPI_SWIGLU = 1, EPI_RESID = 2, EPI_F32OUT = 3 };
 struct GemmArgs {
   int epi;
   int M, K;
@@ -42,6 +42,11 @@ struct GemmArgs {
   const int32_t* row_pos; // optional per-row positions (decode), else row % seq_len
 };
 hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s);
+
+// ---- gemv.hip --------------------------------------------------------------
+// The same products for M <= 16 rows (bf16, K % 128 == 0), streaming the
+// weights: rope is a per-row table [M, dh/2]; EPI_F32OUT writes fp32 A W^T.
+hipError_t launch_gemv(const GemmArgs& a, hipStream_t s);
 
 // ---- selector.hip ----------------------------------------------------------
 // Block summaries kbar[b, Hkv, NB, dh] of the complete blocks of K[b, n, Hkv, dh]
@@ -83,6 +88,8 @@ struct AttnArgs {
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 
 // ---- decode.hip ------------------------------------------------------------
+// rope[r, i] for the positions pos[r] of the new tokens (fp64 math).
+hipError_t launch_rope_rows(const int32_t* pos, float2* rope, int b, int dh, float base, hipStream_t s);
 struct DecodeArgs {
   int b, H, Hkv, dh, B, K, d, F;
   float sm_scale, eps, rope_base;
@@ -113,8 +120,9 @@ hipError_t launch_decode_attention(int dtype, const void* q, const DecodeArgs& c
 // ---- model_ends.hip --------------------------------------------------------
 hipError_t launch_embed(int dtype, int b, int n, const int32_t* ids, const void* table, int vocab,
                         const void* img, int n_img, void* x, int d, hipStream_t s);
-hipError_t launch_lm_head(int dtype, int b, int d, const void* u, const void* w_lm, int vocab,
-                          float* logits, int32_t* tokens, float* part_val, int32_t* part_idx,
-                          hipStream_t s);
+// tokens[r] = argmax of logits[r, :V] (lowest index on ties); scratch pv/pi
+// hold `slices` partial results per row.
+hipError_t launch_argmax(const float* logits, int b, int V, float* pv, int32_t* pi, int slices, int32_t* tokens,
+                         hipStream_t s);
 
 }  // namespace sas

@@ -269,6 +269,60 @@ def profiler_stop() -> list:
     return out
 
 
+def alloc_cache(cfg: Config, batch: int, max_len: int, page_size: int = 16, device="cuda",
+                shuffle_pages: bool = True, seed: int = 0) -> PagedCache:
+    """Zeroed paged KV cache for `batch` sequences of up to `max_len` tokens.
+    Pages are handed out in a seeded random order so that logical and
+    physical order differ."""
+    dt = torch.bfloat16 if cfg.dtype == SAS_BF16 else torch.float32
+    per_seq = -(-max_len // page_size)
+    num_pages = batch * per_seq
+    Hkv, dh = cfg.n_kv_heads, cfg.head_dim
+    k_pages = torch.zeros(num_pages, Hkv, page_size, dh, dtype=dt, device=device)
+    v_pages = torch.zeros_like(k_pages)
+    order = torch.randperm(num_pages, generator=torch.Generator().manual_seed(seed)) if shuffle_pages \
+        else torch.arange(num_pages)
+    block_table = order.to(torch.int32).reshape(batch, per_seq).to(device)
+    nblk = -(-max_len // cfg.block_size)
+    k_summary = torch.zeros(batch, Hkv, nblk, dh, dtype=dt, device=device)
+    return PagedCache(k_pages, v_pages, block_table, k_summary, page_size)
+
+
+def decode_step(cfg: Config, x, pos, W: dict, cache: PagedCache, *, sel_idx: bool = True,
+                ws: Workspace | None = None):
+    """One SAS decode step of one layer.  x [b, d]; pos [b] int32 (device)."""
+    b = x.shape[0]
+    y = torch.empty_like(x)
+    sel = torch.empty(b, cfg.n_kv_heads, cfg.top_k, dtype=torch.int32, device=x.device) if sel_idx else None
+    cs = cache.struct()
+    wsp, wsn = _ws(ws, workspace_size(cfg, OP_DECODE, b, 0))
+    _check(lib().sas_decode_step(C.byref(cfg), b, _ptr(x), _ptr(pos), C.byref(weights_struct(W)), C.byref(cs),
+                                 _ptr(y), _ptr(sel), wsp, wsn, _stream()))
+    return y, sel
+
+
+def embed(cfg: Config, ids, table, img=None):
+    """x [b, n, d] from token ids [b, n] (int32, -1 = next image row)."""
+    b, n = ids.shape
+    n_img = 0 if img is None else img.shape[1]
+    x = torch.empty(b, n, table.shape[1], dtype=table.dtype, device=table.device)
+    _check(lib().sas_embed(C.byref(cfg), b, n, _ptr(ids), _ptr(table), table.shape[0], _ptr(img), n_img, _ptr(x),
+                           _stream()))
+    return x
+
+
+def lm_head_argmax(cfg: Config, h, gamma, w_lm, *, logits: bool = False, ws: Workspace | None = None):
+    """Greedy next tokens [b] (int32) and optionally the fp32 logits."""
+    b = h.shape[0]
+    V = w_lm.shape[0]
+    tok = torch.empty(b, dtype=torch.int32, device=h.device)
+    lg = torch.empty(b, V, dtype=torch.float32, device=h.device) if logits else None
+    wsp, wsn = _ws(ws, workspace_size(cfg, OP_LM_HEAD, b, V))
+    _check(lib().sas_lm_head_argmax(C.byref(cfg), b, _ptr(h), _ptr(gamma), _ptr(w_lm), V, _ptr(lg), _ptr(tok),
+                                    wsp, wsn, _stream()))
+    return tok, lg
+
+
 def to_device(arr, dtype: str, device="cuda"):
     """float32 NumPy array (values exact in `dtype`) -> device tensor."""
     t = torch.from_numpy(arr)
