@@ -32,6 +32,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="7b_layer_1k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true", help="skip the decode-step measurement")
     ap.add_argument("--cpu-threads", type=int, default=0, help="oracle BLAS threads (0: affinity, max 16)")
     return ap.parse_args()
 
@@ -120,9 +121,83 @@ def main():
         "kernels_ms": {k: round(v, 4) for k, v in sorted(kern_ms.items(), key=lambda kv: -kv[1] * kern_calls[kv[0]])},
     }
 
+    if not args.no_decode:
+        del x, W, ws
+        torch.cuda.empty_cache()
+        line["decode"] = decode_bench(args.steps, args.warmup)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, x_np, W_np, cores)
     print(json.dumps(line), flush=True)
+
+
+def decode_bench(steps, warmup, n_inst=4):
+    """SAS decode step (Alg. 2) of one 7B-shape layer at the serving
+    workload's shape: 8 sequences, dense prefill of 2048 tokens into 16-token
+    pages, then steps at positions 2048, 2049, ...  Four layer instances with
+    their own weights and caches are chained so that every step streams its
+    weights from HBM (4 x 405 MB exceeds the 256 MB last-level cache)."""
+    import torch
+    from paper_2609_13141_amd import configs, inputs, sas
+    w = configs.STACK_DECODE
+    dev = "cuda:0"
+    W0 = sas.weights_to_device(inputs.layer_weights(w), w.dtype, dev)
+    Ws = [W0] + [{k: (None if v is None else v.clone()) for k, v in W0.items()} for _ in range(n_inst - 1)]
+    x = sas.to_device(inputs.embeddings(w), w.dtype, dev)
+    cfg_p, cfg_d = sas.make_config(w, "dense"), sas.make_config(w, "sparse")
+    max_len = w.seq_len + warmup + 2 * steps + 1
+    caches = [sas.alloc_cache(cfg_d, w.batch, max_len, page_size=w.page_size, seed=l) for l in range(n_inst)]
+    ws = sas.Workspace(dev)
+    for l in range(n_inst):
+        sas.layer_forward(cfg_p, x, Ws[l], stats=False, cache=caches[l], ws=ws)
+    h0 = x[:, -1].contiguous()
+    del x
+    poss = [torch.full((w.batch,), t, dtype=torch.int32, device=dev) for t in range(w.seq_len, max_len)]
+
+    def step(t):
+        h = h0
+        for l in range(n_inst):
+            h, _ = sas.decode_step(cfg_d, h, poss[t - w.seq_len], Ws[l], caches[l], sel_idx=False, ws=ws)
+        return h
+
+    t = w.seq_len
+    for _ in range(warmup):
+        step(t)
+        t += 1
+    torch.cuda.synchronize()
+    t_first = t
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step(t)
+        t += 1
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / (steps * n_inst)
+    # algorithmic bytes of one layer-step: weights, kept K/V, summaries, appended K/V
+    B, K, dh, Hkv, b = w.block_size, w.top_k, w.head_dim, w.n_kv_heads, w.batch
+    tot = 0.0
+    for tt in range(t_first, t):
+        ct = tt // B
+        kept = B * min(K, ct) + (tt % B) + 1
+        tot += 2.0 * w.linear_params() + b * Hkv * (kept * dh * 2 * 2 + ct * dh * 2 + 2 * dh * 2)
+    nbytes = tot / steps
+    sas.profiler_start(64 * steps * n_inst + 64)
+    for _ in range(steps):
+        step(t)
+        t += 1
+    recs = sas.profiler_stop()
+    fam = {}
+    for name, v in recs:
+        fam.setdefault(name, []).append(v)
+    kms = {k: sum(v) / len(v) for k, v in fam.items()}
+    gu_bytes = 2.0 * w.d_model * 2 * w.d_ff
+    return {"workload": f"{w.name}: one layer's decode step, batch {b}, positions {t_first}..{t_first + steps - 1}, "
+                        f"pages of {w.page_size}, B={B}, K={K}",
+            "ms_per_layer_step": round(ms, 4),
+            "tokens_per_s_32_layers": round(b / (32 * ms * 1e-3), 1),
+            "bytes_per_layer_step": int(nbytes),
+            "hbm_gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+            "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "gate_up_gemv_gbs": round(gu_bytes / (kms["dec_gate_up"] * 1e-3) / 1e9, 1),
+            "kernels_ms": {k: round(v, 4) for k, v in sorted(kms.items(), key=lambda kv: -kv[1])}}
 
 
 def cpu_baseline(w, x_np, W_np, cores):

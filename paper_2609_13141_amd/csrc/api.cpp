@@ -330,6 +330,8 @@ sas_status check_cache(const sas_config* c, const sas_paged_kv* kv) {
   if (c->block_size % kv->page_size != 0)
     return fail(SAS_ERR_INVALID_ARGUMENT, "block_size %d is not a multiple of page_size %d", c->block_size,
                 kv->page_size);
+  if (c->block_size / kv->page_size > 64)
+    return fail(SAS_ERR_UNSUPPORTED, "block_size / page_size = %d (supported: <= 64)", c->block_size / kv->page_size);
   if (kv->max_blocks > 2048)
     return fail(SAS_ERR_UNSUPPORTED, "max_blocks %d (supported: <= 2048)", kv->max_blocks);
   return SAS_OK;

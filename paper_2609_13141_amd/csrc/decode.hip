@@ -257,33 +257,29 @@ hipError_t launch_decode_select(int dtype, const void* q, const DecodeArgs& c, i
 }
 
 // ---- sparse attention of the new tokens ----------------------------------------
-// Workgroup per (chunk, group, sequence); chunk ch < K is the ch-th kept block,
-// ch == K the current block [B*floor(p/B), p].  Keys and values of the chunk
-// are gathered from the pages into LDS; for every query head of the group the
-// partial (max, sum of exp, unnormalised output) is written, in fp32.
-constexpr int DA_THREADS = 256;
-
-template <typename T, int DH>
-__global__ void __launch_bounds__(DA_THREADS) decode_attn_kernel(const T* __restrict__ q, DecodeArgs c,
-                                                                 const int32_t* __restrict__ sel,
-                                                                 float* __restrict__ part_ml,
-                                                                 float* __restrict__ part_o) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  const int B = c.B;
-  float* Ks = (float*)smem;               // [B][DH + 1]
-  float* Vs = Ks + (size_t)B * (DH + 1);  // [B][DH]
-  float* Ps = Vs + (size_t)B * DH;        // [B]
-  __shared__ float red[DA_THREADS / 64];
-  __shared__ float qv[DH];
-
-  const int tid = threadIdx.x;
+// One wave per (chunk, group, sequence); chunk ch < K is the ch-th kept block,
+// ch == K the current block [B*floor(p/B), p].  Nothing is staged in LDS: with
+// NC = dh/8 lanes per key, lane l holds the 8-value slice l % NC of keys
+// l / NC + (64/NC) * it, loaded with coalesced 16-byte loads (a page of one KV
+// head is contiguous).  A key's score is the partial dot product reduced over
+// its NC lanes with shuffles; P V accumulates per slice and is reduced over
+// the lanes that share a slice.  The partial (max, sum of exp, unnormalised
+// output) is written in fp32 and merged by decode_combine_kernel.
+template <typename T, int DH, int MAXKEYS>
+__global__ void __launch_bounds__(64) decode_attn_kernel(const T* __restrict__ q, DecodeArgs c,
+                                                         const int32_t* __restrict__ sel,
+                                                         float* __restrict__ part_ml, float* __restrict__ part_o) {
+  constexpr int NC = DH / 8;          // lanes per key (one 8-value slice each)
+  constexpr int KPI = 64 / NC;        // keys per load instruction
+  constexpr int IT = MAXKEYS / KPI;   // load steps
+  const int lane = threadIdx.x;
   const int ch = blockIdx.x, g = blockIdx.y, i = blockIdx.z;
-  const int K = c.K, G = c.H / c.Hkv;
+  const int K = c.K, G = c.H / c.Hkv, B = c.B;
   const int p = c.pos[i];
   int first = 0, count = 0;  // key positions [first, first + count)
   if (p >= 0) {
     if (ch < K) {
-      const int m = K > 0 ? sel[((size_t)i * c.Hkv + g) * K + ch] : -1;
+      const int m = sel[((size_t)i * c.Hkv + g) * K + ch];
       if (m >= 0) {
         first = m * B;
         count = B;
@@ -293,72 +289,82 @@ __global__ void __launch_bounds__(DA_THREADS) decode_attn_kernel(const T* __rest
       count = p - first + 1;
     }
   }
-  const PageGeom PG = geom_of(c);
-  // stage the chunk, 8 values per load (a missing page reads as zero)
-  {
-    constexpr int NC = DH / 8;
-    constexpr int MAXIT = 128 * NC / DA_THREADS;  // B <= 128
-#pragma unroll
-    for (int it = 0; it < MAXIT; ++it) {
-      const int e = tid + it * DA_THREADS;
-      if (e >= count * NC) break;
-      const int kl = e / NC, c8 = e % NC;
-      const long long off = PG.offset(i, g, first + kl, c.Hkv, DH);
-      Vec8<T> kv, vv;
-      if (off >= 0) {
-        kv.load((const T*)c.k_pages + off + c8 * 8);
-        vv.load((const T*)c.v_pages + off + c8 * 8);
-      }
-#pragma unroll
-      for (int x = 0; x < 8; ++x) {
-        Ks[kl * (DH + 1) + c8 * 8 + x] = off >= 0 ? kv.get(x) : 0.f;
-        Vs[kl * DH + c8 * 8 + x] = off >= 0 ? vv.get(x) : 0.f;
-      }
-    }
+  const int sl = lane % NC, kq = lane / NC;
+  // page ids of the chunk (blocks are page aligned): lane j holds page j
+  const int ps = c.page_size;
+  const int npg = (count + ps - 1) / ps;
+  int pid = -1;
+  if (lane < npg) {
+    const int pi = first / ps + lane;
+    if (pi < c.max_pages) pid = c.block_table[(size_t)i * c.max_pages + pi];
+    if (pid >= c.num_pages) pid = -1;
   }
+  const size_t kvstride = (size_t)c.Hkv * ps * DH;  // elements per page
   for (int hg = 0; hg < G; ++hg) {
     const int h = g * G + hg;
-    __syncthreads();
-    for (int j = tid; j < DH; j += DA_THREADS) qv[j] = Act<T>::to_f32(q[((size_t)i * c.H + h) * DH + j]);
-    __syncthreads();
-    // scores, one thread per key
-    float sc = -INFINITY;
-    for (int kl = tid; kl < count; kl += DA_THREADS) {
+    float qs[8];
+    {
+      Vec8<T> v;
+      v.load(q + ((size_t)i * c.H + h) * DH + sl * 8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qs[e] = v.get(e) * c.sm_scale;
+    }
+    float sc[IT];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int kl = kq + KPI * it;
+      sc[it] = -INFINITY;
+      if (KPI * it >= count) continue;
+      const int page = __shfl(pid, kl / ps, 64);
+      const bool ok = kl < count && page >= 0;
+      Vec8<T> kv;
+      if (ok) kv.load((const T*)c.k_pages + (size_t)page * kvstride + ((size_t)g * ps + kl % ps) * DH + sl * 8);
       float acc = 0.f;
-#pragma unroll 8
-      for (int j = 0; j < DH; ++j) acc = fmaf(qv[j], Ks[kl * (DH + 1) + j], acc);
-      acc *= c.sm_scale;
-      Ps[kl] = acc;
-      sc = fmaxf(sc, acc);
-    }
-    sc = wave_max(sc);
-    if ((tid & 63) == 0) red[tid >> 6] = sc;
-    __syncthreads();
-    float mx = red[0];
+      if (ok) {
 #pragma unroll
-    for (int w = 1; w < DA_THREADS / 64; ++w) mx = fmaxf(mx, red[w]);
-    __syncthreads();
-    float ls = 0.f;
-    for (int kl = tid; kl < count; kl += DA_THREADS) {
-      const float e = expf(Ps[kl] - mx);
-      Ps[kl] = e;
-      ls += e;
-    }
-    ls = wave_sum(ls);
-    if ((tid & 63) == 0) red[tid >> 6] = ls;
-    __syncthreads();
-    float lsum = 0.f;
+        for (int e = 0; e < 8; ++e) acc = fmaf(qs[e], kv.get(e), acc);
+      }
 #pragma unroll
-    for (int w = 0; w < DA_THREADS / 64; ++w) lsum += red[w];
+      for (int o = NC / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
+      sc[it] = kl < count ? acc : -INFINITY;
+      mx = fmaxf(mx, sc[it]);
+    }
+    mx = wave_max(mx);
+    float ls = 0.f, o[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = 0.f;
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int kl = kq + KPI * it;
+      if (KPI * it >= count) continue;
+      const int page = __shfl(pid, kl / ps, 64);
+      const bool ok = kl < count && page >= 0;
+      Vec8<T> vv;
+      if (ok) vv.load((const T*)c.v_pages + (size_t)page * kvstride + ((size_t)g * ps + kl % ps) * DH + sl * 8);
+      const float pk = kl < count ? __expf(sc[it] - mx) : 0.f;
+      ls += pk;
+      if (ok) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = fmaf(pk, vv.get(e), o[e]);
+      }
+    }
+    // lanes sharing a slice hold different keys: reduce over them
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+#pragma unroll
+      for (int off = NC; off < 64; off <<= 1) o[e] += __shfl_xor(o[e], off, 64);
+#pragma unroll
+    for (int off = NC; off < 64; off <<= 1) ls += __shfl_xor(ls, off, 64);  // each key once per slice
     const size_t pidx = ((size_t)i * c.H + h) * (K + 1) + ch;
-    for (int d = tid; d < DH; d += DA_THREADS) {
-      float acc = 0.f;
-      for (int kl = 0; kl < count; ++kl) acc = fmaf(Ps[kl], Vs[kl * DH + d], acc);
-      part_o[pidx * DH + d] = acc;
+    if (kq == 0) {
+      float4* dst = (float4*)(part_o + pidx * DH + sl * 8);
+      dst[0] = make_float4(o[0], o[1], o[2], o[3]);
+      dst[1] = make_float4(o[4], o[5], o[6], o[7]);
     }
-    if (tid == 0) {
+    if (lane == 0) {
       part_ml[pidx * 2 + 0] = count > 0 ? mx : -INFINITY;
-      part_ml[pidx * 2 + 1] = count > 0 ? lsum : 0.f;
+      part_ml[pidx * 2 + 1] = count > 0 ? ls : 0.f;
     }
   }
 }
@@ -389,21 +395,23 @@ hipError_t launch_decode_attention(int dtype, const void* q, const DecodeArgs& c
                                    float* part_ml, float* part_o, void* O, hipStream_t s) {
   const int nch = c.K + 1;
   dim3 grid(nch, c.Hkv, c.b);
-  const size_t lds = ((size_t)c.B * (c.dh + 1) + (size_t)c.B * c.dh + c.B) * sizeof(float);
-  static bool attr = false;
-  if (!attr) {
-    const void* fns[4] = {(const void*)decode_attn_kernel<bf16_t, 128>, (const void*)decode_attn_kernel<bf16_t, 64>,
-                          (const void*)decode_attn_kernel<float, 128>, (const void*)decode_attn_kernel<float, 64>};
-    for (auto f : fns) (void)hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 4096);
-    attr = true;
-  }
+#define DA_LAUNCH(T, DH, MK) \
+  decode_attn_kernel<T, DH, MK><<<grid, 64, 0, s>>>((const T*)q, c, sel, part_ml, part_o)
+  const bool wide = c.B > 64;
   if (dtype == SAS_BF16) {
-    if (c.dh == 128) decode_attn_kernel<bf16_t, 128><<<grid, DA_THREADS, lds, s>>>((const bf16_t*)q, c, sel, part_ml, part_o);
-    else decode_attn_kernel<bf16_t, 64><<<grid, DA_THREADS, lds, s>>>((const bf16_t*)q, c, sel, part_ml, part_o);
+    if (c.dh == 128) {
+      if (wide) DA_LAUNCH(bf16_t, 128, 128); else DA_LAUNCH(bf16_t, 128, 64);
+    } else {
+      if (wide) DA_LAUNCH(bf16_t, 64, 128); else DA_LAUNCH(bf16_t, 64, 64);
+    }
   } else {
-    if (c.dh == 128) decode_attn_kernel<float, 128><<<grid, DA_THREADS, lds, s>>>((const float*)q, c, sel, part_ml, part_o);
-    else decode_attn_kernel<float, 64><<<grid, DA_THREADS, lds, s>>>((const float*)q, c, sel, part_ml, part_o);
+    if (c.dh == 128) {
+      if (wide) DA_LAUNCH(float, 128, 128); else DA_LAUNCH(float, 128, 64);
+    } else {
+      if (wide) DA_LAUNCH(float, 64, 128); else DA_LAUNCH(float, 64, 64);
+    }
   }
+#undef DA_LAUNCH
   const int tot = c.b * c.H * c.dh;
   if (dtype == SAS_BF16)
     decode_combine_kernel<bf16_t><<<cdiv(tot, 256), 256, 0, s>>>(part_ml, part_o, c.b, c.H, nch, c.dh, (bf16_t*)O);
