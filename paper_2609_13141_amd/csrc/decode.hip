@@ -11,6 +11,8 @@
 // geometry and skips what falls outside.
 #include <float.h>
 
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -257,114 +259,222 @@ hipError_t launch_decode_select(int dtype, const void* q, const DecodeArgs& c, i
 }
 
 // ---- sparse attention of the new tokens ----------------------------------------
-// One wave per (chunk, group, sequence); chunk ch < K is the ch-th kept block,
-// ch == K the current block [B*floor(p/B), p].  Nothing is staged in LDS: with
-// NC = dh/8 lanes per key, lane l holds the 8-value slice l % NC of keys
-// l / NC + (64/NC) * it, loaded with coalesced 16-byte loads (a page of one KV
-// head is contiguous).  A key's score is the partial dot product reduced over
-// its NC lanes with shuffles; P V accumulates per slice and is reduced over
-// the lanes that share a slice.  The partial (max, sum of exp, unnormalised
-// output) is written in fp32 and merged by decode_combine_kernel.
-template <typename T, int DH, int MAXKEYS>
-__global__ void __launch_bounds__(64) decode_attn_kernel(const T* __restrict__ q, DecodeArgs c,
-                                                         const int32_t* __restrict__ sel,
-                                                         float* __restrict__ part_ml, float* __restrict__ part_o) {
-  constexpr int NC = DH / 8;          // lanes per key (one 8-value slice each)
-  constexpr int KPI = 64 / NC;        // keys per load instruction
-  constexpr int IT = MAXKEYS / KPI;   // load steps
-  const int lane = threadIdx.x;
-  const int ch = blockIdx.x, g = blockIdx.y, i = blockIdx.z;
-  const int K = c.K, G = c.H / c.Hkv, B = c.B;
+// One workgroup of NW waves per (split, head chunk, group, sequence).  The kept
+// keys of a group are walked in segments of SEG keys: the K selected blocks in
+// selection order (a block of B > SEG keys is B / SEG segments), then the
+// current block [B*floor(p/B), p].  A split is a contiguous range of segments;
+// the workgroup first resolves where each of its segments starts (one pass,
+// into LDS), then deals them to its waves round-robin.  Nothing else is staged
+// in LDS: with NC = dh/8 lanes per key, lane l holds the 8-value slice l % NC
+// of keys l / NC + (64/NC) * it, loaded with coalesced 16-byte loads (a page of
+// one KV head is contiguous).  A wave holds K and V of two segments in
+// registers and issues the loads of the next segment before it computes the
+// current one; the keys serve every head of the head chunk.  A key's score is
+// the partial dot product reduced over its NC lanes; each wave keeps an online
+// softmax per head (running max, sum of exp, unnormalised P V per slice).  The
+// waves are merged in LDS; with one split the result is O itself, otherwise an
+// fp32 partial (max, sum of exp, unnormalised output) that
+// decode_combine_kernel merges.
+template <typename T, int DH>
+struct DecodeSeg {
+  static constexpr int NC = DH / 8;                          // lanes per key
+  static constexpr int KPI = 64 / NC;                        // keys per load instruction
+  static constexpr int SEG = 8192 / (DH * (int)sizeof(T));   // keys per segment: K and V in 64 VGPRs
+  static constexpr int IT = SEG / KPI;                       // load steps per segment
+  Vec8<T> k[IT], v[IT];
+  bool ok[IT];
+  int count;
+};
+
+constexpr int DSEG_MAX = 33 * 8;  // segments of a split: (K + 1) blocks of at most 8 segments
+
+template <typename T, int DH, int GMAX, int NW>
+__global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restrict__ q, DecodeArgs c,
+                                                              const int32_t* __restrict__ sel, int nsplit,
+                                                              float* __restrict__ part_ml,
+                                                              float* __restrict__ part_o, T* __restrict__ O) {
+  using Seg = DecodeSeg<T, DH>;
+  constexpr int NC = Seg::NC, KPI = Seg::KPI, SEG = Seg::SEG, IT = Seg::IT;
+  __shared__ float sm_o[NW][GMAX][DH];
+  __shared__ float sm_ml[NW][GMAX][2];
+  __shared__ int sm_first[DSEG_MAX], sm_count[DSEG_MAX];
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int G = c.H / c.Hkv, nhc = (G + GMAX - 1) / GMAX;
+  const int split = blockIdx.x / nhc, hc = blockIdx.x % nhc;
+  const int g = blockIdx.y, i = blockIdx.z;
+  const int K = c.K, B = c.B;
+  const int spb = B > SEG ? B / SEG : 1;  // segments per block
+  const int seg_len = B > SEG ? SEG : B;
+  const int nseg = (K + 1) * spb;
+  const int per = (nseg + nsplit - 1) / nsplit;
+  const int s0 = split * per, s1 = min(nseg, s0 + per);
   const int p = c.pos[i];
-  int first = 0, count = 0;  // key positions [first, first + count)
-  if (p >= 0) {
-    if (ch < K) {
-      const int m = sel[((size_t)i * c.Hkv + g) * K + ch];
-      if (m >= 0) {
-        first = m * B;
-        count = B;
-      }
-    } else {
-      first = (p / B) * B;
-      count = p - first + 1;
-    }
-  }
   const int sl = lane % NC, kq = lane / NC;
-  // page ids of the chunk (blocks are page aligned): lane j holds page j
   const int ps = c.page_size;
-  const int npg = (count + ps - 1) / ps;
-  int pid = -1;
-  if (lane < npg) {
-    const int pi = first / ps + lane;
-    if (pi < c.max_pages) pid = c.block_table[(size_t)i * c.max_pages + pi];
-    if (pid >= c.num_pages) pid = -1;
-  }
   const size_t kvstride = (size_t)c.Hkv * ps * DH;  // elements per page
-  for (int hg = 0; hg < G; ++hg) {
-    const int h = g * G + hg;
-    float qs[8];
-    {
-      Vec8<T> v;
-      v.load(q + ((size_t)i * c.H + h) * DH + sl * 8);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) qs[e] = v.get(e) * c.sm_scale;
+
+  // key range [first, first + count) of every segment of the split
+  for (int t = threadIdx.x; t < s1 - s0; t += NW * 64) {
+    const int sg = s0 + t, ch = sg / spb, sub = sg % spb;
+    int first = 0, count = 0;
+    if (p >= 0) {
+      if (ch < K) {
+        const int mb = sel[((size_t)i * c.Hkv + g) * K + ch];
+        if (mb >= 0) {
+          first = mb * B + sub * seg_len;
+          count = seg_len;
+        }
+      } else {
+        first = (p / B) * B + sub * seg_len;
+        count = max(0, min(seg_len, p - first + 1));
+      }
     }
-    float sc[IT];
-    float mx = -INFINITY;
+    sm_first[t] = first;
+    sm_count[t] = count;
+  }
+  __syncthreads();
+
+  auto load = [&](Seg& S, int t) {
+    const int first = sm_first[t];
+    S.count = sm_count[t];
+    // page ids of the segment: lane j holds the j-th page from the one holding `first`
+    // (a segment spans at most 64 pages)
+    const int koff = first % ps;
+    const int npg = (koff + S.count + ps - 1) / ps;
+    int pid = -1;
+    if (lane < npg) {
+      const int pi = first / ps + lane;
+      if (pi < c.max_pages) pid = c.block_table[(size_t)i * c.max_pages + pi];
+      if (pid >= c.num_pages) pid = -1;
+    }
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
       const int kl = kq + KPI * it;
-      sc[it] = -INFINITY;
-      if (KPI * it >= count) continue;
-      const int page = __shfl(pid, kl / ps, 64);
-      const bool ok = kl < count && page >= 0;
-      Vec8<T> kv;
-      if (ok) kv.load((const T*)c.k_pages + (size_t)page * kvstride + ((size_t)g * ps + kl % ps) * DH + sl * 8);
-      float acc = 0.f;
-      if (ok) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc = fmaf(qs[e], kv.get(e), acc);
-      }
-#pragma unroll
-      for (int o = NC / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
-      sc[it] = kl < count ? acc : -INFINITY;
-      mx = fmaxf(mx, sc[it]);
-    }
-    mx = wave_max(mx);
-    float ls = 0.f, o[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) o[e] = 0.f;
-#pragma unroll
-    for (int it = 0; it < IT; ++it) {
-      const int kl = kq + KPI * it;
-      if (KPI * it >= count) continue;
-      const int page = __shfl(pid, kl / ps, 64);
-      const bool ok = kl < count && page >= 0;
-      Vec8<T> vv;
-      if (ok) vv.load((const T*)c.v_pages + (size_t)page * kvstride + ((size_t)g * ps + kl % ps) * DH + sl * 8);
-      const float pk = kl < count ? __expf(sc[it] - mx) : 0.f;
-      ls += pk;
-      if (ok) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] = fmaf(pk, vv.get(e), o[e]);
+      const int a = koff + kl;  // offset from the start of the first page
+      const int page = __shfl(pid, min(a / ps, 63), 64);
+      S.ok[it] = kl < S.count && page >= 0;
+      if (S.ok[it]) {
+        const size_t off = (size_t)page * kvstride + ((size_t)g * ps + a % ps) * DH + sl * 8;
+        S.k[it].load((const T*)c.k_pages + off);
+        S.v[it].load((const T*)c.v_pages + off);
       }
     }
-    // lanes sharing a slice hold different keys: reduce over them
+  };
+
+  float m[GMAX], l[GMAX], o[GMAX][8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
+  for (int hg = 0; hg < GMAX; ++hg) {
+    m[hg] = -INFINITY;
+    l[hg] = 0.f;
 #pragma unroll
-      for (int off = NC; off < 64; off <<= 1) o[e] += __shfl_xor(o[e], off, 64);
+    for (int e = 0; e < 8; ++e) o[hg][e] = 0.f;
+  }
+  auto compute = [&](const Seg& S) {
+    if (S.count <= 0) return;
 #pragma unroll
-    for (int off = NC; off < 64; off <<= 1) ls += __shfl_xor(ls, off, 64);  // each key once per slice
-    const size_t pidx = ((size_t)i * c.H + h) * (K + 1) + ch;
+    for (int hg = 0; hg < GMAX; ++hg) {
+      const int hl = hc * GMAX + hg;
+      if (hl >= G) break;
+      const int h = g * G + hl;
+      float qs[8];
+      {
+        Vec8<T> v;
+        v.load(q + ((size_t)i * c.H + h) * DH + sl * 8);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qs[e] = v.get(e) * c.sm_scale;
+      }
+      float sc[IT];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int it = 0; it < IT; ++it) {
+        float acc = 0.f;
+        if (S.ok[it]) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc = fmaf(qs[e], S.k[it].get(e), acc);
+        }
+#pragma unroll
+        for (int off = NC / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+        sc[it] = kq + KPI * it < S.count ? acc : -INFINITY;
+        mx = fmaxf(mx, sc[it]);
+      }
+      mx = wave_max(mx);
+      const float mn = fmaxf(m[hg], mx);
+      const float scale = __expf(m[hg] - mn);
+      m[hg] = mn;
+      l[hg] *= scale;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[hg][e] *= scale;
+#pragma unroll
+      for (int it = 0; it < IT; ++it) {
+        const float pk = kq + KPI * it < S.count ? __expf(sc[it] - mn) : 0.f;
+        l[hg] += pk;
+        if (S.ok[it]) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[hg][e] = fmaf(pk, S.v[it].get(e), o[hg][e]);
+        }
+      }
+    }
+  };
+
+  // two segments in registers: the next one's loads are in flight while one is computed
+  const int ns = s1 - s0;
+  Seg sa, sb;
+  if (wave < ns) load(sa, wave);
+  for (int t = wave; t < ns; t += 2 * NW) {
+    if (t + NW < ns) load(sb, t + NW);
+    compute(sa);
+    if (t + NW >= ns) break;
+    if (t + 2 * NW < ns) load(sa, t + 2 * NW);
+    compute(sb);
+  }
+
+  // lanes sharing a slice hold different keys: reduce over them, then merge the waves
+#pragma unroll
+  for (int hg = 0; hg < GMAX; ++hg) {
+#pragma unroll
+    for (int off = NC; off < 64; off <<= 1) {
+      l[hg] += __shfl_xor(l[hg], off, 64);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[hg][e] += __shfl_xor(o[hg][e], off, 64);
+    }
     if (kq == 0) {
-      float4* dst = (float4*)(part_o + pidx * DH + sl * 8);
-      dst[0] = make_float4(o[0], o[1], o[2], o[3]);
-      dst[1] = make_float4(o[4], o[5], o[6], o[7]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sm_o[wave][hg][sl * 8 + e] = o[hg][e];
     }
     if (lane == 0) {
-      part_ml[pidx * 2 + 0] = count > 0 ? mx : -INFINITY;
-      part_ml[pidx * 2 + 1] = count > 0 ? ls : 0.f;
+      sm_ml[wave][hg][0] = m[hg];
+      sm_ml[wave][hg][1] = l[hg];
+    }
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < GMAX * DH; idx += NW * 64) {
+    const int hg = idx / DH, d = idx % DH;
+    const int hl = hc * GMAX + hg;
+    if (hl >= G) break;
+    const int h = g * G + hl;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) mx = fmaxf(mx, sm_ml[w][hg][0]);
+    float num = 0.f, den = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float mw = sm_ml[w][hg][0];
+      if (mw == -INFINITY) continue;
+      const float wt = __expf(mw - mx);
+      num += wt * sm_o[w][hg][d];
+      den += wt * sm_ml[w][hg][1];
+    }
+    const size_t ih = (size_t)i * c.H + h;
+    if (nsplit == 1) {
+      O[ih * DH + d] = Act<T>::from_f32(den > 0.f ? num / den : 0.f);
+    } else {
+      const size_t pidx = ih * nsplit + split;
+      part_o[pidx * DH + d] = num;
+      if (d == 0) {
+        part_ml[pidx * 2 + 0] = den > 0.f ? mx : -INFINITY;
+        part_ml[pidx * 2 + 1] = den;
+      }
     }
   }
 }
@@ -393,30 +503,40 @@ __global__ void decode_combine_kernel(const float* __restrict__ part_ml, const f
 
 hipError_t launch_decode_attention(int dtype, const void* q, const DecodeArgs& c, const int32_t* sel,
                                    float* part_ml, float* part_o, void* O, hipStream_t s) {
-  const int nch = c.K + 1;
-  dim3 grid(nch, c.Hkv, c.b);
-#define DA_LAUNCH(T, DH, MK) \
-  decode_attn_kernel<T, DH, MK><<<grid, 64, 0, s>>>((const T*)q, c, sel, part_ml, part_o)
-  const bool wide = c.B > 64;
+  constexpr int NW = 8;
+  const int G = c.H / c.Hkv;
+  // heads per workgroup: up to 4, whose softmax state fits in registers beside two segments
+  const int gmax = G <= 1 ? 1 : G <= 2 ? 2 : 4;
+  const int nhc = cdiv(G, gmax);
+  // splits of the kept keys: enough workgroups for 256 CUs; the partial
+  // buffers hold K + 1 per head
+  const int groups = c.b * c.Hkv * nhc;
+  const int nsplit = std::max(1, std::min(c.K + 1, cdiv(256, groups)));
+  dim3 grid(nsplit * nhc, c.Hkv, c.b);
+#define DA_LAUNCH(T, DH, GM)                                                                                   \
+  decode_attn_kernel<T, DH, GM, NW><<<grid, NW * 64, 0, s>>>((const T*)q, c, sel, nsplit, part_ml, part_o, \
+                                                              (T*)O)
+#define DA_GMAX(T, DH)                       \
+  do {                                       \
+    if (gmax == 1) DA_LAUNCH(T, DH, 1);      \
+    else if (gmax == 2) DA_LAUNCH(T, DH, 2); \
+    else DA_LAUNCH(T, DH, 4);                \
+  } while (0)
   if (dtype == SAS_BF16) {
-    if (c.dh == 128) {
-      if (wide) DA_LAUNCH(bf16_t, 128, 128); else DA_LAUNCH(bf16_t, 128, 64);
-    } else {
-      if (wide) DA_LAUNCH(bf16_t, 64, 128); else DA_LAUNCH(bf16_t, 64, 64);
-    }
+    if (c.dh == 128) DA_GMAX(bf16_t, 128);
+    else DA_GMAX(bf16_t, 64);
   } else {
-    if (c.dh == 128) {
-      if (wide) DA_LAUNCH(float, 128, 128); else DA_LAUNCH(float, 128, 64);
-    } else {
-      if (wide) DA_LAUNCH(float, 64, 128); else DA_LAUNCH(float, 64, 64);
-    }
+    if (c.dh == 128) DA_GMAX(float, 128);
+    else DA_GMAX(float, 64);
   }
+#undef DA_GMAX
 #undef DA_LAUNCH
+  if (nsplit == 1) return hipGetLastError();
   const int tot = c.b * c.H * c.dh;
   if (dtype == SAS_BF16)
-    decode_combine_kernel<bf16_t><<<cdiv(tot, 256), 256, 0, s>>>(part_ml, part_o, c.b, c.H, nch, c.dh, (bf16_t*)O);
+    decode_combine_kernel<bf16_t><<<cdiv(tot, 256), 256, 0, s>>>(part_ml, part_o, c.b, c.H, nsplit, c.dh, (bf16_t*)O);
   else
-    decode_combine_kernel<float><<<cdiv(tot, 256), 256, 0, s>>>(part_ml, part_o, c.b, c.H, nch, c.dh, (float*)O);
+    decode_combine_kernel<float><<<cdiv(tot, 256), 256, 0, s>>>(part_ml, part_o, c.b, c.H, nsplit, c.dh, (float*)O);
   return hipGetLastError();
 }
 

@@ -3,10 +3,12 @@
 //
 // One workgroup per 16 output columns; its waves split K.  v_mfma_f32_16x16x32_bf16
 // takes A (activations, 16 rows, rows >= M zero) and W^T (16 columns).  The
-// MFMA only needs A and B to enumerate k the same way, so each lane covers 32
-// consecutive k of its weight row per 4 MFMAs: lane l reads the 64 contiguous
-// bytes [kb + 32*(l/16), +32) of row (l%16), i.e. a wave reads 16 rows x 256
-// contiguous bytes per 4 MFMAs.  Partial sums of the waves are added in LDS.
+// MFMA only needs A and B to enumerate k the same way, so the k slice of MFMA
+// j of a 128-wide chunk is chosen to make each load instruction contiguous per
+// row: lane l reads the 16 bytes at k = kb + 32 j + 8 (l/16) of row l % 16, so
+// one instruction covers 16 rows x 64 contiguous bytes (half a cache line each)
+// and the chunk's four instructions cover 16 rows x 256 bytes.  Partial sums of
+// the waves are added in LDS.
 //
 // Column groups of the pair epilogues hold 8 first-half and 8 second-half
 // columns (RoPE: i and i + dh/2 of a head; SwiGLU: gate f and up f); a lane's
@@ -75,7 +77,7 @@ __global__ void __launch_bounds__(NW * 64) gemv_kernel(GemvParams P) {
     for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int k = (ch + u) * 128 + kg * 32 + j * 8;
+        const int k = (ch + u) * 128 + j * 32 + kg * 8;
         w[u * 4 + j] = *(const uint4*)(wr + k);
         a[u * 4 + j] = *(const uint4*)(ar + k);
       }
@@ -88,7 +90,7 @@ __global__ void __launch_bounds__(NW * 64) gemv_kernel(GemvParams P) {
   for (; ch < c1; ++ch) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int k = ch * 128 + kg * 32 + j * 8;
+      const int k = ch * 128 + j * 32 + kg * 8;
       uint4 w = *(const uint4*)(wr + k);
       uint4 a = avalid ? *(const uint4*)(ar + k) : make_uint4(0, 0, 0, 0);
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(bf16x8_t*)&a, *(bf16x8_t*)&w, acc, 0, 0, 0);

@@ -28,14 +28,18 @@ CASES = [
     W_(dtype="f32", index=71),
     W_(head_dim=128, n_heads=2, n_kv_heads=1, block_size=32, top_k=1, seq_len=100, index=72),
     W_(block_size=64, top_k=1, seq_len=150, batch=2, index=73),
+    # GQA groups of 7 heads (two head chunks of the decode attention) and of 8
+    W_(head_dim=128, n_heads=7, n_kv_heads=1, d_model=448, block_size=16, top_k=2, seq_len=90, index=78),
+    W_(head_dim=64, n_heads=16, n_kv_heads=2, d_model=512, block_size=32, top_k=2, seq_len=110, index=79),
 ]
+CASE_IDS = ["bf16-dh64-B16", "f32-dh64-B16", "bf16-dh128-B32", "bf16-dh64-B64", "bf16-dh128-B16-G7", "bf16-dh64-B32-G8"]
 
 
 def _oracle_W(Wl):
     return {k: (None if a is None else f64(a)) for k, a in Wl.items()}
 
 
-@pytest.mark.parametrize("w", CASES, ids=[f"{w.dtype}-dh{w.head_dim}-B{w.block_size}" for w in CASES])
+@pytest.mark.parametrize("w", CASES, ids=CASE_IDS)
 @pytest.mark.parametrize("proj", [False, True])
 def test_prefill_then_decode_matches_oracle(w, proj):
     n0 = w.seq_len - 21 if w.block_size < 64 else 100
@@ -99,6 +103,43 @@ def test_decode_equals_sparse_prefill_on_gpu(w):
         assert same == total       # the same kernels compute Q/K in both paths
     else:
         assert same / total >= 0.97
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+@pytest.mark.parametrize("page", [128, 32])
+def test_decode_wide_blocks_match_oracle(dt, page):
+    # B = 128: a block is several key segments of the decode attention, and
+    # with 128-token pages a segment can start inside a page
+    w = W_(dtype=dt, block_size=128, top_k=2, seq_len=420, batch=2, index=80)
+    n0 = 400
+    print(f"\n[case] decode wide blocks {dt} page={page}", flush=True)
+    x = inputs.embeddings(w)
+    Wl = inputs.layer_weights(w)
+    Wd = sas.weights_to_device(Wl, dt)
+    xd = sas.to_device(x, dt)
+    cfg_d = sas.make_config(w, "sparse")
+    cache = sas.alloc_cache(cfg_d, w.batch, w.seq_len, page_size=page, seed=7)
+    sas.layer_forward(sas.make_config(w, "dense"), xd[:, :n0].contiguous(), Wd, stats=False, cache=cache)
+    sp = spec_of(w, "sparse")
+    ocache = oracle.DecodeCache(w.batch, w.seq_len, sp)
+    pre = oracle.layer_forward(f64(x[:, :n0]), _oracle_W(Wl), spec_of(w, "dense"))
+    for bi in range(w.batch):
+        ocache.fill_prefill(bi, pre["K"][bi], pre["V"][bi], pre["k_summary"][bi])
+    agree = total = 0
+    for t in range(n0, w.seq_len, 5):
+        if t > n0:  # teacher-forced positions in between, so the oracle cache stays aligned
+            for tt in range(t - 4, t):
+                pos = torch.full((w.batch,), tt, dtype=torch.int32, device="cuda")
+                sas.decode_step(cfg_d, xd[:, tt].contiguous(), pos, Wd, cache)
+                oracle.decode_step(f64(x[:, tt]), np.full(w.batch, tt), _oracle_W(Wl), ocache, sp)
+        pos = torch.full((w.batch,), t, dtype=torch.int32, device="cuda")
+        y, sel = sas.decode_step(cfg_d, xd[:, t].contiguous(), pos, Wd, cache)
+        torch.cuda.synchronize()
+        yo, selo = oracle.decode_step(f64(x[:, t]), np.full(w.batch, t), _oracle_W(Wl), ocache, sp)
+        assert_close(y.float().cpu().numpy(), yo, dt, f"y at t={t}")
+        agree += int(np.all(sel.cpu().numpy() == selo, axis=-1).sum())
+        total += w.batch * w.n_kv_heads
+    assert agree / total >= (1.0 if dt == "f32" else 0.97), agree / total
 
 
 def test_cache_holds_prefill_keys_values_and_summaries():
