@@ -14,6 +14,9 @@ its fraction of the bf16 MFMA peak, the roofline of the dominant kernel
 and the fp64 CPU oracle timed on the host over one layer forward.
 """
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -23,6 +26,12 @@ BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 HBM_PEAK_GBS = 8000.0
 
 METRIC = "prefill tokens/s per layer + % bf16 MFMA peak; decode % HBM GB/s"
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+GEMM_SRC = os.path.join(HERE, "paper_2609_13141_amd", "csrc", "gemm.hip")
+TRAFFIC_FILE = os.path.join(HERE, "profiles", "gemm_gate_up_7b_layer_1k_traffic.txt")
+DOM_KERNEL = "gemm_bf16_pipe_kernel<1, 256, 128, 4, 2, 64, 3, true>"  # the gate/up launch at 1024 rows
+COPY_BYTES = 512 * 2**20  # calibration copy: reads and writes this many bytes once
 
 
 def parse():
@@ -34,11 +43,92 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-step measurement")
     ap.add_argument("--cpu-threads", type=int, default=0, help="oracle BLAS threads (0: affinity, max 16)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain device copy of %d MiB (reference for HBM counters)" % (COPY_BYTES >> 20))
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write the gate/up GEMM traffic summary from two rocprofv3 --pmc runs and exit")
     return ap.parse_args()
+
+
+def source_hash():
+    with open(GEMM_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def pmc_per_dispatch(run_dir, counter):
+    """Mean per-dispatch value of `counter` for the dominant GEMM and for the
+    calibration copy, from a rocprofv3 --pmc csv run directory."""
+    files = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {run_dir}")
+    vals = {"gemm": {}, "copy": {}}
+    for f in files:
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"]
+            key = "gemm" if DOM_KERNEL in name else ("copy" if "copy" in name.lower() else None)
+            if key:
+                d = vals[key]
+                d[r["Dispatch_Id"]] = d.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+    out = {}
+    for k, d in vals.items():
+        if not d:
+            raise SystemExit(f"{counter}: no {k} dispatch found in {run_dir}")
+        v = sorted(d.values())
+        if k == "copy":
+            v = v[-2:]  # the two calibration copies are by far the largest copy dispatches
+        out[k] = sum(v) / len(v)
+    return out
+
+
+def write_traffic_summary(fetch_dir, write_dir):
+    """HBM traffic per launch of the gate/up GEMM: FETCH_SIZE and WRITE_SIZE
+    (KiB per dispatch) scaled by what they read for a copy of known size."""
+    fe = pmc_per_dispatch(fetch_dir, "FETCH_SIZE")
+    wr = pmc_per_dispatch(write_dir, "WRITE_SIZE")
+    f_fetch = COPY_BYTES / (fe["copy"] * 1024.0)
+    f_write = COPY_BYTES / (wr["copy"] * 1024.0)
+    fetch_b = fe["gemm"] * 1024.0 * f_fetch
+    write_b = wr["gemm"] * 1024.0 * f_write
+    lines = [
+        "# HBM traffic of the gate/up GEMM (7b_layer_1k, 1024 x 4096 x 2*11008) per launch",
+        f"# kernel: {DOM_KERNEL}",
+        "# rocprofv3 --pmc FETCH_SIZE (then WRITE_SIZE) -- python3 bench.py --no-decode --no-cpu-baseline "
+        "--steps 5 --warmup 2 --calibrate-copy",
+        f"# calibration: plain copy of {COPY_BYTES} bytes read {fe['copy']:.0f} KiB fetch, {wr['copy']:.0f} KiB write",
+        f"source_sha={source_hash()}",
+        f"fetch_kib_raw={fe['gemm']:.1f}",
+        f"write_kib_raw={wr['gemm']:.1f}",
+        f"fetch_factor={f_fetch:.4f}",
+        f"write_factor={f_write:.4f}",
+        f"fetch_bytes={fetch_b:.0f}",
+        f"write_bytes={write_b:.0f}",
+        f"traffic_bytes={fetch_b + write_b:.0f}",
+    ]
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def measured_traffic():
+    """Traffic per launch from the committed counter summary, or None if the
+    GEMM source changed since the counters were taken."""
+    try:
+        kv = dict(l.strip().split("=", 1) for l in open(TRAFFIC_FILE) if "=" in l and not l.startswith("#"))
+    except OSError:
+        return None
+    if kv.get("source_sha") != source_hash():
+        return None
+    return int(float(kv["traffic_bytes"]))
 
 
 def main():
     args = parse()
+    if args.pmc_summary:
+        write_traffic_summary(*args.pmc_summary)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the SAS hot path here is single-GPU "
               "(run with --gpus 1)", file=sys.stderr)
@@ -86,6 +176,13 @@ def main():
     for _ in range(args.steps):
         step()
     recs = sas.profiler_stop()
+    if args.calibrate_copy:
+        src = torch.empty(COPY_BYTES // 2, dtype=torch.bfloat16, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     fam = {}
     for name, t in recs:
         fam.setdefault(name, []).append(t)
@@ -116,7 +213,7 @@ def main():
         "mfma_frac": round(tflops / BF16_PEAK_TFLOPS, 4),
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(dom_tf, 2),
                      "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(dom_tf / BF16_PEAK_TFLOPS, 4),
-                     "traffic": None, "alg_gflop_per_launch": round(dom_flops / 1e9, 3),
+                     "traffic": measured_traffic(), "alg_gflop_per_launch": round(dom_flops / 1e9, 3),
                      "avg_ms": round(kern_ms[dom], 4)},
         "kernels_ms": {k: round(v, 4) for k, v in sorted(kern_ms.items(), key=lambda kv: -kv[1] * kern_calls[kv[0]])},
     }
