@@ -132,3 +132,54 @@ def model_ends(w: Workload, seed: int = 0) -> dict:
         "token_ids": ids,
         "img_embed": img,
     }
+
+
+def layer_weights_device(w: Workload, layer: int = 0, seed: int = 0, device="cuda"):
+    """Layer weights drawn on the GPU, for stacks too large to draw on the host
+    (32 layers of the 7B shape are 6.5 G values): N(0, weight_std) from
+    torch's Philox generator seeded per (workload, tensor, layer), rounded to
+    the activation dtype; RMSNorm gains 1.  Same shapes and distribution as
+    layer_weights(); the values differ (they are not compared with the oracle)."""
+    import torch
+
+    d, H, Hkv, dh, F = w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.d_ff
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    shapes = {"wq": (H * dh, d), "wk": (Hkv * dh, d), "wv": (Hkv * dh, d), "wo": (d, H * dh),
+              "w_gate": (F, d), "w_up": (F, d), "w_down": (d, F)}
+    out = {"rms1": torch.ones(d, dtype=dt, device=device), "rms2": torch.ones(d, dtype=dt, device=device),
+           "w_gq": None, "w_gk": None}
+    for name, shape in shapes.items():
+        g = torch.Generator(device=device)
+        g.manual_seed(int(np.random.SeedSequence(entropy=seed, spawn_key=(w.index, _key(name), layer))
+                          .generate_state(1, np.uint64)[0] & 0x7FFFFFFFFFFFFFFF))
+        out[name] = (torch.randn(shape, generator=g, device=device, dtype=torch.float32) * w.weight_std).to(dt)
+    return out
+
+
+def model_ends_device(w: Workload, seed: int = 0, device="cuda") -> dict:
+    """model_ends() for large vocabularies: the embedding table and LM head
+    ([vocab, d]) drawn on the GPU as in layer_weights_device(); prompt token
+    ids and image embeddings drawn on the host exactly as model_ends()."""
+    import torch
+
+    d, V = w.d_model, w.vocab
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    kinds = token_kinds(w)
+    n_img = int(kinds.sum())
+    ids = stream(w, "tokens", 0, seed).integers(0, V, size=(w.batch, w.seq_len), dtype=np.int64)
+    ids = np.where(kinds[None, :] == 1, -1, ids).astype(np.int32)
+    img = normal(w, "img_embed", (w.batch, n_img, d), w.img_scale, 0, seed)
+
+    def draw(name, shape, std):
+        g = torch.Generator(device=device)
+        g.manual_seed(int(np.random.SeedSequence(entropy=seed, spawn_key=(w.index, _key(name), 0))
+                          .generate_state(1, np.uint64)[0] & 0x7FFFFFFFFFFFFFFF))
+        return (torch.randn(shape, generator=g, device=device, dtype=torch.float32) * std).to(dt)
+
+    return {
+        "embed": draw("embed", (V, d), 1.0),
+        "w_lm": draw("w_lm", (V, d), w.weight_std),
+        "rms_final": torch.ones(d, dtype=dt, device=device),
+        "token_ids": torch.from_numpy(ids).to(device),
+        "img_embed": torch.from_numpy(img).to(device=device, dtype=dt),
+    }

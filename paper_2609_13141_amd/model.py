@@ -1,0 +1,74 @@
+"""A decoder stack served with SAS (Sec. 5.1, Alg. 2), over the C ABI.
+
+The prompt is prefilled densely through every layer, which fills each
+layer's paged KV cache and block summaries; every generated token is then
+embedded, runs the SAS decode step in each layer (Top-K blocks per KV group
+by the selector, attention to them plus the current block without gate bias)
+and the greedy LM head (final RMSNorm, logits in fp32, lowest id on ties).
+Every step runs in the library's kernels; this module only sequences them.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import sas
+from .configs import Workload
+
+
+class Stack:
+    def __init__(self, w: Workload, layers: list, ends: dict, *, max_len: int, page_size: int | None = None,
+                 device="cuda"):
+        """layers: per-layer device weight dicts; ends: device tensors
+        'embed' [V, d], 'w_lm' [V, d], 'rms_final' [d]."""
+        self.w = w
+        self.layers = layers
+        self.ends = ends
+        self.device = device
+        self.cfg_prefill = sas.make_config(w, "dense")
+        self.cfg_decode = sas.make_config(w, "sparse")
+        ps = page_size or w.page_size
+        self.caches = [sas.alloc_cache(self.cfg_decode, w.batch, max_len, page_size=ps, device=device, seed=l)
+                       for l in range(len(layers))]
+        self.ws = sas.Workspace(device)
+        self.max_len = max_len
+        self.pos = None
+
+    def prefill(self, ids, img=None, *, logits: bool = False):
+        """ids [b, n] int32 on the device (-1 = next image embedding row);
+        returns the first generated token of every sequence [b] int32 (and
+        its fp32 logits when asked)."""
+        x = sas.embed(self.cfg_prefill, ids, self.ends["embed"], img)
+        for W, cache in zip(self.layers, self.caches):
+            x = sas.layer_forward(self.cfg_prefill, x, W, stats=False, cache=cache, ws=self.ws)["y"]
+        self.pos = ids.shape[1]
+        tok, lg = sas.lm_head_argmax(self.cfg_decode, x[:, -1].contiguous(), self.ends["rms_final"],
+                                     self.ends["w_lm"], logits=logits, ws=self.ws)
+        return (tok, lg) if logits else tok
+
+    def positions(self, steps: int):
+        """Device position vectors for the next `steps` decode steps."""
+        b = self.w.batch
+        return [torch.full((b,), self.pos + s, dtype=torch.int32, device=self.device) for s in range(steps)]
+
+    def step(self, tok, pos, *, logits: bool = False, sel_idx: bool = False):
+        """One generated token per sequence: tok [b] at positions pos [b]
+        (device int32).  Returns the next tokens (and logits / per-layer
+        selections when asked)."""
+        x = sas.embed(self.cfg_decode, tok.view(-1, 1), self.ends["embed"])[:, 0].contiguous()
+        sels = []
+        for W, cache in zip(self.layers, self.caches):
+            x, sel = sas.decode_step(self.cfg_decode, x, pos, W, cache, sel_idx=sel_idx, ws=self.ws)
+            sels.append(sel)
+        nxt, lg = sas.lm_head_argmax(self.cfg_decode, x, self.ends["rms_final"], self.ends["w_lm"], logits=logits,
+                                     ws=self.ws)
+        self.pos += 1
+        return nxt, lg, (sels if sel_idx else None)
+
+    def generate(self, ids, img, steps: int):
+        """Greedy generation: [b, steps + 1] tokens (the prefill's and `steps` more)."""
+        tok = self.prefill(ids, img)
+        out = [tok]
+        for pos in self.positions(steps):
+            tok, _, _ = self.step(tok, pos)
+            out.append(tok)
+        return torch.stack(out, 1)
