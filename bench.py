@@ -42,6 +42,7 @@ def parse():
     ap.add_argument("--workload", default="7b_layer_1k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-step measurement")
+    ap.add_argument("--no-long-decode", action="store_true", help="skip the 64K..512K-context decode sweep")
     ap.add_argument("--cpu-threads", type=int, default=0, help="oracle BLAS threads (0: affinity, max 16)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain device copy of %d MiB (reference for HBM counters)" % (COPY_BYTES >> 20))
@@ -222,6 +223,10 @@ def main():
         del x, W, ws
         torch.cuda.empty_cache()
         line["decode"] = decode_bench(args.warmup)
+        torch.cuda.empty_cache()
+    if not args.no_long_decode:
+        line["decode_long"] = decode_long_bench()
+        torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, x_np, W_np, cores)
     print(json.dumps(line), flush=True)
@@ -295,6 +300,66 @@ def decode_bench(warmup):
             "prefill_tokens_per_s_per_layer": round(w.tokens / (prefill_ms * 1e-3 / L), 1),
             "gate_up_gemv_gbs": round(gu_bytes / (kms["dec_gate_up"] * 1e-3) / 1e9, 1),
             "kernels_ms": {k: round(v, 4) for k, v in sorted(kms.items(), key=lambda kv: -kv[1])}}
+
+
+def decode_long_bench(steps=10, warmup=3):
+    """One 7B-shape layer's SAS decode step at 64K..512K tokens of context,
+    batch 1 and 8, K = 32 blocks of 64 (the paper's default budget): the
+    selection scores every cached block summary (8192 at 512K) and attends
+    to the 32 kept blocks plus the current one.  The caches are filled on
+    the GPU with synthetic N(0,1) keys, values and summaries (timing does not
+    depend on their values); positions start 20 tokens before the end."""
+    import torch
+    from paper_2609_13141_amd import configs, inputs, sas
+    base = configs.LONG_DECODE
+    dev = "cuda:0"
+    Wd = inputs.layer_weights_device(base, device=dev)
+    out = []
+    for b in (1, 8):
+        for ctx in (65536, 131072, 262144, 524288):
+            w = base.with_(batch=b, seq_len=ctx)
+            cfg = sas.make_config(w, "sparse")
+            cache = sas.alloc_cache(cfg, b, ctx, page_size=w.page_size, device=dev, seed=b)
+            cache.k_pages.normal_()
+            cache.v_pages.normal_()
+            cache.k_summary.normal_()
+            x = torch.randn(b, w.d_model, device=dev).to(torch.bfloat16)
+            ws = sas.Workspace(dev)
+            p0 = ctx - 20
+            poss = [torch.full((b,), p0 + s, dtype=torch.int32, device=dev) for s in range(warmup + steps + 3)]
+            for s in range(warmup):
+                sas.decode_step(cfg, x, poss[s], Wd, cache, sel_idx=False, ws=ws)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for s in range(warmup, warmup + steps):
+                sas.decode_step(cfg, x, poss[s], Wd, cache, sel_idx=False, ws=ws)
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t0) * 1e3 / steps
+            sas.profiler_start(64 * 3 + 16)
+            for s in range(warmup + steps, warmup + steps + 3):
+                sas.decode_step(cfg, x, poss[s], Wd, cache, sel_idx=False, ws=ws)
+            recs = sas.profiler_stop()
+            fam = {}
+            for name, v in recs:
+                fam.setdefault(name, []).append(v)
+            kms = {k: sum(v) / len(v) for k, v in fam.items()}
+            B, K, dh, Hkv = w.block_size, w.top_k, w.head_dim, w.n_kv_heads
+            tot = 0.0
+            for t in range(p0 + warmup, p0 + warmup + steps):
+                ct = t // B
+                kept = B * min(K, ct) + (t % B) + 1
+                tot += 2.0 * w.linear_params() + b * Hkv * (kept * dh * 2 * 2 + ct * dh * 2 + 2 * dh * 2)
+            nbytes = tot / steps
+            sel_ms = kms.get("dec_select", 0.0)
+            out.append({"context": ctx, "batch": b, "ms_per_layer_step": round(ms, 4),
+                        "bytes_per_layer_step": int(nbytes),
+                        "hbm_gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                        "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                        "select_ms": round(sel_ms, 4), "select_share": round(sel_ms / sum(kms.values()), 3),
+                        "summary_bytes": b * Hkv * (ctx // B) * dh * 2})
+            del cache, ws
+            torch.cuda.empty_cache()
+    return out
 
 
 def cpu_baseline(w, x_np, W_np, cores):

@@ -67,8 +67,9 @@ typedef enum {
   SAS_OP_ATTENTION = 0, /* sas_attention_prefill: batch, seq_len */
   SAS_OP_MLP = 1,       /* sas_mlp_forward: batch = tokens, seq_len ignored */
   SAS_OP_LAYER = 2,     /* sas_layer_forward: batch, seq_len */
-  SAS_OP_DECODE = 3,    /* sas_decode_step: batch, seq_len = max context */
-  SAS_OP_LM_HEAD = 4    /* sas_lm_head_argmax: batch, seq_len = vocab */
+  SAS_OP_DECODE = 3,    /* sas_decode_step: batch, seq_len = max context (tokens) */
+  SAS_OP_LM_HEAD = 4,   /* sas_lm_head_argmax: batch, seq_len = vocab */
+  SAS_OP_DECODE_SELECT = 5 /* sas_decode_select: batch, seq_len = max context (tokens) */
 } sas_op;
 
 typedef struct {
@@ -208,6 +209,24 @@ sas_status sas_decode_step(const sas_config* cfg, int32_t batch, const void* x,
                            const int32_t* pos, const sas_layer_weights* w,
                            sas_paged_kv* cache, void* y, int32_t* sel_idx,
                            void* ws, size_t ws_bytes, void* stream);
+
+/* The selection of a decode step alone (Alg. 2's Top-K over the block
+ * summaries; Sec. 5.1), for long contexts where it dominates the step:
+ * q [b, H, dh] holds the post-RoPE query heads of the new tokens (activation
+ * dtype, DEVICE), pos [b] their positions (DEVICE int32).  Each KV group's
+ * gate query (its heads summed, then w_gq [Hkv, dh, dh] when not NULL) is
+ * scored against the cache's summaries of the floor(pos/B) complete blocks
+ * (exact fp64 dot products) and the Top-K (score descending, lower block
+ * first on ties) is written to sel_idx [b, Hkv, K], ascending, -1 padded.
+ * Only cache->k_summary and cache->max_blocks (<= 8192, i.e. 512K tokens at
+ * B = 64) are read; nothing is appended.  Caches of more than 256 blocks
+ * need sas_workspace_size(cfg, SAS_OP_DECODE_SELECT, batch, max context)
+ * bytes of ws (b * Hkv * max_blocks doubles); sas_decode_step takes the
+ * same path and needs the same room beyond its other scratch. */
+sas_status sas_decode_select(const sas_config* cfg, int32_t batch, const void* q,
+                             const int32_t* pos, const void* w_gq,
+                             const sas_paged_kv* cache, int32_t* sel_idx,
+                             void* ws, size_t ws_bytes, void* stream);
 
 /* Token embedding for the model ends: x [b, n, d] = table[ids] for ids >= 0;
  * an id < 0 marks an image slot, filled with the next row of

@@ -34,12 +34,12 @@ from .selector import (block_summaries, gate_query, selector_scores,
                        normalized_log_gate, topk_blocks, select)
 from .attention import sas_attention
 from .layer import (Spec, layer_forward, mlp_forward, attention_prefill,
-                    DecodeCache, decode_step, embed_tokens, lm_head_argmax)
+                    DecodeCache, decode_step, decode_select, embed_tokens, lm_head_argmax)
 
 __all__ = [
     "rho", "round_bf16", "round_f32", "rmsnorm", "rope", "silu",
     "block_summaries", "gate_query", "selector_scores", "normalized_log_gate",
     "topk_blocks", "select", "sas_attention", "Spec", "layer_forward",
     "mlp_forward", "attention_prefill", "DecodeCache", "decode_step",
-    "embed_tokens", "lm_head_argmax",
+    "decode_select", "embed_tokens", "lm_head_argmax",
 ]

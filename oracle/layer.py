@@ -179,6 +179,28 @@ def decode_step(x, pos, W, cache, spec):
     return y, sel_all
 
 
+def decode_select(q, pos, kbar, spec, w_gq=None):
+    """The selection of a decode step (Alg. 2) alone: q[b, H, dh] query heads
+    of the new tokens at positions pos[b]; kbar[b, Hkv, M, dh] the cached
+    block summaries.  Each group's gate query scores the floor(pos/B)
+    complete blocks and keeps the Top-K under (r desc, m asc).  Returns
+    sel[b, Hkv, K] ascending, -1 padded, and r[b][Hkv, C]."""
+    q = _f64(q)
+    b = q.shape[0]
+    Hkv, Kb, B = spec.n_kv_heads, spec.top_k, spec.block_size
+    sel = np.full((b, Hkv, max(Kb, 0)), -1, dtype=np.int64)
+    rs = []
+    for bi in range(b):
+        ct = min(int(pos[bi]) // B, kbar.shape[2]) if pos[bi] >= 0 else 0
+        qhat = gate_query(q[bi:bi + 1], spec.group, spec.dtype, _f64(w_gq))     # [Hkv,1,dh]
+        r = selector_scores(qhat, _f64(kbar[bi])[:, :ct])                        # [Hkv,1,ct]
+        for g in range(Hkv):
+            chosen, _ = topk_blocks(r[g, 0], ct, Kb)
+            sel[bi, g, :len(chosen)] = chosen
+        rs.append(r[:, 0])
+    return sel, rs
+
+
 def embed_tokens(ids, table, img_embed=None):
     """x[b, n, d]: row table[id] for id >= 0; image slots (id < 0) take the
     next row of img_embed[b, n_img, d] in order."""

@@ -119,5 +119,14 @@ GQA_16K = Workload(
     n_heads=28, n_kv_heads=4, head_dim=128, d_ff=18944, block_size=64, top_k=32,
     mode="gated", segments=(("img", 64 * 248), ("txt", 512)), index=4)
 
-WORKLOADS = (TINY, L7B_1K, L7B_4K_B4, STACK_DECODE, GQA_16K)
+# Long-context decode (the paper's measured regime): one 7B-shape layer's
+# SAS decode step at contexts of 64K..512K tokens (seq_len = the context),
+# the paper's default budget K = 32 blocks of 64; cache contents synthetic.
+LONG_DECODE = Workload(
+    name="7b_layer_decode_64k_512k", dtype="bf16", batch=8, seq_len=524288,
+    d_model=4096, n_heads=32, n_kv_heads=32, head_dim=128, d_ff=11008,
+    block_size=64, top_k=32, mode="sparse", segments=(("txt", 524288),),
+    page_size=16, index=5)
+
+WORKLOADS = (TINY, L7B_1K, L7B_4K_B4, STACK_DECODE, GQA_16K, LONG_DECODE)
 BY_NAME = {w.name: w for w in WORKLOADS}

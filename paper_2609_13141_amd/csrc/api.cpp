@@ -332,8 +332,8 @@ sas_status check_cache(const sas_config* c, const sas_paged_kv* kv) {
                 kv->page_size);
   if (c->block_size / kv->page_size > 64)
     return fail(SAS_ERR_UNSUPPORTED, "block_size / page_size = %d (supported: <= 64)", c->block_size / kv->page_size);
-  if (kv->max_blocks > 2048)
-    return fail(SAS_ERR_UNSUPPORTED, "max_blocks %d (supported: <= 2048)", kv->max_blocks);
+  if (kv->max_blocks > DSEL_MAX_BLOCKS)
+    return fail(SAS_ERR_UNSUPPORTED, "max_blocks %d (supported: <= %d)", kv->max_blocks, DSEL_MAX_BLOCKS);
   return SAS_OK;
 }
 
@@ -386,10 +386,22 @@ struct DecodeWs {
   float* part_o;
   void* o;
   void* h1;
+  double* scores;
   MlpWs mlp;
 };
 
-DecodeWs carve_decode(Carve& cv, const sas_config* c, int b) {
+// selector scores of the long-context path: b * Hkv * max_blocks doubles
+double* carve_scores(Carve& cv, const sas_config* c, int b, int max_blocks) {
+  if (max_blocks <= DSEL_WAVE_MAX_BLOCKS) return nullptr;
+  return (double*)cv.take((size_t)b * c->n_kv_heads * max_blocks * sizeof(double));
+}
+
+// max context (tokens) -> summary blocks the workspace must cover
+int blocks_of(const sas_config* c, int max_context) {
+  return max_context > 0 ? (int)cdiv(max_context, c->block_size) : 0;
+}
+
+DecodeWs carve_decode(Carve& cv, const sas_config* c, int b, int max_blocks) {
   const size_t ab = act_bytes(c);
   const size_t H = c->n_heads, Hkv = c->n_kv_heads, dh = c->head_dim, K = c->top_k;
   DecodeWs w;
@@ -404,6 +416,7 @@ DecodeWs carve_decode(Carve& cv, const sas_config* c, int b) {
   w.part_o = (float*)cv.take((size_t)b * H * (K + 1) * dh * 4);
   w.o = cv.take((size_t)b * H * dh * ab);
   w.h1 = cv.take((size_t)b * c->d_model * ab);
+  w.scores = carve_scores(cv, c, b, max_blocks);
   w.mlp = carve_mlp(cv, c, (size_t)b);
   return w;
 }
@@ -475,8 +488,13 @@ size_t sas_workspace_size(const sas_config* c, int32_t op, int32_t batch, int32_
       carve_layer(cv, c, batch, seq_len);
       break;
     case SAS_OP_DECODE:
-      if (check_config(c, true) != SAS_OK) return 0;
-      carve_decode(cv, c, batch);
+      if (check_config(c, true) != SAS_OK || blocks_of(c, seq_len) > DSEL_MAX_BLOCKS) return 0;
+      carve_decode(cv, c, batch, blocks_of(c, seq_len));
+      break;
+    case SAS_OP_DECODE_SELECT:
+      if (check_config(c, false) != SAS_OK || blocks_of(c, seq_len) > DSEL_MAX_BLOCKS) return 0;
+      cv.take(1);
+      carve_scores(cv, c, batch, blocks_of(c, seq_len));
       break;
     case SAS_OP_LM_HEAD:
       if (seq_len <= 0 || !c || (c->dtype != SAS_F32 && c->dtype != SAS_BF16) || c->d_model <= 0) return 0;
@@ -633,7 +651,7 @@ sas_status sas_decode_step(const sas_config* c, int32_t batch, const void* x, co
   if (!cache) return fail(SAS_ERR_INVALID_ARGUMENT, "cache is NULL");
   SAS_TRY(check_cache(c, cache));
   Carve cv(ws);
-  DecodeWs dw = carve_decode(cv, c, batch);
+  DecodeWs dw = carve_decode(cv, c, batch, cache->max_blocks);
   SAS_TRY(check_ws(ws, ws_bytes, cv.off));
   hipStream_t s = (hipStream_t)stream;
   const DecodeArgs da = decode_args(c, batch, pos, cache, w);
@@ -673,7 +691,7 @@ sas_status sas_decode_step(const sas_config* c, int32_t batch, const void* x, co
   }
   {
     Timed tm("dec_select", s);
-    HIP_TRY(launch_decode_select(c->dtype, dw.q, da, sel, s), "decode select");
+    HIP_TRY(launch_decode_select(c->dtype, dw.q, da, sel, dw.scores, s), "decode select");
   }
   {
     Timed tm("dec_attention", s);
@@ -721,6 +739,34 @@ sas_status sas_decode_step(const sas_config* c, int32_t batch, const void* x, co
   {
     Timed tm("dec_down", s);
     HIP_TRY(small_gemm(c->dtype, dg, s), "down gemm");
+  }
+  return SAS_OK;
+}
+
+sas_status sas_decode_select(const sas_config* c, int32_t batch, const void* q, const int32_t* pos,
+                             const void* w_gq, const sas_paged_kv* cache, int32_t* sel_idx, void* ws,
+                             size_t ws_bytes, void* stream) {
+  SAS_TRY(check_config(c, false));
+  if (batch <= 0) return fail(SAS_ERR_INVALID_ARGUMENT, "batch %d must be positive", batch);
+  SAS_TRY(check_ptr(q, "q", true));
+  SAS_TRY(check_ptr(pos, "pos", true));
+  SAS_TRY(check_ptr(w_gq, "w_gq", false));
+  SAS_TRY(check_ptr(sel_idx, "sel_idx", true));
+  if (!cache) return fail(SAS_ERR_INVALID_ARGUMENT, "cache is NULL");
+  SAS_TRY(check_ptr(cache->k_summary, "cache.k_summary", true));
+  if (cache->max_blocks <= 0 || cache->max_blocks > DSEL_MAX_BLOCKS)
+    return fail(SAS_ERR_UNSUPPORTED, "max_blocks %d (supported: 1..%d)", cache->max_blocks, DSEL_MAX_BLOCKS);
+  Carve cv(ws);
+  cv.take(1);
+  double* scores = carve_scores(cv, c, batch, cache->max_blocks);
+  SAS_TRY(check_ws(ws, ws_bytes, cv.off));
+  sas_layer_weights w = {};
+  w.w_gq = w_gq;
+  const DecodeArgs da = decode_args(c, batch, pos, cache, &w);
+  hipStream_t s = (hipStream_t)stream;
+  {
+    Timed tm("dec_select", s);
+    HIP_TRY(launch_decode_select(c->dtype, q, da, sel_idx, scores, s), "decode select");
   }
   return SAS_OK;
 }

@@ -188,19 +188,18 @@ hipError_t launch_kv_append(int dtype, const void* k, const void* v, const Decod
 // projected; scores: sequential fp64 sums over ascending j; rank of a block =
 // number of blocks strictly ahead of it under (r desc, m asc); kept if rank < K,
 // written in ascending block order.
-constexpr int DSEL_MAXB = 2048;  // historical blocks per query supported by this kernel
 
 template <typename T>
 __global__ void __launch_bounds__(64) decode_select_kernel(const T* __restrict__ q, DecodeArgs c,
                                                            int32_t* __restrict__ sel) {
   __shared__ double qh[128];
   __shared__ double qp[128];
-  __shared__ double rs[DSEL_MAXB];
+  __shared__ double rs[DSEL_WAVE_MAX_BLOCKS];
   const int lane = threadIdx.x;
   const int g = blockIdx.x, i = blockIdx.y;
   const int G = c.H / c.Hkv, dh = c.dh, K = c.K;
   const int p = c.pos[i];
-  const int ct = max(0, min(p / c.B, min(c.max_blocks, DSEL_MAXB)));
+  const int ct = max(0, min(p / c.B, min(c.max_blocks, DSEL_WAVE_MAX_BLOCKS)));
   for (int j = lane; j < dh; j += 64) {
     double acc = 0.0;
     for (int h = 0; h < G; ++h) acc += (double)Act<T>::to_f32(q[((size_t)i * c.H + g * G + h) * dh + j]);
@@ -250,11 +249,215 @@ __global__ void __launch_bounds__(64) decode_select_kernel(const T* __restrict__
   for (int s2 = base + lane; s2 < K; s2 += 64) out[s2] = -1;
 }
 
-hipError_t launch_decode_select(int dtype, const void* q, const DecodeArgs& c, int32_t* sel, hipStream_t s) {
+// ---- selection over long contexts ----------------------------------------------
+// Caches of more than DSEL_WAVE_MAX_BLOCKS blocks take two phases.  decode_score_kernel:
+// a workgroup per ROWS blocks of one (group, sequence) stages their summary
+// rows in LDS with coalesced 16-byte loads (rows padded by 16 bytes so the
+// lanes of one 128-bit read pass hit distinct banks) and gives each thread one
+// block, whose score r is the same sequential fp64 sum over ascending j as in
+// the single-wave kernel; scores go to a scratch row per (sequence, group).
+// decode_topk_kernel: a workgroup of 1024 threads per (group, sequence) holds
+// the scores as order-preserving 64-bit keys (-0 folded into +0, so equal
+// scores tie) in registers, KPT consecutive blocks per thread, and finds the
+// key of the K-th largest by eight passes of 8-bit radix histograms in LDS.
+// Every key above it is kept, and of the keys equal to it the lowest block
+// indices; block-wide scans in block order write them ascending.
+constexpr int DSEL_TOPK_KPT = 8;      // blocks per thread of the radix Top-K
+constexpr int DSEL_TOPK_NT = 1024;
+constexpr int DSEL_LONG_MAXB = DSEL_TOPK_KPT * DSEL_TOPK_NT;  // 8192 blocks: 512K tokens at B = 64
+static_assert(DSEL_LONG_MAXB == DSEL_MAX_BLOCKS, "selection limit");
+
+template <typename T, int DH, int ROWS>
+__global__ void __launch_bounds__(ROWS) decode_score_kernel(const T* __restrict__ q, DecodeArgs c,
+                                                            double* __restrict__ scores) {
+  constexpr int RS = DH * (int)sizeof(T) + 16;  // bytes per staged row
+  constexpr int CH = DH * (int)sizeof(T) / 16;  // 16-byte chunks per row
+  __shared__ double qh[DH], qp[DH];
+  __shared__ __align__(16) unsigned char rows[ROWS * RS];
+  const int tid = threadIdx.x;
+  const int g = blockIdx.y, i = blockIdx.z;
+  const int m0 = blockIdx.x * ROWS;
+  const int p = c.pos[i];
+  const int ct = p < 0 ? 0 : min(p / c.B, c.max_blocks);
+  if (m0 >= ct) return;
+  const int G = c.H / c.Hkv;
+  for (int j = tid; j < DH; j += ROWS) {
+    double acc = 0.0;
+    for (int h = 0; h < G; ++h) acc += (double)Act<T>::to_f32(q[((size_t)i * c.H + g * G + h) * DH + j]);
+    qh[j] = (double)Act<T>::to_f32(Act<T>::from_f64(acc));
+  }
+  __syncthreads();
+  if (c.w_gq) {
+    const T* W = (const T*)c.w_gq + (size_t)g * DH * DH;
+    for (int kk = tid; kk < DH; kk += ROWS) {
+      double acc = 0.0;
+      for (int j = 0; j < DH; ++j) acc = fma((double)Act<T>::to_f32(W[(size_t)kk * DH + j]), qh[j], acc);
+      qp[kk] = (double)Act<T>::to_f32(Act<T>::from_f64(acc));
+    }
+    __syncthreads();
+    for (int j = tid; j < DH; j += ROWS) qh[j] = qp[j];
+  }
+  const T* ks = (const T*)c.k_summary + ((size_t)i * c.Hkv + g) * c.max_blocks * DH;
+  const int nrow = min(ROWS, ct - m0);
+  for (int x = tid; x < nrow * CH; x += ROWS) {
+    const int r = x / CH, cc = x % CH;
+    *(uint4*)(rows + r * RS + cc * 16) = *(const uint4*)((const unsigned char*)(ks + (size_t)(m0 + r) * DH) + cc * 16);
+  }
+  __syncthreads();
+  if (tid < nrow) {
+    const T* row = (const T*)(rows + tid * RS);
+    double acc = 0.0;
+    for (int j0 = 0; j0 < DH; j0 += 8) {
+      Vec8<T> v;
+      v.load(row + j0);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc = fma(qh[j0 + e], (double)v.get(e), acc);
+    }
+    scores[((size_t)i * c.Hkv + g) * c.max_blocks + m0 + tid] = acc;
+  }
+}
+
+// exclusive prefix sum of v over the workgroup in thread order; total in *tot
+__device__ __forceinline__ int block_exclusive_scan(int v, int* wsum, int* tot) {
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, nw = blockDim.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wsum[wv] = x;
+  __syncthreads();
+  int before = 0, all = 0;
+  for (int w = 0; w < nw; ++w) {
+    const int sw = wsum[w];
+    before += w < wv ? sw : 0;
+    all += sw;
+  }
+  __syncthreads();
+  *tot = all;
+  return before + x - v;
+}
+
+__global__ void __launch_bounds__(DSEL_TOPK_NT) decode_topk_kernel(const double* __restrict__ scores, DecodeArgs c,
+                                                                   int32_t* __restrict__ sel) {
+  constexpr int KPT = DSEL_TOPK_KPT;
+  __shared__ int hist[256];
+  __shared__ int sh_digit, sh_above;
+  __shared__ int wsum[DSEL_TOPK_NT / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int g = blockIdx.x, i = blockIdx.y;
+  const int K = c.K;
+  int32_t* out = sel + ((size_t)i * c.Hkv + g) * K;
+  const int p = c.pos[i];
+  const int ct = p < 0 ? 0 : min(p / c.B, c.max_blocks);
+  const int kk = min(K, ct);
+  const double* rs = scores + ((size_t)i * c.Hkv + g) * c.max_blocks;
+  unsigned long long key[KPT];
+#pragma unroll
+  for (int e = 0; e < KPT; ++e) {
+    const int m = tid * KPT + e;
+    key[e] = 0;
+    if (m < ct) {
+      const unsigned long long u = (unsigned long long)__double_as_longlong(rs[m] + 0.0);  // -0 -> +0
+      key[e] = (u >> 63) ? ~u : (u | (1ull << 63));
+    }
+  }
+  unsigned long long prefix = 0, pmask = 0;
+  int need = kk;
+  const bool all = ct <= K;  // every historical block is kept
+  if (!all) {
+    for (int pass = 7; pass >= 0; --pass) {
+      const int sh = 8 * pass;
+      for (int x = tid; x < 256; x += DSEL_TOPK_NT) hist[x] = 0;
+      __syncthreads();
+#pragma unroll
+      for (int e = 0; e < KPT; ++e)
+        if (tid * KPT + e < ct && (key[e] & pmask) == prefix) atomicAdd(&hist[(int)((key[e] >> sh) & 255)], 1);
+      __syncthreads();
+      if (wv == 0) {
+        // lane l holds digits 255-4l .. 252-4l (descending); find the digit whose
+        // bin holds the need-th largest remaining key
+        int cnt[4], cum = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          cnt[e] = hist[255 - 4 * lane - e];
+          cum += cnt[e];
+        }
+        int x = cum;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(x, o, 64);
+          if (lane >= o) x += y;
+        }
+        int above = x - cum;  // keys with a higher digit than this lane's first
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (above < need && above + cnt[e] >= need) {
+            sh_digit = 255 - 4 * lane - e;
+            sh_above = above;
+          }
+          above += cnt[e];
+        }
+      }
+      __syncthreads();
+      need -= sh_above;
+      prefix |= (unsigned long long)sh_digit << sh;
+      pmask |= 255ull << sh;
+      __syncthreads();
+    }
+  }
+  // prefix = key of the K-th largest; keep every key above it and the `need`
+  // lowest-index keys equal to it
+  int n_eq = 0;
+#pragma unroll
+  for (int e = 0; e < KPT; ++e) n_eq += (!all && tid * KPT + e < ct && key[e] == prefix) ? 1 : 0;
+  int tot;
+  const int eq_before = block_exclusive_scan(n_eq, wsum, &tot);
+  bool keep[KPT];
+  int n_keep = 0, eq_seen = 0;
+#pragma unroll
+  for (int e = 0; e < KPT; ++e) {
+    const bool valid = tid * KPT + e < ct;
+    bool k = valid && (all || key[e] > prefix);
+    if (valid && !all && key[e] == prefix) {
+      k = eq_before + eq_seen < need;
+      ++eq_seen;
+    }
+    keep[e] = k;
+    n_keep += k ? 1 : 0;
+  }
+  const int slot0 = block_exclusive_scan(n_keep, wsum, &tot);
+  int slot = slot0;
+#pragma unroll
+  for (int e = 0; e < KPT; ++e)
+    if (keep[e]) {
+      if (slot < K) out[slot] = tid * KPT + e;
+      ++slot;
+    }
+  for (int s2 = kk + tid; s2 < K; s2 += DSEL_TOPK_NT) out[s2] = -1;
+}
+
+hipError_t launch_decode_select(int dtype, const void* q, const DecodeArgs& c, int32_t* sel, double* scores,
+                                hipStream_t s) {
   if (c.K <= 0) return hipSuccess;
-  dim3 grid(c.Hkv, c.b);
-  if (dtype == SAS_BF16) decode_select_kernel<bf16_t><<<grid, 64, 0, s>>>((const bf16_t*)q, c, sel);
-  else decode_select_kernel<float><<<grid, 64, 0, s>>>((const float*)q, c, sel);
+  if (c.max_blocks <= DSEL_WAVE_MAX_BLOCKS) {
+    dim3 grid(c.Hkv, c.b);
+    if (dtype == SAS_BF16) decode_select_kernel<bf16_t><<<grid, 64, 0, s>>>((const bf16_t*)q, c, sel);
+    else decode_select_kernel<float><<<grid, 64, 0, s>>>((const float*)q, c, sel);
+    return hipGetLastError();
+  }
+  if (c.max_blocks > DSEL_LONG_MAXB || !scores) return hipErrorInvalidValue;
+  if (dtype == SAS_BF16) {
+    dim3 grid(cdiv(c.max_blocks, 128), c.Hkv, c.b);
+    if (c.dh == 128) decode_score_kernel<bf16_t, 128, 128><<<grid, 128, 0, s>>>((const bf16_t*)q, c, scores);
+    else decode_score_kernel<bf16_t, 64, 128><<<grid, 128, 0, s>>>((const bf16_t*)q, c, scores);
+  } else {
+    dim3 grid(cdiv(c.max_blocks, 64), c.Hkv, c.b);
+    if (c.dh == 128) decode_score_kernel<float, 128, 64><<<grid, 64, 0, s>>>((const float*)q, c, scores);
+    else decode_score_kernel<float, 64, 64><<<grid, 64, 0, s>>>((const float*)q, c, scores);
+  }
+  decode_topk_kernel<<<dim3(c.Hkv, c.b), DSEL_TOPK_NT, 0, s>>>(scores, c, sel);
   return hipGetLastError();
 }
 

@@ -111,7 +111,11 @@ hipError_t launch_cache_fill(int dtype, const void* K, const void* V, const void
 hipError_t launch_kv_append(int dtype, const void* k, const void* v, const DecodeArgs& c,
                             void* kplain_scratch, hipStream_t s);
 // Top-K per (seq, group) against the cached summaries -> sel [b, Hkv, K].
-hipError_t launch_decode_select(int dtype, const void* q, const DecodeArgs& c, int32_t* sel,
+// Caches of more than DSEL_WAVE_MAX_BLOCKS blocks (up to DSEL_MAX_BLOCKS)
+// need `scores`, b * Hkv * max_blocks doubles of scratch.
+constexpr int DSEL_WAVE_MAX_BLOCKS = 256;
+constexpr int DSEL_MAX_BLOCKS = 8192;
+hipError_t launch_decode_select(int dtype, const void* q, const DecodeArgs& c, int32_t* sel, double* scores,
                                 hipStream_t s);
 // Sparse attention of the new tokens over current block + selected blocks.
 hipError_t launch_decode_attention(int dtype, const void* q, const DecodeArgs& c, const int32_t* sel,

@@ -20,11 +20,11 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsas.so")
 SAS_OK, SAS_ERR_INVALID_ARGUMENT, SAS_ERR_UNSUPPORTED, SAS_ERR_WORKSPACE, SAS_ERR_HIP = 0, -1, -2, -3, -4
 SAS_F32, SAS_BF16 = 0, 1
 MODES = {"dense": 0, "sparse": 1, "gated": 2}
-OP_ATTENTION, OP_MLP, OP_LAYER, OP_DECODE, OP_LM_HEAD = 0, 1, 2, 3, 4
+OP_ATTENTION, OP_MLP, OP_LAYER, OP_DECODE, OP_LM_HEAD, OP_DECODE_SELECT = 0, 1, 2, 3, 4, 5
 TORCH_DTYPE = {"bf16": torch.bfloat16, "f32": torch.float32}
 
 EXPORTS = ("sas_workspace_size", "sas_attention_prefill", "sas_mlp_forward", "sas_layer_forward",
-           "sas_decode_step", "sas_embed", "sas_lm_head_argmax", "sas_last_error", "sas_version",
+           "sas_decode_step", "sas_decode_select", "sas_embed", "sas_lm_head_argmax", "sas_last_error", "sas_version",
            "sas_profiler_start", "sas_profiler_stop", "sas_profiler_record")
 
 
@@ -91,6 +91,8 @@ def lib() -> C.CDLL:
     L.sas_decode_step.restype = i32
     L.sas_decode_step.argtypes = [C.POINTER(Config), i32, vp, vp, C.POINTER(LayerWeights), C.POINTER(PagedKV),
                                   vp, vp, vp, sz, vp]
+    L.sas_decode_select.restype = i32
+    L.sas_decode_select.argtypes = [C.POINTER(Config), i32, vp, vp, vp, C.POINTER(PagedKV), vp, vp, sz, vp]
     L.sas_embed.restype = i32
     L.sas_embed.argtypes = [C.POINTER(Config), i32, i32, vp, vp, i32, vp, i32, vp, vp]
     L.sas_lm_head_argmax.restype = i32
@@ -213,6 +215,10 @@ class PagedCache:
                        self.k_pages.shape[0], self.page_size, self.block_table.shape[1],
                        self.k_summary.shape[2])
 
+    def max_context(self, cfg: Config) -> int:
+        """Tokens the summary cache covers (what the workspace is sized for)."""
+        return self.k_summary.shape[2] * cfg.block_size
+
 
 def layer_forward(cfg: Config, x, W: dict, *, stats: bool = True, lse=True, sel_idx=True, log_gate=False,
                   tau=False, k_summary=False, taps: bool = False, cache: PagedCache | None = None,
@@ -295,10 +301,22 @@ def decode_step(cfg: Config, x, pos, W: dict, cache: PagedCache, *, sel_idx: boo
     y = torch.empty_like(x)
     sel = torch.empty(b, cfg.n_kv_heads, cfg.top_k, dtype=torch.int32, device=x.device) if sel_idx else None
     cs = cache.struct()
-    wsp, wsn = _ws(ws, workspace_size(cfg, OP_DECODE, b, 0))
+    wsp, wsn = _ws(ws, workspace_size(cfg, OP_DECODE, b, cache.max_context(cfg)))
     _check(lib().sas_decode_step(C.byref(cfg), b, _ptr(x), _ptr(pos), C.byref(weights_struct(W)), C.byref(cs),
                                  _ptr(y), _ptr(sel), wsp, wsn, _stream()))
     return y, sel
+
+
+def decode_select(cfg: Config, q, pos, cache: PagedCache, w_gq=None, ws: Workspace | None = None):
+    """Top-K blocks per KV group for the new tokens' query heads q [b, H, dh]
+    at positions pos [b] (device int32) against the cache's summaries."""
+    b = q.shape[0]
+    sel = torch.empty(b, cfg.n_kv_heads, cfg.top_k, dtype=torch.int32, device=q.device)
+    cs = cache.struct()
+    wsp, wsn = _ws(ws, workspace_size(cfg, OP_DECODE_SELECT, b, cache.max_context(cfg)))
+    _check(lib().sas_decode_select(C.byref(cfg), b, _ptr(q), _ptr(pos), _ptr(w_gq), C.byref(cs), _ptr(sel), wsp,
+                                   wsn, _stream()))
+    return sel
 
 
 def embed(cfg: Config, ids, table, img=None):

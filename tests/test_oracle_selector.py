@@ -172,3 +172,31 @@ def test_f32_selector_is_sequential_fp64():
     for j in range(dh):
         acc = acc + float(st["qhat"][0, t, j]) * float(st["kbar"][0, 2, j])
     assert st["r"][0, t, 2] == acc
+
+
+def test_decode_select_brute_force_with_exact_keys():
+    # Alg. 2's selection alone: gate query of the group's heads against the
+    # cached summaries of the floor(pos/B) complete blocks, Top-K under
+    # (r desc, m asc), ascending output, -1 padding; positions past the cache
+    # capacity see only the cached blocks
+    rng = np.random.default_rng(12)
+    b, H, Hkv, dh, B, K, M = 3, 4, 2, 8, 16, 5, 40
+    q = bf16_values(rng, (b, H, dh))
+    kbar = bf16_values(rng, (b, Hkv, M, dh))
+    kbar[:, :, 7] = kbar[:, :, 3]          # exact ties: the lower block must win
+    kbar[:, :, 20] = kbar[:, :, 3]
+    spec = oracle.Spec(H, Hkv, dh, B, K, "sparse", "bf16", 10000.0, 1e-6)
+    G = H // Hkv
+    for pos in ([0, 15, 16], [4 * B + 3, 5 * B, 6 * B - 1], [21 * B + 2, M * B + 70, -1]):
+        sel, _ = oracle.decode_select(q, np.array(pos), kbar, spec)
+        for bi in range(b):
+            c = 0 if pos[bi] < 0 else min(pos[bi] // B, M)
+            for g in range(Hkv):
+                qs = [sum(Fraction(q[bi, h, j]) for h in range(g * G, (g + 1) * G)) for j in range(dh)]
+                qh = [Fraction(oracle.round_bf16(np.array([float(v)]))[0]) for v in qs]
+                keys = [(sum(qh[j] * Fraction(kbar[bi, g, m, j]) for j in range(dh)), m) for m in range(c)]
+                ranked = sorted(keys, key=lambda km: (-km[0], km[1]))
+                want = sorted(m for _, m in ranked[:min(K, c)])
+                got = [int(m) for m in sel[bi, g] if m >= 0]
+                assert got == want, (pos[bi], g, got, want)
+                assert all(m == -1 for m in sel[bi, g][len(want):])
