@@ -24,6 +24,9 @@ Parity status of each part (how it is pinned by the oracle self-tests):
   selector but does not define its architecture; its arithmetic is pinned by
   exact rational brute force and planted rankings.  The architecture itself
   is "parity unpinned" by the paper (it is this build's reading).
+* attention backward, gate backward, selector backward: pinned against
+  torch autograd on a dense masked formulation and by central finite
+  differences of the fp64 forward.
 * normalized log gate, Top-K, attention: pinned by closed forms (q = 0),
   V = const, reductions to textbook causal / block-local attention computed
   by torch's scaled_dot_product_attention, causality, shift invariance and
@@ -33,6 +36,7 @@ from .numerics import rho, round_bf16, round_f32, rmsnorm, rope, silu
 from .selector import (block_summaries, gate_query, selector_scores,
                        normalized_log_gate, topk_blocks, select)
 from .attention import sas_attention
+from .backward import sas_attention_backward, gate_backward, selector_backward
 from .layer import (Spec, layer_forward, mlp_forward, attention_prefill,
                     DecodeCache, decode_step, decode_select, embed_tokens, lm_head_argmax)
 
@@ -42,4 +46,5 @@ __all__ = [
     "topk_blocks", "select", "sas_attention", "Spec", "layer_forward",
     "mlp_forward", "attention_prefill", "DecodeCache", "decode_step",
     "decode_select", "embed_tokens", "lm_head_argmax",
+    "sas_attention_backward", "gate_backward", "selector_backward",
 ]
