@@ -69,7 +69,8 @@ typedef enum {
   SAS_OP_LAYER = 2,     /* sas_layer_forward: batch, seq_len */
   SAS_OP_DECODE = 3,    /* sas_decode_step: batch, seq_len = max context (tokens) */
   SAS_OP_LM_HEAD = 4,   /* sas_lm_head_argmax: batch, seq_len = vocab */
-  SAS_OP_DECODE_SELECT = 5 /* sas_decode_select: batch, seq_len = max context (tokens) */
+  SAS_OP_DECODE_SELECT = 5, /* sas_decode_select: batch, seq_len = max context (tokens) */
+  SAS_OP_ATTENTION_BACKWARD = 6 /* sas_attention_backward: batch, seq_len */
 } sas_op;
 
 typedef struct {
@@ -177,6 +178,46 @@ size_t sas_workspace_size(const sas_config* cfg, int32_t op, int32_t batch, int3
 sas_status sas_attention_prefill(const sas_config* cfg, int32_t batch, int32_t seq_len,
                                  const sas_attn_in* in, sas_attn_out* out,
                                  void* ws, size_t ws_bytes, void* stream);
+
+/* Inputs of sas_attention_backward: the forward's inputs and outputs.
+ *  q [b,n,H,dh], k, v [b,n,Hkv,dh], o [b,n,H,dh] (sas_attention_prefill's
+ *  output), d_o [b,n,H,dh] the upstream gradient (activation dtype);
+ *  lse [b,H,n] fp32 (the forward's LSE); sel_idx [b,Hkv,n,K] and, in GATED
+ *  mode, log_gate [b,Hkv,n,ceil(n/B)] fp32 (the forward's selection and
+ *  normalized log gates; unused in DENSE mode). */
+typedef struct {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* o;
+  const void* d_o;
+  const float* lse;
+  const int32_t* sel_idx;
+  const float* log_gate;
+} sas_bwd_in;
+
+/* Outputs of sas_attention_backward: dq [b,n,H,dh], dk, dv [b,n,Hkv,dh]
+ * (activation dtype), dlog_gate [b,Hkv,n,K] fp32 or NULL: the gradient of
+ * each selected block's log gate (GATED), summed over the group's heads, at
+ * the slots of sel_idx (0 in empty slots). */
+typedef struct {
+  void* dq;
+  void* dk;
+  void* dv;
+  float* dlog_gate;
+} sas_bwd_out;
+
+/* Backward of the attention of sas_attention_prefill (Sec. 4.3, Eq.
+ * ours_train; App. E's recomputation backward), the kernel of the training
+ * step of Alg. 1: recomputes the attended sets and probabilities from the
+ * forward's LSE and selection and writes dQ, dK, dV and the block log-gate
+ * gradient dlog g_m = sum over the group's heads and the block's keys of
+ * p_i (dO.v_i - dO.o) (the inner-gate gradient of Eq. gate_posi, for log g).
+ * cfg->mode must be the forward's.  ws: sas_workspace_size(cfg,
+ * SAS_OP_ATTENTION_BACKWARD, batch, seq_len). */
+sas_status sas_attention_backward(const sas_config* cfg, int32_t batch, int32_t seq_len,
+                                  const sas_bwd_in* in, sas_bwd_out* out,
+                                  void* ws, size_t ws_bytes, void* stream);
 
 /* y = x + SwiGLU(RMSNorm(x)) for `tokens` rows of width d_model:
  * u = RMSNorm(x) * rms2; a = silu(u W_gate^T) * (u W_up^T); y = x + a W_down^T.

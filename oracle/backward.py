@@ -75,8 +75,10 @@ def sas_attention_backward(Q, K, V, dO, B, mode, sel=None, log_gate=None, sm_sca
                 o = p @ Vg
                 ds = p * (Vg @ do - do @ o)
                 dQ[t, h] = sm * (ds @ Kg)
-                np.add.at(dK[:, g, :], idx, sm * ds[:, None] * q[None, :])
-                np.add.at(dV[:, g, :], idx, p[:, None] * do[None, :])
+                # the attended keys of one query are distinct (disjoint blocks), so
+                # indexed accumulation adds each contribution once
+                dK[idx, g, :] += sm * ds[:, None] * q[None, :]
+                dV[idx, g, :] += p[:, None] * do[None, :]
                 if mode == "gated":
                     for m in np.unique(blk[blk >= 0]):
                         dL[g, t, m] += ds[blk == m].sum()

@@ -421,6 +421,24 @@ DecodeWs carve_decode(Carve& cv, const sas_config* c, int b, int max_blocks) {
   return w;
 }
 
+struct BwdWs {
+  float* delta;
+  float* dlg_head;
+  uint8_t* chunk_mask;
+  float* sel_bias;
+};
+
+BwdWs carve_backward(Carve& cv, const sas_config* c, int b, int n) {
+  const size_t H = c->n_heads, Hkv = c->n_kv_heads, K = c->top_k > 0 ? c->top_k : 0;
+  const size_t NB = cdiv(n, c->block_size), nqc = cdiv(n, 32);
+  BwdWs w;
+  w.delta = (float*)cv.take((size_t)b * H * n * 4);
+  w.dlg_head = (float*)cv.take((size_t)b * H * n * K * 4);
+  w.chunk_mask = (uint8_t*)cv.take(align_up((size_t)b * Hkv * nqc * NB, 4));
+  w.sel_bias = (float*)cv.take((size_t)b * Hkv * n * K * 4);
+  return w;
+}
+
 constexpr int ARGMAX_SLICES = 64;
 
 struct LmWs {
@@ -479,6 +497,10 @@ size_t sas_workspace_size(const sas_config* c, int32_t op, int32_t batch, int32_
       if (seq_len <= 0 || check_config(c, false) != SAS_OK) return 0;
       carve_attention(cv, c, batch, seq_len);
       break;
+    case SAS_OP_ATTENTION_BACKWARD:
+      if (seq_len <= 0 || check_config(c, false) != SAS_OK) return 0;
+      carve_backward(cv, c, batch, seq_len);
+      break;
     case SAS_OP_MLP:
       if (check_config(c, true) != SAS_OK) return 0;
       carve_mlp(cv, c, (size_t)batch);
@@ -505,6 +527,73 @@ size_t sas_workspace_size(const sas_config* c, int32_t op, int32_t batch, int32_
   }
   g_err.clear();
   return cv.off;
+}
+
+sas_status sas_attention_backward(const sas_config* c, int32_t batch, int32_t seq_len, const sas_bwd_in* in,
+                                  sas_bwd_out* out, void* ws, size_t ws_bytes, void* stream) {
+  SAS_TRY(check_config(c, false));
+  if (batch <= 0 || seq_len <= 0)
+    return fail(SAS_ERR_INVALID_ARGUMENT, "batch %d and seq_len %d must be positive", batch, seq_len);
+  if (!in || !out) return fail(SAS_ERR_INVALID_ARGUMENT, "in/out is NULL");
+  SAS_TRY(check_ptr(in->q, "in.q", true));
+  SAS_TRY(check_ptr(in->k, "in.k", true));
+  SAS_TRY(check_ptr(in->v, "in.v", true));
+  SAS_TRY(check_ptr(in->o, "in.o", true));
+  SAS_TRY(check_ptr(in->d_o, "in.d_o", true));
+  SAS_TRY(check_ptr(in->lse, "in.lse", true));
+  const bool sparse = c->mode != SAS_MODE_DENSE && c->top_k > 0;
+  SAS_TRY(check_ptr(in->sel_idx, "in.sel_idx", sparse));
+  SAS_TRY(check_ptr(in->log_gate, "in.log_gate", sparse && c->mode == SAS_MODE_GATED));
+  SAS_TRY(check_ptr(out->dq, "out.dq", true));
+  SAS_TRY(check_ptr(out->dk, "out.dk", true));
+  SAS_TRY(check_ptr(out->dv, "out.dv", true));
+  SAS_TRY(check_ptr(out->dlog_gate, "out.dlog_gate", false));
+  Carve cv(ws);
+  BwdWs bw = carve_backward(cv, c, batch, seq_len);
+  SAS_TRY(check_ws(ws, ws_bytes, cv.off));
+  hipStream_t s = (hipStream_t)stream;
+  const int K = c->top_k > 0 ? c->top_k : 0;
+  const int NB = (int)cdiv(seq_len, c->block_size);
+  if (sparse && c->mode == SAS_MODE_GATED) {
+    Timed tm("bwd_gather_gate", s);
+    HIP_TRY(launch_gather_gate(in->sel_idx, in->log_gate, batch, seq_len, c->n_kv_heads, K, NB, bw.sel_bias, s),
+            "gather gate");
+  }
+  BwdArgs a = {};
+  a.b = batch;
+  a.n = seq_len;
+  a.H = c->n_heads;
+  a.Hkv = c->n_kv_heads;
+  a.dh = c->head_dim;
+  a.B = c->block_size;
+  a.K = sparse ? K : 0;
+  a.mode = c->mode;
+  a.sm_scale = sm_scale_of(c);
+  a.Q = in->q;
+  a.Kt = in->k;
+  a.V = in->v;
+  a.O = in->o;
+  a.dO = in->d_o;
+  a.lse = in->lse;
+  a.sel = sparse ? in->sel_idx : nullptr;
+  a.sel_bias = bw.sel_bias;
+  a.dQ = out->dq;
+  a.dK = out->dk;
+  a.dV = out->dv;
+  a.dlog_gate = out->dlog_gate;
+  a.delta = bw.delta;
+  a.dlg_head = bw.dlg_head;
+  a.chunk_mask = bw.chunk_mask;
+  if (out->dlog_gate && (c->mode != SAS_MODE_GATED || K == 0)) {
+    Timed tm("bwd_zero", s);
+    HIP_TRY(launch_fill_f32(out->dlog_gate, (size_t)batch * c->n_kv_heads * seq_len * (K > 0 ? K : 0), 0.f, s),
+            "zero dlog_gate");
+  }
+  {
+    Timed tm("attention_bwd", s);
+    HIP_TRY(launch_attention_backward(c->dtype, a, s), "attention backward");
+  }
+  return SAS_OK;
 }
 
 sas_status sas_attention_prefill(const sas_config* c, int32_t batch, int32_t seq_len, const sas_attn_in* in,

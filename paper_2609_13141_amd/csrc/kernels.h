@@ -87,6 +87,34 @@ struct AttnArgs {
 };
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 
+// ---- backward.hip ----------------------------------------------------------
+struct BwdArgs {
+  int b, n, H, Hkv, dh, B, K, mode;
+  float sm_scale;
+  const void* Q;          // [b, n, H, dh]
+  const void* Kt;         // [b, n, Hkv, dh]
+  const void* V;          // [b, n, Hkv, dh]
+  const void* O;          // [b, n, H, dh] forward output
+  const void* dO;         // [b, n, H, dh]
+  const float* lse;       // [b, H, n] forward LSE (natural log)
+  const int32_t* sel;     // [b, Hkv, n, K]
+  const float* sel_bias;  // [b, Hkv, n, K] (GATED)
+  void* dQ;               // [b, n, H, dh]
+  void* dK;               // [b, n, Hkv, dh]
+  void* dV;
+  float* dlog_gate;       // [b, Hkv, n, K] or null
+  // scratch
+  float* delta;           // [b, H, n]
+  float* dlg_head;        // [b, H, n, K]
+  uint8_t* chunk_mask;    // [b, Hkv, ceil(n/32), ceil(n/B)] (bf16 path)
+};
+hipError_t launch_attention_backward(int dtype, const BwdArgs& a, hipStream_t s);
+// p[0..n) = v with a kernel (capturable in a graph, unlike a memset node)
+hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t s);
+// bias[b, g, t, k] = log_gate[b, g, t, sel[b, g, t, k]] (0 for empty slots)
+hipError_t launch_gather_gate(const int32_t* sel, const float* log_gate, int b, int n, int Hkv, int K, int NB,
+                              float* bias, hipStream_t s);
+
 // ---- decode.hip ------------------------------------------------------------
 // rope[r, i] for the positions pos[r] of the new tokens (fp64 math).
 hipError_t launch_rope_rows(const int32_t* pos, float2* rope, int b, int dh, float base, hipStream_t s);

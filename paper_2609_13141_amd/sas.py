@@ -20,11 +20,11 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsas.so")
 SAS_OK, SAS_ERR_INVALID_ARGUMENT, SAS_ERR_UNSUPPORTED, SAS_ERR_WORKSPACE, SAS_ERR_HIP = 0, -1, -2, -3, -4
 SAS_F32, SAS_BF16 = 0, 1
 MODES = {"dense": 0, "sparse": 1, "gated": 2}
-OP_ATTENTION, OP_MLP, OP_LAYER, OP_DECODE, OP_LM_HEAD, OP_DECODE_SELECT = 0, 1, 2, 3, 4, 5
+OP_ATTENTION, OP_MLP, OP_LAYER, OP_DECODE, OP_LM_HEAD, OP_DECODE_SELECT, OP_ATTENTION_BACKWARD = 0, 1, 2, 3, 4, 5, 6
 TORCH_DTYPE = {"bf16": torch.bfloat16, "f32": torch.float32}
 
 EXPORTS = ("sas_workspace_size", "sas_attention_prefill", "sas_mlp_forward", "sas_layer_forward",
-           "sas_decode_step", "sas_decode_select", "sas_embed", "sas_lm_head_argmax", "sas_last_error", "sas_version",
+           "sas_decode_step", "sas_decode_select", "sas_attention_backward", "sas_embed", "sas_lm_head_argmax", "sas_last_error", "sas_version",
            "sas_profiler_start", "sas_profiler_stop", "sas_profiler_record")
 
 
@@ -49,6 +49,14 @@ class AttnIn(C.Structure):
 class AttnOut(C.Structure):
     _fields_ = [("o", C.c_void_p), ("lse", C.c_void_p), ("k_summary", C.c_void_p),
                 ("sel_idx", C.c_void_p), ("log_gate", C.c_void_p), ("tau", C.c_void_p)]
+
+
+class BwdIn(C.Structure):
+    _fields_ = [(f, C.c_void_p) for f in ("q", "k", "v", "o", "d_o", "lse", "sel_idx", "log_gate")]
+
+
+class BwdOut(C.Structure):
+    _fields_ = [(f, C.c_void_p) for f in ("dq", "dk", "dv", "dlog_gate")]
 
 
 class LayerWeights(C.Structure):
@@ -93,6 +101,9 @@ def lib() -> C.CDLL:
                                   vp, vp, vp, sz, vp]
     L.sas_decode_select.restype = i32
     L.sas_decode_select.argtypes = [C.POINTER(Config), i32, vp, vp, vp, C.POINTER(PagedKV), vp, vp, sz, vp]
+    L.sas_attention_backward.restype = i32
+    L.sas_attention_backward.argtypes = [C.POINTER(Config), i32, i32, C.POINTER(BwdIn), C.POINTER(BwdOut), vp, sz,
+                                         vp]
     L.sas_embed.restype = i32
     L.sas_embed.argtypes = [C.POINTER(Config), i32, i32, vp, vp, i32, vp, i32, vp, vp]
     L.sas_lm_head_argmax.restype = i32
@@ -188,6 +199,22 @@ def attention_prefill(cfg: Config, q, k, v, w_gq=None, w_gk=None, *, lse=True, k
     aout = AttnOut(*[_ptr(out.get(f)) for f in ("o", "lse", "k_summary", "sel_idx", "log_gate", "tau")])
     wsp, wsn = _ws(ws, workspace_size(cfg, OP_ATTENTION, b, n))
     _check(lib().sas_attention_prefill(C.byref(cfg), b, n, C.byref(ain), C.byref(aout), wsp, wsn, _stream()))
+    return out
+
+
+def attention_backward(cfg: Config, q, k, v, o, d_o, lse, sel_idx=None, log_gate=None, *, dlog_gate: bool = True,
+                       ws: Workspace | None = None) -> dict:
+    """dQ, dK, dV (and the selected blocks' log-gate gradient) of the attention
+    given the forward's inputs, its output o, LSE and selection, and d_o."""
+    b, n, H, dh = q.shape
+    Hkv, K = cfg.n_kv_heads, max(cfg.top_k, 0)
+    out = {"dq": torch.empty_like(q), "dk": torch.empty_like(k), "dv": torch.empty_like(v)}
+    if dlog_gate:
+        out["dlog_gate"] = torch.empty(b, Hkv, n, K, dtype=torch.float32, device=q.device)
+    bi = BwdIn(*[_ptr(t) for t in (q, k, v, o, d_o, lse, sel_idx, log_gate)])
+    bo = BwdOut(*[_ptr(out.get(f)) for f in ("dq", "dk", "dv", "dlog_gate")])
+    wsp, wsn = _ws(ws, workspace_size(cfg, OP_ATTENTION_BACKWARD, b, n))
+    _check(lib().sas_attention_backward(C.byref(cfg), b, n, C.byref(bi), C.byref(bo), wsp, wsn, _stream()))
     return out
 
 
