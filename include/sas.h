@@ -70,7 +70,8 @@ typedef enum {
   SAS_OP_DECODE = 3,    /* sas_decode_step: batch, seq_len = max context (tokens) */
   SAS_OP_LM_HEAD = 4,   /* sas_lm_head_argmax: batch, seq_len = vocab */
   SAS_OP_DECODE_SELECT = 5, /* sas_decode_select: batch, seq_len = max context (tokens) */
-  SAS_OP_ATTENTION_BACKWARD = 6 /* sas_attention_backward: batch, seq_len */
+  SAS_OP_ATTENTION_BACKWARD = 6, /* sas_attention_backward: batch, seq_len */
+  SAS_OP_SELECTOR_BACKWARD = 7   /* sas_selector_backward: batch, seq_len */
 } sas_op;
 
 typedef struct {
@@ -218,6 +219,53 @@ typedef struct {
 sas_status sas_attention_backward(const sas_config* cfg, int32_t batch, int32_t seq_len,
                                   const sas_bwd_in* in, sas_bwd_out* out,
                                   void* ws, size_t ws_bytes, void* stream);
+
+/* Inputs of sas_selector_backward.  q [b,n,H,dh], k [b,n,Hkv,dh] (the
+ * forward's post-RoPE queries and keys, activation dtype); w_gq, w_gk
+ * [Hkv,dh,dh] or NULL (the selector's optional projections, as given to the
+ * forward); sel_idx [b,Hkv,n,K] and log_gate [b,Hkv,n,ceil(n/B)] fp32 (the
+ * forward's selection and normalized log gates); dlog_gate [b,Hkv,n,K] fp32
+ * (sas_attention_backward's output, or any gradient of the selected blocks'
+ * log gates at the slots of sel_idx). */
+typedef struct {
+  const void* q;
+  const void* k;
+  const void* w_gq;
+  const void* w_gk;
+  const int32_t* sel_idx;
+  const float* log_gate;
+  const float* dlog_gate;
+} sas_sel_bwd_in;
+
+/* Outputs of sas_selector_backward, all fp32, each optional except as noted:
+ *  ds [b,Hkv,n,ceil(n/B)]: gradient of the selector scores s (0 for blocks
+ *    that are not historical for the row);
+ *  dqhat [b,Hkv,n,dh]: gradient of the (projected) gate queries;
+ *  dkbar [b,Hkv,ceil(n/B),dh]: gradient of the (projected) block summaries
+ *    (0 for an incomplete last block);
+ *  dw_gq, dw_gk [Hkv,dh,dh]: gradients of the projections, summed over the
+ *    batch; required when the projection is given, ignored otherwise. */
+typedef struct {
+  float* ds;
+  float* dqhat;
+  float* dkbar;
+  float* dw_gq;
+  float* dw_gk;
+} sas_sel_bwd_out;
+
+/* Backward of the selector (Alg. 1's update of the selector parameters):
+ * dlog g -> ds through the normalized log gate of Eq. normalized_log_gate
+ * (ds_m = dlog g_m - g_m sum over the row's historical blocks of dlog g, the
+ * softmax backward of App. D.3 with dlog g = 0 off the selected set), then
+ * through the scores s = qhat.kbar / (G sqrt(dh)) to the gate queries and
+ * summaries and, when given, to W_gq and W_gk.  The Top-K set is piecewise
+ * constant and passes no gradient; the roundings of the forward are taken
+ * as identities.  Gate queries and summaries are recomputed from q and k.
+ * With top_k = 0 every output is zero.  ws: sas_workspace_size(cfg,
+ * SAS_OP_SELECTOR_BACKWARD, batch, seq_len). */
+sas_status sas_selector_backward(const sas_config* cfg, int32_t batch, int32_t seq_len,
+                                 const sas_sel_bwd_in* in, sas_sel_bwd_out* out,
+                                 void* ws, size_t ws_bytes, void* stream);
 
 /* y = x + SwiGLU(RMSNorm(x)) for `tokens` rows of width d_model:
  * u = RMSNorm(x) * rms2; a = silu(u W_gate^T) * (u W_up^T); y = x + a W_down^T.

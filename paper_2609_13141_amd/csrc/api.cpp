@@ -5,6 +5,7 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <algorithm>
 #include <string>
 #include <vector>
 
@@ -439,6 +440,60 @@ BwdWs carve_backward(Carve& cv, const sas_config* c, int b, int n) {
   return w;
 }
 
+// Selector backward scratch.  The reductions over t (dkbar, dW_gq) and over
+// the batch (dW) go through split partials summed in a fixed order.
+struct SelBwdWs {
+  void* kplain;
+  void* ksum;
+  void* qplain;
+  void* qhat;
+  float* ds;
+  float* dqhat;
+  float* dkbar;
+  float* part;
+};
+
+// k splits of a reduction of length K feeding `tiles` output tiles per batch
+// entry, for Z entries: enough workgroups to fill the chip, each split >= 256
+int sel_bwd_splits(int tiles, int Z, int K) {
+  const int want = cdiv(1024, tiles * Z);
+  return std::max(1, std::min(want, cdiv(K, 256)));
+}
+
+struct SelBwdShape {
+  int NB, Z, s_dkbar, s_dwq, s_dwk;
+  size_t part_floats;
+};
+
+SelBwdShape sel_bwd_shape(const sas_config* c, int b, int n) {
+  SelBwdShape h;
+  const int dh = c->head_dim, Hkv = c->n_kv_heads;
+  h.NB = cdiv(n, c->block_size);
+  h.Z = b * Hkv;
+  const int tdh = cdiv(dh, 64);
+  h.s_dkbar = sel_bwd_splits(cdiv(h.NB, 64) * tdh, h.Z, n);
+  h.s_dwq = sel_bwd_splits(tdh * tdh, h.Z, n);
+  h.s_dwk = sel_bwd_splits(tdh * tdh, h.Z, h.NB);
+  const size_t z = h.Z;
+  h.part_floats = std::max({z * h.s_dkbar * h.NB * dh, z * h.s_dwq * dh * dh, z * h.s_dwk * dh * dh});
+  return h;
+}
+
+SelBwdWs carve_selector_backward(Carve& cv, const sas_config* c, int b, int n) {
+  const size_t ab = act_bytes(c), Hkv = c->n_kv_heads, dh = c->head_dim;
+  const SelBwdShape h = sel_bwd_shape(c, b, n);
+  SelBwdWs w;
+  w.kplain = cv.take((size_t)b * Hkv * h.NB * dh * ab);
+  w.ksum = cv.take((size_t)b * Hkv * h.NB * dh * ab);
+  w.qplain = cv.take((size_t)b * Hkv * n * dh * ab);
+  w.qhat = cv.take((size_t)b * Hkv * n * dh * ab);
+  w.ds = (float*)cv.take((size_t)b * Hkv * n * h.NB * 4);
+  w.dqhat = (float*)cv.take((size_t)b * Hkv * n * dh * 4);
+  w.dkbar = (float*)cv.take((size_t)b * Hkv * h.NB * dh * 4);
+  w.part = (float*)cv.take(h.part_floats * 4);
+  return w;
+}
+
 constexpr int ARGMAX_SLICES = 64;
 
 struct LmWs {
@@ -500,6 +555,10 @@ size_t sas_workspace_size(const sas_config* c, int32_t op, int32_t batch, int32_
     case SAS_OP_ATTENTION_BACKWARD:
       if (seq_len <= 0 || check_config(c, false) != SAS_OK) return 0;
       carve_backward(cv, c, batch, seq_len);
+      break;
+    case SAS_OP_SELECTOR_BACKWARD:
+      if (seq_len <= 0 || check_config(c, false) != SAS_OK) return 0;
+      carve_selector_backward(cv, c, batch, seq_len);
       break;
     case SAS_OP_MLP:
       if (check_config(c, true) != SAS_OK) return 0;
@@ -592,6 +651,104 @@ sas_status sas_attention_backward(const sas_config* c, int32_t batch, int32_t se
   {
     Timed tm("attention_bwd", s);
     HIP_TRY(launch_attention_backward(c->dtype, a, s), "attention backward");
+  }
+  return SAS_OK;
+}
+
+sas_status sas_selector_backward(const sas_config* c, int32_t batch, int32_t seq_len, const sas_sel_bwd_in* in,
+                                 sas_sel_bwd_out* out, void* ws, size_t ws_bytes, void* stream) {
+  SAS_TRY(check_config(c, false));
+  if (batch <= 0 || seq_len <= 0)
+    return fail(SAS_ERR_INVALID_ARGUMENT, "batch %d and seq_len %d must be positive", batch, seq_len);
+  if (!in || !out) return fail(SAS_ERR_INVALID_ARGUMENT, "in/out is NULL");
+  const int K = c->top_k;
+  SAS_TRY(check_ptr(in->q, "in.q", true));
+  SAS_TRY(check_ptr(in->k, "in.k", true));
+  SAS_TRY(check_ptr(in->w_gq, "in.w_gq", false));
+  SAS_TRY(check_ptr(in->w_gk, "in.w_gk", false));
+  SAS_TRY(check_ptr(in->sel_idx, "in.sel_idx", K > 0));
+  SAS_TRY(check_ptr(in->log_gate, "in.log_gate", K > 0));
+  SAS_TRY(check_ptr(in->dlog_gate, "in.dlog_gate", K > 0));
+  SAS_TRY(check_ptr(out->ds, "out.ds", false));
+  SAS_TRY(check_ptr(out->dqhat, "out.dqhat", false));
+  SAS_TRY(check_ptr(out->dkbar, "out.dkbar", false));
+  SAS_TRY(check_ptr(out->dw_gq, "out.dw_gq", in->w_gq != nullptr));
+  SAS_TRY(check_ptr(out->dw_gk, "out.dw_gk", in->w_gk != nullptr));
+  Carve cv(ws);
+  SelBwdWs w = carve_selector_backward(cv, c, batch, seq_len);
+  SAS_TRY(check_ws(ws, ws_bytes, cv.off));
+  hipStream_t s = (hipStream_t)stream;
+  const int n = seq_len, H = c->n_heads, Hkv = c->n_kv_heads, dh = c->head_dim, B = c->block_size;
+  const SelBwdShape h = sel_bwd_shape(c, batch, n);
+  const int NB = h.NB;
+  const size_t rows = (size_t)batch * Hkv * n;
+  float* dw_gq = in->w_gq ? out->dw_gq : nullptr;
+  float* dw_gk = in->w_gk ? out->dw_gk : nullptr;
+  if (K == 0) {  // no selected block: every gradient is zero
+    Timed tm("sel_bwd_zero", s);
+    HIP_TRY(launch_fill_f32(out->ds, out->ds ? rows * NB : 0, 0.f, s), "zero ds");
+    HIP_TRY(launch_fill_f32(out->dqhat, out->dqhat ? rows * dh : 0, 0.f, s), "zero dqhat");
+    HIP_TRY(launch_fill_f32(out->dkbar, out->dkbar ? (size_t)batch * Hkv * NB * dh : 0, 0.f, s), "zero dkbar");
+    HIP_TRY(launch_fill_f32(dw_gq, dw_gq ? (size_t)Hkv * dh * dh : 0, 0.f, s), "zero dw_gq");
+    HIP_TRY(launch_fill_f32(dw_gk, dw_gk ? (size_t)Hkv * dh * dh : 0, 0.f, s), "zero dw_gk");
+    return SAS_OK;
+  }
+  {
+    Timed tm("summaries", s);
+    HIP_TRY(launch_block_summaries(c->dtype, in->k, batch, n, Hkv, dh, B, in->w_gk, w.kplain, w.ksum, s),
+            "block summaries");
+  }
+  {
+    Timed tm("gate_query", s);
+    HIP_TRY(launch_gate_query(c->dtype, in->q, batch, n, H, Hkv, dh, in->w_gq, w.qplain, w.qhat, s), "gate query");
+  }
+  float* ds = out->ds ? out->ds : w.ds;
+  {
+    Timed tm("sel_bwd_ds", s);
+    HIP_TRY(launch_selector_ds(in->sel_idx, in->log_gate, in->dlog_gate, batch, n, Hkv, K, B, ds, s), "ds");
+  }
+  // s = r / (G sqrt(dh)) with r = qhat . kbar
+  const float dr_scale = 1.0f / ((float)(H / Hkv) * sqrtf((float)dh));
+  float* dqhat = out->dqhat ? out->dqhat : w.dqhat;
+  float* dkbar = out->dkbar ? out->dkbar : w.dkbar;
+  Timed tm("sel_bwd_gemm", s);
+  if (out->dqhat || dw_gq) {  // dqhat[t] = c sum_m ds[t, m] kbar[m]
+    SmallGemm g = {};
+    g.M = n, g.N = dh, g.K = NB, g.Z = h.Z, g.splits = 1, g.alpha = dr_scale;
+    g.A = ds, g.sAz = (long long)n * NB, g.sAi = NB, g.sAk = 1;
+    g.Bm = w.ksum, g.sBz = (long long)NB * dh, g.sBk = dh, g.sBj = 1;
+    g.C = dqhat, g.sCz = (long long)n * dh, g.sCs = 0, g.sCi = dh;
+    HIP_TRY(launch_small_gemm(c->dtype, g, s), "dqhat");
+  }
+  if (out->dkbar || dw_gk) {  // dkbar[m] = c sum_t ds[t, m] qhat[t]
+    const size_t E = (size_t)NB * dh;
+    SmallGemm g = {};
+    g.M = NB, g.N = dh, g.K = n, g.Z = h.Z, g.splits = h.s_dkbar, g.alpha = dr_scale;
+    g.A = ds, g.sAz = (long long)n * NB, g.sAi = 1, g.sAk = NB;
+    g.Bm = w.qhat, g.sBz = (long long)n * dh, g.sBk = dh, g.sBj = 1;
+    const bool direct = h.s_dkbar == 1;
+    g.C = direct ? dkbar : w.part, g.sCz = direct ? (long long)E : (long long)(E * h.s_dkbar), g.sCs = E, g.sCi = dh;
+    HIP_TRY(launch_small_gemm(c->dtype, g, s), "dkbar");
+    if (!direct) HIP_TRY(launch_partial_sum(w.part, 1, h.Z, h.s_dkbar, E, dkbar, s), "dkbar sum");
+  }
+  const size_t E = (size_t)dh * dh;
+  if (dw_gq) {  // dW_gq[g] = sum_b sum_t dqhat[t]^T qhat0[t]
+    SmallGemm g = {};
+    g.M = dh, g.N = dh, g.K = n, g.Z = h.Z, g.splits = h.s_dwq, g.alpha = 1.f;
+    g.A = dqhat, g.sAz = (long long)n * dh, g.sAi = 1, g.sAk = dh;
+    g.Bm = w.qplain, g.sBz = (long long)n * dh, g.sBk = dh, g.sBj = 1;
+    g.C = w.part, g.sCz = (long long)(E * h.s_dwq), g.sCs = E, g.sCi = dh;
+    HIP_TRY(launch_small_gemm(c->dtype, g, s), "dw_gq");
+    HIP_TRY(launch_partial_sum(w.part, batch, Hkv, h.s_dwq, E, dw_gq, s), "dw_gq sum");
+  }
+  if (dw_gk) {  // dW_gk[g] = sum_b sum_m dkbar[m]^T kbar0[m]
+    SmallGemm g = {};
+    g.M = dh, g.N = dh, g.K = NB, g.Z = h.Z, g.splits = h.s_dwk, g.alpha = 1.f;
+    g.A = dkbar, g.sAz = (long long)NB * dh, g.sAi = 1, g.sAk = dh;
+    g.Bm = w.kplain, g.sBz = (long long)NB * dh, g.sBk = dh, g.sBj = 1;
+    g.C = w.part, g.sCz = (long long)(E * h.s_dwk), g.sCs = E, g.sCi = dh;
+    HIP_TRY(launch_small_gemm(c->dtype, g, s), "dw_gk");
+    HIP_TRY(launch_partial_sum(w.part, batch, Hkv, h.s_dwk, E, dw_gk, s), "dw_gk sum");
   }
   return SAS_OK;
 }

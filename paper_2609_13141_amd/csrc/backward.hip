@@ -9,6 +9,11 @@
 //   dlog g[g, t, slot of m] = sum_{h in g} sum_{i in B_m} ds_i   (GATED)
 // Pass 1 walks queries (dQ and the per-head block sums of ds); pass 2 walks
 // keys (dK, dV) and visits only the query chunks that attend them.
+//
+// Selector (the end of this file): the gate's softmax backward gives the
+// score gradient ds of each row's historical blocks; the scores are inner
+// products of gate queries and block summaries, so their gradients (and
+// those of the optional projections) are small batched GEMMs over ds.
 #include <float.h>
 
 #include "common.h"
@@ -652,6 +657,138 @@ hipError_t launch_gather_gate(const int32_t* sel, const float* log_gate, int b, 
   const size_t tot = (size_t)b * Hkv * n * K;
   if (tot == 0) return hipSuccess;
   bwd_gather_gate_kernel<<<(unsigned)cdiv(tot, 256), 256, 0, s>>>(sel, log_gate, b, n, Hkv, K, NB, bias);
+  return hipGetLastError();
+}
+
+// ---- selector ------------------------------------------------------------------
+// one wave per row (b, g, t); lane k < K holds slot k
+__global__ void __launch_bounds__(256) selector_ds_kernel(const int32_t* __restrict__ sel,
+                                                          const float* __restrict__ log_gate,
+                                                          const float* __restrict__ dlog_gate, int rows, int n,
+                                                          int K, int B, int NB, float* __restrict__ ds) {
+  const int row = (int)(((size_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6), lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  const int C = (row % n) / B;
+  const int sk = lane < K ? sel[(size_t)row * K + lane] : -1;
+  const float dk = sk >= 0 ? dlog_gate[(size_t)row * K + lane] : 0.f;
+  const float D = wave_sum(dk);
+  const float* lg = log_gate + (size_t)row * NB;
+  float* out = ds + (size_t)row * NB;
+  for (int m0 = 0; m0 < NB; m0 += 64) {
+    const int m = m0 + lane;
+    float v = 0.f;
+    if (m < C) v = -expf(lg[m]) * D;
+    for (int k = 0; k < K; ++k) {
+      const int s = __shfl(sk, k, 64);
+      const float d = __shfl(dk, k, 64);
+      if (s == m && m < C) v += d;
+    }
+    if (m < NB) out[m] = v;
+  }
+}
+
+hipError_t launch_selector_ds(const int32_t* sel, const float* log_gate, const float* dlog_gate, int b, int n,
+                              int Hkv, int K, int B, float* ds, hipStream_t s) {
+  const int rows = b * Hkv * n;
+  if (rows <= 0) return hipSuccess;
+  if (K > 64) return hipErrorInvalidValue;
+  selector_ds_kernel<<<cdiv(rows, 4), 256, 0, s>>>(sel, log_gate, dlog_gate, rows, n, K, B, cdiv(n, B), ds);
+  return hipGetLastError();
+}
+
+// 64 x 64 output tile per workgroup, 16-deep k steps staged in LDS as fp32;
+// thread (tx, ty) owns rows ty + 16 r and columns tx + 16 c.  Tile loads run
+// along whichever of the operand's two indices is contiguous.
+template <typename T>
+__global__ void __launch_bounds__(256) small_gemm_kernel(SmallGemm P) {
+  __shared__ float As[16][64 + 4];
+  __shared__ float Bs[16][64 + 4];
+  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+  const int j0 = blockIdx.x * 64, i0 = blockIdx.y * 64;
+  const int z = blockIdx.z / P.splits, sp = blockIdx.z % P.splits;
+  const int kc = (P.K + P.splits - 1) / P.splits;
+  const int kb = sp * kc, ke = min(P.K, kb + kc);
+  const float* A = P.A + z * P.sAz;
+  const T* Bm = (const T*)P.Bm + z * P.sBz;
+  float acc[4][4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[r][c] = 0.f;
+  for (int k0 = kb; k0 < ke; k0 += 16) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int idx = tid + e * 256;
+      int ii, kk;
+      if (P.sAi == 1) {
+        ii = idx & 63;
+        kk = idx >> 6;
+      } else {
+        kk = idx & 15;
+        ii = idx >> 4;
+      }
+      const int i = i0 + ii, k = k0 + kk;
+      As[kk][ii] = (i < P.M && k < ke) ? A[i * P.sAi + k * P.sAk] : 0.f;
+      int jj;
+      if (P.sBj == 1) {
+        jj = idx & 63;
+        kk = idx >> 6;
+      } else {
+        kk = idx & 15;
+        jj = idx >> 4;
+      }
+      const int j = j0 + jj, k2 = k0 + kk;
+      Bs[kk][jj] = (j < P.N && k2 < ke) ? Act<T>::to_f32(Bm[j * P.sBj + k2 * P.sBk]) : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float a[4], bv[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) a[r] = As[kk][ty + 16 * r];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) bv[c] = Bs[kk][tx + 16 * c];
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[r][c] = fmaf(a[r], bv[c], acc[r][c]);
+    }
+    __syncthreads();
+  }
+  float* C = P.C + z * P.sCz + sp * P.sCs;
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int i = i0 + ty + 16 * r, j = j0 + tx + 16 * c;
+      if (i < P.M && j < P.N) C[i * P.sCi + j] = P.alpha * acc[r][c];
+    }
+}
+
+hipError_t launch_small_gemm(int dtype, const SmallGemm& g, hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0 || g.Z <= 0) return hipSuccess;
+  if (g.splits < 1 || (size_t)g.Z * g.splits > 65535) return hipErrorInvalidValue;
+  dim3 grid(cdiv(g.N, 64), cdiv(g.M, 64), g.Z * g.splits);
+  if (dtype == SAS_BF16) small_gemm_kernel<bf16_t><<<grid, 256, 0, s>>>(g);
+  else small_gemm_kernel<float><<<grid, 256, 0, s>>>(g);
+  return hipGetLastError();
+}
+
+__global__ void partial_sum_kernel(const float* __restrict__ part, int U, int ZO, int S, size_t E,
+                                   float* __restrict__ out) {
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (size_t)ZO * E) return;
+  const size_t zo = idx / E, e = idx % E;
+  float acc = 0.f;
+  for (int u = 0; u < U; ++u)
+    for (int q = 0; q < S; ++q) acc += part[(((size_t)u * ZO + zo) * S + q) * E + e];
+  out[idx] = acc;
+}
+
+hipError_t launch_partial_sum(const float* part, int U, int ZO, int S, size_t E, float* out, hipStream_t s) {
+  const size_t tot = (size_t)ZO * E;
+  if (tot == 0) return hipSuccess;
+  partial_sum_kernel<<<(unsigned)cdiv(tot, 256), 256, 0, s>>>(part, U, ZO, S, E, out);
   return hipGetLastError();
 }
 

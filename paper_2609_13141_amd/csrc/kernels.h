@@ -7,6 +7,7 @@
 namespace sas {
 
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+inline size_t cdiv(size_t a, int b) { return (a + (size_t)b - 1) / (size_t)b; }
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // ---- elementwise.hip -------------------------------------------------------
@@ -114,6 +115,27 @@ hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t s);
 // bias[b, g, t, k] = log_gate[b, g, t, sel[b, g, t, k]] (0 for empty slots)
 hipError_t launch_gather_gate(const int32_t* sel, const float* log_gate, int b, int n, int Hkv, int K, int NB,
                               float* bias, hipStream_t s);
+// Selector backward.  ds[r, m] for rows r = (b, g, t) and m < NB:
+// [m selected] dlog_gate[r, slot of m] - exp(log_gate[r, m]) sum_slots dlog_gate[r, .]
+// for m < t / B (the row's historical blocks), 0 otherwise.
+hipError_t launch_selector_ds(const int32_t* sel, const float* log_gate, const float* dlog_gate, int b, int n,
+                              int Hkv, int K, int B, float* ds, hipStream_t s);
+// C(z, split)[i, j] = alpha sum_{k in split} A(z)[i, k] B(z)[k, j] for z < Z: fp32
+// A, B in the activation dtype, fp32 C; strides in elements.  With splits > 1
+// each split writes its own partial at C + split * sCs.
+struct SmallGemm {
+  int M, N, K, Z, splits;
+  float alpha;
+  const float* A;
+  long long sAz, sAi, sAk;
+  const void* Bm;
+  long long sBz, sBk, sBj;
+  float* C;
+  long long sCz, sCs, sCi;
+};
+hipError_t launch_small_gemm(int dtype, const SmallGemm& g, hipStream_t s);
+// out[zo, e] = sum_{u < U} sum_{q < S} part[((u ZO + zo) S + q) E + e]
+hipError_t launch_partial_sum(const float* part, int U, int ZO, int S, size_t E, float* out, hipStream_t s);
 
 // ---- decode.hip ------------------------------------------------------------
 // rope[r, i] for the positions pos[r] of the new tokens (fp64 math).

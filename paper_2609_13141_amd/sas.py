@@ -20,11 +20,12 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsas.so")
 SAS_OK, SAS_ERR_INVALID_ARGUMENT, SAS_ERR_UNSUPPORTED, SAS_ERR_WORKSPACE, SAS_ERR_HIP = 0, -1, -2, -3, -4
 SAS_F32, SAS_BF16 = 0, 1
 MODES = {"dense": 0, "sparse": 1, "gated": 2}
-OP_ATTENTION, OP_MLP, OP_LAYER, OP_DECODE, OP_LM_HEAD, OP_DECODE_SELECT, OP_ATTENTION_BACKWARD = 0, 1, 2, 3, 4, 5, 6
+(OP_ATTENTION, OP_MLP, OP_LAYER, OP_DECODE, OP_LM_HEAD, OP_DECODE_SELECT, OP_ATTENTION_BACKWARD,
+ OP_SELECTOR_BACKWARD) = range(8)
 TORCH_DTYPE = {"bf16": torch.bfloat16, "f32": torch.float32}
 
 EXPORTS = ("sas_workspace_size", "sas_attention_prefill", "sas_mlp_forward", "sas_layer_forward",
-           "sas_decode_step", "sas_decode_select", "sas_attention_backward", "sas_embed", "sas_lm_head_argmax", "sas_last_error", "sas_version",
+           "sas_decode_step", "sas_decode_select", "sas_attention_backward", "sas_selector_backward", "sas_embed", "sas_lm_head_argmax", "sas_last_error", "sas_version",
            "sas_profiler_start", "sas_profiler_stop", "sas_profiler_record")
 
 
@@ -57,6 +58,14 @@ class BwdIn(C.Structure):
 
 class BwdOut(C.Structure):
     _fields_ = [(f, C.c_void_p) for f in ("dq", "dk", "dv", "dlog_gate")]
+
+
+class SelBwdIn(C.Structure):
+    _fields_ = [(f, C.c_void_p) for f in ("q", "k", "w_gq", "w_gk", "sel_idx", "log_gate", "dlog_gate")]
+
+
+class SelBwdOut(C.Structure):
+    _fields_ = [(f, C.c_void_p) for f in ("ds", "dqhat", "dkbar", "dw_gq", "dw_gk")]
 
 
 class LayerWeights(C.Structure):
@@ -215,6 +224,33 @@ def attention_backward(cfg: Config, q, k, v, o, d_o, lse, sel_idx=None, log_gate
     bo = BwdOut(*[_ptr(out.get(f)) for f in ("dq", "dk", "dv", "dlog_gate")])
     wsp, wsn = _ws(ws, workspace_size(cfg, OP_ATTENTION_BACKWARD, b, n))
     _check(lib().sas_attention_backward(C.byref(cfg), b, n, C.byref(bi), C.byref(bo), wsp, wsn, _stream()))
+    return out
+
+
+def selector_backward(cfg: Config, q, k, sel_idx, log_gate, dlog_gate, w_gq=None, w_gk=None, *, ds: bool = True,
+                      dqhat: bool = True, dkbar: bool = True, ws: Workspace | None = None) -> dict:
+    """Selector gradients from the selected blocks' log-gate gradient: ds
+    [b,Hkv,n,NB], dqhat [b,Hkv,n,dh], dkbar [b,Hkv,NB,dh] and, for given
+    projections, dw_gq / dw_gk [Hkv,dh,dh] (all fp32)."""
+    b, n, H, dh = q.shape
+    Hkv = cfg.n_kv_heads
+    NB = -(-n // cfg.block_size)
+    dev = q.device
+    out = {}
+    if ds:
+        out["ds"] = torch.empty(b, Hkv, n, NB, dtype=torch.float32, device=dev)
+    if dqhat:
+        out["dqhat"] = torch.empty(b, Hkv, n, dh, dtype=torch.float32, device=dev)
+    if dkbar:
+        out["dkbar"] = torch.empty(b, Hkv, NB, dh, dtype=torch.float32, device=dev)
+    if w_gq is not None:
+        out["dw_gq"] = torch.empty(Hkv, dh, dh, dtype=torch.float32, device=dev)
+    if w_gk is not None:
+        out["dw_gk"] = torch.empty(Hkv, dh, dh, dtype=torch.float32, device=dev)
+    si = SelBwdIn(*[_ptr(t) for t in (q, k, w_gq, w_gk, sel_idx, log_gate, dlog_gate)])
+    so = SelBwdOut(*[_ptr(out.get(f)) for f in ("ds", "dqhat", "dkbar", "dw_gq", "dw_gk")])
+    wsp, wsn = _ws(ws, workspace_size(cfg, OP_SELECTOR_BACKWARD, b, n))
+    _check(lib().sas_selector_backward(C.byref(cfg), b, n, C.byref(si), C.byref(so), wsp, wsn, _stream()))
     return out
 
 
