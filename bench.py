@@ -43,6 +43,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-step measurement")
     ap.add_argument("--no-long-decode", action="store_true", help="skip the 64K..512K-context decode sweep")
+    ap.add_argument("--no-backward", action="store_true", help="skip the training-step backward measurement")
     ap.add_argument("--cpu-threads", type=int, default=0, help="oracle BLAS threads (0: affinity, max 16)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain device copy of %d MiB (reference for HBM counters)" % (COPY_BYTES >> 20))
@@ -227,6 +228,9 @@ def main():
     if not args.no_long_decode:
         line["decode_long"] = decode_long_bench()
         torch.cuda.empty_cache()
+    if not args.no_backward:
+        line["backward"] = backward_bench()
+        torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, x_np, W_np, cores)
     print(json.dumps(line), flush=True)
@@ -359,6 +363,73 @@ def decode_long_bench(steps=10, warmup=3):
                         "summary_bytes": b * Hkv * (ctx // B) * dh * 2})
             del cache, ws
             torch.cuda.empty_cache()
+    return out
+
+
+def backward_bench(steps=10, warmup=3):
+    """The kernels of the method's training step (Alg. 1; App. E's
+    recomputation backward): the attention backward (dQ, dK, dV and the
+    selected blocks' log-gate gradient) and the selector backward (score,
+    gate-query and summary gradients), after one GATED forward of the same
+    inputs.  Q, K, V and dO are N(0,1) drawn on the GPU (seeded); timing
+    depends on the inputs only through which blocks are selected.
+    Algorithmic FLOPs of the attention backward: 10 dh per attended
+    (query, key) pair and head (QK^T and dO V^T recomputed, dQ, dK, dV)."""
+    import torch
+    from paper_2609_13141_amd import configs, sas
+    dev = "cuda:0"
+    out = []
+    for name in ("7b_layer_4k_b4", "gqa28x4_layer_16k"):
+        w = configs.BY_NAME[name]
+        g = torch.Generator(device=dev)
+        g.manual_seed(1000 + w.index)
+        b, n, H, Hkv, dh = w.batch, w.seq_len, w.n_heads, w.n_kv_heads, w.head_dim
+
+        def rnd(*shape):
+            return torch.randn(*shape, generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+        q, k, v, d_o = rnd(b, n, H, dh), rnd(b, n, Hkv, dh), rnd(b, n, Hkv, dh), rnd(b, n, H, dh)
+        cfg = sas.make_config(w)
+        ws_f, ws_b, ws_s = sas.Workspace(dev), sas.Workspace(dev), sas.Workspace(dev)
+        fw = sas.attention_prefill(cfg, q, k, v, log_gate=True, ws=ws_f)
+
+        def bwd():
+            ab = sas.attention_backward(cfg, q, k, v, fw["o"], d_o, fw["lse"], fw["sel_idx"], fw["log_gate"],
+                                        ws=ws_b)
+            sas.selector_backward(cfg, q, k, fw["sel_idx"], fw["log_gate"], ab["dlog_gate"], ws=ws_s)
+        for _ in range(warmup):
+            bwd()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            bwd()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / steps
+        sas.profiler_start(64 * steps + 64)
+        for _ in range(steps):
+            bwd()
+            sas.attention_prefill(cfg, q, k, v, log_gate=True, ws=ws_f)
+        recs = sas.profiler_stop()
+        fam = {}
+        for nm, t in recs:
+            fam.setdefault(nm, []).append(t)
+        kms = {kk: sum(vv) / len(vv) for kk, vv in fam.items()}
+        flops = 10.0 * dh * H * b * w.attended_pairs()
+        att_ms = kms["attention_bwd"]
+        tf = flops / (att_ms * 1e-3) / 1e12
+        sel_ms = sum(kms.get(kk, 0.0) for kk in ("sel_bwd_ds", "sel_bwd_gemm"))
+        out.append({"workload": f"{w.name}: batch {b}, {n} tokens, {H}/{Hkv} heads, dh {dh}, B={w.block_size}, "
+                                f"K={w.top_k}, GATED",
+                    "ms_per_backward": round(ms, 4),
+                    "attention_bwd_ms": round(att_ms, 4),
+                    "attention_bwd_gflop": round(flops / 1e9, 2),
+                    "attention_bwd_tflops": round(tf, 1),
+                    "mfma_frac": round(tf / BF16_PEAK_TFLOPS, 4),
+                    "attention_fwd_ms": round(kms["attention"], 4),
+                    "bwd_over_fwd": round(att_ms / kms["attention"], 2),
+                    "selector_bwd_ms": round(sel_ms, 4),
+                    "kernels_ms": {kk: round(vv, 4) for kk, vv in sorted(kms.items(), key=lambda kv: -kv[1])}})
+        del q, k, v, d_o, fw, ws_f, ws_b, ws_s
+        torch.cuda.empty_cache()
     return out
 
 

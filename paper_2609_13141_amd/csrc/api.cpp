@@ -426,6 +426,7 @@ struct BwdWs {
   float* delta;
   float* dlg_head;
   uint8_t* chunk_mask;
+  uint32_t* selmask;
   float* sel_bias;
 };
 
@@ -436,6 +437,7 @@ BwdWs carve_backward(Carve& cv, const sas_config* c, int b, int n) {
   w.delta = (float*)cv.take((size_t)b * H * n * 4);
   w.dlg_head = (float*)cv.take((size_t)b * H * n * K * 4);
   w.chunk_mask = (uint8_t*)cv.take(align_up((size_t)b * Hkv * nqc * NB, 4));
+  w.selmask = (uint32_t*)cv.take((size_t)b * Hkv * n * cdiv(NB, (size_t)32) * 4);
   w.sel_bias = (float*)cv.take((size_t)b * Hkv * n * K * 4);
   return w;
 }
@@ -607,6 +609,8 @@ sas_status sas_attention_backward(const sas_config* c, int32_t batch, int32_t se
   SAS_TRY(check_ptr(out->dk, "out.dk", true));
   SAS_TRY(check_ptr(out->dv, "out.dv", true));
   SAS_TRY(check_ptr(out->dlog_gate, "out.dlog_gate", false));
+  if (c->dtype == SAS_BF16 && seq_len > BWD_MAX_SEQ)
+    return fail(SAS_ERR_UNSUPPORTED, "seq_len %d (the bf16 backward supports <= %d)", seq_len, BWD_MAX_SEQ);
   Carve cv(ws);
   BwdWs bw = carve_backward(cv, c, batch, seq_len);
   SAS_TRY(check_ws(ws, ws_bytes, cv.off));
@@ -643,6 +647,8 @@ sas_status sas_attention_backward(const sas_config* c, int32_t batch, int32_t se
   a.delta = bw.delta;
   a.dlg_head = bw.dlg_head;
   a.chunk_mask = bw.chunk_mask;
+  a.selmask = bw.selmask;
+  a.log_gate = sparse && c->mode == SAS_MODE_GATED ? in->log_gate : nullptr;
   if (out->dlog_gate && (c->mode != SAS_MODE_GATED || K == 0)) {
     Timed tm("bwd_zero", s);
     HIP_TRY(launch_fill_f32(out->dlog_gate, (size_t)batch * c->n_kv_heads * seq_len * (K > 0 ? K : 0), 0.f, s),

@@ -185,32 +185,61 @@ __global__ void fill_f32_kernel(float* p, size_t n, float v) {
 // ---- bf16 path ------------------------------------------------------------------
 constexpr float BLOG2E = 1.4426950408889634f;
 
-// Pass 1 (dQ and the per-head block sums of ds): the forward kernel's
-// layout -- one workgroup = 4 waves = 128 queries of one (batch, head), each
-// lane owning one query of S^T = K Q^T (v_mfma_f32_32x32x16_bf16) -- with
-// dP^T = V dO^T computed the same way, dS^T = P^T (dP^T - Delta) formed in
-// registers and fed back as the B operand of dQ^T += K^T dS^T (K staged
-// transposed in LDS, read in the accumulator's key permutation).  Tiles no
-// query of the workgroup attends are skipped.
-template <int DH, bool SINGLE>
+__device__ __forceinline__ void bwd_barrier() {  // LDS writes/reads done, then s_barrier (no vmcnt drain)
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// next set bit at or after p in an LDS bitmask of `count` bits (count if none)
+__device__ __forceinline__ int next_set(const uint32_t* bits, int p, int count) {
+  while (p < count) {
+    const uint32_t w = bits[p >> 5] >> (p & 31);
+    if (w) return p + __builtin_ctz(w);
+    p = (p | 31) + 1;
+  }
+  return count;
+}
+
+// Pass 1 (dQ and the per-head block sums of ds): one workgroup = 4 waves =
+// 128 queries of one (batch, head), each lane owning one query of S^T = K Q^T
+// (v_mfma_f32_32x32x16_bf16), with dP^T = V dO^T computed the same way;
+// dS^T = P^T (dP^T - Delta) is formed in registers and fed back as the B
+// operand of dQ^T += K^T dS^T (K staged transposed in LDS, read in the
+// accumulator's key permutation).  The key tiles any query of the workgroup
+// attends are flagged in LDS first; each tile's K and V are loaded into
+// registers while the previous tile is multiplied.  Sub-blocks of
+// 2^LSB = min(B, 64) keys carry one bias per query; a sub-block of an
+// accumulator element is known at compile time (the lane-dependent part of
+// its key index is below 8).
+template <int DH, int LSB>
 __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
   constexpr int KP = DH + 8;
   constexpr int TP = 64 + 4;
-  constexpr int KPG = DH / 32;
+  constexpr int KPG = DH / 32;   // keys per thread in the tile staging
+  constexpr int C8 = DH / 8;
+  constexpr int NSUB = 64 >> LSB;
+  constexpr int KMAX = 32;
   __shared__ __align__(16) bf16_t Ks[64 * KP];
   __shared__ __align__(16) bf16_t Vs[64 * KP];
   __shared__ __align__(16) bf16_t Kt[DH * TP];
+  __shared__ int sel_s[128 * KMAX];
+  __shared__ float sbias_s[128 * KMAX];
+  __shared__ float dlg_s[128 * KMAX];
+  __shared__ uint32_t need[BWD_MAX_SEQ / 64 / 32];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lk = lane >> 5;
   const int qtile = gridDim.x - 1 - blockIdx.x;
   const int h = blockIdx.y, bi = blockIdx.z;
   const int G = P.H / P.Hkv, g = h / G;
-  const int n = P.n, B = P.B, Kn = P.K;
-  const int t = qtile * 128 + wave * 32 + lr;
+  const int n = P.n, B = P.B;
+  const int Kn = P.mode == SAS_MODE_DENSE ? 0 : P.K;
+  const int qrow = wave * 32 + lr;  // query row of this lane in the workgroup
+  const int t = qtile * 128 + qrow;
   const bool qvalid = t < n;
   const int beta = qvalid ? t / B : -1;
-  const int bshift = 31 - __clz(B < 64 ? B : 64);
+  const bool gated = P.mode == SAS_MODE_GATED;
+  const bool dense = P.mode == SAS_MODE_DENSE;
+  const int ntiles = (n + 63) / 64;
 
   bf16x8_t qb[DH / 16], dob[DH / 16];
   {
@@ -228,20 +257,29 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
   const size_t hrow = ((size_t)bi * P.H + h) * n + (qvalid ? t : 0);
   const float lse2 = qvalid ? P.lse[hrow] * BLOG2E : 0.f;
   const float delta = qvalid ? P.delta[hrow] : 0.f;
-  float* dlg = (P.dlg_head && qvalid) ? P.dlg_head + hrow * Kn : nullptr;
 
-  const int32_t* selp = nullptr;
-  const float* biasp = nullptr;
-  int cur = 0, next_sel = 0x7fffffff;
-  if (P.mode != SAS_MODE_DENSE && qvalid && Kn > 0) {
+  // selection rows of the workgroup's queries (lane pair lk = 0, 1 splits the slots)
+  for (int w = tid; w < (ntiles + 31) / 32; w += 256) need[w] = 0;
+  if (Kn > 0 && qvalid) {
     const size_t row = (((size_t)bi * P.Hkv + g) * n + t) * Kn;
-    selp = P.sel + row;
-    biasp = P.sel_bias + row;
-    const int s0 = selp[0];
-    next_sel = s0 >= 0 ? s0 : 0x7fffffff;
+    for (int k = lk; k < Kn; k += 2) {
+      sel_s[qrow * KMAX + k] = P.sel[row + k];
+      if (gated) sbias_s[qrow * KMAX + k] = P.sel_bias[row + k] * BLOG2E;
+      dlg_s[qrow * KMAX + k] = 0.f;
+    }
   }
-  const bool gated = P.mode == SAS_MODE_GATED;
-  const bool dense = P.mode == SAS_MODE_DENSE;
+  __syncthreads();
+  // key tiles this workgroup attends: every query's current block, its selected blocks
+  if (qvalid && lk == 0) {
+    const int a0 = dense ? 0 : beta * B;
+    for (int tl = a0 / 64; tl <= t / 64; ++tl) atomicOr(&need[tl >> 5], 1u << (tl & 31));
+    for (int k = 0; k < Kn; ++k) {
+      const int m = sel_s[qrow * KMAX + k];
+      if (m < 0 || m >= beta) break;  // slots are ascending historical blocks, -1 padded
+      for (int tl = (m * B) / 64; tl <= ((m + 1) * B - 1) / 64; ++tl) atomicOr(&need[tl >> 5], 1u << (tl & 31));
+    }
+  }
+  __syncthreads();
 
   floatx16_t dq[DH / 32];
 #pragma unroll
@@ -249,78 +287,79 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) dq[dt][v] = 0.f;
   const float qk_scale = P.sm_scale * BLOG2E;
-
-  const int t_hi = min(n, qtile * 128 + 128) - 1;
-  const int last_tile = t_hi / 64;
   const bf16_t* Kg = (const bf16_t*)P.Kt + (size_t)g * DH;
   const bf16_t* Vg = (const bf16_t*)P.V + (size_t)g * DH;
   const size_t kstride = (size_t)P.Hkv * DH;
   const size_t kbase = (size_t)bi * n;
+  const int c8 = tid % C8, kg = tid / C8;
+  uint4 rk[KPG], rv[KPG];
+  auto prefetch = [&](int kt) {
+#pragma unroll
+    for (int q = 0; q < KPG; ++q) {
+      const int key = kt * 64 + kg * KPG + q;
+      const size_t go = (kbase + key) * kstride + c8 * 8;
+      rk[q] = key < n ? *(const uint4*)(Kg + go) : make_uint4(0, 0, 0, 0);
+      rv[q] = key < n ? *(const uint4*)(Vg + go) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto commit = [&]() {
+#pragma unroll
+    for (int q = 0; q < KPG; ++q) {
+      *(uint4*)(Ks + (kg * KPG + q) * KP + c8 * 8) = rk[q];
+      *(uint4*)(Vs + (kg * KPG + q) * KP + c8 * 8) = rv[q];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int sh = (e & 1) * 16, wd = e >> 1;
+      bf16_t* dst = Kt + (c8 * 8 + e) * TP + kg * KPG;
+      uint32_t x[KPG];
+#pragma unroll
+      for (int q = 0; q < KPG; ++q) x[q] = (((const uint32_t*)&rk[q])[wd] >> sh) & 0xffffu;
+      if constexpr (KPG == 4) {
+        *(uint2*)dst = make_uint2(x[0] | (x[1] << 16), x[2] | (x[3] << 16));
+      } else {
+        *(uint32_t*)dst = x[0] | (x[1] << 16);
+      }
+    }
+  };
 
-  for (int kt = 0; kt <= last_tile; ++kt) {
+  int cur = 0;  // this query's next selection slot
+  int next_sel = 0x7fffffff;
+  if (Kn > 0 && qvalid) {
+    const int s0 = sel_s[qrow * KMAX];
+    next_sel = s0 >= 0 ? s0 : 0x7fffffff;
+  }
+  int kt = next_set(need, 0, ntiles);
+  if (kt < ntiles) prefetch(kt);
+  while (kt < ntiles) {
+    commit();
+    bwd_barrier();
+    const int nkt = next_set(need, kt + 1, ntiles);
+    if (nkt < ntiles) prefetch(nkt);
     const int k0 = kt * 64;
-    constexpr int NSUB = SINGLE ? 1 : 4;
-    float bsub[NSUB];
+
+    // this query's offset (log2-domain bias - LSE) per sub-block; -inf: not attended
+    float offs[NSUB];
     int slot[NSUB];
-    bool need = false;
 #pragma unroll
     for (int sb = 0; sb < NSUB; ++sb) {
-      bsub[sb] = -INFINITY;
+      offs[sb] = -INFINITY;
       slot[sb] = -1;
-      const int kstart = k0 + (sb << bshift);
-      if (!qvalid || kstart > t || (!SINGLE && (sb << bshift) >= 64)) continue;
+      const int kstart = k0 + (sb << LSB);
+      if (!qvalid || kstart > t) continue;
       const int m = kstart / B;
       if (m == beta || dense) {
-        bsub[sb] = 0.f;
+        offs[sb] = -lse2;
       } else if (m == next_sel) {
-        bsub[sb] = gated ? biasp[cur] * BLOG2E : 0.f;
+        offs[sb] = (gated ? sbias_s[qrow * KMAX + cur] : 0.f) - lse2;
         slot[sb] = cur;
-        if (kstart + (1 << bshift) >= (m + 1) * B) {
+        if (kstart + (1 << LSB) >= (m + 1) * B) {
           ++cur;
-          const int s1 = cur < Kn ? selp[cur] : -1;
+          const int s1 = cur < Kn ? sel_s[qrow * KMAX + cur] : -1;
           next_sel = s1 >= 0 ? s1 : 0x7fffffff;
         }
       }
-      need |= bsub[sb] != -INFINITY;
     }
-    if (!__syncthreads_or(need)) continue;
-
-    // stage K and V row-major and K transposed
-    {
-#pragma unroll
-      for (int i = 0; i < (64 * DH / 8) / 256; ++i) {
-        const int c = tid + i * 256;
-        const int kr = c / (DH / 8), c8 = c % (DH / 8);
-        const int key = k0 + kr;
-        const size_t go = (kbase + key) * kstride + c8 * 8;
-        uint4 ku = key < n ? *(const uint4*)(Kg + go) : make_uint4(0, 0, 0, 0);
-        uint4 vu = key < n ? *(const uint4*)(Vg + go) : make_uint4(0, 0, 0, 0);
-        *(uint4*)(Ks + kr * KP + c8 * 8) = ku;
-        *(uint4*)(Vs + kr * KP + c8 * 8) = vu;
-      }
-      const int c8 = tid % (DH / 8), kg = tid / (DH / 8);
-      uint32_t w[KPG][4];
-#pragma unroll
-      for (int q = 0; q < KPG; ++q) {
-        const int key = k0 + kg * KPG + q;
-        uint4 ku = key < n ? *(const uint4*)(Kg + (kbase + key) * kstride + c8 * 8) : make_uint4(0, 0, 0, 0);
-        w[q][0] = ku.x; w[q][1] = ku.y; w[q][2] = ku.z; w[q][3] = ku.w;
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int sh = (e & 1) * 16;
-        bf16_t* dst = Kt + (c8 * 8 + e) * TP + kg * KPG;
-        if constexpr (KPG == 4) {
-          uint2 pk;
-          pk.x = ((w[0][e >> 1] >> sh) & 0xffffu) | (((w[1][e >> 1] >> sh) & 0xffffu) << 16);
-          pk.y = ((w[2][e >> 1] >> sh) & 0xffffu) | (((w[3][e >> 1] >> sh) & 0xffffu) << 16);
-          *(uint2*)dst = pk;
-        } else {
-          *(uint32_t*)dst = ((w[0][e >> 1] >> sh) & 0xffffu) | (((w[1][e >> 1] >> sh) & 0xffffu) << 16);
-        }
-      }
-    }
-    __syncthreads();
 
     floatx16_t sc[2], dp[2];
 #pragma unroll
@@ -338,7 +377,7 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
         dp[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, dob[ks], dp[st], 0, 0, 0);
       }
     }
-    const int lim = t - k0;
+    const bool diag = k0 + 63 > qtile * 128;  // keys past some query of the workgroup: mask key > t
     float dsum[NSUB];
 #pragma unroll
     for (int sb = 0; sb < NSUB; ++sb) dsum[sb] = 0.f;
@@ -346,45 +385,29 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int kl = st * 32 + 8 * (v >> 2) + 4 * lk + (v & 3);
-        int sb = 0;
-        float bb;
-        if constexpr (SINGLE) {
-          bb = bsub[0];
-        } else {
-          sb = kl >> bshift;
-          bb = sb == 0 ? bsub[0] : sb == 1 ? bsub[1] : sb == 2 ? bsub[2] : bsub[3];
-        }
-        float ds = 0.f;
-        if (kl <= lim && bb != -INFINITY) {
-          const float p = __builtin_amdgcn_exp2f(sc[st][v] * qk_scale + bb - lse2);
-          ds = p * (dp[st][v] - delta);
-        }
+        const int klc = st * 32 + 8 * (v >> 2);  // key offset without the lane part (4 lk + v % 4 < 8)
+        const int sb = klc >> LSB;
+        float p = __builtin_amdgcn_exp2f(fmaf(sc[st][v], qk_scale, offs[sb]));
+        if (diag && k0 + klc + 4 * lk + (v & 3) > t) p = 0.f;
+        const float ds = p * (dp[st][v] - delta);
         sc[st][v] = ds;
-        if constexpr (SINGLE) dsum[0] += ds;
-        else {
-          if (sb == 0) dsum[0] += ds;
-          else if (sb == 1) dsum[1] += ds;
-          else if (sb == 2) dsum[2] += ds;
-          else dsum[3] += ds;
-        }
+        dsum[sb] += ds;
       }
-    if (dlg) {
 #pragma unroll
-      for (int sb = 0; sb < NSUB; ++sb) {
-        const float tot = dsum[sb] + __shfl_xor(dsum[sb], 32, 64);
-        if (slot[sb] >= 0 && lk == 0) dlg[slot[sb]] += tot;
-      }
+    for (int sb = 0; sb < NSUB; ++sb) {
+      const float tot = dsum[sb] + __shfl_xor(dsum[sb], 32, 64);
+      if (slot[sb] >= 0 && lk == 0) dlg_s[qrow * KMAX + slot[sb]] += tot;
     }
     // dQ^T += K^T dS^T, 16 keys per step in the accumulator's key permutation
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      bf16x8_t pb;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        bf16_t hb = f32_to_bf16(sc[ks >> 1][8 * (ks & 1) + e]);
-        pb[e] = *(__bf16*)&hb;
-      }
+      const int st = ks >> 1, v0 = 8 * (ks & 1);
+      uint4 su;
+      su.x = pack_bf16x2(sc[st][v0 + 0], sc[st][v0 + 1]);
+      su.y = pack_bf16x2(sc[st][v0 + 2], sc[st][v0 + 3]);
+      su.z = pack_bf16x2(sc[st][v0 + 4], sc[st][v0 + 5]);
+      su.w = pack_bf16x2(sc[st][v0 + 6], sc[st][v0 + 7]);
+      const bf16x8_t pb = *(const bf16x8_t*)&su;
 #pragma unroll
       for (int dt = 0; dt < DH / 32; ++dt) {
         const bf16_t* kr = Kt + (dt * 32 + lr) * TP + 16 * ks + 4 * lk;
@@ -394,9 +417,15 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
         dq[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(bf16x8_t*)&u, pb, dq[dt], 0, 0, 0);
       }
     }
+    bwd_barrier();
+    kt = nkt;
   }
 
   if (!qvalid) return;
+  if (P.dlg_head && lk == 0) {
+    float* dlg = P.dlg_head + hrow * P.K;
+    for (int k = 0; k < Kn; ++k) dlg[k] = dlg_s[qrow * KMAX + k];
+  }
   bf16_t* op = (bf16_t*)P.dQ + (((size_t)bi * n + t) * P.H + h) * DH;
   const float sm = P.sm_scale;
 #pragma unroll
@@ -404,10 +433,8 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
 #pragma unroll
     for (int v4 = 0; v4 < 4; ++v4) {
       const int d0 = dt * 32 + 8 * v4 + 4 * lk;
-      const uint32_t w0 = (uint32_t)f32_to_bf16(dq[dt][4 * v4 + 0] * sm) |
-                          ((uint32_t)f32_to_bf16(dq[dt][4 * v4 + 1] * sm) << 16);
-      const uint32_t w1 = (uint32_t)f32_to_bf16(dq[dt][4 * v4 + 2] * sm) |
-                          ((uint32_t)f32_to_bf16(dq[dt][4 * v4 + 3] * sm) << 16);
+      const uint32_t w0 = pack_bf16x2(dq[dt][4 * v4 + 0] * sm, dq[dt][4 * v4 + 1] * sm);
+      const uint32_t w1 = pack_bf16x2(dq[dt][4 * v4 + 2] * sm, dq[dt][4 * v4 + 3] * sm);
       *(uint2*)(op + d0) = make_uint2(w0, w1);
     }
 }
@@ -426,38 +453,75 @@ __global__ void bwd_chunk_mask_kernel(const int32_t* __restrict__ sel, int b, in
   mask[(bg * nqc + t / 32) * NB + m] = 1;
 }
 
-// Pass 2 (dK, dV): one workgroup of 2 waves per 64 keys of one (batch, KV
+// selection bitmask of each row: bit m of word m / 32 is set when block m is selected
+__global__ void bwd_selmask_kernel(const int32_t* __restrict__ sel, size_t rows, int K, int NW,
+                                   uint32_t* __restrict__ mask) {
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= rows * NW) return;
+  const size_t row = idx / NW;
+  const int w = (int)(idx % NW);
+  uint32_t bits = 0;
+  for (int k = 0; k < K; ++k) {
+    const int m = sel[row * K + k];
+    if (m >= 0 && (m >> 5) == w) bits |= 1u << (m & 31);
+  }
+  mask[idx] = bits;
+}
+
+// Pass 2 (dK, dV): one workgroup of 4 waves per 128 keys of one (batch, KV
 // group); each wave owns 32 keys, held in registers as the B operands of
 // S = Q K^T and dP = dO V^T over 32-query chunks (lane = key, 16 query rows).
-// For every chunk that attends the tile and every head of the group, the
-// chunk's Q and dO are staged in LDS both row-major (A of S and dP) and
-// transposed (A of dK^T += Q^T dS and dV^T += dO^T P, read in the
-// accumulator's query permutation); P and dS stay in registers.
+// The chunks that attend the tile (their queries reach into its blocks, or
+// select one) are flagged in LDS first.  Work items are (chunk, head of the
+// group); the Q and dO rows of the next item are loaded into registers while
+// the current one is multiplied, then written to LDS both row-major (A of S
+// and dP) and transposed (A of dK^T += Q^T dS and dV^T += dO^T P, read in the
+// accumulator's query permutation).  P and dS stay in registers.
 template <int DH>
-__global__ void __launch_bounds__(128) bwd_dkv_bf16_kernel(BwdArgs P) {
+__global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
+  constexpr int NTH = 256, KT = 128;
   constexpr int KP = DH + 8;
   constexpr int QP = 32 + 4;
-  constexpr int NTH = 128;
+  constexpr int C8 = DH / 8;      // 16-byte pieces of a row
+  constexpr int QPT = DH / 64;    // chunk rows staged per thread
   __shared__ __align__(16) bf16_t Qs[32 * KP];
   __shared__ __align__(16) bf16_t Ds[32 * KP];
   __shared__ __align__(16) bf16_t Qt[DH * QP];
   __shared__ __align__(16) bf16_t Dt[DH * QP];
-  __shared__ float lse_s[32], delta_s[32];
-  __shared__ float bias_s[32][4];
+  __shared__ __align__(16) float delta_s[32];
+  __shared__ __align__(16) float off_s[8][32];  // log2-domain bias - LSE per (sub-block, row); -inf: not attended
+  __shared__ uint32_t flags[BWD_MAX_SEQ / 32 / 32];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lk = lane >> 5;
-  const int ktile = blockIdx.x, g = blockIdx.y, bi = blockIdx.z;
+  const int k0 = blockIdx.x * KT, g = blockIdx.y, bi = blockIdx.z;
   const int n = P.n, B = P.B, H = P.H, G = H / P.Hkv;
-  const int k0 = ktile * 64;
   const int key = k0 + wave * 32 + lr;
   const bool kvalid = key < n;
   const int bshift = 31 - __clz(B < 64 ? B : 64);
-  const int nsb = 64 >> bshift;  // SAS blocks (or parts of one) in the tile
-  const int m_lo = k0 / B, m_hi = min(n - 1, k0 + 63) / B;
+  const int nsb = KT >> bshift;  // sub-blocks of min(B, 64) keys in the tile: 2, 4 or 8
+  const int m_lo = k0 / B, m_hi = min(n - 1, k0 + KT - 1) / B;
   const int NB = (n + B - 1) / B;
+  const int NW = (NB + 31) / 32;
   const int nqc = (n + 31) / 32;
-  const uint8_t* cmask = P.chunk_mask ? P.chunk_mask + ((size_t)bi * P.Hkv + g) * nqc * NB : nullptr;
+  const bool dense = P.mode == SAS_MODE_DENSE, gated = P.mode == SAS_MODE_GATED;
+  const bool use_mask = !dense && P.K > 0;
+  const size_t grow = ((size_t)bi * P.Hkv + g) * n;  // first row of (b, g) in [b, Hkv, n, ...]
+
+  // chunks attending the tile
+  const int qc0 = k0 / 32;
+  for (int w = tid; w < (nqc + 31) / 32; w += NTH) flags[w] = 0;
+  __syncthreads();
+  {
+    const uint8_t* cm = use_mask ? P.chunk_mask + ((size_t)bi * P.Hkv + g) * nqc * NB : nullptr;
+    for (int qc = qc0 + tid; qc < nqc; qc += NTH) {
+      bool any = dense || (qc * 32) / B <= m_hi;
+      if (!any && cm)
+        for (int m = m_lo; m <= m_hi; ++m) any |= cm[(size_t)qc * NB + m] != 0;
+      if (any) atomicOr(&flags[qc >> 5], 1u << (qc & 31));
+    }
+  }
+  __syncthreads();
 
   bf16x8_t kb[DH / 16], vb[DH / 16];
   {
@@ -479,128 +543,145 @@ __global__ void __launch_bounds__(128) bwd_dkv_bf16_kernel(BwdArgs P) {
       dv[dt][v] = 0.f;
     }
   const float qk_scale = P.sm_scale * BLOG2E;
-  const bool dense = P.mode == SAS_MODE_DENSE;
 
-  for (int qc = k0 / 32; qc < nqc; ++qc) {
-    const int q0 = qc * 32;
-    // does any query of the chunk attend a key of the tile?  (the chunk reaches
-    // into the tile's current blocks, or selects one of them; thread j checks
-    // block m_lo + j, at most 64 / B + 1 of them)
-    bool any = dense || (q0 / B <= m_hi);
-    if (!any && cmask && tid <= m_hi - m_lo) any = cmask[(size_t)qc * NB + m_lo + tid] != 0;
-    if (!__syncthreads_or(any)) continue;
-    for (int hg = 0; hg < G; ++hg) {
-      const int h = g * G + hg;
-      // stage the chunk: Q, dO row-major and transposed; LSE, Delta; block biases
-      for (int c = tid; c < 32 * (DH / 8); c += NTH) {
-        const int qr = c / (DH / 8), c8 = c % (DH / 8);
-        const int t = q0 + qr;
-        const size_t off = (((size_t)bi * n + t) * H + h) * DH + c8 * 8;
-        uint4 qu = t < n ? *(const uint4*)((const bf16_t*)P.Q + off) : make_uint4(0, 0, 0, 0);
-        uint4 du = t < n ? *(const uint4*)((const bf16_t*)P.dO + off) : make_uint4(0, 0, 0, 0);
-        *(uint4*)(Qs + qr * KP + c8 * 8) = qu;
-        *(uint4*)(Ds + qr * KP + c8 * 8) = du;
-      }
-      if (tid < (DH / 8) * 8) {
-        const int c8 = tid % (DH / 8), qg = tid / (DH / 8);  // 8 query groups of 4
-        uint32_t wq[4][4], wd[4][4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int t = q0 + qg * 4 + q;
-          const size_t off = (((size_t)bi * n + t) * H + h) * DH + c8 * 8;
-          uint4 qu = t < n ? *(const uint4*)((const bf16_t*)P.Q + off) : make_uint4(0, 0, 0, 0);
-          uint4 du = t < n ? *(const uint4*)((const bf16_t*)P.dO + off) : make_uint4(0, 0, 0, 0);
-          wq[q][0] = qu.x; wq[q][1] = qu.y; wq[q][2] = qu.z; wq[q][3] = qu.w;
-          wd[q][0] = du.x; wd[q][1] = du.y; wd[q][2] = du.z; wd[q][3] = du.w;
-        }
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int sh = (e & 1) * 16;
-          uint2 pq, pd;
-          pq.x = ((wq[0][e >> 1] >> sh) & 0xffffu) | (((wq[1][e >> 1] >> sh) & 0xffffu) << 16);
-          pq.y = ((wq[2][e >> 1] >> sh) & 0xffffu) | (((wq[3][e >> 1] >> sh) & 0xffffu) << 16);
-          pd.x = ((wd[0][e >> 1] >> sh) & 0xffffu) | (((wd[1][e >> 1] >> sh) & 0xffffu) << 16);
-          pd.y = ((wd[2][e >> 1] >> sh) & 0xffffu) | (((wd[3][e >> 1] >> sh) & 0xffffu) << 16);
-          *(uint2*)(Qt + (c8 * 8 + e) * QP + qg * 4) = pq;
-          *(uint2*)(Dt + (c8 * 8 + e) * QP + qg * 4) = pd;
-        }
-      }
-      if (tid < 32) {
-        const int t = q0 + tid;
-        const size_t hr = ((size_t)bi * H + h) * n + (t < n ? t : 0);
-        lse_s[tid] = t < n ? P.lse[hr] * BLOG2E : 0.f;
-        delta_s[tid] = t < n ? P.delta[hr] : 0.f;
-      }
-      for (int j = tid; j < 32 * 4; j += NTH) {
-        const int qr = j & 31, sb = j >> 5;
-        const int t = q0 + qr;
-        float bb = -INFINITY;
-        if (t < n && sb < nsb) {
-          const int kstart = k0 + (sb << bshift);
-          int slot;
-          if (kstart <= t) bb = block_bias(P, bi, g, t, kstart / B, slot);
-          if (bb != -INFINITY) bb *= BLOG2E;
-        }
-        bias_s[qr][sb] = bb;
-      }
-      __syncthreads();
+  // staging roles: rows qg * QPT + i, 16-byte piece c8; lse/delta row tid; bias (row, sub-block)
+  const int c8 = tid % C8, qg = tid / C8;
+  const int bq = tid & 31, bsb = tid >> 5;
+  uint4 rq[QPT], rd[QPT];
+  float r_lse = 0.f, r_delta = 0.f, r_lg = 0.f;
+  uint32_t r_mw = 0;
 
-      floatx16_t sc, dp;
+  auto prefetch = [&](int qc, int hg) {
+    const int q0 = qc * 32, h = g * G + hg;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        sc[v] = 0.f;
-        dp[v] = 0.f;
-      }
-#pragma unroll
-      for (int ks = 0; ks < DH / 16; ++ks) {
-        const bf16x8_t aq = *(const bf16x8_t*)(Qs + lr * KP + ks * 16 + lk * 8);
-        sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq, kb[ks], sc, 0, 0, 0);
-        const bf16x8_t ad = *(const bf16x8_t*)(Ds + lr * KP + ks * 16 + lk * 8);
-        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ad, vb[ks], dp, 0, 0, 0);
-      }
-      // lane: key column `key`; rows = queries q0 + 8 (v / 4) + 4 lk + v % 4
-      const int sbk = (wave * 32 + lr) >> bshift;
-      floatx16_t pp;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int qr = 8 * (v >> 2) + 4 * lk + (v & 3);
-        const int t = q0 + qr;
-        const float bb = bias_s[qr][sbk];
-        float p = 0.f, ds = 0.f;
-        if (kvalid && key <= t && bb != -INFINITY) {
-          p = __builtin_amdgcn_exp2f(sc[v] * qk_scale + bb - lse_s[qr]);
-          ds = p * (dp[v] - delta_s[qr]);
-        }
-        pp[v] = p;
-        sc[v] = ds;
-      }
-      // dV^T += dO^T P and dK^T += Q^T dS, 16 queries per step in the accumulator's query permutation
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        bf16x8_t pb, sb8;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          bf16_t hp = f32_to_bf16(pp[8 * ks + e]);
-          bf16_t hs = f32_to_bf16(sc[8 * ks + e]);
-          pb[e] = *(__bf16*)&hp;
-          sb8[e] = *(__bf16*)&hs;
-        }
-#pragma unroll
-        for (int dt = 0; dt < DH / 32; ++dt) {
-          const bf16_t* dr = Dt + (dt * 32 + lr) * QP + 16 * ks + 4 * lk;
-          const uint2 dlo = *(const uint2*)dr;
-          const uint2 dhi = *(const uint2*)(dr + 8);
-          uint4 du = make_uint4(dlo.x, dlo.y, dhi.x, dhi.y);
-          dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(bf16x8_t*)&du, pb, dv[dt], 0, 0, 0);
-          const bf16_t* qrp = Qt + (dt * 32 + lr) * QP + 16 * ks + 4 * lk;
-          const uint2 qlo = *(const uint2*)qrp;
-          const uint2 qhi = *(const uint2*)(qrp + 8);
-          uint4 qu = make_uint4(qlo.x, qlo.y, qhi.x, qhi.y);
-          dk[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(bf16x8_t*)&qu, sb8, dk[dt], 0, 0, 0);
-        }
-      }
-      __syncthreads();
+    for (int i = 0; i < QPT; ++i) {
+      const int t = q0 + qg * QPT + i;
+      const size_t off = (((size_t)bi * n + t) * H + h) * DH + c8 * 8;
+      rq[i] = t < n ? *(const uint4*)((const bf16_t*)P.Q + off) : make_uint4(0, 0, 0, 0);
+      rd[i] = t < n ? *(const uint4*)((const bf16_t*)P.dO + off) : make_uint4(0, 0, 0, 0);
     }
+    if (tid < 32) {
+      const int t = q0 + tid;
+      r_delta = t < n ? P.delta[((size_t)bi * H + h) * n + t] : 0.f;
+    }
+    if (bsb < nsb) {
+      const int t = q0 + bq, kstart = k0 + (bsb << bshift), m = kstart / B;
+      r_lse = t < n ? P.lse[((size_t)bi * H + h) * n + t] : 0.f;
+      if (t < n && kstart <= t && m != t / B) {
+        r_mw = use_mask ? P.selmask[(grow + t) * NW + (m >> 5)] : 0u;
+        r_lg = gated && use_mask ? P.log_gate[(grow + t) * NB + m] : 0.f;
+      }
+    }
+  };
+  auto commit = [&](int qc) {
+    const int q0 = qc * 32;
+#pragma unroll
+    for (int i = 0; i < QPT; ++i) {
+      *(uint4*)(Qs + (qg * QPT + i) * KP + c8 * 8) = rq[i];
+      *(uint4*)(Ds + (qg * QPT + i) * KP + c8 * 8) = rd[i];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int sh = (e & 1) * 16;
+      const int wd = e >> 1;
+      if constexpr (QPT == 2) {
+        const uint32_t pq = ((((const uint32_t*)&rq[0])[wd] >> sh) & 0xffffu) |
+                            (((((const uint32_t*)&rq[1])[wd] >> sh) & 0xffffu) << 16);
+        const uint32_t pd = ((((const uint32_t*)&rd[0])[wd] >> sh) & 0xffffu) |
+                            (((((const uint32_t*)&rd[1])[wd] >> sh) & 0xffffu) << 16);
+        *(uint32_t*)(Qt + (c8 * 8 + e) * QP + qg * 2) = pq;
+        *(uint32_t*)(Dt + (c8 * 8 + e) * QP + qg * 2) = pd;
+      } else {
+        Qt[(c8 * 8 + e) * QP + qg] = (bf16_t)((((const uint32_t*)&rq[0])[wd] >> sh) & 0xffffu);
+        Dt[(c8 * 8 + e) * QP + qg] = (bf16_t)((((const uint32_t*)&rd[0])[wd] >> sh) & 0xffffu);
+      }
+    }
+    if (tid < 32) delta_s[tid] = r_delta;
+    if (bsb < nsb) {
+      const int t = q0 + bq, kstart = k0 + (bsb << bshift), m = kstart / B;
+      float bb = -INFINITY;
+      if (t < n && kstart <= t) {
+        if (m == t / B || dense) bb = 0.f;
+        else if ((r_mw >> (m & 31)) & 1u) bb = gated ? r_lg * BLOG2E : 0.f;
+      }
+      off_s[bsb][bq] = bb - r_lse * BLOG2E;
+    }
+  };
+
+  int qc = next_set(flags, qc0, nqc), hg = 0;
+  if (qc < nqc) prefetch(qc, 0);
+  while (qc < nqc) {
+    commit(qc);
+    bwd_barrier();
+    int nq = qc, nh = hg + 1;
+    if (nh == G) {
+      nh = 0;
+      nq = next_set(flags, qc + 1, nqc);
+    }
+    if (nq < nqc) prefetch(nq, nh);
+    const int q0 = qc * 32;
+
+    floatx16_t sc, dp;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      sc[v] = 0.f;
+      dp[v] = 0.f;
+    }
+#pragma unroll
+    for (int ks = 0; ks < DH / 16; ++ks) {
+      const bf16x8_t aq = *(const bf16x8_t*)(Qs + lr * KP + ks * 16 + lk * 8);
+      sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq, kb[ks], sc, 0, 0, 0);
+      const bf16x8_t ad = *(const bf16x8_t*)(Ds + lr * KP + ks * 16 + lk * 8);
+      dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ad, vb[ks], dp, 0, 0, 0);
+    }
+    // lane: key column `key`; rows = queries q0 + 8 j + 4 lk + i (v = 4 j + i)
+    const int sbk = (wave * 32 + lr) >> bshift;
+    const bool diag = q0 < k0 + KT;  // the chunk meets the tile's diagonal: mask key > t
+    floatx16_t pp;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float4 of = *(const float4*)&off_s[sbk][8 * j + 4 * lk];
+      const float4 de = *(const float4*)&delta_s[8 * j + 4 * lk];
+      const float ofv[4] = {of.x, of.y, of.z, of.w}, dev[4] = {de.x, de.y, de.z, de.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int v = 4 * j + i;
+        float p = __builtin_amdgcn_exp2f(fmaf(sc[v], qk_scale, ofv[i]));
+        if (diag && key > q0 + 8 * j + 4 * lk + i) p = 0.f;
+        pp[v] = p;
+        sc[v] = p * (dp[v] - dev[i]);
+      }
+    }
+    // dV^T += dO^T P and dK^T += Q^T dS, 16 queries per step in the accumulator's query permutation
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      uint4 pu, su;
+      pu.x = pack_bf16x2(pp[8 * ks + 0], pp[8 * ks + 1]);
+      pu.y = pack_bf16x2(pp[8 * ks + 2], pp[8 * ks + 3]);
+      pu.z = pack_bf16x2(pp[8 * ks + 4], pp[8 * ks + 5]);
+      pu.w = pack_bf16x2(pp[8 * ks + 6], pp[8 * ks + 7]);
+      su.x = pack_bf16x2(sc[8 * ks + 0], sc[8 * ks + 1]);
+      su.y = pack_bf16x2(sc[8 * ks + 2], sc[8 * ks + 3]);
+      su.z = pack_bf16x2(sc[8 * ks + 4], sc[8 * ks + 5]);
+      su.w = pack_bf16x2(sc[8 * ks + 6], sc[8 * ks + 7]);
+      const bf16x8_t pb = *(const bf16x8_t*)&pu, sb8 = *(const bf16x8_t*)&su;
+#pragma unroll
+      for (int dt = 0; dt < DH / 32; ++dt) {
+        const bf16_t* dr = Dt + (dt * 32 + lr) * QP + 16 * ks + 4 * lk;
+        const uint2 dlo = *(const uint2*)dr;
+        const uint2 dhi = *(const uint2*)(dr + 8);
+        uint4 du = make_uint4(dlo.x, dlo.y, dhi.x, dhi.y);
+        dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(bf16x8_t*)&du, pb, dv[dt], 0, 0, 0);
+        const bf16_t* qrp = Qt + (dt * 32 + lr) * QP + 16 * ks + 4 * lk;
+        const uint2 qlo = *(const uint2*)qrp;
+        const uint2 qhi = *(const uint2*)(qrp + 8);
+        uint4 qu = make_uint4(qlo.x, qlo.y, qhi.x, qhi.y);
+        dk[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(bf16x8_t*)&qu, sb8, dk[dt], 0, 0, 0);
+      }
+    }
+    bwd_barrier();
+    qc = nq;
+    hg = nh;
   }
   if (!kvalid) return;
   const size_t off = (((size_t)bi * n + key) * P.Hkv + g) * DH;
@@ -612,37 +693,47 @@ __global__ void __launch_bounds__(128) bwd_dkv_bf16_kernel(BwdArgs P) {
 #pragma unroll
     for (int v4 = 0; v4 < 4; ++v4) {
       const int d0 = dt * 32 + 8 * v4 + 4 * lk;
-      uint32_t w0 = (uint32_t)f32_to_bf16(dk[dt][4 * v4 + 0] * sm) | ((uint32_t)f32_to_bf16(dk[dt][4 * v4 + 1] * sm) << 16);
-      uint32_t w1 = (uint32_t)f32_to_bf16(dk[dt][4 * v4 + 2] * sm) | ((uint32_t)f32_to_bf16(dk[dt][4 * v4 + 3] * sm) << 16);
+      uint32_t w0 = pack_bf16x2(dk[dt][4 * v4 + 0] * sm, dk[dt][4 * v4 + 1] * sm);
+      uint32_t w1 = pack_bf16x2(dk[dt][4 * v4 + 2] * sm, dk[dt][4 * v4 + 3] * sm);
       *(uint2*)(dkp + d0) = make_uint2(w0, w1);
-      w0 = (uint32_t)f32_to_bf16(dv[dt][4 * v4 + 0]) | ((uint32_t)f32_to_bf16(dv[dt][4 * v4 + 1]) << 16);
-      w1 = (uint32_t)f32_to_bf16(dv[dt][4 * v4 + 2]) | ((uint32_t)f32_to_bf16(dv[dt][4 * v4 + 3]) << 16);
+      w0 = pack_bf16x2(dv[dt][4 * v4 + 0], dv[dt][4 * v4 + 1]);
+      w1 = pack_bf16x2(dv[dt][4 * v4 + 2], dv[dt][4 * v4 + 3]);
       *(uint2*)(dvp + d0) = make_uint2(w0, w1);
     }
 }
 
 static hipError_t launch_attention_backward_bf16(const BwdArgs& P, hipStream_t s) {
+  if (P.n > BWD_MAX_SEQ) return hipErrorInvalidValue;
   const int NB = cdiv(P.n, P.B), nqc = cdiv(P.n, 32);
   BwdArgs Q = P;
-  if (P.mode == SAS_MODE_DENSE || P.K <= 0) Q.chunk_mask = nullptr;  // no selected blocks to mark
-  if (Q.chunk_mask) {
+  const bool marks = P.mode != SAS_MODE_DENSE && P.K > 0;  // selected blocks to mark
+  if (!marks) {
+    Q.chunk_mask = nullptr;
+    Q.selmask = nullptr;
+  } else {
     const size_t bytes = (size_t)P.b * P.Hkv * nqc * NB;
     fill_f32_kernel<<<(unsigned)cdiv(cdiv(bytes, 4), 256), 256, 0, s>>>((float*)P.chunk_mask, cdiv(bytes, 4), 0.f);
     const size_t tot = (size_t)P.b * P.Hkv * P.n * P.K;
     bwd_chunk_mask_kernel<<<(unsigned)cdiv(tot, 256), 256, 0, s>>>(P.sel, P.b, P.n, P.Hkv, P.K, NB, P.chunk_mask);
+    const size_t rows = (size_t)P.b * P.Hkv * P.n;
+    const int NW = cdiv(NB, 32);
+    bwd_selmask_kernel<<<(unsigned)cdiv(rows * NW, 256), 256, 0, s>>>(P.sel, rows, P.K, NW, P.selmask);
   }
+  if (P.K > 32) return hipErrorInvalidValue;
   dim3 g1(cdiv(P.n, 128), P.H, P.b);
-  const bool single = P.B >= 64;
+  const int lsb = P.B >= 64 ? 6 : (P.B == 32 ? 5 : 4);
   if (P.dh == 128) {
-    if (single) bwd_dq_bf16_kernel<128, true><<<g1, 256, 0, s>>>(P);
-    else bwd_dq_bf16_kernel<128, false><<<g1, 256, 0, s>>>(P);
+    if (lsb == 6) bwd_dq_bf16_kernel<128, 6><<<g1, 256, 0, s>>>(Q);
+    else if (lsb == 5) bwd_dq_bf16_kernel<128, 5><<<g1, 256, 0, s>>>(Q);
+    else bwd_dq_bf16_kernel<128, 4><<<g1, 256, 0, s>>>(Q);
   } else {
-    if (single) bwd_dq_bf16_kernel<64, true><<<g1, 256, 0, s>>>(P);
-    else bwd_dq_bf16_kernel<64, false><<<g1, 256, 0, s>>>(P);
+    if (lsb == 6) bwd_dq_bf16_kernel<64, 6><<<g1, 256, 0, s>>>(Q);
+    else if (lsb == 5) bwd_dq_bf16_kernel<64, 5><<<g1, 256, 0, s>>>(Q);
+    else bwd_dq_bf16_kernel<64, 4><<<g1, 256, 0, s>>>(Q);
   }
-  dim3 g2(cdiv(P.n, 64), P.Hkv, P.b);
-  if (P.dh == 128) bwd_dkv_bf16_kernel<128><<<g2, 128, 0, s>>>(Q);
-  else bwd_dkv_bf16_kernel<64><<<g2, 128, 0, s>>>(Q);
+  dim3 g2(cdiv(P.n, 128), P.Hkv, P.b);
+  if (P.dh == 128) bwd_dkv_bf16_kernel<128><<<g2, 256, 0, s>>>(Q);
+  else bwd_dkv_bf16_kernel<64><<<g2, 256, 0, s>>>(Q);
   return hipGetLastError();
 }
 

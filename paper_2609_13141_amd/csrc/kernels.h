@@ -107,8 +107,12 @@ struct BwdArgs {
   // scratch
   float* delta;           // [b, H, n]
   float* dlg_head;        // [b, H, n, K]
+  const float* log_gate;  // [b, Hkv, n, ceil(n/B)] (GATED)
   uint8_t* chunk_mask;    // [b, Hkv, ceil(n/32), ceil(n/B)] (bf16 path)
+  uint32_t* selmask;      // [b, Hkv, n, ceil(ceil(n/B)/32)] bit m: block m selected (bf16 path)
 };
+// longest sequence of the bf16 attention backward (query chunks of 32 tracked in LDS)
+constexpr int BWD_MAX_SEQ = 262144;
 hipError_t launch_attention_backward(int dtype, const BwdArgs& a, hipStream_t s);
 // p[0..n) = v with a kernel (capturable in a graph, unlike a memset node)
 hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t s);
