@@ -27,6 +27,11 @@ Parity status of each part (how it is pinned by the oracle self-tests):
 * attention backward, gate backward, selector backward: pinned against
   torch autograd on a dense masked formulation and by central finite
   differences of the fp64 forward.
+* gating formulations of Table 1 (inner/outer gate, softmax/sigmoid/raw
+  activation, sparse/full scope, straight-through hard gate, score noise):
+  pinned against torch autograd on dense masked formulations (the hard gate
+  in its multiplicative form with zero gates), torch's log_softmax and
+  logsigmoid, Top-K ordering properties and reductions to the plain modes.
 * normalized log gate, Top-K, attention: pinned by closed forms (q = 0),
   V = const, reductions to textbook causal / block-local attention computed
   by torch's scaled_dot_product_attention, causality, shift invariance and
@@ -37,6 +42,8 @@ from .selector import (block_summaries, gate_query, selector_scores,
                        normalized_log_gate, topk_blocks, select)
 from .attention import sas_attention
 from .backward import sas_attention_backward, gate_backward, selector_backward
+from .variants import (log_gates, select_variant, variant_attention, variant_attention_backward,
+                       gate_backward_act)
 from .layer import (Spec, layer_forward, mlp_forward, attention_prefill,
                     DecodeCache, decode_step, decode_select, embed_tokens, lm_head_argmax)
 
@@ -47,4 +54,6 @@ __all__ = [
     "mlp_forward", "attention_prefill", "DecodeCache", "decode_step",
     "decode_select", "embed_tokens", "lm_head_argmax",
     "sas_attention_backward", "gate_backward", "selector_backward",
+    "log_gates", "select_variant", "variant_attention", "variant_attention_backward",
+    "gate_backward_act",
 ]
