@@ -62,6 +62,28 @@ typedef enum { SAS_F32 = 0, SAS_BF16 = 1 } sas_dtype;
  *          bias log g_m, the current block carries 0 (Eq. ours_train). */
 typedef enum { SAS_MODE_DENSE = 0, SAS_MODE_SPARSE = 1, SAS_MODE_GATED = 2 } sas_mode;
 
+/* Gating formulations of the training ablation (Sec. 4.1, Table 1); they
+ * apply to GATED mode only and default to SAS's choices (all zero).
+ *  gate_pos:  INNER adds log g_m to the logits (Eq. ours_train); OUTER keeps
+ *             the logits unbiased and weights the values of block m by g_m,
+ *             o = sum_i p_i g_b(i) v_i.
+ *  gate_act:  log g_m = s_m - LSE over the historical blocks (SOFTMAX,
+ *             Eq. normalized_log_gate), log sigmoid(s_m) (SIGMOID) or s_m
+ *             itself added to the logits (RAW).
+ *  scope:     SPARSE attends the current block and the Top-K blocks; FULL
+ *             attends every earlier token, each historical block with its gate.
+ *  gate_ste:  1 = straight-through hard gate: the forward attends the current
+ *             block and the Top-K blocks with unit gates; the backward passes
+ *             the hard gate's gradient to the soft gate (for a block outside
+ *             the Top-K, the limit of the inner-gate gradient at g -> 0,
+ *             App. D.2), to the Top-K blocks (scope SPARSE) or to every
+ *             historical block (scope FULL).
+ * OUTER supports SOFTMAX and SIGMOID and no straight-through gate (RAW
+ * defines no gate value); other combinations return SAS_ERR_UNSUPPORTED. */
+typedef enum { SAS_GATE_INNER = 0, SAS_GATE_OUTER = 1 } sas_gate_pos;
+typedef enum { SAS_ACT_SOFTMAX = 0, SAS_ACT_SIGMOID = 1, SAS_ACT_RAW = 2 } sas_gate_act;
+typedef enum { SAS_SCOPE_SPARSE = 0, SAS_SCOPE_FULL = 1 } sas_scope;
+
 /* Operation codes for sas_workspace_size. */
 typedef enum {
   SAS_OP_ATTENTION = 0, /* sas_attention_prefill: batch, seq_len */
@@ -87,30 +109,41 @@ typedef struct {
   float sm_scale;      /* attention scale; <= 0 selects 1/sqrt(head_dim) */
   int32_t dtype;       /* sas_dtype */
   int32_t mode;        /* sas_mode (prefill only; decode always uses SPARSE) */
+  int32_t gate_pos;    /* sas_gate_pos (GATED only) */
+  int32_t gate_act;    /* sas_gate_act (GATED only) */
+  int32_t scope;       /* sas_scope (GATED only) */
+  int32_t gate_ste;    /* 0 or 1 (GATED only) */
 } sas_config;
 
 /* Attention inputs (post-RoPE), the paper's problem statement (Alg. 1/2):
  * q [b, n, H, dh], k and v [b, n, Hkv, dh]; optional selector projections
- * w_gq, w_gk [Hkv, dh, dh] ([out, in] per group; NULL = identity). */
+ * w_gq, w_gk [Hkv, dh, dh] ([out, in] per group; NULL = identity);
+ * score_noise [b, Hkv, n, ceil(n/B)] fp32 or NULL: added to the selector
+ * scores s before the gate activation and before Top-K (the noisy "full*"
+ * scope of Table 1); with noise the Top-K ranks s + noise (s evaluated in
+ * fp64 as r / (G sqrt(dh))), without it the raw scores r. */
 typedef struct {
   const void* q;
   const void* k;
   const void* v;
   const void* w_gq;
   const void* w_gk;
+  const float* score_noise;
 } sas_attn_in;
 
 /* Attention outputs.  NB = ceil(n / B).
  *  o         [b, n, H, dh]   attention output (activation dtype)
- *  lse       [b, H, n]       fp32 natural-log sum of exp of the biased,
- *                            scaled logits over the attended set (optional)
+ *  lse       [b, H, n]       fp32 natural-log sum of exp of the scaled
+ *                            logits (with the inner gate's bias) over the
+ *                            attended set (optional)
  *  k_summary [b, Hkv, NB, dh] selector key summary of every complete block
  *                            (after w_gk); incomplete-block rows are zero
  *                            (optional)
  *  sel_idx   [b, Hkv, n, K]  int32 kept historical blocks, ascending, -1
  *                            padded (optional)
  *  log_gate  [b, Hkv, n, NB] fp32 log g of every historical block of every
- *                            query, -inf where m >= floor(t / B) (optional)
+ *                            query (per cfg->gate_act), -inf where
+ *                            m >= floor(t / B) (optional)
  *  tau       [b, Hkv, n]     fp32 log gate of the lowest-ranked kept block
  *                            when floor(t/B) > K >= 1, +inf when K = 0 <
  *                            floor(t/B), -inf otherwise (optional)
@@ -185,7 +218,8 @@ sas_status sas_attention_prefill(const sas_config* cfg, int32_t batch, int32_t s
  *  output), d_o [b,n,H,dh] the upstream gradient (activation dtype);
  *  lse [b,H,n] fp32 (the forward's LSE); sel_idx [b,Hkv,n,K] and, in GATED
  *  mode, log_gate [b,Hkv,n,ceil(n/B)] fp32 (the forward's selection and
- *  normalized log gates; unused in DENSE mode). */
+ *  log gates; unused in DENSE mode).  cfg must be the forward's, gating
+ *  fields included. */
 typedef struct {
   const void* q;
   const void* k;
@@ -200,12 +234,18 @@ typedef struct {
 /* Outputs of sas_attention_backward: dq [b,n,H,dh], dk, dv [b,n,Hkv,dh]
  * (activation dtype), dlog_gate [b,Hkv,n,K] fp32 or NULL: the gradient of
  * each selected block's log gate (GATED), summed over the group's heads, at
- * the slots of sel_idx (0 in empty slots). */
+ * the slots of sel_idx (0 in empty slots; scope SPARSE only);
+ * dlog_gate_full [b,Hkv,n,ceil(n/B)] fp32 or NULL: the same gradient for
+ * every block (0 where a block receives none), required in GATED mode with
+ * scope FULL or the straight-through gate.  With the straight-through gate
+ * the value is g_m times the gradient of the hard gate (the gradient of log g
+ * under the straight-through rule). */
 typedef struct {
   void* dq;
   void* dk;
   void* dv;
   float* dlog_gate;
+  float* dlog_gate_full;
 } sas_bwd_out;
 
 /* Backward of the attention of sas_attention_prefill (Sec. 4.3, Eq.
@@ -226,7 +266,9 @@ sas_status sas_attention_backward(const sas_config* cfg, int32_t batch, int32_t 
  * forward); sel_idx [b,Hkv,n,K] and log_gate [b,Hkv,n,ceil(n/B)] fp32 (the
  * forward's selection and normalized log gates); dlog_gate [b,Hkv,n,K] fp32
  * (sas_attention_backward's output, or any gradient of the selected blocks'
- * log gates at the slots of sel_idx). */
+ * log gates at the slots of sel_idx); dlog_gate_full [b,Hkv,n,ceil(n/B)]
+ * fp32 or NULL: when given, the gradient of every block's log gate, used
+ * instead of sel_idx and dlog_gate (scope FULL, straight-through gate). */
 typedef struct {
   const void* q;
   const void* k;
@@ -235,6 +277,7 @@ typedef struct {
   const int32_t* sel_idx;
   const float* log_gate;
   const float* dlog_gate;
+  const float* dlog_gate_full;
 } sas_sel_bwd_in;
 
 /* Outputs of sas_selector_backward, all fp32, each optional except as noted:
@@ -254,14 +297,17 @@ typedef struct {
 } sas_sel_bwd_out;
 
 /* Backward of the selector (Alg. 1's update of the selector parameters):
- * dlog g -> ds through the normalized log gate of Eq. normalized_log_gate
- * (ds_m = dlog g_m - g_m sum over the row's historical blocks of dlog g, the
- * softmax backward of App. D.3 with dlog g = 0 off the selected set), then
+ * dlog g -> ds through the gate activation: for SOFTMAX, Eq.
+ * normalized_log_gate's ds_m = dlog g_m - g_m sum over the row's historical
+ * blocks of dlog g (the softmax backward of App. D.3); for SIGMOID
+ * ds_m = dlog g_m (1 - g_m); for RAW ds_m = dlog g_m; then
  * through the scores s = qhat.kbar / (G sqrt(dh)) to the gate queries and
  * summaries and, when given, to W_gq and W_gk.  The Top-K set is piecewise
  * constant and passes no gradient; the roundings of the forward are taken
  * as identities.  Gate queries and summaries are recomputed from q and k.
- * With top_k = 0 every output is zero.  ws: sas_workspace_size(cfg,
+ * With top_k = 0 and no dlog_gate_full every output is zero.  Score noise
+ * (sas_attn_in.score_noise) is additive and needs no input here: log_gate
+ * already holds the noisy gates.  ws: sas_workspace_size(cfg,
  * SAS_OP_SELECTOR_BACKWARD, batch, seq_len). */
 sas_status sas_selector_backward(const sas_config* cfg, int32_t batch, int32_t seq_len,
                                  const sas_sel_bwd_in* in, sas_sel_bwd_out* out,

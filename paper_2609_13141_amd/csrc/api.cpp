@@ -103,6 +103,14 @@ sas_status check_config(const sas_config* c, bool need_mlp) {
     return fail(SAS_ERR_UNSUPPORTED, "block_size %d (supported: 16, 32, 64, 128)", c->block_size);
   if (c->top_k < 0) return fail(SAS_ERR_INVALID_ARGUMENT, "top_k %d is negative", c->top_k);
   if (c->top_k > 32) return fail(SAS_ERR_UNSUPPORTED, "top_k %d (supported: 0..32)", c->top_k);
+  if (c->gate_pos < SAS_GATE_INNER || c->gate_pos > SAS_GATE_OUTER || c->gate_act < SAS_ACT_SOFTMAX ||
+      c->gate_act > SAS_ACT_RAW || c->scope < SAS_SCOPE_SPARSE || c->scope > SAS_SCOPE_FULL || c->gate_ste < 0 ||
+      c->gate_ste > 1)
+    return fail(SAS_ERR_INVALID_ARGUMENT, "gating fields out of range (pos %d, act %d, scope %d, ste %d)",
+                c->gate_pos, c->gate_act, c->scope, c->gate_ste);
+  if (c->mode == SAS_MODE_GATED && c->gate_pos == SAS_GATE_OUTER && (c->gate_act == SAS_ACT_RAW || c->gate_ste))
+    return fail(SAS_ERR_UNSUPPORTED, "the outer gate supports the softmax and sigmoid activations without the "
+                                     "straight-through gate");
   if (need_mlp) {
     if (c->d_model <= 0 || c->d_ff <= 0)
       return fail(SAS_ERR_INVALID_ARGUMENT, "d_model %d and d_ff %d must be positive", c->d_model, c->d_ff);
@@ -117,6 +125,12 @@ sas_status check_config(const sas_config* c, bool need_mlp) {
 float sm_scale_of(const sas_config* c) {
   return c->sm_scale > 0.f ? c->sm_scale : 1.0f / sqrtf((float)c->head_dim);
 }
+
+bool gated_of(const sas_config* c) { return c->mode == SAS_MODE_GATED; }
+// the forward attends every historical block with its gate (needs the log-gate table)
+bool full_fwd(const sas_config* c) { return gated_of(c) && c->scope == SAS_SCOPE_FULL && !c->gate_ste; }
+// the backward produces a gradient for every historical block
+bool full_grad(const sas_config* c) { return gated_of(c) && c->scope == SAS_SCOPE_FULL; }
 
 // Bump allocator over the caller's workspace (offsets aligned to 256 bytes).
 struct Carve {
@@ -137,6 +151,7 @@ struct AttnWs {
   void* qhat;
   int32_t* sel;
   float* sel_bias;
+  float* gate_table;  // log gates of every block (full scope, when the caller does not ask for them)
 };
 
 AttnWs carve_attention(Carve& cv, const sas_config* c, int b, int n) {
@@ -152,6 +167,7 @@ AttnWs carve_attention(Carve& cv, const sas_config* c, int b, int n) {
   w.qhat = cv.take(qb);
   w.sel = (int32_t*)cv.take(rows * 4);
   w.sel_bias = (float*)cv.take(rows * 4);
+  w.gate_table = full_fwd(c) ? (float*)cv.take((size_t)b * c->n_kv_heads * n * NB * 4) : nullptr;
   return w;
 }
 
@@ -203,10 +219,11 @@ LayerWs carve_layer(Carve& cv, const sas_config* c, int b, int n) {
 sas_status run_attention(const sas_config* c, int b, int n, const void* q, const void* k, const void* v,
                          const void* w_gq, const void* w_gk, void* o, float* lse, void* k_summary,
                          int32_t* sel_idx, float* log_gate, float* tau, const AttnWs& ws,
-                         hipStream_t s, bool need_summary = false) {
+                         hipStream_t s, bool need_summary = false, const float* noise = nullptr) {
   const int NB = cdiv(n, c->block_size);
   const int H = c->n_heads, Hkv = c->n_kv_heads, dh = c->head_dim;
   const bool need_sel = c->mode != SAS_MODE_DENSE || sel_idx || log_gate || tau || k_summary || need_summary;
+  if (full_fwd(c) && !log_gate) log_gate = ws.gate_table;
   void* ksum = k_summary ? k_summary : ws.ksum;
   int32_t* sel = sel_idx ? sel_idx : ws.sel;
   if (need_sel) {
@@ -235,6 +252,8 @@ sas_status run_attention(const sas_config* c, int b, int n, const void* q, const
     sa.sel_bias = ws.sel_bias;
     sa.log_gate = log_gate;
     sa.tau = tau;
+    sa.noise = noise;
+    sa.act = gated_of(c) ? c->gate_act : SAS_ACT_SOFTMAX;
     {
       Timed tm("select", s);
       HIP_TRY(launch_select(c->dtype, sa, s), "select");
@@ -248,7 +267,8 @@ sas_status run_attention(const sas_config* c, int b, int n, const void* q, const
   aa.dh = dh;
   aa.B = c->block_size;
   aa.K = c->top_k;
-  aa.mode = c->mode;
+  // the straight-through gate's forward attends the Top-K blocks with unit gates
+  aa.mode = gated_of(c) && c->gate_ste ? SAS_MODE_SPARSE : c->mode;
   aa.sm_scale = sm_scale_of(c);
   aa.Q = q;
   aa.Kt = k;
@@ -257,6 +277,9 @@ sas_status run_attention(const sas_config* c, int b, int n, const void* q, const
   aa.sel_bias = ws.sel_bias;
   aa.O = o;
   aa.lse = lse;
+  aa.outer = gated_of(c) && c->gate_pos == SAS_GATE_OUTER;
+  aa.full = full_fwd(c);
+  aa.gate_table = log_gate;
   {
     Timed tm("attention", s);
     HIP_TRY(launch_attention(c->dtype, aa, s), "attention");
@@ -428,6 +451,8 @@ struct BwdWs {
   uint8_t* chunk_mask;
   uint32_t* selmask;
   float* sel_bias;
+  float* dlg_head_full;  // [b, H, n, NB] (full scope)
+  float* dlg_slots;      // [b, Hkv, n, K] per-slot gradient when only the table is asked for
 };
 
 BwdWs carve_backward(Carve& cv, const sas_config* c, int b, int n) {
@@ -439,6 +464,8 @@ BwdWs carve_backward(Carve& cv, const sas_config* c, int b, int n) {
   w.chunk_mask = (uint8_t*)cv.take(align_up((size_t)b * Hkv * nqc * NB, 4));
   w.selmask = (uint32_t*)cv.take((size_t)b * Hkv * n * cdiv(NB, (size_t)32) * 4);
   w.sel_bias = (float*)cv.take((size_t)b * Hkv * n * K * 4);
+  w.dlg_head_full = full_grad(c) ? (float*)cv.take((size_t)b * H * n * NB * 4) : nullptr;
+  w.dlg_slots = (float*)cv.take((size_t)b * Hkv * n * K * 4);
   return w;
 }
 
@@ -596,40 +623,50 @@ sas_status sas_attention_backward(const sas_config* c, int32_t batch, int32_t se
   if (batch <= 0 || seq_len <= 0)
     return fail(SAS_ERR_INVALID_ARGUMENT, "batch %d and seq_len %d must be positive", batch, seq_len);
   if (!in || !out) return fail(SAS_ERR_INVALID_ARGUMENT, "in/out is NULL");
+  const bool gated = gated_of(c), fullf = full_fwd(c), fullg = full_grad(c);
+  const int K = c->top_k > 0 ? c->top_k : 0;
+  // the walk over selected blocks: SPARSE, GATED with the sparse scope, and the straight-through gate
+  const bool walk = c->mode != SAS_MODE_DENSE && K > 0 && !fullf;
   SAS_TRY(check_ptr(in->q, "in.q", true));
   SAS_TRY(check_ptr(in->k, "in.k", true));
   SAS_TRY(check_ptr(in->v, "in.v", true));
   SAS_TRY(check_ptr(in->o, "in.o", true));
   SAS_TRY(check_ptr(in->d_o, "in.d_o", true));
   SAS_TRY(check_ptr(in->lse, "in.lse", true));
-  const bool sparse = c->mode != SAS_MODE_DENSE && c->top_k > 0;
-  SAS_TRY(check_ptr(in->sel_idx, "in.sel_idx", sparse));
-  SAS_TRY(check_ptr(in->log_gate, "in.log_gate", sparse && c->mode == SAS_MODE_GATED));
+  SAS_TRY(check_ptr(in->sel_idx, "in.sel_idx", walk));
+  SAS_TRY(check_ptr(in->log_gate, "in.log_gate", gated && (walk || fullg)));
   SAS_TRY(check_ptr(out->dq, "out.dq", true));
   SAS_TRY(check_ptr(out->dk, "out.dk", true));
   SAS_TRY(check_ptr(out->dv, "out.dv", true));
   SAS_TRY(check_ptr(out->dlog_gate, "out.dlog_gate", false));
+  SAS_TRY(check_ptr(out->dlog_gate_full, "out.dlog_gate_full", fullg));
+  if (fullg && out->dlog_gate)
+    return fail(SAS_ERR_INVALID_ARGUMENT, "scope FULL has no per-slot gradient: pass dlog_gate_full only");
   if (c->dtype == SAS_BF16 && seq_len > BWD_MAX_SEQ)
     return fail(SAS_ERR_UNSUPPORTED, "seq_len %d (the bf16 backward supports <= %d)", seq_len, BWD_MAX_SEQ);
   Carve cv(ws);
   BwdWs bw = carve_backward(cv, c, batch, seq_len);
   SAS_TRY(check_ws(ws, ws_bytes, cv.off));
   hipStream_t s = (hipStream_t)stream;
-  const int K = c->top_k > 0 ? c->top_k : 0;
+  const int Hkv = c->n_kv_heads;
   const int NB = (int)cdiv(seq_len, c->block_size);
-  if (sparse && c->mode == SAS_MODE_GATED) {
+  const size_t rows = (size_t)batch * Hkv * seq_len;
+  if (walk && gated) {
     Timed tm("bwd_gather_gate", s);
-    HIP_TRY(launch_gather_gate(in->sel_idx, in->log_gate, batch, seq_len, c->n_kv_heads, K, NB, bw.sel_bias, s),
+    HIP_TRY(launch_gather_gate(in->sel_idx, in->log_gate, batch, seq_len, Hkv, K, NB, bw.sel_bias, s),
             "gather gate");
   }
+  // per-slot gradient: asked for, or needed to build the table of the sparse scope
+  float* slots = nullptr;
+  if (gated && walk && !fullg) slots = out->dlog_gate ? out->dlog_gate : (out->dlog_gate_full ? bw.dlg_slots : nullptr);
   BwdArgs a = {};
   a.b = batch;
   a.n = seq_len;
   a.H = c->n_heads;
-  a.Hkv = c->n_kv_heads;
+  a.Hkv = Hkv;
   a.dh = c->head_dim;
   a.B = c->block_size;
-  a.K = sparse ? K : 0;
+  a.K = walk ? K : 0;
   a.mode = c->mode;
   a.sm_scale = sm_scale_of(c);
   a.Q = in->q;
@@ -638,25 +675,36 @@ sas_status sas_attention_backward(const sas_config* c, int32_t batch, int32_t se
   a.O = in->o;
   a.dO = in->d_o;
   a.lse = in->lse;
-  a.sel = sparse ? in->sel_idx : nullptr;
+  a.sel = walk ? in->sel_idx : nullptr;
   a.sel_bias = bw.sel_bias;
   a.dQ = out->dq;
   a.dK = out->dk;
   a.dV = out->dv;
-  a.dlog_gate = out->dlog_gate;
+  a.dlog_gate = slots;
   a.delta = bw.delta;
   a.dlg_head = bw.dlg_head;
   a.chunk_mask = bw.chunk_mask;
   a.selmask = bw.selmask;
-  a.log_gate = sparse && c->mode == SAS_MODE_GATED ? in->log_gate : nullptr;
-  if (out->dlog_gate && (c->mode != SAS_MODE_GATED || K == 0)) {
+  a.log_gate = gated ? in->log_gate : nullptr;
+  a.outer = gated && c->gate_pos == SAS_GATE_OUTER;
+  a.full = fullg;
+  a.ste = gated && c->gate_ste;
+  a.dlog_gate_full = fullg ? out->dlog_gate_full : nullptr;
+  a.dlg_head_full = bw.dlg_head_full;
+  {
     Timed tm("bwd_zero", s);
-    HIP_TRY(launch_fill_f32(out->dlog_gate, (size_t)batch * c->n_kv_heads * seq_len * (K > 0 ? K : 0), 0.f, s),
-            "zero dlog_gate");
+    if (out->dlog_gate && !slots) HIP_TRY(launch_fill_f32(out->dlog_gate, rows * K, 0.f, s), "zero dlog_gate");
+    if (out->dlog_gate_full && !fullg && !slots)
+      HIP_TRY(launch_fill_f32(out->dlog_gate_full, rows * NB, 0.f, s), "zero dlog_gate_full");
   }
   {
     Timed tm("attention_bwd", s);
     HIP_TRY(launch_attention_backward(c->dtype, a, s), "attention backward");
+  }
+  if (slots && out->dlog_gate_full) {
+    Timed tm("bwd_scatter", s);
+    HIP_TRY(launch_scatter_slots(in->sel_idx, slots, batch, seq_len, Hkv, K, NB, out->dlog_gate_full, s),
+            "scatter slots");
   }
   return SAS_OK;
 }
@@ -668,13 +716,16 @@ sas_status sas_selector_backward(const sas_config* c, int32_t batch, int32_t seq
     return fail(SAS_ERR_INVALID_ARGUMENT, "batch %d and seq_len %d must be positive", batch, seq_len);
   if (!in || !out) return fail(SAS_ERR_INVALID_ARGUMENT, "in/out is NULL");
   const int K = c->top_k;
+  const float* dfull = in->dlog_gate_full;
+  const bool slots = K > 0 && !dfull;  // per-slot input
   SAS_TRY(check_ptr(in->q, "in.q", true));
   SAS_TRY(check_ptr(in->k, "in.k", true));
   SAS_TRY(check_ptr(in->w_gq, "in.w_gq", false));
   SAS_TRY(check_ptr(in->w_gk, "in.w_gk", false));
-  SAS_TRY(check_ptr(in->sel_idx, "in.sel_idx", K > 0));
-  SAS_TRY(check_ptr(in->log_gate, "in.log_gate", K > 0));
-  SAS_TRY(check_ptr(in->dlog_gate, "in.dlog_gate", K > 0));
+  SAS_TRY(check_ptr(in->sel_idx, "in.sel_idx", slots));
+  SAS_TRY(check_ptr(in->log_gate, "in.log_gate", slots || dfull));
+  SAS_TRY(check_ptr(in->dlog_gate, "in.dlog_gate", slots));
+  SAS_TRY(check_ptr(dfull, "in.dlog_gate_full", false));
   SAS_TRY(check_ptr(out->ds, "out.ds", false));
   SAS_TRY(check_ptr(out->dqhat, "out.dqhat", false));
   SAS_TRY(check_ptr(out->dkbar, "out.dkbar", false));
@@ -690,7 +741,7 @@ sas_status sas_selector_backward(const sas_config* c, int32_t batch, int32_t seq
   const size_t rows = (size_t)batch * Hkv * n;
   float* dw_gq = in->w_gq ? out->dw_gq : nullptr;
   float* dw_gk = in->w_gk ? out->dw_gk : nullptr;
-  if (K == 0) {  // no selected block: every gradient is zero
+  if (K == 0 && !dfull) {  // no selected block: every gradient is zero
     Timed tm("sel_bwd_zero", s);
     HIP_TRY(launch_fill_f32(out->ds, out->ds ? rows * NB : 0, 0.f, s), "zero ds");
     HIP_TRY(launch_fill_f32(out->dqhat, out->dqhat ? rows * dh : 0, 0.f, s), "zero dqhat");
@@ -711,7 +762,9 @@ sas_status sas_selector_backward(const sas_config* c, int32_t batch, int32_t seq
   float* ds = out->ds ? out->ds : w.ds;
   {
     Timed tm("sel_bwd_ds", s);
-    HIP_TRY(launch_selector_ds(in->sel_idx, in->log_gate, in->dlog_gate, batch, n, Hkv, K, B, ds, s), "ds");
+    HIP_TRY(launch_selector_ds(slots ? in->sel_idx : nullptr, in->log_gate, in->dlog_gate, dfull,
+                               gated_of(c) ? c->gate_act : SAS_ACT_SOFTMAX, batch, n, Hkv, slots ? K : 0, B, ds, s),
+            "ds");
   }
   // s = r / (G sqrt(dh)) with r = qhat . kbar
   const float dr_scale = 1.0f / ((float)(H / Hkv) * sqrtf((float)dh));
@@ -770,6 +823,7 @@ sas_status sas_attention_prefill(const sas_config* c, int32_t batch, int32_t seq
   SAS_TRY(check_ptr(in->v, "in.v", true));
   SAS_TRY(check_ptr(in->w_gq, "in.w_gq", false));
   SAS_TRY(check_ptr(in->w_gk, "in.w_gk", false));
+  SAS_TRY(check_ptr(in->score_noise, "in.score_noise", false));
   SAS_TRY(check_ptr(out->o, "out.o", true));
   SAS_TRY(check_ptr(out->lse, "out.lse", false));
   SAS_TRY(check_ptr(out->k_summary, "out.k_summary", false));
@@ -780,7 +834,8 @@ sas_status sas_attention_prefill(const sas_config* c, int32_t batch, int32_t seq
   AttnWs aw = carve_attention(cv, c, batch, seq_len);
   SAS_TRY(check_ws(ws, ws_bytes, cv.off));
   SAS_TRY(run_attention(c, batch, seq_len, in->q, in->k, in->v, in->w_gq, in->w_gk, out->o, out->lse,
-                        out->k_summary, out->sel_idx, out->log_gate, out->tau, aw, (hipStream_t)stream));
+                        out->k_summary, out->sel_idx, out->log_gate, out->tau, aw, (hipStream_t)stream, false,
+                        in->score_noise));
   return SAS_OK;
 }
 

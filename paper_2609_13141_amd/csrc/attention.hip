@@ -1,7 +1,8 @@
 // SAS attention forward (Eq. ours_train for GATED, Alg. 2's attended set for
 // SPARSE, causal Eq. fula for DENSE), fused with the block gate and the
 // block mask in a tiled online softmax (the kernel described in App. E of
-// the paper, redesigned for CDNA4 wave64 MFMA).
+// the paper, redesigned for CDNA4 wave64 MFMA), with the gating
+// formulations of Table 1 as flags (outer gate, full scope).
 //
 // bf16 kernel layout: one workgroup = 4 waves = 128 consecutive queries of
 // one (batch, head); each wave owns 32 queries.  Scores are computed
@@ -10,17 +11,23 @@
 // partner lane l^32.  The exponentiated scores P^T stay in registers and are
 // fed straight back as the B operand of O^T = V^T P^T: the key order in which
 // the accumulator holds P^T is a fixed permutation of the key index, and V^T
-// is read from LDS in that same permutation, so no shuffle is needed.  KV
-// tiles of 64 keys are staged in LDS (K row-major, V transposed); a tile
-// that no query of the workgroup attends to is skipped.
+// is read from LDS in that same permutation, so no shuffle is needed.
+//
+// The 64-key tiles that any query of the workgroup attends are flagged in an
+// LDS bitmask first (every query's current block and selected blocks, or
+// every earlier tile for DENSE and the full scope); each flagged tile's K and
+// V are loaded into registers while the previous tile is multiplied, then
+// written to LDS (K row-major, V transposed).  The selection rows of the
+// workgroup's queries are staged in LDS, and each lane walks its ascending
+// list with a cursor while the tiles advance.
 //
 // Per (query t, key i) with m = block(i) = i / B and beta = block(t):
-//   m == beta : current block, causal (i <= t), bias 0 (unit gate);
-//   m <  beta : DENSE -> bias 0; SPARSE/GATED -> kept iff m is in the
-//               query group's selected list, bias log g_m (GATED) or 0;
+//   m == beta : current block, causal (i <= t), unit gate;
+//   m <  beta : DENSE -> unit gate; SPARSE/GATED -> kept iff m is selected
+//               (every m for the full scope), gate g_m (GATED) or 1;
 //   m >  beta : masked.
-// The selection list of a query is ascending, so each lane walks it with a
-// cursor while the KV tiles advance.
+// The gate enters as the logit bias log g_m (inner) or as a weight g_m on
+// the block's values (outer; the softmax then normalizes unbiased logits).
 #include <float.h>
 
 #include "common.h"
@@ -31,24 +38,40 @@ namespace sas {
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 
-template <int DH, bool SINGLE>
+template <int DH, int LSB>
 __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
-  constexpr int KP = DH + 8;  // K tile row pitch (elements)
-  constexpr int VP = 64 + 4;  // V^T tile row pitch (elements)
-  constexpr int KPG = DH / 32;  // keys per V-staging group (4 for DH=128, 2 for DH=64)
+  constexpr int KP = DH + 8;    // K tile row pitch (elements)
+  constexpr int VP = 64 + 4;    // V^T tile row pitch (elements)
+  constexpr int KPG = DH / 32;  // keys per thread in the tile staging
+  constexpr int C8 = DH / 8;
+  constexpr int NSUB = 64 >> LSB;  // sub-blocks of min(B, 64) keys in a tile
+  constexpr int KMAX = 32;
   __shared__ __align__(16) bf16_t Ks[64 * KP];
   __shared__ __align__(16) bf16_t Vt[DH * VP];
+  __shared__ int sel_s[128 * KMAX];
+  __shared__ float sbias_s[128 * KMAX];
+  __shared__ uint32_t need[ATTN_MAX_SEQ / 64 / 32];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lk = lane >> 5;
   const int qtile = gridDim.x - 1 - blockIdx.x;  // heavy (late) tiles first
   const int h = blockIdx.y, bi = blockIdx.z;
   const int G = P.H / P.Hkv, g = h / G;
-  const int n = P.n, B = P.B, Kn = P.K;
-  const int t = qtile * 128 + wave * 32 + lr;
+  const int n = P.n, B = P.B;
+  const int qrow = wave * 32 + lr;
+  const int t = qtile * 128 + qrow;
   const bool qvalid = t < n;
   const int beta = qvalid ? t / B : -1;
-  const int bshift = 31 - __clz(B < 64 ? B : 64);  // log2 of keys per SAS block inside a tile
+  const bool gated = P.mode == SAS_MODE_GATED;
+  const bool full = gated && P.full;  // every historical block, gates from the table
+  const bool every = P.mode == SAS_MODE_DENSE || full;
+  const bool outer = gated && P.outer;
+  const int Kn = every ? 0 : P.K;
+  const int ntiles = (n + 63) / 64;
+  const int t_hi = min(n, qtile * 128 + 128) - 1;  // last query of the workgroup
+  const int last_tile = t_hi / 64;
+  const size_t grow = ((size_t)bi * P.Hkv + g) * n;  // first (b, g) row of [b, Hkv, n, ...]
+  const int NB = (n + B - 1) / B;
 
   // Q^T as the B operand: lane supplies Q[t][ks*16 + lk*8 + 0..7]
   bf16x8_t qb[DH / 16];
@@ -61,19 +84,30 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
     }
   }
 
-  // selection cursor over the ascending list of kept blocks
-  const int32_t* selp = nullptr;
-  const float* biasp = nullptr;
-  int cur = 0, next_sel = 0x7fffffff;
-  if (P.mode != SAS_MODE_DENSE && qvalid && Kn > 0) {
-    const size_t row = (((size_t)bi * P.Hkv + g) * n + t) * Kn;
-    selp = P.sel + row;
-    biasp = P.sel_bias + row;
-    const int s0 = selp[0];
-    next_sel = s0 >= 0 ? s0 : 0x7fffffff;
+  // selection rows (the lane pair lk = 0, 1 splits the slots) and the tile flags
+  for (int w = tid; w < (ntiles + 31) / 32; w += 256) {
+    const int lo = w * 32;
+    uint32_t bits = 0;
+    if (every && lo <= last_tile) bits = last_tile - lo >= 31 ? 0xffffffffu : ((1u << (last_tile - lo + 1)) - 1u);
+    need[w] = bits;
   }
-  const bool gated = P.mode == SAS_MODE_GATED;
-  const bool dense = P.mode == SAS_MODE_DENSE;
+  if (Kn > 0 && qvalid) {
+    const size_t row = (grow + t) * Kn;
+    for (int k = lk; k < Kn; k += 2) {
+      sel_s[qrow * KMAX + k] = P.sel[row + k];
+      if (gated) sbias_s[qrow * KMAX + k] = P.sel_bias[row + k];
+    }
+  }
+  __syncthreads();
+  if (!every && qvalid && lk == 0) {
+    for (int tl = (beta * B) / 64; tl <= t / 64; ++tl) atomicOr(&need[tl >> 5], 1u << (tl & 31));
+    for (int k = 0; k < Kn; ++k) {
+      const int m = sel_s[qrow * KMAX + k];
+      if (m < 0 || m >= beta) break;  // slots are ascending historical blocks, -1 padded
+      for (int tl = (m * B) / 64; tl <= ((m + 1) * B - 1) / 64; ++tl) atomicOr(&need[tl >> 5], 1u << (tl & 31));
+    }
+  }
+  __syncthreads();
 
   floatx16_t o[DH / 32];
 #pragma unroll
@@ -83,75 +117,90 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
   float m_run = -INFINITY, l_run = 0.f;
   const float qk_scale = P.sm_scale * LOG2E;
 
-  const int t_hi = min(n, qtile * 128 + 128) - 1;  // last query of the workgroup
-  const int last_tile = t_hi / 64;
   const bf16_t* Kg = (const bf16_t*)P.Kt + (size_t)g * DH;
   const bf16_t* Vg = (const bf16_t*)P.V + (size_t)g * DH;
   const size_t kstride = (size_t)P.Hkv * DH;  // elements between consecutive keys
   const size_t kbase = (size_t)bi * n;
+  const int c8 = tid % C8, kg = tid / C8;
+  uint4 rk[KPG], rv[KPG];
+  float r_lg[NSUB];  // full scope: this lane's log gates of the tile's blocks
+  auto prefetch = [&](int kt) {
+#pragma unroll
+    for (int q = 0; q < KPG; ++q) {
+      const int key = kt * 64 + kg * KPG + q;
+      const size_t go = (kbase + key) * kstride + c8 * 8;
+      rk[q] = key < n ? *(const uint4*)(Kg + go) : make_uint4(0, 0, 0, 0);
+      rv[q] = key < n ? *(const uint4*)(Vg + go) : make_uint4(0, 0, 0, 0);
+    }
+    if (full) {
+#pragma unroll
+      for (int sb = 0; sb < NSUB; ++sb) {
+        const int m = (kt * 64 + (sb << LSB)) / B;
+        r_lg[sb] = (qvalid && m < beta) ? P.gate_table[(grow + t) * NB + m] : 0.f;
+      }
+    }
+  };
+  auto commit = [&]() {
+#pragma unroll
+    for (int q = 0; q < KPG; ++q) *(uint4*)(Ks + (kg * KPG + q) * KP + c8 * 8) = rk[q];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int sh = (e & 1) * 16, wd = e >> 1;
+      bf16_t* dst = Vt + (c8 * 8 + e) * VP + kg * KPG;
+      uint32_t x[KPG];
+#pragma unroll
+      for (int q = 0; q < KPG; ++q) x[q] = (((const uint32_t*)&rv[q])[wd] >> sh) & 0xffffu;
+      if constexpr (KPG == 4) {
+        *(uint2*)dst = make_uint2(x[0] | (x[1] << 16), x[2] | (x[3] << 16));
+      } else {
+        *(uint32_t*)dst = x[0] | (x[1] << 16);
+      }
+    }
+  };
 
-  for (int kt = 0; kt <= last_tile; ++kt) {
+  int cur = 0, next_sel = 0x7fffffff;  // selection cursor of this lane's query
+  if (Kn > 0 && qvalid) {
+    const int s0 = sel_s[qrow * KMAX];
+    next_sel = s0 >= 0 ? s0 : 0x7fffffff;
+  }
+  int kt = next_set(need, 0, ntiles);
+  if (kt < ntiles) prefetch(kt);
+  while (kt < ntiles) {
+    commit();
+    lds_barrier();
     const int k0 = kt * 64;
-    // bias (base-2 domain) of each SAS block of this tile for this lane's
-    // query, -inf when masked; one block per tile when B >= 64
-    constexpr int NSUB = SINGLE ? 1 : 4;
-    float bsub[NSUB];
-    bool need = false;
+    // logit offset (log2 domain; -inf: not attended) and value weight of each sub-block
+    float offs[NSUB], wts[NSUB];
 #pragma unroll
     for (int sb = 0; sb < NSUB; ++sb) {
-      bsub[sb] = -INFINITY;
-      const int kstart = k0 + (sb << bshift);
-      if (!qvalid || kstart > t || (!SINGLE && (sb << bshift) >= 64)) continue;
+      offs[sb] = -INFINITY;
+      wts[sb] = 1.f;
+      const int kstart = k0 + (sb << LSB);
+      if (!qvalid || kstart > t) continue;
       const int m = kstart / B;
-      if (m == beta || dense) {
-        bsub[sb] = 0.f;
+      float lg = 0.f;
+      bool att = false;
+      if (m == beta || P.mode == SAS_MODE_DENSE) {
+        att = true;
+      } else if (full) {
+        att = true;
+        lg = r_lg[sb];
       } else if (m == next_sel) {
-        bsub[sb] = gated ? biasp[cur] * LOG2E : 0.f;
-        // a block wider than a tile is consumed at its last tile
-        if (kstart + (1 << bshift) >= (m + 1) * B) {
+        att = true;
+        lg = gated ? sbias_s[qrow * KMAX + cur] : 0.f;
+        if (kstart + (1 << LSB) >= (m + 1) * B) {  // a block wider than a tile is consumed at its last tile
           ++cur;
-          const int s1 = cur < Kn ? selp[cur] : -1;
+          const int s1 = cur < Kn ? sel_s[qrow * KMAX + cur] : -1;
           next_sel = s1 >= 0 ? s1 : 0x7fffffff;
         }
       }
-      need |= bsub[sb] != -INFINITY;
-    }
-    // also orders this tile's LDS writes after the previous tile's reads
-    if (!__syncthreads_or(need)) continue;
-
-    // stage K row-major and V transposed; each lane transposes KPG keys x 8 dims
-    {
-#pragma unroll
-      for (int i = 0; i < (64 * DH / 8) / 256; ++i) {
-        const int c = tid + i * 256;
-        const int kr = c / (DH / 8), c8 = c % (DH / 8);
-        const int key = k0 + kr;
-        uint4 ku = key < n ? *(const uint4*)(Kg + (kbase + key) * kstride + c8 * 8) : make_uint4(0, 0, 0, 0);
-        *(uint4*)(Ks + kr * KP + c8 * 8) = ku;
-      }
-      const int c8 = tid % (DH / 8), kg = tid / (DH / 8);
-      uint32_t w[KPG][4];
-#pragma unroll
-      for (int q = 0; q < KPG; ++q) {
-        const int key = k0 + kg * KPG + q;
-        uint4 vu = key < n ? *(const uint4*)(Vg + (kbase + key) * kstride + c8 * 8) : make_uint4(0, 0, 0, 0);
-        w[q][0] = vu.x; w[q][1] = vu.y; w[q][2] = vu.z; w[q][3] = vu.w;
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int sh = (e & 1) * 16;
-        bf16_t* dst = Vt + (c8 * 8 + e) * VP + kg * KPG;
-        if constexpr (KPG == 4) {
-          uint2 pk;
-          pk.x = ((w[0][e >> 1] >> sh) & 0xffffu) | (((w[1][e >> 1] >> sh) & 0xffffu) << 16);
-          pk.y = ((w[2][e >> 1] >> sh) & 0xffffu) | (((w[3][e >> 1] >> sh) & 0xffffu) << 16);
-          *(uint2*)dst = pk;
-        } else {
-          *(uint32_t*)dst = ((w[0][e >> 1] >> sh) & 0xffffu) | (((w[1][e >> 1] >> sh) & 0xffffu) << 16);
-        }
+      if (att) {
+        offs[sb] = outer ? 0.f : lg * LOG2E;
+        wts[sb] = outer ? __builtin_amdgcn_exp2f(lg * LOG2E) : 1.f;
       }
     }
-    __syncthreads();
+    const int nkt = next_set(need, kt + 1, ntiles);
+    if (nkt < ntiles) prefetch(nkt);
 
     // S^T = K Q^T for keys [0,32) and [32,64) of the tile
     floatx16_t s[2];
@@ -165,22 +214,16 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
         s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qb[ks], s[st], 0, 0, 0);
       }
     }
-    // scale, bias, mask; row max over this lane's 32 keys and the partner's
-    const int lim = t - k0;  // keys kl <= lim are causal for this lane
+    // scale + offset, causal mask on the diagonal tiles; row max with the partner lane
+    const bool diag = k0 + 63 > qtile * 128;
     float mx = -INFINITY;
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int kl = st * 32 + 8 * (v >> 2) + 4 * lk + (v & 3);
-        float bb;
-        if constexpr (SINGLE) {
-          bb = bsub[0];
-        } else {
-          const int sb = kl >> bshift;
-          bb = sb == 0 ? bsub[0] : sb == 1 ? bsub[1] : sb == 2 ? bsub[2] : bsub[3];
-        }
-        const float x = (kl <= lim) ? s[st][v] * qk_scale + bb : -INFINITY;
+        const int klc = st * 32 + 8 * (v >> 2);  // key offset without the lane part (4 lk + v % 4 < 8)
+        float x = fmaf(s[st][v], qk_scale, offs[klc >> LSB]);
+        if (diag && k0 + klc + 4 * lk + (v & 3) > t) x = -INFINITY;
         s[st][v] = x;
         mx = fmaxf(mx, x);
       }
@@ -194,8 +237,8 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const float p = __builtin_amdgcn_exp2f(s[st][v] - m_use);
-        s[st][v] = p;
         rs += p;
+        s[st][v] = outer ? p * wts[(st * 32 + 8 * (v >> 2)) >> LSB] : p;
       }
     rs += __shfl_xor(rs, 32, 64);
     l_run = l_run * alpha + rs;
@@ -208,12 +251,13 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
     // O^T += V^T P^T, 16 keys per step in the accumulator's key permutation
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      bf16x8_t pb;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        bf16_t hb = f32_to_bf16(s[ks >> 1][8 * (ks & 1) + e]);
-        pb[e] = *(__bf16*)&hb;
-      }
+      const int st = ks >> 1, v0 = 8 * (ks & 1);
+      uint4 pu;
+      pu.x = pack_bf16x2(s[st][v0 + 0], s[st][v0 + 1]);
+      pu.y = pack_bf16x2(s[st][v0 + 2], s[st][v0 + 3]);
+      pu.z = pack_bf16x2(s[st][v0 + 4], s[st][v0 + 5]);
+      pu.w = pack_bf16x2(s[st][v0 + 6], s[st][v0 + 7]);
+      const bf16x8_t pb = *(const bf16x8_t*)&pu;
 #pragma unroll
       for (int dt = 0; dt < DH / 32; ++dt) {
         const bf16_t* vr = Vt + (dt * 32 + lr) * VP + 16 * ks + 4 * lk;
@@ -223,6 +267,8 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
         o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(bf16x8_t*)&u, pb, o[dt], 0, 0, 0);
       }
     }
+    lds_barrier();
+    kt = nkt;
   }
 
   if (!qvalid) return;
@@ -233,10 +279,8 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
 #pragma unroll
     for (int v4 = 0; v4 < 4; ++v4) {
       const int d0 = dt * 32 + 8 * v4 + 4 * lk;
-      const uint32_t w0 = (uint32_t)f32_to_bf16(o[dt][4 * v4 + 0] * inv_l) |
-                          ((uint32_t)f32_to_bf16(o[dt][4 * v4 + 1] * inv_l) << 16);
-      const uint32_t w1 = (uint32_t)f32_to_bf16(o[dt][4 * v4 + 2] * inv_l) |
-                          ((uint32_t)f32_to_bf16(o[dt][4 * v4 + 3] * inv_l) << 16);
+      const uint32_t w0 = pack_bf16x2(o[dt][4 * v4 + 0] * inv_l, o[dt][4 * v4 + 1] * inv_l);
+      const uint32_t w1 = pack_bf16x2(o[dt][4 * v4 + 2] * inv_l, o[dt][4 * v4 + 3] * inv_l);
       *(uint2*)(op + d0) = make_uint2(w0, w1);
     }
   if (P.lse && lk == 0) P.lse[((size_t)bi * P.H + h) * n + t] = (m_run + log2f(l_run)) * LN2;
@@ -262,7 +306,7 @@ __global__ void attn_f32_kernel(AttnArgs P) {
     acc[j] = 0.f;
   }
   float mrun = -INFINITY, lrun = 0.f;
-  auto visit = [&](int i, float bias) {
+  auto visit = [&](int i, float bias, float w) {
     const float* k = Kg + (((size_t)bi * n + i) * P.Hkv + g) * DH;
     const float* v = Vg + (((size_t)bi * n + i) * P.Hkv + g) * DH;
     float z = 0.f;
@@ -272,22 +316,39 @@ __global__ void attn_f32_kernel(AttnArgs P) {
     float mn = fmaxf(mrun, z);
     float a = expf(mrun - mn), p = expf(z - mn);
     lrun = lrun * a + p;
+    const float pw = p * w;
 #pragma unroll
-    for (int j = 0; j < DH; ++j) acc[j] = acc[j] * a + p * v[j];
+    for (int j = 0; j < DH; ++j) acc[j] = acc[j] * a + pw * v[j];
     mrun = mn;
   };
   const int beta = t / B;
+  const bool gated = P.mode == SAS_MODE_GATED;
+  const bool outer = gated && P.outer;
+  // log gate lg of a kept historical block -> (logit bias, value weight)
+  auto gate = [&](float lg, float& w) -> float {
+    w = outer ? expf(lg) : 1.f;
+    return outer ? 0.f : lg;
+  };
+  const size_t row = ((size_t)bi * P.Hkv + g) * n + t;
   if (P.mode == SAS_MODE_DENSE) {
-    for (int i = 0; i <= t; ++i) visit(i, 0.f);
-  } else {
-    const size_t row = (((size_t)bi * P.Hkv + g) * n + t) * P.K;
-    for (int k = 0; k < P.K; ++k) {
-      int m = P.sel[row + k];
-      if (m < 0) break;
-      float bias = P.mode == SAS_MODE_GATED ? P.sel_bias[row + k] : 0.f;
-      for (int i = m * B; i < (m + 1) * B; ++i) visit(i, bias);
+    for (int i = 0; i <= t; ++i) visit(i, 0.f, 1.f);
+  } else if (gated && P.full) {
+    const int NB = (n + B - 1) / B;
+    for (int m = 0; m < beta; ++m) {
+      float w;
+      const float bias = gate(P.gate_table[row * NB + m], w);
+      for (int i = m * B; i < (m + 1) * B; ++i) visit(i, bias, w);
     }
-    for (int i = beta * B; i <= t; ++i) visit(i, 0.f);
+    for (int i = beta * B; i <= t; ++i) visit(i, 0.f, 1.f);
+  } else {
+    for (int k = 0; k < P.K; ++k) {
+      int m = P.sel[row * P.K + k];
+      if (m < 0) break;
+      float w = 1.f, bias = 0.f;
+      if (gated) bias = gate(P.sel_bias[row * P.K + k], w);
+      for (int i = m * B; i < (m + 1) * B; ++i) visit(i, bias, w);
+    }
+    for (int i = beta * B; i <= t; ++i) visit(i, 0.f, 1.f);
   }
   float* o = (float*)P.O + (((size_t)bi * n + t) * P.H + h) * DH;
 #pragma unroll
@@ -298,14 +359,17 @@ __global__ void attn_f32_kernel(AttnArgs P) {
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
   if (a.n <= 0 || a.b <= 0) return hipSuccess;
   if (dtype == SAS_BF16) {
+    if (a.n > ATTN_MAX_SEQ || a.K > 32) return hipErrorInvalidValue;
     dim3 grid(cdiv(a.n, 128), a.H, a.b);
-    const bool single = a.B >= 64;
+    const int lsb = a.B >= 64 ? 6 : (a.B == 32 ? 5 : 4);
     if (a.dh == 128) {
-      if (single) attn_bf16_kernel<128, true><<<grid, 256, 0, s>>>(a);
-      else attn_bf16_kernel<128, false><<<grid, 256, 0, s>>>(a);
+      if (lsb == 6) attn_bf16_kernel<128, 6><<<grid, 256, 0, s>>>(a);
+      else if (lsb == 5) attn_bf16_kernel<128, 5><<<grid, 256, 0, s>>>(a);
+      else attn_bf16_kernel<128, 4><<<grid, 256, 0, s>>>(a);
     } else {
-      if (single) attn_bf16_kernel<64, true><<<grid, 256, 0, s>>>(a);
-      else attn_bf16_kernel<64, false><<<grid, 256, 0, s>>>(a);
+      if (lsb == 6) attn_bf16_kernel<64, 6><<<grid, 256, 0, s>>>(a);
+      else if (lsb == 5) attn_bf16_kernel<64, 5><<<grid, 256, 0, s>>>(a);
+      else attn_bf16_kernel<64, 4><<<grid, 256, 0, s>>>(a);
     }
   } else {
     size_t tot = (size_t)a.b * a.H * a.n;

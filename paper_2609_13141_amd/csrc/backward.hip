@@ -35,24 +35,52 @@ __global__ void bwd_delta_kernel(const T* __restrict__ O, const T* __restrict__ 
   if (lane == 0) delta[((size_t)bi * H + h) * n + t] = acc;
 }
 
-// key range / bias of the sets: returns the bias of block m for query t (natural
-// log domain), -inf when m is not attended; `slot` = its selection slot or -1
-__device__ __forceinline__ float block_bias(const BwdArgs& P, int bi, int g, int t, int m, int& slot) {
-  slot = -1;
+// How block m enters the attention of query t and its gradient (natural-log
+// domain): att = attended (dQ, dK, dV terms); grad = receives a log-gate
+// gradient; bias = logit bias; w = value weight; lg = the block's log gate;
+// slot = its selection slot (-1 if none).
+struct BlockGate {
+  bool att, grad;
+  float bias, w, lg;
+  int slot;
+};
+
+__device__ BlockGate block_gate(const BwdArgs& P, int bi, int g, int t, int m) {
+  BlockGate r = {false, false, 0.f, 1.f, 0.f, -1};
   const int beta = t / P.B;
-  if (m > beta) return -INFINITY;
-  if (m == beta || P.mode == SAS_MODE_DENSE) return 0.f;
-  if (P.K <= 0) return -INFINITY;
-  const size_t row = (((size_t)bi * P.Hkv + g) * P.n + t) * P.K;
-  for (int k = 0; k < P.K; ++k) {
-    const int s = P.sel[row + k];
-    if (s < 0 || s > m) break;
-    if (s == m) {
-      slot = k;
-      return P.mode == SAS_MODE_GATED ? P.sel_bias[row + k] : 0.f;
+  if (m > beta) return r;
+  if (m == beta || P.mode == SAS_MODE_DENSE) {
+    r.att = true;
+    return r;
+  }
+  const bool gated = P.mode == SAS_MODE_GATED;
+  const size_t row = ((size_t)bi * P.Hkv + g) * P.n + t;
+  const int NB = (P.n + P.B - 1) / P.B;
+  if (gated && P.full && !P.ste) {  // every historical block, gate from the table
+    r.att = r.grad = true;
+    r.lg = P.log_gate[row * NB + m];
+  } else {
+    for (int k = 0; k < P.K; ++k) {
+      const int s = P.sel[row * P.K + k];
+      if (s < 0 || s > m) break;
+      if (s == m) {
+        r.att = true;
+        r.grad = gated;
+        r.slot = k;
+        r.lg = gated ? P.sel_bias[row * P.K + k] : 0.f;
+        break;
+      }
+    }
+    if (!r.att && gated && P.ste && P.full) {  // straight-through gradient of a dropped block
+      r.grad = true;
+      r.lg = P.log_gate[row * NB + m];
     }
   }
-  return -INFINITY;
+  if (gated && !P.ste) {
+    if (P.outer) r.w = expf(r.lg);
+    else r.bias = r.lg;
+  }
+  return r;
 }
 
 // ---- fp32 path ------------------------------------------------------------------
@@ -64,10 +92,12 @@ __global__ void __launch_bounds__(64) bwd_dq_f32_kernel(BwdArgs P) {
   if (idx >= (size_t)P.b * P.H * n) return;
   const int t = (int)(idx % n), h = (int)((idx / n) % P.H), bi = (int)(idx / ((size_t)n * P.H));
   const int G = P.H / P.Hkv, g = h / G, B = P.B;
+  const int NB = (n + B - 1) / B;
   const float* q = (const float*)P.Q + (((size_t)bi * n + t) * P.H + h) * DH;
   const float* dO = (const float*)P.dO + (((size_t)bi * n + t) * P.H + h) * DH;
-  const float lse = P.lse[((size_t)bi * P.H + h) * n + t];
-  const float delta = P.delta[((size_t)bi * P.H + h) * n + t];
+  const size_t hrow = ((size_t)bi * P.H + h) * n + t;
+  const float lse = P.lse[hrow];
+  const float delta = P.delta[hrow];
   float qv[DH], dov[DH], dq[DH];
 #pragma unroll
   for (int j = 0; j < DH; ++j) {
@@ -75,12 +105,11 @@ __global__ void __launch_bounds__(64) bwd_dq_f32_kernel(BwdArgs P) {
     dov[j] = dO[j];
     dq[j] = 0.f;
   }
-  float* dlg = P.dlg_head ? P.dlg_head + (((size_t)bi * P.H + h) * n + t) * P.K : nullptr;
+  float* dlg = P.dlg_head ? P.dlg_head + hrow * P.K : nullptr;
   const int beta = t / B;
   for (int m = 0; m <= beta; ++m) {
-    int slot;
-    const float bias = block_bias(P, bi, g, t, m, slot);
-    if (bias == -INFINITY) continue;
+    const BlockGate bg = block_gate(P, bi, g, t, m);
+    if (!bg.att && !bg.grad) continue;
     const int i1 = m == beta ? t : (m + 1) * B - 1;
     float dsum = 0.f;
     for (int i = m * B; i <= i1; ++i) {
@@ -92,13 +121,19 @@ __global__ void __launch_bounds__(64) bwd_dq_f32_kernel(BwdArgs P) {
         z = fmaf(qv[j], k[j], z);
         dp = fmaf(dov[j], v[j], dp);
       }
-      const float p = expf(z * P.sm_scale + bias - lse);
-      const float ds = p * (dp - delta);
-      dsum += ds;
+      const float p = expf(z * P.sm_scale + bg.bias - lse);
+      const float dpw = bg.w * dp;
+      const float ds = p * (dpw - delta);
+      dsum += P.outer ? p * dpw : ds;
+      if (bg.att) {
 #pragma unroll
-      for (int j = 0; j < DH; ++j) dq[j] = fmaf(ds * P.sm_scale, k[j], dq[j]);
+        for (int j = 0; j < DH; ++j) dq[j] = fmaf(ds * P.sm_scale, k[j], dq[j]);
+      }
     }
-    if (dlg && slot >= 0) dlg[slot] = dsum;
+    if (bg.grad && m < beta) {
+      if (P.full) P.dlg_head_full[hrow * NB + m] = dsum;
+      else if (dlg && bg.slot >= 0) dlg[bg.slot] = dsum;
+    }
   }
   float* dqp = (float*)P.dQ + (((size_t)bi * n + t) * P.H + h) * DH;
 #pragma unroll
@@ -124,9 +159,8 @@ __global__ void __launch_bounds__(64) bwd_dkv_f32_kernel(BwdArgs P) {
     dv[j] = 0.f;
   }
   for (int t = i; t < n; ++t) {
-    int slot;
-    const float bias = block_bias(P, bi, g, t, m, slot);
-    if (bias == -INFINITY) continue;
+    const BlockGate bg = block_gate(P, bi, g, t, m);
+    if (!bg.att) continue;
     for (int h = g * G; h < (g + 1) * G; ++h) {
       const float* q = (const float*)P.Q + (((size_t)bi * n + t) * P.H + h) * DH;
       const float* dO = (const float*)P.dO + (((size_t)bi * n + t) * P.H + h) * DH;
@@ -137,12 +171,13 @@ __global__ void __launch_bounds__(64) bwd_dkv_f32_kernel(BwdArgs P) {
         dp = fmaf(dO[j], vv[j], dp);
       }
       const size_t hr = ((size_t)bi * P.H + h) * n + t;
-      const float p = expf(z * P.sm_scale + bias - P.lse[hr]);
-      const float ds = p * (dp - P.delta[hr]);
+      const float p = expf(z * P.sm_scale + bg.bias - P.lse[hr]);
+      const float ds = p * (bg.w * dp - P.delta[hr]);
+      const float pw = p * bg.w;
 #pragma unroll
       for (int j = 0; j < DH; ++j) {
         dk[j] = fmaf(ds * P.sm_scale, q[j], dk[j]);
-        dv[j] = fmaf(p, dO[j], dv[j]);
+        dv[j] = fmaf(pw, dO[j], dv[j]);
       }
     }
   }
@@ -156,7 +191,9 @@ __global__ void __launch_bounds__(64) bwd_dkv_f32_kernel(BwdArgs P) {
 }
 
 // dLogG[b, g, t, slot] = sum over the group's heads of the per-head block sums
-__global__ void bwd_dlog_gate_sum_kernel(const float* __restrict__ dlg_head, int b, int n, int H, int Hkv, int K,
+// (times the block's gate for the straight-through gate: the gradient of log g)
+__global__ void bwd_dlog_gate_sum_kernel(const float* __restrict__ dlg_head, const float* __restrict__ sel_bias,
+                                         int ste, int b, int n, int H, int Hkv, int K,
                                          float* __restrict__ dlog_gate) {
   const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (size_t)b * Hkv * n * K) return;
@@ -165,7 +202,44 @@ __global__ void bwd_dlog_gate_sum_kernel(const float* __restrict__ dlg_head, int
   const int G = H / Hkv;
   float s = 0.f;
   for (int h = g * G; h < (g + 1) * G; ++h) s += dlg_head[(((size_t)bi * H + h) * n + t) * K + k];
-  dlog_gate[idx] = s;
+  dlog_gate[idx] = ste ? s * expf(sel_bias[idx]) : s;
+}
+
+// the same for every block (full scope): 0 for blocks that are not historical
+__global__ void bwd_dlog_gate_full_sum_kernel(const float* __restrict__ dlg_head_full,
+                                              const float* __restrict__ log_gate, int ste, int b, int n, int H,
+                                              int Hkv, int B, int NB, float* __restrict__ out) {
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (size_t)b * Hkv * n * NB) return;
+  const int m = (int)(idx % NB), t = (int)((idx / NB) % n), g = (int)((idx / ((size_t)NB * n)) % Hkv);
+  const int bi = (int)(idx / ((size_t)NB * n * Hkv));
+  float s = 0.f;
+  if (m < t / B) {
+    const int G = H / Hkv;
+    for (int h = g * G; h < (g + 1) * G; ++h) s += dlg_head_full[(((size_t)bi * H + h) * n + t) * NB + m];
+    if (ste) s *= expf(log_gate[idx]);
+  }
+  out[idx] = s;
+}
+
+__global__ void bwd_scatter_slots_kernel(const int32_t* __restrict__ sel, const float* __restrict__ slots,
+                                         size_t rows, int K, int NB, float* __restrict__ table) {
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= rows * NB) return;
+  const size_t row = idx / NB;
+  const int m = (int)(idx % NB);
+  float v = 0.f;
+  for (int k = 0; k < K; ++k)
+    if (sel[row * K + k] == m) v += slots[row * K + k];
+  table[idx] = v;
+}
+
+hipError_t launch_scatter_slots(const int32_t* sel, const float* slots, int b, int n, int Hkv, int K, int NB,
+                                float* table, hipStream_t s) {
+  const size_t rows = (size_t)b * Hkv * n;
+  if (rows * NB == 0) return hipSuccess;
+  bwd_scatter_slots_kernel<<<(unsigned)cdiv(rows * NB, 256), 256, 0, s>>>(sel, slots, rows, K, NB, table);
+  return hipGetLastError();
 }
 
 // log gate of each selected slot: bias[b, g, t, k] = log_gate[b, g, t, sel[b, g, t, k]]
@@ -184,20 +258,6 @@ __global__ void fill_f32_kernel(float* p, size_t n, float v) {
 
 // ---- bf16 path ------------------------------------------------------------------
 constexpr float BLOG2E = 1.4426950408889634f;
-
-__device__ __forceinline__ void bwd_barrier() {  // LDS writes/reads done, then s_barrier (no vmcnt drain)
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
-// next set bit at or after p in an LDS bitmask of `count` bits (count if none)
-__device__ __forceinline__ int next_set(const uint32_t* bits, int p, int count) {
-  while (p < count) {
-    const uint32_t w = bits[p >> 5] >> (p & 31);
-    if (w) return p + __builtin_ctz(w);
-    p = (p | 31) + 1;
-  }
-  return count;
-}
 
 // Pass 1 (dQ and the per-head block sums of ds): one workgroup = 4 waves =
 // 128 queries of one (batch, head), each lane owning one query of S^T = K Q^T
@@ -232,14 +292,22 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
   const int h = blockIdx.y, bi = blockIdx.z;
   const int G = P.H / P.Hkv, g = h / G;
   const int n = P.n, B = P.B;
-  const int Kn = P.mode == SAS_MODE_DENSE ? 0 : P.K;
   const int qrow = wave * 32 + lr;  // query row of this lane in the workgroup
   const int t = qtile * 128 + qrow;
   const bool qvalid = t < n;
   const int beta = qvalid ? t / B : -1;
   const bool gated = P.mode == SAS_MODE_GATED;
   const bool dense = P.mode == SAS_MODE_DENSE;
+  const bool full = gated && P.full;           // a gradient for every historical block
+  const bool fullatt = full && !P.ste;         // ... which are all attended
+  const bool ste = gated && P.ste, outer = gated && P.outer;
+  const bool every = dense || full;            // every tile up to the query
+  const int Kn = (dense || fullatt) ? 0 : P.K;
   const int ntiles = (n + 63) / 64;
+  const int NB = (n + B - 1) / B;
+  const size_t grow = ((size_t)bi * P.Hkv + g) * n;
+  const int t_hi = min(n, qtile * 128 + 128) - 1;
+  const int last_tile = t_hi / 64;
 
   bf16x8_t qb[DH / 16], dob[DH / 16];
   {
@@ -259,20 +327,24 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
   const float delta = qvalid ? P.delta[hrow] : 0.f;
 
   // selection rows of the workgroup's queries (lane pair lk = 0, 1 splits the slots)
-  for (int w = tid; w < (ntiles + 31) / 32; w += 256) need[w] = 0;
+  for (int w = tid; w < (ntiles + 31) / 32; w += 256) {
+    const int lo = w * 32;
+    uint32_t bits = 0;
+    if (every && lo <= last_tile) bits = last_tile - lo >= 31 ? 0xffffffffu : ((1u << (last_tile - lo + 1)) - 1u);
+    need[w] = bits;
+  }
   if (Kn > 0 && qvalid) {
-    const size_t row = (((size_t)bi * P.Hkv + g) * n + t) * Kn;
+    const size_t row = (grow + t) * Kn;
     for (int k = lk; k < Kn; k += 2) {
       sel_s[qrow * KMAX + k] = P.sel[row + k];
-      if (gated) sbias_s[qrow * KMAX + k] = P.sel_bias[row + k] * BLOG2E;
+      if (gated) sbias_s[qrow * KMAX + k] = P.sel_bias[row + k];
       dlg_s[qrow * KMAX + k] = 0.f;
     }
   }
   __syncthreads();
   // key tiles this workgroup attends: every query's current block, its selected blocks
-  if (qvalid && lk == 0) {
-    const int a0 = dense ? 0 : beta * B;
-    for (int tl = a0 / 64; tl <= t / 64; ++tl) atomicOr(&need[tl >> 5], 1u << (tl & 31));
+  if (!every && qvalid && lk == 0) {
+    for (int tl = (beta * B) / 64; tl <= t / 64; ++tl) atomicOr(&need[tl >> 5], 1u << (tl & 31));
     for (int k = 0; k < Kn; ++k) {
       const int m = sel_s[qrow * KMAX + k];
       if (m < 0 || m >= beta) break;  // slots are ascending historical blocks, -1 padded
@@ -293,6 +365,7 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
   const size_t kbase = (size_t)bi * n;
   const int c8 = tid % C8, kg = tid / C8;
   uint4 rk[KPG], rv[KPG];
+  float r_lg[NSUB];  // full scope: this query's log gates of the tile's blocks
   auto prefetch = [&](int kt) {
 #pragma unroll
     for (int q = 0; q < KPG; ++q) {
@@ -300,6 +373,13 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
       const size_t go = (kbase + key) * kstride + c8 * 8;
       rk[q] = key < n ? *(const uint4*)(Kg + go) : make_uint4(0, 0, 0, 0);
       rv[q] = key < n ? *(const uint4*)(Vg + go) : make_uint4(0, 0, 0, 0);
+    }
+    if (full) {
+#pragma unroll
+      for (int sb = 0; sb < NSUB; ++sb) {
+        const int m = (kt * 64 + (sb << LSB)) / B;
+        r_lg[sb] = (qvalid && m < beta) ? P.log_gate[(grow + t) * NB + m] : 0.f;
+      }
     }
   };
   auto commit = [&]() {
@@ -329,37 +409,58 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
     const int s0 = sel_s[qrow * KMAX];
     next_sel = s0 >= 0 ? s0 : 0x7fffffff;
   }
+  float blk_acc = 0.f;  // full scope: running sum of a block wider than a tile
   int kt = next_set(need, 0, ntiles);
   if (kt < ntiles) prefetch(kt);
   while (kt < ntiles) {
     commit();
-    bwd_barrier();
-    const int nkt = next_set(need, kt + 1, ntiles);
-    if (nkt < ntiles) prefetch(nkt);
+    lds_barrier();
     const int k0 = kt * 64;
 
-    // this query's offset (log2-domain bias - LSE) per sub-block; -inf: not attended
-    float offs[NSUB];
+    // per sub-block: offset (log2-domain bias - LSE; -inf: neither attended nor
+    // receiving a gradient), value weight, attended, selection slot
+    float offs[NSUB], wts[NSUB];
+    bool attb[NSUB], gradb[NSUB];
     int slot[NSUB];
 #pragma unroll
     for (int sb = 0; sb < NSUB; ++sb) {
       offs[sb] = -INFINITY;
+      wts[sb] = 1.f;
+      attb[sb] = gradb[sb] = false;
       slot[sb] = -1;
       const int kstart = k0 + (sb << LSB);
       if (!qvalid || kstart > t) continue;
       const int m = kstart / B;
+      float lg = 0.f;
       if (m == beta || dense) {
-        offs[sb] = -lse2;
-      } else if (m == next_sel) {
-        offs[sb] = (gated ? sbias_s[qrow * KMAX + cur] : 0.f) - lse2;
-        slot[sb] = cur;
-        if (kstart + (1 << LSB) >= (m + 1) * B) {
-          ++cur;
-          const int s1 = cur < Kn ? sel_s[qrow * KMAX + cur] : -1;
-          next_sel = s1 >= 0 ? s1 : 0x7fffffff;
+        attb[sb] = true;
+      } else if (fullatt) {
+        attb[sb] = gradb[sb] = true;
+        lg = r_lg[sb];
+      } else {
+        if (m == next_sel) {
+          attb[sb] = true;
+          gradb[sb] = gated;
+          lg = gated ? sbias_s[qrow * KMAX + cur] : 0.f;
+          slot[sb] = cur;
+          if (kstart + (1 << LSB) >= (m + 1) * B) {
+            ++cur;
+            const int s1 = cur < Kn ? sel_s[qrow * KMAX + cur] : -1;
+            next_sel = s1 >= 0 ? s1 : 0x7fffffff;
+          }
+        } else if (ste && full) {
+          gradb[sb] = true;  // straight-through gradient of a dropped block
+          lg = r_lg[sb];
         }
       }
+      if (attb[sb] || gradb[sb]) {
+        const bool biased = gated && !ste && !outer && m != beta;
+        offs[sb] = (biased ? lg * BLOG2E : 0.f) - lse2;
+        if (outer && m != beta) wts[sb] = __builtin_amdgcn_exp2f(lg * BLOG2E);
+      }
     }
+    const int nkt = next_set(need, kt + 1, ntiles);
+    if (nkt < ntiles) prefetch(nkt);
 
     floatx16_t sc[2], dp[2];
 #pragma unroll
@@ -389,14 +490,26 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
         const int sb = klc >> LSB;
         float p = __builtin_amdgcn_exp2f(fmaf(sc[st][v], qk_scale, offs[sb]));
         if (diag && k0 + klc + 4 * lk + (v & 3) > t) p = 0.f;
-        const float ds = p * (dp[st][v] - delta);
-        sc[st][v] = ds;
-        dsum[sb] += ds;
+        const float dpw = outer ? wts[sb] * dp[st][v] : dp[st][v];
+        const float ds = p * (dpw - delta);
+        sc[st][v] = attb[sb] ? ds : 0.f;
+        dsum[sb] += outer ? p * dpw : ds;
       }
 #pragma unroll
     for (int sb = 0; sb < NSUB; ++sb) {
       const float tot = dsum[sb] + __shfl_xor(dsum[sb], 32, 64);
-      if (slot[sb] >= 0 && lk == 0) dlg_s[qrow * KMAX + slot[sb]] += tot;
+      if (lk == 0 && gradb[sb]) {
+        if (full) {
+          const int kstart = k0 + (sb << LSB), m = kstart / B;
+          blk_acc += tot;
+          if (kstart + (1 << LSB) >= (m + 1) * B) {  // the block's last sub-block
+            P.dlg_head_full[hrow * NB + m] = blk_acc;
+            blk_acc = 0.f;
+          }
+        } else if (slot[sb] >= 0) {
+          dlg_s[qrow * KMAX + slot[sb]] += tot;
+        }
+      }
     }
     // dQ^T += K^T dS^T, 16 keys per step in the accumulator's key permutation
 #pragma unroll
@@ -417,12 +530,12 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
         dq[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(bf16x8_t*)&u, pb, dq[dt], 0, 0, 0);
       }
     }
-    bwd_barrier();
+    lds_barrier();
     kt = nkt;
   }
 
   if (!qvalid) return;
-  if (P.dlg_head && lk == 0) {
+  if (P.dlg_head && !full && lk == 0) {
     float* dlg = P.dlg_head + hrow * P.K;
     for (int k = 0; k < Kn; ++k) dlg[k] = dlg_s[qrow * KMAX + k];
   }
@@ -490,6 +603,7 @@ __global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
   __shared__ __align__(16) bf16_t Dt[DH * QP];
   __shared__ __align__(16) float delta_s[32];
   __shared__ __align__(16) float off_s[8][32];  // log2-domain bias - LSE per (sub-block, row); -inf: not attended
+  __shared__ __align__(16) float wt_s[8][32];   // value weight per (sub-block, row) (outer gate)
   __shared__ uint32_t flags[BWD_MAX_SEQ / 32 / 32];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -505,7 +619,9 @@ __global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
   const int NW = (NB + 31) / 32;
   const int nqc = (n + 31) / 32;
   const bool dense = P.mode == SAS_MODE_DENSE, gated = P.mode == SAS_MODE_GATED;
-  const bool use_mask = !dense && P.K > 0;
+  const bool ste = gated && P.ste, outer = gated && P.outer;
+  const bool fullatt = gated && P.full && !P.ste;  // every historical block attended, gates from the table
+  const bool use_mask = !dense && !fullatt && P.K > 0;
   const size_t grow = ((size_t)bi * P.Hkv + g) * n;  // first row of (b, g) in [b, Hkv, n, ...]
 
   // chunks attending the tile
@@ -515,7 +631,7 @@ __global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
   {
     const uint8_t* cm = use_mask ? P.chunk_mask + ((size_t)bi * P.Hkv + g) * nqc * NB : nullptr;
     for (int qc = qc0 + tid; qc < nqc; qc += NTH) {
-      bool any = dense || (qc * 32) / B <= m_hi;
+      bool any = dense || fullatt || (qc * 32) / B <= m_hi;
       if (!any && cm)
         for (int m = m_lo; m <= m_hi; ++m) any |= cm[(size_t)qc * NB + m] != 0;
       if (any) atomicOr(&flags[qc >> 5], 1u << (qc & 31));
@@ -569,7 +685,7 @@ __global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
       r_lse = t < n ? P.lse[((size_t)bi * H + h) * n + t] : 0.f;
       if (t < n && kstart <= t && m != t / B) {
         r_mw = use_mask ? P.selmask[(grow + t) * NW + (m >> 5)] : 0u;
-        r_lg = gated && use_mask ? P.log_gate[(grow + t) * NB + m] : 0.f;
+        r_lg = gated && (use_mask || fullatt) ? P.log_gate[(grow + t) * NB + m] : 0.f;
       }
     }
   };
@@ -599,12 +715,18 @@ __global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
     if (tid < 32) delta_s[tid] = r_delta;
     if (bsb < nsb) {
       const int t = q0 + bq, kstart = k0 + (bsb << bshift), m = kstart / B;
-      float bb = -INFINITY;
+      float bb = -INFINITY, w = 1.f;
       if (t < n && kstart <= t) {
-        if (m == t / B || dense) bb = 0.f;
-        else if ((r_mw >> (m & 31)) & 1u) bb = gated ? r_lg * BLOG2E : 0.f;
+        if (m == t / B || dense) {
+          bb = 0.f;
+        } else if (fullatt || ((r_mw >> (m & 31)) & 1u)) {
+          const bool gate = gated && !ste;
+          bb = gate && !outer ? r_lg * BLOG2E : 0.f;
+          if (gate && outer) w = __builtin_amdgcn_exp2f(r_lg * BLOG2E);
+        }
       }
       off_s[bsb][bq] = bb - r_lse * BLOG2E;
+      wt_s[bsb][bq] = w;
     }
   };
 
@@ -612,7 +734,7 @@ __global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
   if (qc < nqc) prefetch(qc, 0);
   while (qc < nqc) {
     commit(qc);
-    bwd_barrier();
+    lds_barrier();
     int nq = qc, nh = hg + 1;
     if (nh == G) {
       nh = 0;
@@ -642,14 +764,17 @@ __global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
     for (int j = 0; j < 4; ++j) {
       const float4 of = *(const float4*)&off_s[sbk][8 * j + 4 * lk];
       const float4 de = *(const float4*)&delta_s[8 * j + 4 * lk];
+      float4 wt = make_float4(1.f, 1.f, 1.f, 1.f);
+      if (outer) wt = *(const float4*)&wt_s[sbk][8 * j + 4 * lk];
       const float ofv[4] = {of.x, of.y, of.z, of.w}, dev[4] = {de.x, de.y, de.z, de.w};
+      const float wv[4] = {wt.x, wt.y, wt.z, wt.w};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int v = 4 * j + i;
         float p = __builtin_amdgcn_exp2f(fmaf(sc[v], qk_scale, ofv[i]));
         if (diag && key > q0 + 8 * j + 4 * lk + i) p = 0.f;
-        pp[v] = p;
-        sc[v] = p * (dp[v] - dev[i]);
+        pp[v] = p * wv[i];
+        sc[v] = p * (wv[i] * dp[v] - dev[i]);
       }
     }
     // dV^T += dO^T P and dK^T += Q^T dS, 16 queries per step in the accumulator's query permutation
@@ -679,7 +804,7 @@ __global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
         dk[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(bf16x8_t*)&qu, sb8, dk[dt], 0, 0, 0);
       }
     }
-    bwd_barrier();
+    lds_barrier();
     qc = nq;
     hg = nh;
   }
@@ -752,38 +877,63 @@ hipError_t launch_gather_gate(const int32_t* sel, const float* log_gate, int b, 
 }
 
 // ---- selector ------------------------------------------------------------------
-// one wave per row (b, g, t); lane k < K holds slot k
+// one wave per row (b, g, t); lane k < K holds slot k (per-slot input)
 __global__ void __launch_bounds__(256) selector_ds_kernel(const int32_t* __restrict__ sel,
                                                           const float* __restrict__ log_gate,
-                                                          const float* __restrict__ dlog_gate, int rows, int n,
-                                                          int K, int B, int NB, float* __restrict__ ds) {
+                                                          const float* __restrict__ dlog_gate,
+                                                          const float* __restrict__ dfull, int act, int rows,
+                                                          int n, int K, int B, int NB, float* __restrict__ ds) {
   const int row = (int)(((size_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6), lane = threadIdx.x & 63;
   if (row >= rows) return;
   const int C = (row % n) / B;
-  const int sk = lane < K ? sel[(size_t)row * K + lane] : -1;
-  const float dk = sk >= 0 ? dlog_gate[(size_t)row * K + lane] : 0.f;
-  const float D = wave_sum(dk);
   const float* lg = log_gate + (size_t)row * NB;
+  const float* dfr = dfull ? dfull + (size_t)row * NB : nullptr;
+  int sk = -1;
+  float dk = 0.f;
+  if (!dfr && lane < K) {
+    sk = sel[(size_t)row * K + lane];
+    if (sk >= 0) dk = dlog_gate[(size_t)row * K + lane];
+  }
+  float D = 0.f;  // sum of the row's log-gate gradient (softmax)
+  if (act == SAS_ACT_SOFTMAX) {
+    if (dfr) {
+      for (int m = lane; m < C; m += 64) D += dfr[m];
+      D = wave_sum(D);
+    } else {
+      D = wave_sum(dk);
+    }
+  }
   float* out = ds + (size_t)row * NB;
   for (int m0 = 0; m0 < NB; m0 += 64) {
     const int m = m0 + lane;
+    float dl = 0.f;
+    if (dfr) {
+      if (m < C) dl = dfr[m];
+    } else {
+      for (int k = 0; k < K; ++k) {  // every lane shuffles (the sources must be active)
+        const int s = __shfl(sk, k, 64);
+        const float d = __shfl(dk, k, 64);
+        if (s == m) dl += d;
+      }
+    }
     float v = 0.f;
-    if (m < C) v = -expf(lg[m]) * D;
-    for (int k = 0; k < K; ++k) {
-      const int s = __shfl(sk, k, 64);
-      const float d = __shfl(dk, k, 64);
-      if (s == m && m < C) v += d;
+    if (m < C) {
+      if (act == SAS_ACT_SOFTMAX) v = dl - expf(lg[m]) * D;
+      else if (act == SAS_ACT_SIGMOID) v = dl * (1.f - expf(lg[m]));
+      else v = dl;
     }
     if (m < NB) out[m] = v;
   }
 }
 
-hipError_t launch_selector_ds(const int32_t* sel, const float* log_gate, const float* dlog_gate, int b, int n,
-                              int Hkv, int K, int B, float* ds, hipStream_t s) {
+hipError_t launch_selector_ds(const int32_t* sel, const float* log_gate, const float* dlog_gate,
+                              const float* dlog_gate_full, int act, int b, int n, int Hkv, int K, int B, float* ds,
+                              hipStream_t s) {
   const int rows = b * Hkv * n;
   if (rows <= 0) return hipSuccess;
   if (K > 64) return hipErrorInvalidValue;
-  selector_ds_kernel<<<cdiv(rows, 4), 256, 0, s>>>(sel, log_gate, dlog_gate, rows, n, K, B, cdiv(n, B), ds);
+  selector_ds_kernel<<<cdiv(rows, 4), 256, 0, s>>>(sel, log_gate, dlog_gate, dlog_gate_full, act, rows, n, K, B,
+                                                   cdiv(n, B), ds);
   return hipGetLastError();
 }
 
@@ -892,9 +1042,10 @@ hipError_t launch_attention_backward(int dtype, const BwdArgs& a, hipStream_t s)
   else
     bwd_delta_kernel<float><<<cdiv(waves, 4), 256, 0, s>>>((const float*)a.O, (const float*)a.dO, a.b, a.n, a.H,
                                                              a.dh, a.delta);
-  const bool need_dlg = a.dlog_gate && a.mode == SAS_MODE_GATED && a.K > 0;
+  const bool need_dlg = a.dlog_gate && a.mode == SAS_MODE_GATED && a.K > 0 && !a.full;
   BwdArgs P = a;
   if (!need_dlg) P.dlg_head = nullptr;
+  if (!(a.mode == SAS_MODE_GATED && a.full)) P.dlg_head_full = nullptr;
   if (P.dlg_head) {
     const size_t tot = (size_t)a.b * a.H * a.n * a.K;
     fill_f32_kernel<<<(unsigned)cdiv(tot, 256), 256, 0, s>>>(P.dlg_head, tot, 0.f);
@@ -914,8 +1065,14 @@ hipError_t launch_attention_backward(int dtype, const BwdArgs& a, hipStream_t s)
   }
   if (need_dlg) {
     const size_t tot = (size_t)a.b * a.Hkv * a.n * a.K;
-    bwd_dlog_gate_sum_kernel<<<(unsigned)cdiv(tot, 256), 256, 0, s>>>(P.dlg_head, a.b, a.n, a.H, a.Hkv, a.K,
-                                                                        a.dlog_gate);
+    bwd_dlog_gate_sum_kernel<<<(unsigned)cdiv(tot, 256), 256, 0, s>>>(P.dlg_head, a.sel_bias, a.ste, a.b, a.n,
+                                                                        a.H, a.Hkv, a.K, a.dlog_gate);
+  }
+  if (P.dlg_head_full) {
+    const int NB = cdiv(a.n, a.B);
+    const size_t tot = (size_t)a.b * a.Hkv * a.n * NB;
+    bwd_dlog_gate_full_sum_kernel<<<(unsigned)cdiv(tot, 256), 256, 0, s>>>(
+        P.dlg_head_full, a.log_gate, a.ste, a.b, a.n, a.H, a.Hkv, a.B, NB, a.dlog_gate_full);
   }
   return hipGetLastError();
 }

@@ -32,6 +32,23 @@ __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
   return __builtin_bit_cast(bf16_t, (__bf16)f);
 }
 
+// Workgroup barrier after this wave's LDS accesses complete (s_waitcnt
+// lgkmcnt(0); s_barrier).  Unlike __syncthreads() it does not wait for
+// outstanding global loads, so loads issued for the next step stay in flight.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// next set bit at or after p in an LDS bitmask of `count` bits (count if none)
+__device__ __forceinline__ int next_set(const uint32_t* bits, int p, int count) {
+  while (p < count) {
+    const uint32_t w = bits[p >> 5] >> (p & 31);
+    if (w) return p + __builtin_ctz(w);
+    p = (p | 31) + 1;
+  }
+  return count;
+}
+
 // double -> bfloat16 directly (one rounding, ties to even), including
 // subnormal results and overflow to infinity.
 __device__ __forceinline__ bf16_t f64_to_bf16(double d) {

@@ -71,6 +71,8 @@ struct SelectArgs {
   float* sel_bias;        // [b, Hkv, n, K] log g of each kept block (required)
   float* log_gate;        // [b, Hkv, n, NB] optional
   float* tau;             // [b, Hkv, n] optional
+  const float* noise;     // [b, Hkv, n, NB] added to the scores (optional)
+  int act;                // sas_gate_act
 };
 hipError_t launch_select(int dtype, const SelectArgs& a, hipStream_t s);
 
@@ -85,8 +87,13 @@ struct AttnArgs {
   const float* sel_bias;  // [b, Hkv, n, K] (GATED)
   void* O;                // [b, n, H, dh]
   float* lse;             // [b, H, n] optional
+  int outer;              // GATED: the gate weights the values instead of biasing the logits
+  int full;               // GATED: every historical block attended, gates from gate_table
+  const float* gate_table;  // [b, Hkv, n, NB] log gates (full scope)
 };
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
+// longest sequence of the bf16 attention forward (key tiles of 64 tracked in LDS)
+constexpr int ATTN_MAX_SEQ = 1 << 20;
 
 // ---- backward.hip ----------------------------------------------------------
 struct BwdArgs {
@@ -110,20 +117,29 @@ struct BwdArgs {
   const float* log_gate;  // [b, Hkv, n, ceil(n/B)] (GATED)
   uint8_t* chunk_mask;    // [b, Hkv, ceil(n/32), ceil(n/B)] (bf16 path)
   uint32_t* selmask;      // [b, Hkv, n, ceil(ceil(n/B)/32)] bit m: block m selected (bf16 path)
+  // gating formulation (GATED): outer gate; full scope; straight-through hard gate
+  int outer, full, ste;
+  float* dlog_gate_full;  // [b, Hkv, n, NB] output (full scope / straight-through)
+  float* dlg_head_full;   // [b, H, n, NB] scratch (full scope / straight-through)
 };
 // longest sequence of the bf16 attention backward (query chunks of 32 tracked in LDS)
 constexpr int BWD_MAX_SEQ = 262144;
 hipError_t launch_attention_backward(int dtype, const BwdArgs& a, hipStream_t s);
 // p[0..n) = v with a kernel (capturable in a graph, unlike a memset node)
 hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t s);
+// table[r, m] = sum over the slots k of row r with sel[r, k] == m of slots[r, k]
+hipError_t launch_scatter_slots(const int32_t* sel, const float* slots, int b, int n, int Hkv, int K, int NB,
+                                float* table, hipStream_t s);
 // bias[b, g, t, k] = log_gate[b, g, t, sel[b, g, t, k]] (0 for empty slots)
 hipError_t launch_gather_gate(const int32_t* sel, const float* log_gate, int b, int n, int Hkv, int K, int NB,
                               float* bias, hipStream_t s);
-// Selector backward.  ds[r, m] for rows r = (b, g, t) and m < NB:
-// [m selected] dlog_gate[r, slot of m] - exp(log_gate[r, m]) sum_slots dlog_gate[r, .]
-// for m < t / B (the row's historical blocks), 0 otherwise.
-hipError_t launch_selector_ds(const int32_t* sel, const float* log_gate, const float* dlog_gate, int b, int n,
-                              int Hkv, int K, int B, float* ds, hipStream_t s);
+// Selector backward.  ds[r, m] for rows r = (b, g, t), m < NB, from the log-gate
+// gradient dl (per slot: dlog_gate at the slots of sel; or the full table):
+// SOFTMAX dl_m - exp(log_gate[r, m]) sum_m' dl_m'; SIGMOID dl_m (1 - exp(log_gate));
+// RAW dl_m; for m < t / B (the row's historical blocks), 0 otherwise.
+hipError_t launch_selector_ds(const int32_t* sel, const float* log_gate, const float* dlog_gate,
+                              const float* dlog_gate_full, int act, int b, int n, int Hkv, int K, int B, float* ds,
+                              hipStream_t s);
 // C(z, split)[i, j] = alpha sum_{k in split} A(z)[i, k] B(z)[k, j] for z < Z: fp32
 // A, B in the activation dtype, fp32 C; strides in elements.  With splits > 1
 // each split writes its own partial at C + split * sCs.

@@ -155,7 +155,9 @@ __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
   const int ct = valid ? t / P.B : 0;
   const int t_last = min(P.n - 1, t0 + WAVE - 1);
   const int cmax = t_last / P.B;  // wave-uniform loop bound
-  const double inv_scale = 1.0 / ((double)G * sqrt((double)DH));
+  const double den = (double)G * sqrt((double)DH);  // s = r / (G sqrt(dh))
+  const double inv_scale = 1.0 / den;
+  const float* noise = (P.noise && valid) ? P.noise + (((size_t)bi * P.Hkv + g) * P.n + t) * P.NB : nullptr;
 
   // stage the 64 gate queries: either the precomputed (projected) rows, or
   // the group's query heads summed here in fp64 and rounded once
@@ -236,8 +238,9 @@ __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
     for (int mm = 0; mm < SEL_MC; ++mm) {
       const int m = m0 + mm;
       if (mm >= mc || m >= ct) continue;
-      const double rv = r[mm];
-      const double sv = rv * inv_scale;
+      // ranking key: the raw score r, or the noisy score s + noise when noise is given
+      const double sv = noise ? r[mm] / den + (double)noise[m] : r[mm] * inv_scale;
+      const double rv = noise ? sv : r[mm];
       if (sv > mrun) {
         lrun = lrun * expf((float)(mrun - sv)) + 1.f;
         mrun = sv;
@@ -262,6 +265,13 @@ __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
   }
   if (!valid) return;
   const double lse = (ct > 0) ? mrun + log((double)lrun) : 0.0;
+  const int act = P.act;
+  auto log_gate_of = [&](double key) -> double {  // log g of a block from its ranking key
+    const double sv = noise ? key : key * inv_scale;
+    if (act == SAS_ACT_SOFTMAX) return sv - lse;
+    if (act == SAS_ACT_SIGMOID) return sv >= 0.0 ? -log1p(exp(-sv)) : sv - log1p(exp(sv));
+    return sv;
+  };
   const int K = P.K;
   const int kk = min(K, ct);
   const size_t row = ((size_t)bi * P.Hkv + g) * P.n + t;
@@ -275,7 +285,7 @@ __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
 #pragma unroll
       for (int i = 0; i < KMAX; ++i)
         if (i == K - 1) rk = tr[i];
-      tau = (float)(rk * inv_scale - lse);
+      tau = (float)log_gate_of(rk);
     }
     P.tau[row] = tau;
   }
@@ -303,7 +313,7 @@ __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
   for (int i = 0; i < KMAX; ++i) {
     if (i < K) {
       sel[i] = (i < kk) ? tm[i] : -1;
-      sb[i] = (i < kk) ? (float)(tr[i] * inv_scale - lse) : 0.f;
+      sb[i] = (i < kk) ? (float)log_gate_of(tr[i]) : 0.f;
     }
   }
 
@@ -317,7 +327,7 @@ __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
         double acc = 0.0;
         for (int j = 0; j < DH; ++j)
           acc = fma((double)Act<T>::to_f32(qs[lane][j]), (double)Act<T>::to_f32(kr[j]), acc);
-        v = (float)(acc * inv_scale - lse);
+        v = (float)log_gate_of(noise ? acc / den + (double)noise[m] : acc);
       }
       lg[m] = v;
     }

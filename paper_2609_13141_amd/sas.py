@@ -20,6 +20,9 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsas.so")
 SAS_OK, SAS_ERR_INVALID_ARGUMENT, SAS_ERR_UNSUPPORTED, SAS_ERR_WORKSPACE, SAS_ERR_HIP = 0, -1, -2, -3, -4
 SAS_F32, SAS_BF16 = 0, 1
 MODES = {"dense": 0, "sparse": 1, "gated": 2}
+GATE_POS = {"inner": 0, "outer": 1}
+GATE_ACT = {"softmax": 0, "sigmoid": 1, "raw": 2}
+SCOPES = {"sparse": 0, "full": 1}
 (OP_ATTENTION, OP_MLP, OP_LAYER, OP_DECODE, OP_LM_HEAD, OP_DECODE_SELECT, OP_ATTENTION_BACKWARD,
  OP_SELECTOR_BACKWARD) = range(8)
 TORCH_DTYPE = {"bf16": torch.bfloat16, "f32": torch.float32}
@@ -39,12 +42,13 @@ class Config(C.Structure):
     _fields_ = [("d_model", C.c_int32), ("n_heads", C.c_int32), ("n_kv_heads", C.c_int32),
                 ("head_dim", C.c_int32), ("d_ff", C.c_int32), ("block_size", C.c_int32),
                 ("top_k", C.c_int32), ("rope_base", C.c_float), ("rms_eps", C.c_float),
-                ("sm_scale", C.c_float), ("dtype", C.c_int32), ("mode", C.c_int32)]
+                ("sm_scale", C.c_float), ("dtype", C.c_int32), ("mode", C.c_int32),
+                ("gate_pos", C.c_int32), ("gate_act", C.c_int32), ("scope", C.c_int32), ("gate_ste", C.c_int32)]
 
 
 class AttnIn(C.Structure):
     _fields_ = [("q", C.c_void_p), ("k", C.c_void_p), ("v", C.c_void_p), ("w_gq", C.c_void_p),
-                ("w_gk", C.c_void_p)]
+                ("w_gk", C.c_void_p), ("score_noise", C.c_void_p)]
 
 
 class AttnOut(C.Structure):
@@ -57,11 +61,12 @@ class BwdIn(C.Structure):
 
 
 class BwdOut(C.Structure):
-    _fields_ = [(f, C.c_void_p) for f in ("dq", "dk", "dv", "dlog_gate")]
+    _fields_ = [(f, C.c_void_p) for f in ("dq", "dk", "dv", "dlog_gate", "dlog_gate_full")]
 
 
 class SelBwdIn(C.Structure):
-    _fields_ = [(f, C.c_void_p) for f in ("q", "k", "w_gq", "w_gk", "sel_idx", "log_gate", "dlog_gate")]
+    _fields_ = [(f, C.c_void_p) for f in ("q", "k", "w_gq", "w_gk", "sel_idx", "log_gate", "dlog_gate",
+                                          "dlog_gate_full")]
 
 
 class SelBwdOut(C.Structure):
@@ -144,10 +149,13 @@ def _stream():
     return C.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
-def make_config(w: Workload, mode: str | None = None, sm_scale: float = 0.0) -> Config:
+def make_config(w: Workload, mode: str | None = None, sm_scale: float = 0.0, *, gate_pos: str = "inner",
+                gate_act: str = "softmax", scope: str = "sparse", ste: bool = False) -> Config:
+    """Library config of a workload; the gating keywords select one of the
+    training formulations of Table 1 (GATED mode only)."""
     return Config(w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.d_ff, w.block_size, w.top_k,
                   w.rope_base, w.rms_eps, sm_scale, SAS_BF16 if w.dtype == "bf16" else SAS_F32,
-                  MODES[mode or w.mode])
+                  MODES[mode or w.mode], GATE_POS[gate_pos], GATE_ACT[gate_act], SCOPES[scope], int(ste))
 
 
 def workspace_size(cfg: Config, op: int, batch: int, seq_len: int) -> int:
@@ -186,8 +194,9 @@ def weights_struct(W: dict) -> LayerWeights:
 
 
 def attention_prefill(cfg: Config, q, k, v, w_gq=None, w_gk=None, *, lse=True, k_summary=True,
-                      sel_idx=True, log_gate=False, tau=False, ws: Workspace | None = None) -> dict:
-    """Selector + SAS attention.  q [b,n,H,dh], k/v [b,n,Hkv,dh] on the GPU."""
+                      sel_idx=True, log_gate=False, tau=False, noise=None, ws: Workspace | None = None) -> dict:
+    """Selector + SAS attention.  q [b,n,H,dh], k/v [b,n,Hkv,dh] on the GPU;
+    noise [b,Hkv,n,NB] fp32 (optional) is added to the selector scores."""
     b, n, H, dh = q.shape
     Hkv = k.shape[2]
     B, K = cfg.block_size, cfg.top_k
@@ -204,7 +213,7 @@ def attention_prefill(cfg: Config, q, k, v, w_gq=None, w_gk=None, *, lse=True, k
         out["log_gate"] = torch.empty(b, Hkv, n, NB, dtype=torch.float32, device=dev)
     if tau:
         out["tau"] = torch.empty(b, Hkv, n, dtype=torch.float32, device=dev)
-    ain = AttnIn(_ptr(q), _ptr(k), _ptr(v), _ptr(w_gq), _ptr(w_gk))
+    ain = AttnIn(_ptr(q), _ptr(k), _ptr(v), _ptr(w_gq), _ptr(w_gk), _ptr(noise))
     aout = AttnOut(*[_ptr(out.get(f)) for f in ("o", "lse", "k_summary", "sel_idx", "log_gate", "tau")])
     wsp, wsn = _ws(ws, workspace_size(cfg, OP_ATTENTION, b, n))
     _check(lib().sas_attention_prefill(C.byref(cfg), b, n, C.byref(ain), C.byref(aout), wsp, wsn, _stream()))
@@ -212,23 +221,30 @@ def attention_prefill(cfg: Config, q, k, v, w_gq=None, w_gk=None, *, lse=True, k
 
 
 def attention_backward(cfg: Config, q, k, v, o, d_o, lse, sel_idx=None, log_gate=None, *, dlog_gate: bool = True,
-                       ws: Workspace | None = None) -> dict:
-    """dQ, dK, dV (and the selected blocks' log-gate gradient) of the attention
-    given the forward's inputs, its output o, LSE and selection, and d_o."""
+                       dlog_gate_full: bool = False, ws: Workspace | None = None) -> dict:
+    """dQ, dK, dV and the log-gate gradient of the attention given the
+    forward's inputs, its output o, LSE and selection, and d_o: per selection
+    slot (dlog_gate, sparse scope) and/or per block (dlog_gate_full; the only
+    form for the full scope)."""
     b, n, H, dh = q.shape
     Hkv, K = cfg.n_kv_heads, max(cfg.top_k, 0)
+    NB = -(-n // cfg.block_size)
+    full = cfg.mode == MODES["gated"] and cfg.scope == SCOPES["full"]
     out = {"dq": torch.empty_like(q), "dk": torch.empty_like(k), "dv": torch.empty_like(v)}
-    if dlog_gate:
+    if dlog_gate and not full:
         out["dlog_gate"] = torch.empty(b, Hkv, n, K, dtype=torch.float32, device=q.device)
+    if dlog_gate_full or full:
+        out["dlog_gate_full"] = torch.empty(b, Hkv, n, NB, dtype=torch.float32, device=q.device)
     bi = BwdIn(*[_ptr(t) for t in (q, k, v, o, d_o, lse, sel_idx, log_gate)])
-    bo = BwdOut(*[_ptr(out.get(f)) for f in ("dq", "dk", "dv", "dlog_gate")])
+    bo = BwdOut(*[_ptr(out.get(f)) for f in ("dq", "dk", "dv", "dlog_gate", "dlog_gate_full")])
     wsp, wsn = _ws(ws, workspace_size(cfg, OP_ATTENTION_BACKWARD, b, n))
     _check(lib().sas_attention_backward(C.byref(cfg), b, n, C.byref(bi), C.byref(bo), wsp, wsn, _stream()))
     return out
 
 
 def selector_backward(cfg: Config, q, k, sel_idx, log_gate, dlog_gate, w_gq=None, w_gk=None, *, ds: bool = True,
-                      dqhat: bool = True, dkbar: bool = True, ws: Workspace | None = None) -> dict:
+                      dqhat: bool = True, dkbar: bool = True, dlog_gate_full=None,
+                      ws: Workspace | None = None) -> dict:
     """Selector gradients from the selected blocks' log-gate gradient: ds
     [b,Hkv,n,NB], dqhat [b,Hkv,n,dh], dkbar [b,Hkv,NB,dh] and, for given
     projections, dw_gq / dw_gk [Hkv,dh,dh] (all fp32)."""
@@ -247,7 +263,7 @@ def selector_backward(cfg: Config, q, k, sel_idx, log_gate, dlog_gate, w_gq=None
         out["dw_gq"] = torch.empty(Hkv, dh, dh, dtype=torch.float32, device=dev)
     if w_gk is not None:
         out["dw_gk"] = torch.empty(Hkv, dh, dh, dtype=torch.float32, device=dev)
-    si = SelBwdIn(*[_ptr(t) for t in (q, k, w_gq, w_gk, sel_idx, log_gate, dlog_gate)])
+    si = SelBwdIn(*[_ptr(t) for t in (q, k, w_gq, w_gk, sel_idx, log_gate, dlog_gate, dlog_gate_full)])
     so = SelBwdOut(*[_ptr(out.get(f)) for f in ("ds", "dqhat", "dkbar", "dw_gq", "dw_gk")])
     wsp, wsn = _ws(ws, workspace_size(cfg, OP_SELECTOR_BACKWARD, b, n))
     _check(lib().sas_selector_backward(C.byref(cfg), b, n, C.byref(si), C.byref(so), wsp, wsn, _stream()))

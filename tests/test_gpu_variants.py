@@ -1,0 +1,135 @@
+"""GPU parity of the gating formulations of Table 1 (gate position,
+activation, scope, straight-through hard gate, score noise) against the fp64
+oracle: the selection (bit-exact) and log gates, the attention forward, the
+attention backward with the per-block log-gate gradient, and the selector's
+score gradient through each activation."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle.variants import gate_backward_act, select_variant, variant_attention, variant_attention_backward
+from paper_2609_13141_amd import configs, inputs, sas
+
+from helpers import assert_close, f64
+
+pytestmark = pytest.mark.gpu
+
+
+def W(dtype="bf16", n=200, H=4, Hkv=2, dh=64, B=16, K=2, b=2, index=140):
+    return configs.Workload(name="variant", dtype=dtype, batch=b, seq_len=n, d_model=256, n_heads=H,
+                            n_kv_heads=Hkv, head_dim=dh, d_ff=512, block_size=B, top_k=K, mode="gated",
+                            segments=(("img", n // 2), ("txt", n - n // 2)), index=index)
+
+
+# (pos, act, scope, ste, noise): Table 1's rows and the sparse-scope counterparts
+FORMS = [
+    ("inner", "softmax", "full", False, False),
+    ("outer", "softmax", "full", False, False),
+    ("inner", "sigmoid", "full", False, False),
+    ("inner", "raw", "full", False, False),
+    ("inner", "softmax", "full", True, False),
+    ("inner", "softmax", "sparse", False, True),
+    ("outer", "softmax", "sparse", False, False),
+    ("inner", "softmax", "sparse", True, False),
+    ("inner", "sigmoid", "sparse", False, False),
+    ("outer", "sigmoid", "full", False, False),
+]
+SHAPES = [
+    W(),
+    W(dtype="f32", index=141),
+    W(dh=128, B=64, K=2, n=300, H=4, Hkv=4, b=1, index=142),
+    W(dh=128, B=32, K=3, n=250, H=4, Hkv=1, b=1, index=143),
+]
+CASES = [(f, w) for f in FORMS for w in SHAPES[:2]] + [(FORMS[0], SHAPES[2]), (FORMS[1], SHAPES[3]),
+                                                     (FORMS[4], SHAPES[2]), (FORMS[5], SHAPES[3])]
+
+
+def _id(c):
+    (pos, act, scope, ste, noise), w = c
+    return (f"{pos}-{act}-{scope}{'-ste' if ste else ''}{'-noise' if noise else ''}-{w.dtype}-dh{w.head_dim}"
+            f"-B{w.block_size}-K{w.top_k}-n{w.seq_len}")
+
+
+def _noise(w):
+    NB = -(-w.seq_len // w.block_size)
+    g = inputs.stream(w, "score_noise")
+    u = g.random(size=(w.batch, w.n_kv_heads, w.seq_len, NB), dtype=np.float32)
+    return (-np.log(-np.log(np.clip(u, 1e-7, 1 - 1e-7)))).astype(np.float32)  # Gumbel(0, 1)
+
+
+@pytest.mark.parametrize("case", CASES, ids=[_id(c) for c in CASES])
+def test_variant_forward_backward_match_oracle(case):
+    (pos, act, scope, ste, noisy), w = case
+    print(f"\n[case] {_id(case)}", flush=True)
+    q, k, v = inputs.qkv(w)
+    d_o = inputs.normal(w, "d_o", q.shape, 1.0)
+    eps = _noise(w) if noisy else None
+    cfg = sas.make_config(w, gate_pos=pos, gate_act=act, scope=scope, ste=ste)
+    dt = w.dtype
+    qd, kd, vd, dod = (sas.to_device(a, dt) for a in (q, k, v, d_o))
+    nd = None if eps is None else torch.from_numpy(eps).cuda()
+    fw = sas.attention_prefill(cfg, qd, kd, vd, log_gate=True, noise=nd)
+    bw = sas.attention_backward(cfg, qd, kd, vd, fw["o"], dod, fw["lse"], fw["sel_idx"], fw["log_gate"],
+                                dlog_gate=False, dlog_gate_full=True)
+    sb = sas.selector_backward(cfg, qd, kd, None, fw["log_gate"], None, dlog_gate_full=bw["dlog_gate_full"])
+    torch.cuda.synchronize()
+    tol = 2e-2 if dt == "bf16" else 2e-5
+    B, n = w.block_size, w.seq_len
+    nf = n // B
+    for bi in range(w.batch):
+        st = select_variant(f64(q[bi]), f64(k[bi]), B, w.top_k, dt, act=act,
+                            noise=None if eps is None else f64(eps[bi]))
+        sel, lg = st["sel"], st["log_gate"]
+        np.testing.assert_array_equal(fw["sel_idx"][bi].cpu().numpy(), sel)
+        glg = fw["log_gate"][bi].cpu().numpy()
+        fin = np.isfinite(lg)
+        np.testing.assert_array_equal(np.isfinite(glg), fin)
+        assert_close(glg[fin], lg[fin], dt, "log_gate", tol=1e-5)
+        _, O, LSE = variant_attention(f64(q[bi]), f64(k[bi]), f64(v[bi]), B, dt, sel, lg, pos, scope, ste)
+        assert_close(fw["o"][bi].float().cpu().numpy(), O, dt, f"O b={bi}")
+        assert_close(fw["lse"][bi].cpu().numpy(), LSE, dt, f"LSE b={bi}", tol=1e-3 if dt == "bf16" else 1e-5)
+        dQ, dK, dV, dLG = variant_attention_backward(f64(q[bi]), f64(k[bi]), f64(v[bi]), f64(d_o[bi]), B, sel, lg,
+                                                     pos, scope, ste)
+        assert_close(bw["dq"][bi].float().cpu().numpy(), dQ, dt, f"dQ b={bi}", tol=tol)
+        assert_close(bw["dk"][bi].float().cpu().numpy(), dK, dt, f"dK b={bi}", tol=tol)
+        assert_close(bw["dv"][bi].float().cpu().numpy(), dV, dt, f"dV b={bi}", tol=tol)
+        assert_close(bw["dlog_gate_full"][bi].cpu().numpy(), dLG, dt, f"dLogG b={bi}", tol=tol)
+        # the selector's score gradient from the oracle's own log-gate gradient chain
+        ds = gate_backward_act(dLG[:, :, :nf], st["s"], st["ct"], act)
+        got = sb["ds"][bi].cpu().numpy()
+        assert_close(got[:, :, :nf], ds, dt, f"ds b={bi}", tol=tol)
+        assert np.all(got[:, :, nf:] == 0)
+
+
+def test_variant_selector_backward_exact_input():
+    """The selector backward alone, fed the oracle's per-block log-gate
+    gradient: fp32 arithmetic on identical inputs, bar 1e-4, each activation."""
+    w = W(index=150)
+    q, k, v = inputs.qkv(w)
+    for act in ("softmax", "sigmoid", "raw"):
+        cfg = sas.make_config(w, gate_act=act, scope="full")
+        qd, kd, vd = (sas.to_device(a, "bf16") for a in (q, k, v))
+        fw = sas.attention_prefill(cfg, qd, kd, vd, log_gate=True)
+        rng = np.random.default_rng(5)
+        NB = -(-w.seq_len // w.block_size)
+        dl = rng.standard_normal((w.batch, w.n_kv_heads, w.seq_len, NB)).astype(np.float32)
+        sb = sas.selector_backward(cfg, qd, kd, None, fw["log_gate"], None, dlog_gate_full=torch.from_numpy(dl).cuda())
+        torch.cuda.synchronize()
+        nf = w.seq_len // w.block_size
+        for bi in range(w.batch):
+            st = select_variant(f64(q[bi]), f64(k[bi]), w.block_size, w.top_k, "bf16", act=act)
+            ds = gate_backward_act(f64(dl[bi][:, :, :nf]), st["s"], st["ct"], act)
+            assert_close(sb["ds"][bi, :, :, :nf].cpu().numpy(), ds, "bf16", f"ds {act}", tol=1e-4)
+            ref = oracle.selector_backward(ds, st["qhat"], st["kbar_proj"], w.group, w.head_dim)
+            assert_close(sb["dqhat"][bi].cpu().numpy(), ref["dqhat"], "bf16", f"dqhat {act}", tol=1e-4)
+            assert_close(sb["dkbar"][bi, :, :nf].cpu().numpy(), ref["dkbar"], "bf16", f"dkbar {act}", tol=1e-4)
+
+
+def test_unsupported_forms_are_rejected():
+    w = W(index=151)
+    q, k, v = inputs.qkv(w)
+    qd, kd, vd = (sas.to_device(a, "bf16") for a in (q, k, v))
+    for kw in ({"gate_pos": "outer", "gate_act": "raw"}, {"gate_pos": "outer", "ste": True}):
+        with pytest.raises(sas.SasError, match="outer gate"):
+            sas.attention_prefill(sas.make_config(w, **kw), qd, kd, vd)
