@@ -32,6 +32,10 @@ Parity status of each part (how it is pinned by the oracle self-tests):
   pinned against torch autograd on dense masked formulations (the hard gate
   in its multiplicative form with zero gates), torch's log_softmax and
   logsigmoid, Top-K ordering properties and reductions to the plain modes.
+* selection statistics (mass coverage, full-attention reference sets with
+  the group majority vote, overlap recall): pinned against torch softmax
+  masses and torch.topk, closed forms (q = 0, every block kept, equal value
+  norms) and hand-worked votes and recalls.
 * normalized log gate, Top-K, attention: pinned by closed forms (q = 0),
   V = const, reductions to textbook causal / block-local attention computed
   by torch's scaled_dot_product_attention, causality, shift invariance and
@@ -44,6 +48,7 @@ from .attention import sas_attention
 from .backward import sas_attention_backward, gate_backward, selector_backward
 from .variants import (log_gates, select_variant, variant_attention, variant_attention_backward,
                        gate_backward_act)
+from .stats import mass_coverage, block_mass_topk, majority_vote, selection_sets, overlap_recall
 from .layer import (Spec, layer_forward, mlp_forward, attention_prefill,
                     DecodeCache, decode_step, decode_select, embed_tokens, lm_head_argmax)
 
@@ -55,5 +60,6 @@ __all__ = [
     "decode_select", "embed_tokens", "lm_head_argmax",
     "sas_attention_backward", "gate_backward", "selector_backward",
     "log_gates", "select_variant", "variant_attention", "variant_attention_backward",
-    "gate_backward_act",
+    "gate_backward_act", "mass_coverage", "block_mass_topk", "majority_vote", "selection_sets",
+    "overlap_recall",
 ]
