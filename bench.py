@@ -44,6 +44,7 @@ def parse():
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-step measurement")
     ap.add_argument("--no-long-decode", action="store_true", help="skip the 64K..512K-context decode sweep")
     ap.add_argument("--no-backward", action="store_true", help="skip the training-step backward measurement")
+    ap.add_argument("--no-stats", action="store_true", help="skip the selection-statistics measurement")
     ap.add_argument("--cpu-threads", type=int, default=0, help="oracle BLAS threads (0: affinity, max 16)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain device copy of %d MiB (reference for HBM counters)" % (COPY_BYTES >> 20))
@@ -230,6 +231,9 @@ def main():
         torch.cuda.empty_cache()
     if not args.no_backward:
         line["backward"] = backward_bench()
+        torch.cuda.empty_cache()
+    if not args.no_stats:
+        line["stats"] = stats_bench()
         torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, x_np, W_np, cores)
@@ -431,6 +435,53 @@ def backward_bench(steps=10, warmup=3):
         del q, k, v, d_o, fw, ws_f, ws_b, ws_s
         torch.cuda.empty_cache()
     return out
+
+
+def stats_bench(steps=10, warmup=3):
+    """The selection statistics of Sec. 6.1 for one layer of 7b_layer_4k_b4
+    (4 x 4096 tokens, 32 heads, B = 64, K = 16): mass coverage with both
+    weightings and the accumulation of the selected and full-attention
+    reference block sets.  A dense causal Q K^T pass: 2 dh flops per
+    (query, key <= query) pair and head, plus per-head Top-K and votes."""
+    import torch
+    from paper_2609_13141_amd import configs, sas
+    dev = "cuda:0"
+    w = configs.BY_NAME["7b_layer_4k_b4"]
+    g = torch.Generator(device=dev)
+    g.manual_seed(2000 + w.index)
+    b, n, H, Hkv, dh = w.batch, w.seq_len, w.n_heads, w.n_kv_heads, w.head_dim
+    q, k, v = (torch.randn(*s, generator=g, device=dev).to(torch.bfloat16)
+               for s in ((b, n, H, dh), (b, n, Hkv, dh), (b, n, Hkv, dh)))
+    cfg = sas.make_config(w)
+    fw = sas.attention_prefill(cfg, q, k, v)
+    su, ru = sas.alloc_union(cfg, b, n), sas.alloc_union(cfg, b, n)
+    ws = sas.Workspace(dev)
+
+    def run():
+        sas.selection_stats(cfg, q, k, v, fw["sel_idx"], sel_union=su, ref_union=ru, ws=ws)
+    for _ in range(warmup):
+        run()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        run()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    sas.profiler_start(16 * steps + 16)
+    for _ in range(steps):
+        run()
+    recs = sas.profiler_stop()
+    fam = {}
+    for nm, t in recs:
+        fam.setdefault(nm, []).append(t)
+    kms = {kk: sum(vv) / len(vv) for kk, vv in fam.items()}
+    flops = 2.0 * dh * H * b * n * (n + 1) / 2
+    inter, tot, rec = sas.overlap_recall(su, ru)
+    return {"workload": f"{w.name}: batch {b}, {n} tokens, {H}/{Hkv} heads, dh {dh}, B={w.block_size}, K={w.top_k}",
+            "ms_per_layer": round(ms, 4), "pass_gflop": round(flops / 1e9, 2),
+            "pass_tflops": round(flops / (kms["stats"] * 1e-3) / 1e12, 1),
+            "recall_random_inputs": round(rec, 4),
+            "kernels_ms": {kk: round(vv, 4) for kk, vv in sorted(kms.items(), key=lambda kv: -kv[1])}}
 
 
 def cpu_baseline(w, x_np, W_np, cores):

@@ -93,7 +93,8 @@ typedef enum {
   SAS_OP_LM_HEAD = 4,   /* sas_lm_head_argmax: batch, seq_len = vocab */
   SAS_OP_DECODE_SELECT = 5, /* sas_decode_select: batch, seq_len = max context (tokens) */
   SAS_OP_ATTENTION_BACKWARD = 6, /* sas_attention_backward: batch, seq_len */
-  SAS_OP_SELECTOR_BACKWARD = 7   /* sas_selector_backward: batch, seq_len */
+  SAS_OP_SELECTOR_BACKWARD = 7,  /* sas_selector_backward: batch, seq_len */
+  SAS_OP_SELECTION_STATS = 8     /* sas_selection_stats: batch, seq_len */
 } sas_op;
 
 typedef struct {
@@ -312,6 +313,49 @@ typedef struct {
 sas_status sas_selector_backward(const sas_config* cfg, int32_t batch, int32_t seq_len,
                                  const sas_sel_bwd_in* in, sas_sel_bwd_out* out,
                                  void* ws, size_t ws_bytes, void* stream);
+
+/* Inputs of sas_selection_stats: one layer's post-RoPE q [b,n,H,dh], k and
+ * v [b,n,Hkv,dh] (activation dtype) and its selection sel_idx [b,Hkv,n,K]
+ * (as sas_attention_prefill writes it; unused in DENSE mode). */
+typedef struct {
+  const void* q;
+  const void* k;
+  const void* v;
+  const int32_t* sel_idx;
+} sas_stats_in;
+
+/* Outputs of sas_selection_stats, each optional.  W = ceil(ceil(n/B)/32).
+ *  cov, cov_v [b,H,n] fp32: Eq. mass_coverage of the query's attended set
+ *    (current block + selected blocks) over its causal context, with
+ *    w_i = exp(z_i) and w_i = exp(z_i + log||v_i||_2), z_i = sm q.k_i
+ *    (unbiased logits);
+ *  sel_union [b,Hkv,n,W] uint32: bit m of word m/32 is OR-ed in for every
+ *    selected block (the union over the layers it is called for);
+ *  ref_union [b,Hkv,n,W] uint32: the same for the full-attention reference
+ *    set: per head the top_k historical blocks by attention mass (ties to
+ *    the lower block), per KV group the blocks picked by more than half of
+ *    the group's heads (Sec. 6.1's majority vote).
+ * The unions accumulate: clear them before the first layer. */
+typedef struct {
+  float* cov;
+  float* cov_v;
+  uint32_t* sel_union;
+  uint32_t* ref_union;
+} sas_stats_out;
+
+/* Selection-analysis statistics of one layer (Sec. 6.1, Eq. mass_coverage
+ * and the per-layer sets of Eq. overlap_recall).  A dense causal pass over
+ * Q K^T (no values are multiplied).  ws: sas_workspace_size(cfg,
+ * SAS_OP_SELECTION_STATS, batch, seq_len). */
+sas_status sas_selection_stats(const sas_config* cfg, int32_t batch, int32_t seq_len,
+                               const sas_stats_in* in, sas_stats_out* out,
+                               void* ws, size_t ws_bytes, void* stream);
+
+/* Eq. overlap_recall's counts over two accumulated bitmasks of `words`
+ * uint32 words (DEVICE): counts[0] = |sel & ref|, counts[1] = |ref|
+ * (uint64, DEVICE, overwritten); Recall = counts[0] / counts[1]. */
+sas_status sas_overlap_recall(int64_t words, const uint32_t* sel_union, const uint32_t* ref_union,
+                              uint64_t* counts, void* stream);
 
 /* y = x + SwiGLU(RMSNorm(x)) for `tokens` rows of width d_model:
  * u = RMSNorm(x) * rms2; a = silu(u W_gate^T) * (u W_up^T); y = x + a W_down^T.

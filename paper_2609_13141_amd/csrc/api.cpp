@@ -523,6 +523,21 @@ SelBwdWs carve_selector_backward(Carve& cv, const sas_config* c, int b, int n) {
   return w;
 }
 
+struct StatsWs {
+  float* lvn;
+  float* blk_lse;
+  uint32_t* head_mask;
+};
+
+StatsWs carve_stats(Carve& cv, const sas_config* c, int b, int n) {
+  const size_t H = c->n_heads, Hkv = c->n_kv_heads, NB = cdiv(n, c->block_size);
+  StatsWs w;
+  w.lvn = (float*)cv.take((size_t)b * n * Hkv * 4);
+  w.blk_lse = (float*)cv.take((size_t)b * H * n * NB * 4);
+  w.head_mask = (uint32_t*)cv.take((size_t)b * H * n * cdiv(NB, (size_t)32) * 4);
+  return w;
+}
+
 constexpr int ARGMAX_SLICES = 64;
 
 struct LmWs {
@@ -588,6 +603,10 @@ size_t sas_workspace_size(const sas_config* c, int32_t op, int32_t batch, int32_
     case SAS_OP_SELECTOR_BACKWARD:
       if (seq_len <= 0 || check_config(c, false) != SAS_OK) return 0;
       carve_selector_backward(cv, c, batch, seq_len);
+      break;
+    case SAS_OP_SELECTION_STATS:
+      if (seq_len <= 0 || check_config(c, false) != SAS_OK) return 0;
+      carve_stats(cv, c, batch, seq_len);
       break;
     case SAS_OP_MLP:
       if (check_config(c, true) != SAS_OK) return 0;
@@ -809,6 +828,79 @@ sas_status sas_selector_backward(const sas_config* c, int32_t batch, int32_t seq
     HIP_TRY(launch_small_gemm(c->dtype, g, s), "dw_gk");
     HIP_TRY(launch_partial_sum(w.part, batch, Hkv, h.s_dwk, E, dw_gk, s), "dw_gk sum");
   }
+  return SAS_OK;
+}
+
+sas_status sas_selection_stats(const sas_config* c, int32_t batch, int32_t seq_len, const sas_stats_in* in,
+                               sas_stats_out* out, void* ws, size_t ws_bytes, void* stream) {
+  SAS_TRY(check_config(c, false));
+  if (batch <= 0 || seq_len <= 0)
+    return fail(SAS_ERR_INVALID_ARGUMENT, "batch %d and seq_len %d must be positive", batch, seq_len);
+  if (!in || !out) return fail(SAS_ERR_INVALID_ARGUMENT, "in/out is NULL");
+  const bool walk = c->mode != SAS_MODE_DENSE && c->top_k > 0;
+  SAS_TRY(check_ptr(in->q, "in.q", true));
+  SAS_TRY(check_ptr(in->k, "in.k", true));
+  SAS_TRY(check_ptr(in->v, "in.v", out->cov_v != nullptr));
+  SAS_TRY(check_ptr(in->sel_idx, "in.sel_idx", walk && (out->cov || out->cov_v || out->sel_union)));
+  SAS_TRY(check_ptr(out->cov, "out.cov", false));
+  SAS_TRY(check_ptr(out->cov_v, "out.cov_v", false));
+  SAS_TRY(check_ptr(out->sel_union, "out.sel_union", false));
+  SAS_TRY(check_ptr(out->ref_union, "out.ref_union", false));
+  if (seq_len > ATTN_MAX_SEQ) return fail(SAS_ERR_UNSUPPORTED, "seq_len %d (supported <= %d)", seq_len, ATTN_MAX_SEQ);
+  Carve cv(ws);
+  StatsWs w = carve_stats(cv, c, batch, seq_len);
+  SAS_TRY(check_ws(ws, ws_bytes, cv.off));
+  hipStream_t s = (hipStream_t)stream;
+  const int n = seq_len, Hkv = c->n_kv_heads, NB = (int)cdiv(n, c->block_size);
+  const int K = c->top_k > 0 ? c->top_k : 0;
+  if (out->sel_union && walk) {
+    Timed tm("stats_union", s);
+    HIP_TRY(launch_sel_union(in->sel_idx, (size_t)batch * Hkv * n, K, NB, out->sel_union, s), "selection union");
+  }
+  if (!out->cov && !out->cov_v && !out->ref_union) return SAS_OK;
+  if (out->cov_v) {
+    Timed tm("stats_vnorm", s);
+    HIP_TRY(launch_vnorm(c->dtype, in->v, (size_t)batch * n * Hkv, c->head_dim, w.lvn, s), "value norms");
+  } else {
+    HIP_TRY(launch_fill_f32(w.lvn, (size_t)batch * n * Hkv, 0.f, s), "value norms");
+  }
+  StatsArgs a = {};
+  a.b = batch;
+  a.n = n;
+  a.H = c->n_heads;
+  a.Hkv = Hkv;
+  a.dh = c->head_dim;
+  a.B = c->block_size;
+  a.K = walk ? K : 0;
+  a.mode = c->mode;
+  a.sm_scale = sm_scale_of(c);
+  a.Q = in->q;
+  a.Kt = in->k;
+  a.sel = walk ? in->sel_idx : nullptr;
+  a.lvn = w.lvn;
+  a.cov = out->cov;
+  a.cov_v = out->cov_v;
+  a.blk_lse = out->ref_union ? w.blk_lse : nullptr;
+  {
+    Timed tm("stats", s);
+    HIP_TRY(launch_stats(c->dtype, a, s), "selection stats");
+  }
+  if (out->ref_union) {
+    Timed tm("stats_reference", s);
+    HIP_TRY(launch_ref_sets(w.blk_lse, batch, n, c->n_heads, Hkv, c->block_size, K, w.head_mask, out->ref_union, s),
+            "reference sets");
+  }
+  return SAS_OK;
+}
+
+sas_status sas_overlap_recall(int64_t words, const uint32_t* sel_union, const uint32_t* ref_union, uint64_t* counts,
+                              void* stream) {
+  if (words < 0) return fail(SAS_ERR_INVALID_ARGUMENT, "words %lld is negative", (long long)words);
+  SAS_TRY(check_ptr(sel_union, "sel_union", words > 0));
+  SAS_TRY(check_ptr(ref_union, "ref_union", words > 0));
+  SAS_TRY(check_ptr(counts, "counts", true));
+  HIP_TRY(launch_overlap_count(sel_union, ref_union, (size_t)words, (unsigned long long*)counts, (hipStream_t)stream),
+          "overlap counts");
   return SAS_OK;
 }
 

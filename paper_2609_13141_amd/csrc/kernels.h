@@ -157,6 +157,30 @@ hipError_t launch_small_gemm(int dtype, const SmallGemm& g, hipStream_t s);
 // out[zo, e] = sum_{u < U} sum_{q < S} part[((u ZO + zo) S + q) E + e]
 hipError_t launch_partial_sum(const float* part, int U, int ZO, int S, size_t E, float* out, hipStream_t s);
 
+// ---- stats.hip -------------------------------------------------------------
+// lvn[r] = log2 ||v_r|| over rows of dh values
+hipError_t launch_vnorm(int dtype, const void* V, size_t rows, int dh, float* lvn, hipStream_t s);
+struct StatsArgs {
+  int b, n, H, Hkv, dh, B, K, mode;
+  float sm_scale;
+  const void* Q;          // [b, n, H, dh]
+  const void* Kt;         // [b, n, Hkv, dh]
+  const int32_t* sel;     // [b, Hkv, n, K] (unused in DENSE)
+  const float* lvn;       // [b, n, Hkv] log2 of the value norms
+  float* cov;             // [b, H, n] or null
+  float* cov_v;           // [b, H, n] or null
+  float* blk_lse;         // [b, H, n, NB] log2 mass of each historical block, or null
+};
+hipError_t launch_stats(int dtype, const StatsArgs& a, hipStream_t s);
+// per-head Top-K by block mass -> head_mask [b, H, n, W]; majority per group OR-ed into uni [b, Hkv, n, W]
+hipError_t launch_ref_sets(const float* blk_lse, int b, int n, int H, int Hkv, int B, int K, uint32_t* head_mask,
+                           uint32_t* uni, hipStream_t s);
+// OR the selection rows into uni [rows, W]
+hipError_t launch_sel_union(const int32_t* sel, size_t rows, int K, int NB, uint32_t* uni, hipStream_t s);
+// counts[0] = |a & b|, counts[1] = |b| over `words` words
+hipError_t launch_overlap_count(const uint32_t* a, const uint32_t* b, size_t words, unsigned long long* counts,
+                                hipStream_t s);
+
 // ---- decode.hip ------------------------------------------------------------
 // rope[r, i] for the positions pos[r] of the new tokens (fp64 math).
 hipError_t launch_rope_rows(const int32_t* pos, float2* rope, int b, int dh, float base, hipStream_t s);

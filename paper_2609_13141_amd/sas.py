@@ -24,11 +24,11 @@ GATE_POS = {"inner": 0, "outer": 1}
 GATE_ACT = {"softmax": 0, "sigmoid": 1, "raw": 2}
 SCOPES = {"sparse": 0, "full": 1}
 (OP_ATTENTION, OP_MLP, OP_LAYER, OP_DECODE, OP_LM_HEAD, OP_DECODE_SELECT, OP_ATTENTION_BACKWARD,
- OP_SELECTOR_BACKWARD) = range(8)
+ OP_SELECTOR_BACKWARD, OP_SELECTION_STATS) = range(9)
 TORCH_DTYPE = {"bf16": torch.bfloat16, "f32": torch.float32}
 
 EXPORTS = ("sas_workspace_size", "sas_attention_prefill", "sas_mlp_forward", "sas_layer_forward",
-           "sas_decode_step", "sas_decode_select", "sas_attention_backward", "sas_selector_backward", "sas_embed", "sas_lm_head_argmax", "sas_last_error", "sas_version",
+           "sas_decode_step", "sas_decode_select", "sas_attention_backward", "sas_selector_backward", "sas_selection_stats", "sas_overlap_recall", "sas_embed", "sas_lm_head_argmax", "sas_last_error", "sas_version",
            "sas_profiler_start", "sas_profiler_stop", "sas_profiler_record")
 
 
@@ -62,6 +62,14 @@ class BwdIn(C.Structure):
 
 class BwdOut(C.Structure):
     _fields_ = [(f, C.c_void_p) for f in ("dq", "dk", "dv", "dlog_gate", "dlog_gate_full")]
+
+
+class StatsIn(C.Structure):
+    _fields_ = [(f, C.c_void_p) for f in ("q", "k", "v", "sel_idx")]
+
+
+class StatsOut(C.Structure):
+    _fields_ = [(f, C.c_void_p) for f in ("cov", "cov_v", "sel_union", "ref_union")]
 
 
 class SelBwdIn(C.Structure):
@@ -118,6 +126,14 @@ def lib() -> C.CDLL:
     L.sas_attention_backward.restype = i32
     L.sas_attention_backward.argtypes = [C.POINTER(Config), i32, i32, C.POINTER(BwdIn), C.POINTER(BwdOut), vp, sz,
                                          vp]
+    L.sas_selector_backward.restype = i32
+    L.sas_selector_backward.argtypes = [C.POINTER(Config), i32, i32, C.POINTER(SelBwdIn), C.POINTER(SelBwdOut), vp,
+                                        sz, vp]
+    L.sas_selection_stats.restype = i32
+    L.sas_selection_stats.argtypes = [C.POINTER(Config), i32, i32, C.POINTER(StatsIn), C.POINTER(StatsOut), vp, sz,
+                                      vp]
+    L.sas_overlap_recall.restype = i32
+    L.sas_overlap_recall.argtypes = [C.c_int64, vp, vp, vp, vp]
     L.sas_embed.restype = i32
     L.sas_embed.argtypes = [C.POINTER(Config), i32, i32, vp, vp, i32, vp, i32, vp, vp]
     L.sas_lm_head_argmax.restype = i32
@@ -268,6 +284,43 @@ def selector_backward(cfg: Config, q, k, sel_idx, log_gate, dlog_gate, w_gq=None
     wsp, wsn = _ws(ws, workspace_size(cfg, OP_SELECTOR_BACKWARD, b, n))
     _check(lib().sas_selector_backward(C.byref(cfg), b, n, C.byref(si), C.byref(so), wsp, wsn, _stream()))
     return out
+
+
+def union_words(cfg: Config, n: int) -> int:
+    """uint32 words per (query, group) row of a block bitmask."""
+    return -(-(-(-n // cfg.block_size)) // 32)
+
+
+def alloc_union(cfg: Config, b: int, n: int, device="cuda"):
+    """Zeroed block bitmask [b, Hkv, n, W] (int32 storage of uint32 words)."""
+    return torch.zeros(b, cfg.n_kv_heads, n, union_words(cfg, n), dtype=torch.int32, device=device)
+
+
+def selection_stats(cfg: Config, q, k, v=None, sel_idx=None, *, cov: bool = True, cov_v: bool = True,
+                    sel_union=None, ref_union=None, ws: Workspace | None = None) -> dict:
+    """Mass coverage (cov, cov_v [b,H,n]) of the attended sets and OR-accumulation
+    of the selected / full-attention reference block sets into the given
+    bitmasks (see alloc_union)."""
+    b, n, H, dh = q.shape
+    out = {}
+    if cov:
+        out["cov"] = torch.empty(b, H, n, dtype=torch.float32, device=q.device)
+    if cov_v:
+        out["cov_v"] = torch.empty(b, H, n, dtype=torch.float32, device=q.device)
+    si = StatsIn(*[_ptr(t) for t in (q, k, v, sel_idx)])
+    so = StatsOut(_ptr(out.get("cov")), _ptr(out.get("cov_v")), _ptr(sel_union), _ptr(ref_union))
+    wsp, wsn = _ws(ws, workspace_size(cfg, OP_SELECTION_STATS, b, n))
+    _check(lib().sas_selection_stats(C.byref(cfg), b, n, C.byref(si), C.byref(so), wsp, wsn, _stream()))
+    return out
+
+
+def overlap_recall(sel_union, ref_union):
+    """Eq. overlap_recall of two accumulated bitmasks: (|I n I*|, |I*|, recall)."""
+    counts = torch.empty(2, dtype=torch.int64, device=sel_union.device)
+    _check(lib().sas_overlap_recall(C.c_int64(sel_union.numel()), _ptr(sel_union), _ptr(ref_union), _ptr(counts),
+                                    _stream()))
+    inter, tot = (int(x) for x in counts.cpu())
+    return inter, tot, (inter / tot if tot else float("nan"))
 
 
 def mlp_forward(cfg: Config, x, W: dict, ws: Workspace | None = None):
