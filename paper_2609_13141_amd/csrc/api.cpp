@@ -152,6 +152,7 @@ struct AttnWs {
   int32_t* sel;
   float* sel_bias;
   float* gate_table;  // log gates of every block (full scope, when the caller does not ask for them)
+  float* row_lse;     // per-row LSE of the scores while the log-gate table is finished
 };
 
 AttnWs carve_attention(Carve& cv, const sas_config* c, int b, int n) {
@@ -168,6 +169,7 @@ AttnWs carve_attention(Carve& cv, const sas_config* c, int b, int n) {
   w.sel = (int32_t*)cv.take(rows * 4);
   w.sel_bias = (float*)cv.take(rows * 4);
   w.gate_table = full_fwd(c) ? (float*)cv.take((size_t)b * c->n_kv_heads * n * NB * 4) : nullptr;
+  w.row_lse = (float*)cv.take((size_t)b * c->n_kv_heads * n * 4);
   return w;
 }
 
@@ -254,6 +256,7 @@ sas_status run_attention(const sas_config* c, int b, int n, const void* q, const
     sa.tau = tau;
     sa.noise = noise;
     sa.act = gated_of(c) ? c->gate_act : SAS_ACT_SOFTMAX;
+    sa.row_lse = ws.row_lse;
     {
       Timed tm("select", s);
       HIP_TRY(launch_select(c->dtype, sa, s), "select");

@@ -73,6 +73,7 @@ struct SelectArgs {
   float* tau;             // [b, Hkv, n] optional
   const float* noise;     // [b, Hkv, n, NB] added to the scores (optional)
   int act;                // sas_gate_act
+  float* row_lse;         // [b, Hkv, n] scratch (required with log_gate)
 };
 hipError_t launch_select(int dtype, const SelectArgs& a, hipStream_t s);
 

@@ -139,14 +139,31 @@ hipError_t launch_block_summaries(int dtype, const void* K, int b, int n, int Hk
 }
 
 // ---------------------------------------------------------------------------
-// Selection: one wave per 64 consecutive query rows of one (batch, group).
-constexpr int SEL_MC = 16;  // summaries staged in LDS per step
+// Selection: one workgroup of SEL_NW waves per 64 consecutive query rows of
+// one (batch, group); lane = query row.  The 64 gate queries are staged in
+// LDS once; the waves split the historical blocks into contiguous ranges and
+// walk theirs in chunks of SEL_MC summaries staged in LDS as fp64 (one exact
+// fp64 FMA chain per (row, block), j ascending), each keeping a register
+// Top-K and a running LSE.  The waves' lists are then merged into wave 0's in
+// wave order, which reproduces a single ascending scan (strict comparisons
+// keep the lower block first on equal scores).
+constexpr int SEL_MC = 8;   // summaries per wave per step
+constexpr int SEL_NW = 4;   // waves per workgroup
+
+__device__ __forceinline__ void lds_fence() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
 template <typename T, int DH, int KMAX>
-__global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
-  __shared__ __align__(16) float kb[SEL_MC][DH];       // summaries of the current chunk
-  __shared__ __align__(16) T qs[WAVE][DH + 8];         // this wave's 64 gate queries
-  const int lane = threadIdx.x;
+__global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
+  constexpr int KB_BYTES = SEL_NW * SEL_MC * DH * 8;
+  constexpr int MG_BYTES = KMAX * WAVE * 12 + WAVE * 8 + WAVE * 4;
+  __shared__ __align__(16) unsigned char pool[KB_BYTES > MG_BYTES ? KB_BYTES : MG_BYTES];
+  __shared__ __align__(16) T qs[WAVE][DH + 8];  // the 64 gate queries
+  double(*kb)[SEL_MC][DH] = (double(*)[SEL_MC][DH])pool;            // [SEL_NW][SEL_MC][DH]
+  double* mg_r = (double*)pool;                                      // merge: [KMAX][WAVE] keys
+  int* mg_m = (int*)(pool + KMAX * WAVE * 8);                        // [KMAX][WAVE] blocks
+  double* mg_mx = (double*)(pool + KMAX * WAVE * 12);                // [WAVE] running max
+  float* mg_l = (float*)(pool + KMAX * WAVE * 12 + WAVE * 8);        // [WAVE] running sum
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = blockIdx.y, bi = blockIdx.z;
   const int t0 = blockIdx.x * WAVE;
   const int t = t0 + lane;
@@ -154,19 +171,24 @@ __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
   const int G = P.H / P.Hkv;
   const int ct = valid ? t / P.B : 0;
   const int t_last = min(P.n - 1, t0 + WAVE - 1);
-  const int cmax = t_last / P.B;  // wave-uniform loop bound
+  const int cmax = t_last / P.B;  // workgroup-uniform block count
   const double den = (double)G * sqrt((double)DH);  // s = r / (G sqrt(dh))
   const double inv_scale = 1.0 / den;
-  const float* noise = (P.noise && valid) ? P.noise + (((size_t)bi * P.Hkv + g) * P.n + t) * P.NB : nullptr;
+  const size_t row = ((size_t)bi * P.Hkv + g) * P.n + t;
+  const float* noise = (P.noise && valid) ? P.noise + row * P.NB : nullptr;
+  // the log-gate table row of this query: raw scores written as they are computed (softmax:
+  // the LSE is subtracted at the end), the other activations' gates written directly
+  float* lgrow = (P.log_gate && valid) ? P.log_gate + row * P.NB : nullptr;
+  const int act = P.act;
 
   // stage the 64 gate queries: either the precomputed (projected) rows, or
   // the group's query heads summed here in fp64 and rounded once
   {
     constexpr int NC = DH / 8;  // 8-value chunks per row
     const int rows = t_last - t0 + 1;
-#pragma unroll 4
-    for (int i = 0; i < NC; ++i) {
-      const int c = lane + i * WAVE;
+#pragma unroll
+    for (int i = 0; i < NC / SEL_NW; ++i) {
+      const int c = tid + i * SEL_NW * WAVE;
       const int r = c / NC, c8 = c % NC;
       const int rr = min(r, rows - 1);
       double acc[8];
@@ -190,6 +212,7 @@ __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
       for (int e = 0; e < 8; ++e) qs[r][c8 * 8 + e] = r < rows ? Act<T>::from_f64(acc[e]) : Act<T>::from_f32(0.f);
     }
   }
+  __syncthreads();
 
   double tr[KMAX];
   int tm[KMAX];
@@ -200,11 +223,26 @@ __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
   }
   double mrun = -DBL_MAX;  // running max of s
   float lrun = 0.f;        // running sum of exp(s - mrun)
+  auto insert = [&](double cr, int cm) {
+    if (!(cr > tr[KMAX - 1])) return;
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) {
+      const bool better = cr > tr[i];  // strict: an equal key keeps the earlier (lower) block ahead
+      const double orr = tr[i];
+      const int om = tm[i];
+      tr[i] = better ? cr : orr;
+      tm[i] = better ? cm : om;
+      cr = better ? orr : cr;
+      cm = better ? om : cm;
+    }
+  };
 
   const T* kbar = (const T*)P.kbar + ((size_t)bi * P.Hkv + g) * (size_t)P.NB * DH;
-  for (int m0 = 0; m0 < cmax; m0 += SEL_MC) {
-    const int mc = min(SEL_MC, cmax - m0);
-    __syncthreads();
+  const int per = (cmax + SEL_NW - 1) / SEL_NW;
+  const int mb = wave * per, me = min(cmax, mb + per);
+  double(*kw)[DH] = kb[wave];
+  for (int m0 = mb; m0 < me; m0 += SEL_MC) {
+    const int mc = min(SEL_MC, me - m0);
     {
       constexpr int NC = DH / 8;
 #pragma unroll
@@ -214,26 +252,24 @@ __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
         Vec8<T> v;
         v.load(kbar + (size_t)(m0 + min(r, mc - 1)) * DH + c8 * 8);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) kb[r][c8 * 8 + e] = r < mc ? v.get(e) : 0.f;
+        for (int e = 0; e < 8; ++e) kw[r][c8 * 8 + e] = r < mc ? (double)v.get(e) : 0.0;
       }
     }
-    __syncthreads();
+    lds_fence();
     // r[mm] = sum_j q_j kbar[m0+mm]_j: one fp64 FMA chain per block, j ascending
     double r[SEL_MC];
 #pragma unroll
     for (int mm = 0; mm < SEL_MC; ++mm) r[mm] = 0.0;
-    for (int j = 0; j < DH; j += 4) {
+    for (int j = 0; j < DH; j += 2) {
       const double q0 = Act<T>::to_f32(qs[lane][j]), q1 = Act<T>::to_f32(qs[lane][j + 1]);
-      const double q2 = Act<T>::to_f32(qs[lane][j + 2]), q3 = Act<T>::to_f32(qs[lane][j + 3]);
 #pragma unroll
       for (int mm = 0; mm < SEL_MC; ++mm) {
-        const float4 k4 = *(const float4*)&kb[mm][j];
-        r[mm] = fma(q0, (double)k4.x, r[mm]);
-        r[mm] = fma(q1, (double)k4.y, r[mm]);
-        r[mm] = fma(q2, (double)k4.z, r[mm]);
-        r[mm] = fma(q3, (double)k4.w, r[mm]);
+        const double2 k2 = *(const double2*)&kw[mm][j];
+        r[mm] = fma(q0, k2.x, r[mm]);
+        r[mm] = fma(q1, k2.y, r[mm]);
       }
     }
+    lds_fence();  // this wave's reads of the chunk are done before it is restaged
 #pragma unroll
     for (int mm = 0; mm < SEL_MC; ++mm) {
       const int m = m0 + mm;
@@ -241,31 +277,49 @@ __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
       // ranking key: the raw score r, or the noisy score s + noise when noise is given
       const double sv = noise ? r[mm] / den + (double)noise[m] : r[mm] * inv_scale;
       const double rv = noise ? sv : r[mm];
+      if (lgrow) {
+        double gv = sv;
+        if (act == SAS_ACT_SIGMOID) gv = sv >= 0.0 ? -log1p(exp(-sv)) : sv - log1p(exp(sv));
+        lgrow[m] = (float)gv;
+      }
       if (sv > mrun) {
         lrun = lrun * expf((float)(mrun - sv)) + 1.f;
         mrun = sv;
       } else {
         lrun += expf((float)(sv - mrun));
       }
-      if (rv > tr[KMAX - 1]) {
-        double cr = rv;
-        int cm = m;
-#pragma unroll
-        for (int i = 0; i < KMAX; ++i) {
-          const bool better = cr > tr[i];  // strict: an equal key keeps the lower index ahead
-          const double orr = tr[i];
-          const int om = tm[i];
-          tr[i] = better ? cr : orr;
-          tm[i] = better ? cm : om;
-          cr = better ? orr : cr;
-          cm = better ? om : cm;
-        }
-      }
+      insert(rv, m);
     }
   }
-  if (!valid) return;
+  __syncthreads();
+  // merge the other waves' lists into wave 0's, in wave order
+  for (int w = 1; w < SEL_NW; ++w) {
+    if (wave == w) {
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i) {
+        mg_r[i * WAVE + lane] = tr[i];
+        mg_m[i * WAVE + lane] = tm[i];
+      }
+      mg_mx[lane] = mrun;
+      mg_l[lane] = lrun;
+    }
+    __syncthreads();
+    if (wave == 0) {
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i) insert(mg_r[i * WAVE + lane], mg_m[i * WAVE + lane]);
+      const double om = mg_mx[lane];
+      const float ol = mg_l[lane];
+      if (om > mrun) {
+        lrun = lrun * expf((float)(mrun - om)) + ol;
+        mrun = om;
+      } else if (ol > 0.f) {
+        lrun += ol * expf((float)(om - mrun));
+      }
+    }
+    __syncthreads();
+  }
+  if (wave != 0 || !valid) return;
   const double lse = (ct > 0) ? mrun + log((double)lrun) : 0.0;
-  const int act = P.act;
   auto log_gate_of = [&](double key) -> double {  // log g of a block from its ranking key
     const double sv = noise ? key : key * inv_scale;
     if (act == SAS_ACT_SOFTMAX) return sv - lse;
@@ -274,7 +328,6 @@ __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
   };
   const int K = P.K;
   const int kk = min(K, ct);
-  const size_t row = ((size_t)bi * P.Hkv + g) * P.n + t;
 
   if (P.tau) {
     float tau;
@@ -317,39 +370,42 @@ __global__ void __launch_bounds__(64) select_kernel(SelectArgs P) {
     }
   }
 
-  if (P.log_gate) {
-    // every historical block's log gate: the scores again, same summation order
-    float* lg = P.log_gate + row * P.NB;
-    for (int m = 0; m < P.NB; ++m) {
-      float v = -INFINITY;
-      if (m < ct) {
-        const T* kr = kbar + (size_t)m * DH;
-        double acc = 0.0;
-        for (int j = 0; j < DH; ++j)
-          acc = fma((double)Act<T>::to_f32(qs[lane][j]), (double)Act<T>::to_f32(kr[j]), acc);
-        v = (float)log_gate_of(noise ? acc / den + (double)noise[m] : acc);
-      }
-      lg[m] = v;
-    }
-  }
+  if (lgrow) P.row_lse[row] = (float)lse;  // finish_table_kernel subtracts it (softmax)
+}
+
+// finish the log-gate table: softmax gates are the written scores minus the
+// row's LSE; blocks m >= C_t are not historical (-inf)
+__global__ void finish_table_kernel(float* __restrict__ table, const float* __restrict__ row_lse, size_t rows,
+                                    int n, int B, int NB, int softmax) {
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= rows * NB) return;
+  const size_t row = idx / NB;
+  const int m = (int)(idx % NB), ct = (int)(row % n) / B;
+  table[idx] = m < ct ? (softmax ? table[idx] - row_lse[row] : table[idx]) : -INFINITY;
 }
 
 template <typename T, int DH>
 static void run_select(const SelectArgs& a, hipStream_t s) {
   dim3 grid(cdiv(a.n, WAVE), a.Hkv, a.b);
-  if (a.K <= 8) select_kernel<T, DH, 8><<<grid, WAVE, 0, s>>>(a);
-  else if (a.K <= 16) select_kernel<T, DH, 16><<<grid, WAVE, 0, s>>>(a);
-  else select_kernel<T, DH, 32><<<grid, WAVE, 0, s>>>(a);
+  if (a.K <= 8) select_kernel<T, DH, 8><<<grid, SEL_NW * WAVE, 0, s>>>(a);
+  else if (a.K <= 16) select_kernel<T, DH, 16><<<grid, SEL_NW * WAVE, 0, s>>>(a);
+  else select_kernel<T, DH, 32><<<grid, SEL_NW * WAVE, 0, s>>>(a);
 }
 
 hipError_t launch_select(int dtype, const SelectArgs& a, hipStream_t s) {
   if (a.n <= 0 || a.b <= 0) return hipSuccess;
+  if (a.log_gate && !a.row_lse) return hipErrorInvalidValue;
   if (dtype == SAS_BF16) {
     if (a.dh == 128) run_select<bf16_t, 128>(a, s);
     else run_select<bf16_t, 64>(a, s);
   } else {
     if (a.dh == 128) run_select<float, 128>(a, s);
     else run_select<float, 64>(a, s);
+  }
+  if (a.log_gate) {
+    const size_t rows = (size_t)a.b * a.Hkv * a.n;
+    finish_table_kernel<<<(unsigned)cdiv(rows * a.NB, 256), 256, 0, s>>>(a.log_gate, a.row_lse, rows, a.n, a.B, a.NB,
+                                                                          a.act == SAS_ACT_SOFTMAX);
   }
   return hipGetLastError();
 }
