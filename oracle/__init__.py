@@ -36,6 +36,9 @@ Parity status of each part (how it is pinned by the oracle self-tests):
   the group majority vote, overlap recall): pinned against torch softmax
   masses and torch.topk, closed forms (q = 0, every block kept, equal value
   norms) and hand-worked votes and recalls.
+* packed documents (varlen): a one-document table reproduces the unpacked
+  oracle; packed rows match torch autograd on a dense masked formulation with
+  a block-diagonal document mask; documents are independent.
 * normalized log gate, Top-K, attention: pinned by closed forms (q = 0),
   V = const, reductions to textbook causal / block-local attention computed
   by torch's scaled_dot_product_attention, causality, shift invariance and
@@ -49,6 +52,7 @@ from .backward import sas_attention_backward, gate_backward, selector_backward
 from .variants import (log_gates, select_variant, variant_attention, variant_attention_backward,
                        gate_backward_act)
 from .stats import mass_coverage, block_mass_topk, majority_vote, selection_sets, overlap_recall
+from .varlen import doc_spans, select_packed, attention_packed, backward_packed, coverage_packed
 from .layer import (Spec, layer_forward, mlp_forward, attention_prefill,
                     DecodeCache, decode_step, decode_select, embed_tokens, lm_head_argmax)
 
@@ -61,5 +65,5 @@ __all__ = [
     "sas_attention_backward", "gate_backward", "selector_backward",
     "log_gates", "select_variant", "variant_attention", "variant_attention_backward",
     "gate_backward_act", "mass_coverage", "block_mass_topk", "majority_vote", "selection_sets",
-    "overlap_recall",
+    "overlap_recall", "doc_spans", "select_packed", "attention_packed", "backward_packed", "coverage_packed",
 ]
