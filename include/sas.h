@@ -122,7 +122,16 @@ typedef struct {
  * score_noise [b, Hkv, n, ceil(n/B)] fp32 or NULL: added to the selector
  * scores s before the gate activation and before Top-K (the noisy "full*"
  * scope of Table 1); with noise the Top-K ranks s + noise (s evaluated in
- * fp64 as r / (G sqrt(dh))), without it the raw scores r. */
+ * fp64 as r / (G sqrt(dh))), without it the raw scores r.
+ * doc_first_block [b, ceil(n/B)] int32 or NULL: variable-length packing of
+ * several documents into one row.  Entry m is the first block of the
+ * document that block m belongs to (non-decreasing, <= m).  Documents start
+ * on block boundaries (every document but a row's last is a whole number of
+ * blocks long).  A query's context, historical blocks, selection and
+ * normalizer are those of its own document; NULL = one document per row.
+ * The table is not checked (it is device memory): entries outside [0, m]
+ * are clamped into it, and a table that breaks the rules above gives
+ * unspecified (but in-bounds) results. */
 typedef struct {
   const void* q;
   const void* k;
@@ -130,6 +139,7 @@ typedef struct {
   const void* w_gq;
   const void* w_gk;
   const float* score_noise;
+  const int32_t* doc_first_block;
 } sas_attn_in;
 
 /* Attention outputs.  NB = ceil(n / B).
@@ -230,6 +240,7 @@ typedef struct {
   const float* lse;
   const int32_t* sel_idx;
   const float* log_gate;
+  const int32_t* doc_first_block;  /* the forward's packing table or NULL */
 } sas_bwd_in;
 
 /* Outputs of sas_attention_backward: dq [b,n,H,dh], dk, dv [b,n,Hkv,dh]
@@ -279,6 +290,7 @@ typedef struct {
   const float* log_gate;
   const float* dlog_gate;
   const float* dlog_gate_full;
+  const int32_t* doc_first_block;  /* the forward's packing table or NULL */
 } sas_sel_bwd_in;
 
 /* Outputs of sas_selector_backward, all fp32, each optional except as noted:
@@ -322,6 +334,7 @@ typedef struct {
   const void* k;
   const void* v;
   const int32_t* sel_idx;
+  const int32_t* doc_first_block;  /* packing table (as in sas_attn_in) or NULL */
 } sas_stats_in;
 
 /* Outputs of sas_selection_stats, each optional.  W = ceil(ceil(n/B)/32).

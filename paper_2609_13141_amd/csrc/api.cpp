@@ -221,7 +221,8 @@ LayerWs carve_layer(Carve& cv, const sas_config* c, int b, int n) {
 sas_status run_attention(const sas_config* c, int b, int n, const void* q, const void* k, const void* v,
                          const void* w_gq, const void* w_gk, void* o, float* lse, void* k_summary,
                          int32_t* sel_idx, float* log_gate, float* tau, const AttnWs& ws,
-                         hipStream_t s, bool need_summary = false, const float* noise = nullptr) {
+                         hipStream_t s, bool need_summary = false, const float* noise = nullptr,
+                         const int32_t* doc = nullptr) {
   const int NB = cdiv(n, c->block_size);
   const int H = c->n_heads, Hkv = c->n_kv_heads, dh = c->head_dim;
   const bool need_sel = c->mode != SAS_MODE_DENSE || sel_idx || log_gate || tau || k_summary || need_summary;
@@ -257,6 +258,7 @@ sas_status run_attention(const sas_config* c, int b, int n, const void* q, const
     sa.noise = noise;
     sa.act = gated_of(c) ? c->gate_act : SAS_ACT_SOFTMAX;
     sa.row_lse = ws.row_lse;
+    sa.doc = doc;
     {
       Timed tm("select", s);
       HIP_TRY(launch_select(c->dtype, sa, s), "select");
@@ -283,6 +285,7 @@ sas_status run_attention(const sas_config* c, int b, int n, const void* q, const
   aa.outer = gated_of(c) && c->gate_pos == SAS_GATE_OUTER;
   aa.full = full_fwd(c);
   aa.gate_table = log_gate;
+  aa.doc = doc;
   {
     Timed tm("attention", s);
     HIP_TRY(launch_attention(c->dtype, aa, s), "attention");
@@ -713,6 +716,7 @@ sas_status sas_attention_backward(const sas_config* c, int32_t batch, int32_t se
   a.ste = gated && c->gate_ste;
   a.dlog_gate_full = fullg ? out->dlog_gate_full : nullptr;
   a.dlg_head_full = bw.dlg_head_full;
+  a.doc = in->doc_first_block;
   {
     Timed tm("bwd_zero", s);
     if (out->dlog_gate && !slots) HIP_TRY(launch_fill_f32(out->dlog_gate, rows * K, 0.f, s), "zero dlog_gate");
@@ -785,7 +789,8 @@ sas_status sas_selector_backward(const sas_config* c, int32_t batch, int32_t seq
   {
     Timed tm("sel_bwd_ds", s);
     HIP_TRY(launch_selector_ds(slots ? in->sel_idx : nullptr, in->log_gate, in->dlog_gate, dfull,
-                               gated_of(c) ? c->gate_act : SAS_ACT_SOFTMAX, batch, n, Hkv, slots ? K : 0, B, ds, s),
+                               gated_of(c) ? c->gate_act : SAS_ACT_SOFTMAX, batch, n, Hkv, slots ? K : 0, B, ds,
+                               in->doc_first_block, s),
             "ds");
   }
   // s = r / (G sqrt(dh)) with r = qhat . kbar
@@ -884,13 +889,15 @@ sas_status sas_selection_stats(const sas_config* c, int32_t batch, int32_t seq_l
   a.cov = out->cov;
   a.cov_v = out->cov_v;
   a.blk_lse = out->ref_union ? w.blk_lse : nullptr;
+  a.doc = in->doc_first_block;
   {
     Timed tm("stats", s);
     HIP_TRY(launch_stats(c->dtype, a, s), "selection stats");
   }
   if (out->ref_union) {
     Timed tm("stats_reference", s);
-    HIP_TRY(launch_ref_sets(w.blk_lse, batch, n, c->n_heads, Hkv, c->block_size, K, w.head_mask, out->ref_union, s),
+    HIP_TRY(launch_ref_sets(w.blk_lse, batch, n, c->n_heads, Hkv, c->block_size, K, w.head_mask, out->ref_union,
+                            in->doc_first_block, s),
             "reference sets");
   }
   return SAS_OK;
@@ -919,6 +926,7 @@ sas_status sas_attention_prefill(const sas_config* c, int32_t batch, int32_t seq
   SAS_TRY(check_ptr(in->w_gq, "in.w_gq", false));
   SAS_TRY(check_ptr(in->w_gk, "in.w_gk", false));
   SAS_TRY(check_ptr(in->score_noise, "in.score_noise", false));
+  SAS_TRY(check_ptr(in->doc_first_block, "in.doc_first_block", false));
   SAS_TRY(check_ptr(out->o, "out.o", true));
   SAS_TRY(check_ptr(out->lse, "out.lse", false));
   SAS_TRY(check_ptr(out->k_summary, "out.k_summary", false));
@@ -930,7 +938,7 @@ sas_status sas_attention_prefill(const sas_config* c, int32_t batch, int32_t seq
   SAS_TRY(check_ws(ws, ws_bytes, cv.off));
   SAS_TRY(run_attention(c, batch, seq_len, in->q, in->k, in->v, in->w_gq, in->w_gk, out->o, out->lse,
                         out->k_summary, out->sel_idx, out->log_gate, out->tau, aw, (hipStream_t)stream, false,
-                        in->score_noise));
+                        in->score_noise, in->doc_first_block));
   return SAS_OK;
 }
 

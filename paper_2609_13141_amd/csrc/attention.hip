@@ -72,6 +72,9 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
   const int last_tile = t_hi / 64;
   const size_t grow = ((size_t)bi * P.Hkv + g) * n;  // first (b, g) row of [b, Hkv, n, ...]
   const int NB = (n + B - 1) / B;
+  const int fb = qvalid ? doc_first(P.doc, bi, NB, t, B) : 0;  // first block of the query's document
+  // the workgroup's earliest document start (queries are ascending): its first possible key tile
+  const int first_tile = doc_first(P.doc, bi, NB, qtile * 128, B) * B / 64;
 
   // Q^T as the B operand: lane supplies Q[t][ks*16 + lk*8 + 0..7]
   bf16x8_t qb[DH / 16];
@@ -89,6 +92,8 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
     const int lo = w * 32;
     uint32_t bits = 0;
     if (every && lo <= last_tile) bits = last_tile - lo >= 31 ? 0xffffffffu : ((1u << (last_tile - lo + 1)) - 1u);
+    if (every && lo + 31 >= first_tile && lo < first_tile) bits &= ~((1u << (first_tile - lo)) - 1u);
+    if (lo + 31 < first_tile) bits = 0;
     need[w] = bits;
   }
   if (Kn > 0 && qvalid) {
@@ -136,7 +141,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
 #pragma unroll
       for (int sb = 0; sb < NSUB; ++sb) {
         const int m = (kt * 64 + (sb << LSB)) / B;
-        r_lg[sb] = (qvalid && m < beta) ? P.gate_table[(grow + t) * NB + m] : 0.f;
+        r_lg[sb] = (qvalid && m < beta && m >= fb) ? P.gate_table[(grow + t) * NB + m] : 0.f;
       }
     }
   };
@@ -180,10 +185,10 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
       const int m = kstart / B;
       float lg = 0.f;
       bool att = false;
-      if (m == beta || P.mode == SAS_MODE_DENSE) {
+      if (m == beta || (P.mode == SAS_MODE_DENSE && m >= fb)) {
         att = true;
       } else if (full) {
-        att = true;
+        att = m >= fb;
         lg = r_lg[sb];
       } else if (m == next_sel) {
         att = true;
@@ -330,11 +335,12 @@ __global__ void attn_f32_kernel(AttnArgs P) {
     return outer ? 0.f : lg;
   };
   const size_t row = ((size_t)bi * P.Hkv + g) * n + t;
+  const int NB = (n + B - 1) / B;
+  const int fb = doc_first(P.doc, bi, NB, t, B);
   if (P.mode == SAS_MODE_DENSE) {
-    for (int i = 0; i <= t; ++i) visit(i, 0.f, 1.f);
+    for (int i = fb * B; i <= t; ++i) visit(i, 0.f, 1.f);
   } else if (gated && P.full) {
-    const int NB = (n + B - 1) / B;
-    for (int m = 0; m < beta; ++m) {
+    for (int m = fb; m < beta; ++m) {
       float w;
       const float bias = gate(P.gate_table[row * NB + m], w);
       for (int i = m * B; i < (m + 1) * B; ++i) visit(i, bias, w);

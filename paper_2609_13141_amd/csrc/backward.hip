@@ -48,7 +48,8 @@ struct BlockGate {
 __device__ BlockGate block_gate(const BwdArgs& P, int bi, int g, int t, int m) {
   BlockGate r = {false, false, 0.f, 1.f, 0.f, -1};
   const int beta = t / P.B;
-  if (m > beta) return r;
+  const int NBr = (P.n + P.B - 1) / P.B;
+  if (m > beta || (m < beta && m < doc_first(P.doc, bi, NBr, t, P.B))) return r;  // outside the document
   if (m == beta || P.mode == SAS_MODE_DENSE) {
     r.att = true;
     return r;
@@ -208,13 +209,14 @@ __global__ void bwd_dlog_gate_sum_kernel(const float* __restrict__ dlg_head, con
 // the same for every block (full scope): 0 for blocks that are not historical
 __global__ void bwd_dlog_gate_full_sum_kernel(const float* __restrict__ dlg_head_full,
                                               const float* __restrict__ log_gate, int ste, int b, int n, int H,
-                                              int Hkv, int B, int NB, float* __restrict__ out) {
+                                              int Hkv, int B, int NB, float* __restrict__ out,
+                                              const int32_t* __restrict__ doc) {
   const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (size_t)b * Hkv * n * NB) return;
   const int m = (int)(idx % NB), t = (int)((idx / NB) % n), g = (int)((idx / ((size_t)NB * n)) % Hkv);
   const int bi = (int)(idx / ((size_t)NB * n * Hkv));
   float s = 0.f;
-  if (m < t / B) {
+  if (m < t / B && m >= doc_first(doc, bi, NB, t, B)) {
     const int G = H / Hkv;
     for (int h = g * G; h < (g + 1) * G; ++h) s += dlg_head_full[(((size_t)bi * H + h) * n + t) * NB + m];
     if (ste) s *= expf(log_gate[idx]);
@@ -308,6 +310,8 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
   const size_t grow = ((size_t)bi * P.Hkv + g) * n;
   const int t_hi = min(n, qtile * 128 + 128) - 1;
   const int last_tile = t_hi / 64;
+  const int fb = qvalid ? doc_first(P.doc, bi, NB, t, B) : 0;  // first block of the query's document
+  const int first_tile = doc_first(P.doc, bi, NB, qtile * 128, B) * B / 64;
 
   bf16x8_t qb[DH / 16], dob[DH / 16];
   {
@@ -331,6 +335,8 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
     const int lo = w * 32;
     uint32_t bits = 0;
     if (every && lo <= last_tile) bits = last_tile - lo >= 31 ? 0xffffffffu : ((1u << (last_tile - lo + 1)) - 1u);
+    if (every && lo + 31 >= first_tile && lo < first_tile) bits &= ~((1u << (first_tile - lo)) - 1u);
+    if (lo + 31 < first_tile) bits = 0;
     need[w] = bits;
   }
   if (Kn > 0 && qvalid) {
@@ -378,7 +384,7 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
 #pragma unroll
       for (int sb = 0; sb < NSUB; ++sb) {
         const int m = (kt * 64 + (sb << LSB)) / B;
-        r_lg[sb] = (qvalid && m < beta) ? P.log_gate[(grow + t) * NB + m] : 0.f;
+        r_lg[sb] = (qvalid && m < beta && m >= fb) ? P.log_gate[(grow + t) * NB + m] : 0.f;
       }
     }
   };
@@ -432,8 +438,10 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
       if (!qvalid || kstart > t) continue;
       const int m = kstart / B;
       float lg = 0.f;
-      if (m == beta || dense) {
+      if (m == beta || (dense && m >= fb)) {
         attb[sb] = true;
+      } else if (m < fb) {
+        // outside the query's document
       } else if (fullatt) {
         attb[sb] = gradb[sb] = true;
         lg = r_lg[sb];
@@ -631,7 +639,9 @@ __global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
   {
     const uint8_t* cm = use_mask ? P.chunk_mask + ((size_t)bi * P.Hkv + g) * nqc * NB : nullptr;
     for (int qc = qc0 + tid; qc < nqc; qc += NTH) {
-      bool any = dense || fullatt || (qc * 32) / B <= m_hi;
+      // the chunk reaches into the tile's current blocks, or (dense / full scope) its
+      // earliest row's document starts at or before the tile's last block
+      bool any = ((dense || fullatt) && doc_first(P.doc, bi, NB, qc * 32, B) <= m_hi) || (qc * 32) / B <= m_hi;
       if (!any && cm)
         for (int m = m_lo; m <= m_hi; ++m) any |= cm[(size_t)qc * NB + m] != 0;
       if (any) atomicOr(&flags[qc >> 5], 1u << (qc & 31));
@@ -666,6 +676,7 @@ __global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
   uint4 rq[QPT], rd[QPT];
   float r_lse = 0.f, r_delta = 0.f, r_lg = 0.f;
   uint32_t r_mw = 0;
+  int r_fb = 0;  // first block of the row's document
 
   auto prefetch = [&](int qc, int hg) {
     const int q0 = qc * 32, h = g * G + hg;
@@ -683,6 +694,7 @@ __global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
     if (bsb < nsb) {
       const int t = q0 + bq, kstart = k0 + (bsb << bshift), m = kstart / B;
       r_lse = t < n ? P.lse[((size_t)bi * H + h) * n + t] : 0.f;
+      r_fb = t < n ? doc_first(P.doc, bi, NB, t, B) : 0;
       if (t < n && kstart <= t && m != t / B) {
         r_mw = use_mask ? P.selmask[(grow + t) * NW + (m >> 5)] : 0u;
         r_lg = gated && (use_mask || fullatt) ? P.log_gate[(grow + t) * NB + m] : 0.f;
@@ -717,9 +729,9 @@ __global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
       const int t = q0 + bq, kstart = k0 + (bsb << bshift), m = kstart / B;
       float bb = -INFINITY, w = 1.f;
       if (t < n && kstart <= t) {
-        if (m == t / B || dense) {
+        if (m == t / B || (dense && m >= r_fb)) {
           bb = 0.f;
-        } else if (fullatt || ((r_mw >> (m & 31)) & 1u)) {
+        } else if ((fullatt && m >= r_fb) || ((r_mw >> (m & 31)) & 1u)) {
           const bool gate = gated && !ste;
           bb = gate && !outer ? r_lg * BLOG2E : 0.f;
           if (gate && outer) w = __builtin_amdgcn_exp2f(r_lg * BLOG2E);
@@ -882,10 +894,12 @@ __global__ void __launch_bounds__(256) selector_ds_kernel(const int32_t* __restr
                                                           const float* __restrict__ log_gate,
                                                           const float* __restrict__ dlog_gate,
                                                           const float* __restrict__ dfull, int act, int rows,
-                                                          int n, int K, int B, int NB, float* __restrict__ ds) {
+                                                          int n, int Hkv, int K, int B, int NB,
+                                                          float* __restrict__ ds, const int32_t* __restrict__ doc) {
   const int row = (int)(((size_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6), lane = threadIdx.x & 63;
   if (row >= rows) return;
   const int C = (row % n) / B;
+  const int F = doc_first(doc, row / (n * Hkv), NB, row % n, B);  // historical blocks are [F, C)
   const float* lg = log_gate + (size_t)row * NB;
   const float* dfr = dfull ? dfull + (size_t)row * NB : nullptr;
   int sk = -1;
@@ -897,7 +911,7 @@ __global__ void __launch_bounds__(256) selector_ds_kernel(const int32_t* __restr
   float D = 0.f;  // sum of the row's log-gate gradient (softmax)
   if (act == SAS_ACT_SOFTMAX) {
     if (dfr) {
-      for (int m = lane; m < C; m += 64) D += dfr[m];
+      for (int m = F + lane; m < C; m += 64) D += dfr[m];
       D = wave_sum(D);
     } else {
       D = wave_sum(dk);
@@ -908,7 +922,7 @@ __global__ void __launch_bounds__(256) selector_ds_kernel(const int32_t* __restr
     const int m = m0 + lane;
     float dl = 0.f;
     if (dfr) {
-      if (m < C) dl = dfr[m];
+      if (m < C && m >= F) dl = dfr[m];
     } else {
       for (int k = 0; k < K; ++k) {  // every lane shuffles (the sources must be active)
         const int s = __shfl(sk, k, 64);
@@ -917,7 +931,7 @@ __global__ void __launch_bounds__(256) selector_ds_kernel(const int32_t* __restr
       }
     }
     float v = 0.f;
-    if (m < C) {
+    if (m < C && m >= F) {
       if (act == SAS_ACT_SOFTMAX) v = dl - expf(lg[m]) * D;
       else if (act == SAS_ACT_SIGMOID) v = dl * (1.f - expf(lg[m]));
       else v = dl;
@@ -928,12 +942,12 @@ __global__ void __launch_bounds__(256) selector_ds_kernel(const int32_t* __restr
 
 hipError_t launch_selector_ds(const int32_t* sel, const float* log_gate, const float* dlog_gate,
                               const float* dlog_gate_full, int act, int b, int n, int Hkv, int K, int B, float* ds,
-                              hipStream_t s) {
+                              const int32_t* doc, hipStream_t s) {
   const int rows = b * Hkv * n;
   if (rows <= 0) return hipSuccess;
   if (K > 64) return hipErrorInvalidValue;
-  selector_ds_kernel<<<cdiv(rows, 4), 256, 0, s>>>(sel, log_gate, dlog_gate, dlog_gate_full, act, rows, n, K, B,
-                                                   cdiv(n, B), ds);
+  selector_ds_kernel<<<cdiv(rows, 4), 256, 0, s>>>(sel, log_gate, dlog_gate, dlog_gate_full, act, rows, n, Hkv, K, B,
+                                                   cdiv(n, B), ds, doc);
   return hipGetLastError();
 }
 
@@ -1072,7 +1086,7 @@ hipError_t launch_attention_backward(int dtype, const BwdArgs& a, hipStream_t s)
     const int NB = cdiv(a.n, a.B);
     const size_t tot = (size_t)a.b * a.Hkv * a.n * NB;
     bwd_dlog_gate_full_sum_kernel<<<(unsigned)cdiv(tot, 256), 256, 0, s>>>(
-        P.dlg_head_full, a.log_gate, a.ste, a.b, a.n, a.H, a.Hkv, a.B, NB, a.dlog_gate_full);
+        P.dlg_head_full, a.log_gate, a.ste, a.b, a.n, a.H, a.Hkv, a.B, NB, a.dlog_gate_full, a.doc);
   }
   return hipGetLastError();
 }

@@ -49,6 +49,13 @@ hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s);
 // weights: rope is a per-row table [M, dh/2]; EPI_F32OUT writes fp32 A W^T.
 hipError_t launch_gemv(const GemmArgs& a, hipStream_t s);
 
+// Variable-length packing: doc[b, NB] holds, for each block, the first block of
+// its document; a query's historical blocks are [doc_first(t), t / B).  The
+// entry is clamped to [0, t / B] so that no table can send an index out of range.
+__device__ __forceinline__ int doc_first(const int32_t* doc, int bi, int NB, int t, int B) {
+  return doc ? min(max(doc[(size_t)bi * NB + t / B], 0), t / B) : 0;
+}
+
 // ---- selector.hip ----------------------------------------------------------
 // Block summaries kbar[b, Hkv, NB, dh] of the complete blocks of K[b, n, Hkv, dh]
 // (mean, fp64 ascending sum, rounded once); incomplete rows zeroed.  When
@@ -74,6 +81,7 @@ struct SelectArgs {
   const float* noise;     // [b, Hkv, n, NB] added to the scores (optional)
   int act;                // sas_gate_act
   float* row_lse;         // [b, Hkv, n] scratch (required with log_gate)
+  const int32_t* doc;     // [b, NB] first block of each block's document, or null
 };
 hipError_t launch_select(int dtype, const SelectArgs& a, hipStream_t s);
 
@@ -91,6 +99,7 @@ struct AttnArgs {
   int outer;              // GATED: the gate weights the values instead of biasing the logits
   int full;               // GATED: every historical block attended, gates from gate_table
   const float* gate_table;  // [b, Hkv, n, NB] log gates (full scope)
+  const int32_t* doc;     // [b, NB] first block of each block's document, or null
 };
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 // longest sequence of the bf16 attention forward (key tiles of 64 tracked in LDS)
@@ -122,6 +131,7 @@ struct BwdArgs {
   int outer, full, ste;
   float* dlog_gate_full;  // [b, Hkv, n, NB] output (full scope / straight-through)
   float* dlg_head_full;   // [b, H, n, NB] scratch (full scope / straight-through)
+  const int32_t* doc;     // [b, NB] first block of each block's document, or null
 };
 // longest sequence of the bf16 attention backward (query chunks of 32 tracked in LDS)
 constexpr int BWD_MAX_SEQ = 262144;
@@ -140,7 +150,7 @@ hipError_t launch_gather_gate(const int32_t* sel, const float* log_gate, int b, 
 // RAW dl_m; for m < t / B (the row's historical blocks), 0 otherwise.
 hipError_t launch_selector_ds(const int32_t* sel, const float* log_gate, const float* dlog_gate,
                               const float* dlog_gate_full, int act, int b, int n, int Hkv, int K, int B, float* ds,
-                              hipStream_t s);
+                              const int32_t* doc, hipStream_t s);
 // C(z, split)[i, j] = alpha sum_{k in split} A(z)[i, k] B(z)[k, j] for z < Z: fp32
 // A, B in the activation dtype, fp32 C; strides in elements.  With splits > 1
 // each split writes its own partial at C + split * sCs.
@@ -171,11 +181,12 @@ struct StatsArgs {
   float* cov;             // [b, H, n] or null
   float* cov_v;           // [b, H, n] or null
   float* blk_lse;         // [b, H, n, NB] log2 mass of each historical block, or null
+  const int32_t* doc;     // [b, NB] first block of each block's document, or null
 };
 hipError_t launch_stats(int dtype, const StatsArgs& a, hipStream_t s);
 // per-head Top-K by block mass -> head_mask [b, H, n, W]; majority per group OR-ed into uni [b, Hkv, n, W]
 hipError_t launch_ref_sets(const float* blk_lse, int b, int n, int H, int Hkv, int B, int K, uint32_t* head_mask,
-                           uint32_t* uni, hipStream_t s);
+                           uint32_t* uni, const int32_t* doc, hipStream_t s);
 // OR the selection rows into uni [rows, W]
 hipError_t launch_sel_union(const int32_t* sel, size_t rows, int K, int NB, uint32_t* uni, hipStream_t s);
 // counts[0] = |a & b|, counts[1] = |b| over `words` words

@@ -170,8 +170,10 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
   const bool valid = t < P.n;
   const int G = P.H / P.Hkv;
   const int ct = valid ? t / P.B : 0;
+  const int fb = valid ? doc_first(P.doc, bi, P.NB, t, P.B) : 0;  // first block of the query's document
   const int t_last = min(P.n - 1, t0 + WAVE - 1);
   const int cmax = t_last / P.B;  // workgroup-uniform block count
+  const int mlo = doc_first(P.doc, bi, P.NB, t0, P.B);  // the rows' earliest document start
   const double den = (double)G * sqrt((double)DH);  // s = r / (G sqrt(dh))
   const double inv_scale = 1.0 / den;
   const size_t row = ((size_t)bi * P.Hkv + g) * P.n + t;
@@ -238,8 +240,8 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
   };
 
   const T* kbar = (const T*)P.kbar + ((size_t)bi * P.Hkv + g) * (size_t)P.NB * DH;
-  const int per = (cmax + SEL_NW - 1) / SEL_NW;
-  const int mb = wave * per, me = min(cmax, mb + per);
+  const int per = (cmax - mlo + SEL_NW - 1) / SEL_NW;
+  const int mb = mlo + wave * per, me = min(cmax, mb + per);
   double(*kw)[DH] = kb[wave];
   for (int m0 = mb; m0 < me; m0 += SEL_MC) {
     const int mc = min(SEL_MC, me - m0);
@@ -273,7 +275,7 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
 #pragma unroll
     for (int mm = 0; mm < SEL_MC; ++mm) {
       const int m = m0 + mm;
-      if (mm >= mc || m >= ct) continue;
+      if (mm >= mc || m >= ct || m < fb) continue;
       // ranking key: the raw score r, or the noisy score s + noise when noise is given
       const double sv = noise ? r[mm] / den + (double)noise[m] : r[mm] * inv_scale;
       const double rv = noise ? sv : r[mm];
@@ -319,7 +321,7 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
     __syncthreads();
   }
   if (wave != 0 || !valid) return;
-  const double lse = (ct > 0) ? mrun + log((double)lrun) : 0.0;
+  const double lse = (ct > fb) ? mrun + log((double)lrun) : 0.0;
   auto log_gate_of = [&](double key) -> double {  // log g of a block from its ranking key
     const double sv = noise ? key : key * inv_scale;
     if (act == SAS_ACT_SOFTMAX) return sv - lse;
@@ -327,11 +329,12 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
     return sv;
   };
   const int K = P.K;
-  const int kk = min(K, ct);
+  const int C = ct - fb;  // historical blocks of the query (its own document)
+  const int kk = min(K, C);
 
   if (P.tau) {
     float tau;
-    if (ct <= K) tau = -INFINITY;
+    if (C <= K) tau = -INFINITY;
     else if (K == 0) tau = INFINITY;
     else {
       double rk = tr[0];
@@ -376,12 +379,13 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
 // finish the log-gate table: softmax gates are the written scores minus the
 // row's LSE; blocks m >= C_t are not historical (-inf)
 __global__ void finish_table_kernel(float* __restrict__ table, const float* __restrict__ row_lse, size_t rows,
-                                    int n, int B, int NB, int softmax) {
+                                    int n, int Hkv, int B, int NB, int softmax, const int32_t* __restrict__ doc) {
   const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= rows * NB) return;
   const size_t row = idx / NB;
-  const int m = (int)(idx % NB), ct = (int)(row % n) / B;
-  table[idx] = m < ct ? (softmax ? table[idx] - row_lse[row] : table[idx]) : -INFINITY;
+  const int t = (int)(row % n), bi = (int)(row / ((size_t)n * Hkv));
+  const int m = (int)(idx % NB), ct = t / B, fb = doc_first(doc, bi, NB, t, B);
+  table[idx] = (m < ct && m >= fb) ? (softmax ? table[idx] - row_lse[row] : table[idx]) : -INFINITY;
 }
 
 template <typename T, int DH>
@@ -404,8 +408,8 @@ hipError_t launch_select(int dtype, const SelectArgs& a, hipStream_t s) {
   }
   if (a.log_gate) {
     const size_t rows = (size_t)a.b * a.Hkv * a.n;
-    finish_table_kernel<<<(unsigned)cdiv(rows * a.NB, 256), 256, 0, s>>>(a.log_gate, a.row_lse, rows, a.n, a.B, a.NB,
-                                                                          a.act == SAS_ACT_SOFTMAX);
+    finish_table_kernel<<<(unsigned)cdiv(rows * a.NB, 256), 256, 0, s>>>(a.log_gate, a.row_lse, rows, a.n, a.Hkv, a.B,
+                                                                          a.NB, a.act == SAS_ACT_SOFTMAX, a.doc);
   }
   return hipGetLastError();
 }

@@ -70,6 +70,8 @@ __global__ void __launch_bounds__(256, 2) stats_bf16_kernel(StatsArgs P) {
   const int last_tile = t_hi / 64;
   const size_t grow = ((size_t)bi * P.Hkv + g) * n;
   const size_t hrow = ((size_t)bi * P.H + h) * n + (qvalid ? t : 0);
+  const int fb = qvalid ? doc_first(P.doc, bi, NB, t, B) : 0;  // the query's document starts at block fb
+  const int first_tile = doc_first(P.doc, bi, NB, qtile * 128, B) * B / 64;
 
   bf16x8_t qb[DH / 16];
   {
@@ -111,8 +113,8 @@ __global__ void __launch_bounds__(256, 2) stats_bf16_kernel(StatsArgs P) {
     const int s0 = sel_s[qrow * KMAX];
     next_sel = s0 >= 0 ? s0 : 0x7fffffff;
   }
-  prefetch(0);
-  for (int kt = 0; kt <= last_tile; ++kt) {
+  prefetch(first_tile);
+  for (int kt = first_tile; kt <= last_tile; ++kt) {
 #pragma unroll
     for (int q = 0; q < KPG; ++q) *(uint4*)(Ks + (kg * KPG + q) * KP + c8 * 8) = rk[q];
     if (tid < 64) lv_s[tid] = rl;
@@ -123,7 +125,7 @@ __global__ void __launch_bounds__(256, 2) stats_bf16_kernel(StatsArgs P) {
 #pragma unroll
     for (int sb = 0; sb < NSUB; ++sb) {
       const int kstart = k0 + (sb << LSB);
-      ctx[sb] = qvalid && kstart <= t;
+      ctx[sb] = qvalid && kstart <= t && kstart / B >= fb;
       inS[sb] = false;
       if (!ctx[sb]) continue;
       const int m = kstart / B;
@@ -238,7 +240,7 @@ __global__ void stats_f32_kernel(StatsArgs P) {
   for (int j = 0; j < DH; ++j) qv[j] = q[j];
   float m_raw = -INFINITY, m_val = -INFINITY, l_all = 0.f, l_S = 0.f, l_vall = 0.f, l_vS = 0.f;
   int cur = 0;
-  for (int m = 0; m <= beta; ++m) {
+  for (int m = doc_first(P.doc, bi, NB, t, B); m <= beta; ++m) {
     bool in = m == beta || P.mode == SAS_MODE_DENSE;
     if (!in && P.K > 0) {
       while (cur < P.K && P.sel[row * P.K + cur] >= 0 && P.sel[row * P.K + cur] < m) ++cur;
@@ -288,12 +290,13 @@ __global__ void stats_f32_kernel(StatsArgs P) {
 // Per-head Top-K historical blocks by block mass (descending, lower block
 // first on ties), as a bitmask row [W words]; one thread per (b, h, t).
 template <int KMAX>
-__global__ void ref_topk_kernel(const float* __restrict__ blk_lse, size_t rows, int n, int B, int K, int NB, int W,
-                                uint32_t* __restrict__ head_mask) {
+__global__ void ref_topk_kernel(const float* __restrict__ blk_lse, size_t rows, int n, int H, int B, int K, int NB,
+                                int W, uint32_t* __restrict__ head_mask, const int32_t* __restrict__ doc) {
   const size_t r = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (r >= rows) return;
   const int t = (int)(r % n);
   const int C = t / B;
+  const int F = doc_first(doc, (int)(r / ((size_t)n * H)), NB, t, B);  // historical blocks [F, C)
   float tv[KMAX];
   int tm[KMAX];
 #pragma unroll
@@ -302,7 +305,7 @@ __global__ void ref_topk_kernel(const float* __restrict__ blk_lse, size_t rows, 
     tm[i] = 0x7fffffff;
   }
   const float* row = blk_lse + r * NB;
-  for (int m = 0; m < C; ++m) {
+  for (int m = F; m < C; ++m) {
     float cv = row[m];
     int cm = m;
     if (!(cv > tv[KMAX - 1] || (cv == tv[KMAX - 1] && cm < tm[KMAX - 1]))) continue;
@@ -318,7 +321,7 @@ __global__ void ref_topk_kernel(const float* __restrict__ blk_lse, size_t rows, 
       cm = better ? om : cm;
     }
   }
-  const int kk = min(K, C);
+  const int kk = min(K, C - F);
   uint32_t* out = head_mask + r * W;
   for (int w = 0; w < W; ++w) {
     uint32_t bits = 0;
@@ -434,14 +437,14 @@ hipError_t launch_stats(int dtype, const StatsArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_ref_sets(const float* blk_lse, int b, int n, int H, int Hkv, int B, int K, uint32_t* head_mask,
-                           uint32_t* uni, hipStream_t s) {
+                           uint32_t* uni, const int32_t* doc, hipStream_t s) {
   const int NB = cdiv(n, B), W = cdiv(NB, 32);
   const size_t rows = (size_t)b * H * n;
   if (rows == 0) return hipSuccess;
   const unsigned grid = (unsigned)cdiv(rows, 128);
-  if (K <= 8) ref_topk_kernel<8><<<grid, 128, 0, s>>>(blk_lse, rows, n, B, K, NB, W, head_mask);
-  else if (K <= 16) ref_topk_kernel<16><<<grid, 128, 0, s>>>(blk_lse, rows, n, B, K, NB, W, head_mask);
-  else ref_topk_kernel<32><<<grid, 128, 0, s>>>(blk_lse, rows, n, B, K, NB, W, head_mask);
+  if (K <= 8) ref_topk_kernel<8><<<grid, 128, 0, s>>>(blk_lse, rows, n, H, B, K, NB, W, head_mask, doc);
+  else if (K <= 16) ref_topk_kernel<16><<<grid, 128, 0, s>>>(blk_lse, rows, n, H, B, K, NB, W, head_mask, doc);
+  else ref_topk_kernel<32><<<grid, 128, 0, s>>>(blk_lse, rows, n, H, B, K, NB, W, head_mask, doc);
   const size_t tot = (size_t)b * Hkv * n * W;
   vote_union_kernel<<<(unsigned)cdiv(tot, 256), 256, 0, s>>>(head_mask, b, n, H, Hkv, W, uni);
   return hipGetLastError();

@@ -48,7 +48,7 @@ class Config(C.Structure):
 
 class AttnIn(C.Structure):
     _fields_ = [("q", C.c_void_p), ("k", C.c_void_p), ("v", C.c_void_p), ("w_gq", C.c_void_p),
-                ("w_gk", C.c_void_p), ("score_noise", C.c_void_p)]
+                ("w_gk", C.c_void_p), ("score_noise", C.c_void_p), ("doc_first_block", C.c_void_p)]
 
 
 class AttnOut(C.Structure):
@@ -57,7 +57,7 @@ class AttnOut(C.Structure):
 
 
 class BwdIn(C.Structure):
-    _fields_ = [(f, C.c_void_p) for f in ("q", "k", "v", "o", "d_o", "lse", "sel_idx", "log_gate")]
+    _fields_ = [(f, C.c_void_p) for f in ("q", "k", "v", "o", "d_o", "lse", "sel_idx", "log_gate", "doc_first_block")]
 
 
 class BwdOut(C.Structure):
@@ -65,7 +65,7 @@ class BwdOut(C.Structure):
 
 
 class StatsIn(C.Structure):
-    _fields_ = [(f, C.c_void_p) for f in ("q", "k", "v", "sel_idx")]
+    _fields_ = [(f, C.c_void_p) for f in ("q", "k", "v", "sel_idx", "doc_first_block")]
 
 
 class StatsOut(C.Structure):
@@ -74,7 +74,7 @@ class StatsOut(C.Structure):
 
 class SelBwdIn(C.Structure):
     _fields_ = [(f, C.c_void_p) for f in ("q", "k", "w_gq", "w_gk", "sel_idx", "log_gate", "dlog_gate",
-                                          "dlog_gate_full")]
+                                          "dlog_gate_full", "doc_first_block")]
 
 
 class SelBwdOut(C.Structure):
@@ -210,9 +210,11 @@ def weights_struct(W: dict) -> LayerWeights:
 
 
 def attention_prefill(cfg: Config, q, k, v, w_gq=None, w_gk=None, *, lse=True, k_summary=True,
-                      sel_idx=True, log_gate=False, tau=False, noise=None, ws: Workspace | None = None) -> dict:
+                      sel_idx=True, log_gate=False, tau=False, noise=None, doc=None,
+                      ws: Workspace | None = None) -> dict:
     """Selector + SAS attention.  q [b,n,H,dh], k/v [b,n,Hkv,dh] on the GPU;
-    noise [b,Hkv,n,NB] fp32 (optional) is added to the selector scores."""
+    noise [b,Hkv,n,NB] fp32 (optional) is added to the selector scores; doc
+    [b,NB] int32 (optional) packs several block-aligned documents per row."""
     b, n, H, dh = q.shape
     Hkv = k.shape[2]
     B, K = cfg.block_size, cfg.top_k
@@ -229,7 +231,7 @@ def attention_prefill(cfg: Config, q, k, v, w_gq=None, w_gk=None, *, lse=True, k
         out["log_gate"] = torch.empty(b, Hkv, n, NB, dtype=torch.float32, device=dev)
     if tau:
         out["tau"] = torch.empty(b, Hkv, n, dtype=torch.float32, device=dev)
-    ain = AttnIn(_ptr(q), _ptr(k), _ptr(v), _ptr(w_gq), _ptr(w_gk), _ptr(noise))
+    ain = AttnIn(_ptr(q), _ptr(k), _ptr(v), _ptr(w_gq), _ptr(w_gk), _ptr(noise), _ptr(doc))
     aout = AttnOut(*[_ptr(out.get(f)) for f in ("o", "lse", "k_summary", "sel_idx", "log_gate", "tau")])
     wsp, wsn = _ws(ws, workspace_size(cfg, OP_ATTENTION, b, n))
     _check(lib().sas_attention_prefill(C.byref(cfg), b, n, C.byref(ain), C.byref(aout), wsp, wsn, _stream()))
@@ -237,7 +239,7 @@ def attention_prefill(cfg: Config, q, k, v, w_gq=None, w_gk=None, *, lse=True, k
 
 
 def attention_backward(cfg: Config, q, k, v, o, d_o, lse, sel_idx=None, log_gate=None, *, dlog_gate: bool = True,
-                       dlog_gate_full: bool = False, ws: Workspace | None = None) -> dict:
+                       dlog_gate_full: bool = False, doc=None, ws: Workspace | None = None) -> dict:
     """dQ, dK, dV and the log-gate gradient of the attention given the
     forward's inputs, its output o, LSE and selection, and d_o: per selection
     slot (dlog_gate, sparse scope) and/or per block (dlog_gate_full; the only
@@ -251,7 +253,7 @@ def attention_backward(cfg: Config, q, k, v, o, d_o, lse, sel_idx=None, log_gate
         out["dlog_gate"] = torch.empty(b, Hkv, n, K, dtype=torch.float32, device=q.device)
     if dlog_gate_full or full:
         out["dlog_gate_full"] = torch.empty(b, Hkv, n, NB, dtype=torch.float32, device=q.device)
-    bi = BwdIn(*[_ptr(t) for t in (q, k, v, o, d_o, lse, sel_idx, log_gate)])
+    bi = BwdIn(*[_ptr(t) for t in (q, k, v, o, d_o, lse, sel_idx, log_gate, doc)])
     bo = BwdOut(*[_ptr(out.get(f)) for f in ("dq", "dk", "dv", "dlog_gate", "dlog_gate_full")])
     wsp, wsn = _ws(ws, workspace_size(cfg, OP_ATTENTION_BACKWARD, b, n))
     _check(lib().sas_attention_backward(C.byref(cfg), b, n, C.byref(bi), C.byref(bo), wsp, wsn, _stream()))
@@ -259,7 +261,7 @@ def attention_backward(cfg: Config, q, k, v, o, d_o, lse, sel_idx=None, log_gate
 
 
 def selector_backward(cfg: Config, q, k, sel_idx, log_gate, dlog_gate, w_gq=None, w_gk=None, *, ds: bool = True,
-                      dqhat: bool = True, dkbar: bool = True, dlog_gate_full=None,
+                      dqhat: bool = True, dkbar: bool = True, dlog_gate_full=None, doc=None,
                       ws: Workspace | None = None) -> dict:
     """Selector gradients from the selected blocks' log-gate gradient: ds
     [b,Hkv,n,NB], dqhat [b,Hkv,n,dh], dkbar [b,Hkv,NB,dh] and, for given
@@ -279,7 +281,7 @@ def selector_backward(cfg: Config, q, k, sel_idx, log_gate, dlog_gate, w_gq=None
         out["dw_gq"] = torch.empty(Hkv, dh, dh, dtype=torch.float32, device=dev)
     if w_gk is not None:
         out["dw_gk"] = torch.empty(Hkv, dh, dh, dtype=torch.float32, device=dev)
-    si = SelBwdIn(*[_ptr(t) for t in (q, k, w_gq, w_gk, sel_idx, log_gate, dlog_gate, dlog_gate_full)])
+    si = SelBwdIn(*[_ptr(t) for t in (q, k, w_gq, w_gk, sel_idx, log_gate, dlog_gate, dlog_gate_full, doc)])
     so = SelBwdOut(*[_ptr(out.get(f)) for f in ("ds", "dqhat", "dkbar", "dw_gq", "dw_gk")])
     wsp, wsn = _ws(ws, workspace_size(cfg, OP_SELECTOR_BACKWARD, b, n))
     _check(lib().sas_selector_backward(C.byref(cfg), b, n, C.byref(si), C.byref(so), wsp, wsn, _stream()))
@@ -297,7 +299,7 @@ def alloc_union(cfg: Config, b: int, n: int, device="cuda"):
 
 
 def selection_stats(cfg: Config, q, k, v=None, sel_idx=None, *, cov: bool = True, cov_v: bool = True,
-                    sel_union=None, ref_union=None, ws: Workspace | None = None) -> dict:
+                    sel_union=None, ref_union=None, doc=None, ws: Workspace | None = None) -> dict:
     """Mass coverage (cov, cov_v [b,H,n]) of the attended sets and OR-accumulation
     of the selected / full-attention reference block sets into the given
     bitmasks (see alloc_union)."""
@@ -307,7 +309,7 @@ def selection_stats(cfg: Config, q, k, v=None, sel_idx=None, *, cov: bool = True
         out["cov"] = torch.empty(b, H, n, dtype=torch.float32, device=q.device)
     if cov_v:
         out["cov_v"] = torch.empty(b, H, n, dtype=torch.float32, device=q.device)
-    si = StatsIn(*[_ptr(t) for t in (q, k, v, sel_idx)])
+    si = StatsIn(*[_ptr(t) for t in (q, k, v, sel_idx, doc)])
     so = StatsOut(_ptr(out.get("cov")), _ptr(out.get("cov_v")), _ptr(sel_union), _ptr(ref_union))
     wsp, wsn = _ws(ws, workspace_size(cfg, OP_SELECTION_STATS, b, n))
     _check(lib().sas_selection_stats(C.byref(cfg), b, n, C.byref(si), C.byref(so), wsp, wsn, _stream()))
