@@ -29,6 +29,7 @@ struct GemmParams {
   const float2* rope;
   const int32_t* row_pos;
   int group_m;       // M tiles per group of the tile order (0: M-fastest over all tiles, no XCD remap)
+  int n_off, n_cnt;  // gemm_bf16_lds_kernel: logical columns [n_off, n_off + n_cnt) of this launch
 };
 
 // Tile of workgroup `bid`.  Workgroups are dispatched round-robin over the 8
@@ -629,6 +630,317 @@ gemm_bf16_reg_kernel(GemmParams P) {
   gemm_epilogue_t<EPI, TM, TN, FM, FN>(P, acc, m0, n0, wm, wn, lr, lk);
 }
 
+
+// ---- 8-wave direct-to-LDS kernel with an LDS-staged epilogue (K % 64 == 0) --
+// Two waves per SIMD: a wave's direct-to-LDS load instructions stall its own
+// issue for tens of cycles, and the second wave keeps the matrix core busy
+// meanwhile.  Per 64-wide k-tile a wave runs four 16-deep MFMA steps and reads
+// the fragments of the next step while the current one multiplies.  The
+// workgroup barrier of k-tile kt sits before its last step (every wave's reads
+// of kt are complete there); after it the stage of kt is refilled with k-tile
+// kt + STAGES and the reads of k-tile kt + 1 start under the last step's MFMAs.
+// Fragment reads are plain LDS loads: the compiler's waits (one per step) are
+// the ones this schedule needs.
+//
+// The epilogue stages 32 rows of a wave's tile at a time in LDS and writes
+// 16-byte stores (8 bf16 per lane) instead of one 2-byte store per
+// accumulator element.  RESID stages fp32 sums and fetches the residual before
+// the staging so that its latency overlaps it; SWIGLU stages bf16 results;
+// QKV stages the two halves of each rotary pair in fp32 and rotates on the way
+// out, reading 8 consecutive rotary entries (64 bytes) per lane.  It needs
+// 8 | N (RESID) or 8 | npairs and 16 | dh (pair epilogues); other shapes use
+// gemm_epilogue_t.
+template <int EPI, int TN>
+constexpr int epi_region_bytes() {
+  return EPI == EPI_SWIGLU ? 32 * (TN / 2) * 2 : 32 * TN * 4;
+}
+
+__device__ __forceinline__ uint4 pack8_bf16(const float* x) {
+  uint4 r;
+  r.x = pack_bf16x2(x[0], x[1]);
+  r.y = pack_bf16x2(x[2], x[3]);
+  r.z = pack_bf16x2(x[4], x[5]);
+  r.w = pack_bf16x2(x[6], x[7]);
+  return r;
+}
+
+template <int EPI, int TM, int TN, int FM, int FN>
+__device__ __forceinline__ void gemm_epilogue_lds(const GemmParams& P, floatx16_t (&acc)[FM][FN], int m0, int n0,
+                                                  int wm, int wn, int lr, int lk, unsigned char* region) {
+  const int lane = lk * 32 + lr;
+  const int colbase = n0 + wn * TN;
+  const int rowbase = m0 + wm * TM;
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int brow = rowbase + i * 32;
+    // accumulator element v of subtile (i, j) is row 8*(v/4) + 4*lk + v%4, column j*32 + lr
+    if constexpr (EPI == EPI_RESID) {
+      constexpr int GPR = TN / 8, G = 32 * GPR, IT = (G + 63) / 64;
+      uint4 rv[IT];
+#pragma unroll
+      for (int it = 0; it < IT; ++it) {
+        const int g = it * 64 + lane;
+        const int r = min(g / GPR, 31), c8 = (g % GPR) * 8;
+        const int row = min(brow + r, P.M - 1), col = min(colbase + c8, P.N - 8);
+        rv[it] = *(const uint4*)(P.resid + (size_t)row * P.N + col);
+      }
+      float* st = (float*)region;
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) st[(8 * (v >> 2) + 4 * lk + (v & 3)) * TN + j * 32 + lr] = acc[i][j][v];
+      // a wave's LDS accesses complete in order: the reads below see its writes
+#pragma unroll
+      for (int it = 0; it < IT; ++it) {
+        const int g = it * 64 + lane;
+        if (G % 64 != 0 && g >= G) break;
+        const int r = g / GPR, c8 = (g % GPR) * 8;
+        const int row = brow + r, col = colbase + c8;
+        const float4 a = *(const float4*)(st + r * TN + c8);
+        const float4 b = *(const float4*)(st + r * TN + c8 + 4);
+        if (row < P.M && col < P.N) {
+          float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+          const uint32_t rw[4] = {rv[it].x, rv[it].y, rv[it].z, rv[it].w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            x[2 * e] += __uint_as_float(rw[e] << 16);
+            x[2 * e + 1] += __uint_as_float(rw[e] & 0xffff0000u);
+          }
+          *(uint4*)(P.out + (size_t)row * P.N + col) = pack8_bf16(x);
+        }
+      }
+    } else if constexpr (EPI == EPI_SWIGLU) {
+      constexpr int NP = TN / 2, GPR = NP / 8, G = 32 * GPR;
+      bf16_t* st = (bf16_t*)region;
+#pragma unroll
+      for (int jp = 0; jp < FN / 2; ++jp)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          st[(8 * (v >> 2) + 4 * lk + (v & 3)) * NP + jp * 32 + lr] =
+              f32_to_bf16(silu_f(acc[i][2 * jp][v]) * acc[i][2 * jp + 1][v]);
+      const int pbase = colbase >> 1;  // colbase is a multiple of 64
+#pragma unroll
+      for (int g0 = 0; g0 < G; g0 += 64) {
+        const int g = g0 + lane;
+        if (G % 64 != 0 && g >= G) break;
+        const int r = g / GPR, q8 = (g % GPR) * 8;
+        const int row = brow + r, p = pbase + q8;
+        if (row >= P.M || p >= P.npairs) continue;
+        *(uint4*)(P.out + (size_t)row * P.npairs + p) = *(const uint4*)(st + r * NP + q8);
+      }
+    } else {
+      constexpr int NP = TN / 2, GPR = NP / 8, G = 32 * GPR;
+      constexpr int IT = (G + 63) / 64, BATCH = 2;
+      const int hh = P.dh >> 1;
+      const int pbase = colbase >> 1;
+      const int pb = P.row_pos ? 0 : brow % P.seq_len;  // wave-uniform
+      float* st = (float*)region;  // [2][32][NP]: first and second halves of the pairs
+#pragma unroll
+      for (int jp = 0; jp < FN / 2; ++jp)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int r = 8 * (v >> 2) + 4 * lk + (v & 3);
+          st[r * NP + jp * 32 + lr] = acc[i][2 * jp][v];
+          st[32 * NP + r * NP + jp * 32 + lr] = acc[i][2 * jp + 1][v];
+        }
+#pragma unroll
+      for (int b0 = 0; b0 < IT; b0 += BATCH) {
+        float4 cs[BATCH][4];  // 8 (cos, sin) entries per group, fetched before use
+#pragma unroll
+        for (int it = b0; it < b0 + BATCH && it < IT; ++it) {
+          const int g = min(it * 64 + lane, G - 1);
+          const int r = g / GPR, q8 = (g % GPR) * 8;
+          const int p = min(pbase + q8, P.npairs - 8);
+          const int hd = p / hh, ir = p - hd * hh;
+          int pos;
+          if (P.row_pos) pos = P.row_pos[min(brow + r, P.M - 1)];
+          else if (P.seq_len >= 32) pos = pb + r >= P.seq_len ? pb + r - P.seq_len : pb + r;
+          else pos = min(brow + r, P.M - 1) % P.seq_len;
+          const float4* rp = (const float4*)(P.rope + (size_t)pos * hh + ir);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) cs[it - b0][e] = rp[e];
+        }
+#pragma unroll
+        for (int it = b0; it < b0 + BATCH && it < IT; ++it) {
+          const int g = it * 64 + lane;
+          if (G % 64 != 0 && g >= G) break;
+          const int r = g / GPR, q8 = (g % GPR) * 8;
+          const int row = brow + r, p = pbase + q8;
+          if (row >= P.M || p >= P.npairs) continue;
+          const int hd = p / hh, ir = p - hd * hh;
+          float x1[8], x2[8];
+          *(float4*)&x1[0] = *(const float4*)(st + r * NP + q8);
+          *(float4*)&x1[4] = *(const float4*)(st + r * NP + q8 + 4);
+          *(float4*)&x2[0] = *(const float4*)(st + 32 * NP + r * NP + q8);
+          *(float4*)&x2[4] = *(const float4*)(st + 32 * NP + r * NP + q8 + 4);
+          bf16_t* dst;
+          size_t ld;
+          if (hd < P.H) {
+            dst = P.out + (size_t)hd * P.dh + ir;
+            ld = (size_t)P.H * P.dh;
+          } else if (hd < P.H + P.Hkv) {
+            dst = P.out1 + (size_t)(hd - P.H) * P.dh + ir;
+            ld = (size_t)P.Hkv * P.dh;
+          } else {
+            dst = P.out2 + (size_t)(hd - P.H - P.Hkv) * P.dh + ir;
+            ld = (size_t)P.Hkv * P.dh;
+          }
+          if (hd < P.H + P.Hkv) {
+            const float* c = (const float*)cs[it - b0];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const float co = c[2 * e], si = c[2 * e + 1];
+              const float o1 = x1[e] * co - x2[e] * si;
+              const float o2 = x2[e] * co + x1[e] * si;
+              x1[e] = o1;
+              x2[e] = o2;
+            }
+          }
+          dst += (size_t)row * ld;
+          *(uint4*)dst = pack8_bf16(x1);
+          *(uint4*)(dst + hh) = pack8_bf16(x2);
+        }
+      }
+    }
+  }
+}
+
+template <int EPI, int BM, int BN, int WM, int WN, int STAGES>
+__global__ void __launch_bounds__(WM * WN * 64)
+gemm_bf16_lds_kernel(GemmParams P) {
+  constexpr int BKT = 64, KK = 4;
+  constexpr int NW = WM * WN;
+  constexpr int TM = BM / WM, TN = BN / WN;
+  constexpr int FM = TM / 32, FN = TN / 32, NF = FM + FN, NMF = FM * FN;
+  constexpr int CPR = BKT / 8, RPG = 16 / CPR;  // swizzle as in gemm_bf16_pipe_kernel
+  constexpr int AI = BM * CPR / (64 * NW);
+  constexpr int BI = BN * CPR / (64 * NW);
+  constexpr int LI = AI + BI;
+  static_assert(AI * 64 * NW == BM * CPR && BI * 64 * NW == BN * CPR, "tile/threads mismatch");
+  static_assert(EPI == EPI_RESID || TN % 64 == 0, "pair epilogues need 64-column wave tiles");
+  static_assert(STAGES >= 2 && (STAGES - 1) * LI <= 63, "vmcnt range");
+  constexpr int STAGE = (BM + BN) * BKT;  // elements per stage
+  static_assert(NW * epi_region_bytes<EPI, TN>() <= STAGES * STAGE * 2, "epilogue staging exceeds the stages");
+
+  extern __shared__ __align__(16) unsigned char smem[];
+  bf16_t* S = (bf16_t*)smem;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int Mt = (P.M + BM - 1) / BM, Nt = (P.n_cnt + BN - 1) / BN;
+  int mt, nt;
+  tile_of(blockIdx.x, Mt, Nt, P.group_m, mt, nt);
+  const int m0 = mt * BM, n0 = P.n_off + nt * BN;
+
+  // per-lane sources of the direct-to-LDS loads (rows clamped; results of
+  // clamped rows are never stored)
+  uint32_t a_off[AI];
+  const bf16_t* b_src[BI];
+#pragma unroll
+  for (int j = 0; j < AI; ++j) {
+    const int c = (wave * AI + j) * 64 + lane;
+    const int r = c / CPR, cc = (c % CPR) ^ ((r / RPG) % CPR);
+    const int gr = min(m0 + r, P.M - 1);
+    a_off[j] = (uint32_t)gr * (uint32_t)P.K + cc * 8;
+  }
+#pragma unroll
+  for (int j = 0; j < BI; ++j) {
+    const int c = (wave * BI + j) * 64 + lane;
+    const int r = c / CPR, cc = (c % CPR) ^ ((r / RPG) % CPR);
+    const bf16_t* row = b_row<bf16_t>(P.epi, n0 + r, P.N, P.npairs, P.K, P.B0, P.B1, P.B2, P.H, P.Hkv, P.dh);
+    b_src[j] = (row ? row : P.B0) + cc * 8;
+  }
+  // load j (0 <= j < LI) of k-tile kt into its stage
+  auto issue1 = [&](int kt, int j) {
+    const int k0 = kt * BKT;
+    bf16_t* st = S + (kt % STAGES) * STAGE;
+    if (j < AI)
+      __builtin_amdgcn_global_load_lds((const void*)(P.A + a_off[j] + k0),
+                                       (lds_void_t*)(st + (wave * AI + j) * 64 * 8), 16, 0, 0);
+    else
+      __builtin_amdgcn_global_load_lds((const void*)(b_src[j - AI] + k0),
+                                       (lds_void_t*)(st + BM * BKT + (wave * BI + j - AI) * 64 * 8), 16, 0, 0);
+  };
+
+  floatx16_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  const int lr = lane & 31, lk = lane >> 5;
+  int foff[NF];  // element offset of fragment g's row in a stage: A0..A(FM-1), B0..B(FN-1)
+#pragma unroll
+  for (int g = 0; g < NF; ++g)
+    foff[g] = g < FM ? (wm * TM + g * 32 + lr) * BKT : BM * BKT + (wn * TN + (g - FM) * 32 + lr) * BKT;
+  const int sw = (lr / RPG) % CPR;  // fragment row bases are multiples of 32
+  auto rd_off = [&](int kt, int kk) -> int { return (kt % STAGES) * STAGE + (((kk * 2 + lk) ^ sw) << 3); };
+  bf16x8_t fr[2][NF];
+
+  const int nk = P.K / BKT;
+  const int npro = nk < STAGES ? nk : STAGES;
+  for (int t = 0; t < npro; ++t)
+#pragma unroll
+    for (int j = 0; j < LI; ++j) issue1(t, j);
+  if (nk >= STAGES) wait_vmcnt<(STAGES - 1) * LI>();
+  else wait_vmcnt<0>();
+  barrier_lds();
+  {
+    const bf16_t* a0 = S + rd_off(0, 0);
+#pragma unroll
+    for (int g = 0; g < NF; ++g) fr[0][g] = *(const bf16x8_t*)(a0 + foff[g]);
+  }
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const bool has_next = kt + 1 < nk;
+    const bool refill = kt + STAGES < nk;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      const int cur = kk & 1, nxt = cur ^ 1;
+      if (kk == KK - 1 && has_next) {
+        // k-tile kt+1 must have landed for every wave; loads issued after it
+        // are those of k-tiles kt+2 .. kt+STAGES-1
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        if (kt + STAGES - 1 < nk) wait_vmcnt<(STAGES - 2) * LI>();
+        else wait_vmcnt<0>();
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      const bool more = kk + 1 < KK || has_next;
+      const bf16_t* na = S + (kk + 1 < KK ? rd_off(kt, kk + 1) : rd_off(kt + 1, 0));
+      int m = 0;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[cur][i], fr[cur][FM + j], acc[i][j], 0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
+          if (more && m < NF) fr[nxt][m] = *(const bf16x8_t*)(na + foff[m]);
+          if (kk == KK - 1 && refill) {
+#pragma unroll
+            for (int q = m * LI / NMF; q < (m + 1) * LI / NMF; ++q) issue1(kt + STAGES, q);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+          ++m;
+        }
+#pragma unroll
+      for (int g = NMF; g < NF; ++g)
+        if (more) fr[nxt][g] = *(const bf16x8_t*)(na + foff[g]);
+    }
+  }
+  const bool fast = EPI == EPI_RESID ? (P.N % 8) == 0
+                                     : (P.npairs % 8) == 0 && (EPI == EPI_SWIGLU || (P.dh % 16) == 0);
+  if (fast) {
+    barrier_lds();  // every wave is done with the stages
+    gemm_epilogue_lds<EPI, TM, TN, FM, FN>(P, acc, m0, n0, wm, wn, lr, lk, smem + wave * epi_region_bytes<EPI, TN>());
+  } else {
+    gemm_epilogue_t<EPI, TM, TN, FM, FN>(P, acc, m0, n0, wm, wn, lr, lk);
+  }
+}
+
 // ---- fp32 path: one thread per (row, logical pair or column) ----------------
 __global__ void gemm_f32_kernel(int epi, int M, int K, int N, int npairs, const float* __restrict__ A,
                                 const float* __restrict__ B0, const float* __restrict__ B1,
@@ -734,6 +1046,29 @@ static hipError_t run_pipe(const GemmParams& P, hipStream_t s) {
   return run_pipe_t<EPI_QKV_ROPE, BM, BN, WM, WN, BKT, STAGES, DB>(P, s);
 }
 
+
+template <int EPI, int BM, int BN, int WM, int WN, int STAGES>
+static hipError_t run_lds_t(const GemmParams& P, hipStream_t s) {
+  constexpr int NT = WM * WN * 64;
+  const int tiles = ((P.M + BM - 1) / BM) * ((P.n_cnt + BN - 1) / BN);
+  const size_t lds = (size_t)STAGES * (BM + BN) * 64 * sizeof(bf16_t);
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute((const void*)gemm_bf16_lds_kernel<EPI, BM, BN, WM, WN, STAGES>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    attr = true;
+  }
+  hipLaunchKernelGGL((gemm_bf16_lds_kernel<EPI, BM, BN, WM, WN, STAGES>), dim3(tiles), dim3(NT), lds, s, P);
+  return hipGetLastError();
+}
+
+template <int BM, int BN, int WM, int WN, int STAGES>
+static hipError_t run_lds(const GemmParams& P, hipStream_t s) {
+  if (P.epi == EPI_RESID) return run_lds_t<EPI_RESID, BM, BN, WM, WN, STAGES>(P, s);
+  if (P.epi == EPI_SWIGLU) return run_lds_t<EPI_SWIGLU, BM, BN, WM, WN, STAGES>(P, s);
+  return run_lds_t<EPI_QKV_ROPE, BM, BN, WM, WN, STAGES>(P, s);
+}
+
 static bool attrs_done = false;
 
 hipError_t launch_gemm(int dtype, const GemmArgs& g, hipStream_t s) {
@@ -776,6 +1111,8 @@ hipError_t launch_gemm(int dtype, const GemmArgs& g, hipStream_t s) {
   P.Hkv = g.n_kv_heads;
   P.dh = g.head_dim;
   P.group_m = 8;
+  P.n_off = 0;
+  P.n_cnt = nlog;
   P.seq_len = g.seq_len;
   P.rope = g.rope;
   P.row_pos = g.row_pos;
@@ -784,14 +1121,26 @@ hipError_t launch_gemm(int dtype, const GemmArgs& g, hipStream_t s) {
   if (g.K % 64 == 0) {
     // Tile choice from measurements on MI355X with the weights streamed
     // from HBM, as in a layer (grouped, XCD-aware tile order).  Long M:
-    // 256x256 with 8 waves.  Short M, where each CU's operand stream from L2
-    // rather than the MFMA rate bounds the product: 256x128 with three
-    // direct-to-LDS stages for the wide SwiGLU product, four stages of
-    // 128x128 for long K, else the register-staged 128x128 with 8 waves.
-    if (g.M >= 4096) return run_pipe<256, 256, 2, 4, 64, 2, true>(P, s);
-    if (nlog >= 16384) return run_pipe<256, 128, 4, 2, 64, 3, true>(P, s);
-    if (g.K >= 8192) return run_pipe<128, 128, 2, 2, 64, 4, true>(P, s);
-    return run_reg<128, 128, 4, 2, 2>(P, s);
+    // 256x256 tiles.  Short M: 256x256 tiles where they fill the
+    // CUs; when they would take a second, partly empty round, one full
+    // round of 256x256 tiles followed by 256x128 tiles for the remaining
+    // columns; narrow products (N < 8192) with 128x128 tiles.
+    if (g.M >= 4096) return run_lds<256, 256, 2, 4, 2>(P, s);
+    if (nlog >= 8192) {
+      const int mt = (g.M + 255) / 256, nt = (nlog + 255) / 256;
+      const int full = 256 / mt;  // 256-column tiles per full round
+      if ((long)mt * nt > 256 && full > 0) {
+        GemmParams P1 = P, P2 = P;
+        P1.n_cnt = full * 256;
+        P2.n_off = full * 256;
+        P2.n_cnt = nlog - full * 256;
+        hipError_t e = run_lds<256, 256, 2, 4, 2>(P1, s);
+        if (e != hipSuccess) return e;
+        return run_lds<256, 128, 4, 2, 3>(P2, s);
+      }
+      return run_lds<256, 256, 2, 4, 2>(P, s);
+    }
+    return run_lds<128, 128, 4, 2, 4>(P, s);
   }
   if (big_tiles >= 256) return run_bf16<256, 256, 2, 4>(P, s);
   return run_bf16<128, 128, 2, 2>(P, s);
