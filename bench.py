@@ -30,7 +30,8 @@ METRIC = "prefill tokens/s per layer + % bf16 MFMA peak; decode % HBM GB/s"
 HERE = os.path.dirname(os.path.abspath(__file__))
 GEMM_SRC = os.path.join(HERE, "paper_2609_13141_amd", "csrc", "gemm.hip")
 TRAFFIC_FILE = os.path.join(HERE, "profiles", "gemm_gate_up_7b_layer_1k_traffic.txt")
-DOM_KERNEL = "gemm_bf16_pipe_kernel<1, 256, 128, 4, 2, 64, 3, true>"  # the gate/up launch at 1024 rows
+# the gate/up GEMM at 1024 rows: one round of 256x256 tiles, then 256x128 tiles
+DOM_KERNELS = ("gemm_bf16_lds_kernel<1, 256, 256, 2, 4, 2>", "gemm_bf16_lds_kernel<1, 256, 128, 4, 2, 3>")
 COPY_BYTES = 512 * 2**20  # calibration copy: reads and writes this many bytes once
 
 
@@ -59,18 +60,22 @@ def source_hash():
 
 
 def pmc_per_dispatch(run_dir, counter):
-    """Mean per-dispatch value of `counter` for the dominant GEMM and for the
+    """Per-call value of `counter` for the dominant GEMM (the sum over its
+    launches of each kernel's mean per dispatch) and the mean for the
     calibration copy, from a rocprofv3 --pmc csv run directory."""
     files = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
     if not files:
         raise SystemExit(f"no counter_collection.csv under {run_dir}")
-    vals = {"gemm": {}, "copy": {}}
+    keys = list(DOM_KERNELS) + ["copy"]
+    vals = {k: {} for k in keys}
     for f in files:
         for r in csv.DictReader(open(f)):
             if r["Counter_Name"] != counter:
                 continue
             name = r["Kernel_Name"]
-            key = "gemm" if DOM_KERNEL in name else ("copy" if "copy" in name.lower() else None)
+            key = next((k for k in DOM_KERNELS if k in name), None)
+            if key is None and "copy" in name.lower():
+                key = "copy"
             if key:
                 d = vals[key]
                 d[r["Dispatch_Id"]] = d.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
@@ -82,6 +87,7 @@ def pmc_per_dispatch(run_dir, counter):
         if k == "copy":
             v = v[-2:]  # the two calibration copies are by far the largest copy dispatches
         out[k] = sum(v) / len(v)
+    out["gemm"] = sum(out[k] for k in DOM_KERNELS)
     return out
 
 
@@ -96,7 +102,7 @@ def write_traffic_summary(fetch_dir, write_dir):
     write_b = wr["gemm"] * 1024.0 * f_write
     lines = [
         "# HBM traffic of the gate/up GEMM (7b_layer_1k, 1024 x 4096 x 2*11008) per launch",
-        f"# kernel: {DOM_KERNEL}",
+        f"# kernels (summed per call): {', '.join(DOM_KERNELS)}",
         "# rocprofv3 --pmc FETCH_SIZE (then WRITE_SIZE) -- python3 bench.py --no-decode --no-cpu-baseline "
         "--steps 5 --warmup 2 --calibrate-copy",
         f"# calibration: plain copy of {COPY_BYTES} bytes read {fe['copy']:.0f} KiB fetch, {wr['copy']:.0f} KiB write",
