@@ -1067,13 +1067,16 @@ sas_status sas_decode_step(const sas_config* c, int32_t batch, const void* x, co
   const DecodeArgs da = decode_args(c, batch, pos, cache, w);
   const int H = c->n_heads, Hkv = c->n_kv_heads, dh = c->head_dim;
   int32_t* sel = sel_idx ? sel_idx : dw.sel;
-  {
-    Timed tm("rope_rows", s);
-    HIP_TRY(launch_rope_rows(pos, dw.rope, batch, dh, c->rope_base, s), "rope rows");
-  }
+  // The first RMSNorm launch also writes the rotary rows of the positions.  On
+  // the skinny-GEMM path the QKV product appends K/V to the cache itself
+  // (unless a summary projection follows the append).
+  const bool gemv = c->dtype == SAS_BF16 && batch <= 16 && c->d_model % 128 == 0;
+  const bool fused_append = gemv && !da.w_gk;
   {
     Timed tm("rmsnorm", s);
-    HIP_TRY(launch_rmsnorm(c->dtype, x, w->rms1, dw.u1, batch, c->d_model, c->rms_eps, s), "rmsnorm");
+    HIP_TRY(launch_rmsnorm_rope(c->dtype, x, w->rms1, dw.u1, batch, c->d_model, c->rms_eps, pos, dw.rope, dh,
+                                c->rope_base, s),
+            "rmsnorm");
   }
   GemmArgs g = {};
   g.epi = EPI_QKV_ROPE;
@@ -1091,11 +1094,13 @@ sas_status sas_decode_step(const sas_config* c, int32_t batch, const void* x, co
   g.n_kv_heads = Hkv;
   g.head_dim = dh;
   g.rope = dw.rope;
+  g.row_pos = fused_append ? pos : nullptr;
+  g.append = fused_append ? &da : nullptr;
   {
     Timed tm("dec_qkv", s);
     HIP_TRY(small_gemm(c->dtype, g, s), "qkv gemm");
   }
-  {
+  if (!fused_append) {
     Timed tm("dec_append", s);
     HIP_TRY(launch_kv_append(c->dtype, dw.k, dw.v, da, dw.kplain, s), "kv append");
   }

@@ -18,20 +18,6 @@
 
 namespace sas {
 
-struct PageGeom {
-  const int32_t* table;
-  int num_pages, ps, max_pages;
-  // element offset of (seq, group, position) in the page pool, or -1
-  __device__ __forceinline__ long long offset(int i, int g, int p, int Hkv, int dh) const {
-    if (p < 0) return -1;
-    const int pi = p / ps;
-    if (pi >= max_pages) return -1;
-    const int page = table[(size_t)i * max_pages + pi];
-    if (page < 0 || page >= num_pages) return -1;
-    return (((long long)page * Hkv + g) * ps + (p % ps)) * dh;
-  }
-};
-
 __device__ __forceinline__ PageGeom geom_of(const DecodeArgs& c) {
   PageGeom G;
   G.table = c.block_table;
@@ -39,22 +25,6 @@ __device__ __forceinline__ PageGeom geom_of(const DecodeArgs& c) {
   G.ps = c.page_size;
   G.max_pages = c.max_pages;
   return G;
-}
-
-// ---- rotary table for the positions of the new tokens -----------------------
-__global__ void rope_rows_kernel(const int32_t* __restrict__ pos, float2* __restrict__ rope, int b, int half,
-                                 int dh, double base) {
-  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= b * half) return;
-  const int r = idx / half, i = idx % half;
-  const double ang = (double)pos[r] * pow(base, -2.0 * (double)i / (double)dh);
-  rope[idx] = make_float2((float)cos(ang), (float)sin(ang));
-}
-
-hipError_t launch_rope_rows(const int32_t* pos, float2* rope, int b, int dh, float base, hipStream_t s) {
-  const int tot = b * (dh / 2);
-  rope_rows_kernel<<<cdiv(tot, 256), 256, 0, s>>>(pos, rope, b, dh / 2, dh, (double)base);
-  return hipGetLastError();
 }
 
 // ---- prefill -> cache ---------------------------------------------------------

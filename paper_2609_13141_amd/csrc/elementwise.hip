@@ -6,21 +6,36 @@ namespace sas {
 
 // One workgroup of 256 threads per row; each thread keeps its 16-byte
 // chunks of the row in registers between the sum of squares (fp32) and the
-// scaled write, rounded once to the activation dtype.
-template <typename T, int CPT>
+// scaled write, rounded once to the activation dtype.  With ROPE the
+// workgroup also writes its row's rotary table entries for position pos[row]
+// (rope[row, i] = (cos, sin) of pos * base^(-2i/dh), fp64, rounded to fp32),
+// computed while the row's loads are in flight.
+template <typename T, int CPT, bool ROPE>
 __global__ void __launch_bounds__(256) rmsnorm_kernel(const T* __restrict__ x, const T* __restrict__ gamma,
-                                                      T* __restrict__ out, int d, float eps) {
+                                                      T* __restrict__ out, int d, float eps,
+                                                      const int32_t* __restrict__ pos, float2* __restrict__ rope,
+                                                      int dh, double base) {
   constexpr int EPC = 16 / sizeof(T);  // elements per 16-byte chunk
   const size_t row = blockIdx.x;
   const T* xr = x + row * (size_t)d;
   T* o = out + row * (size_t)d;
   const int nch = d / EPC;
   uint4 v[CPT];
-  float ss = 0.f;
 #pragma unroll
   for (int i = 0; i < CPT; ++i) {
     const int c = threadIdx.x + i * 256;
     v[i] = c < nch ? *(const uint4*)(xr + (size_t)c * EPC) : make_uint4(0, 0, 0, 0);
+  }
+  if constexpr (ROPE) {
+    const int half = dh >> 1;
+    for (int i = threadIdx.x; i < half; i += 256) {
+      const double ang = (double)pos[row] * pow(base, -2.0 * (double)i / (double)dh);
+      rope[row * (size_t)half + i] = make_float2((float)cos(ang), (float)sin(ang));
+    }
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
     const T* e = (const T*)&v[i];
 #pragma unroll
     for (int k = 0; k < EPC; ++k) {
@@ -49,14 +64,19 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const T* __restrict__ x, c
   }
 }
 
-hipError_t launch_rmsnorm(int dtype, const void* x, const void* gamma, void* out, int rows, int d,
-                          float eps, hipStream_t s) {
+hipError_t launch_rmsnorm_rope(int dtype, const void* x, const void* gamma, void* out, int rows, int d, float eps,
+                               const int32_t* pos, float2* rope, int dh, float base, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   // d is a multiple of 8 (validated); up to 16 chunks of 16 bytes per thread
   const int epc = dtype == SAS_BF16 ? 8 : 4;
   const int cpt = (d / epc + 255) / 256;
   if (cpt > 16) return hipErrorInvalidValue;
-#define RMS_LAUNCH(T, C) rmsnorm_kernel<T, C><<<rows, 256, 0, s>>>((const T*)x, (const T*)gamma, (T*)out, d, eps)
+  if (rope && !pos) return hipErrorInvalidValue;
+#define RMS_LAUNCH(T, C)                                                                                      \
+  (rope ? rmsnorm_kernel<T, C, true><<<rows, 256, 0, s>>>((const T*)x, (const T*)gamma, (T*)out, d, eps, pos, \
+                                                          rope, dh, (double)base)                             \
+        : rmsnorm_kernel<T, C, false><<<rows, 256, 0, s>>>((const T*)x, (const T*)gamma, (T*)out, d, eps,     \
+                                                           nullptr, nullptr, dh, 0.0))
   if (dtype == SAS_BF16) {
     if (cpt <= 2) RMS_LAUNCH(bf16_t, 2);
     else if (cpt <= 4) RMS_LAUNCH(bf16_t, 4);
@@ -68,6 +88,11 @@ hipError_t launch_rmsnorm(int dtype, const void* x, const void* gamma, void* out
   }
 #undef RMS_LAUNCH
   return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(int dtype, const void* x, const void* gamma, void* out, int rows, int d,
+                          float eps, hipStream_t s) {
+  return launch_rmsnorm_rope(dtype, x, gamma, out, rows, d, eps, nullptr, nullptr, 0, 0.f, s);
 }
 
 __global__ void rope_table_kernel(float2* __restrict__ rope, int n, int half, int dh, double base) {

@@ -30,6 +30,14 @@ struct GemvParams {
   bf16_t* out2;
   int H, Hkv, dh;
   const float2* rope;  // [M, dh/2] per-row rotary table
+  const int32_t* pos;  // [M] positions (cache append)
+  // cache append (QKV epilogue): K/V rows into their pages, and the summary of
+  // a block completed by this position (NULL k_pages: no append)
+  void* k_pages;
+  void* v_pages;
+  void* k_summary;
+  PageGeom geom;
+  int B, max_blocks;
 };
 
 // weight row of local column c (0..15) of column group gi
@@ -149,8 +157,40 @@ __global__ void __launch_bounds__(NW * 64) gemv_kernel(GemvParams P) {
       x1 = o1;
       x2 = o2;
     }
-    dst[ir] = f32_to_bf16(x1);
-    dst[ir + hh] = f32_to_bf16(x2);
+    const bf16_t b1 = f32_to_bf16(x1), b2 = f32_to_bf16(x2);
+    dst[ir] = b1;
+    dst[ir + hh] = b2;
+    if (P.k_pages && hd >= P.H) {
+      // cache append of this row's K or V, dimensions ir and ir + dh/2
+      const bool isk = hd < P.H + P.Hkv;
+      const int g = isk ? hd - P.H : hd - P.H - P.Hkv;
+      const int ps = P.pos[row];
+      const long long off = P.geom.offset(row, g, ps, P.Hkv, P.dh);
+      if (off < 0) continue;
+      bf16_t* pg = (bf16_t*)(isk ? P.k_pages : P.v_pages) + off;
+      pg[ir] = b1;
+      pg[ir + hh] = b2;
+      if (!isk || (ps + 1) % P.B != 0 || ps / P.B >= P.max_blocks) continue;
+      // this position completes block m: its summary in these two dimensions
+      // (fp64 sum over ascending positions, the new key last)
+      const int m = ps / P.B;
+      double s1 = 0.0, s2 = 0.0;
+      for (int q = m * P.B; q < ps; ++q) {
+        const long long o = P.geom.offset(row, g, q, P.Hkv, P.dh);
+        float k1 = 0.f, k2 = 0.f;  // a position without a page adds zero
+        if (o >= 0) {
+          k1 = bf16_to_f32(((const bf16_t*)P.k_pages)[o + ir]);
+          k2 = bf16_to_f32(((const bf16_t*)P.k_pages)[o + ir + hh]);
+        }
+        s1 += (double)k1;
+        s2 += (double)k2;
+      }
+      s1 += (double)bf16_to_f32(b1);
+      s2 += (double)bf16_to_f32(b2);
+      bf16_t* sm = (bf16_t*)P.k_summary + (((size_t)row * P.Hkv + g) * P.max_blocks + m) * P.dh;
+      sm[ir] = Act<bf16_t>::from_f64(s1 / (double)P.B);
+      sm[ir + hh] = Act<bf16_t>::from_f64(s2 / (double)P.B);
+    }
   }
 }
 
@@ -175,6 +215,26 @@ hipError_t launch_gemv(const GemmArgs& g, hipStream_t s) {
   P.Hkv = g.n_kv_heads;
   P.dh = g.head_dim;
   P.rope = g.rope;
+  P.pos = g.row_pos;
+  P.k_pages = nullptr;
+  P.v_pages = nullptr;
+  P.k_summary = nullptr;
+  P.geom = PageGeom{nullptr, 0, 1, 0};
+  P.B = 1;
+  P.max_blocks = 0;
+  if (g.epi == EPI_QKV_ROPE) {
+    if (!g.rope) return hipErrorInvalidValue;
+    if (g.append) {
+      if (!g.row_pos) return hipErrorInvalidValue;
+      const DecodeArgs& c = *g.append;
+      P.k_pages = c.k_pages;
+      P.v_pages = c.v_pages;
+      P.k_summary = c.k_summary;
+      P.geom = PageGeom{c.block_table, c.num_pages, c.page_size, c.max_pages};
+      P.B = c.B;
+      P.max_blocks = c.max_blocks;
+    }
+  }
   const int groups = (g.epi == EPI_RESID || g.epi == EPI_F32OUT) ? (g.N + 15) / 16 : (P.npairs + 7) / 8;
   // fewer column groups -> more waves per group, to keep enough loads in flight
   if (groups < 1024) gemv_kernel<8><<<groups, 512, 0, s>>>(P);

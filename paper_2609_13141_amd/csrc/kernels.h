@@ -14,6 +14,11 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // out[r, :] = x[r, :] / sqrt(mean(x[r, :]^2) + eps) * gamma   (fp32 math)
 hipError_t launch_rmsnorm(int dtype, const void* x, const void* gamma, void* out, int rows, int d,
                           float eps, hipStream_t s);
+// RMSNorm and, in the same launch, the rotary table rows of positions pos[row]
+// (rope [rows, dh/2] float2, (cos, sin) of pos * base^(-2i/dh) evaluated in fp64);
+// rope == NULL: norm only.
+hipError_t launch_rmsnorm_rope(int dtype, const void* x, const void* gamma, void* out, int rows, int d, float eps,
+                               const int32_t* pos, float2* rope, int dh, float base, hipStream_t s);
 // rope[p, i] = (cos(p * theta_i), sin(p * theta_i)), theta_i = base^(-2i/dh),
 // for p in [0, n), i in [0, dh/2); computed in fp64, stored as float2.
 hipError_t launch_rope_table(float2* rope, int n, int dh, float base, hipStream_t s);
@@ -41,6 +46,10 @@ struct GemmArgs {
   int n_heads, n_kv_heads, head_dim, seq_len;
   const float2* rope;
   const int32_t* row_pos; // optional per-row positions (decode), else row % seq_len
+  // decode (launch_gemv, EPI_QKV_ROPE): `append` (optional, with row_pos the
+  // rows' positions) also writes K/V into the paged cache and completes block
+  // summaries
+  const struct DecodeArgs* append;
 };
 hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s);
 
@@ -194,8 +203,6 @@ hipError_t launch_overlap_count(const uint32_t* a, const uint32_t* b, size_t wor
                                 hipStream_t s);
 
 // ---- decode.hip ------------------------------------------------------------
-// rope[r, i] for the positions pos[r] of the new tokens (fp64 math).
-hipError_t launch_rope_rows(const int32_t* pos, float2* rope, int b, int dh, float base, hipStream_t s);
 struct DecodeArgs {
   int b, H, Hkv, dh, B, K, d, F;
   float sm_scale, eps, rope_base;
@@ -208,6 +215,21 @@ struct DecodeArgs {
   int num_pages, page_size, max_pages, max_blocks;
   const void* w_gq;
   const void* w_gk;
+};
+
+// Page geometry of the cache: element offset of (sequence i, group g,
+// position p) in the page pool, or -1 when the position has no page.
+struct PageGeom {
+  const int32_t* table;
+  int num_pages, ps, max_pages;
+  __device__ __forceinline__ long long offset(int i, int g, int p, int Hkv, int dh) const {
+    if (p < 0) return -1;
+    const int pi = p / ps;
+    if (pi >= max_pages) return -1;
+    const int page = table[(size_t)i * max_pages + pi];
+    if (page < 0 || page >= num_pages) return -1;
+    return (((long long)page * Hkv + g) * ps + (p % ps)) * dh;
+  }
 };
 // Writes K/V of positions 0..n-1 of every sequence into the pages and copies
 // the complete-block summaries into the summary cache.
