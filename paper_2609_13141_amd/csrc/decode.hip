@@ -437,7 +437,11 @@ hipError_t launch_decode_select(int dtype, const void* q, const DecodeArgs& c, i
 // selection order (a block of B > SEG keys is B / SEG segments), then the
 // current block [B*floor(p/B), p].  A split is a contiguous range of segments;
 // the workgroup first resolves where each of its segments starts (one pass,
-// into LDS), then deals them to its waves round-robin.  Nothing else is staged
+// into LDS) and the page ids of every block it touches (a block's pages are
+// consecutive entries of the block table), so that a segment's key and value
+// loads depend on no global load: a wait on the page ids would also wait for
+// the loads of the segment in flight before it.  Segments are dealt to the
+// waves round-robin.  Keys and values are not staged
 // in LDS: with NC = dh/8 lanes per key, lane l holds the 8-value slice l % NC
 // of keys l / NC + (64/NC) * it, loaded with coalesced 16-byte loads (a page of
 // one KV head is contiguous).  A wave holds K and V of two segments in
@@ -459,7 +463,8 @@ struct DecodeSeg {
   int count;
 };
 
-constexpr int DSEG_MAX = 33 * 8;  // segments of a split: (K + 1) blocks of at most 8 segments
+constexpr int DSEG_MAX = 33 * 8;   // segments of a split: (K + 1) blocks of at most 8 segments
+constexpr int DPAGE_MAX = 33 * 64;  // page ids of a split: (K + 1) blocks of at most 64 pages
 
 template <typename T, int DH, int GMAX, int NW>
 __global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restrict__ q, DecodeArgs c,
@@ -470,7 +475,8 @@ __global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restric
   constexpr int NC = Seg::NC, KPI = Seg::KPI, SEG = Seg::SEG, IT = Seg::IT;
   __shared__ float sm_o[NW][GMAX][DH];
   __shared__ float sm_ml[NW][GMAX][2];
-  __shared__ int sm_first[DSEG_MAX], sm_count[DSEG_MAX];
+  __shared__ int sm_count[DSEG_MAX];
+  __shared__ int sm_pages[DPAGE_MAX];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int G = c.H / c.Hkv, nhc = (G + GMAX - 1) / GMAX;
@@ -487,51 +493,58 @@ __global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restric
   const int ps = c.page_size;
   const size_t kvstride = (size_t)c.Hkv * ps * DH;  // elements per page
 
-  // key range [first, first + count) of every segment of the split
+  // block of selection slot ch (slot K: the current block), -1 if none
+  auto block_of = [&](int ch) -> int {
+    if (p < 0) return -1;
+    return ch < K ? sel[((size_t)i * c.Hkv + g) * K + ch] : p / B;
+  };
+  // page ids of the blocks the split touches, and key count of every segment
+  const int ppb = B / ps;  // pages per block (B is a multiple of the page size, ppb <= 64)
+  const int ch0 = s0 / spb;
+  const int nbl = s1 > s0 ? (s1 - 1) / spb - ch0 + 1 : 0;
+  for (int t = threadIdx.x; t < nbl * ppb; t += NW * 64) {
+    const int mb = block_of(ch0 + t / ppb);
+    int pid = -1;
+    if (mb >= 0) {
+      const int pi = mb * ppb + t % ppb;
+      if (pi < c.max_pages) pid = c.block_table[(size_t)i * c.max_pages + pi];
+      if (pid >= c.num_pages) pid = -1;
+    }
+    sm_pages[t] = pid;
+  }
   for (int t = threadIdx.x; t < s1 - s0; t += NW * 64) {
     const int sg = s0 + t, ch = sg / spb, sub = sg % spb;
-    int first = 0, count = 0;
-    if (p >= 0) {
-      if (ch < K) {
-        const int mb = sel[((size_t)i * c.Hkv + g) * K + ch];
-        if (mb >= 0) {
-          first = mb * B + sub * seg_len;
-          count = seg_len;
-        }
-      } else {
-        first = (p / B) * B + sub * seg_len;
-        count = max(0, min(seg_len, p - first + 1));
-      }
-    }
-    sm_first[t] = first;
+    const int mb = block_of(ch);
+    int count = 0;
+    if (mb >= 0) count = ch < K ? seg_len : max(0, min(seg_len, p - (mb * B + sub * seg_len) + 1));
     sm_count[t] = count;
   }
   __syncthreads();
 
+  const int ns = s1 - s0;
+  // segment t of the split into S; t >= ns gives an empty segment (count 0,
+  // loads of the pool's start), so that every call issues the same loads
   auto load = [&](Seg& S, int t) {
-    const int first = sm_first[t];
-    S.count = sm_count[t];
-    // page ids of the segment: lane j holds the j-th page from the one holding `first`
-    // (a segment spans at most 64 pages)
-    const int koff = first % ps;
-    const int npg = (koff + S.count + ps - 1) / ps;
-    int pid = -1;
-    if (lane < npg) {
-      const int pi = first / ps + lane;
-      if (pi < c.max_pages) pid = c.block_table[(size_t)i * c.max_pages + pi];
-      if (pid >= c.num_pages) pid = -1;
-    }
+    const bool live = t < ns;
+    const int sg = s0 + (live ? t : 0), chl = sg / spb - ch0;
+    const int base = (sg % spb) * seg_len;  // the segment's first key within its block
+    S.count = live ? sm_count[t] : 0;
+    // offsets first, then every load unconditionally (keys without a page read
+    // the start of the pool and are masked by ok): loads under divergent
+    // branches make the compiler wait for all loads in flight before each one
+    size_t off[IT];
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
       const int kl = kq + KPI * it;
-      const int a = koff + kl;  // offset from the start of the first page
-      const int page = __shfl(pid, min(a / ps, 63), 64);
-      S.ok[it] = kl < S.count && page >= 0;
-      if (S.ok[it]) {
-        const size_t off = (size_t)page * kvstride + ((size_t)g * ps + a % ps) * DH + sl * 8;
-        S.k[it].load((const T*)c.k_pages + off);
-        S.v[it].load((const T*)c.v_pages + off);
-      }
+      const int a = base + kl;  // key within the block
+      const int page = kl < S.count ? sm_pages[chl * ppb + a / ps] : -1;
+      S.ok[it] = page >= 0;
+      off[it] = S.ok[it] ? (size_t)page * kvstride + ((size_t)g * ps + a % ps) * DH + sl * 8 : 0;
+    }
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      S.k[it].load((const T*)c.k_pages + off[it]);
+      S.v[it].load((const T*)c.v_pages + off[it]);
     }
   };
 
@@ -543,29 +556,35 @@ __global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restric
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[hg][e] = 0.f;
   }
+  // Every lane reads every K and V register of the segment, whatever the keys'
+  // validity (keys without data contribute zero through selects): the
+  // compiler's wait for a segment's loads then does not depend on a branch,
+  // and the next loads into these registers need no wait for older loads.
+  // the scaled query slices of the chunk's heads, loaded once: a query load
+  // issued after a segment's loads would make its use wait for all of them
+  float qsl[GMAX][8];
+#pragma unroll
+  for (int hg = 0; hg < GMAX; ++hg) {
+    const int hl = min(hc * GMAX + hg, G - 1);
+    Vec8<T> v;
+    v.load(q + ((size_t)i * c.H + g * G + hl) * DH + sl * 8);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) qsl[hg][e] = v.get(e) * c.sm_scale;
+  }
   auto compute = [&](const Seg& S) {
-    if (S.count <= 0) return;
 #pragma unroll
     for (int hg = 0; hg < GMAX; ++hg) {
       const int hl = hc * GMAX + hg;
       if (hl >= G) break;
-      const int h = g * G + hl;
-      float qs[8];
-      {
-        Vec8<T> v;
-        v.load(q + ((size_t)i * c.H + h) * DH + sl * 8);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) qs[e] = v.get(e) * c.sm_scale;
-      }
+      const float* qs = qsl[hg];
       float sc[IT];
       float mx = -INFINITY;
 #pragma unroll
       for (int it = 0; it < IT; ++it) {
         float acc = 0.f;
-        if (S.ok[it]) {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) acc = fmaf(qs[e], S.k[it].get(e), acc);
-        }
+        for (int e = 0; e < 8; ++e) acc = fmaf(qs[e], S.k[it].get(e), acc);
+        acc = S.ok[it] ? acc : 0.f;
 #pragma unroll
         for (int off = NC / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
         sc[it] = kq + KPI * it < S.count ? acc : -INFINITY;
@@ -573,32 +592,35 @@ __global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restric
       }
       mx = wave_max(mx);
       const float mn = fmaxf(m[hg], mx);
-      const float scale = __expf(m[hg] - mn);
+      const bool any = mn > -INFINITY;  // some key so far (uniform across the wave)
+      const float scale = any ? __expf(m[hg] - mn) : 1.f;
       m[hg] = mn;
       l[hg] *= scale;
 #pragma unroll
       for (int e = 0; e < 8; ++e) o[hg][e] *= scale;
 #pragma unroll
       for (int it = 0; it < IT; ++it) {
-        const float pk = kq + KPI * it < S.count ? __expf(sc[it] - mn) : 0.f;
+        const float pk = any && kq + KPI * it < S.count ? __expf(sc[it] - mn) : 0.f;
         l[hg] += pk;
-        if (S.ok[it]) {
+        const float pv = S.ok[it] ? pk : 0.f;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) o[hg][e] = fmaf(pk, S.v[it].get(e), o[hg][e]);
+        for (int e = 0; e < 8; ++e) {
+          const float vv = S.ok[it] ? S.v[it].get(e) : 0.f;
+          o[hg][e] = fmaf(pv, vv, o[hg][e]);
         }
       }
     }
   };
 
-  // two segments in registers: the next one's loads are in flight while one is computed
-  const int ns = s1 - s0;
+  // two segments in registers: the next one's loads are in flight while one
+  // is computed.  Loads and computes are unconditional (empty segments past
+  // the end), so the compiler's waits count exactly the other buffer's loads.
   Seg sa, sb;
-  if (wave < ns) load(sa, wave);
+  load(sa, wave);
   for (int t = wave; t < ns; t += 2 * NW) {
-    if (t + NW < ns) load(sb, t + NW);
+    load(sb, t + NW);
     compute(sa);
-    if (t + NW >= ns) break;
-    if (t + 2 * NW < ns) load(sa, t + 2 * NW);
+    load(sa, t + 2 * NW);
     compute(sb);
   }
 
