@@ -459,6 +459,7 @@ struct BwdWs {
   float* sel_bias;
   float* dlg_head_full;  // [b, H, n, NB] (full scope)
   float* dlg_slots;      // [b, Hkv, n, K] per-slot gradient when only the table is asked for
+  uint32_t* queue;       // job counters of the pass kernels
 };
 
 BwdWs carve_backward(Carve& cv, const sas_config* c, int b, int n) {
@@ -472,6 +473,7 @@ BwdWs carve_backward(Carve& cv, const sas_config* c, int b, int n) {
   w.sel_bias = (float*)cv.take((size_t)b * Hkv * n * K * 4);
   w.dlg_head_full = full_grad(c) ? (float*)cv.take((size_t)b * H * n * NB * 4) : nullptr;
   w.dlg_slots = (float*)cv.take((size_t)b * Hkv * n * K * 4);
+  w.queue = (uint32_t*)cv.take(256);
   return w;
 }
 
@@ -710,6 +712,7 @@ sas_status sas_attention_backward(const sas_config* c, int32_t batch, int32_t se
   a.dlg_head = bw.dlg_head;
   a.chunk_mask = bw.chunk_mask;
   a.selmask = bw.selmask;
+  a.queue = bw.queue;
   a.log_gate = gated ? in->log_gate : nullptr;
   a.outer = gated && c->gate_pos == SAS_GATE_OUTER;
   a.full = fullg;

@@ -15,6 +15,9 @@
 // products of gate queries and block summaries, so their gradients (and
 // those of the optional projections) are small batched GEMMs over ds.
 #include <float.h>
+#include <stdint.h>
+
+#include <algorithm>
 
 #include "common.h"
 #include "kernels.h"
@@ -273,7 +276,7 @@ constexpr float BLOG2E = 1.4426950408889634f;
 // accumulator element is known at compile time (the lane-dependent part of
 // its key index is below 8).
 template <int DH, int LSB>
-__global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
+__device__ __forceinline__ void bwd_dq_bf16_job(const BwdArgs& P, const int qtile, const int h, const int bi) {
   constexpr int KP = DH + 8;
   constexpr int TP = 64 + 4;
   constexpr int KPG = DH / 32;   // keys per thread in the tile staging
@@ -290,8 +293,6 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lk = lane >> 5;
-  const int qtile = gridDim.x - 1 - blockIdx.x;
-  const int h = blockIdx.y, bi = blockIdx.z;
   const int G = P.H / P.Hkv, g = h / G;
   const int n = P.n, B = P.B;
   const int qrow = wave * 32 + lr;  // query row of this lane in the workgroup
@@ -560,6 +561,34 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
     }
 }
 
+// Work queue of the pass kernels: the grid holds only as many workgroups as
+// the chip runs at once, and each takes the next job from a counter in global
+// memory until none is left.  Jobs vary in length by the causal prefix they
+// walk (up to 64x), and a launch of one workgroup per job leaves a large
+// share of the compute units idle while the dispatcher waits for the next
+// workgroup's unit; jobs are numbered longest first.  The counter is reset by
+// the launch before the kernel runs; every workgroup leaves the loop once the
+// counter passes the job count.
+__device__ __forceinline__ int bwd_next_job(uint32_t* counter) {
+  __shared__ int job_s;
+  __syncthreads();  // every thread has finished the previous job (and read job_s)
+  if (threadIdx.x == 0) job_s = (int)atomicAdd(counter, 1u);
+  __syncthreads();
+  return job_s;
+}
+
+template <int DH, int LSB>
+__global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
+  const int nqt = (P.n + 127) / 128, per = P.H * P.b;
+  const int njobs = nqt * per;
+  for (;;) {
+    const int job = bwd_next_job(P.queue);
+    if (job >= njobs) break;
+    const int r = job % per;  // the longest (last) query tiles first, heads and batch inside
+    bwd_dq_bf16_job<DH, LSB>(P, nqt - 1 - job / per, r % P.H, r / P.H);
+  }
+}
+
 // which 32-query chunks select which blocks: mask[b, g, t / 32, m] = 1
 __global__ void bwd_chunk_mask_kernel(const int32_t* __restrict__ sel, int b, int n, int Hkv, int K, int NB,
                                       uint8_t* __restrict__ mask) {
@@ -599,7 +628,7 @@ __global__ void bwd_selmask_kernel(const int32_t* __restrict__ sel, size_t rows,
 // and dP) and transposed (A of dK^T += Q^T dS and dV^T += dO^T P, read in the
 // accumulator's query permutation).  P and dS stay in registers.
 template <int DH>
-__global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
+__device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int ktile, const int g, const int bi) {
   constexpr int NTH = 256, KT = 128;
   constexpr int KP = DH + 8;
   constexpr int QP = 32 + 4;
@@ -616,7 +645,7 @@ __global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lk = lane >> 5;
-  const int k0 = blockIdx.x * KT, g = blockIdx.y, bi = blockIdx.z;
+  const int k0 = ktile * KT;
   const int n = P.n, B = P.B, H = P.H, G = H / P.Hkv;
   const int key = k0 + wave * 32 + lr;
   const bool kvalid = key < n;
@@ -839,6 +868,28 @@ __global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
     }
 }
 
+template <int DH>
+__global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
+  const int nkt = (P.n + 127) / 128, per = P.Hkv * P.b;
+  const int njobs = nkt * per;
+  for (;;) {
+    const int job = bwd_next_job(P.queue + 1);
+    if (job >= njobs) break;
+    const int r = job % per;  // the first (longest) key tiles first
+    bwd_dkv_bf16_job<DH>(P, job / per, r % P.Hkv, r / P.Hkv);
+  }
+}
+
+// workgroups of `kernel` (256 threads) resident on the current device at once
+template <typename F>
+static int resident_workgroups(F kernel) {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, 256, 0) != hipSuccess) return 0;
+  return cus * std::max(per_cu, 1);
+}
+
 static hipError_t launch_attention_backward_bf16(const BwdArgs& P, hipStream_t s) {
   if (P.n > BWD_MAX_SEQ) return hipErrorInvalidValue;
   const int NB = cdiv(P.n, P.B), nqc = cdiv(P.n, 32);
@@ -857,20 +908,19 @@ static hipError_t launch_attention_backward_bf16(const BwdArgs& P, hipStream_t s
     bwd_selmask_kernel<<<(unsigned)cdiv(rows * NW, 256), 256, 0, s>>>(P.sel, rows, P.K, NW, P.selmask);
   }
   if (P.K > 32) return hipErrorInvalidValue;
-  dim3 g1(cdiv(P.n, 128), P.H, P.b);
+  if (!P.queue) return hipErrorInvalidValue;
+  fill_f32_kernel<<<1, 64, 0, s>>>((float*)P.queue, 2, 0.f);  // both job counters to zero
   const int lsb = P.B >= 64 ? 6 : (P.B == 32 ? 5 : 4);
-  if (P.dh == 128) {
-    if (lsb == 6) bwd_dq_bf16_kernel<128, 6><<<g1, 256, 0, s>>>(Q);
-    else if (lsb == 5) bwd_dq_bf16_kernel<128, 5><<<g1, 256, 0, s>>>(Q);
-    else bwd_dq_bf16_kernel<128, 4><<<g1, 256, 0, s>>>(Q);
-  } else {
-    if (lsb == 6) bwd_dq_bf16_kernel<64, 6><<<g1, 256, 0, s>>>(Q);
-    else if (lsb == 5) bwd_dq_bf16_kernel<64, 5><<<g1, 256, 0, s>>>(Q);
-    else bwd_dq_bf16_kernel<64, 4><<<g1, 256, 0, s>>>(Q);
-  }
-  dim3 g2(cdiv(P.n, 128), P.Hkv, P.b);
-  if (P.dh == 128) bwd_dkv_bf16_kernel<128><<<g2, 256, 0, s>>>(Q);
-  else bwd_dkv_bf16_kernel<64><<<g2, 256, 0, s>>>(Q);
+  auto dq = P.dh == 128 ? (lsb == 6 ? bwd_dq_bf16_kernel<128, 6> : lsb == 5 ? bwd_dq_bf16_kernel<128, 5>
+                                                                            : bwd_dq_bf16_kernel<128, 4>)
+                        : (lsb == 6 ? bwd_dq_bf16_kernel<64, 6> : lsb == 5 ? bwd_dq_bf16_kernel<64, 5>
+                                                                           : bwd_dq_bf16_kernel<64, 4>);
+  auto dkv = P.dh == 128 ? bwd_dkv_bf16_kernel<128> : bwd_dkv_bf16_kernel<64>;
+  const long long jq = (long long)cdiv(P.n, 128) * P.H * P.b, jk = (long long)cdiv(P.n, 128) * P.Hkv * P.b;
+  const int rq = resident_workgroups(dq), rk = resident_workgroups(dkv);
+  if (rq <= 0 || rk <= 0 || jq > INT32_MAX || jk > INT32_MAX) return hipErrorInvalidValue;
+  if (jq > 0) dq<<<(unsigned)std::min<long long>(jq, rq), 256, 0, s>>>(Q);
+  if (jk > 0) dkv<<<(unsigned)std::min<long long>(jk, rk), 256, 0, s>>>(Q);
   return hipGetLastError();
 }
 

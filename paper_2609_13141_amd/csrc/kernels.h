@@ -141,6 +141,7 @@ struct BwdArgs {
   float* dlog_gate_full;  // [b, Hkv, n, NB] output (full scope / straight-through)
   float* dlg_head_full;   // [b, H, n, NB] scratch (full scope / straight-through)
   const int32_t* doc;     // [b, NB] first block of each block's document, or null
+  uint32_t* queue;        // [2] job counters of the bf16 pass kernels (reset by the launch)
 };
 // longest sequence of the bf16 attention backward (query chunks of 32 tracked in LDS)
 constexpr int BWD_MAX_SEQ = 262144;
