@@ -153,6 +153,7 @@ struct AttnWs {
   float* sel_bias;
   float* gate_table;  // log gates of every block (full scope, when the caller does not ask for them)
   float* row_lse;     // per-row LSE of the scores while the log-gate table is finished
+  uint32_t* queue;    // job counter of the attention kernel
 };
 
 AttnWs carve_attention(Carve& cv, const sas_config* c, int b, int n) {
@@ -170,6 +171,7 @@ AttnWs carve_attention(Carve& cv, const sas_config* c, int b, int n) {
   w.sel_bias = (float*)cv.take(rows * 4);
   w.gate_table = full_fwd(c) ? (float*)cv.take((size_t)b * c->n_kv_heads * n * NB * 4) : nullptr;
   w.row_lse = (float*)cv.take((size_t)b * c->n_kv_heads * n * 4);
+  w.queue = (uint32_t*)cv.take(256);
   return w;
 }
 
@@ -286,6 +288,7 @@ sas_status run_attention(const sas_config* c, int b, int n, const void* q, const
   aa.full = full_fwd(c);
   aa.gate_table = log_gate;
   aa.doc = doc;
+  aa.queue = ws.queue;
   {
     Timed tm("attention", s);
     HIP_TRY(launch_attention(c->dtype, aa, s), "attention");

@@ -29,17 +29,25 @@
 // The gate enters as the logit bias log g_m (inner) or as a weight g_m on
 // the block's values (outer; the softmax then normalizes unbiased logits).
 #include <float.h>
+#include <stdint.h>
+
+#include <algorithm>
 
 #include "common.h"
 #include "kernels.h"
 
 namespace sas {
 
+__global__ void fill_u32_kernel(uint32_t* p, int n, uint32_t v) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 
 template <int DH, int LSB>
-__global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
+__device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile, const int h, const int bi) {
   constexpr int KP = DH + 8;    // K tile row pitch (elements)
   constexpr int VP = 64 + 4;    // V^T tile row pitch (elements)
   constexpr int KPG = DH / 32;  // keys per thread in the tile staging
@@ -54,8 +62,6 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lk = lane >> 5;
-  const int qtile = gridDim.x - 1 - blockIdx.x;  // heavy (late) tiles first
-  const int h = blockIdx.y, bi = blockIdx.z;
   const int G = P.H / P.Hkv, g = h / G;
   const int n = P.n, B = P.B;
   const int qrow = wave * 32 + lr;
@@ -291,6 +297,20 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
   if (P.lse && lk == 0) P.lse[((size_t)bi * P.H + h) * n + t] = (m_run + log2f(l_run)) * LN2;
 }
 
+// One job (query tile, head, batch entry) per workgroup (grid = job count, no
+// queue) or the work queue; the heavy (late) query tiles first.
+template <int DH, int LSB>
+__global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
+  const int nqt = (P.n + 127) / 128, per = P.H * P.b;
+  const int njobs = nqt * per;
+  for (int it = 0;; ++it) {
+    const int job = P.queue ? queue_next_job(P.queue) : (it == 0 ? (int)blockIdx.x : njobs);
+    if (job >= njobs) break;
+    const int r = job % per;
+    attn_bf16_job<DH, LSB>(P, nqt - 1 - job / per, r % P.H, r / P.H);
+  }
+}
+
 // ---- fp32: one thread per (batch, head, query), online softmax in fp32 ----
 template <int DH>
 __global__ void attn_f32_kernel(AttnArgs P) {
@@ -366,17 +386,22 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
   if (a.n <= 0 || a.b <= 0) return hipSuccess;
   if (dtype == SAS_BF16) {
     if (a.n > ATTN_MAX_SEQ || a.K > 32) return hipErrorInvalidValue;
-    dim3 grid(cdiv(a.n, 128), a.H, a.b);
     const int lsb = a.B >= 64 ? 6 : (a.B == 32 ? 5 : 4);
-    if (a.dh == 128) {
-      if (lsb == 6) attn_bf16_kernel<128, 6><<<grid, 256, 0, s>>>(a);
-      else if (lsb == 5) attn_bf16_kernel<128, 5><<<grid, 256, 0, s>>>(a);
-      else attn_bf16_kernel<128, 4><<<grid, 256, 0, s>>>(a);
-    } else {
-      if (lsb == 6) attn_bf16_kernel<64, 6><<<grid, 256, 0, s>>>(a);
-      else if (lsb == 5) attn_bf16_kernel<64, 5><<<grid, 256, 0, s>>>(a);
-      else attn_bf16_kernel<64, 4><<<grid, 256, 0, s>>>(a);
+    auto kern = a.dh == 128 ? (lsb == 6 ? attn_bf16_kernel<128, 6> : lsb == 5 ? attn_bf16_kernel<128, 5>
+                                                                             : attn_bf16_kernel<128, 4>)
+                            : (lsb == 6 ? attn_bf16_kernel<64, 6> : lsb == 5 ? attn_bf16_kernel<64, 5>
+                                                                            : attn_bf16_kernel<64, 4>);
+    const long long jobs = (long long)cdiv(a.n, 128) * a.H * a.b;
+    const int res = resident_workgroups(kern, 256);
+    if (res <= 0 || jobs > INT32_MAX) return hipErrorInvalidValue;
+    AttnArgs A = a;
+    A.queue = nullptr;
+    if (jobs > res) {
+      if (!a.queue) return hipErrorInvalidValue;
+      fill_u32_kernel<<<1, 64, 0, s>>>(a.queue, 1, 0u);
+      A.queue = a.queue;
     }
+    kern<<<(unsigned)std::min<long long>(jobs, res), 256, 0, s>>>(A);
   } else {
     size_t tot = (size_t)a.b * a.H * a.n;
     unsigned grid = (unsigned)((tot + 127) / 128);

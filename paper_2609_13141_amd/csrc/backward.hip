@@ -561,28 +561,13 @@ __device__ __forceinline__ void bwd_dq_bf16_job(const BwdArgs& P, const int qtil
     }
 }
 
-// Work queue of the pass kernels: the grid holds only as many workgroups as
-// the chip runs at once, and each takes the next job from a counter in global
-// memory until none is left.  Jobs vary in length by the causal prefix they
-// walk (up to 64x), and a launch of one workgroup per job leaves a large
-// share of the compute units idle while the dispatcher waits for the next
-// workgroup's unit; jobs are numbered longest first.  The counter is reset by
-// the launch before the kernel runs; every workgroup leaves the loop once the
-// counter passes the job count.
-__device__ __forceinline__ int bwd_next_job(uint32_t* counter) {
-  __shared__ int job_s;
-  __syncthreads();  // every thread has finished the previous job (and read job_s)
-  if (threadIdx.x == 0) job_s = (int)atomicAdd(counter, 1u);
-  __syncthreads();
-  return job_s;
-}
-
+// One job per workgroup (grid = job count, no queue) or the work queue.
 template <int DH, int LSB>
 __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
   const int nqt = (P.n + 127) / 128, per = P.H * P.b;
   const int njobs = nqt * per;
-  for (;;) {
-    const int job = bwd_next_job(P.queue);
+  for (int it = 0;; ++it) {
+    const int job = P.queue ? queue_next_job(P.queue) : (it == 0 ? (int)blockIdx.x : njobs);
     if (job >= njobs) break;
     const int r = job % per;  // the longest (last) query tiles first, heads and batch inside
     bwd_dq_bf16_job<DH, LSB>(P, nqt - 1 - job / per, r % P.H, r / P.H);
@@ -872,22 +857,12 @@ template <int DH>
 __global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
   const int nkt = (P.n + 127) / 128, per = P.Hkv * P.b;
   const int njobs = nkt * per;
-  for (;;) {
-    const int job = bwd_next_job(P.queue + 1);
+  for (int it = 0;; ++it) {
+    const int job = P.queue ? queue_next_job(P.queue) : (it == 0 ? (int)blockIdx.x : njobs);
     if (job >= njobs) break;
     const int r = job % per;  // the first (longest) key tiles first
     bwd_dkv_bf16_job<DH>(P, job / per, r % P.Hkv, r / P.Hkv);
   }
-}
-
-// workgroups of `kernel` (256 threads) resident on the current device at once
-template <typename F>
-static int resident_workgroups(F kernel) {
-  int dev = 0, cus = 0, per_cu = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, 256, 0) != hipSuccess) return 0;
-  return cus * std::max(per_cu, 1);
 }
 
 static hipError_t launch_attention_backward_bf16(const BwdArgs& P, hipStream_t s) {
@@ -909,7 +884,6 @@ static hipError_t launch_attention_backward_bf16(const BwdArgs& P, hipStream_t s
   }
   if (P.K > 32) return hipErrorInvalidValue;
   if (!P.queue) return hipErrorInvalidValue;
-  fill_f32_kernel<<<1, 64, 0, s>>>((float*)P.queue, 2, 0.f);  // both job counters to zero
   const int lsb = P.B >= 64 ? 6 : (P.B == 32 ? 5 : 4);
   auto dq = P.dh == 128 ? (lsb == 6 ? bwd_dq_bf16_kernel<128, 6> : lsb == 5 ? bwd_dq_bf16_kernel<128, 5>
                                                                             : bwd_dq_bf16_kernel<128, 4>)
@@ -917,10 +891,14 @@ static hipError_t launch_attention_backward_bf16(const BwdArgs& P, hipStream_t s
                                                                            : bwd_dq_bf16_kernel<64, 4>);
   auto dkv = P.dh == 128 ? bwd_dkv_bf16_kernel<128> : bwd_dkv_bf16_kernel<64>;
   const long long jq = (long long)cdiv(P.n, 128) * P.H * P.b, jk = (long long)cdiv(P.n, 128) * P.Hkv * P.b;
-  const int rq = resident_workgroups(dq), rk = resident_workgroups(dkv);
+  const int rq = resident_workgroups(dq, 256), rk = resident_workgroups(dkv, 256);
   if (rq <= 0 || rk <= 0 || jq > INT32_MAX || jk > INT32_MAX) return hipErrorInvalidValue;
-  if (jq > 0) dq<<<(unsigned)std::min<long long>(jq, rq), 256, 0, s>>>(Q);
-  if (jk > 0) dkv<<<(unsigned)std::min<long long>(jk, rk), 256, 0, s>>>(Q);
+  if (jq > rq || jk > rk) fill_f32_kernel<<<1, 64, 0, s>>>((float*)P.queue, 2, 0.f);  // job counters to zero
+  BwdArgs A = Q;
+  A.queue = jq > rq ? P.queue : nullptr;
+  if (jq > 0) dq<<<(unsigned)std::min<long long>(jq, rq), 256, 0, s>>>(A);
+  A.queue = jk > rk ? P.queue + 1 : nullptr;
+  if (jk > 0) dkv<<<(unsigned)std::min<long long>(jk, rk), 256, 0, s>>>(A);
   return hipGetLastError();
 }
 

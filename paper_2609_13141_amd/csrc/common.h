@@ -120,4 +120,31 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Work queue of the attention kernels: the grid holds only as many
+// workgroups as the chip runs at once, and each takes the next job from a
+// counter in global memory until none is left.  Their jobs (query or key
+// tiles) vary in length by the causal prefix they walk, and a launch of one
+// workgroup per job leaves a large share of the compute units idle while the
+// dispatcher waits to place the next workgroup; jobs are numbered longest
+// first.  The counter is reset by the launch before the kernel runs, and
+// every workgroup leaves once the counter has passed the job count.
+__device__ __forceinline__ int queue_next_job(uint32_t* counter) {
+  __shared__ int job_s;
+  __syncthreads();  // every thread has finished the previous job and read job_s
+  if (threadIdx.x == 0) job_s = (int)atomicAdd(counter, 1u);
+  __syncthreads();
+  return job_s;
+}
+
+// workgroups of `kernel` with `threads` threads resident on the current device
+// at once (0 when the runtime cannot tell)
+template <typename F>
+inline int resident_workgroups(F kernel, int threads) {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess) return 0;
+  return cus * (per_cu > 0 ? per_cu : 1);
+}
+
 }  // namespace sas

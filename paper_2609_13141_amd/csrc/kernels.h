@@ -109,6 +109,7 @@ struct AttnArgs {
   int full;               // GATED: every historical block attended, gates from gate_table
   const float* gate_table;  // [b, Hkv, n, NB] log gates (full scope)
   const int32_t* doc;     // [b, NB] first block of each block's document, or null
+  uint32_t* queue;        // job counter of the bf16 kernel's work queue (reset by the launch)
 };
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 // longest sequence of the bf16 attention forward (key tiles of 64 tracked in LDS)
@@ -141,7 +142,7 @@ struct BwdArgs {
   float* dlog_gate_full;  // [b, Hkv, n, NB] output (full scope / straight-through)
   float* dlg_head_full;   // [b, H, n, NB] scratch (full scope / straight-through)
   const int32_t* doc;     // [b, NB] first block of each block's document, or null
-  uint32_t* queue;        // [2] job counters of the bf16 pass kernels (reset by the launch)
+  uint32_t* queue;        // [2] job counters of the bf16 pass kernels' work queues (reset by the launch)
 };
 // longest sequence of the bf16 attention backward (query chunks of 32 tracked in LDS)
 constexpr int BWD_MAX_SEQ = 262144;
