@@ -538,6 +538,7 @@ struct StatsWs {
   float* lvn;
   float* blk_lse;
   uint32_t* head_mask;
+  uint32_t* queue;  // job counter of the statistics kernel
 };
 
 StatsWs carve_stats(Carve& cv, const sas_config* c, int b, int n) {
@@ -546,6 +547,7 @@ StatsWs carve_stats(Carve& cv, const sas_config* c, int b, int n) {
   w.lvn = (float*)cv.take((size_t)b * n * Hkv * 4);
   w.blk_lse = (float*)cv.take((size_t)b * H * n * NB * 4);
   w.head_mask = (uint32_t*)cv.take((size_t)b * H * n * cdiv(NB, (size_t)32) * 4);
+  w.queue = (uint32_t*)cv.take(256);
   return w;
 }
 
@@ -896,6 +898,7 @@ sas_status sas_selection_stats(const sas_config* c, int32_t batch, int32_t seq_l
   a.cov_v = out->cov_v;
   a.blk_lse = out->ref_union ? w.blk_lse : nullptr;
   a.doc = in->doc_first_block;
+  a.queue = w.queue;
   {
     Timed tm("stats", s);
     HIP_TRY(launch_stats(c->dtype, a, s), "selection stats");

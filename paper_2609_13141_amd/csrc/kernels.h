@@ -193,6 +193,7 @@ struct StatsArgs {
   float* cov_v;           // [b, H, n] or null
   float* blk_lse;         // [b, H, n, NB] log2 mass of each historical block, or null
   const int32_t* doc;     // [b, NB] first block of each block's document, or null
+  uint32_t* queue;        // job counter of the bf16 kernel's work queue (reset by the launch)
 };
 hipError_t launch_stats(int dtype, const StatsArgs& a, hipStream_t s);
 // per-head Top-K by block mass -> head_mask [b, H, n, W]; majority per group OR-ed into uni [b, Hkv, n, W]

@@ -165,7 +165,7 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
   float* mg_l = (float*)(pool + KMAX * WAVE * 12 + WAVE * 8);        // [WAVE] running sum
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = blockIdx.y, bi = blockIdx.z;
-  const int t0 = blockIdx.x * WAVE;
+  const int t0 = (gridDim.x - 1 - blockIdx.x) * WAVE;  // the late rows (more blocks to score) first
   const int t = t0 + lane;
   const bool valid = t < P.n;
   const int G = P.H / P.Hkv;

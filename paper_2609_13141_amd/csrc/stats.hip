@@ -12,6 +12,10 @@
 // logits for the reference Top-K.
 #include <float.h>
 
+#include <stdint.h>
+
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -43,7 +47,7 @@ __device__ __forceinline__ float lse2(float a, float b) {
 }
 
 template <int DH, int LSB>
-__global__ void __launch_bounds__(256, 2) stats_bf16_kernel(StatsArgs P) {
+__device__ __forceinline__ void stats_bf16_job(const StatsArgs& P, const int qtile, const int h, const int bi) {
   constexpr int KP = DH + 8;
   constexpr int KPG = DH / 32;
   constexpr int C8 = DH / 8;
@@ -55,8 +59,6 @@ __global__ void __launch_bounds__(256, 2) stats_bf16_kernel(StatsArgs P) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lk = lane >> 5;
-  const int qtile = gridDim.x - 1 - blockIdx.x;
-  const int h = blockIdx.y, bi = blockIdx.z;
   const int G = P.H / P.Hkv, g = h / G;
   const int n = P.n, B = P.B;
   const int qrow = wave * 32 + lr;
@@ -221,6 +223,20 @@ __global__ void __launch_bounds__(256, 2) stats_bf16_kernel(StatsArgs P) {
   if (!qvalid || lk != 0) return;
   if (P.cov) P.cov[hrow] = l_S / l_all;
   if (P.cov_v) P.cov_v[hrow] = l_vS / l_vall;
+}
+
+// One job (query tile, head, batch entry) per workgroup (grid = job count, no
+// queue) or the work queue; the heavy (late) query tiles first.
+template <int DH, int LSB>
+__global__ void __launch_bounds__(256, 2) stats_bf16_kernel(StatsArgs P) {
+  const int nqt = (P.n + 127) / 128, per = P.H * P.b;
+  const int njobs = nqt * per;
+  for (int it = 0;; ++it) {
+    const int job = P.queue ? queue_next_job(P.queue) : (it == 0 ? (int)blockIdx.x : njobs);
+    if (job >= njobs) break;
+    const int r = job % per;
+    stats_bf16_job<DH, LSB>(P, nqt - 1 - job / per, r % P.H, r / P.H);
+  }
 }
 
 // fp32: one thread per (batch, head, query), sums in fp32 against running maxima
@@ -422,17 +438,23 @@ hipError_t launch_stats(int dtype, const StatsArgs& a, hipStream_t s) {
     else stats_f32_kernel<64><<<(unsigned)cdiv(tot, 64), 64, 0, s>>>(a);
     return hipGetLastError();
   }
-  dim3 grid(cdiv(a.n, 128), a.H, a.b);
   const int lsb = a.B >= 64 ? 6 : (a.B == 32 ? 5 : 4);
-  if (a.dh == 128) {
-    if (lsb == 6) stats_bf16_kernel<128, 6><<<grid, 256, 0, s>>>(a);
-    else if (lsb == 5) stats_bf16_kernel<128, 5><<<grid, 256, 0, s>>>(a);
-    else stats_bf16_kernel<128, 4><<<grid, 256, 0, s>>>(a);
-  } else {
-    if (lsb == 6) stats_bf16_kernel<64, 6><<<grid, 256, 0, s>>>(a);
-    else if (lsb == 5) stats_bf16_kernel<64, 5><<<grid, 256, 0, s>>>(a);
-    else stats_bf16_kernel<64, 4><<<grid, 256, 0, s>>>(a);
+  auto kern = a.dh == 128 ? (lsb == 6 ? stats_bf16_kernel<128, 6> : lsb == 5 ? stats_bf16_kernel<128, 5>
+                                                                              : stats_bf16_kernel<128, 4>)
+                          : (lsb == 6 ? stats_bf16_kernel<64, 6> : lsb == 5 ? stats_bf16_kernel<64, 5>
+                                                                             : stats_bf16_kernel<64, 4>);
+  const long long jobs = (long long)cdiv(a.n, 128) * a.H * a.b;
+  const int res = resident_workgroups(kern, 256);
+  if (res <= 0 || jobs > INT32_MAX) return hipErrorInvalidValue;
+  StatsArgs A = a;
+  A.queue = nullptr;
+  if (jobs > res) {
+    if (!a.queue) return hipErrorInvalidValue;
+    const hipError_t e = launch_fill_f32((float*)a.queue, 1, 0.f, s);  // the job counter to zero
+    if (e != hipSuccess) return e;
+    A.queue = a.queue;
   }
+  kern<<<(unsigned)std::min<long long>(jobs, res), 256, 0, s>>>(A);
   return hipGetLastError();
 }
 
