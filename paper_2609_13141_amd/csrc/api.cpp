@@ -457,8 +457,10 @@ DecodeWs carve_decode(Carve& cv, const sas_config* c, int b, int max_blocks) {
 struct BwdWs {
   float* delta;
   float* dlg_head;
-  uint8_t* chunk_mask;
   uint32_t* selmask;
+  int* tile_cnt;
+  int* tile_off;
+  int* tile_rows;
   float* sel_bias;
   float* dlg_head_full;  // [b, H, n, NB] (full scope)
   float* dlg_slots;      // [b, Hkv, n, K] per-slot gradient when only the table is asked for
@@ -467,11 +469,14 @@ struct BwdWs {
 
 BwdWs carve_backward(Carve& cv, const sas_config* c, int b, int n) {
   const size_t H = c->n_heads, Hkv = c->n_kv_heads, K = c->top_k > 0 ? c->top_k : 0;
-  const size_t NB = cdiv(n, c->block_size), nqc = cdiv(n, 32);
+  const size_t NB = cdiv(n, c->block_size);
   BwdWs w;
   w.delta = (float*)cv.take((size_t)b * H * n * 4);
   w.dlg_head = (float*)cv.take((size_t)b * H * n * K * 4);
-  w.chunk_mask = (uint8_t*)cv.take(align_up((size_t)b * Hkv * nqc * NB, 4));
+  const size_t ntk = cdiv(n, 64);
+  w.tile_cnt = (int*)cv.take((size_t)b * Hkv * ntk * 4);
+  w.tile_off = (int*)cv.take((size_t)b * Hkv * ntk * 4);
+  w.tile_rows = (int*)cv.take(K > 0 ? (size_t)b * Hkv * n * 2 * (K + 1) * 4 : 0);
   w.selmask = (uint32_t*)cv.take((size_t)b * Hkv * n * cdiv(NB, (size_t)32) * 4);
   w.sel_bias = (float*)cv.take((size_t)b * Hkv * n * K * 4);
   w.dlg_head_full = full_grad(c) ? (float*)cv.take((size_t)b * H * n * NB * 4) : nullptr;
@@ -715,8 +720,10 @@ sas_status sas_attention_backward(const sas_config* c, int32_t batch, int32_t se
   a.dlog_gate = slots;
   a.delta = bw.delta;
   a.dlg_head = bw.dlg_head;
-  a.chunk_mask = bw.chunk_mask;
   a.selmask = bw.selmask;
+  a.tile_cnt = bw.tile_cnt;
+  a.tile_off = bw.tile_off;
+  a.tile_rows = bw.tile_rows;
   a.queue = bw.queue;
   a.log_gate = gated ? in->log_gate : nullptr;
   a.outer = gated && c->gate_pos == SAS_GATE_OUTER;

@@ -574,20 +574,6 @@ __global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
   }
 }
 
-// which 32-query chunks select which blocks: mask[b, g, t / 32, m] = 1
-__global__ void bwd_chunk_mask_kernel(const int32_t* __restrict__ sel, int b, int n, int Hkv, int K, int NB,
-                                      uint8_t* __restrict__ mask) {
-  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (size_t)b * Hkv * n * K) return;
-  const int m = sel[idx];
-  if (m < 0 || m >= NB) return;
-  const size_t bgt = idx / K;  // (b, g, t)
-  const int t = (int)(bgt % n);
-  const size_t bg = bgt / n;
-  const int nqc = (n + 31) / 32;
-  mask[(bg * nqc + t / 32) * NB + m] = 1;
-}
-
 // selection bitmask of each row: bit m of word m / 32 is set when block m is selected
 __global__ void bwd_selmask_kernel(const int32_t* __restrict__ sel, size_t rows, int K, int NW,
                                    uint32_t* __restrict__ mask) {
@@ -603,29 +589,100 @@ __global__ void bwd_selmask_kernel(const int32_t* __restrict__ sel, size_t rows,
   mask[idx] = bits;
 }
 
-// Pass 2 (dK, dV): one workgroup of 4 waves per 128 keys of one (batch, KV
+// The rows of (b, g) that attend key tile j (keys 64 j .. 64 j + 63), in
+// ascending order: the rows t >= 64 j whose own block lies in the tile (the
+// causal part of the current block) and every later row that selected one of
+// the tile's blocks (at most four; they share one mask word since a tile
+// starts at a multiple of 64 / B blocks).  Without `rows` the kernel writes
+// the count of tile j; with it, the rows at off[tile].  One workgroup of 256
+// threads per (tile, group, batch entry); the ballot prefix sums keep the
+// order, so the lists are an exact function of the selection.
+__global__ void __launch_bounds__(256) bwd_tile_rows_kernel(const uint32_t* __restrict__ selmask, int n, int Hkv,
+                                                            int B, int NW, int ntiles, int* __restrict__ cnt,
+                                                            const int* __restrict__ off, int* __restrict__ rows) {
+  __shared__ int wsum[4];
+  const int j = blockIdx.x, g = blockIdx.y, bi = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const size_t tile = ((size_t)bi * Hkv + g) * ntiles + j;
+  const int k0 = j * 64, m_lo = k0 / B, m_hi = min(n - 1, k0 + 63) / B;
+  const int own_end = min(n, (m_hi + 1) * B);
+  const uint32_t bits = ((2u << (m_hi - m_lo)) - 1u) << (m_lo & 31);
+  const uint32_t* sm = selmask + ((size_t)bi * Hkv + g) * (size_t)n * NW + (m_lo >> 5);
+  const int base = rows ? off[tile] : 0;
+  int total = 0;
+  for (int t0 = k0; t0 < n; t0 += 256) {
+    const int t = t0 + tid;
+    bool f = false;
+    if (t < n) f = t < own_end || (sm[(size_t)t * NW] & bits) != 0;
+    const uint64_t bal = __ballot(f);
+    if (lane == 0) wsum[wave] = __popcll(bal);
+    __syncthreads();
+    int before = __popcll(bal & ((1ull << lane) - 1ull)), all = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      before += w < wave ? wsum[w] : 0;
+      all += wsum[w];
+    }
+    if (rows && f) rows[base + total + before] = t;
+    total += all;
+    __syncthreads();  // wsum is rewritten by the next step
+  }
+  if (!rows && tid == 0) cnt[tile] = total;
+}
+
+// exclusive prefix sum of the tile counts (one workgroup of 1024 threads; each
+// thread sums a contiguous range, then the ranges are offset in order)
+__global__ void __launch_bounds__(1024) bwd_rows_scan_kernel(const int* __restrict__ cnt, int T, int* __restrict__ off) {
+  __shared__ int part[1024];
+  const int tid = threadIdx.x;
+  const int per = (T + 1023) / 1024, lo = min(T, tid * per), hi = min(T, lo + per);
+  int s = 0;
+  for (int i = lo; i < hi; ++i) s += cnt[i];
+  part[tid] = s;
+  __syncthreads();
+  if (tid == 0) {
+    int run = 0;
+    for (int i = 0; i < 1024; ++i) {
+      const int v = part[i];
+      part[i] = run;
+      run += v;
+    }
+  }
+  __syncthreads();
+  int run = part[tid];
+  for (int i = lo; i < hi; ++i) {
+    off[i] = run;
+    run += cnt[i];
+  }
+}
+
+// Pass 2 (dK, dV): one workgroup of 2 waves per 64 keys of one (batch, KV
 // group); each wave owns 32 keys, held in registers as the B operands of
-// S = Q K^T and dP = dO V^T over 32-query chunks (lane = key, 16 query rows).
-// The chunks that attend the tile (their queries reach into its blocks, or
-// select one) are flagged in LDS first.  Work items are (chunk, head of the
-// group); the Q and dO rows of the next item are loaded into registers while
-// the current one is multiplied, then written to LDS both row-major (A of S
-// and dP) and transposed (A of dK^T += Q^T dS and dV^T += dO^T P, read in the
-// accumulator's query permutation).  P and dS stay in registers.
+// S = Q K^T and dP = dO V^T over chunks of 32 query rows (lane = key, 16 rows
+// per lane).  The rows are those of the tile's list (selections), or, when
+// every earlier block is attended (DENSE, full scope), the consecutive rows
+// from the tile on, in chunks of 32 that reach the tile.  Work items are
+// (chunk, head of the group); the row indices of the next chunk are read one
+// chunk ahead, and the Q and dO rows of the next item are loaded into
+// registers while the current one is multiplied, then written to LDS both
+// row-major (A of S and dP) and transposed (A of dK^T += Q^T dS and
+// dV^T += dO^T P, read in the accumulator's row permutation).  P and dS stay
+// in registers; the causal mask compares each key with its row's index.
 template <int DH>
 __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int ktile, const int g, const int bi) {
-  constexpr int NTH = 256, KT = 128;
+  constexpr int NTH = 128, KT = 64;
   constexpr int KP = DH + 8;
   constexpr int QP = 32 + 4;
-  constexpr int C8 = DH / 8;      // 16-byte pieces of a row
-  constexpr int QPT = DH / 64;    // chunk rows staged per thread
+  constexpr int C8 = DH / 8;            // 16-byte pieces of a row
+  constexpr int QPT = 32 * C8 / NTH;    // chunk rows staged per thread (4 or 2)
   __shared__ __align__(16) bf16_t Qs[32 * KP];
   __shared__ __align__(16) bf16_t Ds[32 * KP];
   __shared__ __align__(16) bf16_t Qt[DH * QP];
   __shared__ __align__(16) bf16_t Dt[DH * QP];
   __shared__ __align__(16) float delta_s[32];
-  __shared__ __align__(16) float off_s[8][32];  // log2-domain bias - LSE per (sub-block, row); -inf: not attended
-  __shared__ __align__(16) float wt_s[8][32];   // value weight per (sub-block, row) (outer gate)
+  __shared__ __align__(16) int trow_s[32];      // row index of each staged row (n: none)
+  __shared__ __align__(16) float off_s[4][32];  // log2-domain bias - LSE per (sub-block, row); -inf: not attended
+  __shared__ __align__(16) float wt_s[4][32];   // value weight per (sub-block, row) (outer gate)
   __shared__ uint32_t flags[BWD_MAX_SEQ / 32 / 32];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -635,33 +692,38 @@ __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int kti
   const int key = k0 + wave * 32 + lr;
   const bool kvalid = key < n;
   const int bshift = 31 - __clz(B < 64 ? B : 64);
-  const int nsb = KT >> bshift;  // sub-blocks of min(B, 64) keys in the tile: 2, 4 or 8
-  const int m_lo = k0 / B, m_hi = min(n - 1, k0 + KT - 1) / B;
+  const int nsb = KT >> bshift;  // sub-blocks of min(B, 64) keys in the tile: 1, 2 or 4
+  const int m_hi = min(n - 1, k0 + KT - 1) / B;
   const int NB = (n + B - 1) / B;
   const int NW = (NB + 31) / 32;
   const int nqc = (n + 31) / 32;
   const bool dense = P.mode == SAS_MODE_DENSE, gated = P.mode == SAS_MODE_GATED;
   const bool ste = gated && P.ste, outer = gated && P.outer;
   const bool fullatt = gated && P.full && !P.ste;  // every historical block attended, gates from the table
-  const bool use_mask = !dense && !fullatt && P.K > 0;
+  const bool use_list = P.tile_rows != nullptr;    // selections: the tile's row list
   const size_t grow = ((size_t)bi * P.Hkv + g) * n;  // first row of (b, g) in [b, Hkv, n, ...]
+  const int ntk = (n + KT - 1) / KT;
+  int lbase = 0, lcnt = 0;
+  if (use_list) {
+    const size_t tile = ((size_t)bi * P.Hkv + g) * ntk + ktile;
+    lbase = P.tile_off[tile];
+    lcnt = P.tile_cnt[tile];
+  }
+  const int nchunk = use_list ? (lcnt + 31) / 32 : nqc;
 
-  // chunks attending the tile
-  const int qc0 = k0 / 32;
-  for (int w = tid; w < (nqc + 31) / 32; w += NTH) flags[w] = 0;
-  __syncthreads();
-  {
-    const uint8_t* cm = use_mask ? P.chunk_mask + ((size_t)bi * P.Hkv + g) * nqc * NB : nullptr;
+  // without a list: the chunks that reach the tile (their rows lie in its blocks, or,
+  // every earlier block being attended, their earliest row's document starts in time)
+  const int qc0 = use_list ? 0 : k0 / 32;
+  if (!use_list) {
+    for (int w = tid; w < (nqc + 31) / 32; w += NTH) flags[w] = 0;
+    __syncthreads();
     for (int qc = qc0 + tid; qc < nqc; qc += NTH) {
-      // the chunk reaches into the tile's current blocks, or (dense / full scope) its
-      // earliest row's document starts at or before the tile's last block
-      bool any = ((dense || fullatt) && doc_first(P.doc, bi, NB, qc * 32, B) <= m_hi) || (qc * 32) / B <= m_hi;
-      if (!any && cm)
-        for (int m = m_lo; m <= m_hi; ++m) any |= cm[(size_t)qc * NB + m] != 0;
+      const bool any = ((dense || fullatt) && doc_first(P.doc, bi, NB, qc * 32, B) <= m_hi) || (qc * 32) / B <= m_hi;
       if (any) atomicOr(&flags[qc >> 5], 1u << (qc & 31));
     }
+    __syncthreads();
   }
-  __syncthreads();
+  auto next_chunk = [&](int c) { return use_list ? c : next_set(flags, c, nqc); };
 
   bf16x8_t kb[DH / 16], vb[DH / 16];
   {
@@ -684,39 +746,63 @@ __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int kti
     }
   const float qk_scale = P.sm_scale * BLOG2E;
 
-  // staging roles: rows qg * QPT + i, 16-byte piece c8; lse/delta row tid; bias (row, sub-block)
+  // staging roles: rows qg * QPT + i, 16-byte piece c8; row index / delta row bq (tid < 32);
+  // bias (row bq, sub-block bsb)
   const int c8 = tid % C8, qg = tid / C8;
   const int bq = tid & 31, bsb = tid >> 5;
+  // row index of staged row r of chunk c (n: none)
+  auto row_of = [&](int c, int r) -> int {
+    if (use_list) {
+      const int i = c * 32 + r;
+      return i < lcnt ? P.tile_rows[lbase + i] : n;
+    }
+    const int t = c * 32 + r;
+    return t < n ? t : n;
+  };
+  // row indices of the chunk being loaded (rt, bt) and of the chunk after it (rt_n, bt_n)
+  int rt[QPT], rt_n[QPT], bt = n, bt_n = n;
   uint4 rq[QPT], rd[QPT];
   float r_lse = 0.f, r_delta = 0.f, r_lg = 0.f;
   uint32_t r_mw = 0;
   int r_fb = 0;  // first block of the row's document
+  int pc = -1;   // chunk whose row indices are in rt
 
+  auto load_rows = [&](int c, int* dst, int& b) {
+#pragma unroll
+    for (int i = 0; i < QPT; ++i) dst[i] = c < nchunk ? row_of(c, qg * QPT + i) : n;
+    b = c < nchunk ? row_of(c, bq) : n;
+  };
   auto prefetch = [&](int qc, int hg) {
-    const int q0 = qc * 32, h = g * G + hg;
+    if (qc != pc) {  // a new chunk: its rows were read one chunk ahead
+#pragma unroll
+      for (int i = 0; i < QPT; ++i) rt[i] = rt_n[i];
+      bt = bt_n;
+      pc = qc;
+      load_rows(next_chunk(qc + 1), rt_n, bt_n);
+    }
+    const int h = g * G + hg;
 #pragma unroll
     for (int i = 0; i < QPT; ++i) {
-      const int t = q0 + qg * QPT + i;
+      const int t = rt[i];
       const size_t off = (((size_t)bi * n + t) * H + h) * DH + c8 * 8;
       rq[i] = t < n ? *(const uint4*)((const bf16_t*)P.Q + off) : make_uint4(0, 0, 0, 0);
       rd[i] = t < n ? *(const uint4*)((const bf16_t*)P.dO + off) : make_uint4(0, 0, 0, 0);
     }
-    if (tid < 32) {
-      const int t = q0 + tid;
-      r_delta = t < n ? P.delta[((size_t)bi * H + h) * n + t] : 0.f;
-    }
+    const int t = bt;
+    if (tid < 32) r_delta = t < n ? P.delta[((size_t)bi * H + h) * n + t] : 0.f;
     if (bsb < nsb) {
-      const int t = q0 + bq, kstart = k0 + (bsb << bshift), m = kstart / B;
+      const int kstart = k0 + (bsb << bshift), m = kstart / B;
       r_lse = t < n ? P.lse[((size_t)bi * H + h) * n + t] : 0.f;
       r_fb = t < n ? doc_first(P.doc, bi, NB, t, B) : 0;
+      r_mw = 0u;
+      r_lg = 0.f;
       if (t < n && kstart <= t && m != t / B) {
-        r_mw = use_mask ? P.selmask[(grow + t) * NW + (m >> 5)] : 0u;
-        r_lg = gated && (use_mask || fullatt) ? P.log_gate[(grow + t) * NB + m] : 0.f;
+        r_mw = use_list ? P.selmask[(grow + t) * NW + (m >> 5)] : 0u;
+        r_lg = gated && (use_list || fullatt) ? P.log_gate[(grow + t) * NB + m] : 0.f;
       }
     }
   };
-  auto commit = [&](int qc) {
-    const int q0 = qc * 32;
+  auto commit = [&]() {
 #pragma unroll
     for (int i = 0; i < QPT; ++i) {
       *(uint4*)(Qs + (qg * QPT + i) * KP + c8 * 8) = rq[i];
@@ -726,21 +812,28 @@ __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int kti
     for (int e = 0; e < 8; ++e) {
       const int sh = (e & 1) * 16;
       const int wd = e >> 1;
-      if constexpr (QPT == 2) {
-        const uint32_t pq = ((((const uint32_t*)&rq[0])[wd] >> sh) & 0xffffu) |
-                            (((((const uint32_t*)&rq[1])[wd] >> sh) & 0xffffu) << 16);
-        const uint32_t pd = ((((const uint32_t*)&rd[0])[wd] >> sh) & 0xffffu) |
-                            (((((const uint32_t*)&rd[1])[wd] >> sh) & 0xffffu) << 16);
-        *(uint32_t*)(Qt + (c8 * 8 + e) * QP + qg * 2) = pq;
-        *(uint32_t*)(Dt + (c8 * 8 + e) * QP + qg * 2) = pd;
+      uint32_t x[QPT], y[QPT];
+#pragma unroll
+      for (int i = 0; i < QPT; ++i) {
+        x[i] = (((const uint32_t*)&rq[i])[wd] >> sh) & 0xffffu;
+        y[i] = (((const uint32_t*)&rd[i])[wd] >> sh) & 0xffffu;
+      }
+      bf16_t* qd = Qt + (c8 * 8 + e) * QP + qg * QPT;
+      bf16_t* dd = Dt + (c8 * 8 + e) * QP + qg * QPT;
+      if constexpr (QPT == 4) {
+        *(uint2*)qd = make_uint2(x[0] | (x[1] << 16), x[2] | (x[3] << 16));
+        *(uint2*)dd = make_uint2(y[0] | (y[1] << 16), y[2] | (y[3] << 16));
       } else {
-        Qt[(c8 * 8 + e) * QP + qg] = (bf16_t)((((const uint32_t*)&rq[0])[wd] >> sh) & 0xffffu);
-        Dt[(c8 * 8 + e) * QP + qg] = (bf16_t)((((const uint32_t*)&rd[0])[wd] >> sh) & 0xffffu);
+        *(uint32_t*)qd = x[0] | (x[1] << 16);
+        *(uint32_t*)dd = y[0] | (y[1] << 16);
       }
     }
-    if (tid < 32) delta_s[tid] = r_delta;
+    if (tid < 32) {
+      delta_s[tid] = r_delta;
+      trow_s[tid] = bt;
+    }
     if (bsb < nsb) {
-      const int t = q0 + bq, kstart = k0 + (bsb << bshift), m = kstart / B;
+      const int t = bt, kstart = k0 + (bsb << bshift), m = kstart / B;
       float bb = -INFINITY, w = 1.f;
       if (t < n && kstart <= t) {
         if (m == t / B || (dense && m >= r_fb)) {
@@ -756,18 +849,18 @@ __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int kti
     }
   };
 
-  int qc = next_set(flags, qc0, nqc), hg = 0;
-  if (qc < nqc) prefetch(qc, 0);
-  while (qc < nqc) {
-    commit(qc);
+  int qc = next_chunk(qc0), hg = 0;
+  load_rows(qc, rt_n, bt_n);
+  if (qc < nchunk) prefetch(qc, 0);
+  while (qc < nchunk) {
+    commit();
     lds_barrier();
     int nq = qc, nh = hg + 1;
     if (nh == G) {
       nh = 0;
-      nq = next_set(flags, qc + 1, nqc);
+      nq = next_chunk(qc + 1);
     }
-    if (nq < nqc) prefetch(nq, nh);
-    const int q0 = qc * 32;
+    if (nq < nchunk) prefetch(nq, nh);
 
     floatx16_t sc, dp;
 #pragma unroll
@@ -782,28 +875,30 @@ __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int kti
       const bf16x8_t ad = *(const bf16x8_t*)(Ds + lr * KP + ks * 16 + lk * 8);
       dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ad, vb[ks], dp, 0, 0, 0);
     }
-    // lane: key column `key`; rows = queries q0 + 8 j + 4 lk + i (v = 4 j + i)
+    // lane: key column `key`; staged rows 8 j + 4 lk + i (v = 4 j + i)
     const int sbk = (wave * 32 + lr) >> bshift;
-    const bool diag = q0 < k0 + KT;  // the chunk meets the tile's diagonal: mask key > t
+    const bool diag = trow_s[0] < k0 + KT - 1;  // some row precedes a key of the tile: mask key > row
     floatx16_t pp;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const float4 of = *(const float4*)&off_s[sbk][8 * j + 4 * lk];
       const float4 de = *(const float4*)&delta_s[8 * j + 4 * lk];
+      const int4 tr = *(const int4*)&trow_s[8 * j + 4 * lk];
       float4 wt = make_float4(1.f, 1.f, 1.f, 1.f);
       if (outer) wt = *(const float4*)&wt_s[sbk][8 * j + 4 * lk];
       const float ofv[4] = {of.x, of.y, of.z, of.w}, dev[4] = {de.x, de.y, de.z, de.w};
       const float wv[4] = {wt.x, wt.y, wt.z, wt.w};
+      const int trv[4] = {tr.x, tr.y, tr.z, tr.w};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int v = 4 * j + i;
         float p = __builtin_amdgcn_exp2f(fmaf(sc[v], qk_scale, ofv[i]));
-        if (diag && key > q0 + 8 * j + 4 * lk + i) p = 0.f;
+        if (diag && key > trv[i]) p = 0.f;
         pp[v] = p * wv[i];
         sc[v] = p * (wv[i] * dp[v] - dev[i]);
       }
     }
-    // dV^T += dO^T P and dK^T += Q^T dS, 16 queries per step in the accumulator's query permutation
+    // dV^T += dO^T P and dK^T += Q^T dS, 16 rows per step in the accumulator's row permutation
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       uint4 pu, su;
@@ -854,8 +949,8 @@ __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int kti
 }
 
 template <int DH>
-__global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
-  const int nkt = (P.n + 127) / 128, per = P.Hkv * P.b;
+__global__ void __launch_bounds__(128) bwd_dkv_bf16_kernel(BwdArgs P) {
+  const int nkt = (P.n + 63) / 64, per = P.Hkv * P.b;
   const int njobs = nkt * per;
   for (int it = 0;; ++it) {
     const int job = P.queue ? queue_next_job(P.queue) : (it == 0 ? (int)blockIdx.x : njobs);
@@ -867,38 +962,50 @@ __global__ void __launch_bounds__(256) bwd_dkv_bf16_kernel(BwdArgs P) {
 
 static hipError_t launch_attention_backward_bf16(const BwdArgs& P, hipStream_t s) {
   if (P.n > BWD_MAX_SEQ) return hipErrorInvalidValue;
-  const int NB = cdiv(P.n, P.B), nqc = cdiv(P.n, 32);
-  BwdArgs Q = P;
-  const bool marks = P.mode != SAS_MODE_DENSE && P.K > 0;  // selected blocks to mark
-  if (!marks) {
-    Q.chunk_mask = nullptr;
-    Q.selmask = nullptr;
-  } else {
-    const size_t bytes = (size_t)P.b * P.Hkv * nqc * NB;
-    fill_f32_kernel<<<(unsigned)cdiv(cdiv(bytes, 4), 256), 256, 0, s>>>((float*)P.chunk_mask, cdiv(bytes, 4), 0.f);
-    const size_t tot = (size_t)P.b * P.Hkv * P.n * P.K;
-    bwd_chunk_mask_kernel<<<(unsigned)cdiv(tot, 256), 256, 0, s>>>(P.sel, P.b, P.n, P.Hkv, P.K, NB, P.chunk_mask);
-    const size_t rows = (size_t)P.b * P.Hkv * P.n;
-    const int NW = cdiv(NB, 32);
-    bwd_selmask_kernel<<<(unsigned)cdiv(rows * NW, 256), 256, 0, s>>>(P.sel, rows, P.K, NW, P.selmask);
-  }
   if (P.K > 32) return hipErrorInvalidValue;
   if (!P.queue) return hipErrorInvalidValue;
+  const int NB = cdiv(P.n, P.B), NW = cdiv(NB, 32), ntk = cdiv(P.n, 64);
+  BwdArgs Q = P;
+  const bool marks = P.mode != SAS_MODE_DENSE && P.K > 0;  // selected blocks to mark
+  const bool fullatt = P.mode == SAS_MODE_GATED && P.full && !P.ste;
+  Q.tile_rows = nullptr;
+  Q.tile_cnt = nullptr;
+  Q.tile_off = nullptr;
+  if (!marks) {
+    Q.selmask = nullptr;
+  } else {
+    const size_t rows = (size_t)P.b * P.Hkv * P.n;
+    bwd_selmask_kernel<<<(unsigned)cdiv(rows * NW, 256), 256, 0, s>>>(P.sel, rows, P.K, NW, P.selmask);
+    if (!fullatt) {
+      // each tile's list of attending rows: counts, offsets, rows
+      if (!P.tile_rows || !P.tile_cnt || !P.tile_off) return hipErrorInvalidValue;
+      const long long T = (long long)P.b * P.Hkv * ntk;
+      if (T > INT32_MAX || rows * 2 * (P.K + 1) > (size_t)INT32_MAX) return hipErrorInvalidValue;
+      const dim3 grid(ntk, P.Hkv, P.b);
+      bwd_tile_rows_kernel<<<grid, 256, 0, s>>>(P.selmask, P.n, P.Hkv, P.B, NW, ntk, P.tile_cnt, nullptr, nullptr);
+      bwd_rows_scan_kernel<<<1, 1024, 0, s>>>(P.tile_cnt, (int)T, P.tile_off);
+      bwd_tile_rows_kernel<<<grid, 256, 0, s>>>(P.selmask, P.n, P.Hkv, P.B, NW, ntk, P.tile_cnt, P.tile_off,
+                                                P.tile_rows);
+      Q.tile_rows = P.tile_rows;
+      Q.tile_cnt = P.tile_cnt;
+      Q.tile_off = P.tile_off;
+    }
+  }
   const int lsb = P.B >= 64 ? 6 : (P.B == 32 ? 5 : 4);
   auto dq = P.dh == 128 ? (lsb == 6 ? bwd_dq_bf16_kernel<128, 6> : lsb == 5 ? bwd_dq_bf16_kernel<128, 5>
                                                                             : bwd_dq_bf16_kernel<128, 4>)
                         : (lsb == 6 ? bwd_dq_bf16_kernel<64, 6> : lsb == 5 ? bwd_dq_bf16_kernel<64, 5>
                                                                            : bwd_dq_bf16_kernel<64, 4>);
   auto dkv = P.dh == 128 ? bwd_dkv_bf16_kernel<128> : bwd_dkv_bf16_kernel<64>;
-  const long long jq = (long long)cdiv(P.n, 128) * P.H * P.b, jk = (long long)cdiv(P.n, 128) * P.Hkv * P.b;
-  const int rq = resident_workgroups(dq, 256), rk = resident_workgroups(dkv, 256);
+  const long long jq = (long long)cdiv(P.n, 128) * P.H * P.b, jk = (long long)ntk * P.Hkv * P.b;
+  const int rq = resident_workgroups(dq, 256), rk = resident_workgroups(dkv, 128);
   if (rq <= 0 || rk <= 0 || jq > INT32_MAX || jk > INT32_MAX) return hipErrorInvalidValue;
   if (jq > rq || jk > rk) fill_f32_kernel<<<1, 64, 0, s>>>((float*)P.queue, 2, 0.f);  // job counters to zero
   BwdArgs A = Q;
   A.queue = jq > rq ? P.queue : nullptr;
   if (jq > 0) dq<<<(unsigned)std::min<long long>(jq, rq), 256, 0, s>>>(A);
   A.queue = jk > rk ? P.queue + 1 : nullptr;
-  if (jk > 0) dkv<<<(unsigned)std::min<long long>(jk, rk), 256, 0, s>>>(A);
+  if (jk > 0) dkv<<<(unsigned)std::min<long long>(jk, rk), 128, 0, s>>>(A);
   return hipGetLastError();
 }
 

@@ -135,8 +135,12 @@ struct BwdArgs {
   float* delta;           // [b, H, n]
   float* dlg_head;        // [b, H, n, K]
   const float* log_gate;  // [b, Hkv, n, ceil(n/B)] (GATED)
-  uint8_t* chunk_mask;    // [b, Hkv, ceil(n/32), ceil(n/B)] (bf16 path)
   uint32_t* selmask;      // [b, Hkv, n, ceil(ceil(n/B)/32)] bit m: block m selected (bf16 path)
+  // rows attending each 64-key tile (bf16 path, selections): counts and offsets
+  // [b, Hkv, ceil(n/64)], ascending row indices (at most 2 (K+1) per row)
+  int* tile_cnt;
+  int* tile_off;
+  int* tile_rows;
   // gating formulation (GATED): outer gate; full scope; straight-through hard gate
   int outer, full, ste;
   float* dlog_gate_full;  // [b, Hkv, n, NB] output (full scope / straight-through)
