@@ -274,7 +274,11 @@ constexpr float BLOG2E = 1.4426950408889634f;
 // registers while the previous tile is multiplied.  Sub-blocks of
 // 2^LSB = min(B, 64) keys carry one bias per query; a sub-block of an
 // accumulator element is known at compile time (the lane-dependent part of
-// its key index is below 8).
+// its key index is below 8).  Each lane walks its query's ascending
+// selection row from global memory (the next slot read one slot ahead) and
+// writes a slot's block sum once the slot's last sub-block is done; a tile is
+// processed as two halves of 32 keys to keep the live registers low enough
+// for two workgroups per compute unit.
 template <int DH, int LSB>
 __device__ __forceinline__ void bwd_dq_bf16_job(const BwdArgs& P, const int qtile, const int h, const int bi) {
   constexpr int KP = DH + 8;
@@ -282,13 +286,9 @@ __device__ __forceinline__ void bwd_dq_bf16_job(const BwdArgs& P, const int qtil
   constexpr int KPG = DH / 32;   // keys per thread in the tile staging
   constexpr int C8 = DH / 8;
   constexpr int NSUB = 64 >> LSB;
-  constexpr int KMAX = 32;
   __shared__ __align__(16) bf16_t Ks[64 * KP];
   __shared__ __align__(16) bf16_t Vs[64 * KP];
   __shared__ __align__(16) bf16_t Kt[DH * TP];
-  __shared__ int sel_s[128 * KMAX];
-  __shared__ float sbias_s[128 * KMAX];
-  __shared__ float dlg_s[128 * KMAX];
   __shared__ uint32_t need[BWD_MAX_SEQ / 64 / 32];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -331,7 +331,7 @@ __device__ __forceinline__ void bwd_dq_bf16_job(const BwdArgs& P, const int qtil
   const float lse2 = qvalid ? P.lse[hrow] * BLOG2E : 0.f;
   const float delta = qvalid ? P.delta[hrow] : 0.f;
 
-  // selection rows of the workgroup's queries (lane pair lk = 0, 1 splits the slots)
+  // key tiles of every earlier block (DENSE, full scope), from the workgroup's earliest document start
   for (int w = tid; w < (ntiles + 31) / 32; w += 256) {
     const int lo = w * 32;
     uint32_t bits = 0;
@@ -340,20 +340,14 @@ __device__ __forceinline__ void bwd_dq_bf16_job(const BwdArgs& P, const int qtil
     if (lo + 31 < first_tile) bits = 0;
     need[w] = bits;
   }
-  if (Kn > 0 && qvalid) {
-    const size_t row = (grow + t) * Kn;
-    for (int k = lk; k < Kn; k += 2) {
-      sel_s[qrow * KMAX + k] = P.sel[row + k];
-      if (gated) sbias_s[qrow * KMAX + k] = P.sel_bias[row + k];
-      dlg_s[qrow * KMAX + k] = 0.f;
-    }
-  }
   __syncthreads();
+  // this query's selection row: slots are ascending historical blocks, -1 padded
+  const size_t srow = (grow + (qvalid ? t : 0)) * (size_t)Kn;
   // key tiles this workgroup attends: every query's current block, its selected blocks
   if (!every && qvalid && lk == 0) {
     for (int tl = (beta * B) / 64; tl <= t / 64; ++tl) atomicOr(&need[tl >> 5], 1u << (tl & 31));
     for (int k = 0; k < Kn; ++k) {
-      const int m = sel_s[qrow * KMAX + k];
+      const int m = P.sel[srow + k];
       if (m < 0 || m >= beta) break;  // slots are ascending historical blocks, -1 padded
       for (int tl = (m * B) / 64; tl <= ((m + 1) * B - 1) / 64; ++tl) atomicOr(&need[tl >> 5], 1u << (tl & 31));
     }
@@ -410,13 +404,18 @@ __device__ __forceinline__ void bwd_dq_bf16_job(const BwdArgs& P, const int qtil
     }
   };
 
-  int cur = 0;  // this query's next selection slot
-  int next_sel = 0x7fffffff;
-  if (Kn > 0 && qvalid) {
-    const int s0 = sel_s[qrow * KMAX];
-    next_sel = s0 >= 0 ? s0 : 0x7fffffff;
-  }
-  float blk_acc = 0.f;  // full scope: running sum of a block wider than a tile
+  // the walk over this query's slots: slot `cur` (block next_sel, bias b_cur) and the
+  // one after it (read one slot ahead, so the read is done by the time it is needed)
+  auto sel_at = [&](int k) -> int { return qvalid && k < Kn ? P.sel[srow + k] : -1; };
+  auto bias_at = [&](int k) -> float { return gated && qvalid && k < Kn ? P.sel_bias[srow + k] : 0.f; };
+  int cur = 0;
+  int next_sel = sel_at(0);
+  float b_cur = bias_at(0);
+  int s_nx = sel_at(1);
+  float b_nx = bias_at(1);
+  if (next_sel < 0) next_sel = 0x7fffffff;
+  float blk_acc = 0.f;   // full scope: running sum of a block wider than a tile
+  float slot_acc = 0.f;  // the current slot's running sum (a block may span two tiles)
   int kt = next_set(need, 0, ntiles);
   if (kt < ntiles) prefetch(kt);
   while (kt < ntiles) {
@@ -450,12 +449,14 @@ __device__ __forceinline__ void bwd_dq_bf16_job(const BwdArgs& P, const int qtil
         if (m == next_sel) {
           attb[sb] = true;
           gradb[sb] = gated;
-          lg = gated ? sbias_s[qrow * KMAX + cur] : 0.f;
+          lg = b_cur;
           slot[sb] = cur;
           if (kstart + (1 << LSB) >= (m + 1) * B) {
             ++cur;
-            const int s1 = cur < Kn ? sel_s[qrow * KMAX + cur] : -1;
-            next_sel = s1 >= 0 ? s1 : 0x7fffffff;
+            next_sel = s_nx >= 0 ? s_nx : 0x7fffffff;
+            b_cur = b_nx;
+            s_nx = sel_at(cur + 1);
+            b_nx = bias_at(cur + 1);
           }
         } else if (ste && full) {
           gradb[sb] = true;  // straight-through gradient of a dropped block
@@ -471,72 +472,74 @@ __device__ __forceinline__ void bwd_dq_bf16_job(const BwdArgs& P, const int qtil
     const int nkt = next_set(need, kt + 1, ntiles);
     if (nkt < ntiles) prefetch(nkt);
 
-    floatx16_t sc[2], dp[2];
-#pragma unroll
-    for (int st = 0; st < 2; ++st) {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        sc[st][v] = 0.f;
-        dp[st][v] = 0.f;
-      }
-#pragma unroll
-      for (int ks = 0; ks < DH / 16; ++ks) {
-        const bf16x8_t a = *(const bf16x8_t*)(Ks + (st * 32 + lr) * KP + ks * 16 + lk * 8);
-        sc[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qb[ks], sc[st], 0, 0, 0);
-        const bf16x8_t av = *(const bf16x8_t*)(Vs + (st * 32 + lr) * KP + ks * 16 + lk * 8);
-        dp[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, dob[ks], dp[st], 0, 0, 0);
-      }
-    }
     const bool diag = k0 + 63 > qtile * 128;  // keys past some query of the workgroup: mask key > t
     float dsum[NSUB];
 #pragma unroll
     for (int sb = 0; sb < NSUB; ++sb) dsum[sb] = 0.f;
+    // the tile's two halves of 32 keys one after the other (fewer live registers):
+    // S^T, dP^T of the half, dS^T in registers, then its two 16-key steps of dQ^T += K^T dS^T
 #pragma unroll
-    for (int st = 0; st < 2; ++st)
+    for (int st = 0; st < 2; ++st) {
+      floatx16_t sc, dp;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        sc[v] = 0.f;
+        dp[v] = 0.f;
+      }
+#pragma unroll
+      for (int ks = 0; ks < DH / 16; ++ks) {
+        const bf16x8_t a = *(const bf16x8_t*)(Ks + (st * 32 + lr) * KP + ks * 16 + lk * 8);
+        sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qb[ks], sc, 0, 0, 0);
+        const bf16x8_t av = *(const bf16x8_t*)(Vs + (st * 32 + lr) * KP + ks * 16 + lk * 8);
+        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, dob[ks], dp, 0, 0, 0);
+      }
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int klc = st * 32 + 8 * (v >> 2);  // key offset without the lane part (4 lk + v % 4 < 8)
         const int sb = klc >> LSB;
-        float p = __builtin_amdgcn_exp2f(fmaf(sc[st][v], qk_scale, offs[sb]));
+        float p = __builtin_amdgcn_exp2f(fmaf(sc[v], qk_scale, offs[sb]));
         if (diag && k0 + klc + 4 * lk + (v & 3) > t) p = 0.f;
-        const float dpw = outer ? wts[sb] * dp[st][v] : dp[st][v];
+        const float dpw = outer ? wts[sb] * dp[v] : dp[v];
         const float ds = p * (dpw - delta);
-        sc[st][v] = attb[sb] ? ds : 0.f;
+        sc[v] = attb[sb] ? ds : 0.f;
         dsum[sb] += outer ? p * dpw : ds;
       }
 #pragma unroll
-    for (int sb = 0; sb < NSUB; ++sb) {
-      const float tot = dsum[sb] + __shfl_xor(dsum[sb], 32, 64);
-      if (lk == 0 && gradb[sb]) {
-        if (full) {
-          const int kstart = k0 + (sb << LSB), m = kstart / B;
-          blk_acc += tot;
-          if (kstart + (1 << LSB) >= (m + 1) * B) {  // the block's last sub-block
-            P.dlg_head_full[hrow * NB + m] = blk_acc;
-            blk_acc = 0.f;
-          }
-        } else if (slot[sb] >= 0) {
-          dlg_s[qrow * KMAX + slot[sb]] += tot;
+      for (int kk = 0; kk < 2; ++kk) {
+        const int ks = 2 * st + kk, v0 = 8 * kk;
+        uint4 su;
+        su.x = pack_bf16x2(sc[v0 + 0], sc[v0 + 1]);
+        su.y = pack_bf16x2(sc[v0 + 2], sc[v0 + 3]);
+        su.z = pack_bf16x2(sc[v0 + 4], sc[v0 + 5]);
+        su.w = pack_bf16x2(sc[v0 + 6], sc[v0 + 7]);
+        const bf16x8_t pb = *(const bf16x8_t*)&su;
+#pragma unroll
+        for (int dt = 0; dt < DH / 32; ++dt) {
+          const bf16_t* kr = Kt + (dt * 32 + lr) * TP + 16 * ks + 4 * lk;
+          const uint2 lo = *(const uint2*)kr;
+          const uint2 hi = *(const uint2*)(kr + 8);
+          uint4 u = make_uint4(lo.x, lo.y, hi.x, hi.y);
+          dq[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(bf16x8_t*)&u, pb, dq[dt], 0, 0, 0);
         }
       }
     }
-    // dQ^T += K^T dS^T, 16 keys per step in the accumulator's key permutation
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const int st = ks >> 1, v0 = 8 * (ks & 1);
-      uint4 su;
-      su.x = pack_bf16x2(sc[st][v0 + 0], sc[st][v0 + 1]);
-      su.y = pack_bf16x2(sc[st][v0 + 2], sc[st][v0 + 3]);
-      su.z = pack_bf16x2(sc[st][v0 + 4], sc[st][v0 + 5]);
-      su.w = pack_bf16x2(sc[st][v0 + 6], sc[st][v0 + 7]);
-      const bf16x8_t pb = *(const bf16x8_t*)&su;
-#pragma unroll
-      for (int dt = 0; dt < DH / 32; ++dt) {
-        const bf16_t* kr = Kt + (dt * 32 + lr) * TP + 16 * ks + 4 * lk;
-        const uint2 lo = *(const uint2*)kr;
-        const uint2 hi = *(const uint2*)(kr + 8);
-        uint4 u = make_uint4(lo.x, lo.y, hi.x, hi.y);
-        dq[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(bf16x8_t*)&u, pb, dq[dt], 0, 0, 0);
+    for (int sb = 0; sb < NSUB; ++sb) {
+      const float tot = dsum[sb] + __shfl_xor(dsum[sb], 32, 64);
+      const int kstart = k0 + (sb << LSB), m = kstart / B;
+      const bool last = kstart + (1 << LSB) >= (m + 1) * B;  // the block's last sub-block
+      if (lk == 0 && full && gradb[sb]) {
+        blk_acc += tot;
+        if (last) {
+          P.dlg_head_full[hrow * NB + m] = blk_acc;
+          blk_acc = 0.f;
+        }
+      } else if (lk == 0 && !full && slot[sb] >= 0) {
+        if (gradb[sb]) slot_acc += tot;
+        if (last) {  // the slot is complete
+          if (P.dlg_head) P.dlg_head[hrow * P.K + slot[sb]] = slot_acc;
+          slot_acc = 0.f;
+        }
       }
     }
     lds_barrier();
@@ -544,9 +547,9 @@ __device__ __forceinline__ void bwd_dq_bf16_job(const BwdArgs& P, const int qtil
   }
 
   if (!qvalid) return;
-  if (P.dlg_head && !full && lk == 0) {
+  if (P.dlg_head && !full && lk == 0) {  // slots never reached (padding) get zero
     float* dlg = P.dlg_head + hrow * P.K;
-    for (int k = 0; k < Kn; ++k) dlg[k] = dlg_s[qrow * KMAX + k];
+    for (int k = cur; k < Kn; ++k) dlg[k] = 0.f;
   }
   bf16_t* op = (bf16_t*)P.dQ + (((size_t)bi * n + t) * P.H + h) * DH;
   const float sm = P.sm_scale;
@@ -562,8 +565,10 @@ __device__ __forceinline__ void bwd_dq_bf16_job(const BwdArgs& P, const int qtil
 }
 
 // One job per workgroup (grid = job count, no queue) or the work queue.
+// two workgroups per compute unit where the registers allow it without spills
+// (one sub-block per tile, or dh = 64)
 template <int DH, int LSB>
-__global__ void __launch_bounds__(256) bwd_dq_bf16_kernel(BwdArgs P) {
+__global__ void __launch_bounds__(256, LSB == 6 || DH == 64 ? 2 : 1) bwd_dq_bf16_kernel(BwdArgs P) {
   const int nqt = (P.n + 127) / 128, per = P.H * P.b;
   const int njobs = nqt * per;
   for (int it = 0;; ++it) {
