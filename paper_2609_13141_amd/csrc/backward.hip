@@ -661,10 +661,13 @@ __global__ void __launch_bounds__(1024) bwd_rows_scan_kernel(const int* __restri
   }
 }
 
-// Pass 2 (dK, dV): one workgroup of 2 waves per 64 keys of one (batch, KV
-// group); each wave owns 32 keys, held in registers as the B operands of
-// S = Q K^T and dP = dO V^T over chunks of 32 query rows (lane = key, 16 rows
-// per lane).  The rows are those of the tile's list (selections), or, when
+// Pass 2 (dK, dV): one workgroup of 4 waves per 64 keys of one (batch, KV
+// group); a pair of waves owns 32 keys and splits the head dimension: each
+// wave holds its half of the keys' K and V as the B operands of the partial
+// products S = Q K^T and dP = dO V^T over its dimensions (lane = key, 16 rows
+// per lane) and accumulates dK and dV for its dimensions only; the two
+// partial products are exchanged through LDS and added (the same sum in both
+// waves), which keeps a wave within 256 registers (two waves per SIMD).  The rows are those of the tile's list (selections), or, when
 // every earlier block is attended (DENSE, full scope), the consecutive rows
 // from the tile on, in chunks of 32 that reach the tile.  Work items are
 // (chunk, head of the group); the row indices of the next chunk are read one
@@ -675,11 +678,12 @@ __global__ void __launch_bounds__(1024) bwd_rows_scan_kernel(const int* __restri
 // in registers; the causal mask compares each key with its row's index.
 template <int DH>
 __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int ktile, const int g, const int bi) {
-  constexpr int NTH = 128, KT = 64;
+  constexpr int NTH = 256, KT = 64;
   constexpr int KP = DH + 8;
   constexpr int QP = 32 + 4;
   constexpr int C8 = DH / 8;            // 16-byte pieces of a row
-  constexpr int QPT = 32 * C8 / NTH;    // chunk rows staged per thread (4 or 2)
+  constexpr int QPT = 32 * C8 / NTH;    // chunk rows staged per thread (2 or 1)
+  constexpr int DHH = DH / 2;           // dimensions of a wave
   __shared__ __align__(16) bf16_t Qs[32 * KP];
   __shared__ __align__(16) bf16_t Ds[32 * KP];
   __shared__ __align__(16) bf16_t Qt[DH * QP];
@@ -689,12 +693,14 @@ __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int kti
   __shared__ __align__(16) float off_s[4][32];  // log2-domain bias - LSE per (sub-block, row); -inf: not attended
   __shared__ __align__(16) float wt_s[4][32];   // value weight per (sub-block, row) (outer gate)
   __shared__ uint32_t flags[BWD_MAX_SEQ / 32 / 32];
+  __shared__ __align__(16) float xs[4][2][16][64];  // each wave's partial S and dP
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lk = lane >> 5;
+  const int kh = wave >> 1, dhf = wave & 1;  // key half, dimension half
   const int k0 = ktile * KT;
   const int n = P.n, B = P.B, H = P.H, G = H / P.Hkv;
-  const int key = k0 + wave * 32 + lr;
+  const int key = k0 + kh * 32 + lr;
   const bool kvalid = key < n;
   const int bshift = 31 - __clz(B < 64 ? B : 64);
   const int nsb = KT >> bshift;  // sub-blocks of min(B, 64) keys in the tile: 1, 2 or 4
@@ -730,20 +736,20 @@ __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int kti
   }
   auto next_chunk = [&](int c) { return use_list ? c : next_set(flags, c, nqc); };
 
-  bf16x8_t kb[DH / 16], vb[DH / 16];
+  bf16x8_t kb[DHH / 16], vb[DHH / 16];
   {
-    const size_t off = (((size_t)bi * n + (kvalid ? key : 0)) * P.Hkv + g) * DH;
+    const size_t off = (((size_t)bi * n + (kvalid ? key : 0)) * P.Hkv + g) * DH + dhf * DHH;
 #pragma unroll
-    for (int ks = 0; ks < DH / 16; ++ks) {
+    for (int ks = 0; ks < DHH / 16; ++ks) {
       uint4 u = kvalid ? *(const uint4*)((const bf16_t*)P.Kt + off + ks * 16 + lk * 8) : make_uint4(0, 0, 0, 0);
       kb[ks] = *(bf16x8_t*)&u;
       uint4 w = kvalid ? *(const uint4*)((const bf16_t*)P.V + off + ks * 16 + lk * 8) : make_uint4(0, 0, 0, 0);
       vb[ks] = *(bf16x8_t*)&w;
     }
   }
-  floatx16_t dk[DH / 32], dv[DH / 32];
+  floatx16_t dk[DHH / 32], dv[DHH / 32];
 #pragma unroll
-  for (int dt = 0; dt < DH / 32; ++dt)
+  for (int dt = 0; dt < DHH / 32; ++dt)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       dk[dt][v] = 0.f;
@@ -825,12 +831,12 @@ __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int kti
       }
       bf16_t* qd = Qt + (c8 * 8 + e) * QP + qg * QPT;
       bf16_t* dd = Dt + (c8 * 8 + e) * QP + qg * QPT;
-      if constexpr (QPT == 4) {
-        *(uint2*)qd = make_uint2(x[0] | (x[1] << 16), x[2] | (x[3] << 16));
-        *(uint2*)dd = make_uint2(y[0] | (y[1] << 16), y[2] | (y[3] << 16));
-      } else {
+      if constexpr (QPT == 2) {
         *(uint32_t*)qd = x[0] | (x[1] << 16);
         *(uint32_t*)dd = y[0] | (y[1] << 16);
+      } else {
+        *(uint16_t*)qd = (uint16_t)x[0];
+        *(uint16_t*)dd = (uint16_t)y[0];
       }
     }
     if (tid < 32) {
@@ -874,56 +880,70 @@ __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int kti
       dp[v] = 0.f;
     }
 #pragma unroll
-    for (int ks = 0; ks < DH / 16; ++ks) {
-      const bf16x8_t aq = *(const bf16x8_t*)(Qs + lr * KP + ks * 16 + lk * 8);
+    for (int ks = 0; ks < DHH / 16; ++ks) {
+      const bf16x8_t aq = *(const bf16x8_t*)(Qs + lr * KP + dhf * DHH + ks * 16 + lk * 8);
       sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq, kb[ks], sc, 0, 0, 0);
-      const bf16x8_t ad = *(const bf16x8_t*)(Ds + lr * KP + ks * 16 + lk * 8);
+      const bf16x8_t ad = *(const bf16x8_t*)(Ds + lr * KP + dhf * DHH + ks * 16 + lk * 8);
       dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ad, vb[ks], dp, 0, 0, 0);
     }
-    // lane: key column `key`; staged rows 8 j + 4 lk + i (v = 4 j + i)
-    const int sbk = (wave * 32 + lr) >> bshift;
-    const bool diag = trow_s[0] < k0 + KT - 1;  // some row precedes a key of the tile: mask key > row
-    floatx16_t pp;
+    // the pair's partial products: written, exchanged, added (commutative, the same in both)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const float4 of = *(const float4*)&off_s[sbk][8 * j + 4 * lk];
-      const float4 de = *(const float4*)&delta_s[8 * j + 4 * lk];
-      const int4 tr = *(const int4*)&trow_s[8 * j + 4 * lk];
-      float4 wt = make_float4(1.f, 1.f, 1.f, 1.f);
-      if (outer) wt = *(const float4*)&wt_s[sbk][8 * j + 4 * lk];
-      const float ofv[4] = {of.x, of.y, of.z, of.w}, dev[4] = {de.x, de.y, de.z, de.w};
-      const float wv[4] = {wt.x, wt.y, wt.z, wt.w};
-      const int trv[4] = {tr.x, tr.y, tr.z, tr.w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int v = 4 * j + i;
-        float p = __builtin_amdgcn_exp2f(fmaf(sc[v], qk_scale, ofv[i]));
-        if (diag && key > trv[i]) p = 0.f;
-        pp[v] = p * wv[i];
-        sc[v] = p * (wv[i] * dp[v] - dev[i]);
-      }
+    for (int v = 0; v < 16; ++v) {
+      xs[wave][0][v][lane] = sc[v];
+      xs[wave][1][v][lane] = dp[v];
     }
-    // dV^T += dO^T P and dK^T += Q^T dS, 16 rows per step in the accumulator's row permutation
+    lds_barrier();
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      sc[v] += xs[wave ^ 1][0][v][lane];
+      dp[v] += xs[wave ^ 1][1][v][lane];
+    }
+    // lane: key column `key`; staged rows 8 j + 4 lk + i (v = 4 j + i)
+    const int sbk = (kh * 32 + lr) >> bshift;
+    const bool diag = trow_s[0] < k0 + KT - 1;  // some row precedes a key of the tile: mask key > row
+    // dV^T += dO^T P and dK^T += Q^T dS, 16 rows per step in the accumulator's row permutation;
+    // each step's P and dS are formed and packed just before its MFMAs
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
+      float pv[8], sv[8];
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        const int j = 2 * ks + jj;
+        const float4 of = *(const float4*)&off_s[sbk][8 * j + 4 * lk];
+        const float4 de = *(const float4*)&delta_s[8 * j + 4 * lk];
+        const int4 tr = *(const int4*)&trow_s[8 * j + 4 * lk];
+        float4 wt = make_float4(1.f, 1.f, 1.f, 1.f);
+        if (outer) wt = *(const float4*)&wt_s[sbk][8 * j + 4 * lk];
+        const float ofv[4] = {of.x, of.y, of.z, of.w}, dev[4] = {de.x, de.y, de.z, de.w};
+        const float wv[4] = {wt.x, wt.y, wt.z, wt.w};
+        const int trv[4] = {tr.x, tr.y, tr.z, tr.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int v = 4 * j + i;
+          float p = __builtin_amdgcn_exp2f(fmaf(sc[v], qk_scale, ofv[i]));
+          if (diag && key > trv[i]) p = 0.f;
+          pv[4 * jj + i] = p * wv[i];
+          sv[4 * jj + i] = p * (wv[i] * dp[v] - dev[i]);
+        }
+      }
       uint4 pu, su;
-      pu.x = pack_bf16x2(pp[8 * ks + 0], pp[8 * ks + 1]);
-      pu.y = pack_bf16x2(pp[8 * ks + 2], pp[8 * ks + 3]);
-      pu.z = pack_bf16x2(pp[8 * ks + 4], pp[8 * ks + 5]);
-      pu.w = pack_bf16x2(pp[8 * ks + 6], pp[8 * ks + 7]);
-      su.x = pack_bf16x2(sc[8 * ks + 0], sc[8 * ks + 1]);
-      su.y = pack_bf16x2(sc[8 * ks + 2], sc[8 * ks + 3]);
-      su.z = pack_bf16x2(sc[8 * ks + 4], sc[8 * ks + 5]);
-      su.w = pack_bf16x2(sc[8 * ks + 6], sc[8 * ks + 7]);
+      pu.x = pack_bf16x2(pv[0], pv[1]);
+      pu.y = pack_bf16x2(pv[2], pv[3]);
+      pu.z = pack_bf16x2(pv[4], pv[5]);
+      pu.w = pack_bf16x2(pv[6], pv[7]);
+      su.x = pack_bf16x2(sv[0], sv[1]);
+      su.y = pack_bf16x2(sv[2], sv[3]);
+      su.z = pack_bf16x2(sv[4], sv[5]);
+      su.w = pack_bf16x2(sv[6], sv[7]);
       const bf16x8_t pb = *(const bf16x8_t*)&pu, sb8 = *(const bf16x8_t*)&su;
 #pragma unroll
-      for (int dt = 0; dt < DH / 32; ++dt) {
-        const bf16_t* dr = Dt + (dt * 32 + lr) * QP + 16 * ks + 4 * lk;
+      for (int dt = 0; dt < DHH / 32; ++dt) {
+        const bf16_t* dr = Dt + (dhf * DHH + dt * 32 + lr) * QP + 16 * ks + 4 * lk;
         const uint2 dlo = *(const uint2*)dr;
         const uint2 dhi = *(const uint2*)(dr + 8);
         uint4 du = make_uint4(dlo.x, dlo.y, dhi.x, dhi.y);
         dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(bf16x8_t*)&du, pb, dv[dt], 0, 0, 0);
-        const bf16_t* qrp = Qt + (dt * 32 + lr) * QP + 16 * ks + 4 * lk;
+        const bf16_t* qrp = Qt + (dhf * DHH + dt * 32 + lr) * QP + 16 * ks + 4 * lk;
         const uint2 qlo = *(const uint2*)qrp;
         const uint2 qhi = *(const uint2*)(qrp + 8);
         uint4 qu = make_uint4(qlo.x, qlo.y, qhi.x, qhi.y);
@@ -935,12 +955,12 @@ __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int kti
     hg = nh;
   }
   if (!kvalid) return;
-  const size_t off = (((size_t)bi * n + key) * P.Hkv + g) * DH;
+  const size_t off = (((size_t)bi * n + key) * P.Hkv + g) * DH + dhf * DHH;
   bf16_t* dkp = (bf16_t*)P.dK + off;
   bf16_t* dvp = (bf16_t*)P.dV + off;
   const float sm = P.sm_scale;
 #pragma unroll
-  for (int dt = 0; dt < DH / 32; ++dt)
+  for (int dt = 0; dt < DHH / 32; ++dt)
 #pragma unroll
     for (int v4 = 0; v4 < 4; ++v4) {
       const int d0 = dt * 32 + 8 * v4 + 4 * lk;
@@ -954,7 +974,7 @@ __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int kti
 }
 
 template <int DH>
-__global__ void __launch_bounds__(128) bwd_dkv_bf16_kernel(BwdArgs P) {
+__global__ void __launch_bounds__(256, 2) bwd_dkv_bf16_kernel(BwdArgs P) {
   const int nkt = (P.n + 63) / 64, per = P.Hkv * P.b;
   const int njobs = nkt * per;
   for (int it = 0;; ++it) {
@@ -1003,14 +1023,14 @@ static hipError_t launch_attention_backward_bf16(const BwdArgs& P, hipStream_t s
                                                                            : bwd_dq_bf16_kernel<64, 4>);
   auto dkv = P.dh == 128 ? bwd_dkv_bf16_kernel<128> : bwd_dkv_bf16_kernel<64>;
   const long long jq = (long long)cdiv(P.n, 128) * P.H * P.b, jk = (long long)ntk * P.Hkv * P.b;
-  const int rq = resident_workgroups(dq, 256), rk = resident_workgroups(dkv, 128);
+  const int rq = resident_workgroups(dq, 256), rk = resident_workgroups(dkv, 256);
   if (rq <= 0 || rk <= 0 || jq > INT32_MAX || jk > INT32_MAX) return hipErrorInvalidValue;
   if (jq > rq || jk > rk) fill_f32_kernel<<<1, 64, 0, s>>>((float*)P.queue, 2, 0.f);  // job counters to zero
   BwdArgs A = Q;
   A.queue = jq > rq ? P.queue : nullptr;
   if (jq > 0) dq<<<(unsigned)std::min<long long>(jq, rq), 256, 0, s>>>(A);
   A.queue = jk > rk ? P.queue + 1 : nullptr;
-  if (jk > 0) dkv<<<(unsigned)std::min<long long>(jk, rk), 128, 0, s>>>(A);
+  if (jk > 0) dkv<<<(unsigned)std::min<long long>(jk, rk), 256, 0, s>>>(A);
   return hipGetLastError();
 }
 
