@@ -154,6 +154,9 @@ struct AttnWs {
   float* gate_table;  // log gates of every block (full scope, when the caller does not ask for them)
   float* row_lse;     // per-row LSE of the scores while the log-gate table is finished
   uint32_t* queue;    // job counter of the attention kernel
+  float* part_o;      // parts of split query tiles (short sequences)
+  float* part_ml;
+  long long part_slots;
 };
 
 AttnWs carve_attention(Carve& cv, const sas_config* c, int b, int n) {
@@ -172,6 +175,11 @@ AttnWs carve_attention(Carve& cv, const sas_config* c, int b, int n) {
   w.gate_table = full_fwd(c) ? (float*)cv.take((size_t)b * c->n_kv_heads * n * NB * 4) : nullptr;
   w.row_lse = (float*)cv.take((size_t)b * c->n_kv_heads * n * 4);
   w.queue = (uint32_t*)cv.take(256);
+  // split query tiles: only when the jobs are few (then at most ATTN_MAX_SPLIT parts each)
+  const long long jobs = (long long)cdiv(n, 128) * c->n_heads * b;
+  w.part_slots = jobs < 1024 ? jobs * ATTN_MAX_SPLIT : 0;
+  w.part_o = w.part_slots ? (float*)cv.take((size_t)w.part_slots * 128 * c->head_dim * 4) : nullptr;
+  w.part_ml = w.part_slots ? (float*)cv.take((size_t)w.part_slots * 128 * 2 * 4) : nullptr;
   return w;
 }
 
@@ -289,6 +297,10 @@ sas_status run_attention(const sas_config* c, int b, int n, const void* q, const
   aa.gate_table = log_gate;
   aa.doc = doc;
   aa.queue = ws.queue;
+  aa.part_o = c->dtype == SAS_BF16 ? ws.part_o : nullptr;
+  aa.part_ml = c->dtype == SAS_BF16 ? ws.part_ml : nullptr;
+  aa.part_slots = ws.part_slots;
+  aa.split_tiles = 0;
   {
     Timed tm("attention", s);
     HIP_TRY(launch_attention(c->dtype, aa, s), "attention");

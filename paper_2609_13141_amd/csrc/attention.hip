@@ -47,7 +47,8 @@ constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 
 template <int DH, int LSB>
-__device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile, const int h, const int bi) {
+__device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile, const int h, const int bi,
+                                              const int tlo, const int thi, const int slot) {
   constexpr int KP = DH + 8;    // K tile row pitch (elements)
   constexpr int VP = 64 + 4;    // V^T tile row pitch (elements)
   constexpr int KPG = DH / 32;  // keys per thread in the tile staging
@@ -169,14 +170,22 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
     }
   };
 
+  // key tiles [tlo, thi) of this job (a part of the range when the query tile is split);
+  // the selection cursor starts at the first block not consumed before tile tlo
+  const int tend = min(thi, ntiles);
   int cur = 0, next_sel = 0x7fffffff;  // selection cursor of this lane's query
   if (Kn > 0 && qvalid) {
     const int s0 = sel_s[qrow * KMAX];
     next_sel = s0 >= 0 ? s0 : 0x7fffffff;
+    while (next_sel != 0x7fffffff && (next_sel + 1) * B <= tlo * 64) {
+      ++cur;
+      const int s1 = cur < Kn ? sel_s[qrow * KMAX + cur] : -1;
+      next_sel = s1 >= 0 ? s1 : 0x7fffffff;
+    }
   }
-  int kt = next_set(need, 0, ntiles);
-  if (kt < ntiles) prefetch(kt);
-  while (kt < ntiles) {
+  int kt = next_set(need, tlo, tend);
+  if (kt < tend) prefetch(kt);
+  while (kt < tend) {
     commit();
     lds_barrier();
     const int k0 = kt * 64;
@@ -210,8 +219,8 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
         wts[sb] = outer ? __builtin_amdgcn_exp2f(lg * LOG2E) : 1.f;
       }
     }
-    const int nkt = next_set(need, kt + 1, ntiles);
-    if (nkt < ntiles) prefetch(nkt);
+    const int nkt = next_set(need, kt + 1, tend);
+    if (nkt < tend) prefetch(nkt);
 
     // S^T = K Q^T for keys [0,32) and [32,64) of the tile
     floatx16_t s[2];
@@ -282,6 +291,17 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
     kt = nkt;
   }
 
+  if (slot >= 0) {  // a part of a split query tile: unnormalized sums and (max, sum) per row
+    float* po = P.part_o + ((size_t)slot * 128 + qrow) * DH;
+#pragma unroll
+    for (int dt = 0; dt < DH / 32; ++dt)
+#pragma unroll
+      for (int v4 = 0; v4 < 4; ++v4)
+        *(float4*)(po + dt * 32 + 8 * v4 + 4 * lk) =
+            make_float4(o[dt][4 * v4 + 0], o[dt][4 * v4 + 1], o[dt][4 * v4 + 2], o[dt][4 * v4 + 3]);
+    if (lk == 0) *(float2*)(P.part_ml + ((size_t)slot * 128 + qrow) * 2) = make_float2(m_run, l_run);
+    return;
+  }
   if (!qvalid) return;
   const float inv_l = 1.0f / l_run;
   bf16_t* op = (bf16_t*)P.O + (((size_t)bi * n + t) * P.H + h) * DH;
@@ -297,18 +317,97 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
   if (P.lse && lk == 0) P.lse[((size_t)bi * P.H + h) * n + t] = (m_run + log2f(l_run)) * LN2;
 }
 
-// One job (query tile, head, batch entry) per workgroup (grid = job count, no
-// queue) or the work queue; the heavy (late) query tiles first.
-template <int DH, int LSB>
-__global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P) {
+// Splitting a query tile's key range: with fewer jobs than resident
+// workgroups the longest job bounds the kernel, so a tile whose causal range
+// holds more than `split_tiles` key tiles is cut into up to ATTN_MAX_SPLIT
+// parts of about equal tile counts, merged afterwards by attn_combine_kernel.
+__device__ __forceinline__ int attn_tiles(int n, int qtile) { return (min(n, qtile * 128 + 128) - 1) / 64 + 1; }
+__device__ __forceinline__ int attn_splits(int n, int qtile, int split_tiles) {
+  if (split_tiles <= 0) return 1;
+  return min(ATTN_MAX_SPLIT, (attn_tiles(n, qtile) + split_tiles - 1) / split_tiles);
+}
+// job -> (query tile, head, batch entry, part); the latest query tiles first, a tile's
+// parts consecutive; jbase: the job index of the tile's first job
+__device__ __forceinline__ void attn_job_of(const AttnArgs& P, int job, int& qtile, int& h, int& bi, int& part,
+                                            int& nparts, int& jbase) {
   const int nqt = (P.n + 127) / 128, per = P.H * P.b;
-  const int njobs = nqt * per;
+  jbase = 0;
+  for (qtile = nqt - 1; qtile > 0; --qtile) {
+    const int cnt = attn_splits(P.n, qtile, P.split_tiles) * per;
+    if (job < jbase + cnt) break;
+    jbase += cnt;
+  }
+  nparts = attn_splits(P.n, qtile, P.split_tiles);
+  int r = job - jbase;
+  part = r % nparts;
+  r /= nparts;
+  h = r % P.H;
+  bi = r / P.H;
+}
+
+// One job (query tile or part of it, head, batch entry) per workgroup (grid =
+// job count, no queue) or the work queue; the heavy (late) query tiles first.
+template <int DH, int LSB>
+__global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P, int njobs) {
   for (int it = 0;; ++it) {
     const int job = P.queue ? queue_next_job(P.queue) : (it == 0 ? (int)blockIdx.x : njobs);
     if (job >= njobs) break;
-    const int r = job % per;
-    attn_bf16_job<DH, LSB>(P, nqt - 1 - job / per, r % P.H, r / P.H);
+    int qtile, h, bi, part, nparts, jbase;
+    attn_job_of(P, job, qtile, h, bi, part, nparts, jbase);
+    const int nt = attn_tiles(P.n, qtile), per_part = (nt + nparts - 1) / nparts;
+    attn_bf16_job<DH, LSB>(P, qtile, h, bi, part * per_part, nparts > 1 ? (part + 1) * per_part : 1 << 30,
+                           nparts > 1 ? job : -1);
   }
+}
+
+// Merge of a split query tile's parts: thread per (batch, head, query, 8
+// dimensions); rows of unsplit tiles are skipped.
+__global__ void attn_combine_kernel(AttnArgs P) {
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int n = P.n, C8 = P.dh / 8;
+  if (idx >= (size_t)P.b * P.H * n * C8) return;
+  const int c8 = (int)(idx % C8);
+  size_t r = idx / C8;
+  const int t = (int)(r % n);
+  r /= n;
+  const int h = (int)(r % P.H), bi = (int)(r / P.H);
+  const int qtile = t / 128, nparts = attn_splits(n, qtile, P.split_tiles);
+  if (nparts <= 1) return;
+  const int nqt = (n + 127) / 128, per = P.H * P.b;
+  int jbase = 0;
+  for (int q = nqt - 1; q > qtile; --q) jbase += attn_splits(n, q, P.split_tiles) * per;
+  const int j0 = jbase + (bi * P.H + h) * nparts, qrow = t - qtile * 128;
+  float mx = -INFINITY;
+  for (int p = 0; p < nparts; ++p) mx = fmaxf(mx, P.part_ml[((size_t)(j0 + p) * 128 + qrow) * 2]);
+  const float mu = mx == -INFINITY ? 0.f : mx;
+  float l = 0.f, acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+  for (int p = 0; p < nparts; ++p) {
+    const size_t row = (size_t)(j0 + p) * 128 + qrow;
+    const float2 ml = *(const float2*)(P.part_ml + row * 2);
+    const float w = __builtin_amdgcn_exp2f(ml.x - mu);
+    l += ml.y * w;
+    const float4 a = *(const float4*)(P.part_o + row * P.dh + c8 * 8);
+    const float4 b = *(const float4*)(P.part_o + row * P.dh + c8 * 8 + 4);
+    acc[0] += a.x * w;
+    acc[1] += a.y * w;
+    acc[2] += a.z * w;
+    acc[3] += a.w * w;
+    acc[4] += b.x * w;
+    acc[5] += b.y * w;
+    acc[6] += b.z * w;
+    acc[7] += b.w * w;
+  }
+  const float inv_l = 1.0f / l;
+  bf16_t* op = (bf16_t*)P.O + (((size_t)bi * n + t) * P.H + h) * P.dh + c8 * 8;
+  uint4 u;
+  u.x = pack_bf16x2(acc[0] * inv_l, acc[1] * inv_l);
+  u.y = pack_bf16x2(acc[2] * inv_l, acc[3] * inv_l);
+  u.z = pack_bf16x2(acc[4] * inv_l, acc[5] * inv_l);
+  u.w = pack_bf16x2(acc[6] * inv_l, acc[7] * inv_l);
+  *(uint4*)op = u;
+  if (P.lse && c8 == 0) P.lse[((size_t)bi * P.H + h) * n + t] = (mu + log2f(l)) * LN2;
 }
 
 // ---- fp32: one thread per (batch, head, query), online softmax in fp32 ----
@@ -391,17 +490,43 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
                                                                              : attn_bf16_kernel<128, 4>)
                             : (lsb == 6 ? attn_bf16_kernel<64, 6> : lsb == 5 ? attn_bf16_kernel<64, 5>
                                                                             : attn_bf16_kernel<64, 4>);
-    const long long jobs = (long long)cdiv(a.n, 128) * a.H * a.b;
+    const int nqt = cdiv(a.n, 128), ntk = cdiv(a.n, 64), per = a.H * a.b;
+    const long long jobs = (long long)nqt * per;
     const int res = resident_workgroups(kern, 256);
     if (res <= 0 || jobs > INT32_MAX) return hipErrorInvalidValue;
     AttnArgs A = a;
     A.queue = nullptr;
-    if (jobs > res) {
+    A.split_tiles = 0;
+    long long total = jobs;
+    if (jobs < res && a.part_o && a.part_ml && jobs * ATTN_MAX_SPLIT <= a.part_slots) {
+      // fewer jobs than resident workgroups: split the long query tiles so that no job
+      // walks much more than the average share of key tiles
+      auto tiles = [&](int q) { return std::min(ntk, (std::min(a.n, q * 128 + 128) - 1) / 64 + 1); };
+      long long W = 0;
+      for (int q = 0; q < nqt; ++q) W += (long long)tiles(q) * per;
+      // the smallest part length whose job count still fits the resident workgroups
+      for (int st = (int)std::max<long long>(2, (W + res - 1) / res); st < ntk; ++st) {
+        long long tot = 0;
+        for (int q = 0; q < nqt; ++q) tot += (long long)std::min(ATTN_MAX_SPLIT, cdiv(tiles(q), st)) * per;
+        if (tot <= res) {
+          if (tot > jobs) {
+            A.split_tiles = st;
+            total = tot;
+          }
+          break;
+        }
+      }
+    }
+    if (total > res) {
       if (!a.queue) return hipErrorInvalidValue;
       fill_u32_kernel<<<1, 64, 0, s>>>(a.queue, 1, 0u);
       A.queue = a.queue;
     }
-    kern<<<(unsigned)std::min<long long>(jobs, res), 256, 0, s>>>(A);
+    kern<<<(unsigned)std::min<long long>(total, res), 256, 0, s>>>(A, (int)total);
+    if (A.split_tiles > 0) {
+      const size_t rows = (size_t)a.b * a.H * a.n * (a.dh / 8);
+      attn_combine_kernel<<<(unsigned)cdiv(rows, 256), 256, 0, s>>>(A);
+    }
   } else {
     size_t tot = (size_t)a.b * a.H * a.n;
     unsigned grid = (unsigned)((tot + 127) / 128);

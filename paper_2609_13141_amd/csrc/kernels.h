@@ -110,10 +110,18 @@ struct AttnArgs {
   const float* gate_table;  // [b, Hkv, n, NB] log gates (full scope)
   const int32_t* doc;     // [b, NB] first block of each block's document, or null
   uint32_t* queue;        // job counter of the bf16 kernel's work queue (reset by the launch)
+  // split query tiles (bf16, fewer jobs than resident workgroups): per job slot 128 rows of
+  // unnormalized sums [slot, 128, dh] and (max, sum) [slot, 128, 2]; null: no splitting
+  float* part_o;
+  float* part_ml;
+  long long part_slots;
+  int split_tiles;        // set by the launch: key tiles per part (0: no split)
 };
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 // longest sequence of the bf16 attention forward (key tiles of 64 tracked in LDS)
 constexpr int ATTN_MAX_SEQ = 1 << 20;
+// parts of a split query tile
+constexpr int ATTN_MAX_SPLIT = 4;
 
 // ---- backward.hip ----------------------------------------------------------
 struct BwdArgs {
