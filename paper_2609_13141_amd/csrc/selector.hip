@@ -142,9 +142,10 @@ hipError_t launch_block_summaries(int dtype, const void* K, int b, int n, int Hk
 // Selection: one workgroup of SEL_NW waves per 64 consecutive query rows of
 // one (batch, group); lane = query row.  The 64 gate queries are staged in
 // LDS once; the waves split the historical blocks into contiguous ranges and
-// walk theirs in chunks of SEL_MC summaries staged in LDS as fp64 (one exact
-// fp64 FMA chain per (row, block), j ascending), each keeping a register
-// Top-K and a running LSE.  The waves' lists are then merged into wave 0's in
+// walk theirs in chunks of SEL_MC summaries staged in LDS as fp32 (exact for
+// bf16 and fp32 summaries, and half the bytes of fp64 per broadcast read),
+// one exact fp64 FMA chain per (row, block), j ascending, each keeping a
+// register Top-K and a running LSE.  The waves' lists are then merged into wave 0's in
 // wave order, which reproduces a single ascending scan (strict comparisons
 // keep the lower block first on equal scores).
 constexpr int SEL_MC = 8;   // summaries per wave per step
@@ -154,11 +155,11 @@ __device__ __forceinline__ void lds_fence() { asm volatile("s_waitcnt lgkmcnt(0)
 
 template <typename T, int DH, int KMAX>
 __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
-  constexpr int KB_BYTES = SEL_NW * SEL_MC * DH * 8;
+  constexpr int KB_BYTES = SEL_NW * SEL_MC * DH * 4;
   constexpr int MG_BYTES = KMAX * WAVE * 12 + WAVE * 8 + WAVE * 4;
   __shared__ __align__(16) unsigned char pool[KB_BYTES > MG_BYTES ? KB_BYTES : MG_BYTES];
   __shared__ __align__(16) T qs[WAVE][DH + 8];  // the 64 gate queries
-  double(*kb)[SEL_MC][DH] = (double(*)[SEL_MC][DH])pool;            // [SEL_NW][SEL_MC][DH]
+  float(*kb)[SEL_MC][DH] = (float(*)[SEL_MC][DH])pool;              // [SEL_NW][SEL_MC][DH] (exact in fp32)
   double* mg_r = (double*)pool;                                      // merge: [KMAX][WAVE] keys
   int* mg_m = (int*)(pool + KMAX * WAVE * 8);                        // [KMAX][WAVE] blocks
   double* mg_mx = (double*)(pool + KMAX * WAVE * 12);                // [WAVE] running max
@@ -184,34 +185,39 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
   const int act = P.act;
 
   // stage the 64 gate queries: either the precomputed (projected) rows, or
-  // the group's query heads summed here in fp64 and rounded once
+  // the group's query heads summed here in fp64 and rounded once; a thread's
+  // loads of one head are issued together
   {
     constexpr int NC = DH / 8;  // 8-value chunks per row
+    constexpr int NI = NC / SEL_NW;
     const int rows = t_last - t0 + 1;
+    double acc[NI][8];
 #pragma unroll
-    for (int i = 0; i < NC / SEL_NW; ++i) {
-      const int c = tid + i * SEL_NW * WAVE;
-      const int r = c / NC, c8 = c % NC;
-      const int rr = min(r, rows - 1);
-      double acc[8];
-      if (P.qhat) {
-        Vec8<T> v;
-        v.load((const T*)P.qhat + (((size_t)bi * P.Hkv + g) * P.n + t0 + rr) * DH + c8 * 8);
+    for (int i = 0; i < NI; ++i)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] = v.get(e);
-      } else {
-        const T* qp = (const T*)P.Q + (((size_t)bi * P.n + t0 + rr) * P.H + (size_t)g * G) * DH + c8 * 8;
+      for (int e = 0; e < 8; ++e) acc[i][e] = 0.0;
+    const int nh = P.qhat ? 1 : G;
+    for (int h = 0; h < nh; ++h) {
+      Vec8<T> v[NI];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] = 0.0;
-        for (int h = 0; h < G; ++h) {
-          Vec8<T> v;
-          v.load(qp + (size_t)h * DH);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) acc[e] += (double)v.get(e);
-        }
+      for (int i = 0; i < NI; ++i) {
+        const int c = tid + i * SEL_NW * WAVE;
+        const int r = c / NC, c8 = c % NC;
+        const int rr = min(r, rows - 1);
+        v[i].load(P.qhat ? (const T*)P.qhat + (((size_t)bi * P.Hkv + g) * P.n + t0 + rr) * DH + c8 * 8
+                         : (const T*)P.Q + (((size_t)bi * P.n + t0 + rr) * P.H + (size_t)g * G + h) * DH + c8 * 8);
       }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) qs[r][c8 * 8 + e] = r < rows ? Act<T>::from_f64(acc[e]) : Act<T>::from_f32(0.f);
+      for (int i = 0; i < NI; ++i)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[i][e] += (double)v[i].get(e);
+    }
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int c = tid + i * SEL_NW * WAVE;
+      const int r = c / NC, c8 = c % NC;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qs[r][c8 * 8 + e] = r < rows ? Act<T>::from_f64(acc[i][e]) : Act<T>::from_f32(0.f);
     }
   }
   __syncthreads();
@@ -242,7 +248,7 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
   const T* kbar = (const T*)P.kbar + ((size_t)bi * P.Hkv + g) * (size_t)P.NB * DH;
   const int per = (cmax - mlo + SEL_NW - 1) / SEL_NW;
   const int mb = mlo + wave * per, me = min(cmax, mb + per);
-  double(*kw)[DH] = kb[wave];
+  float(*kw)[DH] = kb[wave];
   for (int m0 = mb; m0 < me; m0 += SEL_MC) {
     const int mc = min(SEL_MC, me - m0);
     {
@@ -254,7 +260,7 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
         Vec8<T> v;
         v.load(kbar + (size_t)(m0 + min(r, mc - 1)) * DH + c8 * 8);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) kw[r][c8 * 8 + e] = r < mc ? (double)v.get(e) : 0.0;
+        for (int e = 0; e < 8; ++e) kw[r][c8 * 8 + e] = r < mc ? v.get(e) : 0.f;
       }
     }
     lds_fence();
@@ -262,13 +268,17 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
     double r[SEL_MC];
 #pragma unroll
     for (int mm = 0; mm < SEL_MC; ++mm) r[mm] = 0.0;
-    for (int j = 0; j < DH; j += 2) {
-      const double q0 = Act<T>::to_f32(qs[lane][j]), q1 = Act<T>::to_f32(qs[lane][j + 1]);
+    for (int j = 0; j < DH; j += 4) {
+      double qd[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) qd[u] = Act<T>::to_f32(qs[lane][j + u]);
 #pragma unroll
       for (int mm = 0; mm < SEL_MC; ++mm) {
-        const double2 k2 = *(const double2*)&kw[mm][j];
-        r[mm] = fma(q0, k2.x, r[mm]);
-        r[mm] = fma(q1, k2.y, r[mm]);
+        const float4 k4 = *(const float4*)&kw[mm][j];  // four dimensions of one summary (broadcast)
+        r[mm] = fma(qd[0], (double)k4.x, r[mm]);
+        r[mm] = fma(qd[1], (double)k4.y, r[mm]);
+        r[mm] = fma(qd[2], (double)k4.z, r[mm]);
+        r[mm] = fma(qd[3], (double)k4.w, r[mm]);
       }
     }
     lds_fence();  // this wave's reads of the chunk are done before it is restaged
