@@ -1023,12 +1023,11 @@ sas_status sas_layer_forward(const sas_config* c, int32_t batch, int32_t seq_len
   void* h1 = tp.h1 ? tp.h1 : lw.h1;
 
   {
-    Timed tm("rope_table", s);
-    HIP_TRY(launch_rope_table(lw.rope, seq_len, c->head_dim, c->rope_base, s), "rope table");
-  }
-  {
+    // the first norm also writes the rotary table of positions 0 .. seq_len - 1 (rows of the first sequence)
     Timed tm("rmsnorm", s);
-    HIP_TRY(launch_rmsnorm(c->dtype, x, w->rms1, lw.u1, (int)T, c->d_model, c->rms_eps, s), "rmsnorm");
+    HIP_TRY(launch_rmsnorm_rope(c->dtype, x, w->rms1, lw.u1, (int)T, c->d_model, c->rms_eps, nullptr, lw.rope,
+                                c->head_dim, c->rope_base, seq_len, s),
+            "rmsnorm");
   }
   GemmArgs g = {};
   g.epi = EPI_QKV_ROPE;
@@ -1103,7 +1102,7 @@ sas_status sas_decode_step(const sas_config* c, int32_t batch, const void* x, co
   {
     Timed tm("rmsnorm", s);
     HIP_TRY(launch_rmsnorm_rope(c->dtype, x, w->rms1, dw.u1, batch, c->d_model, c->rms_eps, pos, dw.rope, dh,
-                                c->rope_base, s),
+                                c->rope_base, batch, s),
             "rmsnorm");
   }
   GemmArgs g = {};

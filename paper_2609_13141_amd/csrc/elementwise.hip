@@ -1,4 +1,4 @@
-// RMSNorm and the rotary-embedding table.
+// RMSNorm, optionally with the rotary-embedding table of its rows.
 #include "common.h"
 #include "kernels.h"
 
@@ -6,15 +6,16 @@ namespace sas {
 
 // One workgroup of 256 threads per row; each thread keeps its 16-byte
 // chunks of the row in registers between the sum of squares (fp32) and the
-// scaled write, rounded once to the activation dtype.  With ROPE the
-// workgroup also writes its row's rotary table entries for position pos[row]
-// (rope[row, i] = (cos, sin) of pos * base^(-2i/dh), fp64, rounded to fp32),
-// computed while the row's loads are in flight.
+// scaled write, rounded once to the activation dtype.  With ROPE a row
+// below rope_rows also writes its rotary table entries for position pos[row]
+// (the row index itself without pos): rope[row, i] = (cos, sin) of
+// pos * base^(-2i/dh), evaluated in fp64 and rounded to fp32, computed while
+// the row's loads are in flight.
 template <typename T, int CPT, bool ROPE>
 __global__ void __launch_bounds__(256) rmsnorm_kernel(const T* __restrict__ x, const T* __restrict__ gamma,
                                                       T* __restrict__ out, int d, float eps,
                                                       const int32_t* __restrict__ pos, float2* __restrict__ rope,
-                                                      int dh, double base) {
+                                                      int dh, double base, int rope_rows) {
   constexpr int EPC = 16 / sizeof(T);  // elements per 16-byte chunk
   const size_t row = blockIdx.x;
   const T* xr = x + row * (size_t)d;
@@ -28,9 +29,12 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const T* __restrict__ x, c
   }
   if constexpr (ROPE) {
     const int half = dh >> 1;
-    for (int i = threadIdx.x; i < half; i += 256) {
-      const double ang = (double)pos[row] * pow(base, -2.0 * (double)i / (double)dh);
-      rope[row * (size_t)half + i] = make_float2((float)cos(ang), (float)sin(ang));
+    if (row < (size_t)rope_rows) {
+      const double p = pos ? (double)pos[row] : (double)row;
+      for (int i = threadIdx.x; i < half; i += 256) {
+        const double ang = p * pow(base, -2.0 * (double)i / (double)dh);
+        rope[row * (size_t)half + i] = make_float2((float)cos(ang), (float)sin(ang));
+      }
     }
   }
   float ss = 0.f;
@@ -65,18 +69,19 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const T* __restrict__ x, c
 }
 
 hipError_t launch_rmsnorm_rope(int dtype, const void* x, const void* gamma, void* out, int rows, int d, float eps,
-                               const int32_t* pos, float2* rope, int dh, float base, hipStream_t s) {
+                               const int32_t* pos, float2* rope, int dh, float base, int rope_rows,
+                               hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   // d is a multiple of 8 (validated); up to 16 chunks of 16 bytes per thread
   const int epc = dtype == SAS_BF16 ? 8 : 4;
   const int cpt = (d / epc + 255) / 256;
   if (cpt > 16) return hipErrorInvalidValue;
-  if (rope && !pos) return hipErrorInvalidValue;
+  if (rope && rope_rows > rows) return hipErrorInvalidValue;
 #define RMS_LAUNCH(T, C)                                                                                      \
   (rope ? rmsnorm_kernel<T, C, true><<<rows, 256, 0, s>>>((const T*)x, (const T*)gamma, (T*)out, d, eps, pos, \
-                                                          rope, dh, (double)base)                             \
+                                                          rope, dh, (double)base, rope_rows)                  \
         : rmsnorm_kernel<T, C, false><<<rows, 256, 0, s>>>((const T*)x, (const T*)gamma, (T*)out, d, eps,     \
-                                                           nullptr, nullptr, dh, 0.0))
+                                                           nullptr, nullptr, dh, 0.0, 0))
   if (dtype == SAS_BF16) {
     if (cpt <= 2) RMS_LAUNCH(bf16_t, 2);
     else if (cpt <= 4) RMS_LAUNCH(bf16_t, 4);
@@ -92,24 +97,7 @@ hipError_t launch_rmsnorm_rope(int dtype, const void* x, const void* gamma, void
 
 hipError_t launch_rmsnorm(int dtype, const void* x, const void* gamma, void* out, int rows, int d,
                           float eps, hipStream_t s) {
-  return launch_rmsnorm_rope(dtype, x, gamma, out, rows, d, eps, nullptr, nullptr, 0, 0.f, s);
-}
-
-__global__ void rope_table_kernel(float2* __restrict__ rope, int n, int half, int dh, double base) {
-  int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= n * half) return;
-  int p = idx / half, i = idx % half;
-  double theta = pow(base, -2.0 * (double)i / (double)dh);
-  double ang = (double)p * theta;
-  rope[idx] = make_float2((float)cos(ang), (float)sin(ang));
-}
-
-hipError_t launch_rope_table(float2* rope, int n, int dh, float base, hipStream_t s) {
-  int half = dh / 2;
-  int tot = n * half;
-  if (tot <= 0) return hipSuccess;
-  rope_table_kernel<<<cdiv(tot, 256), 256, 0, s>>>(rope, n, half, dh, (double)base);
-  return hipGetLastError();
+  return launch_rmsnorm_rope(dtype, x, gamma, out, rows, d, eps, nullptr, nullptr, 0, 0.f, 0, s);
 }
 
 }  // namespace sas

@@ -14,14 +14,12 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // out[r, :] = x[r, :] / sqrt(mean(x[r, :]^2) + eps) * gamma   (fp32 math)
 hipError_t launch_rmsnorm(int dtype, const void* x, const void* gamma, void* out, int rows, int d,
                           float eps, hipStream_t s);
-// RMSNorm and, in the same launch, the rotary table rows of positions pos[row]
-// (rope [rows, dh/2] float2, (cos, sin) of pos * base^(-2i/dh) evaluated in fp64);
-// rope == NULL: norm only.
+// RMSNorm and, in the same launch, the rotary table rows [0, rope_rows) for the
+// positions pos[row] (the row index when pos is NULL): rope [rope_rows, dh/2]
+// float2, (cos, sin) of pos * base^(-2i/dh) evaluated in fp64; rope == NULL: norm only.
 hipError_t launch_rmsnorm_rope(int dtype, const void* x, const void* gamma, void* out, int rows, int d, float eps,
-                               const int32_t* pos, float2* rope, int dh, float base, hipStream_t s);
-// rope[p, i] = (cos(p * theta_i), sin(p * theta_i)), theta_i = base^(-2i/dh),
-// for p in [0, n), i in [0, dh/2); computed in fp64, stored as float2.
-hipError_t launch_rope_table(float2* rope, int n, int dh, float base, hipStream_t s);
+                               const int32_t* pos, float2* rope, int dh, float base, int rope_rows,
+                               hipStream_t s);
 
 // ---- gemm.hip --------------------------------------------------------------
 // C = A[M, K] * B[N, K]^T with one of three fused epilogues.

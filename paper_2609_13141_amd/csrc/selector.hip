@@ -17,7 +17,7 @@ namespace sas {
 
 // ---------------------------------------------------------------------------
 // Block summaries: thread per (b, g, m, 8-dim chunk); the B keys of the block
-// are read 8 at a time (independent 16-byte loads) and summed per dimension
+// are read 16 at a time (independent 16-byte loads) and summed per dimension
 // in fp64 in ascending token order.
 template <typename T>
 __global__ void summaries_kernel(const T* __restrict__ K, T* __restrict__ out, int n, int Hkv, int dh,
@@ -42,12 +42,12 @@ __global__ void summaries_kernel(const T* __restrict__ K, T* __restrict__ out, i
   double acc[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) acc[e] = 0.0;
-  for (int i0 = 0; i0 < B; i0 += 8) {
-    Vec8<T> v[8];
+  for (int i0 = 0; i0 < B; i0 += 16) {  // B is a multiple of 16
+    Vec8<T> v[16];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) v[q].load(p + (size_t)(i0 + q) * stride);
+    for (int q = 0; q < 16; ++q) v[q].load(p + (size_t)(i0 + q) * stride);
 #pragma unroll
-    for (int q = 0; q < 8; ++q)
+    for (int q = 0; q < 16; ++q)
 #pragma unroll
       for (int e = 0; e < 8; ++e) acc[e] += (double)v[q].get(e);
   }
