@@ -142,18 +142,18 @@ hipError_t launch_block_summaries(int dtype, const void* K, int b, int n, int Hk
 // Selection: one workgroup of SEL_NW waves per 64 consecutive query rows of
 // one (batch, group); lane = query row.  The 64 gate queries are staged in
 // LDS once; the waves split the historical blocks into contiguous ranges and
-// walk theirs in chunks of SEL_MC summaries staged in LDS as fp32 (exact for
-// bf16 and fp32 summaries, and half the bytes of fp64 per broadcast read),
-// one exact fp64 FMA chain per (row, block), j ascending, each keeping a
-// register Top-K and a running LSE.  The waves' lists are then merged into wave 0's in
-// wave order, which reproduces a single ascending scan (strict comparisons
-// keep the lower block first on equal scores).
-constexpr int SEL_MC = 8;   // summaries per wave per step
+// walk theirs in chunks of SEL_MC summaries (8, or 4 when no wave has more
+// than 4 blocks) staged in LDS as fp32 (exact for bf16 and fp32 summaries,
+// and half the bytes of fp64 per broadcast read), one exact fp64 FMA chain
+// per (row, block), j ascending, each keeping a register Top-K and a running
+// LSE.  The waves' lists are then merged into wave 0's in wave order, which
+// reproduces a single ascending scan (strict comparisons keep the lower block
+// first on equal scores).
 constexpr int SEL_NW = 4;   // waves per workgroup
 
 __device__ __forceinline__ void lds_fence() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
-template <typename T, int DH, int KMAX>
+template <typename T, int DH, int KMAX, int SEL_MC>
 __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
   constexpr int KB_BYTES = SEL_NW * SEL_MC * DH * 4;
   constexpr int MG_BYTES = KMAX * WAVE * 12 + WAVE * 8 + WAVE * 4;
@@ -252,10 +252,11 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
   for (int m0 = mb; m0 < me; m0 += SEL_MC) {
     const int mc = min(SEL_MC, me - m0);
     {
-      constexpr int NC = DH / 8;
+      constexpr int NC = DH / 8, NCH = SEL_MC * NC;  // 8-value chunks of the staged summaries
 #pragma unroll
-      for (int i = 0; i < SEL_MC * NC / WAVE; ++i) {
+      for (int i = 0; i < (NCH + WAVE - 1) / WAVE; ++i) {
         const int c = lane + i * WAVE;
+        if (NCH % WAVE != 0 && c >= NCH) continue;
         const int r = c / NC, c8 = c % NC;
         Vec8<T> v;
         v.load(kbar + (size_t)(m0 + min(r, mc - 1)) * DH + c8 * 8);
@@ -401,9 +402,16 @@ __global__ void finish_table_kernel(float* __restrict__ table, const float* __re
 template <typename T, int DH>
 static void run_select(const SelectArgs& a, hipStream_t s) {
   dim3 grid(cdiv(a.n, WAVE), a.Hkv, a.b);
-  if (a.K <= 8) select_kernel<T, DH, 8><<<grid, SEL_NW * WAVE, 0, s>>>(a);
-  else if (a.K <= 16) select_kernel<T, DH, 16><<<grid, SEL_NW * WAVE, 0, s>>>(a);
-  else select_kernel<T, DH, 32><<<grid, SEL_NW * WAVE, 0, s>>>(a);
+  // chunks of 4 summaries when no wave has more than 4 blocks to score (short sequences)
+  if (cdiv(a.NB, SEL_NW) <= 4) {
+    if (a.K <= 8) select_kernel<T, DH, 8, 4><<<grid, SEL_NW * WAVE, 0, s>>>(a);
+    else if (a.K <= 16) select_kernel<T, DH, 16, 4><<<grid, SEL_NW * WAVE, 0, s>>>(a);
+    else select_kernel<T, DH, 32, 4><<<grid, SEL_NW * WAVE, 0, s>>>(a);
+  } else {
+    if (a.K <= 8) select_kernel<T, DH, 8, 8><<<grid, SEL_NW * WAVE, 0, s>>>(a);
+    else if (a.K <= 16) select_kernel<T, DH, 16, 8><<<grid, SEL_NW * WAVE, 0, s>>>(a);
+    else select_kernel<T, DH, 32, 8><<<grid, SEL_NW * WAVE, 0, s>>>(a);
+  }
 }
 
 hipError_t launch_select(int dtype, const SelectArgs& a, hipStream_t s) {
