@@ -31,6 +31,7 @@ CASES = [
     W(dh=64, B=128, K=1, n=400, H=2, Hkv=1, index=106),
     W(dtype="f32", dh=128, B=64, K=2, n=200, H=2, Hkv=1, index=107),
     W(K=0, index=108),
+    W(dh=128, B=128, K=2, n=520, H=4, Hkv=2, index=111),
 ]
 IDS = [f"{w.dtype}-{w.mode}-dh{w.head_dim}-B{w.block_size}-K{w.top_k}-n{w.seq_len}-G{w.n_heads // w.n_kv_heads}"
        for w in CASES]
@@ -90,3 +91,27 @@ def test_attention_backward_benchmark_shape():
     assert_close(bw["dq"][0].float().cpu().numpy(), dQ, "bf16", "dQ")
     assert_close(bw["dk"][0].float().cpu().numpy(), dK, "bf16", "dK")
     assert_close(bw["dv"][0].float().cpu().numpy(), dV, "bf16", "dV")
+
+
+def test_attention_backward_4k_b4_work_queue():
+    # 4 x 4096 tokens, 32/32 heads, K = 16: more jobs than resident workgroups, so both passes
+    # run as work queues, and dK/dV walks the per-tile lists of attending rows.  The oracle
+    # checks every row of two heads of the second sequence (one head per KV group: a head's
+    # gradients depend on that head and its group alone, so the oracle runs on the slice).
+    w = configs.BY_NAME["7b_layer_4k_b4"].with_(index=110)
+    print("\n[case] backward at 4 x 4096 (work queues, row lists)", flush=True)
+    q, k, v, d_o, fw, bw = _run(w)
+    bi, heads = 1, [0, 31]
+    st = oracle.select(f64(q[bi][:, heads]), f64(k[bi][:, heads]), w.block_size, w.top_k, "bf16")
+    np.testing.assert_array_equal(fw["sel_idx"][bi][heads].cpu().numpy(), st["sel"])
+    for j, h in enumerate(heads):
+        sl = slice(h, h + 1)
+        dQ, dK, dV, dL = oracle.sas_attention_backward(f64(q[bi][:, sl]), f64(k[bi][:, sl]), f64(v[bi][:, sl]),
+                                                       f64(d_o[bi][:, sl]), w.block_size, "gated",
+                                                       st["sel"][j:j + 1], st["log_gate"][j:j + 1])
+        assert_close(bw["dq"][bi][:, sl].float().cpu().numpy(), dQ, "bf16", f"dQ h={h}")
+        assert_close(bw["dk"][bi][:, sl].float().cpu().numpy(), dK, "bf16", f"dK h={h}")
+        assert_close(bw["dv"][bi][:, sl].float().cpu().numpy(), dV, "bf16", f"dV h={h}")
+        sel = st["sel"][j]
+        want = np.where(sel >= 0, np.take_along_axis(dL[0], np.maximum(sel, 0), axis=1), 0.0)
+        assert_close(bw["dlog_gate"][bi][h].cpu().numpy(), want, "bf16", f"dlog_gate h={h}")
