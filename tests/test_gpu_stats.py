@@ -126,7 +126,28 @@ def test_stats_benchmark_shape_every_row():
     fw = sas.attention_prefill(cfg, qd, kd, vd)
     st = sas.selection_stats(cfg, qd, kd, vd, fw["sel_idx"])
     torch.cuda.synchronize()
-    sel = fw["sel_idx"][0].cpu().numpy()
+    sel = oracle.select(f64(q[0]), f64(k[0]), w.block_size, w.top_k, "bf16")["sel"]
+    np.testing.assert_array_equal(fw["sel_idx"][0].cpu().numpy(), sel)
     cov, cov_v = mass_coverage(f64(q[0]), f64(k[0]), f64(v[0]), w.block_size, sel)
     assert_close(st["cov"][0].cpu().numpy(), cov, "bf16", "cov", tol=1e-4)
     assert_close(st["cov_v"][0].cpu().numpy(), cov_v, "bf16", "cov_v", tol=1e-4)
+
+
+def test_stats_4k_b4_work_queue():
+    # 4 x 4096 tokens, 32/32 heads: more jobs than resident workgroups (work queue); every row
+    # of one head of the last sequence (one head per group: its coverage depends on it alone)
+    w = configs.BY_NAME["7b_layer_4k_b4"].with_(index=172)
+    print("\n[case] stats at 4 x 4096 (work queue)", flush=True)
+    q, k, v = inputs.qkv(w)
+    cfg = sas.make_config(w)
+    qd, kd, vd = (sas.to_device(a, "bf16") for a in (q, k, v))
+    fw = sas.attention_prefill(cfg, qd, kd, vd)
+    st = sas.selection_stats(cfg, qd, kd, vd, fw["sel_idx"])
+    torch.cuda.synchronize()
+    bi, h = 3, 17
+    sl = slice(h, h + 1)
+    sel = oracle.select(f64(q[bi][:, sl]), f64(k[bi][:, sl]), w.block_size, w.top_k, "bf16")["sel"]
+    np.testing.assert_array_equal(fw["sel_idx"][bi][sl].cpu().numpy(), sel)
+    cov, cov_v = mass_coverage(f64(q[bi][:, sl]), f64(k[bi][:, sl]), f64(v[bi][:, sl]), w.block_size, sel)
+    assert_close(st["cov"][bi][sl].cpu().numpy(), cov, "bf16", "cov", tol=1e-4)
+    assert_close(st["cov_v"][bi][sl].cpu().numpy(), cov_v, "bf16", "cov_v", tol=1e-4)
