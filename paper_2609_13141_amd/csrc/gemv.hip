@@ -72,6 +72,34 @@ __global__ void __launch_bounds__(NW * 64) gemv_kernel(GemvParams P) {
   const bool avalid = c < P.M;
   const bf16_t* ar = P.A + (size_t)arow * P.K;
 
+  // QKV epilogue inputs of this lane (pair gi * 8 + c % 8, rows 4 kg + v), read before the
+  // weight stream so their latency (the page offset is a dependent lookup) is hidden by it
+  const int hh = P.dh >> 1;
+  float2 cs_pre[4];
+  long long off_pre[4];
+  int ps_pre[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    cs_pre[v] = make_float2(1.f, 0.f);
+    off_pre[v] = -1;
+    ps_pre[v] = 0;
+  }
+  if (P.epi == EPI_QKV_ROPE && wave == 0) {
+    const int p = min(gi * 8 + (c & 7), P.npairs - 1);
+    const int hd = p / hh, ir = p % hh;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int row = 4 * kg + v;
+      if (row >= P.M) continue;
+      if (hd < P.H + P.Hkv) cs_pre[v] = P.rope[(size_t)row * hh + ir];
+      if (P.k_pages && hd >= P.H) {
+        const int g = hd < P.H + P.Hkv ? hd - P.H : hd - P.H - P.Hkv;
+        ps_pre[v] = P.pos[row];
+        off_pre[v] = P.geom.offset(row, g, ps_pre[v], P.Hkv, P.dh);
+      }
+    }
+  }
+
   // this wave's k range, in chunks of 128
   const int nchunk = P.K / 128;
   const int per = (nchunk + NW - 1) / NW;
@@ -135,7 +163,6 @@ __global__ void __launch_bounds__(NW * 64) gemv_kernel(GemvParams P) {
   for (int v = 0; v < 4; ++v) partner[v] = __shfl_xor(tot[v], 8, 64);
   if (c >= 8 || !cvalid) return;
   const int p = gi * 8 + c;
-  const int hh = P.dh >> 1;
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
     const int row = 4 * kg + v;
@@ -151,7 +178,7 @@ __global__ void __launch_bounds__(NW * 64) gemv_kernel(GemvParams P) {
     else if (hd < P.H + P.Hkv) dst = P.out1 + ((size_t)row * P.Hkv + (hd - P.H)) * P.dh;
     else dst = P.out2 + ((size_t)row * P.Hkv + (hd - P.H - P.Hkv)) * P.dh;
     if (hd < P.H + P.Hkv) {
-      const float2 cs = P.rope[(size_t)row * hh + ir];
+      const float2 cs = cs_pre[v];
       const float o1 = x1 * cs.x - x2 * cs.y;
       const float o2 = x2 * cs.x + x1 * cs.y;
       x1 = o1;
@@ -164,8 +191,8 @@ __global__ void __launch_bounds__(NW * 64) gemv_kernel(GemvParams P) {
       // cache append of this row's K or V, dimensions ir and ir + dh/2
       const bool isk = hd < P.H + P.Hkv;
       const int g = isk ? hd - P.H : hd - P.H - P.Hkv;
-      const int ps = P.pos[row];
-      const long long off = P.geom.offset(row, g, ps, P.Hkv, P.dh);
+      const int ps = ps_pre[v];
+      const long long off = off_pre[v];
       if (off < 0) continue;
       bf16_t* pg = (bf16_t*)(isk ? P.k_pages : P.v_pages) + off;
       pg[ir] = b1;
