@@ -157,9 +157,10 @@ hipError_t launch_kv_append(int dtype, const void* k, const void* v, const Decod
 // One wave per (i, g).  Gate query: rho(sum of the group's heads), optionally
 // projected; scores: sequential fp64 sums over ascending j; rank of a block =
 // number of blocks strictly ahead of it under (r desc, m asc); kept if rank < K,
-// written in ascending block order.
+// written in ascending block order.  A lane reads its summary row with 16-byte
+// loads issued together.
 
-template <typename T>
+template <typename T, int DH>
 __global__ void __launch_bounds__(64) decode_select_kernel(const T* __restrict__ q, DecodeArgs c,
                                                            int32_t* __restrict__ sel) {
   __shared__ double qh[128];
@@ -167,7 +168,7 @@ __global__ void __launch_bounds__(64) decode_select_kernel(const T* __restrict__
   __shared__ double rs[DSEL_WAVE_MAX_BLOCKS];
   const int lane = threadIdx.x;
   const int g = blockIdx.x, i = blockIdx.y;
-  const int G = c.H / c.Hkv, dh = c.dh, K = c.K;
+  const int G = c.H / c.Hkv, dh = DH, K = c.K;
   const int p = c.pos[i];
   const int ct = max(0, min(p / c.B, min(c.max_blocks, DSEL_WAVE_MAX_BLOCKS)));
   for (int j = lane; j < dh; j += 64) {
@@ -189,9 +190,15 @@ __global__ void __launch_bounds__(64) decode_select_kernel(const T* __restrict__
   }
   const T* ks = (const T*)c.k_summary + ((size_t)i * c.Hkv + g) * c.max_blocks * dh;
   for (int m = lane; m < ct; m += 64) {
-    const T* kr = ks + (size_t)m * dh;
+    const T* kr = ks + (size_t)m * DH;
+    Vec8<T> kv[DH / 8];
+#pragma unroll
+    for (int c8 = 0; c8 < DH / 8; ++c8) kv[c8].load(kr + c8 * 8);
     double acc = 0.0;
-    for (int j = 0; j < dh; ++j) acc = fma(qh[j], (double)Act<T>::to_f32(kr[j]), acc);
+#pragma unroll
+    for (int c8 = 0; c8 < DH / 8; ++c8)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc = fma(qh[c8 * 8 + e], (double)kv[c8].get(e), acc);
     rs[m] = acc;
   }
   __syncthreads();
@@ -413,8 +420,14 @@ hipError_t launch_decode_select(int dtype, const void* q, const DecodeArgs& c, i
   if (c.K <= 0) return hipSuccess;
   if (c.max_blocks <= DSEL_WAVE_MAX_BLOCKS) {
     dim3 grid(c.Hkv, c.b);
-    if (dtype == SAS_BF16) decode_select_kernel<bf16_t><<<grid, 64, 0, s>>>((const bf16_t*)q, c, sel);
-    else decode_select_kernel<float><<<grid, 64, 0, s>>>((const float*)q, c, sel);
+    if (c.dh != 64 && c.dh != 128) return hipErrorInvalidValue;
+    if (dtype == SAS_BF16) {
+      if (c.dh == 128) decode_select_kernel<bf16_t, 128><<<grid, 64, 0, s>>>((const bf16_t*)q, c, sel);
+      else decode_select_kernel<bf16_t, 64><<<grid, 64, 0, s>>>((const bf16_t*)q, c, sel);
+    } else {
+      if (c.dh == 128) decode_select_kernel<float, 128><<<grid, 64, 0, s>>>((const float*)q, c, sel);
+      else decode_select_kernel<float, 64><<<grid, 64, 0, s>>>((const float*)q, c, sel);
+    }
     return hipGetLastError();
   }
   if (c.max_blocks > DSEL_LONG_MAXB || !scores) return hipErrorInvalidValue;
