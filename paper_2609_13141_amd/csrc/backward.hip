@@ -24,18 +24,30 @@
 
 namespace sas {
 
-// Delta[b, h, t] = sum_d O[b, t, h, d] dO[b, t, h, d] (fp32)
+// Delta[b, h, t] = sum_d O[b, t, h, d] dO[b, t, h, d] (fp32): dh / 8 threads per
+// row (rows (b, t, h) are contiguous in [b, n, H, dh]), 16-byte loads of 8
+// values each, the partial sums added across the row's lanes.
 template <typename T>
-__global__ void bwd_delta_kernel(const T* __restrict__ O, const T* __restrict__ dO, int b, int n, int H, int dh,
-                                 float* __restrict__ delta) {
-  const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6, lane = threadIdx.x & 63;
-  if (wave >= b * n * H) return;
-  const int h = wave % H, t = (wave / H) % n, bi = wave / (H * n);
-  const size_t off = (((size_t)bi * n + t) * H + h) * dh;
+__global__ void __launch_bounds__(256) bwd_delta_kernel(const T* __restrict__ O, const T* __restrict__ dO, int b,
+                                                        int n, int H, int dh, float* __restrict__ delta) {
+  const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int tpr = dh / 8;  // threads per row: 16 or 8, aligned groups of lanes
+  const size_t rows = (size_t)b * n * H, row = gid / tpr;
+  const int c8 = (int)(gid % tpr);
+  const bool valid = row < rows;
   float acc = 0.f;
-  for (int d = lane; d < dh; d += 64) acc = fmaf(Act<T>::to_f32(O[off + d]), Act<T>::to_f32(dO[off + d]), acc);
-  acc = wave_sum(acc);
-  if (lane == 0) delta[((size_t)bi * H + h) * n + t] = acc;
+  if (valid) {
+    Vec8<T> o, d;
+    o.load(O + row * dh + c8 * 8);
+    d.load(dO + row * dh + c8 * 8);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc = fmaf(o.get(e), d.get(e), acc);
+  }
+  for (int sh = tpr >> 1; sh > 0; sh >>= 1) acc += __shfl_xor(acc, sh, 64);
+  if (valid && c8 == 0) {
+    const int h = (int)(row % H), t = (int)((row / H) % n), bi = (int)(row / ((size_t)H * n));
+    delta[((size_t)bi * H + h) * n + t] = acc;
+  }
 }
 
 // How block m enters the attention of query t and its gradient (natural-log
@@ -1209,13 +1221,14 @@ hipError_t launch_partial_sum(const float* part, int U, int ZO, int S, size_t E,
 
 hipError_t launch_attention_backward(int dtype, const BwdArgs& a, hipStream_t s) {
   if (a.n <= 0 || a.b <= 0) return hipSuccess;
-  const int waves = a.b * a.n * a.H;
+  if (a.dh != 64 && a.dh != 128) return hipErrorInvalidValue;
+  const size_t dthreads = (size_t)a.b * a.n * a.H * (a.dh / 8);
   if (dtype == SAS_BF16)
-    bwd_delta_kernel<bf16_t><<<cdiv(waves, 4), 256, 0, s>>>((const bf16_t*)a.O, (const bf16_t*)a.dO, a.b, a.n, a.H,
-                                                              a.dh, a.delta);
+    bwd_delta_kernel<bf16_t><<<(unsigned)cdiv(dthreads, 256), 256, 0, s>>>((const bf16_t*)a.O, (const bf16_t*)a.dO,
+                                                                            a.b, a.n, a.H, a.dh, a.delta);
   else
-    bwd_delta_kernel<float><<<cdiv(waves, 4), 256, 0, s>>>((const float*)a.O, (const float*)a.dO, a.b, a.n, a.H,
-                                                             a.dh, a.delta);
+    bwd_delta_kernel<float><<<(unsigned)cdiv(dthreads, 256), 256, 0, s>>>((const float*)a.O, (const float*)a.dO,
+                                                                           a.b, a.n, a.H, a.dh, a.delta);
   const bool need_dlg = a.dlog_gate && a.mode == SAS_MODE_GATED && a.K > 0 && !a.full;
   BwdArgs P = a;
   if (!need_dlg) P.dlg_head = nullptr;
