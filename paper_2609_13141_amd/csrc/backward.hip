@@ -1074,12 +1074,21 @@ __global__ void __launch_bounds__(256) selector_ds_kernel(const int32_t* __restr
   const int F = doc_first(doc, row / (n * Hkv), NB, row % n, B);  // historical blocks are [F, C)
   const float* lg = log_gate + (size_t)row * NB;
   const float* dfr = dfull ? dfull + (size_t)row * NB : nullptr;
+  // every load of the row issued together (slot and its gradient, the first 64 log gates),
+  // masked afterwards, so the row costs one memory round trip
   int sk = -1;
   float dk = 0.f;
-  if (!dfr && lane < K) {
-    sk = sel[(size_t)row * K + lane];
-    if (sk >= 0) dk = dlog_gate[(size_t)row * K + lane];
+  const bool has_slot = !dfr && lane < K;
+  {
+    const size_t so = (size_t)row * K + (has_slot ? lane : 0);
+    const int s0 = K > 0 && sel ? sel[so] : -1;
+    const float d0 = K > 0 && !dfr && dlog_gate ? dlog_gate[so] : 0.f;
+    if (has_slot && s0 >= 0) {
+      sk = s0;
+      dk = d0;
+    }
   }
+  const float lg0 = lg[min(lane, NB - 1)];
   float D = 0.f;  // sum of the row's log-gate gradient (softmax)
   if (act == SAS_ACT_SOFTMAX) {
     if (dfr) {
@@ -1104,8 +1113,9 @@ __global__ void __launch_bounds__(256) selector_ds_kernel(const int32_t* __restr
     }
     float v = 0.f;
     if (m < C && m >= F) {
-      if (act == SAS_ACT_SOFTMAX) v = dl - expf(lg[m]) * D;
-      else if (act == SAS_ACT_SIGMOID) v = dl * (1.f - expf(lg[m]));
+      const float lgm = m0 == 0 ? lg0 : lg[m];
+      if (act == SAS_ACT_SOFTMAX) v = dl - expf(lgm) * D;
+      else if (act == SAS_ACT_SIGMOID) v = dl * (1.f - expf(lgm));
       else v = dl;
     }
     if (m < NB) out[m] = v;
