@@ -1133,7 +1133,8 @@ hipError_t launch_selector_ds(const int32_t* sel, const float* log_gate, const f
   return hipGetLastError();
 }
 
-// 64 x 64 output tile per workgroup, 16-deep k steps staged in LDS as fp32;
+// 64 x 64 output tile per workgroup, 16-deep k steps staged in LDS as fp32
+// (the next step's values loaded into registers during this step's FMAs);
 // thread (tx, ty) owns rows ty + 16 r and columns tx + 16 c.  Tile loads run
 // along whichever of the operand's two indices is contiguous.
 template <typename T>
@@ -1152,7 +1153,9 @@ __global__ void __launch_bounds__(256) small_gemm_kernel(SmallGemm P) {
   for (int r = 0; r < 4; ++r)
 #pragma unroll
     for (int c = 0; c < 4; ++c) acc[r][c] = 0.f;
-  for (int k0 = kb; k0 < ke; k0 += 16) {
+  // the next k step's tile values are loaded into registers while this one is multiplied
+  float ra[4], rb[4];
+  auto load = [&](int k0) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int idx = tid + e * 256;
@@ -1165,7 +1168,7 @@ __global__ void __launch_bounds__(256) small_gemm_kernel(SmallGemm P) {
         ii = idx >> 4;
       }
       const int i = i0 + ii, k = k0 + kk;
-      As[kk][ii] = (i < P.M && k < ke) ? A[i * P.sAi + k * P.sAk] : 0.f;
+      ra[e] = (i < P.M && k < ke) ? A[i * P.sAi + k * P.sAk] : 0.f;
       int jj;
       if (P.sBj == 1) {
         jj = idx & 63;
@@ -1175,9 +1178,24 @@ __global__ void __launch_bounds__(256) small_gemm_kernel(SmallGemm P) {
         jj = idx >> 4;
       }
       const int j = j0 + jj, k2 = k0 + kk;
-      Bs[kk][jj] = (j < P.N && k2 < ke) ? Act<T>::to_f32(Bm[j * P.sBj + k2 * P.sBk]) : 0.f;
+      rb[e] = (j < P.N && k2 < ke) ? Act<T>::to_f32(Bm[j * P.sBj + k2 * P.sBk]) : 0.f;
     }
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int idx = tid + e * 256;
+      if (P.sAi == 1) As[idx >> 6][idx & 63] = ra[e];
+      else As[idx & 15][idx >> 4] = ra[e];
+      if (P.sBj == 1) Bs[idx >> 6][idx & 63] = rb[e];
+      else Bs[idx & 15][idx >> 4] = rb[e];
+    }
+  };
+  if (kb < ke) load(kb);
+  for (int k0 = kb; k0 < ke; k0 += 16) {
+    store();
     __syncthreads();
+    if (k0 + 16 < ke) load(k0 + 16);
 #pragma unroll
     for (int kk = 0; kk < 16; ++kk) {
       float a[4], bv[4];
