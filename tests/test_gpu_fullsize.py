@@ -135,3 +135,22 @@ def test_decode_step_at_stack_shape_matches_oracle():
         assert_close(y[bsel].float().cpu().numpy(), yo, "bf16", f"y t={t}")
         same = np.all(sel[bsel].cpu().numpy() == selo, axis=-1)
         assert same.mean() >= 0.97, same.mean()
+
+
+def test_attention_7b_1k_every_row_output():
+    # the benchmark workload's attention (1024 tokens, 32 heads): fewer (query tile, head) jobs
+    # than resident workgroups, so the long query tiles run split and are merged; O and LSE of
+    # every row of the first sequence against the oracle
+    w = configs.L7B_1K.with_(index=173)
+    print("\n[case] attention at the 7B 1024-token shape, every row", flush=True)
+    q, k, v = inputs.qkv(w)
+    cfg = sas.make_config(w)
+    out = sas.attention_prefill(cfg, *(sas.to_device(a, "bf16") for a in (q, k, v)), log_gate=True)
+    torch.cuda.synchronize()
+    from oracle.selector import select
+    st = select(f64(q[0]), f64(k[0]), w.block_size, w.top_k, "bf16")
+    np.testing.assert_array_equal(out["sel_idx"][0].cpu().numpy(), st["sel"])
+    _, O, LSE = oracle.sas_attention(f64(q[0]), f64(k[0]), f64(v[0]), w.block_size, "gated", "bf16",
+                                     st["sel"], st["log_gate"])
+    assert_close(out["o"][0].float().cpu().numpy(), O, "bf16", "O")
+    assert_close(out["lse"][0].cpu().numpy(), LSE, "bf16", "LSE", tol=1e-3)
