@@ -291,7 +291,7 @@ constexpr float BLOG2E = 1.4426950408889634f;
 // writes a slot's block sum once the slot's last sub-block is done; a tile is
 // processed as two halves of 32 keys to keep the live registers low enough
 // for two workgroups per compute unit.
-template <int DH, int LSB>
+template <int DH, int LSB, bool PLAIN>
 __device__ __forceinline__ void bwd_dq_bf16_job(const BwdArgs& P, const int qtile, const int h, const int bi) {
   constexpr int KP = DH + 8;
   constexpr int TP = 64 + 4;
@@ -505,16 +505,24 @@ __device__ __forceinline__ void bwd_dq_bf16_job(const BwdArgs& P, const int qtil
         const bf16x8_t av = *(const bf16x8_t*)(Vs + (st * 32 + lr) * KP + ks * 16 + lk * 8);
         dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, dob[ks], dp, 0, 0, 0);
       }
+      // P, dS^T and the block sums.  PLAIN (no value weights, no straight-through gradient): a
+      // sub-block that is not attended has an offset of -inf, so its dS is already zero
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int klc = st * 32 + 8 * (v >> 2);  // key offset without the lane part (4 lk + v % 4 < 8)
         const int sb = klc >> LSB;
         float p = __builtin_amdgcn_exp2f(fmaf(sc[v], qk_scale, offs[sb]));
         if (diag && k0 + klc + 4 * lk + (v & 3) > t) p = 0.f;
-        const float dpw = outer ? wts[sb] * dp[v] : dp[v];
-        const float ds = p * (dpw - delta);
-        sc[v] = attb[sb] ? ds : 0.f;
-        dsum[sb] += outer ? p * dpw : ds;
+        if constexpr (PLAIN) {
+          const float ds = p * (dp[v] - delta);
+          sc[v] = ds;
+          dsum[sb] += ds;
+        } else {
+          const float dpw = outer ? wts[sb] * dp[v] : dp[v];
+          const float ds = p * (dpw - delta);
+          sc[v] = attb[sb] ? ds : 0.f;
+          dsum[sb] += outer ? p * dpw : ds;
+        }
       }
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
@@ -579,7 +587,7 @@ __device__ __forceinline__ void bwd_dq_bf16_job(const BwdArgs& P, const int qtil
 // One job per workgroup (grid = job count, no queue) or the work queue.
 // two workgroups per compute unit where the registers allow it without spills
 // (one sub-block per tile, or dh = 64)
-template <int DH, int LSB>
+template <int DH, int LSB, bool PLAIN>
 __global__ void __launch_bounds__(256, LSB == 6 || DH == 64 ? 2 : 1) bwd_dq_bf16_kernel(BwdArgs P) {
   const int nqt = (P.n + 127) / 128, per = P.H * P.b;
   const int njobs = nqt * per;
@@ -587,7 +595,7 @@ __global__ void __launch_bounds__(256, LSB == 6 || DH == 64 ? 2 : 1) bwd_dq_bf16
     const int job = P.queue ? queue_next_job(P.queue) : (it == 0 ? (int)blockIdx.x : njobs);
     if (job >= njobs) break;
     const int r = job % per;  // the longest (last) query tiles first, heads and batch inside
-    bwd_dq_bf16_job<DH, LSB>(P, nqt - 1 - job / per, r % P.H, r / P.H);
+    bwd_dq_bf16_job<DH, LSB, PLAIN>(P, nqt - 1 - job / per, r % P.H, r / P.H);
   }
 }
 
@@ -1029,10 +1037,19 @@ static hipError_t launch_attention_backward_bf16(const BwdArgs& P, hipStream_t s
     }
   }
   const int lsb = P.B >= 64 ? 6 : (P.B == 32 ? 5 : 4);
-  auto dq = P.dh == 128 ? (lsb == 6 ? bwd_dq_bf16_kernel<128, 6> : lsb == 5 ? bwd_dq_bf16_kernel<128, 5>
-                                                                            : bwd_dq_bf16_kernel<128, 4>)
-                        : (lsb == 6 ? bwd_dq_bf16_kernel<64, 6> : lsb == 5 ? bwd_dq_bf16_kernel<64, 5>
-                                                                           : bwd_dq_bf16_kernel<64, 4>);
+  // no value weights and no straight-through gradient: the plain elementwise step
+  const bool plain = !(P.mode == SAS_MODE_GATED && (P.outer || P.ste));
+  void (*dq)(BwdArgs);
+  if (plain)
+    dq = P.dh == 128 ? (lsb == 6 ? bwd_dq_bf16_kernel<128, 6, true> : lsb == 5 ? bwd_dq_bf16_kernel<128, 5, true>
+                                                                             : bwd_dq_bf16_kernel<128, 4, true>)
+                     : (lsb == 6 ? bwd_dq_bf16_kernel<64, 6, true> : lsb == 5 ? bwd_dq_bf16_kernel<64, 5, true>
+                                                                            : bwd_dq_bf16_kernel<64, 4, true>);
+  else
+    dq = P.dh == 128 ? (lsb == 6 ? bwd_dq_bf16_kernel<128, 6, false> : lsb == 5 ? bwd_dq_bf16_kernel<128, 5, false>
+                                                                              : bwd_dq_bf16_kernel<128, 4, false>)
+                     : (lsb == 6 ? bwd_dq_bf16_kernel<64, 6, false> : lsb == 5 ? bwd_dq_bf16_kernel<64, 5, false>
+                                                                             : bwd_dq_bf16_kernel<64, 4, false>);
   auto dkv = P.dh == 128 ? bwd_dkv_bf16_kernel<128> : bwd_dkv_bf16_kernel<64>;
   const long long jq = (long long)cdiv(P.n, 128) * P.H * P.b, jk = (long long)ntk * P.Hkv * P.b;
   const int rq = resident_workgroups(dq, 256), rk = resident_workgroups(dkv, 256);
