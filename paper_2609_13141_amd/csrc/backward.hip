@@ -696,7 +696,7 @@ __global__ void __launch_bounds__(1024) bwd_rows_scan_kernel(const int* __restri
 // row-major (A of S and dP) and transposed (A of dK^T += Q^T dS and
 // dV^T += dO^T P, read in the accumulator's row permutation).  P and dS stay
 // in registers; the causal mask compares each key with its row's index.
-template <int DH>
+template <int DH, bool PLAIN>
 __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int ktile, const int g, const int bi) {
   constexpr int NTH = 256, KT = 64;
   constexpr int KP = DH + 8;
@@ -933,7 +933,7 @@ __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int kti
         const float4 de = *(const float4*)&delta_s[8 * j + 4 * lk];
         const int4 tr = *(const int4*)&trow_s[8 * j + 4 * lk];
         float4 wt = make_float4(1.f, 1.f, 1.f, 1.f);
-        if (outer) wt = *(const float4*)&wt_s[sbk][8 * j + 4 * lk];
+        if (!PLAIN && outer) wt = *(const float4*)&wt_s[sbk][8 * j + 4 * lk];
         const float ofv[4] = {of.x, of.y, of.z, of.w}, dev[4] = {de.x, de.y, de.z, de.w};
         const float wv[4] = {wt.x, wt.y, wt.z, wt.w};
         const int trv[4] = {tr.x, tr.y, tr.z, tr.w};
@@ -942,8 +942,13 @@ __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int kti
           const int v = 4 * j + i;
           float p = __builtin_amdgcn_exp2f(fmaf(sc[v], qk_scale, ofv[i]));
           if (diag && key > trv[i]) p = 0.f;
-          pv[4 * jj + i] = p * wv[i];
-          sv[4 * jj + i] = p * (wv[i] * dp[v] - dev[i]);
+          if constexpr (PLAIN) {  // unit value weights
+            pv[4 * jj + i] = p;
+            sv[4 * jj + i] = p * (dp[v] - dev[i]);
+          } else {
+            pv[4 * jj + i] = p * wv[i];
+            sv[4 * jj + i] = p * (wv[i] * dp[v] - dev[i]);
+          }
         }
       }
       uint4 pu, su;
@@ -993,7 +998,7 @@ __device__ __forceinline__ void bwd_dkv_bf16_job(const BwdArgs& P, const int kti
     }
 }
 
-template <int DH>
+template <int DH, bool PLAIN>
 __global__ void __launch_bounds__(256, 2) bwd_dkv_bf16_kernel(BwdArgs P) {
   const int nkt = (P.n + 63) / 64, per = P.Hkv * P.b;
   const int njobs = nkt * per;
@@ -1001,7 +1006,7 @@ __global__ void __launch_bounds__(256, 2) bwd_dkv_bf16_kernel(BwdArgs P) {
     const int job = P.queue ? queue_next_job(P.queue) : (it == 0 ? (int)blockIdx.x : njobs);
     if (job >= njobs) break;
     const int r = job % per;  // the first (longest) key tiles first
-    bwd_dkv_bf16_job<DH>(P, job / per, r % P.Hkv, r / P.Hkv);
+    bwd_dkv_bf16_job<DH, PLAIN>(P, job / per, r % P.Hkv, r / P.Hkv);
   }
 }
 
@@ -1050,7 +1055,8 @@ static hipError_t launch_attention_backward_bf16(const BwdArgs& P, hipStream_t s
                                                                               : bwd_dq_bf16_kernel<128, 4, false>)
                      : (lsb == 6 ? bwd_dq_bf16_kernel<64, 6, false> : lsb == 5 ? bwd_dq_bf16_kernel<64, 5, false>
                                                                              : bwd_dq_bf16_kernel<64, 4, false>);
-  auto dkv = P.dh == 128 ? bwd_dkv_bf16_kernel<128> : bwd_dkv_bf16_kernel<64>;
+  auto dkv = P.dh == 128 ? (plain ? bwd_dkv_bf16_kernel<128, true> : bwd_dkv_bf16_kernel<128, false>)
+                         : (plain ? bwd_dkv_bf16_kernel<64, true> : bwd_dkv_bf16_kernel<64, false>);
   const long long jq = (long long)cdiv(P.n, 128) * P.H * P.b, jk = (long long)ntk * P.Hkv * P.b;
   const int rq = resident_workgroups(dq, 256), rk = resident_workgroups(dkv, 256);
   if (rq <= 0 || rk <= 0 || jq > INT32_MAX || jk > INT32_MAX) return hipErrorInvalidValue;
