@@ -23,7 +23,7 @@ Parity status of each part (how it is pinned by the oracle self-tests):
 * selector (block summaries, gate query, scores): the paper names the
   selector but does not define its architecture; its arithmetic is pinned by
   exact rational brute force and planted rankings.  The architecture itself
-  is "parity unpinned" by the paper (it is this build's reading).
+  is "parity unpinned" by the paper (it is this implementation's reading).
 * attention backward, gate backward, selector backward: pinned against
   torch autograd on a dense masked formulation and by central finite
   differences of the fp64 forward.

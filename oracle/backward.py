@@ -19,7 +19,7 @@ ds_m = dlog g_m - g_m sum_{m' < C_t} dlog g_{m'} with g = softmax(s) over the
 historical blocks.  Only selected blocks carry a bias, so dlog g is zero on
 the others; the Top-K set is piecewise constant and passes no gradient.
 
-Selector (this build's reading of the paper's undefined selector): s =
+Selector (this implementation's reading of the paper's undefined selector): s =
 r / (G sqrt(dh)), r = qhat . kbar, qhat = rho(qhat0 W_gq^T) and kbar =
 rho(kbar0 W_gk^T) when the projections exist (qhat0 = rho(sum of the group's
 query heads), kbar0 = rho(mean pooled keys)).  The backward treats the
