@@ -46,7 +46,7 @@ __global__ void fill_u32_kernel(uint32_t* p, int n, uint32_t v) {
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 
-template <int DH, int LSB>
+template <int DH, int LSB, bool OUTER>
 __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile, const int h, const int bi,
                                               const int tlo, const int thi, const int slot) {
   constexpr int KP = DH + 8;    // K tile row pitch (elements)
@@ -72,7 +72,7 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
   const bool gated = P.mode == SAS_MODE_GATED;
   const bool full = gated && P.full;  // every historical block, gates from the table
   const bool every = P.mode == SAS_MODE_DENSE || full;
-  const bool outer = gated && P.outer;
+  const bool outer = OUTER;  // the launch picks OUTER = GATED with the outer gate
   const int Kn = every ? 0 : P.K;
   const int ntiles = (n + 63) / 64;
   const int t_hi = min(n, qtile * 128 + 128) - 1;  // last query of the workgroup
@@ -258,7 +258,8 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
       for (int v = 0; v < 16; ++v) {
         const float p = __builtin_amdgcn_exp2f(s[st][v] - m_use);
         rs += p;
-        s[st][v] = outer ? p * wts[(st * 32 + 8 * (v >> 2)) >> LSB] : p;
+        if constexpr (OUTER) s[st][v] = p * wts[(st * 32 + 8 * (v >> 2)) >> LSB];
+        else s[st][v] = p;
       }
     rs += __shfl_xor(rs, 32, 64);
     l_run = l_run * alpha + rs;
@@ -347,7 +348,7 @@ __device__ __forceinline__ void attn_job_of(const AttnArgs& P, int job, int& qti
 
 // One job (query tile or part of it, head, batch entry) per workgroup (grid =
 // job count, no queue) or the work queue; the heavy (late) query tiles first.
-template <int DH, int LSB>
+template <int DH, int LSB, bool OUTER>
 __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P, int njobs) {
   for (int it = 0;; ++it) {
     const int job = P.queue ? queue_next_job(P.queue) : (it == 0 ? (int)blockIdx.x : njobs);
@@ -355,7 +356,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P, int njobs
     int qtile, h, bi, part, nparts, jbase;
     attn_job_of(P, job, qtile, h, bi, part, nparts, jbase);
     const int nt = attn_tiles(P.n, qtile), per_part = (nt + nparts - 1) / nparts;
-    attn_bf16_job<DH, LSB>(P, qtile, h, bi, part * per_part, nparts > 1 ? (part + 1) * per_part : 1 << 30,
+    attn_bf16_job<DH, LSB, OUTER>(P, qtile, h, bi, part * per_part, nparts > 1 ? (part + 1) * per_part : 1 << 30,
                            nparts > 1 ? job : -1);
   }
 }
@@ -486,10 +487,18 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
   if (dtype == SAS_BF16) {
     if (a.n > ATTN_MAX_SEQ || a.K > 32) return hipErrorInvalidValue;
     const int lsb = a.B >= 64 ? 6 : (a.B == 32 ? 5 : 4);
-    auto kern = a.dh == 128 ? (lsb == 6 ? attn_bf16_kernel<128, 6> : lsb == 5 ? attn_bf16_kernel<128, 5>
-                                                                             : attn_bf16_kernel<128, 4>)
-                            : (lsb == 6 ? attn_bf16_kernel<64, 6> : lsb == 5 ? attn_bf16_kernel<64, 5>
-                                                                            : attn_bf16_kernel<64, 4>);
+    const bool outer = a.mode == SAS_MODE_GATED && a.outer;
+    void (*kern)(AttnArgs, int);
+    if (outer)
+      kern = a.dh == 128 ? (lsb == 6 ? attn_bf16_kernel<128, 6, true> : lsb == 5 ? attn_bf16_kernel<128, 5, true>
+                                                                             : attn_bf16_kernel<128, 4, true>)
+                         : (lsb == 6 ? attn_bf16_kernel<64, 6, true> : lsb == 5 ? attn_bf16_kernel<64, 5, true>
+                                                                            : attn_bf16_kernel<64, 4, true>);
+    else
+      kern = a.dh == 128 ? (lsb == 6 ? attn_bf16_kernel<128, 6, false> : lsb == 5 ? attn_bf16_kernel<128, 5, false>
+                                                                              : attn_bf16_kernel<128, 4, false>)
+                         : (lsb == 6 ? attn_bf16_kernel<64, 6, false> : lsb == 5 ? attn_bf16_kernel<64, 5, false>
+                                                                             : attn_bf16_kernel<64, 4, false>);
     const int nqt = cdiv(a.n, 128), ntk = cdiv(a.n, 64), per = a.H * a.b;
     const long long jobs = (long long)nqt * per;
     const int res = resident_workgroups(kern, 256);
