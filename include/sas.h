@@ -13,7 +13,7 @@
  * pipeline prefills densely and decodes block-sparsely (Sec. 5.1).
  *
  * Selector (the paper names one but does not define its architecture; this
- * library's reading, shared with its checker): block summary = mean of the
+ * library's reading, shared with the fp64 oracle): block summary = mean of the
  * block's post-RoPE keys, gate query = sum of the group's query heads, both
  * optionally projected by per-group [dh, dh] matrices, score = exact dot
  * product (fp64) scaled by 1/(G*sqrt(dh)).  Top-K ranks the exact score,
@@ -217,8 +217,9 @@ typedef struct {
 /* Bytes of scratch memory an entry point needs (0 on invalid config). */
 size_t sas_workspace_size(const sas_config* cfg, int32_t op, int32_t batch, int32_t seq_len);
 
-/* Selector + SAS attention over given Q/K/V (Alg. 1 lines 1-4 / Alg. 2
- * lines 1-4 applied to every query of a causal prefill; App. E forward).
+/* Selector + SAS attention over given Q/K/V (the scoring, Top-K, gating
+ * and attention steps of Alg. 1 / Alg. 2 applied to every query of a causal
+ * prefill; App. E forward).
  * batch >= 1, seq_len >= 1. out->o is required. */
 sas_status sas_attention_prefill(const sas_config* cfg, int32_t batch, int32_t seq_len,
                                  const sas_attn_in* in, sas_attn_out* out,
