@@ -322,13 +322,15 @@ def decode_bench(warmup):
             "kernels_ms": {k: round(v, 4) for k, v in sorted(kms.items(), key=lambda kv: -kv[1])}}
 
 
-def decode_long_bench(steps=10, warmup=3):
+def decode_long_bench(steps=60, warmup=20):
     """One 7B-shape layer's SAS decode step at 64K..512K tokens of context,
     batch 1 and 8, K = 32 blocks of 64 (the paper's default budget): the
     selection scores every cached block summary (8192 at 512K) and attends
     to the 32 kept blocks plus the current one.  The caches are filled on
     the GPU with synthetic N(0,1) keys, values and summaries (timing does not
-    depend on their values); positions start 20 tokens before the end."""
+    depend on their values); the steps cycle over the last 20 positions (a
+    step at position p attends to positions <= p only, so the later ones
+    written before it do not change its work)."""
     import torch
     from paper_2609_13141_amd import configs, inputs, sas
     base = configs.LONG_DECODE
@@ -346,18 +348,18 @@ def decode_long_bench(steps=10, warmup=3):
             x = torch.randn(b, w.d_model, device=dev).to(torch.bfloat16)
             ws = sas.Workspace(dev)
             p0 = ctx - 20
-            poss = [torch.full((b,), p0 + s, dtype=torch.int32, device=dev) for s in range(warmup + steps + 3)]
+            poss = [torch.full((b,), p0 + s, dtype=torch.int32, device=dev) for s in range(20)]
             for s in range(warmup):
-                sas.decode_step(cfg, x, poss[s], Wd, cache, sel_idx=False, ws=ws)
+                sas.decode_step(cfg, x, poss[s % len(poss)], Wd, cache, sel_idx=False, ws=ws)
             torch.cuda.synchronize()
             t0 = time.perf_counter()
             for s in range(warmup, warmup + steps):
-                sas.decode_step(cfg, x, poss[s], Wd, cache, sel_idx=False, ws=ws)
+                sas.decode_step(cfg, x, poss[s % len(poss)], Wd, cache, sel_idx=False, ws=ws)
             torch.cuda.synchronize()
             ms = (time.perf_counter() - t0) * 1e3 / steps
             sas.profiler_start(64 * 3 + 16)
             for s in range(warmup + steps, warmup + steps + 3):
-                sas.decode_step(cfg, x, poss[s], Wd, cache, sel_idx=False, ws=ws)
+                sas.decode_step(cfg, x, poss[s % len(poss)], Wd, cache, sel_idx=False, ws=ws)
             recs = sas.profiler_stop()
             fam = {}
             for name, v in recs:
@@ -365,7 +367,8 @@ def decode_long_bench(steps=10, warmup=3):
             kms = {k: sum(v) / len(v) for k, v in fam.items()}
             B, K, dh, Hkv = w.block_size, w.top_k, w.head_dim, w.n_kv_heads
             tot = 0.0
-            for t in range(p0 + warmup, p0 + warmup + steps):
+            for s in range(warmup, warmup + steps):
+                t = p0 + s % len(poss)
                 ct = t // B
                 kept = B * min(K, ct) + (t % B) + 1
                 tot += 2.0 * w.linear_params() + b * Hkv * (kept * dh * 2 * 2 + ct * dh * 2 + 2 * dh * 2)
