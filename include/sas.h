@@ -397,11 +397,13 @@ sas_status sas_layer_forward(const sas_config* cfg, int32_t batch, int32_t seq_l
  * block's summary is written; scores the summaries of the floor(pos/B)
  * complete blocks, keeps the Top-K per KV group and attends to them plus the
  * current block without gate bias.  y [b, d]; sel_idx [b, Hkv, K] optional.
+ * taps (optional, any field NULL): the step's post-RoPE q [b, H, dh], k, v
+ * [b, Hkv, dh] and h1 = x + attention [b, d].
  * Positions outside the cache are skipped by the kernels (no write). */
 sas_status sas_decode_step(const sas_config* cfg, int32_t batch, const void* x,
                            const int32_t* pos, const sas_layer_weights* w,
                            sas_paged_kv* cache, void* y, int32_t* sel_idx,
-                           void* ws, size_t ws_bytes, void* stream);
+                           sas_layer_taps* taps, void* ws, size_t ws_bytes, void* stream);
 
 /* The selection of a decode step alone (Alg. 2's Top-K over the block
  * summaries; Sec. 5.1), for long contexts where it dominates the step:

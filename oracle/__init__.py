@@ -47,19 +47,20 @@ Parity status of each part (how it is pinned by the oracle self-tests):
 from .numerics import rho, round_bf16, round_f32, rmsnorm, rope, silu
 from .selector import (block_summaries, gate_query, selector_scores,
                        normalized_log_gate, topk_blocks, select)
-from .attention import sas_attention
+from .attention import causal_attention, sas_attention
 from .backward import sas_attention_backward, gate_backward, selector_backward
 from .variants import (log_gates, select_variant, variant_attention, variant_attention_backward,
                        gate_backward_act)
 from .stats import mass_coverage, block_mass_topk, majority_vote, selection_sets, overlap_recall
 from .varlen import doc_spans, select_packed, attention_packed, backward_packed, coverage_packed
-from .layer import (Spec, layer_forward, mlp_forward, attention_prefill,
+from .layer import (Spec, layer_forward, mlp_forward, attention_prefill, dense_prefill_layer,
                     DecodeCache, decode_step, decode_select, embed_tokens, lm_head_argmax)
 
 __all__ = [
     "rho", "round_bf16", "round_f32", "rmsnorm", "rope", "silu",
     "block_summaries", "gate_query", "selector_scores", "normalized_log_gate",
-    "topk_blocks", "select", "sas_attention", "Spec", "layer_forward",
+    "topk_blocks", "select", "sas_attention", "causal_attention", "Spec", "layer_forward",
+    "dense_prefill_layer",
     "mlp_forward", "attention_prefill", "DecodeCache", "decode_step",
     "decode_select", "embed_tokens", "lm_head_argmax",
     "sas_attention_backward", "gate_backward", "selector_backward",

@@ -70,3 +70,33 @@ def sas_attention(Q, K, V, B, mode, dtype, sel=None, log_gate=None,
             O[ri, g * G:(g + 1) * G, :] = (e @ V[idx, g, :]) / l
             LSE[g * G:(g + 1) * G, ri] = (zmax + np.log(l))[:, 0]
     return rho(O, dtype), O, LSE
+
+
+def causal_attention(Q, K, V, dtype, sm_scale=None):
+    """Standard causal softmax attention (Eq. fula with the causal mask) of
+    one sequence, written as masked score matrices: for query head h (KV
+    head h // G), Z = sm * Q_h K_g^T with Z[t, i] = -inf for i > t,
+    P = softmax over each row, O = P V_g, LSE = log sum_i exp(Z[t, i]).
+    Q[n, H, dh], K/V[n, Hkv, dh] -> O[n, H, dh] (rounded), O_exact (fp64),
+    LSE[H, n].  This is the DENSE mode of ``sas_attention`` for every row at
+    once (the serving prefill of Sec. 5.1 attends densely)."""
+    Q = np.asarray(Q, dtype=np.float64)
+    K = np.asarray(K, dtype=np.float64)
+    V = np.asarray(V, dtype=np.float64)
+    n, H, dh = Q.shape
+    Hkv = K.shape[1]
+    G = H // Hkv
+    sm = (1.0 / math.sqrt(dh)) if (sm_scale is None or sm_scale <= 0) else float(sm_scale)
+    future = np.triu(np.ones((n, n), dtype=bool), k=1)        # key i after query t
+    O = np.zeros((n, H, dh))
+    LSE = np.zeros((H, n))
+    for h in range(H):
+        g = h // G
+        Z = sm * (Q[:, h, :] @ K[:, g, :].T)
+        Z[future] = -np.inf
+        zmax = Z.max(axis=1, keepdims=True)
+        E = np.exp(Z - zmax)
+        L = E.sum(axis=1, keepdims=True)
+        O[:, h, :] = (E @ V[:, g, :]) / L
+        LSE[h] = (zmax + np.log(L))[:, 0]
+    return rho(O, dtype), O, LSE

@@ -18,7 +18,7 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from .attention import sas_attention
+from .attention import causal_attention, sas_attention
 from .numerics import rho, rmsnorm, rope, silu
 from .selector import (block_summaries, gate_query, project_summaries,
                        select, selector_scores, topk_blocks)
@@ -115,6 +115,22 @@ def layer_forward(x, W, spec, rows=None):
     return out
 
 
+def dense_prefill_layer(x, W, spec):
+    """One decoder layer of the serving prefill (Sec. 5.1: the prompt is
+    attended densely) over one sequence x[n, d], every row: u1, Q/K/V with
+    RoPE, causal attention, h1, MLP.  Returns y[n, d] and what the KV cache
+    holds for the decode steps that follow: K, V [n, Hkv, dh] and the block
+    summaries k_summary [Hkv, n // B, dh] (after W_gk when given)."""
+    x = _f64(x)
+    n, d = x.shape
+    Q, K, V = qkv_projection(x[None], W, spec, np.arange(n))
+    O, O_exact, _ = causal_attention(Q[0], K[0], V[0], spec.dtype, spec.sm_scale)
+    h1 = rho(x + O.reshape(n, spec.n_heads * spec.head_dim) @ _f64(W["wo"]).T, spec.dtype)
+    y = mlp_forward(h1, W, spec)
+    kbar = project_summaries(block_summaries(K[0], spec.block_size, spec.dtype), _f64(W.get("w_gk")), spec.dtype)
+    return {"y": y, "h1": h1, "O": O, "O_exact": O_exact, "K": K[0], "V": V[0], "k_summary": kbar}
+
+
 class DecodeCache:
     """Logical KV cache of one layer for a batch of sequences: K/V at every
     position written so far and the selector's summary of every complete
@@ -136,18 +152,20 @@ class DecodeCache:
         self.length[bi] = n
 
 
-def decode_step(x, pos, W, cache, spec):
+def decode_step(x, pos, W, cache, spec, taps=False):
     """One SAS inference step (Alg. 2) of one layer for a batch.
     x[b, d] (activation dtype), pos[b] = position of each new token.
     Appends K/V at pos, completes the block summary when pos + 1 is a
     multiple of B, selects the Top-K historical blocks per KV group against
     the cached summaries and attends to them plus the current block without
-    gate bias.  Returns y[b, d] and sel[b, Hkv, K]."""
+    gate bias.  Returns y[b, d] and sel[b, Hkv, K] (and, with taps, the
+    post-RoPE query heads q[b, H, dh])."""
     x = _f64(x)
     b, d = x.shape
     H, Hkv, dh, B, Kb = spec.n_heads, spec.n_kv_heads, spec.head_dim, spec.block_size, spec.top_k
     G = spec.group
     y = np.zeros((b, d))
+    q_all = np.zeros((b, H, dh))
     sel_all = np.full((b, Hkv, max(Kb, 0)), -1, dtype=np.int64)
     for bi in range(b):
         t = int(pos[bi])
@@ -156,6 +174,7 @@ def decode_step(x, pos, W, cache, spec):
         q = rho(rope((u1 @ _f64(W["wq"]).T).reshape(1, H, dh), p, spec.rope_base), spec.dtype)
         k = rho(rope((u1 @ _f64(W["wk"]).T).reshape(1, Hkv, dh), p, spec.rope_base), spec.dtype)
         v = rho((u1 @ _f64(W["wv"]).T).reshape(1, Hkv, dh), spec.dtype)
+        q_all[bi] = q[0]
         cache.K[bi, t] = k[0]
         cache.V[bi, t] = v[0]
         cache.length[bi] = t + 1
@@ -176,7 +195,7 @@ def decode_step(x, pos, W, cache, spec):
                                 sm_scale=spec.sm_scale)
         h1 = rho(x[bi] + O.reshape(H * dh) @ _f64(W["wo"]).T, spec.dtype)
         y[bi] = mlp_forward(h1[None], W, spec)[0]
-    return y, sel_all
+    return (y, sel_all, q_all) if taps else (y, sel_all)
 
 
 def decode_select(q, pos, kbar, spec, w_gq=None):

@@ -235,16 +235,19 @@ sas_status run_attention(const sas_config* c, int b, int n, const void* q, const
                          const int32_t* doc = nullptr) {
   const int NB = cdiv(n, c->block_size);
   const int H = c->n_heads, Hkv = c->n_kv_heads, dh = c->head_dim;
-  const bool need_sel = c->mode != SAS_MODE_DENSE || sel_idx || log_gate || tau || k_summary || need_summary;
+  // DENSE attention reads no selection: score and select only when a selector output is asked for;
+  // the block summaries alone are needed when the caller or the KV cache wants them
+  const bool need_sel = c->mode != SAS_MODE_DENSE || sel_idx || log_gate || tau;
+  const bool need_ksum = need_sel || k_summary || need_summary;
   if (full_fwd(c) && !log_gate) log_gate = ws.gate_table;
   void* ksum = k_summary ? k_summary : ws.ksum;
   int32_t* sel = sel_idx ? sel_idx : ws.sel;
+  if (need_ksum) {
+    Timed tm("summaries", s);
+    HIP_TRY(launch_block_summaries(c->dtype, k, b, n, Hkv, dh, c->block_size, w_gk, ws.kplain, ksum, s),
+            "block summaries");
+  }
   if (need_sel) {
-    {
-      Timed tm("summaries", s);
-      HIP_TRY(launch_block_summaries(c->dtype, k, b, n, Hkv, dh, c->block_size, w_gk, ws.kplain, ksum, s),
-              "block summaries");
-    }
     if (w_gq) {  // projected gate queries are computed first; otherwise the select kernel sums the heads
       Timed tm("gate_query", s);
       HIP_TRY(launch_gate_query(c->dtype, q, b, n, H, Hkv, dh, w_gq, ws.qplain, ws.qhat, s), "gate query");
@@ -595,6 +598,18 @@ sas_status check_ws(void* ws, size_t ws_bytes, size_t need) {
 }
 
 }  // namespace
+
+namespace sas {
+int set_error(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return status;
+}
+}  // namespace sas
 
 extern "C" {
 
@@ -1076,8 +1091,8 @@ sas_status sas_layer_forward(const sas_config* c, int32_t batch, int32_t seq_len
 }
 
 sas_status sas_decode_step(const sas_config* c, int32_t batch, const void* x, const int32_t* pos,
-                           const sas_layer_weights* w, sas_paged_kv* cache, void* y, int32_t* sel_idx, void* ws,
-                           size_t ws_bytes, void* stream) {
+                           const sas_layer_weights* w, sas_paged_kv* cache, void* y, int32_t* sel_idx,
+                           sas_layer_taps* taps, void* ws, size_t ws_bytes, void* stream) {
   SAS_TRY(check_config(c, true));
   if (batch <= 0) return fail(SAS_ERR_INVALID_ARGUMENT, "batch %d must be positive", batch);
   SAS_TRY(check_ptr(x, "x", true));
@@ -1087,9 +1102,22 @@ sas_status sas_decode_step(const sas_config* c, int32_t batch, const void* x, co
   SAS_TRY(check_weights(w, true, true));
   if (!cache) return fail(SAS_ERR_INVALID_ARGUMENT, "cache is NULL");
   SAS_TRY(check_cache(c, cache));
+  sas_layer_taps tp = {};
+  if (taps) {
+    tp = *taps;
+    SAS_TRY(check_ptr(tp.q, "taps.q", false));
+    SAS_TRY(check_ptr(tp.k, "taps.k", false));
+    SAS_TRY(check_ptr(tp.v, "taps.v", false));
+    SAS_TRY(check_ptr(tp.h1, "taps.h1", false));
+  }
   Carve cv(ws);
   DecodeWs dw = carve_decode(cv, c, batch, cache->max_blocks);
   SAS_TRY(check_ws(ws, ws_bytes, cv.off));
+  // the taps, when given, take the place of the step's own scratch rows
+  if (tp.q) dw.q = tp.q;
+  if (tp.k) dw.k = tp.k;
+  if (tp.v) dw.v = tp.v;
+  if (tp.h1) dw.h1 = tp.h1;
   hipStream_t s = (hipStream_t)stream;
   const DecodeArgs da = decode_args(c, batch, pos, cache, w);
   const int H = c->n_heads, Hkv = c->n_kv_heads, dh = c->head_dim;

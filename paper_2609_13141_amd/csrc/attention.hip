@@ -468,8 +468,8 @@ __global__ void attn_f32_kernel(AttnArgs P) {
     for (int i = beta * B; i <= t; ++i) visit(i, 0.f, 1.f);
   } else {
     for (int k = 0; k < P.K; ++k) {
-      int m = P.sel[row * P.K + k];
-      if (m < 0) break;
+      const int m = P.sel[row * P.K + k];
+      if (m < 0 || m >= beta) break;  // slots are ascending historical blocks, -1 padded
       float w = 1.f, bias = 0.f;
       if (gated) bias = gate(P.sel_bias[row * P.K + k], w);
       for (int i = m * B; i < (m + 1) * B; ++i) visit(i, bias, w);

@@ -298,7 +298,7 @@ gemm_bf16_kernel(GemmParams P) {
   gemm_epilogue<TM, TN, FM, FN>(P, acc, m0, n0, wm, wn, lr, lk);
 }
 
-// ---- direct-to-LDS pipelined variant (K % BKT == 0) ---------------------
+// ---- direct-to-LDS loading (shared by the kernel below) --------------------
 // Global tiles are copied straight into LDS with global_load_lds_dwordx4
 // (each lane writes 16 bytes at M0 + 16*lane), so no VGPRs stage them.  The
 // XOR swizzle of the 16-byte chunks is applied by choosing which global chunk
@@ -322,312 +322,6 @@ __device__ __forceinline__ void wait_vmcnt() {
 // drain vmcnt to zero, i.e. wait for every stage in flight.
 __device__ __forceinline__ void barrier_lds() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
-// LDS fragment reads that the compiler does not track, with explicit waits.
-// Its own waitcnt placement merges the state of loop-carried reads
-// pessimistically and would wait for every read in flight (lgkmcnt(0)) at
-// each step, so reads issued several MFMA steps ahead could not overlap.
-// lds_wait<N> waits until at most N of this wave's LDS reads are pending and
-// is tied to the fragments it releases, so their uses depend on it.
-__device__ __forceinline__ void lds_read_b128(bf16x8_t& d, uint32_t addr) {
-  asm volatile("ds_read_b128 %0, %1" : "=v"(d) : "v"(addr));
-}
-template <int N>
-__device__ __forceinline__ void lds_wait(bf16x8_t& x) {
-  asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(x) : "n"(N));
-}
-__device__ __forceinline__ void lds_tie(bf16x8_t& x) { asm volatile("" : "+v"(x)); }
-
-template <int EPI, int BM, int BN, int WM, int WN, int BKT, int STAGES, bool DB = false>
-__global__ void __launch_bounds__(WM * WN * 64)
-gemm_bf16_pipe_kernel(GemmParams P) {
-  constexpr int NW = WM * WN;
-  constexpr int TM = BM / WM, TN = BN / WN;
-  constexpr int FM = TM / 32, FN = TN / 32;
-  constexpr int CPR = BKT / 8;               // 16-byte chunks per row
-  constexpr int RPG = 16 / CPR;              // rows per 256-byte bank sweep
-  constexpr int AI = BM * CPR / (64 * NW);   // load instructions per wave per stage (A)
-  constexpr int BI = BN * CPR / (64 * NW);
-  static_assert(AI * 64 * NW == BM * CPR && BI * 64 * NW == BN * CPR, "tile/threads mismatch");
-  static_assert(EPI == EPI_RESID || TN % 64 == 0, "pair epilogues need 64-column wave tiles");
-  static_assert((STAGES - 2) * (AI + BI) <= 63, "vmcnt range");
-  constexpr int STAGE = (BM + BN) * BKT;  // elements per stage
-
-  extern __shared__ __align__(16) unsigned char smem[];
-  bf16_t* S = (bf16_t*)smem;
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-  const int Mt = (P.M + BM - 1) / BM, Nt = (P.N + BN - 1) / BN;
-  int mt, nt;
-  tile_of(blockIdx.x, Mt, Nt, P.group_m, mt, nt);
-  const int m0 = mt * BM, n0 = nt * BN;
-
-  // element offsets of this lane's chunks from the operand base (32-bit: the
-  // operands hold fewer than 2^31 elements); B rows may come from three
-  // matrices, so their base pointer is kept per chunk
-  uint32_t a_off[AI];
-  const bf16_t* b_src[BI];
-#pragma unroll
-  for (int j = 0; j < AI; ++j) {
-    const int c = (wave * AI + j) * 64 + lane;
-    const int r = c / CPR, cc = (c % CPR) ^ ((r / RPG) % CPR);
-    const int gr = min(m0 + r, P.M - 1);
-    a_off[j] = (uint32_t)gr * (uint32_t)P.K + cc * 8;
-  }
-#pragma unroll
-  for (int j = 0; j < BI; ++j) {
-    const int c = (wave * BI + j) * 64 + lane;
-    const int r = c / CPR, cc = (c % CPR) ^ ((r / RPG) % CPR);
-    const bf16_t* row = b_row<bf16_t>(P.epi, n0 + r, P.N, P.npairs, P.K, P.B0, P.B1, P.B2, P.H, P.Hkv, P.dh);
-    b_src[j] = (row ? row : P.B0) + cc * 8;
-  }
-
-  auto issue = [&](int kt) {
-    const int k0 = kt * BKT;
-    bf16_t* st = S + (kt % STAGES) * STAGE;
-#pragma unroll
-    for (int j = 0; j < AI; ++j)
-      __builtin_amdgcn_global_load_lds((const void*)(P.A + a_off[j] + k0),
-                                       (lds_void_t*)(st + (wave * AI + j) * 64 * 8), 16, 0, 0);
-#pragma unroll
-    for (int j = 0; j < BI; ++j)
-      __builtin_amdgcn_global_load_lds((const void*)(b_src[j] + k0),
-                                       (lds_void_t*)(st + BM * BKT + (wave * BI + j) * 64 * 8), 16, 0, 0);
-  };
-
-  floatx16_t acc[FM][FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-
-  const int lr = lane & 31, lk = lane >> 5;
-  int aoff[FM], boff[FN];  // element offset of this lane's fragment row
-#pragma unroll
-  for (int i = 0; i < FM; ++i) aoff[i] = (wm * TM + i * 32 + lr) * BKT;
-#pragma unroll
-  for (int j = 0; j < FN; ++j) boff[j] = BM * BKT + (wn * TN + j * 32 + lr) * BKT;
-  const int sw = (lr / RPG) % CPR;  // fragment row bases are multiples of 32
-
-  const int nk = P.K / BKT;
-#pragma unroll
-  for (int t = 0; t < STAGES - 1; ++t)
-    if (t < nk) issue(t);
-  for (int kt = 0; kt < nk; ++kt) {
-    // tile kt has landed once at most (tiles issued after it) * (AI + BI) loads remain
-    if (kt + STAGES - 2 < nk) wait_vmcnt<(STAGES - 2) * (AI + BI)>();
-    else wait_vmcnt<0>();
-    barrier_lds();
-    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
-    const bf16_t* st = S + (kt % STAGES) * STAGE;
-    if constexpr (!DB) {
-#pragma unroll
-      for (int kk = 0; kk < BKT / 16; ++kk) {
-        const int kc = kk * 2 + lk;
-        bf16x8_t fa[FM], fb[FN];
-#pragma unroll
-        for (int i = 0; i < FM; ++i) fa[i] = *(const bf16x8_t*)(st + aoff[i] + ((kc ^ sw) << 3));
-#pragma unroll
-        for (int j = 0; j < FN; ++j) fb[j] = *(const bf16x8_t*)(st + boff[j] + ((kc ^ sw) << 3));
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-          for (int j = 0; j < FN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-      }
-    } else {
-      // The fragments of step kk+1 are read while the MFMAs of step kk run.
-      // sched_barrier(0) after every MFMA keeps this order: the compiler would
-      // otherwise chain MFMAs on one accumulator and wait on each read at once.
-      bf16x8_t fa[2][FM], fb[2][FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i) fa[0][i] = *(const bf16x8_t*)(st + aoff[i] + ((lk ^ sw) << 3));
-#pragma unroll
-      for (int j = 0; j < FN; ++j) fb[0][j] = *(const bf16x8_t*)(st + boff[j] + ((lk ^ sw) << 3));
-#pragma unroll
-      for (int kk = 0; kk < BKT / 16; ++kk) {
-        const int cur = kk & 1, nxt = cur ^ 1;
-        const bool more = kk + 1 < BKT / 16;
-        const int kc = ((kk + 1) * 2 + lk) ^ sw;
-        // read g of step kk+1, in its use order: fa[0], fb[0..FN-1], fa[1..FM-1]
-        auto read_next = [&](int g) {
-          if (g == 0) fa[nxt][0] = *(const bf16x8_t*)(st + aoff[0] + (kc << 3));
-          else if (g <= FN) fb[nxt][g - 1] = *(const bf16x8_t*)(st + boff[g - 1] + (kc << 3));
-          else fa[nxt][g - FN] = *(const bf16x8_t*)(st + aoff[g - FN] + (kc << 3));
-        };
-        int g = 0;
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-          for (int j = 0; j < FN; ++j) {
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j], 0, 0, 0);
-            if (more && g < FM + FN) read_next(g);
-            ++g;
-            __builtin_amdgcn_sched_barrier(0);
-          }
-        // small wave tiles have fewer MFMAs (FM*FN) than reads (FM+FN)
-#pragma unroll
-        for (; g < FM + FN; ++g)
-          if (more) read_next(g);
-      }
-    }
-  }
-  gemm_epilogue_t<EPI, TM, TN, FM, FN>(P, acc, m0, n0, wm, wn, lr, lk);
-}
-
-// ---- register-staged, software-pipelined variant (K % 64 == 0) -----------
-// Same LDS layout and swizzle as above; the operand tiles travel through
-// registers (global -> VGPR -> ds_write) instead of direct-to-LDS loads, and
-// the waits are kept off the MFMA stream:
-//  * fragments are read PD 16-deep steps ahead into a ring of register sets;
-//  * k-tile kt+1 is written to the LDS buffer k-tile kt-1 used, one step
-//    before the barrier that publishes it (inside tile kt, after the first
-//    MFMAs of step 4 - PD), and k-tile kt+2 is fetched into the registers
-//    that write freed, so each fetch has about one k-tile of MFMAs to land;
-//  * after the barrier the reads of tile kt+1's first steps are issued while
-//    tile kt's last MFMAs run.
-template <int EPI, int BM, int BN, int WM, int WN, int PD>
-__global__ void __launch_bounds__(WM * WN * 64)
-gemm_bf16_reg_kernel(GemmParams P) {
-  constexpr int BKT = 64, KK = BKT / 16, STAGES = 2;
-  constexpr int NW = WM * WN;
-  constexpr int TM = BM / WM, TN = BN / WN;
-  constexpr int FM = TM / 32, FN = TN / 32, NF = FM + FN;
-  constexpr int CPR = BKT / 8, RPG = 16 / CPR;
-  constexpr int AI = BM * CPR / (64 * NW);
-  constexpr int BI = BN * CPR / (64 * NW);
-  constexpr int R = PD == 1 ? 2 : 4;  // fragment sets: a divisor of KK, so step kk uses set kk % R
-  static_assert(PD == 1 || PD == 2, "prefetch distance");
-  static_assert(AI * 64 * NW == BM * CPR && BI * 64 * NW == BN * CPR, "tile/threads mismatch");
-  static_assert(EPI == EPI_RESID || TN % 64 == 0, "pair epilogues need 64-column wave tiles");
-  static_assert((PD - 1) * NF <= 15, "lgkmcnt range");
-  constexpr int STAGE = (BM + BN) * BKT;
-  constexpr int BAR_AT = FM * FN >= 2 ? 1 : 0;  // MFMA after which a step's LDS traffic is issued
-
-  extern __shared__ __align__(16) unsigned char smem[];
-  bf16_t* S = (bf16_t*)smem;
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-  const int Mt = (P.M + BM - 1) / BM, Nt = (P.N + BN - 1) / BN;
-  int mt, nt;
-  tile_of(blockIdx.x, Mt, Nt, P.group_m, mt, nt);
-  const int m0 = mt * BM, n0 = nt * BN;
-
-  uint32_t a_off[AI];
-  const bf16_t* b_src[BI];
-#pragma unroll
-  for (int j = 0; j < AI; ++j) {
-    const int c = (wave * AI + j) * 64 + lane;
-    const int r = c / CPR, cc = (c % CPR) ^ ((r / RPG) % CPR);
-    const int gr = min(m0 + r, P.M - 1);
-    a_off[j] = (uint32_t)gr * (uint32_t)P.K + cc * 8;
-  }
-#pragma unroll
-  for (int j = 0; j < BI; ++j) {
-    const int c = (wave * BI + j) * 64 + lane;
-    const int r = c / CPR, cc = (c % CPR) ^ ((r / RPG) % CPR);
-    const bf16_t* row = b_row<bf16_t>(P.epi, n0 + r, P.N, P.npairs, P.K, P.B0, P.B1, P.B2, P.H, P.Hkv, P.dh);
-    b_src[j] = (row ? row : P.B0) + cc * 8;
-  }
-  bf16x8_t ra[AI], rb[BI];
-  auto fetch = [&](int kt) {
-    const int k0 = kt * BKT;
-#pragma unroll
-    for (int j = 0; j < AI; ++j) ra[j] = *(const bf16x8_t*)(P.A + a_off[j] + k0);
-#pragma unroll
-    for (int j = 0; j < BI; ++j) rb[j] = *(const bf16x8_t*)(b_src[j] + k0);
-  };
-  auto commit = [&](int kt) {
-    bf16_t* st = S + (kt % STAGES) * STAGE;
-#pragma unroll
-    for (int j = 0; j < AI; ++j) *(bf16x8_t*)(st + ((wave * AI + j) * 64 + lane) * 8) = ra[j];
-#pragma unroll
-    for (int j = 0; j < BI; ++j) *(bf16x8_t*)(st + BM * BKT + ((wave * BI + j) * 64 + lane) * 8) = rb[j];
-  };
-
-  floatx16_t acc[FM][FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-
-  const int lr = lane & 31, lk = lane >> 5;
-  // fragment g of a set, in use order: A0, B0..B(FN-1), A1..A(FM-1)
-  int foff[NF];
-#pragma unroll
-  for (int g = 0; g < NF; ++g) {
-    if (g == 0) foff[g] = (wm * TM + lr) * BKT;
-    else if (g <= FN) foff[g] = BM * BKT + (wn * TN + (g - 1) * 32 + lr) * BKT;
-    else foff[g] = (wm * TM + (g - FN) * 32 + lr) * BKT;
-  }
-  const int sw = (lr / RPG) % CPR;
-  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16_t*)S;
-  bf16x8_t fr[R][NF];
-  auto read = [&](const bf16_t* st, int kk, int set) {
-    const int kc = ((kk * 2 + lk) ^ sw) << 3;
-    const uint32_t base = lds0 + (uint32_t)(st - S + kc) * 2u;
-#pragma unroll
-    for (int g = 0; g < NF; ++g) lds_read_b128(fr[set][g], base + foff[g] * 2u);
-  };
-  // release fragment set `set`; `later`: the reads of the next step were issued after it
-  auto wait_set = [&](int set, bool later) {
-    if (later) lds_wait<(PD - 1) * NF>(fr[set][0]);
-    else lds_wait<0>(fr[set][0]);
-#pragma unroll
-    for (int g = 1; g < NF; ++g) lds_tie(fr[set][g]);
-  };
-
-  const int nk = P.K / BKT;
-  fetch(0);
-  commit(0);
-  if (nk > 1) fetch(1);
-  barrier_lds();
-#pragma unroll
-  for (int p = 0; p < PD; ++p) read(S, p, p % R);
-
-  for (int kt = 0; kt < nk; ++kt) {
-    const bf16_t* st = S + (kt % STAGES) * STAGE;
-    const bf16_t* sn = S + ((kt + 1) % STAGES) * STAGE;
-    const bool has_next = kt + 1 < nk;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      const int cur = kk % R;
-      const int tk = kk + PD;  // step whose fragments are read during this one
-      // the reads of step kk+1 (PD = 2) were issued after set cur's iff that step exists;
-      // LDS writes issued in between only make the wait stricter
-      wait_set(cur, PD > 1 && (kk + 1 < KK || has_next));
-      int m = 0;
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[cur][i == 0 ? 0 : FN + i], fr[cur][1 + j],
-                                                              acc[i][j], 0, 0, 0);
-          __builtin_amdgcn_sched_barrier(0);
-          if (m == BAR_AT) {
-            if (kk == KK - PD - 1 && has_next) {
-              commit(kt + 1);
-              if (kt + 2 < nk) fetch(kt + 2);
-            }
-            if (kk == KK - PD && has_next) barrier_lds();
-            if (tk < KK) read(st, tk, tk % R);
-            else if (has_next) read(sn, tk - KK, tk % R);
-            __builtin_amdgcn_sched_barrier(0);
-          }
-          ++m;
-        }
-    }
-  }
-  gemm_epilogue_t<EPI, TM, TN, FM, FN>(P, acc, m0, n0, wm, wn, lr, lk);
 }
 
 
@@ -812,7 +506,7 @@ gemm_bf16_lds_kernel(GemmParams P) {
   constexpr int NW = WM * WN;
   constexpr int TM = BM / WM, TN = BN / WN;
   constexpr int FM = TM / 32, FN = TN / 32, NF = FM + FN, NMF = FM * FN;
-  constexpr int CPR = BKT / 8, RPG = 16 / CPR;  // swizzle as in gemm_bf16_pipe_kernel
+  constexpr int CPR = BKT / 8, RPG = 16 / CPR;  // the chunk swizzle described above
   constexpr int AI = BM * CPR / (64 * NW);
   constexpr int BI = BN * CPR / (64 * NW);
   constexpr int LI = AI + BI;
@@ -1000,52 +694,6 @@ static hipError_t run_bf16(const GemmParams& P, hipStream_t s) {
   hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN>), dim3(tiles), dim3(NT), lds, s, P);
   return hipGetLastError();
 }
-
-template <int EPI, int BM, int BN, int WM, int WN, int BKT, int STAGES, bool DB>
-static hipError_t run_pipe_t(const GemmParams& P, hipStream_t s) {
-  constexpr int NT = WM * WN * 64;
-  const int tiles = ((P.M + BM - 1) / BM) * ((P.N + BN - 1) / BN);
-  const size_t lds = (size_t)STAGES * (BM + BN) * BKT * sizeof(bf16_t);
-  static bool attr = false;
-  if (!attr) {
-    (void)hipFuncSetAttribute((const void*)gemm_bf16_pipe_kernel<EPI, BM, BN, WM, WN, BKT, STAGES, DB>,
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    attr = true;
-  }
-  hipLaunchKernelGGL((gemm_bf16_pipe_kernel<EPI, BM, BN, WM, WN, BKT, STAGES, DB>), dim3(tiles), dim3(NT), lds,
-                     s, P);
-  return hipGetLastError();
-}
-
-template <int EPI, int BM, int BN, int WM, int WN, int PD>
-static hipError_t run_reg_t(const GemmParams& P, hipStream_t s) {
-  constexpr int NT = WM * WN * 64;
-  const int tiles = ((P.M + BM - 1) / BM) * ((P.N + BN - 1) / BN);
-  const size_t lds = (size_t)2 * (BM + BN) * 64 * sizeof(bf16_t);
-  static bool attr = false;
-  if (!attr) {
-    (void)hipFuncSetAttribute((const void*)gemm_bf16_reg_kernel<EPI, BM, BN, WM, WN, PD>,
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    attr = true;
-  }
-  hipLaunchKernelGGL((gemm_bf16_reg_kernel<EPI, BM, BN, WM, WN, PD>), dim3(tiles), dim3(NT), lds, s, P);
-  return hipGetLastError();
-}
-
-template <int BM, int BN, int WM, int WN, int PD>
-static hipError_t run_reg(const GemmParams& P, hipStream_t s) {
-  if (P.epi == EPI_RESID) return run_reg_t<EPI_RESID, BM, BN, WM, WN, PD>(P, s);
-  if (P.epi == EPI_SWIGLU) return run_reg_t<EPI_SWIGLU, BM, BN, WM, WN, PD>(P, s);
-  return run_reg_t<EPI_QKV_ROPE, BM, BN, WM, WN, PD>(P, s);
-}
-
-template <int BM, int BN, int WM, int WN, int BKT, int STAGES, bool DB = false>
-static hipError_t run_pipe(const GemmParams& P, hipStream_t s) {
-  if (P.epi == EPI_RESID) return run_pipe_t<EPI_RESID, BM, BN, WM, WN, BKT, STAGES, DB>(P, s);
-  if (P.epi == EPI_SWIGLU) return run_pipe_t<EPI_SWIGLU, BM, BN, WM, WN, BKT, STAGES, DB>(P, s);
-  return run_pipe_t<EPI_QKV_ROPE, BM, BN, WM, WN, BKT, STAGES, DB>(P, s);
-}
-
 
 template <int EPI, int BM, int BN, int WM, int WN, int STAGES>
 static hipError_t run_lds_t(const GemmParams& P, hipStream_t s) {

@@ -10,6 +10,10 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 inline size_t cdiv(size_t a, int b) { return (a + (size_t)b - 1) / (size_t)b; }
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Records the thread's last-error message (returned by sas_last_error) and
+// returns `status`; defined with the C ABI's entry points.
+int set_error(int status, const char* fmt, ...);
+
 // ---- elementwise.hip -------------------------------------------------------
 // out[r, :] = x[r, :] / sqrt(mean(x[r, :]^2) + eps) * gamma   (fp32 math)
 hipError_t launch_rmsnorm(int dtype, const void* x, const void* gamma, void* out, int rows, int d,

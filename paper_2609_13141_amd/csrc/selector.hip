@@ -222,20 +222,30 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
   }
   __syncthreads();
 
+  constexpr int EMPTY = 0x7fffffff;  // block id of an empty slot
   double tr[KMAX];
   int tm[KMAX];
 #pragma unroll
   for (int i = 0; i < KMAX; ++i) {
     tr[i] = -DBL_MAX;
-    tm[i] = 0x7fffffff;
+    tm[i] = EMPTY;
   }
   double mrun = -DBL_MAX;  // running max of s
   float lrun = 0.f;        // running sum of exp(s - mrun)
+  // does key a rank strictly ahead of the slot (b, bm)?  Every key beats an
+  // empty slot (so -inf keys are kept when fewer than K others exist), NaN
+  // ranks below every number, and an equal key keeps the earlier (lower)
+  // block ahead
+  auto beats = [](double a, double b, int bm) -> bool {
+    if (bm == EMPTY) return true;
+    if (a != a) return false;
+    return a > b || b != b;
+  };
   auto insert = [&](double cr, int cm) {
-    if (!(cr > tr[KMAX - 1])) return;
+    if (cm == EMPTY || !beats(cr, tr[KMAX - 1], tm[KMAX - 1])) return;
 #pragma unroll
     for (int i = 0; i < KMAX; ++i) {
-      const bool better = cr > tr[i];  // strict: an equal key keeps the earlier (lower) block ahead
+      const bool better = beats(cr, tr[i], tm[i]);
       const double orr = tr[i];
       const int om = tm[i];
       tr[i] = better ? cr : orr;
@@ -360,7 +370,7 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
   // order the kept blocks by index (odd-even transposition; empty slots last)
 #pragma unroll
   for (int i = 0; i < KMAX; ++i)
-    if (i >= kk) tm[i] = 0x7fffffff;
+    if (i >= kk) tm[i] = EMPTY;
 #pragma unroll
   for (int pass = 0; pass < KMAX; ++pass) {
 #pragma unroll
@@ -379,8 +389,9 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
 #pragma unroll
   for (int i = 0; i < KMAX; ++i) {
     if (i < K) {
-      sel[i] = (i < kk) ? tm[i] : -1;
-      sb[i] = (i < kk) ? (float)log_gate_of(tr[i]) : 0.f;
+      const bool kept = i < kk && tm[i] != EMPTY;
+      sel[i] = kept ? tm[i] : -1;
+      sb[i] = kept ? (float)log_gate_of(tr[i]) : 0.f;
     }
   }
 

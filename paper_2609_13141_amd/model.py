@@ -50,19 +50,25 @@ class Stack:
         b = self.w.batch
         return [torch.full((b,), self.pos + s, dtype=torch.int32, device=self.device) for s in range(steps)]
 
-    def step(self, tok, pos, *, logits: bool = False, sel_idx: bool = False):
+    def step(self, tok, pos, *, logits: bool = False, sel_idx: bool = False, taps: bool = False):
         """One generated token per sequence: tok [b] at positions pos [b]
-        (device int32).  Returns the next tokens (and logits / per-layer
-        selections when asked)."""
+        (device int32).  Returns the next tokens, the logits and per-layer
+        selections when asked, and with taps a per-layer list of
+        {"x": layer input, "q", "k", "v", "h1"}."""
         x = sas.embed(self.cfg_decode, tok.view(-1, 1), self.ends["embed"])[:, 0].contiguous()
-        sels = []
+        sels, tps = [], []
         for W, cache in zip(self.layers, self.caches):
-            x, sel = sas.decode_step(self.cfg_decode, x, pos, W, cache, sel_idx=sel_idx, ws=self.ws)
+            r = sas.decode_step(self.cfg_decode, x, pos, W, cache, sel_idx=sel_idx, taps=taps, ws=self.ws)
+            if taps:
+                r[2]["x"] = x
+                tps.append(r[2])
+            x, sel = r[0], r[1]
             sels.append(sel)
         nxt, lg = sas.lm_head_argmax(self.cfg_decode, x, self.ends["rms_final"], self.ends["w_lm"], logits=logits,
                                      ws=self.ws)
         self.pos += 1
-        return nxt, lg, (sels if sel_idx else None)
+        out = (nxt, lg, (sels if sel_idx else None))
+        return out + (tps,) if taps else out
 
     def generate(self, ids, img, steps: int):
         """Greedy generation: [b, steps + 1] tokens (the prefill's and `steps` more)."""

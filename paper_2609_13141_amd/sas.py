@@ -120,7 +120,7 @@ def lib() -> C.CDLL:
                                     C.POINTER(AttnOut), C.POINTER(LayerTaps), C.POINTER(PagedKV), vp, sz, vp]
     L.sas_decode_step.restype = i32
     L.sas_decode_step.argtypes = [C.POINTER(Config), i32, vp, vp, C.POINTER(LayerWeights), C.POINTER(PagedKV),
-                                  vp, vp, vp, sz, vp]
+                                  vp, vp, C.POINTER(LayerTaps), vp, sz, vp]
     L.sas_decode_select.restype = i32
     L.sas_decode_select.argtypes = [C.POINTER(Config), i32, vp, vp, vp, C.POINTER(PagedKV), vp, vp, sz, vp]
     L.sas_attention_backward.restype = i32
@@ -429,16 +429,27 @@ def alloc_cache(cfg: Config, batch: int, max_len: int, page_size: int = 16, devi
 
 
 def decode_step(cfg: Config, x, pos, W: dict, cache: PagedCache, *, sel_idx: bool = True,
-                ws: Workspace | None = None):
-    """One SAS decode step of one layer.  x [b, d]; pos [b] int32 (device)."""
+                taps: bool = False, ws: Workspace | None = None):
+    """One SAS decode step of one layer.  x [b, d]; pos [b] int32 (device).
+    Returns (y, sel) or, with taps, (y, sel, {"q", "k", "v", "h1"})."""
     b = x.shape[0]
+    H, Hkv, dh = cfg.n_heads, cfg.n_kv_heads, cfg.head_dim
     y = torch.empty_like(x)
-    sel = torch.empty(b, cfg.n_kv_heads, cfg.top_k, dtype=torch.int32, device=x.device) if sel_idx else None
+    sel = torch.empty(b, Hkv, cfg.top_k, dtype=torch.int32, device=x.device) if sel_idx else None
+    tap = None
+    tp = None
+    if taps:
+        tap = {"q": torch.empty(b, H, dh, dtype=x.dtype, device=x.device),
+               "k": torch.empty(b, Hkv, dh, dtype=x.dtype, device=x.device),
+               "v": torch.empty(b, Hkv, dh, dtype=x.dtype, device=x.device),
+               "h1": torch.empty_like(x)}
+        tp = LayerTaps(*[_ptr(tap[f]) for f in ("q", "k", "v", "h1")])
     cs = cache.struct()
     wsp, wsn = _ws(ws, workspace_size(cfg, OP_DECODE, b, cache.max_context(cfg)))
     _check(lib().sas_decode_step(C.byref(cfg), b, _ptr(x), _ptr(pos), C.byref(weights_struct(W)), C.byref(cs),
-                                 _ptr(y), _ptr(sel), wsp, wsn, _stream()))
-    return y, sel
+                                 _ptr(y), _ptr(sel), C.byref(tp) if tp is not None else None, wsp, wsn,
+                                 _stream()))
+    return (y, sel, tap) if taps else (y, sel)
 
 
 def decode_select(cfg: Config, q, pos, cache: PagedCache, w_gq=None, ws: Workspace | None = None):

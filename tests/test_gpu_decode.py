@@ -9,7 +9,8 @@ import torch
 import oracle
 from paper_2609_13141_amd import configs, inputs, sas
 
-from helpers import TOL, assert_close, f64, spec_of
+from oracle.selector import select
+from helpers import TOL, assert_close, cache_keys, check_decode_selection, f64, spec_of
 
 pytestmark = pytest.mark.gpu
 
@@ -60,49 +61,60 @@ def test_prefill_then_decode_matches_oracle(w, proj):
     pre = oracle.layer_forward(f64(x[:, :n0]), _oracle_W(Wl), spec_of(w, "dense"))
     for bi in range(w.batch):
         ocache.fill_prefill(bi, pre["K"][bi], pre["V"][bi], pre["k_summary"][bi])
-    agree = total = 0
+    Wo = _oracle_W(Wl)
+    nd = 0
     for t in range(n0, w.seq_len):
         pos = torch.full((w.batch,), t, dtype=torch.int32, device="cuda")
-        y, sel = sas.decode_step(cfg_d, xd[:, t].contiguous(), pos, Wd, cache)
+        y, sel, tp = sas.decode_step(cfg_d, xd[:, t].contiguous(), pos, Wd, cache, taps=True)
         torch.cuda.synchronize()
-        yo, selo = oracle.decode_step(f64(x[:, t]), np.full(w.batch, t), _oracle_W(Wl), ocache, sp)
+        yo, selo, qo = oracle.decode_step(f64(x[:, t]), np.full(w.batch, t), Wo, ocache, sp, taps=True)
         assert_close(y.float().cpu().numpy(), yo, dt, f"y at t={t}")
-        s = sel.cpu().numpy()
-        agree += int(np.all(s == selo, axis=-1).sum())
-        total += s.shape[0] * s.shape[1]
-    if dt == "f32":
-        assert agree == total
-    else:
-        assert agree / total >= 0.97, agree / total
+        nd += check_decode_selection(sel.cpu().numpy(), tp["q"], cache, t, sp, ocache, q_ref=qo,
+                                     w_gq=Wo.get("w_gq"), w_gk=Wo.get("w_gk"))
+    print(f"  {nd} rows differ from the oracle's own selection, each at a near-tie", flush=True)
 
 
 @pytest.mark.parametrize("w", [W_(dtype="f32", index=74), W_(index=75)], ids=["f32", "bf16"])
 def test_decode_equals_sparse_prefill_on_gpu(w):
     # Alg. 2 applied token by token (decode) equals Alg. 2 applied to every row
-    # (SPARSE prefill): identical selections where the inputs are identical
+    # (SPARSE prefill).  Each path's selection equals the oracle's selector on
+    # that path's own Q/K bits; where the two paths' Q/K bits agree (the query
+    # row and every cached key), their selections are identical.
     n0 = 40
     x = inputs.embeddings(w)
     Wl = inputs.layer_weights(w)
     dt = w.dtype
+    sp = spec_of(w, "sparse")
     Wd = sas.weights_to_device(Wl, dt)
     xd = sas.to_device(x, dt)
-    ref = sas.layer_forward(sas.make_config(w, "sparse"), xd, Wd)
+    ref = sas.layer_forward(sas.make_config(w, "sparse"), xd, Wd, taps=True)
+    torch.cuda.synchronize()
+    qp, kp = f64(ref["q"].float().cpu().numpy()), f64(ref["k"].float().cpu().numpy())
+    for bi in range(w.batch):
+        st = select(qp[bi], kp[bi], w.block_size, w.top_k, dt)
+        np.testing.assert_array_equal(ref["sel_idx"][bi].cpu().numpy(), st["sel"])
     cfg_d = sas.make_config(w, "sparse")
     cache = sas.alloc_cache(cfg_d, w.batch, w.seq_len, page_size=16, seed=3)
     sas.layer_forward(sas.make_config(w, "dense"), xd[:, :n0].contiguous(), Wd, stats=False, cache=cache)
-    same = total = 0
+    same_inputs = 0
     for t in range(n0, w.seq_len):
         pos = torch.full((w.batch,), t, dtype=torch.int32, device="cuda")
-        y, sel = sas.decode_step(cfg_d, xd[:, t].contiguous(), pos, Wd, cache)
+        y, sel, tp = sas.decode_step(cfg_d, xd[:, t].contiguous(), pos, Wd, cache, taps=True)
         torch.cuda.synchronize()
         assert_close(y.float().cpu().numpy(), ref["y"][:, t].float().cpu().numpy(), dt, f"y t={t}")
-        s, r = sel.cpu().numpy(), ref["sel_idx"][:, :, t].cpu().numpy()
-        same += int(np.all(s == r, axis=-1).sum())
-        total += s.shape[0] * s.shape[1]
+        s = sel.cpu().numpy()
+        check_decode_selection(s, tp["q"], cache, t, sp)
+        qd = f64(tp["q"].float().cpu().numpy())
+        ct = t // w.block_size
+        for bi in range(w.batch):
+            kc = cache_keys(cache, bi, ct * w.block_size)
+            if np.array_equal(qd[bi], qp[bi, t]) and np.array_equal(kc, kp[bi, :ct * w.block_size]):
+                same_inputs += 1
+                np.testing.assert_array_equal(s[bi], ref["sel_idx"][bi, :, t].cpu().numpy())
     if dt == "f32":
-        assert same == total       # the same kernels compute Q/K in both paths
-    else:
-        assert same / total >= 0.97
+        assert same_inputs > 0
+    print(f"  {same_inputs} of {w.batch * (w.seq_len - n0)} (sequence, step) pairs had identical Q/K bits "
+          f"in both paths", flush=True)
 
 
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
@@ -125,7 +137,7 @@ def test_decode_wide_blocks_match_oracle(dt, page):
     pre = oracle.layer_forward(f64(x[:, :n0]), _oracle_W(Wl), spec_of(w, "dense"))
     for bi in range(w.batch):
         ocache.fill_prefill(bi, pre["K"][bi], pre["V"][bi], pre["k_summary"][bi])
-    agree = total = 0
+    nd = 0
     for t in range(n0, w.seq_len, 5):
         if t > n0:  # teacher-forced positions in between, so the oracle cache stays aligned
             for tt in range(t - 4, t):
@@ -133,13 +145,12 @@ def test_decode_wide_blocks_match_oracle(dt, page):
                 sas.decode_step(cfg_d, xd[:, tt].contiguous(), pos, Wd, cache)
                 oracle.decode_step(f64(x[:, tt]), np.full(w.batch, tt), _oracle_W(Wl), ocache, sp)
         pos = torch.full((w.batch,), t, dtype=torch.int32, device="cuda")
-        y, sel = sas.decode_step(cfg_d, xd[:, t].contiguous(), pos, Wd, cache)
+        y, sel, tp = sas.decode_step(cfg_d, xd[:, t].contiguous(), pos, Wd, cache, taps=True)
         torch.cuda.synchronize()
-        yo, selo = oracle.decode_step(f64(x[:, t]), np.full(w.batch, t), _oracle_W(Wl), ocache, sp)
+        yo, selo, qo = oracle.decode_step(f64(x[:, t]), np.full(w.batch, t), _oracle_W(Wl), ocache, sp, taps=True)
         assert_close(y.float().cpu().numpy(), yo, dt, f"y at t={t}")
-        agree += int(np.all(sel.cpu().numpy() == selo, axis=-1).sum())
-        total += w.batch * w.n_kv_heads
-    assert agree / total >= (1.0 if dt == "f32" else 0.97), agree / total
+        nd += check_decode_selection(sel.cpu().numpy(), tp["q"], cache, t, sp, ocache, q_ref=qo)
+    print(f"  {nd} rows differ from the oracle's own selection, each at a near-tie", flush=True)
 
 
 def test_cache_holds_prefill_keys_values_and_summaries():

@@ -10,7 +10,7 @@ import torch
 import oracle
 from paper_2609_13141_amd import configs, inputs, sas
 
-from helpers import assert_close, f64, spec_of
+from helpers import assert_close, check_decode_selection, f64, spec_of
 
 pytestmark = pytest.mark.gpu
 
@@ -108,16 +108,16 @@ def test_decode_step_over_long_cache_matches_oracle(dtype):
         nb = p // w.block_size
         cache.k_summary[bi, :, :nb] = torch.from_numpy(kb[bi, :, :nb]).to(device="cuda", dtype=dt)
     x = inputs.normal(w, "x_step", (w.batch, w.d_model), 1.0)
-    y, sel = sas.decode_step(cfg, sas.to_device(x, dtype), torch.tensor(pos, dtype=torch.int32, device="cuda"),
-                             sas.weights_to_device(Wl, dtype), cache)
+    y, sel, tp = sas.decode_step(cfg, sas.to_device(x, dtype), torch.tensor(pos, dtype=torch.int32, device="cuda"),
+                                 sas.weights_to_device(Wl, dtype), cache, taps=True)
     torch.cuda.synchronize()
-    yo, selo = oracle.decode_step(f64(x), pos, {k: (None if a is None else f64(a)) for k, a in Wl.items()}, oc, sp)
+    yo, selo, qo = oracle.decode_step(f64(x), pos, {k: (None if a is None else f64(a)) for k, a in Wl.items()}, oc,
+                                      sp, taps=True)
     assert_close(y.float().cpu().numpy(), yo, dtype, "y")
-    same = np.all(sel.cpu().numpy() == selo, axis=-1)
-    if dtype == "f32":
-        assert same.all()
-    else:
-        assert same.mean() >= 0.5, same   # Q from GEMV rounding may swap near-tied blocks
+    # bit-exact on the step's own query heads; against the oracle's own ones only near-ties may differ
+    nd = check_decode_selection(sel.cpu().numpy(), tp["q"], cache, pos, sp, oc, q_ref=qo,
+                                summaries_from_keys=False)
+    print(f"  {nd} rows differ from the oracle's own selection, each at a near-tie", flush=True)
     # the completed block's summary equals the oracle's
     nb = int(pos[0]) // w.block_size
     got = cache.k_summary[0, :, nb].float().cpu().numpy()

@@ -10,7 +10,9 @@ import torch
 import oracle
 from paper_2609_13141_amd import configs, inputs, sas
 
-from helpers import TOL, assert_close, assert_close_with_infs, f64, spec_of
+from oracle.selector import select
+from helpers import (TOL, assert_close, assert_close_with_infs, assert_selection_near_ties, f64, score_bounds,
+                     spec_of)
 
 pytestmark = pytest.mark.gpu
 
@@ -132,10 +134,15 @@ def test_layer_forward_matches_oracle(w):
     assert_close(out["h1"].float().cpu().numpy(), ref["h1"], w.dtype, "h1")
     assert_close(out["y"].float().cpu().numpy(), ref["y"], w.dtype, "y")
     sel = out["sel_idx"].cpu().numpy()
-    same = np.all(sel == ref["sel"], axis=-1)
-    if w.dtype == "f32":
-        assert same.all()
-    else:
-        # Q/K come from different accumulation orders: a bf16 rounding of Q/K can
-        # differ, which can only swap blocks whose scores nearly tie
-        assert same.mean() >= 0.99, same.mean()
+    qg, kg = out["q"].float().cpu().numpy(), out["k"].float().cpu().numpy()
+    sp = spec_of(w)
+    for bi in range(w.batch):
+        # the oracle's selector on the GPU's own materialised Q/K: bit-exact
+        st = select(f64(qg[bi]), f64(kg[bi]), w.block_size, w.top_k, w.dtype)
+        np.testing.assert_array_equal(sel[bi], st["sel"])
+        # against the oracle's own Q/K: rows may differ only at near-ties within one ulp of Q/K
+        r, bd = score_bounds(ref["Q"][bi], ref["K"][bi], w.block_size, sp.group, w.dtype)
+        np.testing.assert_array_equal(r, ref["r"][bi])
+        nd = assert_selection_near_ties(sel[bi], ref["sel"][bi], r, bd, "layer")
+        print(f"  sequence {bi}: {nd} of {sel[bi].shape[0] * sel[bi].shape[1]} rows differ from the "
+              f"oracle's own selection, each at a near-tie", flush=True)

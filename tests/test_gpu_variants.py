@@ -133,3 +133,29 @@ def test_unsupported_forms_are_rejected():
     for kw in ({"gate_pos": "outer", "gate_act": "raw"}, {"gate_pos": "outer", "ste": True}):
         with pytest.raises(sas.SasError, match="outer gate"):
             sas.attention_prefill(sas.make_config(w, **kw), qd, kd, vd)
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_noise_with_minus_inf_entries_keeps_k_blocks(dt):
+    # blocks whose noisy score is -inf still fill the K slots when fewer than K
+    # other blocks exist (they rank last, lower block first), as in the oracle
+    w = W(dtype=dt, n=180, K=3, b=1, index=150)
+    print(f"\n[case] noise with -inf entries ({dt})", flush=True)
+    q, k, v = inputs.qkv(w)
+    eps = _noise(w)
+    eps[:, :, ::2, 1:] = -np.inf          # even rows: only block 0 has a finite noisy score
+    eps[:, :, 1::4, :] = -np.inf          # every fourth row: no finite noisy score at all
+    cfg = sas.make_config(w, gate_pos="inner", gate_act="softmax", scope="sparse", ste=False)
+    qd, kd, vd = (sas.to_device(a, dt) for a in (q, k, v))
+    fw = sas.attention_prefill(cfg, qd, kd, vd, log_gate=True, noise=torch.from_numpy(eps).cuda())
+    torch.cuda.synchronize()
+    st = select_variant(f64(q[0]), f64(k[0]), w.block_size, w.top_k, dt, act="softmax", noise=f64(eps[0]))
+    sel = fw["sel_idx"][0].cpu().numpy()
+    np.testing.assert_array_equal(sel, st["sel"])
+    ct = np.arange(w.seq_len) // w.block_size
+    assert np.all((sel >= 0).sum(axis=-1) == np.minimum(w.top_k, ct)[None, :])
+    # rows with a finite noisy score: the attention of the kept set (the -inf gates weigh nothing)
+    rows = np.arange(0, w.seq_len, 2)
+    _, O, LSE = variant_attention(f64(q[0]), f64(k[0]), f64(v[0]), w.block_size, dt, st["sel"], st["log_gate"],
+                                  "inner", "sparse", False)
+    assert_close(fw["o"][0].float().cpu().numpy()[rows], O[rows], dt, "O")

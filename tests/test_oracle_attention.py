@@ -209,3 +209,19 @@ def test_rows_subset_matches_full():
     np.testing.assert_array_equal(part["O"][0], full["O"][0][rows])
     np.testing.assert_array_equal(part["sel"][0], full["sel"][0][:, rows])
     np.testing.assert_array_equal(part["LSE"][0], full["LSE"][0][:, rows])
+
+
+@pytest.mark.parametrize("H,Hkv", [(4, 2), (3, 3), (6, 1)])
+def test_causal_attention_matches_sdpa_and_the_gather_form(H, Hkv):
+    # the masked-matrix form of Eq. fula equals torch's causal attention and the
+    # oracle's per-row gather form in DENSE mode, over many blocks
+    rng = np.random.default_rng(30 + H)
+    n, dh = 150, 16
+    Q, K, V = bf16(rng, (n, H, dh)), bf16(rng, (n, Hkv, dh)), bf16(rng, (n, Hkv, dh))
+    O, Oe, LSE = oracle.causal_attention(Q, K, V, "bf16")
+    o, lse = sdpa(Q, K, V, causal=True)
+    np.testing.assert_allclose(Oe, o, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(LSE, lse, rtol=1e-12, atol=1e-12)
+    out = run(Q, K, V, 16, 2, "dense")
+    np.testing.assert_allclose(Oe, out["O_exact"][0], rtol=1e-12, atol=1e-12)
+    np.testing.assert_array_equal(O, oracle.round_bf16(Oe))

@@ -120,3 +120,24 @@ def test_embed_tokens_places_image_rows_in_order():
     img = np.array([[[100.0, 101, 102], [200, 201, 202]]])
     x = oracle.embed_tokens(ids, table, img)
     np.testing.assert_array_equal(x[0], [[100, 101, 102], [6, 7, 8], [200, 201, 202], [0, 1, 2]])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_dense_prefill_layer_equals_layer_forward_dense(dtype):
+    # the serving prefill's layer (masked-matrix attention) equals the per-row
+    # layer in DENSE mode, and the cache contents are its K, V and summaries
+    w = small_workload(dtype=dtype, seq_len=70, segments=(("img", 30), ("txt", 40)), block_size=16)
+    x = f64(inputs.embeddings(w))
+    W = {k: (None if v is None else f64(v)) for k, v in inputs.layer_weights(w, selector_proj=True).items()}
+    sp = spec_of(w, "dense")
+    full = oracle.layer_forward(x, W, sp)
+    for bi in range(w.batch):
+        d = oracle.dense_prefill_layer(x[bi], W, sp)
+        np.testing.assert_array_equal(d["K"], full["K"][bi])
+        np.testing.assert_array_equal(d["V"], full["V"][bi])
+        np.testing.assert_array_equal(d["k_summary"], full["k_summary"][bi])
+        tol = 1e-12 * float(np.abs(full["y"][bi]).max())
+        # roundings of O may differ where the two fp64 attention forms straddle a tie: compare h1/y loosely
+        np.testing.assert_allclose(d["O_exact"], full["O_exact"][bi], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(d["y"], full["y"][bi], rtol=0, atol=max(tol, 4 * float(np.abs(d["y"]).max())
+                                                                             * (2 ** -8 if dtype == "bf16" else 2 ** -23)))
