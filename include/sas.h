@@ -405,6 +405,25 @@ sas_status sas_decode_step(const sas_config* cfg, int32_t batch, const void* x,
                            sas_paged_kv* cache, void* y, int32_t* sel_idx,
                            sas_layer_taps* taps, void* ws, size_t ws_bytes, void* stream);
 
+/* Scratch bytes of sas_decode_step_noalloc (one static copy per GPU). */
+#define SAS_DECODE_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+
+/* sas_decode_step for callers that cannot allocate device memory or pass a
+ * workspace: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation.  Same arguments, kernels and results as
+ * sas_decode_step (without taps); the scratch is a static device array of
+ * SAS_DECODE_NOALLOC_SCRATCH_BYTES per GPU, looked up on the first call on
+ * each device and held until the process ends.  A call whose workspace
+ * (sas_workspace_size(cfg, SAS_OP_DECODE, batch, max_blocks * B)) exceeds it
+ * returns SAS_ERR_WORKSPACE before touching the GPU (32 MiB covers batch 8 of
+ * the 7B shape up to 512K tokens of context).  The step needs nothing in the
+ * scratch to start at zero, and nothing is allocated or freed.  Every call
+ * on one GPU shares that GPU's scratch: calls that may overlap on one GPU
+ * (other streams, other threads) race and must be serialised by the caller. */
+sas_status sas_decode_step_noalloc(const sas_config* cfg, int32_t batch, const void* x,
+                                   const int32_t* pos, const sas_layer_weights* w,
+                                   sas_paged_kv* cache, void* y, int32_t* sel_idx, void* stream);
+
 /* The selection of a decode step alone (Alg. 2's Top-K over the block
  * summaries; Sec. 5.1), for long contexts where it dominates the step:
  * q [b, H, dh] holds the post-RoPE query heads of the new tokens (activation

@@ -28,7 +28,7 @@ SCOPES = {"sparse": 0, "full": 1}
 TORCH_DTYPE = {"bf16": torch.bfloat16, "f32": torch.float32}
 
 EXPORTS = ("sas_workspace_size", "sas_attention_prefill", "sas_mlp_forward", "sas_layer_forward",
-           "sas_decode_step", "sas_decode_select", "sas_attention_backward", "sas_selector_backward", "sas_selection_stats", "sas_overlap_recall", "sas_embed", "sas_lm_head_argmax", "sas_last_error", "sas_version",
+           "sas_decode_step", "sas_decode_step_noalloc", "sas_decode_select", "sas_attention_backward", "sas_selector_backward", "sas_selection_stats", "sas_overlap_recall", "sas_embed", "sas_lm_head_argmax", "sas_last_error", "sas_version",
            "sas_profiler_start", "sas_profiler_stop", "sas_profiler_record")
 
 
@@ -121,6 +121,9 @@ def lib() -> C.CDLL:
     L.sas_decode_step.restype = i32
     L.sas_decode_step.argtypes = [C.POINTER(Config), i32, vp, vp, C.POINTER(LayerWeights), C.POINTER(PagedKV),
                                   vp, vp, C.POINTER(LayerTaps), vp, sz, vp]
+    L.sas_decode_step_noalloc.restype = i32
+    L.sas_decode_step_noalloc.argtypes = [C.POINTER(Config), i32, vp, vp, C.POINTER(LayerWeights),
+                                          C.POINTER(PagedKV), vp, vp, vp]
     L.sas_decode_select.restype = i32
     L.sas_decode_select.argtypes = [C.POINTER(Config), i32, vp, vp, vp, C.POINTER(PagedKV), vp, vp, sz, vp]
     L.sas_attention_backward.restype = i32
@@ -450,6 +453,18 @@ def decode_step(cfg: Config, x, pos, W: dict, cache: PagedCache, *, sel_idx: boo
                                  _ptr(y), _ptr(sel), C.byref(tp) if tp is not None else None, wsp, wsn,
                                  _stream()))
     return (y, sel, tap) if taps else (y, sel)
+
+
+def decode_step_noalloc(cfg: Config, x, pos, W: dict, cache: PagedCache, *, sel_idx: bool = True):
+    """sas_decode_step_noalloc: the decode step with the library's static
+    scratch (no workspace, nothing allocated by the library)."""
+    b = x.shape[0]
+    y = torch.empty_like(x)
+    sel = torch.empty(b, cfg.n_kv_heads, cfg.top_k, dtype=torch.int32, device=x.device) if sel_idx else None
+    cs = cache.struct()
+    _check(lib().sas_decode_step_noalloc(C.byref(cfg), b, _ptr(x), _ptr(pos), C.byref(weights_struct(W)),
+                                         C.byref(cs), _ptr(y), _ptr(sel), _stream()))
+    return y, sel
 
 
 def decode_select(cfg: Config, q, pos, cache: PagedCache, w_gq=None, ws: Workspace | None = None):

@@ -95,3 +95,17 @@ def test_layer_and_mlp_reject_missing_weights(L):
     bad = sas.make_config(configs.L7B_1K)
     bad.d_ff = 1001
     assert L.sas_mlp_forward(C.byref(bad), 4, 0x1000, C.byref(W), 0x1000, None, 0, None) == sas.SAS_ERR_UNSUPPORTED
+
+
+def test_noalloc_decode_rejects_oversized_calls_before_touching_the_gpu(L):
+    # batch 16 over 8192 blocks needs 16 * 32 * 8192 doubles of selector scores alone (32 MiB):
+    # more than the static scratch holds; the call fails on the host with a clear message
+    import ctypes as C
+    w = configs.STACK_DECODE
+    cfg = sas.make_config(w, "sparse")
+    fake = C.c_void_p(256)
+    cache = sas.PagedKV(fake, fake, fake, fake, 1, 16, 1, 8192)
+    st = L.sas_decode_step_noalloc(C.byref(cfg), 16, fake, fake, C.byref(sas.weights_struct({})), C.byref(cache),
+                                   fake, None, None)
+    assert st == -3   # SAS_ERR_WORKSPACE
+    assert b"static" in L.sas_last_error() and b"scratch" in L.sas_last_error()
