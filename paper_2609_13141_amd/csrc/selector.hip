@@ -153,7 +153,7 @@ constexpr int SEL_NW = 4;   // waves per workgroup
 
 __device__ __forceinline__ void lds_fence() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
-template <typename T, int DH, int KMAX, int SEL_MC>
+template <typename T, int DH, int KMAX, int SEL_MC, bool NOISY>
 __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
   constexpr int KB_BYTES = SEL_NW * SEL_MC * DH * 4;
   constexpr int MG_BYTES = KMAX * WAVE * 12 + WAVE * 8 + WAVE * 4;
@@ -178,7 +178,7 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
   const double den = (double)G * sqrt((double)DH);  // s = r / (G sqrt(dh))
   const double inv_scale = 1.0 / den;
   const size_t row = ((size_t)bi * P.Hkv + g) * P.n + t;
-  const float* noise = (P.noise && valid) ? P.noise + row * P.NB : nullptr;
+  const float* noise = (NOISY && valid) ? P.noise + row * P.NB : nullptr;
   // the log-gate table row of this query: raw scores written as they are computed (softmax:
   // the LSE is subtracted at the end), the other activations' gates written directly
   float* lgrow = (P.log_gate && valid) ? P.log_gate + row * P.NB : nullptr;
@@ -232,14 +232,19 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
   }
   double mrun = -DBL_MAX;  // running max of s
   float lrun = 0.f;        // running sum of exp(s - mrun)
-  // does key a rank strictly ahead of the slot (b, bm)?  Every key beats an
-  // empty slot (so -inf keys are kept when fewer than K others exist), NaN
-  // ranks below every number, and an equal key keeps the earlier (lower)
-  // block ahead
+  // does key a rank strictly ahead of the slot (b, bm)?  An equal key keeps
+  // the earlier (lower) block ahead.  Without noise every key is a finite
+  // exact dot product, above the empty slots' -DBL_MAX.  With noise a key can
+  // be -inf (or NaN): every key then beats an empty slot (so such blocks are
+  // kept when fewer than K others exist) and NaN ranks below every number.
   auto beats = [](double a, double b, int bm) -> bool {
-    if (bm == EMPTY) return true;
-    if (a != a) return false;
-    return a > b || b != b;
+    if constexpr (!NOISY) {
+      return a > b;
+    } else {
+      if (bm == EMPTY) return true;
+      if (a != a) return false;
+      return a > b || b != b;
+    }
   };
   auto insert = [&](double cr, int cm) {
     if (cm == EMPTY || !beats(cr, tr[KMAX - 1], tm[KMAX - 1])) return;
@@ -410,19 +415,25 @@ __global__ void finish_table_kernel(float* __restrict__ table, const float* __re
   table[idx] = (m < ct && m >= fb) ? (softmax ? table[idx] - row_lse[row] : table[idx]) : -INFINITY;
 }
 
-template <typename T, int DH>
-static void run_select(const SelectArgs& a, hipStream_t s) {
+template <typename T, int DH, bool NOISY>
+static void run_select_t(const SelectArgs& a, hipStream_t s) {
   dim3 grid(cdiv(a.n, WAVE), a.Hkv, a.b);
   // chunks of 4 summaries when no wave has more than 4 blocks to score (short sequences)
   if (cdiv(a.NB, SEL_NW) <= 4) {
-    if (a.K <= 8) select_kernel<T, DH, 8, 4><<<grid, SEL_NW * WAVE, 0, s>>>(a);
-    else if (a.K <= 16) select_kernel<T, DH, 16, 4><<<grid, SEL_NW * WAVE, 0, s>>>(a);
-    else select_kernel<T, DH, 32, 4><<<grid, SEL_NW * WAVE, 0, s>>>(a);
+    if (a.K <= 8) select_kernel<T, DH, 8, 4, NOISY><<<grid, SEL_NW * WAVE, 0, s>>>(a);
+    else if (a.K <= 16) select_kernel<T, DH, 16, 4, NOISY><<<grid, SEL_NW * WAVE, 0, s>>>(a);
+    else select_kernel<T, DH, 32, 4, NOISY><<<grid, SEL_NW * WAVE, 0, s>>>(a);
   } else {
-    if (a.K <= 8) select_kernel<T, DH, 8, 8><<<grid, SEL_NW * WAVE, 0, s>>>(a);
-    else if (a.K <= 16) select_kernel<T, DH, 16, 8><<<grid, SEL_NW * WAVE, 0, s>>>(a);
-    else select_kernel<T, DH, 32, 8><<<grid, SEL_NW * WAVE, 0, s>>>(a);
+    if (a.K <= 8) select_kernel<T, DH, 8, 8, NOISY><<<grid, SEL_NW * WAVE, 0, s>>>(a);
+    else if (a.K <= 16) select_kernel<T, DH, 16, 8, NOISY><<<grid, SEL_NW * WAVE, 0, s>>>(a);
+    else select_kernel<T, DH, 32, 8, NOISY><<<grid, SEL_NW * WAVE, 0, s>>>(a);
   }
+}
+
+template <typename T, int DH>
+static void run_select(const SelectArgs& a, hipStream_t s) {
+  if (a.noise) run_select_t<T, DH, true>(a, s);
+  else run_select_t<T, DH, false>(a, s);
 }
 
 hipError_t launch_select(int dtype, const SelectArgs& a, hipStream_t s) {
