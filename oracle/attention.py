@@ -21,7 +21,7 @@ import math
 
 import numpy as np
 
-from .numerics import rho
+from .numerics import _POOL, rho
 
 
 def sas_attention(Q, K, V, B, mode, dtype, sel=None, log_gate=None,
@@ -90,7 +90,8 @@ def causal_attention(Q, K, V, dtype, sm_scale=None):
     future = np.triu(np.ones((n, n), dtype=bool), k=1)        # key i after query t
     O = np.zeros((n, H, dh))
     LSE = np.zeros((H, n))
-    for h in range(H):
+
+    def head(h):
         g = h // G
         Z = sm * (Q[:, h, :] @ K[:, g, :].T)
         Z[future] = -np.inf
@@ -99,4 +100,10 @@ def causal_attention(Q, K, V, dtype, sm_scale=None):
         L = E.sum(axis=1, keepdims=True)
         O[:, h, :] = (E @ V[:, g, :]) / L
         LSE[h] = (zmax + np.log(L))[:, 0]
+    # heads are independent: computed on threads when the sequence is long
+    if n >= 512:
+        list(_POOL.map(head, range(H)))
+    else:
+        for h in range(H):
+            head(h)
     return rho(O, dtype), O, LSE

@@ -5,16 +5,35 @@ their layer; the layer here is the usual pre-norm decoder block: RMSNorm,
 rotary position embedding (rotate-half pairing, base 10000), SwiGLU MLP.
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 """
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
 BF16_MAX = (2.0 - 2.0 ** -7) * 2.0 ** 127
 
+# elementwise work on large arrays is split into chunks run on threads (NumPy
+# releases the GIL inside its loops); every element is computed the same way
+_POOL = ThreadPoolExecutor(max_workers=min(16, len(os.sched_getaffinity(0))))
+_CHUNK = 1 << 19
 
-def round_bf16(x):
-    """Round float64 values to the nearest bfloat16 value, ties to even,
-    directly from float64 (8 significant bits; subnormal spacing 2^-133;
-    overflow to +-inf).  Returns float64 holding the bfloat16 values."""
+
+def elementwise(f, x):
+    """f applied to the float64 array x, in chunks of its flattened elements
+    (f must act on each element independently)."""
     x = np.asarray(x, dtype=np.float64)
+    if x.size <= _CHUNK:
+        return f(x)
+    flat = x.reshape(-1)
+    out = np.empty_like(flat)
+
+    def run(i):
+        out[i:i + _CHUNK] = f(flat[i:i + _CHUNK])
+    list(_POOL.map(run, range(0, flat.size, _CHUNK)))
+    return out.reshape(x.shape)
+
+
+def _round_bf16(x):
     out = np.array(x, dtype=np.float64, copy=True)
     fin = np.isfinite(x) & (x != 0.0)
     if np.any(fin):
@@ -25,6 +44,13 @@ def round_bf16(x):
         r = np.where(np.abs(r) > BF16_MAX, np.copysign(np.inf, r), r)
         out[fin] = r
     return out
+
+
+def round_bf16(x):
+    """Round float64 values to the nearest bfloat16 value, ties to even,
+    directly from float64 (8 significant bits; subnormal spacing 2^-133;
+    overflow to +-inf).  Returns float64 holding the bfloat16 values."""
+    return elementwise(_round_bf16, x)
 
 
 def round_f32(x):
@@ -64,8 +90,11 @@ def rope(x, pos, base):
     return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
 
 
-def silu(x):
-    """silu(x) = x / (1 + exp(-x))."""
-    x = np.asarray(x, dtype=np.float64)
+def _silu(x):
     with np.errstate(over="ignore"):
         return x / (1.0 + np.exp(-x))
+
+
+def silu(x):
+    """silu(x) = x / (1 + exp(-x))."""
+    return elementwise(_silu, x)
