@@ -139,7 +139,8 @@ def layer_weights_device(w: Workload, layer: int = 0, seed: int = 0, device="cud
     (32 layers of the 7B shape are 6.5 G values): N(0, weight_std) from
     torch's Philox generator seeded per (workload, tensor, layer), rounded to
     the activation dtype; RMSNorm gains 1.  Same shapes and distribution as
-    layer_weights(); the values differ (they are not compared with the oracle)."""
+    layer_weights(); the values differ (the oracle receives these ones by copying
+    them to the host)."""
     import torch
 
     d, H, Hkv, dh, F = w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.d_ff

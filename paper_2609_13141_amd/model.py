@@ -33,13 +33,18 @@ class Stack:
         self.max_len = max_len
         self.pos = None
 
-    def prefill(self, ids, img=None, *, logits: bool = False):
+    def prefill(self, ids, img=None, *, logits: bool = False, on_layer=None):
         """ids [b, n] int32 on the device (-1 = next image embedding row);
         returns the first generated token of every sequence [b] int32 (and
-        its fp32 logits when asked)."""
+        its fp32 logits when asked).  on_layer(l, x), when given, sees the
+        input x [b, n, d] of every layer l and the last layer's output (l = L)."""
         x = sas.embed(self.cfg_prefill, ids, self.ends["embed"], img)
-        for W, cache in zip(self.layers, self.caches):
+        for l, (W, cache) in enumerate(zip(self.layers, self.caches)):
+            if on_layer is not None:
+                on_layer(l, x)
             x = sas.layer_forward(self.cfg_prefill, x, W, stats=False, cache=cache, ws=self.ws)["y"]
+        if on_layer is not None:
+            on_layer(len(self.layers), x)
         self.pos = ids.shape[1]
         tok, lg = sas.lm_head_argmax(self.cfg_decode, x[:, -1].contiguous(), self.ends["rms_final"],
                                      self.ends["w_lm"], logits=logits, ws=self.ws)
@@ -54,13 +59,14 @@ class Stack:
         """One generated token per sequence: tok [b] at positions pos [b]
         (device int32).  Returns the next tokens, the logits and per-layer
         selections when asked, and with taps a per-layer list of
-        {"x": layer input, "q", "k", "v", "h1"}."""
+        {"x": layer input, "q", "k", "v", "h1", "y": layer output}."""
         x = sas.embed(self.cfg_decode, tok.view(-1, 1), self.ends["embed"])[:, 0].contiguous()
         sels, tps = [], []
         for W, cache in zip(self.layers, self.caches):
             r = sas.decode_step(self.cfg_decode, x, pos, W, cache, sel_idx=sel_idx, taps=taps, ws=self.ws)
             if taps:
                 r[2]["x"] = x
+                r[2]["y"] = r[0]
                 tps.append(r[2])
             x, sel = r[0], r[1]
             sels.append(sel)
