@@ -13,6 +13,8 @@
 // Column groups of the pair epilogues hold 8 first-half and 8 second-half
 // columns (RoPE: i and i + dh/2 of a head; SwiGLU: gate f and up f); a lane's
 // partner is lane ^ 8 after the reduction.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -40,9 +42,12 @@ struct GemvParams {
   int B, max_blocks;
 };
 
-// weight row of local column c (0..15) of column group gi
+// weight row of local column c (0..15) of column group gi (EPI < 0: the
+// epilogue kind is read from P at run time)
+template <int EPI = -1>
 __device__ __forceinline__ const bf16_t* gemv_row(const GemvParams& P, int gi, int c, bool& valid) {
-  if (P.epi == EPI_RESID || P.epi == EPI_F32OUT) {
+  const int epi = EPI >= 0 ? EPI : P.epi;
+  if (epi == EPI_RESID || epi == EPI_F32OUT) {
     const int col = gi * 16 + c;
     valid = col < P.N;
     return P.B0 + (size_t)min(col, P.N - 1) * P.K;
@@ -50,7 +55,7 @@ __device__ __forceinline__ const bf16_t* gemv_row(const GemvParams& P, int gi, i
   const int p = gi * 8 + (c & 7), half = c >> 3;
   valid = p < P.npairs;
   const int pc = min(p, P.npairs - 1);
-  if (P.epi == EPI_SWIGLU) return (half ? P.B1 : P.B0) + (size_t)pc * P.K;
+  if (epi == EPI_SWIGLU) return (half ? P.B1 : P.B0) + (size_t)pc * P.K;
   const int hh = P.dh >> 1;
   const int hd = pc / hh, ir = pc % hh;
   int cc = hd * P.dh + ir + half * hh;
@@ -60,6 +65,141 @@ __device__ __forceinline__ const bf16_t* gemv_row(const GemvParams& P, int gi, i
   return P.B2 + (size_t)(cc - P.Hkv * P.dh) * P.K;
 }
 
+// Epilogue inputs of a lane for column group gi (pair gi * 8 + c % 8, rows
+// 4 kg + v): the QKV epilogue's rotary entries and cache offsets, the RESID
+// epilogue's residual values; loaded before the weights they follow so that
+// their latency is hidden by the weight stream.
+struct GemvPre {
+  float2 cs[4];
+  long long off[4];
+  int ps[4];
+  float res[4];
+};
+
+template <int EPI = -1>
+__device__ __forceinline__ void gemv_prepare(const GemvParams& P, int gi, int c, int kg, GemvPre& e) {
+  const int epi = EPI >= 0 ? EPI : P.epi;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    e.cs[v] = make_float2(1.f, 0.f);
+    e.off[v] = -1;
+    e.ps[v] = 0;
+    e.res[v] = 0.f;
+  }
+  if (epi == EPI_RESID) {
+    const int col = min(gi * 16 + c, P.N - 1);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int row = min(4 * kg + v, P.M - 1);
+      e.res[v] = bf16_to_f32(P.resid[(size_t)row * P.N + col]);
+    }
+    return;
+  }
+  if (epi != EPI_QKV_ROPE) return;
+  const int hh = P.dh >> 1;
+  const int p = min(gi * 8 + (c & 7), P.npairs - 1);
+  const int hd = p / hh, ir = p % hh;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int row = 4 * kg + v;
+    if (row >= P.M) continue;
+    if (hd < P.H + P.Hkv) e.cs[v] = P.rope[(size_t)row * hh + ir];
+    if (P.k_pages && hd >= P.H) {
+      const int g = hd < P.H + P.Hkv ? hd - P.H : hd - P.H - P.Hkv;
+      e.ps[v] = P.pos[row];
+      e.off[v] = P.geom.offset(row, g, e.ps[v], P.Hkv, P.dh);
+    }
+  }
+}
+
+// The fused epilogue of column group gi; `tot` holds column c, rows 4 kg + v.
+template <int EPI = -1>
+__device__ __forceinline__ void gemv_epilogue(const GemvParams& P, int gi, int c, int kg, const floatx4_t& tot,
+                                              const GemvPre& e) {
+  const int epi = EPI >= 0 ? EPI : P.epi;
+  bool cvalid;
+  (void)gemv_row<EPI>(P, gi, c, cvalid);
+  if (epi == EPI_RESID || epi == EPI_F32OUT) {
+    const int col = gi * 16 + c;
+    if (!cvalid) return;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int row = 4 * kg + v;
+      if (row >= P.M) continue;
+      const size_t o = (size_t)row * P.N + col;
+      if (epi == EPI_RESID)
+        ((bf16_t*)P.out)[o] = f32_to_bf16(tot[v] + e.res[v]);
+      else
+        ((float*)P.out)[o] = tot[v];
+    }
+    return;
+  }
+  const int hh = P.dh >> 1;
+  float partner[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) partner[v] = __shfl_xor(tot[v], 8, 64);
+  if (c >= 8 || !cvalid) return;
+  const int p = gi * 8 + c;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int row = 4 * kg + v;
+    if (row >= P.M) continue;
+    float x1 = tot[v], x2 = partner[v];
+    if (epi == EPI_SWIGLU) {
+      ((bf16_t*)P.out)[(size_t)row * P.npairs + p] = f32_to_bf16(x1 / (1.0f + __expf(-x1)) * x2);
+      continue;
+    }
+    const int hd = p / hh, ir = p % hh;
+    bf16_t* dst;
+    if (hd < P.H) dst = (bf16_t*)P.out + ((size_t)row * P.H + hd) * P.dh;
+    else if (hd < P.H + P.Hkv) dst = P.out1 + ((size_t)row * P.Hkv + (hd - P.H)) * P.dh;
+    else dst = P.out2 + ((size_t)row * P.Hkv + (hd - P.H - P.Hkv)) * P.dh;
+    if (hd < P.H + P.Hkv) {
+      const float2 cs = e.cs[v];
+      const float o1 = x1 * cs.x - x2 * cs.y;
+      const float o2 = x2 * cs.x + x1 * cs.y;
+      x1 = o1;
+      x2 = o2;
+    }
+    const bf16_t b1 = f32_to_bf16(x1), b2 = f32_to_bf16(x2);
+    dst[ir] = b1;
+    dst[ir + hh] = b2;
+    if (P.k_pages && hd >= P.H) {
+      // cache append of this row's K or V, dimensions ir and ir + dh/2
+      const bool isk = hd < P.H + P.Hkv;
+      const int g = isk ? hd - P.H : hd - P.H - P.Hkv;
+      const int ps = e.ps[v];
+      const long long off = e.off[v];
+      if (off < 0) continue;
+      bf16_t* pg = (bf16_t*)(isk ? P.k_pages : P.v_pages) + off;
+      pg[ir] = b1;
+      pg[ir + hh] = b2;
+      if (!isk || (ps + 1) % P.B != 0 || ps / P.B >= P.max_blocks) continue;
+      // this position completes block m: its summary in these two dimensions
+      // (fp64 sum over ascending positions, the new key last)
+      const int m = ps / P.B;
+      double s1 = 0.0, s2 = 0.0;
+      for (int q = m * P.B; q < ps; ++q) {
+        const long long o = P.geom.offset(row, g, q, P.Hkv, P.dh);
+        float k1 = 0.f, k2 = 0.f;  // a position without a page adds zero
+        if (o >= 0) {
+          k1 = bf16_to_f32(((const bf16_t*)P.k_pages)[o + ir]);
+          k2 = bf16_to_f32(((const bf16_t*)P.k_pages)[o + ir + hh]);
+        }
+        s1 += (double)k1;
+        s2 += (double)k2;
+      }
+      s1 += (double)bf16_to_f32(b1);
+      s2 += (double)bf16_to_f32(b2);
+      bf16_t* sm = (bf16_t*)P.k_summary + (((size_t)row * P.Hkv + g) * P.max_blocks + m) * P.dh;
+      sm[ir] = Act<bf16_t>::from_f64(s1 / (double)P.B);
+      sm[ir + hh] = Act<bf16_t>::from_f64(s2 / (double)P.B);
+    }
+  }
+}
+
+// One workgroup per 16-column group, its waves splitting K (the shapes the
+// streaming kernel below does not cover).
 template <int NW>
 __global__ void __launch_bounds__(NW * 64) gemv_kernel(GemvParams P) {
   __shared__ floatx4_t part[NW][64];
@@ -71,34 +211,8 @@ __global__ void __launch_bounds__(NW * 64) gemv_kernel(GemvParams P) {
   const int arow = min(c, P.M - 1);
   const bool avalid = c < P.M;
   const bf16_t* ar = P.A + (size_t)arow * P.K;
-
-  // QKV epilogue inputs of this lane (pair gi * 8 + c % 8, rows 4 kg + v), read before the
-  // weight stream so their latency (the page offset is a dependent lookup) is hidden by it
-  const int hh = P.dh >> 1;
-  float2 cs_pre[4];
-  long long off_pre[4];
-  int ps_pre[4];
-#pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    cs_pre[v] = make_float2(1.f, 0.f);
-    off_pre[v] = -1;
-    ps_pre[v] = 0;
-  }
-  if (P.epi == EPI_QKV_ROPE && wave == 0) {
-    const int p = min(gi * 8 + (c & 7), P.npairs - 1);
-    const int hd = p / hh, ir = p % hh;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int row = 4 * kg + v;
-      if (row >= P.M) continue;
-      if (hd < P.H + P.Hkv) cs_pre[v] = P.rope[(size_t)row * hh + ir];
-      if (P.k_pages && hd >= P.H) {
-        const int g = hd < P.H + P.Hkv ? hd - P.H : hd - P.H - P.Hkv;
-        ps_pre[v] = P.pos[row];
-        off_pre[v] = P.geom.offset(row, g, ps_pre[v], P.Hkv, P.dh);
-      }
-    }
-  }
+  GemvPre pre;
+  if (wave == 0) gemv_prepare(P, gi, c, kg, pre);
 
   // this wave's k range, in chunks of 128
   const int nchunk = P.K / 128;
@@ -142,88 +256,116 @@ __global__ void __launch_bounds__(NW * 64) gemv_kernel(GemvParams P) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) tot[v] += p[v];
   }
-  // lane holds column c, rows 4*kg + v
-  if (P.epi == EPI_RESID || P.epi == EPI_F32OUT) {
-    const int col = gi * 16 + c;
-    if (!cvalid) return;
+  gemv_epilogue(P, gi, c, kg, tot, pre);
+}
+
+// ---------------------------------------------------------------------------
+// Streaming kernel: one workgroup of NW waves per compute unit, looping over
+// 16-column groups (group gi = blockIdx.x + j * gridDim.x).  Wave w owns the
+// 32-wide k steps [w * per, w * per + nst) and keeps its slice of the
+// activation rows in registers for the whole launch (KS steps: one 16-byte
+// fragment per lane and step), so the activation is read once per workgroup
+// instead of once per column group, and only weights stream in the loop.
+// The weight fragments of a group flow through a ring of R registers: after
+// the MFMA of step i the ring slot is refilled with step i + R, which past
+// the group's last step is a step of the workgroup's next group, so the
+// stream does not drain between groups.  Steps beyond the wave's range (when
+// K / 32 is not KS * NW) multiply zero activations with weights loaded from a
+// clamped in-range address.  The waves' partial sums meet in LDS
+// (double-buffered, one barrier per group that does not wait for the loads
+// in flight) and one wave, changing from group to group, applies the
+// epilogue.  It pays where each workgroup has several column groups to
+// stream (the SwiGLU product of a layer); with one or two per workgroup the
+// per-group kernel above is faster.
+template <int EPI, int NW, int KS, int R, bool FULL>
+__global__ void __launch_bounds__(NW * 64) gemv_stream_kernel(GemvParams P, int ngroups) {
+  static_assert(KS % R == 0, "the ring must divide the steps");
+  __shared__ floatx4_t part[2][NW][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c = lane & 15, kg = lane >> 4;
+  const int steps = P.K / 32;
+  const int per = FULL ? KS : (steps + NW - 1) / NW;
+  const int s0 = wave * per;
+  const int nst = FULL ? KS : max(0, min(steps, s0 + per) - s0);
+  const int slast = max(min(s0 + nst, steps) - 1, 0);  // last in-range step (clamp target)
+  // k step i of this wave, clamped into its range unless every wave owns KS steps
+  auto step_of = [&](int i) { return FULL ? s0 + i : min(s0 + i, slast); };
+  const bool rvalid = c < P.M;
+
+  // weight fragment of step i of group gi (k clamped into the wave's range)
+  auto wrow = [&](int gi) {
+    bool v;
+    return gemv_row<EPI>(P, gi, c, v) + 8 * kg;
+  };
+  auto wload = [&](const bf16_t* wr, int i) { return *(const uint4*)(wr + (size_t)step_of(i) * 32); };
+  // the activation slice: rows >= M and steps past the wave's range are zero
+  uint4 a[KS];
+  {
+    const bf16_t* ar = P.A + (size_t)min(c, P.M - 1) * P.K + 8 * kg;
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int row = 4 * kg + v;
-      if (row >= P.M) continue;
-      const size_t o = (size_t)row * P.N + col;
-      if (P.epi == EPI_RESID)
-        ((bf16_t*)P.out)[o] = f32_to_bf16(tot[v] + bf16_to_f32(P.resid[o]));
-      else
-        ((float*)P.out)[o] = tot[v];
+    for (int i = 0; i < KS; ++i) {
+      const uint4 v = *(const uint4*)(ar + (size_t)step_of(i) * 32);
+      a[i] = (i < nst && rvalid) ? v : make_uint4(0, 0, 0, 0);
     }
-    return;
   }
-  float partner[4];
+  int gi = blockIdx.x;
+  if (gi >= ngroups) return;
+  const bf16_t* wr = wrow(gi);
+  uint4 w[R];
 #pragma unroll
-  for (int v = 0; v < 4; ++v) partner[v] = __shfl_xor(tot[v], 8, 64);
-  if (c >= 8 || !cvalid) return;
-  const int p = gi * 8 + c;
+  for (int r = 0; r < R; ++r) w[r] = wload(wr, r);
+  for (int it = 0; gi < ngroups; ++it) {
+    const int gn = gi + (int)gridDim.x < ngroups ? gi + (int)gridDim.x : gi;  // next group (or this one again)
+    const bf16_t* wn = wrow(gn);
+    GemvPre pre;
+    const int reducer = it % NW;
+    if (wave == reducer) gemv_prepare<EPI>(P, gi, c, kg, pre);
+    floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    const int row = 4 * kg + v;
-    if (row >= P.M) continue;
-    float x1 = tot[v], x2 = partner[v];
-    if (P.epi == EPI_SWIGLU) {
-      ((bf16_t*)P.out)[(size_t)row * P.npairs + p] = f32_to_bf16(x1 / (1.0f + __expf(-x1)) * x2);
-      continue;
+    for (int i = 0; i < KS; ++i) {
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(bf16x8_t*)&a[i], *(bf16x8_t*)&w[i % R], acc, 0, 0, 0);
+      w[i % R] = i + R < KS ? wload(wr, i + R) : wload(wn, i + R - KS);
     }
-    const int hd = p / hh, ir = p % hh;
-    bf16_t* dst;
-    if (hd < P.H) dst = (bf16_t*)P.out + ((size_t)row * P.H + hd) * P.dh;
-    else if (hd < P.H + P.Hkv) dst = P.out1 + ((size_t)row * P.Hkv + (hd - P.H)) * P.dh;
-    else dst = P.out2 + ((size_t)row * P.Hkv + (hd - P.H - P.Hkv)) * P.dh;
-    if (hd < P.H + P.Hkv) {
-      const float2 cs = cs_pre[v];
-      const float o1 = x1 * cs.x - x2 * cs.y;
-      const float o2 = x2 * cs.x + x1 * cs.y;
-      x1 = o1;
-      x2 = o2;
-    }
-    const bf16_t b1 = f32_to_bf16(x1), b2 = f32_to_bf16(x2);
-    dst[ir] = b1;
-    dst[ir + hh] = b2;
-    if (P.k_pages && hd >= P.H) {
-      // cache append of this row's K or V, dimensions ir and ir + dh/2
-      const bool isk = hd < P.H + P.Hkv;
-      const int g = isk ? hd - P.H : hd - P.H - P.Hkv;
-      const int ps = ps_pre[v];
-      const long long off = off_pre[v];
-      if (off < 0) continue;
-      bf16_t* pg = (bf16_t*)(isk ? P.k_pages : P.v_pages) + off;
-      pg[ir] = b1;
-      pg[ir + hh] = b2;
-      if (!isk || (ps + 1) % P.B != 0 || ps / P.B >= P.max_blocks) continue;
-      // this position completes block m: its summary in these two dimensions
-      // (fp64 sum over ascending positions, the new key last)
-      const int m = ps / P.B;
-      double s1 = 0.0, s2 = 0.0;
-      for (int q = m * P.B; q < ps; ++q) {
-        const long long o = P.geom.offset(row, g, q, P.Hkv, P.dh);
-        float k1 = 0.f, k2 = 0.f;  // a position without a page adds zero
-        if (o >= 0) {
-          k1 = bf16_to_f32(((const bf16_t*)P.k_pages)[o + ir]);
-          k2 = bf16_to_f32(((const bf16_t*)P.k_pages)[o + ir + hh]);
-        }
-        s1 += (double)k1;
-        s2 += (double)k2;
+    part[it & 1][wave][lane] = acc;
+    lds_barrier();
+    if (wave == reducer) {
+      floatx4_t tot = part[it & 1][0][lane];
+#pragma unroll
+      for (int wv = 1; wv < NW; ++wv) {
+        const floatx4_t p = part[it & 1][wv][lane];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) tot[v] += p[v];
       }
-      s1 += (double)bf16_to_f32(b1);
-      s2 += (double)bf16_to_f32(b2);
-      bf16_t* sm = (bf16_t*)P.k_summary + (((size_t)row * P.Hkv + g) * P.max_blocks + m) * P.dh;
-      sm[ir] = Act<bf16_t>::from_f64(s1 / (double)P.B);
-      sm[ir + hh] = Act<bf16_t>::from_f64(s2 / (double)P.B);
+      gemv_epilogue<EPI>(P, gi, c, kg, tot, pre);
     }
+    gi += gridDim.x;
+    wr = wn;
   }
+}
+
+// Streaming launch: 4 waves of 32 steps of 32 (128 registers of activation
+// per lane) and a ring of 8, so K <= 4096; the FULL variant for K = 4096
+// exactly (every wave owns 32 steps: loads at immediate offsets).
+constexpr int GV_NW = 4, GV_KS = 32, GV_R = 8;
+
+static bool gemv_streams(const GemmArgs& g) {
+  return g.epi == EPI_SWIGLU && g.K % 32 == 0 && g.K <= GV_NW * GV_KS * 32;
+}
+
+template <bool FULL>
+static hipError_t run_stream(const GemvParams& P, int groups, hipStream_t s) {
+  auto kern = gemv_stream_kernel<EPI_SWIGLU, GV_NW, GV_KS, GV_R, FULL>;
+  static int resident = 0;
+  if (resident <= 0) resident = resident_workgroups(kern, GV_NW * 64);
+  if (resident <= 0) return hipErrorInvalidValue;
+  kern<<<std::min(groups, resident), GV_NW * 64, 0, s>>>(P, groups);
+  return hipGetLastError();
 }
 
 hipError_t launch_gemv(const GemmArgs& g, hipStream_t s) {
   if (g.M <= 0) return hipSuccess;
-  if (g.M > 16 || g.K % 128 != 0) return hipErrorInvalidValue;
+  const bool stream = gemv_streams(g);
+  if (g.M > 16 || (!stream && g.K % 128 != 0)) return hipErrorInvalidValue;
   GemvParams P;
   P.epi = g.epi;
   P.M = g.M;
@@ -263,6 +405,9 @@ hipError_t launch_gemv(const GemmArgs& g, hipStream_t s) {
     }
   }
   const int groups = (g.epi == EPI_RESID || g.epi == EPI_F32OUT) ? (g.N + 15) / 16 : (P.npairs + 7) / 8;
+  if (stream) {
+    return g.K == GV_NW * GV_KS * 32 ? run_stream<true>(P, groups, s) : run_stream<false>(P, groups, s);
+  }
   // fewer column groups -> more waves per group, to keep enough loads in flight
   if (groups < 1024) gemv_kernel<8><<<groups, 512, 0, s>>>(P);
   else gemv_kernel<4><<<groups, 256, 0, s>>>(P);
