@@ -1,17 +1,29 @@
 #!/usr/bin/env python3
 """Benchmark of the SAS hot path on one MI355X.
 
-A step is one decoder-layer forward of the 7B-shape workload (batch 1,
-1024 tokens: 576 image tokens then 448 text tokens, bf16, GATED SAS attention
-with B = 64, K = 8): RMSNorm, QKV GEMM + RoPE, block summaries, selector and
-Top-K, gated block-sparse attention, O-projection + residual, RMSNorm,
-gate/up GEMM + SwiGLU, down GEMM + residual -- all HIP kernels of libsas.so.
-Inputs are resident in HBM before the timed region.
+Headline workload: 7b_stack32_prefill2k_decode256_b8, the serving job of the
+method (Sec. 5.1, Alg. 2) on a 32-layer 7B-shape stack.  One step is one pass
+over one batch:
+  * dense prefill of 8 sequences x 2048 tokens (576 image + 1472 text)
+    through the 32 layers into 16-token pages: RMSNorm, QKV GEMM + RoPE,
+    block summaries, causal attention, O-projection + residual, RMSNorm,
+    gate/up GEMM + SwiGLU, down GEMM + residual, K/V and summaries into the
+    cache; then the LM head and greedy argmax of the first token;
+  * 256 greedy SAS decode steps (B = 64, K = 16): embedding, every layer's
+    decode step (RMSNorm, QKV + RoPE + append, Top-K selection over the
+    cached block summaries, block-sparse attention, O, MLP), LM head, argmax.
+All in the HIP kernels of libsas.so; weights and prompts resident in HBM
+before the timed region.
 
-Prints one JSON line: tokens/s per layer (value), algorithmic TFLOP/s and
-its fraction of the bf16 MFMA peak, the roofline of the dominant kernel
-(timed with HIP events on its stream over a second pass of the same steps)
-and the fp64 CPU oracle timed on the host over one layer forward.
+`value` = prefill tokens/s per layer (8 x 2048 tokens / (prefill time / 32));
+`decode` carries the decode half of the metric (algorithmic HBM bytes per
+step / step time, against 8 TB/s).  Each carries the roofline of its
+dominant kernel: the prefill's gate/up GEMM and the decode's gate/up GEMV,
+timed with HIP events recorded by the library on the kernels' stream inside
+the timed region.  `layers` times the GATED layer forward (the SAS training-
+form prefill, Eq. ours_train) of the other bf16 workloads, with the
+attention's algorithmic and executed (whole key tiles) FLOPs.
+`cpu_baseline`: the fp64 oracle on a bounded sample of the headline prefill.
 """
 import argparse
 import csv
@@ -23,59 +35,80 @@ import sys
 import time
 
 BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
-HBM_PEAK_GBS = 8000.0
+HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
 
 METRIC = "prefill tokens/s per layer + % bf16 MFMA peak; decode % HBM GB/s"
+HEADLINE = "7b_stack32_prefill2k_decode256_b8"
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-GEMM_SRC = os.path.join(HERE, "paper_2609_13141_amd", "csrc", "gemm.hip")
-TRAFFIC_FILE = os.path.join(HERE, "profiles", "gemm_gate_up_7b_layer_1k_traffic.txt")
-# the gate/up GEMM at 1024 rows: one round of 256x256 tiles, then 256x128 tiles
-DOM_KERNELS = ("gemm_bf16_lds_kernel<1, 256, 256, 2, 4, 2>", "gemm_bf16_lds_kernel<1, 256, 128, 4, 2, 3>")
+CSRC = os.path.join(HERE, "paper_2609_13141_amd", "csrc")
+PROFILES = os.path.join(HERE, "profiles")
 COPY_BYTES = 512 * 2**20  # calibration copy: reads and writes this many bytes once
+
+# Dominant kernels of the headline step and their HBM-traffic summaries
+# (written by --pmc-summary from rocprofv3 --pmc runs of --only-headline).
+DOMINANT = {
+    "prefill": {"family": "gemm_gate_up", "kernel": "gemm_bf16_lds_kernel<1, 256, 256, 2, 4, 2>",
+                "source": "gemm.hip", "file": "gemm_gate_up_7b_stack32_prefill2k_traffic.txt"},
+    "decode": {"family": "dec_gate_up", "kernel": "gemv_stream_kernel<1, 4, 32, 8, true>",
+               "source": "gemv.hip", "file": "gemv_gate_up_7b_stack32_decode_b8_traffic.txt"},
+}
+DECODE_SAMPLE = 8   # the decode GEMV is event-timed on every 8th decode step of the timed region
 
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    # about 0.1 s of layer steps timed after 25 ms of warmup: a 20-step region (12 ms) ends
-    # before the clocks have settled and measured about 12% slower per step
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--workload", default="7b_layer_1k")
+    ap.add_argument("--steps", type=int, default=5, help="timed steps (one step: prefill + 256 decode steps)")
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--only-headline", action="store_true", help="the headline workload only (profiling runs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-decode", action="store_true", help="skip the decode-step measurement")
+    ap.add_argument("--no-layers", action="store_true", help="skip the GATED layer forwards")
     ap.add_argument("--no-long-decode", action="store_true", help="skip the 64K..512K-context decode sweep")
     ap.add_argument("--no-backward", action="store_true", help="skip the training-step backward measurement")
     ap.add_argument("--no-stats", action="store_true", help="skip the selection-statistics measurement")
     ap.add_argument("--cpu-threads", type=int, default=0, help="oracle BLAS threads (0: affinity, max 16)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain device copy of %d MiB (reference for HBM counters)" % (COPY_BYTES >> 20))
+    ap.add_argument("--decode-steps", type=int, default=0,
+                    help="decode steps per step (profiling runs; default: the workload's 256)")
+    ap.add_argument("--only-layer", metavar="NAME", help="time only this workload's GATED layer forward "
+                    "(profiling runs)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
-                    help="write the gate/up GEMM traffic summary from two rocprofv3 --pmc runs and exit")
+                    help="write the dominant kernels' traffic summaries from two rocprofv3 --pmc runs and exit")
+    ap.add_argument("--trace-summary", nargs=2, metavar=("RUN_DIR", "OUT"),
+                    help="write a per-kernel table from a rocprofv3 --kernel-trace --stats run and exit")
+    ap.add_argument("--mfma-summary", nargs=2, metavar=("RUN_DIR", "OUT"),
+                    help="write per-kernel MFMA busy and clock from a rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES "
+                         "GRBM_GUI_ACTIVE SQ_BUSY_CU_CYCLES run and exit")
+    ap.add_argument("--hbm-summary", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "OUT"),
+                    help="write per-kernel HBM bytes from rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE runs of a "
+                         "command with --calibrate-copy and exit")
+    ap.add_argument("--cmd", default="", help="the profiled command, recorded in a summary")
     return ap.parse_args()
 
 
-def source_hash():
-    with open(GEMM_SRC, "rb") as f:
+# ---------------------------------------------------------------------------
+# HBM traffic of the dominant kernels from rocprofv3 counters
+
+def source_hash(name):
+    with open(os.path.join(CSRC, name), "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def pmc_per_dispatch(run_dir, counter):
-    """Per-call value of `counter` for the dominant GEMM (the sum over its
-    launches of each kernel's mean per dispatch) and the mean for the
+def pmc_means(run_dir, counter):
+    """Per-dispatch mean of `counter` for each dominant kernel and for the
     calibration copy, from a rocprofv3 --pmc csv run directory."""
     files = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
     if not files:
         raise SystemExit(f"no counter_collection.csv under {run_dir}")
-    keys = list(DOM_KERNELS) + ["copy"]
-    vals = {k: {} for k in keys}
+    vals = {k: {} for k in list(DOMINANT) + ["copy"]}
     for f in files:
         for r in csv.DictReader(open(f)):
             if r["Counter_Name"] != counter:
                 continue
             name = r["Kernel_Name"]
-            key = next((k for k in DOM_KERNELS if k in name), None)
+            key = next((k for k, d in DOMINANT.items() if d["kernel"] in name), None)
             if key is None and "copy" in name.lower():
                 key = "copy"
             if key:
@@ -88,238 +121,383 @@ def pmc_per_dispatch(run_dir, counter):
         v = sorted(d.values())
         if k == "copy":
             v = v[-2:]  # the two calibration copies are by far the largest copy dispatches
-        out[k] = sum(v) / len(v)
-    out["gemm"] = sum(out[k] for k in DOM_KERNELS)
+        out[k] = (sum(v) / len(v), len(v))
     return out
 
 
-def write_traffic_summary(fetch_dir, write_dir):
-    """HBM traffic per launch of the gate/up GEMM: FETCH_SIZE and WRITE_SIZE
+def write_traffic_summaries(fetch_dir, write_dir):
+    """HBM bytes per launch of each dominant kernel: FETCH_SIZE and WRITE_SIZE
     (KiB per dispatch) scaled by what they read for a copy of known size."""
-    fe = pmc_per_dispatch(fetch_dir, "FETCH_SIZE")
-    wr = pmc_per_dispatch(write_dir, "WRITE_SIZE")
-    f_fetch = COPY_BYTES / (fe["copy"] * 1024.0)
-    f_write = COPY_BYTES / (wr["copy"] * 1024.0)
-    fetch_b = fe["gemm"] * 1024.0 * f_fetch
-    write_b = wr["gemm"] * 1024.0 * f_write
-    lines = [
-        "# HBM traffic of the gate/up GEMM (7b_layer_1k, 1024 x 4096 x 2*11008) per launch",
-        f"# kernels (summed per call): {', '.join(DOM_KERNELS)}",
-        "# rocprofv3 --pmc FETCH_SIZE (then WRITE_SIZE) -- python3 bench.py --no-decode --no-cpu-baseline "
-        "--steps 5 --warmup 2 --calibrate-copy",
-        f"# calibration: plain copy of {COPY_BYTES} bytes read {fe['copy']:.0f} KiB fetch, {wr['copy']:.0f} KiB write",
-        f"source_sha={source_hash()}",
-        f"fetch_kib_raw={fe['gemm']:.1f}",
-        f"write_kib_raw={wr['gemm']:.1f}",
-        f"fetch_factor={f_fetch:.4f}",
-        f"write_factor={f_write:.4f}",
-        f"fetch_bytes={fetch_b:.0f}",
-        f"write_bytes={write_b:.0f}",
-        f"traffic_bytes={fetch_b + write_b:.0f}",
-    ]
-    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
-    with open(TRAFFIC_FILE, "w") as f:
-        f.write("\n".join(lines) + "\n")
+    fe = pmc_means(fetch_dir, "FETCH_SIZE")
+    wr = pmc_means(write_dir, "WRITE_SIZE")
+    f_fetch = COPY_BYTES / (fe["copy"][0] * 1024.0)
+    f_write = COPY_BYTES / (wr["copy"][0] * 1024.0)
+    for key, d in DOMINANT.items():
+        fetch_b = fe[key][0] * 1024.0 * f_fetch
+        write_b = wr[key][0] * 1024.0 * f_write
+        lines = [
+            f"# HBM traffic per launch of the {key} dominant kernel of {HEADLINE} ({d['family']})",
+            f"# kernel: {d['kernel']} ({fe[key][1]} dispatches averaged)",
+            "# cd /tmp && export TMPDIR=/tmp && cd <repo> && rocprofv3 --pmc FETCH_SIZE (then WRITE_SIZE) -d <dir> "
+            "--output-format csv -- python3 bench.py --only-headline --no-cpu-baseline --steps 1 --warmup 0 "
+            "--decode-steps 8 --calibrate-copy",
+            f"# calibration: a plain copy of {COPY_BYTES} bytes reads {fe['copy'][0]:.0f} KiB FETCH_SIZE and "
+            f"{wr['copy'][0]:.0f} KiB WRITE_SIZE",
+            f"source={d['source']}",
+            f"source_sha={source_hash(d['source'])}",
+            f"fetch_kib_raw={fe[key][0]:.1f}",
+            f"write_kib_raw={wr[key][0]:.1f}",
+            f"fetch_factor={f_fetch:.4f}",
+            f"write_factor={f_write:.4f}",
+            f"fetch_bytes={fetch_b:.0f}",
+            f"write_bytes={write_b:.0f}",
+            f"traffic_bytes={fetch_b + write_b:.0f}",
+        ]
+        with open(os.path.join(PROFILES, d["file"]), "w") as f:
+            f.write("\n".join(lines) + "\n")
+        print("\n".join(lines))
+
+
+def short_name(name):
+    """Kernel name without the namespace, return type and parameter list."""
+    n = name.strip('"')
+    for pre in ("void ", "sas::"):
+        if n.startswith(pre):
+            n = n[len(pre):]
+    depth = 0
+    for i, ch in enumerate(n):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            return n[:i]
+    return n
+
+
+def _csv(run_dir, suffix):
+    files = sorted(glob.glob(os.path.join(run_dir, "**", "*" + suffix), recursive=True))
+    if not files:
+        raise SystemExit(f"no *{suffix} under {run_dir}")
+    rows = []
+    for f in files:
+        rows += list(csv.DictReader(open(f)))
+    return rows
+
+
+def _summary_head(title, cmd):
+    return [f"# {title}", "", "Command (from the repository root, after `cd /tmp && export TMPDIR=/tmp`):", "",
+            "```", cmd or "(not recorded)", "```", ""]
+
+
+def write_trace_summary(run_dir, out, cmd, top=40):
+    """Per-kernel calls and durations from rocprofv3 --stats (kernel_stats.csv)."""
+    rows = _csv(run_dir, "kernel_stats.csv")
+    rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    tot = sum(float(r["TotalDurationNs"]) for r in rows)
+    lines = _summary_head("rocprofv3 --kernel-trace --stats: kernel durations", cmd)
+    lines += ["| kernel | calls | avg us | min us | max us | total ms | share |", "|---|---:|---:|---:|---:|---:|---:|"]
+    for r in rows[:top]:
+        lines.append(f"| `{short_name(r['Name'])}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                     f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
+                     f"{float(r['TotalDurationNs']) / 1e6:.3f} | {float(r['TotalDurationNs']) / tot:.1%} |")
+    if len(rows) > top:
+        rest = sum(float(r["TotalDurationNs"]) for r in rows[top:])
+        lines.append(f"| ({len(rows) - top} more kernels) | | | | | {rest / 1e6:.3f} | {rest / tot:.1%} |")
+    open(out, "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
 
-def measured_traffic():
-    """Traffic per launch from the committed counter summary, or None if the
-    GEMM source changed since the counters were taken."""
+def _counter_means(run_dir, peak=False):
+    """{kernel: {counter: mean per dispatch}} (with peak: the largest
+    dispatch's value), dispatch counts and mean durations (ns)."""
+    vals, disp, dur = {}, {}, {}
+    for r in _csv(run_dir, "counter_collection.csv"):
+        k = short_name(r["Kernel_Name"])
+        d = vals.setdefault(k, {}).setdefault(r["Counter_Name"], {})
+        d[r["Dispatch_Id"]] = d.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+        disp.setdefault(k, set()).add(r["Dispatch_Id"])
+        if r.get("Start_Timestamp") and r.get("End_Timestamp"):
+            dur.setdefault(k, {})[r["Dispatch_Id"]] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+    agg = (lambda d: max(d.values())) if peak else (lambda d: sum(d.values()) / len(d))
+    means = {k: {c: agg(d) for c, d in cs.items()} for k, cs in vals.items()}
+    return means, {k: len(v) for k, v in disp.items()}, {k: sum(v.values()) / len(v) for k, v in dur.items()}
+
+
+N_SIMD = 1024   # 256 compute units x 4 SIMDs
+N_XCD = 8
+
+
+def write_mfma_summary(run_dir, out, cmd, min_busy=1e6):
+    """MFMA busy fraction and shader clock per kernel.  GRBM_GUI_ACTIVE is
+    summed over the 8 XCDs (per-XCD cycles = value / 8) and
+    SQ_VALU_MFMA_BUSY_CYCLES over all SIMDs, so busy = MFMA / (1024 x
+    GUI / 8); the clock is the per-XCD cycles over the dispatch duration."""
+    means, n, dur = _counter_means(run_dir)
+    lines = _summary_head("rocprofv3 --pmc: MFMA busy and clock per kernel", cmd)
+    lines += ["MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x GRBM_GUI_ACTIVE / 8 XCDs); "
+              "clock = (GRBM_GUI_ACTIVE / 8) / duration.", "",
+              "| kernel | dispatches | avg us | clock GHz | MFMA busy | CU busy |", "|---|---:|---:|---:|---:|---:|"]
+    rows = [(k, m) for k, m in means.items() if m.get("SQ_VALU_MFMA_BUSY_CYCLES", 0) >= min_busy]
+    rows.sort(key=lambda km: -km[1].get("SQ_VALU_MFMA_BUSY_CYCLES", 0) * n[km[0]])
+    for k, m in rows:
+        gui = m.get("GRBM_GUI_ACTIVE", 0.0) / N_XCD
+        busy = m["SQ_VALU_MFMA_BUSY_CYCLES"] / (N_SIMD * gui) if gui else float("nan")
+        cu = m.get("SQ_BUSY_CU_CYCLES", 0.0) / (256 * gui) if gui else float("nan")
+        us = dur.get(k, 0.0) / 1e3
+        ghz = gui / (us * 1e3) if us else float("nan")
+        lines.append(f"| `{k}` | {n[k]} | {us:.1f} | {ghz:.2f} | {busy:.1%} | {cu:.1%} |")
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def write_hbm_summary(fetch_dir, write_dir, out, cmd, min_kib=64.0):
+    """HBM bytes per dispatch per kernel: FETCH_SIZE and WRITE_SIZE (KiB)
+    scaled by what they read for the plain copy of COPY_BYTES."""
+    fe, nf, dur = _counter_means(fetch_dir)
+    wr, _, _ = _counter_means(write_dir)
+    # the calibration copy: the largest dispatch of a copy kernel
+    cpf, cpw = _counter_means(fetch_dir, peak=True)[0], _counter_means(write_dir, peak=True)[0]
+    copies = [k for k in fe if "copy" in k.lower()]
+    cf = max((cpf[k]["FETCH_SIZE"] for k in copies), default=0.0)
+    cw = max((cpw[k]["WRITE_SIZE"] for k in copies if k in cpw), default=0.0)
+    if not cf or not cw:
+        raise SystemExit("no calibration copy found (run the command with --calibrate-copy)")
+    ff, fw = COPY_BYTES / (cf * 1024.0), COPY_BYTES / (cw * 1024.0)
+    lines = _summary_head("rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE: HBM bytes per dispatch", cmd)
+    lines += [f"Calibration: a plain copy of {COPY_BYTES} bytes reads FETCH_SIZE {cf:.0f} KiB and WRITE_SIZE "
+              f"{cw:.0f} KiB, so the factors are {ff:.4f} (fetch) and {fw:.4f} (write).  The duration is that "
+              "of the FETCH_SIZE run (counters serialise the dispatches).", "",
+              "| kernel | dispatches | avg us | fetch MB | write MB | HBM MB | GB/s |", "|---|---:|---:|---:|---:|---:|---:|"]
+    rows = [k for k in fe if k not in copies and fe[k].get("FETCH_SIZE", 0) >= min_kib]
+    rows.sort(key=lambda k: -fe[k]["FETCH_SIZE"] * nf[k])
+    for k in rows:
+        fb = fe[k]["FETCH_SIZE"] * 1024.0 * ff
+        wb = wr.get(k, {}).get("WRITE_SIZE", 0.0) * 1024.0 * fw
+        us = dur.get(k, 0.0) / 1e3
+        gbs = (fb + wb) / (us * 1e3) if us else float("nan")
+        lines.append(f"| `{k}` | {nf[k]} | {us:.1f} | {fb / 1e6:.1f} | {wb / 1e6:.1f} | {(fb + wb) / 1e6:.1f} | "
+                     f"{gbs:.0f} |")
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def stored_traffic(key):
+    """HBM bytes per launch from the committed counter summary, or None when
+    the kernel's source changed since the counters were taken."""
+    d = DOMINANT[key]
     try:
-        kv = dict(l.strip().split("=", 1) for l in open(TRAFFIC_FILE) if "=" in l and not l.startswith("#"))
+        kv = dict(l.strip().split("=", 1) for l in open(os.path.join(PROFILES, d["file"]))
+                  if "=" in l and not l.startswith("#"))
     except OSError:
         return None
-    if kv.get("source_sha") != source_hash():
+    if kv.get("source_sha") != source_hash(d["source"]):
         return None
     return int(float(kv["traffic_bytes"]))
 
 
-def main():
-    args = parse()
-    if args.pmc_summary:
-        write_traffic_summary(*args.pmc_summary)
-        return
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the SAS hot path here is single-GPU "
-              "(run with --gpus 1)", file=sys.stderr)
-        sys.exit(2)
-    cores = args.cpu_threads or min(16, len(os.sched_getaffinity(0)))
-    for var in ("OPENBLAS_NUM_THREADS", "OMP_NUM_THREADS", "MKL_NUM_THREADS"):
-        os.environ[var] = str(cores)
+# ---------------------------------------------------------------------------
 
-    import numpy as np
-    import torch
-
-    here = os.path.dirname(os.path.abspath(__file__))
-    sys.path.insert(0, here)
-    from paper_2609_13141_amd import configs, inputs, sas
-
-    w = configs.BY_NAME[args.workload]
-    dev = "cuda:0"
-    torch.cuda.set_device(0)
-    x_np = inputs.embeddings(w)
-    W_np = inputs.layer_weights(w)
-    x = sas.to_device(x_np, w.dtype, dev)
-    W = sas.weights_to_device(W_np, w.dtype, dev)
-    cfg = sas.make_config(w)
-    ws = sas.Workspace(dev)
-
-    def step():
-        return sas.layer_forward(cfg, x, W, stats=False, ws=ws)["y"]
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms = (t1 - t0) * 1e3 / args.steps
-    T = w.tokens
-    tok_s = T / (ms * 1e-3)
-    flops = w.prefill_flops()
-    tflops = flops / (ms * 1e-3) / 1e12
-
-    # second pass of the same steps with an event pair around every kernel
-    sas.profiler_start(64 * args.steps + 64)
-    for _ in range(args.steps):
-        step()
-    recs = sas.profiler_stop()
-    if args.calibrate_copy:
-        src = torch.empty(COPY_BYTES // 2, dtype=torch.bfloat16, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(2):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+def family_means(recs):
     fam = {}
     for name, t in recs:
         fam.setdefault(name, []).append(t)
-    kern_ms = {k: sum(v) / len(v) for k, v in fam.items()}
-    kern_calls = {k: len(v) // args.steps for k, v in fam.items()}
-    # dominant kernel: the gate/up GEMM (2 * T * d * 2 * d_ff algorithmic flops per launch)
-    dom = "gemm_gate_up"
-    dom_flops = 2.0 * T * w.d_model * 2 * w.d_ff
-    dom_tf = dom_flops / (kern_ms[dom] * 1e-3) / 1e12
-
-    line = {
-        "metric": METRIC,
-        "value": round(tok_s, 1),
-        "unit": "tokens/s/layer",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms, 4),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16" if w.dtype == "bf16" else "f32",
-        "data": "synthetic (seeded N(0,1) text / N(0,1)*2 image embeddings, N(0,0.02) weights)",
-        "config": {"workload": w.name, "batch": w.batch, "seq_len": w.seq_len, "d_model": w.d_model,
-                   "n_heads": w.n_heads, "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
-                   "d_ff": w.d_ff, "mode": w.mode, "block_size": w.block_size, "top_k": w.top_k},
-        "alg_tflops": round(tflops, 2),
-        "mfma_frac": round(tflops / BF16_PEAK_TFLOPS, 4),
-        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(dom_tf, 2),
-                     "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(dom_tf / BF16_PEAK_TFLOPS, 4),
-                     "traffic": measured_traffic(), "alg_gflop_per_launch": round(dom_flops / 1e9, 3),
-                     "avg_ms": round(kern_ms[dom], 4)},
-        "kernels_ms": {k: round(v, 4) for k, v in sorted(kern_ms.items(), key=lambda kv: -kv[1] * kern_calls[kv[0]])},
-    }
-
-    if not args.no_decode:
-        del x, W, ws
-        torch.cuda.empty_cache()
-        line["decode"] = decode_bench(DECODE_WARMUP)
-        torch.cuda.empty_cache()
-    if not args.no_long_decode:
-        line["decode_long"] = decode_long_bench()
-        torch.cuda.empty_cache()
-    if not args.no_backward:
-        line["backward"] = backward_bench()
-        torch.cuda.empty_cache()
-    if not args.no_stats:
-        line["stats"] = stats_bench()
-        torch.cuda.empty_cache()
-    if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, x_np, W_np, cores)
-    print(json.dumps(line), flush=True)
+    return {k: sum(v) / len(v) for k, v in fam.items()}, {k: len(v) for k, v in fam.items()}
 
 
-# untimed decode steps before the 256 timed ones (fixes the positions 2053..2308)
-DECODE_WARMUP = 5
-
-
-def decode_bench(warmup):
-    """The serving workload of the paper's method (Sec. 5.1, Alg. 2): a
-    32-layer 7B-shape stack, 8 sequences of 576 image + 1472 text tokens
-    prefilled densely into 16-token pages, then greedy SAS decode steps
-    (B = 64, K = 16): every step embeds the 8 new tokens, runs the decode step
-    of each layer (Top-K blocks per KV group, attention to them plus the
-    current block) and the LM head with greedy argmax.  `warmup` untimed
-    steps, then the workload's 256 timed steps; weights and inputs resident
-    in HBM (13 GB of weights per step defeat the 256 MB last-level cache)."""
-    import torch
-    from paper_2609_13141_amd import configs, inputs, model, sas
-    w = configs.STACK_DECODE
-    dev = "cuda:0"
-    layers = [inputs.layer_weights_device(w, layer=l, device=dev) for l in range(w.n_layers)]
-    ends = inputs.model_ends_device(w, device=dev)
-    steps = w.decode_steps
-    max_len = w.seq_len + warmup + steps + 8
-    st = model.Stack(w, layers, ends, max_len=max_len, device=dev)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    tok = st.prefill(ends["token_ids"], ends["img_embed"])
-    torch.cuda.synchronize()
-    prefill_ms = (time.perf_counter() - t0) * 1e3
-    pos_all = st.positions(warmup + steps + 4)
-    for p in pos_all[:warmup]:
-        tok, _, _ = st.step(tok, p)
-    torch.cuda.synchronize()
-    t_first = st.pos
-    t0 = time.perf_counter()
-    for p in pos_all[warmup:warmup + steps]:
-        tok, _, _ = st.step(tok, p)
-    torch.cuda.synchronize()
-    ms = (time.perf_counter() - t0) * 1e3 / steps
-    # algorithmic bytes of one step: every layer's weights, kept K/V and
-    # summaries read, the new K/V written; the embedding rows and LM head
-    B, K, dh, Hkv, b, L = w.block_size, w.top_k, w.head_dim, w.n_kv_heads, w.batch, w.n_layers
+def decode_bytes(w, t_first, steps, batch=None):
+    """Algorithmic HBM bytes of `steps` decode steps of the stack starting at
+    position t_first: every layer's weights, the kept K/V (current block +
+    min(K, C_t) blocks), the summaries scored, the appended K/V; the LM head
+    and the embedding rows."""
+    B, K, dh, Hkv, L = w.block_size, w.top_k, w.head_dim, w.n_kv_heads, w.n_layers
+    b = batch or w.batch
     tot = 0.0
     for t in range(t_first, t_first + steps):
         ct = t // B
         kept = B * min(K, ct) + (t % B) + 1
         per_layer = 2.0 * w.linear_params() + b * Hkv * (kept * dh * 2 * 2 + ct * dh * 2 + 2 * dh * 2)
         tot += L * per_layer + 2.0 * w.vocab * w.d_model + b * w.d_model * 2
-    nbytes = tot / steps
-    # per-kernel view over a few more steps, with an event pair around every launch
-    nprof = 3
-    sas.profiler_start(64 * L * nprof + 256)
-    for p in pos_all[warmup + steps:warmup + steps + nprof]:
+    return tot
+
+
+def headline(args):
+    """The serving job: timed steps of (prefill + 256 decode steps)."""
+    import torch
+    from paper_2609_13141_amd import configs, inputs, model, sas
+    w = configs.BY_NAME[HEADLINE]
+    dev = "cuda:0"
+    L, T, nd = w.n_layers, w.tokens, args.decode_steps or w.decode_steps
+    layers = [inputs.layer_weights_device(w, layer=l, device=dev) for l in range(L)]
+    ends = inputs.model_ends_device(w, device=dev)
+    st = model.Stack(w, layers, ends, max_len=w.seq_len + nd + 8, device=dev)
+    # the decode positions 2048 .. 2303 of every step
+    positions = [torch.full((w.batch,), w.seq_len + s, dtype=torch.int32, device=dev) for s in range(nd)]
+
+    def one_step(dec_sample=0):
+        """Prefill then the decode steps; returns the events bracketing the prefill."""
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        if dec_sample:
+            sas.profiler_select([DOMINANT["prefill"]["family"]])
+        e0.record()
+        tok = st.prefill(ends["token_ids"], ends["img_embed"])
+        e1.record()
+        for s, p in enumerate(positions):
+            if dec_sample:
+                sas.profiler_select([DOMINANT["decode"]["family"]] if s % dec_sample == 0 else [])
+            tok, _, _ = st.step(tok, p)
+        return e0, e1
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    per_step = L + L * ((nd + DECODE_SAMPLE - 1) // DECODE_SAMPLE) + 8
+    sas.profiler_start(per_step * args.steps + 64)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    evs = [one_step(DECODE_SAMPLE) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    recs = sas.profiler_stop()
+    sas.profiler_select(None)
+    ms = (t1 - t0) * 1e3 / args.steps
+    pre_ms = sum(a.elapsed_time(b) for a, b in evs) / args.steps
+    dec_ms = (ms - pre_ms) / nd
+    kms, kcnt = family_means(recs)
+
+    # prefill: value and the gate/up GEMM's roofline
+    tok_s_layer = T / (pre_ms * 1e-3 / L)
+    pre_flops = w.prefill_flops("dense")
+    pre_tf = pre_flops / (pre_ms * 1e-3 / L) / 1e12
+    gu = DOMINANT["prefill"]["family"]
+    gu_flops = 2.0 * T * w.d_model * 2 * w.d_ff
+    gu_tf = gu_flops / (kms[gu] * 1e-3) / 1e12
+    # decode: HBM bytes and the gate/up GEMV's roofline (weights + activations in, activations out)
+    nbytes = decode_bytes(w, w.seq_len, nd) / nd
+    dgu = DOMINANT["decode"]["family"]
+    dgu_bytes = 2.0 * w.d_model * 2 * w.d_ff + w.batch * (w.d_model + w.d_ff) * 2
+    dgu_gbs = dgu_bytes / (kms[dgu] * 1e-3) / 1e9
+    att_alg = 4.0 * w.head_dim * w.n_heads * w.batch * w.attended_pairs("dense")
+    nq = -(-w.seq_len // 128)
+    att_exec = sum(4.0 * w.head_dim * 128 * 64 * min(2 * q + 2, -(-w.seq_len // 64)) for q in range(nq)) \
+        * w.n_heads * w.batch
+
+    # per-kernel view: one more step with every launch timed (not part of the timed region)
+    sas.profiler_start(64 * L * 4 + 256)
+    tok = st.prefill(ends["token_ids"], ends["img_embed"])
+    for p in positions[:4]:
         tok, _, _ = st.step(tok, p)
     recs = sas.profiler_stop()
-    fam = {}
-    for name, v in recs:
-        fam.setdefault(name, []).append(v)
-    kms = {k: sum(v) / len(v) for k, v in fam.items()}
-    gu_bytes = 2.0 * w.d_model * 2 * w.d_ff
-    return {"workload": f"{w.name}: {L} layers, batch {b}, prompt {w.seq_len} tokens (576 image + 1472 text), "
-                        f"pages of {w.page_size}, B={B}, K={K}, greedy steps at positions {t_first}.."
-                        f"{t_first + steps - 1}",
-            "steps": steps, "warmup": warmup,
-            "ms_per_step": round(ms, 4),
-            "tokens_per_s": round(b / (ms * 1e-3), 1),
-            "ms_per_layer_step": round(ms / L, 4),
+    kall, kall_n = family_means(recs)
+    out = {
+        "value": round(tok_s_layer, 1),
+        "ms_per_step": round(ms, 3),
+        "prefill_ms_per_step": round(pre_ms, 3),
+        "prefill_ms_per_layer": round(pre_ms / L, 4),
+        "alg_tflops": round(pre_tf, 1),
+        "mfma_frac": round(pre_tf / BF16_PEAK_TFLOPS, 4),
+        "attention": {"alg_gflop_per_layer": round(att_alg / 1e9, 2), "executed_gflop_per_layer": round(att_exec / 1e9, 2),
+                      "ms_per_layer": round(kall.get("attention", 0.0), 4),
+                      "alg_tflops": round(att_alg / (kall.get("attention", 1e9) * 1e-3) / 1e12, 1),
+                      "executed_tflops": round(att_exec / (kall.get("attention", 1e9) * 1e-3) / 1e12, 1)},
+        "roofline": {"bound": "mfma", "kernel": gu, "achieved": round(gu_tf, 1), "peak": BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(gu_tf / BF16_PEAK_TFLOPS, 4), "traffic": stored_traffic("prefill"),
+                     "traffic_source": "profiles/" + DOMINANT["prefill"]["file"],
+                     "alg_gflop_per_launch": round(gu_flops / 1e9, 1), "avg_ms": round(kms[gu], 4),
+                     "launches_timed": kcnt[gu]},
+        "decode": {
+            "workload": f"{w.name}: {L} layers, batch {w.batch}, positions {w.seq_len}..{w.seq_len + nd - 1} "
+                        f"after the prompt, pages of {w.page_size}, B={w.block_size}, K={w.top_k}, greedy",
+            "steps_per_step": nd,
+            "ms_per_step": round(dec_ms, 4),
+            "tokens_per_s": round(w.batch / (dec_ms * 1e-3), 1),
+            "ms_per_layer_step": round(dec_ms / L, 4),
             "bytes_per_step": int(nbytes),
-            "hbm_gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
-            "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-            "prefill_ms": round(prefill_ms, 2),
-            "prefill_tokens_per_s_per_layer": round(w.tokens / (prefill_ms * 1e-3 / L), 1),
-            "gate_up_gemv_gbs": round(gu_bytes / (kms["dec_gate_up"] * 1e-3) / 1e9, 1),
-            "kernels_ms": {k: round(v, 4) for k, v in sorted(kms.items(), key=lambda kv: -kv[1])}}
+            "hbm_gbs": round(nbytes / (dec_ms * 1e-3) / 1e9, 1),
+            "hbm_frac": round(nbytes / (dec_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "roofline": {"bound": "hbm", "kernel": dgu, "achieved": round(dgu_gbs, 1), "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": round(dgu_gbs / HBM_PEAK_GBS, 4),
+                         "traffic": stored_traffic("decode"),
+                         "traffic_source": "profiles/" + DOMINANT["decode"]["file"],
+                         "alg_bytes_per_launch": int(dgu_bytes), "avg_ms": round(kms[dgu], 4),
+                         "launches_timed": kcnt[dgu]},
+        },
+        "kernels_ms": {k: round(v, 4) for k, v in sorted(kall.items(), key=lambda kv: -kv[1] * kall_n[kv[0]])},
+        "kernel_calls": kall_n,
+    }
+    del st, layers
+    return w, ends, out
+
+
+def attention_executed_flops(w, sel):
+    """MFMA work the attention kernel executes: every (128-query tile, head)
+    job multiplies whole 64-key tiles, those holding any key one of its
+    queries attends (the selected blocks of any of the tile's queries and
+    the current blocks up to the tile's last query).  sel [b, Hkv, n, K]."""
+    import numpy as np
+    b, Hkv, n, K = sel.shape
+    B, G, dh = w.block_size, w.n_heads // w.n_kv_heads, w.head_dim
+    tiles = 0
+    for q0 in range(0, n, 128):
+        q1 = min(n, q0 + 128)
+        rows = sel[:, :, q0:q1, :].reshape(b, Hkv, -1)
+        for bi in range(b):
+            for g in range(Hkv):
+                blk = np.unique(rows[bi, g])
+                blk = blk[blk >= 0]
+                keys = set()
+                for m in blk.tolist():
+                    keys.update(range(m * B // 64, ((m + 1) * B - 1) // 64 + 1))
+                keys.update(range((q0 // B) * B // 64, (q1 - 1) // 64 + 1))   # current blocks (causal)
+                tiles += len(keys)
+    return 4.0 * dh * 128 * 64 * tiles * G
+
+
+def layer_bench(name, steps=30, warmup=10):
+    """One GATED layer forward (RMSNorm, QKV + RoPE, summaries, selector and
+    Top-K, gated block-sparse attention, O + residual, MLP) of a workload."""
+    import numpy as np
+    import torch
+    from paper_2609_13141_amd import configs, inputs, sas
+    w = configs.BY_NAME[name]
+    dev = "cuda:0"
+    x = sas.to_device(inputs.embeddings(w), "bf16", dev)
+    W = inputs.layer_weights_device(w, device=dev)
+    cfg = sas.make_config(w)
+    ws = sas.Workspace(dev)
+
+    def run():
+        return sas.layer_forward(cfg, x, W, stats=False, ws=ws)
+    for _ in range(warmup):
+        run()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        run()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    sas.profiler_start(64 * 5 + 64)
+    for _ in range(5):
+        run()
+    recs = sas.profiler_stop()
+    kms, kn = family_means(recs)
+    sel = sas.layer_forward(cfg, x, W, stats=True, lse=False, sel_idx=True, ws=ws)["sel_idx"].cpu().numpy()
+    flops = w.prefill_flops()
+    att_alg = 4.0 * w.head_dim * w.n_heads * w.batch * w.attended_pairs()
+    att_exec = attention_executed_flops(w, sel)
+    att_ms = kms["attention"]
+    tf = flops / (ms * 1e-3) / 1e12
+    del x, W, ws
+    return {"workload": f"{w.name}: batch {w.batch}, {w.seq_len} tokens, {w.n_heads}/{w.n_kv_heads} heads, "
+                        f"d={w.d_model}, d_ff={w.d_ff}, B={w.block_size}, K={w.top_k}, GATED",
+            "ms_per_layer": round(ms, 4), "tokens_per_s": round(w.tokens / (ms * 1e-3), 1),
+            "alg_gflop": round(flops / 1e9, 1), "alg_tflops": round(tf, 1),
+            "mfma_frac": round(tf / BF16_PEAK_TFLOPS, 4),
+            "attention": {"alg_gflop": round(att_alg / 1e9, 2), "executed_gflop": round(att_exec / 1e9, 2),
+                          "ms": round(att_ms, 4), "alg_tflops": round(att_alg / (att_ms * 1e-3) / 1e12, 1),
+                          "executed_tflops": round(att_exec / (att_ms * 1e-3) / 1e12, 1),
+                          "executed_frac": round(att_exec / (att_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4)},
+            "kernels_ms": {k: round(v, 4) for k, v in sorted(kms.items(), key=lambda kv: -kv[1] * kn[kv[0]])}}
 
 
 def decode_long_bench(steps=60, warmup=20):
@@ -361,10 +539,7 @@ def decode_long_bench(steps=60, warmup=20):
             for s in range(warmup + steps, warmup + steps + 3):
                 sas.decode_step(cfg, x, poss[s % len(poss)], Wd, cache, sel_idx=False, ws=ws)
             recs = sas.profiler_stop()
-            fam = {}
-            for name, v in recs:
-                fam.setdefault(name, []).append(v)
-            kms = {k: sum(v) / len(v) for k, v in fam.items()}
+            kms, _ = family_means(recs)
             B, K, dh, Hkv = w.block_size, w.top_k, w.head_dim, w.n_kv_heads
             tot = 0.0
             for s in range(warmup, warmup + steps):
@@ -428,10 +603,7 @@ def backward_bench(steps=10, warmup=3):
             bwd()
             sas.attention_prefill(cfg, q, k, v, log_gate=True, ws=ws_f)
         recs = sas.profiler_stop()
-        fam = {}
-        for nm, t in recs:
-            fam.setdefault(nm, []).append(t)
-        kms = {kk: sum(vv) / len(vv) for kk, vv in fam.items()}
+        kms, _ = family_means(recs)
         flops = 10.0 * dh * H * b * w.attended_pairs()
         att_ms = kms["attention_bwd"]
         tf = flops / (att_ms * 1e-3) / 1e12
@@ -486,10 +658,7 @@ def stats_bench(steps=10, warmup=3):
     for _ in range(steps):
         run()
     recs = sas.profiler_stop()
-    fam = {}
-    for nm, t in recs:
-        fam.setdefault(nm, []).append(t)
-    kms = {kk: sum(vv) / len(vv) for kk, vv in fam.items()}
+    kms, _ = family_means(recs)
     flops = 2.0 * dh * H * b * n * (n + 1) / 2
     inter, tot, rec = sas.overlap_recall(su, ru)
     return {"workload": f"{w.name}: batch {b}, {n} tokens, {H}/{Hkv} heads, dh {dh}, B={w.block_size}, K={w.top_k}",
@@ -499,27 +668,119 @@ def stats_bench(steps=10, warmup=3):
             "kernels_ms": {kk: round(vv, 4) for kk, vv in sorted(kms.items(), key=lambda kv: -kv[1])}}
 
 
-def cpu_baseline(w, x_np, W_np, cores):
-    """The fp64 oracle, as it stands, over one full layer forward of the same
-    workload on the host cores."""
+def cpu_baseline(w, ends, cores, n_layers=8):
+    """The fp64 oracle, as it stands, on a bounded sample of the headline
+    prefill: the first `n_layers` DENSE layers of one 2048-token sequence,
+    with the stack's own weights copied to the host."""
     import numpy as np
+    import torch
 
     import oracle
     from oracle.layer import Spec
+    from paper_2609_13141_amd import inputs
     try:
         from threadpoolctl import threadpool_info
         used = max([p.get("num_threads", 1) for p in threadpool_info()] or [cores])
     except Exception:
         used = cores
-    spec = Spec(w.n_heads, w.n_kv_heads, w.head_dim, w.block_size, w.top_k, w.mode, w.dtype, w.rope_base,
+    spec = Spec(w.n_heads, w.n_kv_heads, w.head_dim, w.block_size, w.top_k, "dense", w.dtype, w.rope_base,
                 w.rms_eps)
-    x = x_np.astype(np.float64)
-    Wd = {k: (None if a is None else a.astype(np.float64)) for k, a in W_np.items()}
+    ids = ends["token_ids"][:1].cpu().numpy()
+    n_img = int((ids < 0).sum())
+    table = ends["embed"].float().cpu().numpy()
+    x = oracle.embed_tokens(ids, table, ends["img_embed"][:1, :n_img].float().cpu().numpy())[0]
+    del table
+    Ws = []
+    for l in range(n_layers):
+        Wd = inputs.layer_weights_device(w, layer=l, device="cuda:0")
+        Ws.append({k: (None if v is None else v.float().cpu().numpy().astype(np.float64)) for k, v in Wd.items()})
+        del Wd
+    torch.cuda.empty_cache()
     t0 = time.perf_counter()
-    oracle.layer_forward(x, Wd, spec)
+    for l in range(n_layers):
+        x = oracle.dense_prefill_layer(x, Ws[l], spec)["y"]
     dt = time.perf_counter() - t0
-    return {"value": round(w.tokens / dt, 2), "unit": "tokens/s/layer", "cores": int(used), "kind": "oracle",
-            "sample": f"one full layer forward of {w.name} ({w.tokens} tokens), fp64 NumPy, {dt:.2f} s"}
+    return {"value": round(w.seq_len * n_layers / dt, 2), "unit": "tokens/s/layer", "cores": int(used),
+            "kind": "oracle",
+            "sample": f"the first {n_layers} DENSE prefill layers of one {w.seq_len}-token sequence of {w.name} "
+                      f"(every row), fp64 NumPy, {dt:.2f} s"}
+
+
+def main():
+    args = parse()
+    if args.pmc_summary:
+        write_traffic_summaries(*args.pmc_summary)
+        return
+    if args.trace_summary:
+        write_trace_summary(*args.trace_summary, args.cmd)
+        return
+    if args.mfma_summary:
+        write_mfma_summary(*args.mfma_summary, args.cmd)
+        return
+    if args.hbm_summary:
+        write_hbm_summary(*args.hbm_summary, args.cmd)
+        return
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the SAS hot path here is single-GPU "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    cores = args.cpu_threads or min(16, len(os.sched_getaffinity(0)))
+    for var in ("OPENBLAS_NUM_THREADS", "OMP_NUM_THREADS", "MKL_NUM_THREADS"):
+        os.environ[var] = str(cores)
+
+    import torch
+
+    sys.path.insert(0, HERE)
+    torch.cuda.set_device(0)
+    if args.only_layer:
+        print(json.dumps({"layer": layer_bench(args.only_layer)}), flush=True)
+        return
+    w, ends, head = headline(args)
+    line = {
+        "metric": METRIC,
+        "value": head.pop("value"),
+        "unit": "tokens/s/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head.pop("ms_per_step"),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded prompt ids + N(0,1)*2 image embeddings, N(0,1) embedding table, N(0,0.02) "
+                "weights drawn on the GPU)",
+        "config": {"workload": w.name, "batch": w.batch, "seq_len": w.seq_len, "n_layers": w.n_layers,
+                   "decode_steps": args.decode_steps or w.decode_steps, "d_model": w.d_model, "n_heads": w.n_heads,
+                   "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim, "d_ff": w.d_ff, "vocab": w.vocab,
+                   "prefill_mode": "dense", "decode_mode": "sparse", "block_size": w.block_size,
+                   "top_k": w.top_k, "page_size": w.page_size},
+    }
+    line.update(head)
+    if args.calibrate_copy:
+        src = torch.empty(COPY_BYTES // 2, dtype=torch.bfloat16, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    torch.cuda.empty_cache()
+    if not args.only_headline:
+        if not args.no_layers:
+            line["layers"] = [layer_bench(nm) for nm in ("7b_layer_1k", "7b_layer_4k_b4", "gqa28x4_layer_16k")]
+            torch.cuda.empty_cache()
+        if not args.no_long_decode:
+            line["decode_long"] = decode_long_bench()
+            torch.cuda.empty_cache()
+        if not args.no_backward:
+            line["backward"] = backward_bench()
+            torch.cuda.empty_cache()
+        if not args.no_stats:
+            line["stats"] = stats_bench()
+            torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, ends, cores)
+    print(json.dumps(line), flush=True)
 
 
 if __name__ == "__main__":

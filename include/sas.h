@@ -471,9 +471,13 @@ const char* sas_version(void);
  * and returns the number of launches recorded.  After the caller has
  * synchronised the streams, sas_profiler_record(i, &name, &ms) returns the
  * kernel family name ("gemm_gate_up", "attention", ...) and the elapsed
- * milliseconds of launch i.  Not thread-safe; the events live until the next
- * sas_profiler_start. */
+ * milliseconds of launch i.  Not thread-safe; the events are reused by the
+ * next sas_profiler_start (created anew only when it asks for more). */
 int32_t sas_profiler_start(int32_t capacity);
+/* Restrict recording to the named kernel families (comma-separated, e.g.
+ * "gemm_gate_up,dec_gate_up"); NULL records every family, "" none.  Applies
+ * to the launches after the call, until the next call. */
+int32_t sas_profiler_select(const char* families);
 int32_t sas_profiler_stop(void);
 int32_t sas_profiler_record(int32_t i, const char** name, float* ms);
 

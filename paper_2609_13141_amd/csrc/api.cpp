@@ -46,21 +46,47 @@ struct Profiler {
   std::vector<hipEvent_t> ev;
   std::vector<const char*> names;
   int used = 0;
+  bool filtered = false;            // record only the families in `only`
+  std::vector<std::string> only;
   int start(int capacity) {
-    for (auto e : ev) (void)hipEventDestroy(e);
-    ev.clear();
-    names.assign(capacity, nullptr);
-    for (int i = 0; i < 2 * capacity; ++i) {
-      hipEvent_t e;
-      if (hipEventCreate(&e) != hipSuccess) return -1;
-      ev.push_back(e);
+    // the events of an earlier start are reused when there are enough of them
+    if ((int)ev.size() < 2 * capacity) {
+      for (auto e : ev) (void)hipEventDestroy(e);
+      ev.clear();
+      for (int i = 0; i < 2 * capacity; ++i) {
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) return -1;
+        ev.push_back(e);
+      }
     }
+    names.assign(capacity, nullptr);
     used = 0;
     on = true;
     return 0;
   }
+  void select(const char* families) {
+    only.clear();
+    filtered = families != nullptr;
+    if (!families) return;
+    std::string cur;
+    for (const char* p = families;; ++p) {
+      if (*p == ',' || *p == '\0') {
+        if (!cur.empty()) only.push_back(cur);
+        cur.clear();
+        if (*p == '\0') break;
+      } else {
+        cur += *p;
+      }
+    }
+  }
+  bool wanted(const char* name) const {
+    if (!filtered) return true;
+    for (const auto& f : only)
+      if (f == name) return true;
+    return false;
+  }
   int begin(const char* name, hipStream_t s) {
-    if (!on || used >= (int)names.size()) return -1;
+    if (!on || used >= (int)names.size() || !wanted(name)) return -1;
     names[used] = name;
     (void)hipEventRecord(ev[2 * used], s);
     return used++;
@@ -620,6 +646,11 @@ const char* sas_version(void) { return "sas-mi355x 0.1 (gfx950)"; }
 int32_t sas_profiler_start(int32_t capacity) {
   if (capacity <= 0) return fail(SAS_ERR_INVALID_ARGUMENT, "capacity must be positive");
   return g_prof.start(capacity) == 0 ? SAS_OK : fail(SAS_ERR_HIP, "hipEventCreate failed");
+}
+
+int32_t sas_profiler_select(const char* families) {
+  g_prof.select(families);
+  return SAS_OK;
 }
 
 int32_t sas_profiler_stop(void) {

@@ -29,7 +29,7 @@ TORCH_DTYPE = {"bf16": torch.bfloat16, "f32": torch.float32}
 
 EXPORTS = ("sas_workspace_size", "sas_attention_prefill", "sas_mlp_forward", "sas_layer_forward",
            "sas_decode_step", "sas_decode_step_noalloc", "sas_decode_select", "sas_attention_backward", "sas_selector_backward", "sas_selection_stats", "sas_overlap_recall", "sas_embed", "sas_lm_head_argmax", "sas_last_error", "sas_version",
-           "sas_profiler_start", "sas_profiler_stop", "sas_profiler_record")
+           "sas_profiler_start", "sas_profiler_select", "sas_profiler_stop", "sas_profiler_record")
 
 
 class SasError(RuntimeError):
@@ -147,6 +147,8 @@ def lib() -> C.CDLL:
     L.sas_version.argtypes = []
     L.sas_profiler_start.restype = i32
     L.sas_profiler_start.argtypes = [i32]
+    L.sas_profiler_select.restype = i32
+    L.sas_profiler_select.argtypes = [C.c_char_p]
     L.sas_profiler_stop.restype = i32
     L.sas_profiler_stop.argtypes = []
     L.sas_profiler_record.restype = i32
@@ -398,6 +400,12 @@ def layer_forward(cfg: Config, x, W: dict, *, stats: bool = True, lse=True, sel_
 
 def profiler_start(capacity: int = 4096):
     _check(lib().sas_profiler_start(capacity))
+
+
+def profiler_select(families):
+    """Record only these kernel families (an iterable of names; None = all)."""
+    arg = None if families is None else ",".join(families).encode()
+    _check(lib().sas_profiler_select(arg))
 
 
 def profiler_stop() -> list:
