@@ -50,13 +50,24 @@ template <int DH, int LSB, bool OUTER>
 __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile, const int h, const int bi,
                                               const int tlo, const int thi, const int slot) {
   constexpr int KP = DH + 8;    // K tile row pitch (elements)
-  constexpr int VP = 64 + 4;    // V^T tile row pitch (elements)
+  // V^T tile: head dimension d starts at (d / 8) * VGS + (d % 8) * VP
+  // elements (rows 96 apart, groups of 8 rows 776 apart).  A row holds the
+  // tile's 64 keys in 8 pairs of 4-key chunks: pair 2 j + h holds keys
+  // 16 j + 4 h + 0..3 and 16 j + 8 + 4 h + 0..3, the 8 keys one lane group
+  // (h) feeds to the PV product's MFMA step j, so an operand is one 16-byte
+  // read.  The strides were chosen by measuring the LDS bank-conflict
+  // counter for these exact access patterns: the operand reads run without
+  // conflicts and the staging writes (rows 8 apart) with two-way ones.
+  constexpr int VP = 96;
+  constexpr int VGS = 8 * VP + 8;
   constexpr int KPG = DH / 32;  // keys per thread in the tile staging
   constexpr int C8 = DH / 8;
   constexpr int NSUB = 64 >> LSB;  // sub-blocks of min(B, 64) keys in a tile
   constexpr int KMAX = 32;
   __shared__ __align__(16) bf16_t Ks[64 * KP];
-  __shared__ __align__(16) bf16_t Vt[DH * VP];
+  __shared__ __align__(16) bf16_t Vt[DH / 8 * VGS];
+  // selection slots of the workgroup's queries, slot-major ([KMAX][128]):
+  // the lanes of a wave read consecutive words
   __shared__ int sel_s[128 * KMAX];
   __shared__ float sbias_s[128 * KMAX];
   __shared__ uint32_t need[ATTN_MAX_SEQ / 64 / 32];
@@ -106,15 +117,15 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
   if (Kn > 0 && qvalid) {
     const size_t row = (grow + t) * Kn;
     for (int k = lk; k < Kn; k += 2) {
-      sel_s[qrow * KMAX + k] = P.sel[row + k];
-      if (gated) sbias_s[qrow * KMAX + k] = P.sel_bias[row + k];
+      sel_s[k * 128 + qrow] = P.sel[row + k];
+      if (gated) sbias_s[k * 128 + qrow] = P.sel_bias[row + k];
     }
   }
   __syncthreads();
   if (!every && qvalid && lk == 0) {
     for (int tl = (beta * B) / 64; tl <= t / 64; ++tl) atomicOr(&need[tl >> 5], 1u << (tl & 31));
     for (int k = 0; k < Kn; ++k) {
-      const int m = sel_s[qrow * KMAX + k];
+      const int m = sel_s[k * 128 + qrow];
       if (m < 0 || m >= beta) break;  // slots are ascending historical blocks, -1 padded
       for (int tl = (m * B) / 64; tl <= ((m + 1) * B - 1) / 64; ++tl) atomicOr(&need[tl >> 5], 1u << (tl & 31));
     }
@@ -134,15 +145,23 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
   const size_t kstride = (size_t)P.Hkv * DH;  // elements between consecutive keys
   const size_t kbase = (size_t)bi * n;
   const int c8 = tid % C8, kg = tid / C8;
-  uint4 rk[KPG], rv[KPG];
+  // this thread's 16-byte column of keys kg * KPG + q of a tile; element
+  // offsets within the batch entry fit 32 bits (n * Hkv * DH < 2^31)
+  const bf16_t* Kb = Kg + kbase * kstride + c8 * 8;
+  const bf16_t* Vb = Vg + kbase * kstride + c8 * 8;
+  const uint32_t ks32 = (uint32_t)kstride, last_off = (uint32_t)(n - 1) * ks32;
+  u32x4_t rk[KPG], rv[KPG];  // native vectors: the staging stays in registers
   float r_lg[NSUB];  // full scope: this lane's log gates of the tile's blocks
   auto prefetch = [&](int kt) {
+    // keys past the end load the last key's row instead (finite; their
+    // scores are masked and their probabilities are zero)
+    const int r0 = kt * 64 + kg * KPG;
+    const uint32_t off0 = (uint32_t)r0 * ks32;
 #pragma unroll
     for (int q = 0; q < KPG; ++q) {
-      const int key = kt * 64 + kg * KPG + q;
-      const size_t go = (kbase + key) * kstride + c8 * 8;
-      rk[q] = key < n ? *(const uint4*)(Kg + go) : make_uint4(0, 0, 0, 0);
-      rv[q] = key < n ? *(const uint4*)(Vg + go) : make_uint4(0, 0, 0, 0);
+      const uint32_t off = r0 + q < n ? off0 + q * ks32 : last_off;
+      rk[q] = *(const u32x4_t*)(Kb + off);
+      rv[q] = *(const u32x4_t*)(Vb + off);
     }
     if (full) {
 #pragma unroll
@@ -154,18 +173,26 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
   };
   auto commit = [&]() {
 #pragma unroll
-    for (int q = 0; q < KPG; ++q) *(uint4*)(Ks + (kg * KPG + q) * KP + c8 * 8) = rk[q];
+    for (int q = 0; q < KPG; ++q) *(u32x4_t*)(Ks + (kg * KPG + q) * KP + c8 * 8) = rk[q];
+    // V^T: word wd of a key holds dims 2 wd (low half) and 2 wd + 1; one byte
+    // permute joins the same half of two keys
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int sh = (e & 1) * 16, wd = e >> 1;
-      bf16_t* dst = Vt + (c8 * 8 + e) * VP + kg * KPG;
-      uint32_t x[KPG];
+    for (int wd = 0; wd < 4; ++wd) {
+      uint32_t a[KPG];
 #pragma unroll
-      for (int q = 0; q < KPG; ++q) x[q] = (((const uint32_t*)&rv[q])[wd] >> sh) & 0xffffu;
-      if constexpr (KPG == 4) {
-        *(uint2*)dst = make_uint2(x[0] | (x[1] << 16), x[2] | (x[3] << 16));
-      } else {
-        *(uint32_t*)dst = x[0] | (x[1] << 16);
+      for (int q = 0; q < KPG; ++q) a[q] = rv[q][wd];
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        const uint32_t sel = hf ? 0x07060302u : 0x05040100u;
+        // dimension d = 8 c8 + e, keys kg * KPG ..: chunk c = kg * KPG / 4 (its part kg * KPG % 4)
+        const int c = (kg * KPG) >> 2;
+        bf16_t* dst = Vt + c8 * VGS + (2 * wd + hf) * VP + 16 * (c >> 2) + 8 * (c & 1) + 4 * ((c >> 1) & 1) +
+                      ((kg * KPG) & 3);
+        if constexpr (KPG == 4) {
+          *(uint2*)dst = make_uint2(__builtin_amdgcn_perm(a[1], a[0], sel), __builtin_amdgcn_perm(a[3], a[2], sel));
+        } else {
+          *(uint32_t*)dst = __builtin_amdgcn_perm(a[1], a[0], sel);
+        }
       }
     }
   };
@@ -175,11 +202,11 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
   const int tend = min(thi, ntiles);
   int cur = 0, next_sel = 0x7fffffff;  // selection cursor of this lane's query
   if (Kn > 0 && qvalid) {
-    const int s0 = sel_s[qrow * KMAX];
+    const int s0 = sel_s[qrow];
     next_sel = s0 >= 0 ? s0 : 0x7fffffff;
     while (next_sel != 0x7fffffff && (next_sel + 1) * B <= tlo * 64) {
       ++cur;
-      const int s1 = cur < Kn ? sel_s[qrow * KMAX + cur] : -1;
+      const int s1 = cur < Kn ? sel_s[cur * 128 + qrow] : -1;
       next_sel = s1 >= 0 ? s1 : 0x7fffffff;
     }
   }
@@ -207,10 +234,10 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
         lg = r_lg[sb];
       } else if (m == next_sel) {
         att = true;
-        lg = gated ? sbias_s[qrow * KMAX + cur] : 0.f;
+        lg = gated ? sbias_s[cur * 128 + qrow] : 0.f;
         if (kstart + (1 << LSB) >= (m + 1) * B) {  // a block wider than a tile is consumed at its last tile
           ++cur;
-          const int s1 = cur < Kn ? sel_s[qrow * KMAX + cur] : -1;
+          const int s1 = cur < Kn ? sel_s[cur * 128 + qrow] : -1;
           next_sel = s1 >= 0 ? s1 : 0x7fffffff;
         }
       }
@@ -234,40 +261,64 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
         s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qb[ks], s[st], 0, 0, 0);
       }
     }
-    // scale + offset, causal mask on the diagonal tiles; row max with the partner lane
-    const bool diag = k0 + 63 > qtile * 128;
+    // causal mask on the diagonal tiles (raw scores of later keys -> -inf)
+    if (k0 + 63 > qtile * 128) {
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (k0 + st * 32 + 8 * (v >> 2) + 4 * lk + (v & 3) > t) s[st][v] = -INFINITY;
+    }
+    // row max of the logits s * scale + offset: the scale is positive, so per
+    // sub-block the largest raw score gives the largest logit
+    float mxs[NSUB];
+#pragma unroll
+    for (int sb = 0; sb < NSUB; ++sb) mxs[sb] = -INFINITY;
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int sb = (st * 32 + 8 * (v >> 2)) >> LSB;
+        mxs[sb] = fmaxf(mxs[sb], s[st][v]);
+      }
     float mx = -INFINITY;
 #pragma unroll
-    for (int st = 0; st < 2; ++st)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int klc = st * 32 + 8 * (v >> 2);  // key offset without the lane part (4 lk + v % 4 < 8)
-        float x = fmaf(s[st][v], qk_scale, offs[klc >> LSB]);
-        if (diag && k0 + klc + 4 * lk + (v & 3) > t) x = -INFINITY;
-        s[st][v] = x;
-        mx = fmaxf(mx, x);
-      }
+    for (int sb = 0; sb < NSUB; ++sb) mx = fmaxf(mx, fmaf(mxs[sb], qk_scale, offs[sb]));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    float rs = 0.f;
+    // The reference max m_run moves only when a logit exceeds it by more than
+    // 8 (log2 units): the exponentials stay below 2^8 and the accumulators
+    // are rescaled only on those tiles.  Any reference gives the same O and
+    // LSE; the partner lanes share mx and so the decision.
+    const bool upd = mx > m_run + 8.f;
+    float alpha = 1.f;
+    if (upd) {
+      alpha = __builtin_amdgcn_exp2f(m_run - mx);
+      m_run = mx;
+    }
+    const float m_use = m_run == -INFINITY ? 0.f : m_run;
+    float bias[NSUB];
+#pragma unroll
+    for (int sb = 0; sb < NSUB; ++sb) bias[sb] = offs[sb] - m_use;
+    float rs4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const float p = __builtin_amdgcn_exp2f(s[st][v] - m_use);
-        rs += p;
-        if constexpr (OUTER) s[st][v] = p * wts[(st * 32 + 8 * (v >> 2)) >> LSB];
+        const int sb = (st * 32 + 8 * (v >> 2)) >> LSB;
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[st][v], qk_scale, bias[sb]));
+        rs4[v & 3] += p;
+        if constexpr (OUTER) s[st][v] = p * wts[sb];
         else s[st][v] = p;
       }
+    float rs = (rs4[0] + rs4[1]) + (rs4[2] + rs4[3]);
     rs += __shfl_xor(rs, 32, 64);
     l_run = l_run * alpha + rs;
-    m_run = m_new;
+    if (__builtin_amdgcn_ballot_w64(upd) != 0) {
 #pragma unroll
-    for (int dt = 0; dt < DH / 32; ++dt)
+      for (int dt = 0; dt < DH / 32; ++dt)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) o[dt][v] *= alpha;
+        for (int v = 0; v < 16; ++v) o[dt][v] *= alpha;
+    }
 
     // O^T += V^T P^T, 16 keys per step in the accumulator's key permutation
 #pragma unroll
@@ -281,11 +332,9 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
       const bf16x8_t pb = *(const bf16x8_t*)&pu;
 #pragma unroll
       for (int dt = 0; dt < DH / 32; ++dt) {
-        const bf16_t* vr = Vt + (dt * 32 + lr) * VP + 16 * ks + 4 * lk;
-        const uint2 lo = *(const uint2*)vr;
-        const uint2 hi = *(const uint2*)(vr + 8);
-        uint4 u = make_uint4(lo.x, lo.y, hi.x, hi.y);
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(bf16x8_t*)&u, pb, o[dt], 0, 0, 0);
+        // pair 2 ks + lk of dimension dt * 32 + lr
+        const bf16_t* vr = Vt + (4 * dt + (lr >> 3)) * VGS + (lr & 7) * VP + 16 * ks + 8 * lk;
+        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8_t*)vr, pb, o[dt], 0, 0, 0);
       }
     }
     lds_barrier();
@@ -486,6 +535,8 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
   if (a.n <= 0 || a.b <= 0) return hipSuccess;
   if (dtype == SAS_BF16) {
     if (a.n > ATTN_MAX_SEQ || a.K > 32) return hipErrorInvalidValue;
+    // the kernel's key offsets within a batch entry are 32-bit
+    if ((unsigned long long)a.n * a.Hkv * a.dh > 0xffffffffull) return hipErrorInvalidValue;
     const int lsb = a.B >= 64 ? 6 : (a.B == 32 ? 5 : 4);
     const bool outer = a.mode == SAS_MODE_GATED && a.outer;
     void (*kern)(AttnArgs, int);

@@ -23,6 +23,7 @@ __device__ __forceinline__ float bf16_to_f32(bf16_t h) {
 // to nearest even, NaN stays NaN; pack_bf16x2 converts two values at once.
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));  // 16 bytes as a native vector
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   const f32x2_t f = {lo, hi};
   const bf16x2_t h = __builtin_convertvector(f, bf16x2_t);
