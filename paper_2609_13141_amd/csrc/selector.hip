@@ -142,29 +142,32 @@ hipError_t launch_block_summaries(int dtype, const void* K, int b, int n, int Hk
 // Selection: one workgroup of SEL_NW waves per 64 consecutive query rows of
 // one (batch, group); lane = query row.  The 64 gate queries are staged in
 // LDS once; the waves split the historical blocks into contiguous ranges and
-// walk theirs in chunks of SEL_MC summaries (8, or 4 when no wave has more
-// than 4 blocks) staged in LDS as fp32 (exact for bf16 and fp32 summaries,
-// and half the bytes of fp64 per broadcast read), one exact fp64 FMA chain
-// per (row, block), j ascending, each keeping a register Top-K and a running
-// LSE.  The waves' lists are then merged into wave 0's in wave order, which
-// reproduces a single ascending scan (strict comparisons keep the lower block
-// first on equal scores).
-constexpr int SEL_NW = 4;   // waves per workgroup
+// walk theirs in ascending order, in chunks of SEL_MC summaries staged in
+// LDS as fp64 (the next chunk is loaded into registers while the current
+// one is scored), one exact fp64 FMA chain per (row, block), j ascending,
+// each keeping a register Top-K (best first) and a running LSE.  The lists
+// are ordered by score, then by lower block index (the order of a single
+// ascending scan with strict comparisons), and wave 0 merges the others'
+// lists into its own in wave order: the elementwise better of its list and
+// the reversed other list holds the best K as a bitonic sequence, which a
+// bitonic network sorts.
+constexpr int SEL_NW = 4;  // waves per workgroup
 
 __device__ __forceinline__ void lds_fence() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
 template <typename T, int DH, int KMAX, int SEL_MC, bool NOISY>
-__global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
-  constexpr int KB_BYTES = SEL_NW * SEL_MC * DH * 4;
-  constexpr int MG_BYTES = KMAX * WAVE * 12 + WAVE * 8 + WAVE * 4;
-  __shared__ __align__(16) unsigned char pool[KB_BYTES > MG_BYTES ? KB_BYTES : MG_BYTES];
+__global__ void __launch_bounds__(SEL_NW * WAVE) select_kernel(SelectArgs P) {
+  static_assert((KMAX & (KMAX - 1)) == 0, "the merge network needs a power-of-two list");
+  constexpr int KW_BYTES = SEL_NW * SEL_MC * DH * 8;
+  constexpr int MG_BYTES = KMAX * WAVE * 12 + WAVE * 12;
+  __shared__ __align__(16) unsigned char pool[KW_BYTES > MG_BYTES ? KW_BYTES : MG_BYTES];
   __shared__ __align__(16) T qs[WAVE][DH + 8];  // the 64 gate queries
-  float(*kb)[SEL_MC][DH] = (float(*)[SEL_MC][DH])pool;              // [SEL_NW][SEL_MC][DH] (exact in fp32)
-  double* mg_r = (double*)pool;                                      // merge: [KMAX][WAVE] keys
-  int* mg_m = (int*)(pool + KMAX * WAVE * 8);                        // [KMAX][WAVE] blocks
-  double* mg_mx = (double*)(pool + KMAX * WAVE * 12);                // [WAVE] running max
-  float* mg_l = (float*)(pool + KMAX * WAVE * 12 + WAVE * 8);        // [WAVE] running sum
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  double(*kw)[DH] = (double(*)[DH])pool + wave * SEL_MC;  // this wave's staged summaries (exact in fp64)
+  double* mg_r = (double*)pool;                            // merge: [KMAX][WAVE] keys
+  int* mg_m = (int*)(pool + KMAX * WAVE * 8);              // [KMAX][WAVE] blocks
+  double* mg_mx = (double*)(pool + KMAX * WAVE * 12);      // [WAVE] running max
+  float* mg_l = (float*)(pool + KMAX * WAVE * 12 + WAVE * 8);  // [WAVE] running sum
   const int g = blockIdx.y, bi = blockIdx.z;
   const int t0 = (gridDim.x - 1 - blockIdx.x) * WAVE;  // the late rows (more blocks to score) first
   const int t = t0 + lane;
@@ -173,7 +176,7 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
   const int ct = valid ? t / P.B : 0;
   const int fb = valid ? doc_first(P.doc, bi, P.NB, t, P.B) : 0;  // first block of the query's document
   const int t_last = min(P.n - 1, t0 + WAVE - 1);
-  const int cmax = t_last / P.B;  // workgroup-uniform block count
+  const int cmax = t_last / P.B;  // wave-uniform block count
   const int mlo = doc_first(P.doc, bi, P.NB, t0, P.B);  // the rows' earliest document start
   const double den = (double)G * sqrt((double)DH);  // s = r / (G sqrt(dh))
   const double inv_scale = 1.0 / den;
@@ -188,15 +191,15 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
   // the group's query heads summed here in fp64 and rounded once; a thread's
   // loads of one head are issued together
   {
-    constexpr int NC = DH / 8;  // 8-value chunks per row
-    constexpr int NI = NC / SEL_NW;
+    constexpr int NC = DH / 8;       // 8-value chunks per row
+    constexpr int NI = NC / SEL_NW;  // chunks per thread (64 rows x NC chunks)
     const int rows = t_last - t0 + 1;
+    const int nh = P.qhat ? 1 : G;
     double acc[NI][8];
 #pragma unroll
     for (int i = 0; i < NI; ++i)
 #pragma unroll
       for (int e = 0; e < 8; ++e) acc[i][e] = 0.0;
-    const int nh = P.qhat ? 1 : G;
     for (int h = 0; h < nh; ++h) {
       Vec8<T> v[NI];
 #pragma unroll
@@ -246,6 +249,16 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
       return a > b || b != b;
     }
   };
+  // the total order of the lists: a ranks ahead of b (ties: lower block first)
+  auto ahead = [](double a, int am, double b, int bm) -> bool {
+    if constexpr (!NOISY) {
+      return a > b || (a == b && am < bm);
+    } else {
+      const int ca = am == EMPTY ? 2 : (a != a ? 1 : 0), cb = bm == EMPTY ? 2 : (b != b ? 1 : 0);
+      if (ca != cb) return ca < cb;
+      return (ca == 0 && a > b) || ((ca == 1 || a == b) && am < bm);
+    }
+  };
   auto insert = [&](double cr, int cm) {
     if (cm == EMPTY || !beats(cr, tr[KMAX - 1], tm[KMAX - 1])) return;
 #pragma unroll
@@ -263,41 +276,51 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
   const T* kbar = (const T*)P.kbar + ((size_t)bi * P.Hkv + g) * (size_t)P.NB * DH;
   const int per = (cmax - mlo + SEL_NW - 1) / SEL_NW;
   const int mb = mlo + wave * per, me = min(cmax, mb + per);
-  float(*kw)[DH] = kb[wave];
+  // staging: SEL_MC x DH summary values as 8-value chunks, NCL per lane
+  constexpr int NC = DH / 8, NCH = SEL_MC * NC, NCL = (NCH + WAVE - 1) / WAVE;
+  Vec8<T> nx[NCL];
+  auto fetch = [&](int m0) {
+    const int mc = min(SEL_MC, me - m0);
+#pragma unroll
+    for (int i = 0; i < NCL; ++i) {
+      const int c = min(lane + i * WAVE, NCH - 1);
+      nx[i].load(kbar + (size_t)(m0 + min(c / NC, mc - 1)) * DH + (c % NC) * 8);
+    }
+  };
+  if (mb < me) fetch(mb);
   for (int m0 = mb; m0 < me; m0 += SEL_MC) {
     const int mc = min(SEL_MC, me - m0);
-    {
-      constexpr int NC = DH / 8, NCH = SEL_MC * NC;  // 8-value chunks of the staged summaries
 #pragma unroll
-      for (int i = 0; i < (NCH + WAVE - 1) / WAVE; ++i) {
-        const int c = lane + i * WAVE;
-        if (NCH % WAVE != 0 && c >= NCH) continue;
-        const int r = c / NC, c8 = c % NC;
-        Vec8<T> v;
-        v.load(kbar + (size_t)(m0 + min(r, mc - 1)) * DH + c8 * 8);
+    for (int i = 0; i < NCL; ++i) {
+      const int c = lane + i * WAVE;
+      if (NCH % WAVE != 0 && c >= NCH) continue;
+      const int r = c / NC, c8 = c % NC;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) kw[r][c8 * 8 + e] = r < mc ? v.get(e) : 0.f;
-      }
+      for (int e = 0; e < 8; ++e) kw[r][c8 * 8 + e] = r < mc ? (double)nx[i].get(e) : 0.0;
     }
     lds_fence();
+    if (m0 + SEL_MC < me) fetch(m0 + SEL_MC);  // the next chunk, in flight while this one is scored
     // r[mm] = sum_j q_j kbar[m0+mm]_j: one fp64 FMA chain per block, j ascending
     double r[SEL_MC];
 #pragma unroll
     for (int mm = 0; mm < SEL_MC; ++mm) r[mm] = 0.0;
+    // (a bounded unroll: a full one lets the summary reads of every step be
+    // hoisted, more registers than the wave has)
+#pragma unroll 2
     for (int j = 0; j < DH; j += 4) {
       double qd[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) qd[u] = Act<T>::to_f32(qs[lane][j + u]);
 #pragma unroll
       for (int mm = 0; mm < SEL_MC; ++mm) {
-        const float4 k4 = *(const float4*)&kw[mm][j];  // four dimensions of one summary (broadcast)
-        r[mm] = fma(qd[0], (double)k4.x, r[mm]);
-        r[mm] = fma(qd[1], (double)k4.y, r[mm]);
-        r[mm] = fma(qd[2], (double)k4.z, r[mm]);
-        r[mm] = fma(qd[3], (double)k4.w, r[mm]);
+        const double2 k01 = *(const double2*)&kw[mm][j];  // four dimensions of one summary (broadcast)
+        const double2 k23 = *(const double2*)&kw[mm][j + 2];
+        r[mm] = fma(qd[0], k01.x, r[mm]);
+        r[mm] = fma(qd[1], k01.y, r[mm]);
+        r[mm] = fma(qd[2], k23.x, r[mm]);
+        r[mm] = fma(qd[3], k23.y, r[mm]);
       }
     }
-    lds_fence();  // this wave's reads of the chunk are done before it is restaged
 #pragma unroll
     for (int mm = 0; mm < SEL_MC; ++mm) {
       const int m = m0 + mm;
@@ -318,6 +341,7 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
       }
       insert(rv, m);
     }
+    lds_fence();  // this chunk's reads are done before it is restaged
   }
   __syncthreads();
   // merge the other waves' lists into wave 0's, in wave order
@@ -333,8 +357,32 @@ __global__ void __launch_bounds__(SEL_NW * 64) select_kernel(SelectArgs P) {
     }
     __syncthreads();
     if (wave == 0) {
+      // the better of slot i and the other list's slot KMAX-1-i: the best KMAX
+      // of both, descending then ascending (a bitonic sequence)
 #pragma unroll
-      for (int i = 0; i < KMAX; ++i) insert(mg_r[i * WAVE + lane], mg_m[i * WAVE + lane]);
+      for (int i = 0; i < KMAX; ++i) {
+        const double ob = mg_r[(KMAX - 1 - i) * WAVE + lane];
+        const int om = mg_m[(KMAX - 1 - i) * WAVE + lane];
+        if (ahead(ob, om, tr[i], tm[i])) {
+          tr[i] = ob;
+          tm[i] = om;
+        }
+      }
+      // bitonic sort, best first
+#pragma unroll
+      for (int len = KMAX / 2; len >= 1; len >>= 1)
+#pragma unroll
+        for (int i = 0; i < KMAX; ++i)
+          if ((i & len) == 0) {
+            const int j = i + len;
+            const bool sw = ahead(tr[j], tm[j], tr[i], tm[i]);
+            const double ri = tr[i], rj = tr[j];
+            const int mi = tm[i], mj = tm[j];
+            tr[i] = sw ? rj : ri;
+            tr[j] = sw ? ri : rj;
+            tm[i] = sw ? mj : mi;
+            tm[j] = sw ? mi : mj;
+          }
       const double om = mg_mx[lane];
       const float ol = mg_l[lane];
       if (om > mrun) {
