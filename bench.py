@@ -389,6 +389,7 @@ def headline(args):
         tok, _, _ = st.step(tok, p)
     recs = sas.profiler_stop()
     kall, kall_n = family_means(recs)
+    yard = hipblaslt_yardstick(w, dev)
     out = {
         "value": round(tok_s_layer, 1),
         "ms_per_step": round(ms, 3),
@@ -424,9 +425,40 @@ def headline(args):
         },
         "kernels_ms": {k: round(v, 4) for k, v in sorted(kall.items(), key=lambda kv: -kv[1] * kall_n[kv[0]])},
         "kernel_calls": kall_n,
+        "yardstick_hipblaslt_ms": {k: round(v, 4) for k, v in yard.items()},
     }
     del st, layers
     return w, ends, out
+
+
+def hipblaslt_yardstick(w, dev, reps=10, copies=4):
+    """An outside yardstick for the prefill GEMMs: torch's bf16 linear
+    (hipBLASLt) at the same shapes (M = the prefill's tokens), plain
+    products without the fused epilogues, cycling over `copies` weight
+    buffers so that the weights stream from HBM as in a layer."""
+    import torch
+    T = w.tokens
+    shapes = (("gemm_qkv", (w.n_heads + 2 * w.n_kv_heads) * w.head_dim, w.d_model),
+              ("gemm_o", w.d_model, w.n_heads * w.head_dim),
+              ("gemm_gate_up", 2 * w.d_ff, w.d_model),
+              ("gemm_down", w.d_model, w.d_ff))
+    out = {}
+    for fam, N, K in shapes:
+        A = torch.randn(T, K, device=dev).to(torch.bfloat16)
+        Ws = [(torch.randn(N, K, device=dev) * 0.02).to(torch.bfloat16) for _ in range(copies)]
+        for i in range(3):
+            torch.nn.functional.linear(A, Ws[i % copies])
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for i in range(reps):
+            torch.nn.functional.linear(A, Ws[i % copies])
+        e1.record()
+        torch.cuda.synchronize()
+        out[fam] = e0.elapsed_time(e1) / reps
+        del A, Ws
+    torch.cuda.empty_cache()
+    return out
 
 
 def attention_executed_flops(w, sel):
