@@ -14,6 +14,10 @@
 
 using namespace sas;
 
+namespace sas {
+LaunchEvents g_launch_events = {nullptr, nullptr};  // see kernels.h
+}
+
 namespace {
 
 thread_local std::string g_err;
@@ -40,26 +44,30 @@ sas_status hip_check(hipError_t e, const char* what) {
   } while (0)
 #define HIP_TRY(expr, what) SAS_TRY(hip_check((expr), (what)))
 
-// Opt-in kernel timing: a hipEvent pair around every launch on its stream.
+// Opt-in kernel timing: a hipEvent pair around every launch on its stream,
+// and a second pair that a single-kernel launch made through launch_ext
+// records at the kernel's own start and end (used when it was recorded).
 struct Profiler {
   bool on = false;
-  std::vector<hipEvent_t> ev;
+  std::vector<hipEvent_t> ev;  // 4 per record: outer begin, outer end, kernel start, kernel stop
   std::vector<const char*> names;
+  std::vector<char> exact;     // the kernel pair of the record was recorded
   int used = 0;
   bool filtered = false;            // record only the families in `only`
   std::vector<std::string> only;
   int start(int capacity) {
     // the events of an earlier start are reused when there are enough of them
-    if ((int)ev.size() < 2 * capacity) {
+    if ((int)ev.size() < 4 * capacity) {
       for (auto e : ev) (void)hipEventDestroy(e);
       ev.clear();
-      for (int i = 0; i < 2 * capacity; ++i) {
+      for (int i = 0; i < 4 * capacity; ++i) {
         hipEvent_t e;
         if (hipEventCreate(&e) != hipSuccess) return -1;
         ev.push_back(e);
       }
     }
     names.assign(capacity, nullptr);
+    exact.assign(capacity, 0);
     used = 0;
     on = true;
     return 0;
@@ -88,11 +96,15 @@ struct Profiler {
   int begin(const char* name, hipStream_t s) {
     if (!on || used >= (int)names.size() || !wanted(name)) return -1;
     names[used] = name;
-    (void)hipEventRecord(ev[2 * used], s);
+    (void)hipEventRecord(ev[4 * used], s);
+    g_launch_events = LaunchEvents{ev[4 * used + 2], ev[4 * used + 3]};
     return used++;
   }
   void end(int id, hipStream_t s) {
-    if (id >= 0) (void)hipEventRecord(ev[2 * id + 1], s);
+    if (id < 0) return;
+    (void)hipEventRecord(ev[4 * id + 1], s);
+    exact[id] = g_launch_events.start == nullptr;  // consumed by exactly the one launch that took it
+    g_launch_events = LaunchEvents{nullptr, nullptr};
   }
 };
 Profiler g_prof;
@@ -661,7 +673,8 @@ int32_t sas_profiler_stop(void) {
 int32_t sas_profiler_record(int32_t i, const char** name, float* ms) {
   if (i < 0 || i >= g_prof.used) return fail(SAS_ERR_INVALID_ARGUMENT, "record %d out of range", i);
   *name = g_prof.names[i];
-  return hip_check(hipEventElapsedTime(ms, g_prof.ev[2 * i], g_prof.ev[2 * i + 1]), "hipEventElapsedTime");
+  const int k = g_prof.exact[i] ? 2 : 0;
+  return hip_check(hipEventElapsedTime(ms, g_prof.ev[4 * i + k], g_prof.ev[4 * i + k + 1]), "hipEventElapsedTime");
 }
 
 size_t sas_workspace_size(const sas_config* c, int32_t op, int32_t batch, int32_t seq_len) {

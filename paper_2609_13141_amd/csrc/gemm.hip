@@ -706,8 +706,8 @@ static hipError_t run_lds_t(const GemmParams& P, hipStream_t s) {
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     attr = true;
   }
-  hipLaunchKernelGGL((gemm_bf16_lds_kernel<EPI, BM, BN, WM, WN, STAGES>), dim3(tiles), dim3(NT), lds, s, P);
-  return hipGetLastError();
+  return launch_ext(gemm_bf16_lds_kernel<EPI, BM, BN, WM, WN, STAGES>, dim3(tiles), dim3(NT), (uint32_t)lds, s,
+                    P);
 }
 
 template <int BM, int BN, int WM, int WN, int STAGES>
@@ -778,6 +778,7 @@ hipError_t launch_gemm(int dtype, const GemmArgs& g, hipStream_t s) {
       const int mt = (g.M + 255) / 256, nt = (nlog + 255) / 256;
       const int full = 256 / mt;  // 256-column tiles per full round
       if ((long)mt * nt > 256 && full > 0) {
+        g_launch_events = LaunchEvents{nullptr, nullptr};  // two launches: timed around both
         GemmParams P1 = P, P2 = P;
         P1.n_cnt = full * 256;
         P2.n_off = full * 256;

@@ -1,10 +1,35 @@
 // Host-side launchers of the SAS kernels (one translation unit each).
 // Every launcher enqueues on `stream` and returns hipGetLastError().
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace sas {
+
+// Kernel-exact timing for the profiler: when `start` is set, the next launch
+// made through launch_ext records these events at the kernel's own start and
+// end (so the interval excludes the dispatch latency that a pair of stream
+// events around the launch includes) and clears them.  Launches of
+// multi-kernel calls leave them unset.
+struct LaunchEvents {
+  hipEvent_t start, stop;
+};
+extern LaunchEvents g_launch_events;
+
+template <typename... KArgs, typename... Args>
+inline hipError_t launch_ext(void (*kern)(KArgs...), dim3 grid, dim3 block, uint32_t shm, hipStream_t s,
+                             Args... args) {
+  if (g_launch_events.start) {
+    const LaunchEvents e = g_launch_events;
+    g_launch_events = LaunchEvents{nullptr, nullptr};
+    hipExtLaunchKernelGGL(kern, grid, block, shm, s, e.start, e.stop, 0, args...);
+  } else {
+    hipLaunchKernelGGL(kern, grid, block, shm, s, args...);
+  }
+  return hipGetLastError();
+}
+
 
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 inline size_t cdiv(size_t a, int b) { return (a + (size_t)b - 1) / (size_t)b; }
