@@ -249,7 +249,10 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
     const int nkt = next_set(need, kt + 1, tend);
     if (nkt < tend) prefetch(nkt);
 
-    // S^T = K Q^T for keys [0,32) and [32,64) of the tile
+    // S^T = K Q^T for keys [0,32) and [32,64) of the tile.  The MFMA phases
+    // run at a raised wave priority, so that while this wave feeds the
+    // matrix unit the other wave on the SIMD issues its softmax in between.
+    __builtin_amdgcn_s_setprio(2);
     floatx16_t s[2];
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
@@ -261,6 +264,7 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
         s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qb[ks], s[st], 0, 0, 0);
       }
     }
+    __builtin_amdgcn_s_setprio(0);
     // causal mask on the diagonal tiles (raw scores of later keys -> -inf)
     if (k0 + 63 > qtile * 128) {
 #pragma unroll
@@ -321,6 +325,7 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
     }
 
     // O^T += V^T P^T, 16 keys per step in the accumulator's key permutation
+    __builtin_amdgcn_s_setprio(2);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const int st = ks >> 1, v0 = 8 * (ks & 1);
@@ -337,6 +342,7 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
         o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8_t*)vr, pb, o[dt], 0, 0, 0);
       }
     }
+    __builtin_amdgcn_s_setprio(0);
     lds_barrier();
     kt = nkt;
   }
