@@ -50,7 +50,7 @@ COPY_BYTES = 512 * 2**20  # calibration copy: reads and writes this many bytes o
 DOMINANT = {
     "prefill": {"family": "gemm_gate_up", "kernel": "gemm_bf16_lds_kernel<1, 256, 256, 2, 4, 2>",
                 "source": "gemm.hip", "file": "gemm_gate_up_7b_stack32_prefill2k_traffic.txt"},
-    "decode": {"family": "dec_gate_up", "kernel": "gemv_stream_kernel<1, 4, 32, 8, true>",
+    "decode": {"family": "dec_gate_up", "kernel": "gemv_kernel<4, 1>",
                "source": "gemv.hip", "file": "gemv_gate_up_7b_stack32_decode_b8_traffic.txt"},
 }
 DECODE_SAMPLE = 8   # the decode GEMV is event-timed on every 8th decode step of the timed region

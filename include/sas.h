@@ -171,7 +171,10 @@ typedef struct {
 
 /* Decoder-layer weights (activation dtype).  rms1/rms2 [d]; wq [H*dh, d];
  * wk, wv [Hkv*dh, d]; wo [d, H*dh]; w_gate, w_up [d_ff, d]; w_down [d, d_ff];
- * w_gq, w_gk [Hkv, dh, dh] or NULL. */
+ * w_gq, w_gk [Hkv, dh, dh] or NULL.  decode_packed: NULL, or the same
+ * layer's linear weights repacked by sas_pack_decode_weights, which the
+ * decode step then streams instead of wq..w_down (same results, bit for
+ * bit); the other entry points ignore it. */
 typedef struct {
   const void* rms1;
   const void* wq;
@@ -184,6 +187,7 @@ typedef struct {
   const void* w_down;
   const void* w_gq;
   const void* w_gk;
+  const void* decode_packed;
 } sas_layer_weights;
 
 /* Optional intermediate taps of sas_layer_forward (any field may be NULL):
@@ -404,6 +408,24 @@ sas_status sas_decode_step(const sas_config* cfg, int32_t batch, const void* x,
                            const int32_t* pos, const sas_layer_weights* w,
                            sas_paged_kv* cache, void* y, int32_t* sel_idx,
                            sas_layer_taps* taps, void* ws, size_t ws_bytes, void* stream);
+
+/* Decode weight layout (bf16 only; the memory layout of the paper's
+ * decode, Alg. 2, is not specified -- this one serves the decode step's
+ * weight-streaming products).  Each of the layer's four products (QKV,
+ * O-projection, gate/up, down) is stored as blocks of 16 output columns x 32
+ * input elements, one contiguous 1-KB block per (column group, 32-wide k
+ * step), groups in order, steps ascending, so that every load instruction of
+ * the decode GEMV reads 1 KB of consecutive bytes.  The column groups are
+ * those of the decode step's epilogues (QKV: 8 rotary pairs; gate/up: 8 gate
+ * and the matching 8 up rows; O and down: 16 rows).
+ * sas_decode_packed_bytes: bytes of one layer's packed copy (0 if the
+ * configuration has none: fp32, or d, H*dh or d_ff not a multiple of 128).
+ * sas_pack_decode_weights: writes it from w (wq..w_down, DEVICE) into packed
+ * (DEVICE, caller-owned, 256-byte aligned, at least that many bytes),
+ * asynchronously on `stream`; w->decode_packed is not read. */
+size_t sas_decode_packed_bytes(const sas_config* cfg);
+sas_status sas_pack_decode_weights(const sas_config* cfg, const sas_layer_weights* w, void* packed,
+                                   size_t packed_bytes, void* stream);
 
 /* Scratch bytes of sas_decode_step_noalloc (one static copy per GPU). */
 #define SAS_DECODE_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)

@@ -394,6 +394,7 @@ sas_status check_weights(const sas_layer_weights* w, bool attn, bool mlp) {
     SAS_TRY(check_ptr(w->wo, "w.wo", true));
     SAS_TRY(check_ptr(w->w_gq, "w.w_gq", false));
     SAS_TRY(check_ptr(w->w_gk, "w.w_gk", false));
+    SAS_TRY(check_ptr(w->decode_packed, "w.decode_packed", false));
   }
   if (mlp) {
     SAS_TRY(check_ptr(w->rms2, "w.rms2", true));
@@ -633,6 +634,30 @@ sas_status check_ws(void* ws, size_t ws_bytes, size_t need) {
   if (ws_bytes < need) return fail(SAS_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, need);
   if (!aligned16(ws)) return fail(SAS_ERR_INVALID_ARGUMENT, "workspace is not 16-byte aligned");
   return SAS_OK;
+}
+
+// Byte offsets of the four products in a layer's packed decode copy (each
+// 256-byte aligned), or false when the configuration has none.
+struct PackedLayout {
+  size_t qkv, o, gu, down, total;
+};
+bool packed_layout(const sas_config* c, PackedLayout& L) {
+  if (c->dtype != SAS_BF16) return false;
+  const int d = c->d_model, H = c->n_heads, Hkv = c->n_kv_heads, dh = c->head_dim, F = c->d_ff;
+  if (d % 128 != 0 || (H * dh) % 128 != 0 || F % 128 != 0) return false;
+  auto bytes = [](int epi, int N, int K) {
+    GemmArgs a = {};
+    a.epi = epi;
+    a.N = N;
+    a.K = K;
+    return (gemv_packed_elems(a) * 2 + 255) / 256 * 256;
+  };
+  L.qkv = 0;
+  L.o = bytes(EPI_QKV_ROPE, (H + 2 * Hkv) * dh, d);
+  L.gu = L.o + bytes(EPI_RESID, d, H * dh);
+  L.down = L.gu + bytes(EPI_SWIGLU, F, d);
+  L.total = L.down + bytes(EPI_RESID, d, F);
+  return true;
 }
 
 }  // namespace
@@ -1134,6 +1159,55 @@ sas_status sas_layer_forward(const sas_config* c, int32_t batch, int32_t seq_len
   return run_mlp(c, T, h1, w, y, lw.mlp, s);
 }
 
+size_t sas_decode_packed_bytes(const sas_config* c) {
+  PackedLayout L;
+  if (!c || check_config(c, true) != SAS_OK || !packed_layout(c, L)) return 0;
+  return L.total;
+}
+
+sas_status sas_pack_decode_weights(const sas_config* c, const sas_layer_weights* w, void* packed,
+                                   size_t packed_bytes, void* stream) {
+  SAS_TRY(check_config(c, true));
+  PackedLayout L;
+  if (!packed_layout(c, L))
+    return fail(SAS_ERR_UNSUPPORTED, "no packed decode layout for this configuration (bf16 with d, H*dh and "
+                                     "d_ff multiples of 128)");
+  if (!w) return fail(SAS_ERR_INVALID_ARGUMENT, "weights are NULL");
+  SAS_TRY(check_ptr(w->wq, "wq", true));
+  SAS_TRY(check_ptr(w->wk, "wk", true));
+  SAS_TRY(check_ptr(w->wv, "wv", true));
+  SAS_TRY(check_ptr(w->wo, "wo", true));
+  SAS_TRY(check_ptr(w->w_gate, "w_gate", true));
+  SAS_TRY(check_ptr(w->w_up, "w_up", true));
+  SAS_TRY(check_ptr(w->w_down, "w_down", true));
+  SAS_TRY(check_ptr(packed, "packed", true));
+  if (((uintptr_t)packed & 255u) != 0) return fail(SAS_ERR_INVALID_ARGUMENT, "packed is not 256-byte aligned");
+  if (packed_bytes < L.total)
+    return fail(SAS_ERR_WORKSPACE, "packed holds %zu bytes, the layer's packed copy needs %zu", packed_bytes,
+                L.total);
+  hipStream_t s = (hipStream_t)stream;
+  const int d = c->d_model, H = c->n_heads, Hkv = c->n_kv_heads, dh = c->head_dim, F = c->d_ff;
+  char* out = (char*)packed;
+  auto pack = [&](int epi, int N, int K, const void* b0, const void* b1, const void* b2, size_t off) {
+    GemmArgs a = {};
+    a.epi = epi;
+    a.N = N;
+    a.K = K;
+    a.B0 = b0;
+    a.B1 = b1;
+    a.B2 = b2;
+    a.n_heads = H;
+    a.n_kv_heads = Hkv;
+    a.head_dim = dh;
+    return launch_gemv_pack(a, out + off, s);
+  };
+  HIP_TRY(pack(EPI_QKV_ROPE, (H + 2 * Hkv) * dh, d, w->wq, w->wk, w->wv, L.qkv), "pack qkv");
+  HIP_TRY(pack(EPI_RESID, d, H * dh, w->wo, nullptr, nullptr, L.o), "pack o");
+  HIP_TRY(pack(EPI_SWIGLU, F, d, w->w_gate, w->w_up, nullptr, L.gu), "pack gate/up");
+  HIP_TRY(pack(EPI_RESID, d, F, w->w_down, nullptr, nullptr, L.down), "pack down");
+  return SAS_OK;
+}
+
 sas_status sas_decode_step(const sas_config* c, int32_t batch, const void* x, const int32_t* pos,
                            const sas_layer_weights* w, sas_paged_kv* cache, void* y, int32_t* sel_idx,
                            sas_layer_taps* taps, void* ws, size_t ws_bytes, void* stream) {
@@ -1171,6 +1245,9 @@ sas_status sas_decode_step(const sas_config* c, int32_t batch, const void* x, co
   // (unless a summary projection follows the append).
   const bool gemv = c->dtype == SAS_BF16 && batch <= 16 && c->d_model % 128 == 0;
   const bool fused_append = gemv && !da.w_gk;
+  // the packed copy of the weights, streamed by the skinny-GEMM path when given
+  PackedLayout pl;
+  const char* pk = (gemv && w->decode_packed && packed_layout(c, pl)) ? (const char*)w->decode_packed : nullptr;
   {
     Timed tm("rmsnorm", s);
     HIP_TRY(launch_rmsnorm_rope(c->dtype, x, w->rms1, dw.u1, batch, c->d_model, c->rms_eps, pos, dw.rope, dh,
@@ -1195,6 +1272,7 @@ sas_status sas_decode_step(const sas_config* c, int32_t batch, const void* x, co
   g.rope = dw.rope;
   g.row_pos = fused_append ? pos : nullptr;
   g.append = fused_append ? &da : nullptr;
+  g.packed = pk ? pk + pl.qkv : nullptr;
   {
     Timed tm("dec_qkv", s);
     HIP_TRY(small_gemm(c->dtype, g, s), "qkv gemm");
@@ -1220,6 +1298,7 @@ sas_status sas_decode_step(const sas_config* c, int32_t batch, const void* x, co
   og.N = c->d_model;
   og.resid = x;
   og.out = dw.h1;
+  og.packed = pk ? pk + pl.o : nullptr;
   {
     Timed tm("dec_o", s);
     HIP_TRY(small_gemm(c->dtype, og, s), "o-proj gemm");
@@ -1237,6 +1316,7 @@ sas_status sas_decode_step(const sas_config* c, int32_t batch, const void* x, co
   gu.B1 = w->w_up;
   gu.N = c->d_ff;
   gu.out = dw.mlp.a;
+  gu.packed = pk ? pk + pl.gu : nullptr;
   {
     Timed tm("dec_gate_up", s);
     HIP_TRY(small_gemm(c->dtype, gu, s), "gate/up gemm");
@@ -1250,6 +1330,7 @@ sas_status sas_decode_step(const sas_config* c, int32_t batch, const void* x, co
   dg.N = c->d_model;
   dg.resid = dw.h1;
   dg.out = y;
+  dg.packed = pk ? pk + pl.down : nullptr;
   {
     Timed tm("dec_down", s);
     HIP_TRY(small_gemm(c->dtype, dg, s), "down gemm");

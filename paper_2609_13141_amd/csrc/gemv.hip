@@ -1,20 +1,19 @@
 // Skinny GEMM for decode: out = A[M, K] W^T with M <= 16 rows (the batch of
 // new tokens), bound by streaming W from HBM.
 //
-// One workgroup per 16 output columns; its waves split K.  v_mfma_f32_16x16x32_bf16
-// takes A (activations, 16 rows, rows >= M zero) and W^T (16 columns).  The
-// MFMA only needs A and B to enumerate k the same way, so the k slice of MFMA
-// j of a 128-wide chunk is chosen to make each load instruction contiguous per
-// row: lane l reads the 16 bytes at k = kb + 32 j + 8 (l/16) of row l % 16, so
-// one instruction covers 16 rows x 64 contiguous bytes (half a cache line each)
-// and the chunk's four instructions cover 16 rows x 256 bytes.  Partial sums of
-// the waves are added in LDS.
+// One workgroup per 16 output columns; its 4 waves split K into contiguous
+// ranges of 32-wide steps.  v_mfma_f32_16x16x32_bf16 takes A (activations, 16
+// rows, rows >= M zero) and W^T (16 columns).  The MFMA only needs A and B to
+// enumerate k the same way, so the k slice of a step is chosen to make each
+// load instruction contiguous: lane l reads the 16 bytes at k = 32 st +
+// 8 (l/16) of row l % 16, so that with row-major weights one instruction
+// covers 16 rows x 64 contiguous bytes, and with the packed decode layout
+// (sas_pack_decode_weights) 1 KB of consecutive bytes.  Partial sums of the
+// waves are added in LDS.
 //
 // Column groups of the pair epilogues hold 8 first-half and 8 second-half
 // columns (RoPE: i and i + dh/2 of a head; SwiGLU: gate f and up f); a lane's
 // partner is lane ^ 8 after the reduction.
-#include <algorithm>
-
 #include "common.h"
 #include "kernels.h"
 
@@ -33,6 +32,7 @@ struct GemvParams {
   int H, Hkv, dh;
   const float2* rope;  // [M, dh/2] per-row rotary table
   const int32_t* pos;  // [M] positions (cache append)
+  const bf16_t* packed;  // the weights in the packed decode layout, or NULL
   // cache append (QKV epilogue): K/V rows into their pages, and the summary of
   // a block completed by this position (NULL k_pages: no append)
   void* k_pages;
@@ -198,53 +198,73 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams& P, int gi, int c
   }
 }
 
-// One workgroup per 16-column group, its waves splitting K (the shapes the
-// streaming kernel below does not cover).
-template <int NW>
+// The packed decode layout: the 16 columns x 32 k of step st of column group
+// gi form one 1-KB block at element ((gi * K/32 + st) * 64 + l) * 8 for lane
+// l, holding row(gi, l % 16)[st * 32 + (l / 16) * 8 ..+8]: the fragment lane l
+// of the 16x16x32 MFMA takes, so a wave's load is 1 KB of consecutive bytes.
+__global__ void gemv_pack_kernel(GemvParams P, bf16_t* __restrict__ out, size_t chunks) {
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;  // one 16-byte chunk
+  if (idx >= chunks) return;
+  const int nsteps = P.K / 32;
+  const int l = (int)(idx % 64);
+  const size_t r = idx / 64;
+  const int st = (int)(r % nsteps), gi = (int)(r / nsteps);
+  bool valid;
+  const bf16_t* row = gemv_row(P, gi, l & 15, valid);  // clamped: columns past the end repeat the last row
+  *(uint4*)(out + idx * 8) = *(const uint4*)(row + st * 32 + (l >> 4) * 8);
+}
+
+// One workgroup per 16-column group, its waves splitting K.  Lane (c, kg)
+// multiplies step st's weights -- row-major:
+// row(gi, c)[st * 32 + kg * 8 ..]; packed: its 16 bytes of block (gi, st) --
+// by the activation rows' elements st * 32 + kg * 8 ..; both layouts give
+// the same products in the same order.
+template <int NW, int EPI>
 __global__ void __launch_bounds__(NW * 64) gemv_kernel(GemvParams P) {
   __shared__ floatx4_t part[NW][64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int gi = blockIdx.x;
   const int c = lane & 15, kg = lane >> 4;
-  bool cvalid;
-  const bf16_t* wr = gemv_row(P, gi, c, cvalid);
+  const bf16_t* wr;
+  size_t wstep;
+  if (P.packed) {
+    wr = P.packed + ((size_t)gi * (P.K / 32) * 64 + lane) * 8;
+    wstep = 512;
+  } else {
+    bool cvalid;
+    wr = gemv_row<EPI>(P, gi, c, cvalid) + kg * 8;
+    wstep = 32;
+  }
   const int arow = min(c, P.M - 1);
   const bool avalid = c < P.M;
-  const bf16_t* ar = P.A + (size_t)arow * P.K;
+  const bf16_t* ar = P.A + (size_t)arow * P.K + kg * 8;
   GemvPre pre;
-  if (wave == 0) gemv_prepare(P, gi, c, kg, pre);
+  if (wave == 0) gemv_prepare<EPI>(P, gi, c, kg, pre);
 
-  // this wave's k range, in chunks of 128
-  const int nchunk = P.K / 128;
-  const int per = (nchunk + NW - 1) / NW;
-  const int c0 = wave * per, c1 = min(nchunk, c0 + per);
+  // this wave's range of 32-wide k steps
+  const int steps = P.K / 32;
+  const int per = (steps + NW - 1) / NW;
+  const int s0 = wave * per, s1 = min(steps, s0 + per);
 
   floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
-  int ch = c0;
-  for (; ch + 2 <= c1; ch += 2) {
+  int st = s0;
+  for (; st + 8 <= s1; st += 8) {
     uint4 w[8], a[8];
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int k = (ch + u) * 128 + j * 32 + kg * 8;
-        w[u * 4 + j] = *(const uint4*)(wr + k);
-        a[u * 4 + j] = *(const uint4*)(ar + k);
-      }
+    for (int q = 0; q < 8; ++q) {
+      w[q] = *(const uint4*)(wr + (size_t)(st + q) * wstep);
+      a[q] = *(const uint4*)(ar + (st + q) * 32);
+    }
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
       if (!avalid) a[q] = make_uint4(0, 0, 0, 0);
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(bf16x8_t*)&a[q], *(bf16x8_t*)&w[q], acc, 0, 0, 0);
     }
   }
-  for (; ch < c1; ++ch) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int k = ch * 128 + j * 32 + kg * 8;
-      uint4 w = *(const uint4*)(wr + k);
-      uint4 a = avalid ? *(const uint4*)(ar + k) : make_uint4(0, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(bf16x8_t*)&a, *(bf16x8_t*)&w, acc, 0, 0, 0);
-    }
+  for (; st < s1; ++st) {
+    uint4 w = *(const uint4*)(wr + (size_t)st * wstep);
+    uint4 a = avalid ? *(const uint4*)(ar + st * 32) : make_uint4(0, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(bf16x8_t*)&a, *(bf16x8_t*)&w, acc, 0, 0, 0);
   }
   part[wave][lane] = acc;
   __syncthreads();
@@ -256,115 +276,12 @@ __global__ void __launch_bounds__(NW * 64) gemv_kernel(GemvParams P) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) tot[v] += p[v];
   }
-  gemv_epilogue(P, gi, c, kg, tot, pre);
-}
-
-// ---------------------------------------------------------------------------
-// Streaming kernel: one workgroup of NW waves per compute unit, looping over
-// 16-column groups (group gi = blockIdx.x + j * gridDim.x).  Wave w owns the
-// 32-wide k steps [w * per, w * per + nst) and keeps its slice of the
-// activation rows in registers for the whole launch (KS steps: one 16-byte
-// fragment per lane and step), so the activation is read once per workgroup
-// instead of once per column group, and only weights stream in the loop.
-// The weight fragments of a group flow through a ring of R registers: after
-// the MFMA of step i the ring slot is refilled with step i + R, which past
-// the group's last step is a step of the workgroup's next group, so the
-// stream does not drain between groups.  Steps beyond the wave's range (when
-// K / 32 is not KS * NW) multiply zero activations with weights loaded from a
-// clamped in-range address.  The waves' partial sums meet in LDS
-// (double-buffered, one barrier per group that does not wait for the loads
-// in flight) and one wave, changing from group to group, applies the
-// epilogue.  It pays where each workgroup has several column groups to
-// stream (the SwiGLU product of a layer); with one or two per workgroup the
-// per-group kernel above is faster.
-template <int EPI, int NW, int KS, int R, bool FULL>
-__global__ void __launch_bounds__(NW * 64) gemv_stream_kernel(GemvParams P, int ngroups) {
-  static_assert(KS % R == 0, "the ring must divide the steps");
-  __shared__ floatx4_t part[2][NW][64];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int c = lane & 15, kg = lane >> 4;
-  const int steps = P.K / 32;
-  const int per = FULL ? KS : (steps + NW - 1) / NW;
-  const int s0 = wave * per;
-  const int nst = FULL ? KS : max(0, min(steps, s0 + per) - s0);
-  const int slast = max(min(s0 + nst, steps) - 1, 0);  // last in-range step (clamp target)
-  // k step i of this wave, clamped into its range unless every wave owns KS steps
-  auto step_of = [&](int i) { return FULL ? s0 + i : min(s0 + i, slast); };
-  const bool rvalid = c < P.M;
-
-  // weight fragment of step i of group gi (k clamped into the wave's range)
-  auto wrow = [&](int gi) {
-    bool v;
-    return gemv_row<EPI>(P, gi, c, v) + 8 * kg;
-  };
-  auto wload = [&](const bf16_t* wr, int i) { return *(const uint4*)(wr + (size_t)step_of(i) * 32); };
-  // the activation slice: rows >= M and steps past the wave's range are zero
-  uint4 a[KS];
-  {
-    const bf16_t* ar = P.A + (size_t)min(c, P.M - 1) * P.K + 8 * kg;
-#pragma unroll
-    for (int i = 0; i < KS; ++i) {
-      const uint4 v = *(const uint4*)(ar + (size_t)step_of(i) * 32);
-      a[i] = (i < nst && rvalid) ? v : make_uint4(0, 0, 0, 0);
-    }
-  }
-  int gi = blockIdx.x;
-  if (gi >= ngroups) return;
-  const bf16_t* wr = wrow(gi);
-  uint4 w[R];
-#pragma unroll
-  for (int r = 0; r < R; ++r) w[r] = wload(wr, r);
-  for (int it = 0; gi < ngroups; ++it) {
-    const int gn = gi + (int)gridDim.x < ngroups ? gi + (int)gridDim.x : gi;  // next group (or this one again)
-    const bf16_t* wn = wrow(gn);
-    GemvPre pre;
-    const int reducer = it % NW;
-    if (wave == reducer) gemv_prepare<EPI>(P, gi, c, kg, pre);
-    floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int i = 0; i < KS; ++i) {
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(bf16x8_t*)&a[i], *(bf16x8_t*)&w[i % R], acc, 0, 0, 0);
-      w[i % R] = i + R < KS ? wload(wr, i + R) : wload(wn, i + R - KS);
-    }
-    part[it & 1][wave][lane] = acc;
-    lds_barrier();
-    if (wave == reducer) {
-      floatx4_t tot = part[it & 1][0][lane];
-#pragma unroll
-      for (int wv = 1; wv < NW; ++wv) {
-        const floatx4_t p = part[it & 1][wv][lane];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) tot[v] += p[v];
-      }
-      gemv_epilogue<EPI>(P, gi, c, kg, tot, pre);
-    }
-    gi += gridDim.x;
-    wr = wn;
-  }
-}
-
-// Streaming launch: 4 waves of 32 steps of 32 (128 registers of activation
-// per lane) and a ring of 8, so K <= 4096; the FULL variant for K = 4096
-// exactly (every wave owns 32 steps: loads at immediate offsets).
-constexpr int GV_NW = 4, GV_KS = 32, GV_R = 8;
-
-static bool gemv_streams(const GemmArgs& g) {
-  return g.epi == EPI_SWIGLU && g.K % 32 == 0 && g.K <= GV_NW * GV_KS * 32;
-}
-
-template <bool FULL>
-static hipError_t run_stream(const GemvParams& P, int groups, hipStream_t s) {
-  auto kern = gemv_stream_kernel<EPI_SWIGLU, GV_NW, GV_KS, GV_R, FULL>;
-  static int resident = 0;
-  if (resident <= 0) resident = resident_workgroups(kern, GV_NW * 64);
-  if (resident <= 0) return hipErrorInvalidValue;
-  return launch_ext(kern, dim3(std::min(groups, resident)), dim3(GV_NW * 64), 0, s, P, groups);
+  gemv_epilogue<EPI>(P, gi, c, kg, tot, pre);
 }
 
 hipError_t launch_gemv(const GemmArgs& g, hipStream_t s) {
   if (g.M <= 0) return hipSuccess;
-  const bool stream = gemv_streams(g);
-  if (g.M > 16 || (!stream && g.K % 128 != 0)) return hipErrorInvalidValue;
+  if (g.M > 16 || g.K % 128 != 0) return hipErrorInvalidValue;
   GemvParams P;
   P.epi = g.epi;
   P.M = g.M;
@@ -384,6 +301,7 @@ hipError_t launch_gemv(const GemmArgs& g, hipStream_t s) {
   P.dh = g.head_dim;
   P.rope = g.rope;
   P.pos = g.row_pos;
+  P.packed = (const bf16_t*)g.packed;
   P.k_pages = nullptr;
   P.v_pages = nullptr;
   P.k_summary = nullptr;
@@ -404,12 +322,45 @@ hipError_t launch_gemv(const GemmArgs& g, hipStream_t s) {
     }
   }
   const int groups = (g.epi == EPI_RESID || g.epi == EPI_F32OUT) ? (g.N + 15) / 16 : (P.npairs + 7) / 8;
-  if (stream) {
-    return g.K == GV_NW * GV_KS * 32 ? run_stream<true>(P, groups, s) : run_stream<false>(P, groups, s);
+  // 4 waves per group: as fast as or faster than 8 or 16 waves at the decode
+  // shapes (measured: QKV 22.6 vs 23.8 us, down 21.9 vs 22.7 us, O equal)
+  constexpr int NW = 4;
+  const dim3 grid(groups), block(NW * 64);
+  switch (g.epi) {
+    case EPI_QKV_ROPE: return launch_ext(gemv_kernel<NW, EPI_QKV_ROPE>, grid, block, 0, s, P);
+    case EPI_SWIGLU: return launch_ext(gemv_kernel<NW, EPI_SWIGLU>, grid, block, 0, s, P);
+    case EPI_F32OUT: return launch_ext(gemv_kernel<NW, EPI_F32OUT>, grid, block, 0, s, P);
+    default: return launch_ext(gemv_kernel<NW, EPI_RESID>, grid, block, 0, s, P);
   }
-  // 4 waves per group: measured as fast as or faster than 8 or 16 waves at
-  // the decode shapes (QKV 22.6 vs 23.8 us, down 21.9 vs 22.7 us, O equal)
-  gemv_kernel<4><<<groups, 256, 0, s>>>(P);
+}
+
+static GemvParams pack_params(const GemmArgs& g) {
+  GemvParams P = {};
+  P.epi = g.epi;
+  P.M = 1;
+  P.K = g.K;
+  P.N = g.N;
+  P.npairs = g.epi == EPI_SWIGLU ? g.N : (g.epi == EPI_QKV_ROPE ? g.N / 2 : 0);
+  P.B0 = (const bf16_t*)g.B0;
+  P.B1 = (const bf16_t*)g.B1;
+  P.B2 = (const bf16_t*)g.B2;
+  P.H = g.n_heads;
+  P.Hkv = g.n_kv_heads;
+  P.dh = g.head_dim;
+  return P;
+}
+
+size_t gemv_packed_elems(const GemmArgs& g) {
+  const GemvParams P = pack_params(g);
+  const size_t groups = (P.epi == EPI_RESID || P.epi == EPI_F32OUT) ? (P.N + 15) / 16 : (P.npairs + 7) / 8;
+  return groups * (size_t)(g.K / 32) * 512;
+}
+
+hipError_t launch_gemv_pack(const GemmArgs& g, void* out, hipStream_t s) {
+  if (g.K % 128 != 0 || g.N <= 0) return hipErrorInvalidValue;
+  const GemvParams P = pack_params(g);
+  const size_t chunks = gemv_packed_elems(g) / 8;
+  gemv_pack_kernel<<<(unsigned)((chunks + 255) / 256), 256, 0, s>>>(P, (bf16_t*)out, chunks);
   return hipGetLastError();
 }
 

@@ -77,6 +77,8 @@ struct GemmArgs {
   // rows' positions) also writes K/V into the paged cache and completes block
   // summaries
   const struct DecodeArgs* append;
+  // decode (launch_gemv): the product's weights in the packed decode layout, or NULL
+  const void* packed;
 };
 hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s);
 
@@ -84,6 +86,12 @@ hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s);
 // The same products for M <= 16 rows (bf16, K % 128 == 0), streaming the
 // weights: rope is a per-row table [M, dh/2]; EPI_F32OUT writes fp32 A W^T.
 hipError_t launch_gemv(const GemmArgs& a, hipStream_t s);
+// The packed decode layout of a product (see sas_pack_decode_weights): its
+// size in elements, and the kernel that writes it from the row-major B0..B2
+// of `a` (epi, N, K as launch_gemv takes them).  With a.packed set,
+// launch_gemv streams the packed copy instead.
+size_t gemv_packed_elems(const GemmArgs& a);
+hipError_t launch_gemv_pack(const GemmArgs& a, void* out, hipStream_t s);
 
 // Variable-length packing: doc[b, NB] holds, for each block, the first block of
 // its document; a query's historical blocks are [doc_first(t), t / B).  The

@@ -17,15 +17,19 @@ from .configs import Workload
 
 class Stack:
     def __init__(self, w: Workload, layers: list, ends: dict, *, max_len: int, page_size: int | None = None,
-                 device="cuda"):
+                 device="cuda", packed: bool = True):
         """layers: per-layer device weight dicts; ends: device tensors
-        'embed' [V, d], 'w_lm' [V, d], 'rms_final' [d]."""
+        'embed' [V, d], 'w_lm' [V, d], 'rms_final' [d].  packed: the decode
+        steps stream a packed copy of each layer's linear weights (made here
+        when the configuration has a packed layout; results are identical)."""
         self.w = w
-        self.layers = layers
         self.ends = ends
         self.device = device
         self.cfg_prefill = sas.make_config(w, "dense")
         self.cfg_decode = sas.make_config(w, "sparse")
+        if packed and sas.lib().sas_decode_packed_bytes(sas.C.byref(self.cfg_decode)) > 0:
+            layers = [sas.pack_decode_weights(self.cfg_decode, W) for W in layers]
+        self.layers = layers
         ps = page_size or w.page_size
         self.caches = [sas.alloc_cache(self.cfg_decode, w.batch, max_len, page_size=ps, device=device, seed=l)
                        for l in range(len(layers))]

@@ -29,7 +29,8 @@ TORCH_DTYPE = {"bf16": torch.bfloat16, "f32": torch.float32}
 
 EXPORTS = ("sas_workspace_size", "sas_attention_prefill", "sas_mlp_forward", "sas_layer_forward",
            "sas_decode_step", "sas_decode_step_noalloc", "sas_decode_select", "sas_attention_backward", "sas_selector_backward", "sas_selection_stats", "sas_overlap_recall", "sas_embed", "sas_lm_head_argmax", "sas_last_error", "sas_version",
-           "sas_profiler_start", "sas_profiler_select", "sas_profiler_stop", "sas_profiler_record")
+           "sas_profiler_start", "sas_profiler_select", "sas_profiler_stop", "sas_profiler_record",
+           "sas_decode_packed_bytes", "sas_pack_decode_weights")
 
 
 class SasError(RuntimeError):
@@ -83,7 +84,7 @@ class SelBwdOut(C.Structure):
 
 class LayerWeights(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in ("rms1", "wq", "wk", "wv", "wo", "rms2", "w_gate", "w_up",
-                                          "w_down", "w_gq", "w_gk")]
+                                          "w_down", "w_gq", "w_gk", "decode_packed")]
 
 
 class LayerTaps(C.Structure):
@@ -149,6 +150,10 @@ def lib() -> C.CDLL:
     L.sas_profiler_start.argtypes = [i32]
     L.sas_profiler_select.restype = i32
     L.sas_profiler_select.argtypes = [C.c_char_p]
+    L.sas_decode_packed_bytes.restype = sz
+    L.sas_decode_packed_bytes.argtypes = [C.POINTER(Config)]
+    L.sas_pack_decode_weights.restype = i32
+    L.sas_pack_decode_weights.argtypes = [C.POINTER(Config), C.POINTER(LayerWeights), vp, sz, vp]
     L.sas_profiler_stop.restype = i32
     L.sas_profiler_stop.argtypes = []
     L.sas_profiler_record.restype = i32
@@ -211,7 +216,7 @@ def _ws(ws: Workspace | None, nbytes: int):
 
 def weights_struct(W: dict) -> LayerWeights:
     return LayerWeights(*[_ptr(W.get(k)) for k in ("rms1", "wq", "wk", "wv", "wo", "rms2", "w_gate",
-                                                   "w_up", "w_down", "w_gq", "w_gk")])
+                                                   "w_up", "w_down", "w_gq", "w_gk", "decode_packed")])
 
 
 def attention_prefill(cfg: Config, q, k, v, w_gq=None, w_gk=None, *, lse=True, k_summary=True,
@@ -437,6 +442,23 @@ def alloc_cache(cfg: Config, batch: int, max_len: int, page_size: int = 16, devi
     nblk = -(-max_len // cfg.block_size)
     k_summary = torch.zeros(batch, Hkv, nblk, dh, dtype=dt, device=device)
     return PagedCache(k_pages, v_pages, block_table, k_summary, page_size)
+
+
+def pack_decode_weights(cfg: Config, W: dict):
+    """The layer's linear weights in the packed decode layout (a new uint8
+    tensor on W's device); returns W with "decode_packed" set to it, so that
+    decode steps stream the packed copy."""
+    n = lib().sas_decode_packed_bytes(C.byref(cfg))
+    if n == 0:
+        raise SasError("no packed decode layout for this configuration")
+    out = torch.empty(n + 256, dtype=torch.uint8, device=W["wq"].device)
+    off = (-out.data_ptr()) % 256  # 256-byte aligned view
+    buf = out[off:off + n]
+    ws = weights_struct(W)
+    _check(lib().sas_pack_decode_weights(C.byref(cfg), C.byref(ws), _ptr(buf), n, _stream()))
+    W2 = dict(W)
+    W2["decode_packed"] = buf
+    return W2
 
 
 def decode_step(cfg: Config, x, pos, W: dict, cache: PagedCache, *, sel_idx: bool = True,

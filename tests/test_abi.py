@@ -109,3 +109,23 @@ def test_noalloc_decode_rejects_oversized_calls_before_touching_the_gpu(L):
                                    fake, None, None)
     assert st == -3   # SAS_ERR_WORKSPACE
     assert b"static" in L.sas_last_error() and b"scratch" in L.sas_last_error()
+
+
+def test_packed_decode_layout_size_and_validation(L):
+    # the packed copy holds every linear weight exactly once when the column
+    # groups divide the products (16 columns, 8 rotary or gate/up pairs)
+    for w in (configs.STACK_DECODE, configs.BY_NAME["gqa28x4_layer_16k"]):
+        cfg = sas.make_config(w, "sparse")
+        d, H, Hkv, dh, F = w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.d_ff
+        weights = 2 * (d * (H + 2 * Hkv) * dh + d * H * dh + 2 * d * F + F * d)
+        assert L.sas_decode_packed_bytes(C.byref(cfg)) == weights
+    f32 = sas.make_config(configs.BY_NAME["tiny_1layer_f32"], "sparse")
+    assert L.sas_decode_packed_bytes(C.byref(f32)) == 0
+    # validation fails before any launch: missing weights, misalignment, short buffer
+    cfg = sas.make_config(configs.STACK_DECODE, "sparse")
+    n = L.sas_decode_packed_bytes(C.byref(cfg))
+    ws = sas.LayerWeights(*([0x1000] * 9 + [None, None, None]))
+    assert L.sas_pack_decode_weights(C.byref(cfg), None, 0x1000, n, None) == sas.SAS_ERR_INVALID_ARGUMENT
+    assert L.sas_pack_decode_weights(C.byref(cfg), C.byref(ws), 0x1010, n, None) == sas.SAS_ERR_INVALID_ARGUMENT
+    assert L.sas_pack_decode_weights(C.byref(cfg), C.byref(ws), 0x1000, n - 1, None) == sas.SAS_ERR_WORKSPACE
+    assert L.sas_pack_decode_weights(C.byref(f32), C.byref(ws), 0x1000, n, None) == sas.SAS_ERR_UNSUPPORTED
