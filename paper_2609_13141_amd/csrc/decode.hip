@@ -479,6 +479,22 @@ struct DecodeSeg {
 constexpr int DSEG_MAX = 33 * 8;   // segments of a split: (K + 1) blocks of at most 8 segments
 constexpr int DPAGE_MAX = 33 * 64;  // page ids of a split: (K + 1) blocks of at most 64 pages
 
+// Sum over groups of NC consecutive lanes (NC = 8 or 16) with DPP moves:
+// swaps within pairs and quads, then the mirror of each 8 and of each 16.
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+template <int NC>
+__device__ __forceinline__ float lane_group_sum(float v) {
+  static_assert(NC == 8 || NC == 16, "groups of 8 or 16 lanes");
+  v += dpp_move<0xB1>(v);                       // quad_perm 1,0,3,2
+  v += dpp_move<0x4E>(v);                       // quad_perm 2,3,0,1
+  v += dpp_move<0x141>(v);                      // row_half_mirror
+  if constexpr (NC == 16) v += dpp_move<0x140>(v);  // row_mirror
+  return v;
+}
+
 template <typename T, int DH, int GMAX, int NW>
 __global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restrict__ q, DecodeArgs c,
                                                               const int32_t* __restrict__ sel, int nsplit,
@@ -496,14 +512,16 @@ __global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restric
   const int split = blockIdx.x / nhc, hc = blockIdx.x % nhc;
   const int g = blockIdx.y, i = blockIdx.z;
   const int K = c.K, B = c.B;
-  const int spb = B > SEG ? B / SEG : 1;  // segments per block
+  const int spb = B > SEG ? B / SEG : 1;  // segments per block (a power of two)
+  const int spb_shift = __builtin_ctz(spb);
   const int seg_len = B > SEG ? SEG : B;
   const int nseg = (K + 1) * spb;
   const int per = (nseg + nsplit - 1) / nsplit;
   const int s0 = split * per, s1 = min(nseg, s0 + per);
   const int p = c.pos[i];
   const int sl = lane % NC, kq = lane / NC;
-  const int ps = c.page_size;
+  const int ps = c.page_size;  // a power of two (it divides the power-of-two block size)
+  const int pshift = __builtin_ctz(ps);
   const size_t kvstride = (size_t)c.Hkv * ps * DH;  // elements per page
 
   // block of selection slot ch (slot K: the current block), -1 if none
@@ -539,8 +557,8 @@ __global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restric
   // loads of the pool's start), so that every call issues the same loads
   auto load = [&](Seg& S, int t) {
     const bool live = t < ns;
-    const int sg = s0 + (live ? t : 0), chl = sg / spb - ch0;
-    const int base = (sg % spb) * seg_len;  // the segment's first key within its block
+    const int sg = s0 + (live ? t : 0), chl = (sg >> spb_shift) - ch0;
+    const int base = (sg & (spb - 1)) * seg_len;  // the segment's first key within its block
     S.count = live ? sm_count[t] : 0;
     // offsets first, then every load unconditionally (keys without a page read
     // the start of the pool and are masked by ok): loads under divergent
@@ -550,9 +568,9 @@ __global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restric
     for (int it = 0; it < IT; ++it) {
       const int kl = kq + KPI * it;
       const int a = base + kl;  // key within the block
-      const int page = kl < S.count ? sm_pages[chl * ppb + a / ps] : -1;
+      const int page = kl < S.count ? sm_pages[chl * ppb + (a >> pshift)] : -1;
       S.ok[it] = page >= 0;
-      off[it] = S.ok[it] ? (size_t)page * kvstride + ((size_t)g * ps + a % ps) * DH + sl * 8 : 0;
+      off[it] = S.ok[it] ? (size_t)page * kvstride + (uint32_t)(((g << pshift) + (a & (ps - 1))) * DH + sl * 8) : 0;
     }
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
@@ -575,14 +593,24 @@ __global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restric
   // and the next loads into these registers need no wait for older loads.
   // the scaled query slices of the chunk's heads, loaded once: a query load
   // issued after a segment's loads would make its use wait for all of them
+  // (bf16: the raw query pairs, for bf16 dot products; the scale is applied
+  // to the reduced score)
+  constexpr bool BF = sizeof(T) == 2;
   float qsl[GMAX][8];
+  uint32_t qpair[GMAX][4];
 #pragma unroll
   for (int hg = 0; hg < GMAX; ++hg) {
     const int hl = min(hc * GMAX + hg, G - 1);
     Vec8<T> v;
     v.load(q + ((size_t)i * c.H + g * G + hl) * DH + sl * 8);
+    if constexpr (BF) {
+      const uint32_t* w = (const uint32_t*)&v;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) qsl[hg][e] = v.get(e) * c.sm_scale;
+      for (int e = 0; e < 4; ++e) qpair[hg][e] = w[e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qsl[hg][e] = v.get(e) * c.sm_scale;
+    }
   }
   auto compute = [&](const Seg& S) {
 #pragma unroll
@@ -595,11 +623,19 @@ __global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restric
 #pragma unroll
       for (int it = 0; it < IT; ++it) {
         float acc = 0.f;
+        if constexpr (BF) {
+          const uint32_t* kw = (const uint32_t*)&S.k[it];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc = fmaf(qs[e], S.k[it].get(e), acc);
+          for (int e = 0; e < 4; ++e)
+            acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, kw[e]),
+                                                  __builtin_bit_cast(bf16x2_t, qpair[hg][e]), acc, false);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc = fmaf(qs[e], S.k[it].get(e), acc);
+        }
         acc = S.ok[it] ? acc : 0.f;
-#pragma unroll
-        for (int off = NC / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+        acc = lane_group_sum<NC>(acc);
+        if constexpr (BF) acc *= c.sm_scale;
         sc[it] = kq + KPI * it < S.count ? acc : -INFINITY;
         mx = fmaxf(mx, sc[it]);
       }
@@ -615,12 +651,20 @@ __global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restric
       for (int it = 0; it < IT; ++it) {
         const float pk = any && kq + KPI * it < S.count ? __expf(sc[it] - mn) : 0.f;
         l[hg] += pk;
-        const float pv = S.ok[it] ? pk : 0.f;
+        // keys without data read arbitrary bytes: their values are zeroed
+        // (the probability alone would give 0 x NaN)
+        Vec8<T> vz = S.v[it];
+        if constexpr (BF) {
+          uint32_t* vw = (uint32_t*)&vz;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float vv = S.ok[it] ? S.v[it].get(e) : 0.f;
-          o[hg][e] = fmaf(pv, vv, o[hg][e]);
+          for (int e = 0; e < 4; ++e) vw[e] = S.ok[it] ? vw[e] : 0u;
+        } else {
+          float* vf = (float*)&vz;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) vf[e] = S.ok[it] ? vf[e] : 0.f;
         }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[hg][e] = fmaf(pk, vz.get(e), o[hg][e]);
       }
     }
   };
