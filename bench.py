@@ -44,6 +44,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "paper_2609_13141_amd", "csrc")
 PROFILES = os.path.join(HERE, "profiles")
 COPY_BYTES = 512 * 2**20  # calibration copy: reads and writes this many bytes once
+COPY_KERNEL = "__amd_rocclr_copyBuffer"  # the runtime's blit kernel of a device-to-device copy
 
 # Dominant kernels of the headline step and their HBM-traffic summaries
 # (written by --pmc-summary from rocprofv3 --pmc runs of --only-headline).
@@ -109,7 +110,7 @@ def pmc_means(run_dir, counter):
                 continue
             name = r["Kernel_Name"]
             key = next((k for k, d in DOMINANT.items() if d["kernel"] in name), None)
-            if key is None and "copy" in name.lower():
+            if key is None and COPY_KERNEL in name:
                 key = "copy"
             if key:
                 d = vals[key]
@@ -258,7 +259,7 @@ def write_hbm_summary(fetch_dir, write_dir, out, cmd, min_kib=64.0):
     wr, _, _ = _counter_means(write_dir)
     # the calibration copy: the largest dispatch of a copy kernel
     cpf, cpw = _counter_means(fetch_dir, peak=True)[0], _counter_means(write_dir, peak=True)[0]
-    copies = [k for k in fe if "copy" in k.lower()]
+    copies = [k for k in fe if COPY_KERNEL in k]
     cf = max((cpf[k]["FETCH_SIZE"] for k in copies), default=0.0)
     cw = max((cpw[k]["WRITE_SIZE"] for k in copies if k in cpw), default=0.0)
     if not cf or not cw:
@@ -790,6 +791,8 @@ def main():
     }
     line.update(head)
     if args.calibrate_copy:
+        # same dtype, contiguous: torch issues a device-to-device copy, which the
+        # runtime runs as its blit kernel (the one the counter summaries look for)
         src = torch.empty(COPY_BYTES // 2, dtype=torch.bfloat16, device="cuda:0")
         dst = torch.empty_like(src)
         for _ in range(2):

@@ -15,7 +15,7 @@
 using namespace sas;
 
 namespace sas {
-LaunchEvents g_launch_events = {nullptr, nullptr};  // see kernels.h
+LaunchEvents g_launch_events = {nullptr, nullptr, 0};  // see kernels.h
 }
 
 namespace {
@@ -97,14 +97,14 @@ struct Profiler {
     if (!on || used >= (int)names.size() || !wanted(name)) return -1;
     names[used] = name;
     (void)hipEventRecord(ev[4 * used], s);
-    g_launch_events = LaunchEvents{ev[4 * used + 2], ev[4 * used + 3]};
+    g_launch_events = LaunchEvents{ev[4 * used + 2], ev[4 * used + 3], 0};
     return used++;
   }
   void end(int id, hipStream_t s) {
     if (id < 0) return;
     (void)hipEventRecord(ev[4 * id + 1], s);
-    exact[id] = g_launch_events.start == nullptr;  // consumed by exactly the one launch that took it
-    g_launch_events = LaunchEvents{nullptr, nullptr};
+    exact[id] = g_launch_events.taken == 1;  // recorded by the one launch that took them
+    g_launch_events = LaunchEvents{nullptr, nullptr, 0};
   }
 };
 Profiler g_prof;

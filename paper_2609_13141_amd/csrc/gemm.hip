@@ -778,7 +778,7 @@ hipError_t launch_gemm(int dtype, const GemmArgs& g, hipStream_t s) {
       const int mt = (g.M + 255) / 256, nt = (nlog + 255) / 256;
       const int full = 256 / mt;  // 256-column tiles per full round
       if ((long)mt * nt > 256 && full > 0) {
-        g_launch_events = LaunchEvents{nullptr, nullptr};  // two launches: timed around both
+        g_launch_events = LaunchEvents{nullptr, nullptr, 0};  // two launches: timed around both
         GemmParams P1 = P, P2 = P;
         P1.n_cnt = full * 256;
         P2.n_off = full * 256;

@@ -14,6 +14,7 @@ namespace sas {
 // multi-kernel calls leave them unset.
 struct LaunchEvents {
   hipEvent_t start, stop;
+  int taken;  // set by the launch that recorded them
 };
 extern LaunchEvents g_launch_events;
 
@@ -22,7 +23,7 @@ inline hipError_t launch_ext(void (*kern)(KArgs...), dim3 grid, dim3 block, uint
                              Args... args) {
   if (g_launch_events.start) {
     const LaunchEvents e = g_launch_events;
-    g_launch_events = LaunchEvents{nullptr, nullptr};
+    g_launch_events = LaunchEvents{nullptr, nullptr, 1};
     hipExtLaunchKernelGGL(kern, grid, block, shm, s, e.start, e.stop, 0, args...);
   } else {
     hipLaunchKernelGGL(kern, grid, block, shm, s, args...);
