@@ -253,16 +253,35 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
     // run at a raised wave priority, so that while this wave feeds the
     // matrix unit the other wave on the SIMD issues its softmax in between.
     __builtin_amdgcn_s_setprio(2);
+    // The two 32-key halves alternate, so that consecutive MFMAs are
+    // independent, and the K fragments of step ks + 1 are read while step ks
+    // multiplies.
     floatx16_t s[2];
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
+    for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int v = 0; v < 16; ++v) s[st][v] = 0.f;
+    const bf16_t* kf = Ks + lr * KP + lk * 8;
+    bf16x8_t ka0 = *(const bf16x8_t*)kf, ka1 = *(const bf16x8_t*)(kf + 32 * KP);
 #pragma unroll
-      for (int ks = 0; ks < DH / 16; ++ks) {
-        const bf16x8_t a = *(const bf16x8_t*)(Ks + (st * 32 + lr) * KP + ks * 16 + lk * 8);
-        s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qb[ks], s[st], 0, 0, 0);
+    for (int ks = 0; ks < DH / 16; ++ks) {
+      bf16x8_t kn0 = ka0, kn1 = ka1;
+      if (ks + 1 < DH / 16) {
+        kn0 = *(const bf16x8_t*)(kf + (ks + 1) * 16);
+        kn1 = *(const bf16x8_t*)(kf + 32 * KP + (ks + 1) * 16);
       }
+      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka0, qb[ks], s[0], 0, 0, 0);
+      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka1, qb[ks], s[1], 0, 0, 0);
+      ka0 = kn0;
+      ka1 = kn1;
+    }
+    // Keep the reads one step ahead of the MFMAs (the scheduler otherwise
+    // sinks each read next to its consumer to save registers).
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+    for (int ks = 0; ks < DH / 16; ++ks) {
+      if (ks + 1 < DH / 16) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     }
     __builtin_amdgcn_s_setprio(0);
     // causal mask on the diagonal tiles (raw scores of later keys -> -inf)
@@ -401,18 +420,88 @@ __device__ __forceinline__ void attn_job_of(const AttnArgs& P, int job, int& qti
   bi = r / P.H;
 }
 
+// Work-queue order.  The jobs that read the same keys and values are those
+// of one unit (batch entry, kv head): its query tiles and, with grouped
+// queries, the heads that share the kv head.  Each XCD (the workgroups
+// blockIdx % ATTN_XCDS, which the dispatcher places on that die) owns a
+// contiguous share of the units and a counter of its own, so that a unit's
+// jobs run together on one L2.  A unit is split into `unit_parts`
+// interleaved query-tile sets when there are fewer units than XCDs.  Within
+// a share, groups of `unit_group` units (about 2 MB of keys and values) run
+// one after another, each longest query tile first; the last `tail_units`
+// units form one group, so that the share ends on short jobs.  A workgroup
+// whose share is drained takes jobs from the next shares.
+struct AttnQueuePos {
+  int nv, cq, v0;  // units of the share, query-tile slots per unit, first unit
+};
+__device__ __forceinline__ AttnQueuePos attn_share(const AttnArgs& P, int x) {
+  const int nqt = (P.n + 127) / 128, V = P.b * P.Hkv * P.unit_parts;
+  AttnQueuePos s;
+  s.v0 = (int)((long long)x * V / ATTN_XCDS);
+  s.nv = (int)((long long)(x + 1) * V / ATTN_XCDS) - s.v0;
+  s.cq = (nqt + P.unit_parts - 1) / P.unit_parts;
+  return s;
+}
+// position r of share s -> job; false for the empty slots of a ragged interleave
+__device__ __forceinline__ bool attn_queue_job(const AttnArgs& P, const AttnQueuePos& s, int r, int& qtile, int& h,
+                                               int& bi) {
+  const int G = P.H / P.Hkv, nqt = (P.n + 127) / 128;
+  const int tail = min(P.tail_units, s.nv), nh = s.nv - tail, hpos = nh * s.cq * G;
+  int a, se;
+  if (r < hpos) {
+    a = r / (P.unit_group * s.cq * G) * P.unit_group;
+    se = min(P.unit_group, nh - a);
+  } else {
+    a = nh;
+    se = tail;
+  }
+  const int rr = r - a * s.cq * G, i = rr / (se * G), r2 = rr - i * se * G;
+  const int vu = s.v0 + a + r2 / G, hg = r2 % G;
+  const int part = vu % P.unit_parts, u = vu / P.unit_parts;
+  qtile = nqt - 1 - i * P.unit_parts - part;
+  bi = u / P.Hkv;
+  h = (u % P.Hkv) * G + hg;
+  return qtile >= 0;
+}
+
 // One job (query tile or part of it, head, batch entry) per workgroup (grid =
-// job count, no queue) or the work queue; the heavy (late) query tiles first.
+// job count, no queue), or the per-XCD work queues.
 template <int DH, int LSB, bool OUTER>
 __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P, int njobs) {
-  for (int it = 0;; ++it) {
-    const int job = P.queue ? queue_next_job(P.queue) : (it == 0 ? (int)blockIdx.x : njobs);
-    if (job >= njobs) break;
+  if (!P.queue) {
+    const int job = blockIdx.x;
     int qtile, h, bi, part, nparts, jbase;
     attn_job_of(P, job, qtile, h, bi, part, nparts, jbase);
     const int nt = attn_tiles(P.n, qtile), per_part = (nt + nparts - 1) / nparts;
     attn_bf16_job<DH, LSB, OUTER>(P, qtile, h, bi, part * per_part, nparts > 1 ? (part + 1) * per_part : 1 << 30,
-                           nparts > 1 ? job : -1);
+                                  nparts > 1 ? job : -1);
+    return;
+  }
+  __shared__ int3 job_s;
+  const int x0 = blockIdx.x % ATTN_XCDS;
+  int drained = 0;  // thread 0: shares found empty, in visiting order (they stay empty)
+  for (;;) {
+    __syncthreads();  // every thread has finished the previous job and read job_s
+    if (threadIdx.x == 0) {
+      int3 j = make_int3(-1, 0, 0);
+      while (drained < ATTN_XCDS) {
+        const int x = (x0 + drained) % ATTN_XCDS;
+        const AttnQueuePos sh = attn_share(P, x);
+        const uint32_t npos = (uint32_t)sh.nv * sh.cq * (P.H / P.Hkv);
+        const uint32_t r = npos ? atomicAdd(&P.queue[x], 1u) : npos;
+        if (r >= npos) {
+          ++drained;
+          continue;
+        }
+        if (attn_queue_job(P, sh, (int)r, j.x, j.y, j.z)) break;
+        j.x = -1;
+      }
+      job_s = j;
+    }
+    __syncthreads();
+    const int3 j = job_s;
+    if (j.x < 0) break;
+    attn_bf16_job<DH, LSB, OUTER>(P, j.x, j.y, j.z, 0, 1 << 30, -1);
   }
 }
 
@@ -585,8 +674,14 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
     }
     if (total > res) {
       if (!a.queue) return hipErrorInvalidValue;
-      fill_u32_kernel<<<1, 64, 0, s>>>(a.queue, 1, 0u);
+      fill_u32_kernel<<<1, 64, 0, s>>>(a.queue, ATTN_XCDS, 0u);
       A.queue = a.queue;
+      const int U = a.b * a.Hkv;
+      A.unit_parts = U >= ATTN_XCDS ? 1 : cdiv(ATTN_XCDS, U);
+      const long long unit_bytes = (long long)a.n * a.dh * 4;  // keys and values of a unit
+      A.unit_group = (int)std::max<long long>(1, (2ll << 20) / std::max<long long>(1, unit_bytes));
+      A.tail_units = 8;
+      A.unit_group = std::min(A.unit_group, U * A.unit_parts);
     }
     kern<<<(unsigned)std::min<long long>(total, res), 256, 0, s>>>(A, (int)total);
     if (A.split_tiles > 0) {

@@ -145,19 +145,24 @@ struct AttnArgs {
   int full;               // GATED: every historical block attended, gates from gate_table
   const float* gate_table;  // [b, Hkv, n, NB] log gates (full scope)
   const int32_t* doc;     // [b, NB] first block of each block's document, or null
-  uint32_t* queue;        // job counter of the bf16 kernel's work queue (reset by the launch)
+  uint32_t* queue;        // [ATTN_XCDS] job counters of the bf16 kernel's work queue (reset by the launch)
   // split query tiles (bf16, fewer jobs than resident workgroups): per job slot 128 rows of
   // unnormalized sums [slot, 128, dh] and (max, sum) [slot, 128, 2]; null: no splitting
   float* part_o;
   float* part_ml;
   long long part_slots;
   int split_tiles;        // set by the launch: key tiles per part (0: no split)
+  // set by the launch, work-queue order: query-tile interleave of a (batch, kv head)
+  // unit, units per locality group, units of the closing longest-first group
+  int unit_parts, unit_group, tail_units;
 };
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 // longest sequence of the bf16 attention forward (key tiles of 64 tracked in LDS)
 constexpr int ATTN_MAX_SEQ = 1 << 20;
 // parts of a split query tile
 constexpr int ATTN_MAX_SPLIT = 4;
+// accelerator dies (XCDs, each with its own L2) the work queue is split over
+constexpr int ATTN_XCDS = 8;
 
 // ---- backward.hip ----------------------------------------------------------
 struct BwdArgs {
