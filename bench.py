@@ -49,7 +49,7 @@ COPY_KERNEL = "__amd_rocclr_copyBuffer"  # the runtime's blit kernel of a device
 # Dominant kernels of the headline step and their HBM-traffic summaries
 # (written by --pmc-summary from rocprofv3 --pmc runs of --only-headline).
 DOMINANT = {
-    "prefill": {"family": "gemm_gate_up", "kernel": "gemm_bf16_lds_kernel<1, 256, 256, 2, 4, 2>",
+    "prefill": {"family": "gemm_gate_up", "kernel": "gemm_bf16_lds_kernel<1, 256, 256, 2, 4, 2, 64, 16>",
                 "source": "gemm.hip", "file": "gemm_gate_up_7b_stack32_prefill2k_traffic.txt"},
     "decode": {"family": "dec_gate_up", "kernel": "gemv_kernel<4, 1>",
                "source": "gemv.hip", "file": "gemv_gate_up_7b_stack32_decode_b8_traffic.txt"},

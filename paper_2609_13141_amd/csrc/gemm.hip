@@ -9,6 +9,8 @@
 // half (J/32)%2.  A 32x32 MFMA output tile holds column J%32 in lane J%32, so
 // the two halves of a pair sit in neighbouring 32-column subtiles of the same
 // lane.  Plain (residual) GEMMs use the identity mapping.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -71,7 +73,8 @@ __device__ __forceinline__ const T* b_row(int epi, int J, int N, int npairs, int
   return B2 + (size_t)(c - Hkv * dh) * K;
 }
 
-__device__ __forceinline__ float silu_f(float x) { return x / (1.0f + __expf(-x)); }
+// x * sigmoid(x) with the hardware reciprocal (1 ulp) in place of an IEEE division
+__device__ __forceinline__ float silu_f(float x) { return x * __builtin_amdgcn_rcpf(1.0f + __expf(-x)); }
 
 constexpr int BK = 64;
 
@@ -358,16 +361,59 @@ __device__ __forceinline__ uint4 pack8_bf16(const float* x) {
   return r;
 }
 
-template <int EPI, int TM, int TN, int FM, int FN>
-__device__ __forceinline__ void gemm_epilogue_lds(const GemmParams& P, floatx16_t (&acc)[FM][FN], int m0, int n0,
-                                                  int wm, int wn, int lr, int lk, unsigned char* region) {
-  const int lane = lk * 32 + lr;
+template <int EPI, int TM, int TN, int MI>
+__device__ __forceinline__ void gemm_epilogue_lds(
+    const GemmParams& P,
+    typename std::conditional<MI == 32, floatx16_t, floatx4_t>::type (&acc)[TM / MI][TN / MI], int m0, int n0,
+    int wm, int wn, int lane, unsigned char* region) {
   const int colbase = n0 + wn * TN;
   const int rowbase = m0 + wm * TM;
+  // The accumulator elements of the wave tile's 32-row block ib, as (row in the
+  // block, column in the wave tile, value).  MI = 32: element v of subtile
+  // (ib, j) is row 8 (v/4) + 4 (lane/32) + v%4, column 32 j + lane%32.
+  // MI = 16: element v of subtile (2 ib + h, j) is row 16 h + 4 (lane/16) + v,
+  // column 16 j + lane%16.
+  auto for_each_elem = [&](int ib, auto&& f) {
+    if constexpr (MI == 32) {
 #pragma unroll
-  for (int i = 0; i < FM; ++i) {
-    const int brow = rowbase + i * 32;
-    // accumulator element v of subtile (i, j) is row 8*(v/4) + 4*lk + v%4, column j*32 + lr
+      for (int j = 0; j < TN / 32; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) f(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3), j * 32 + (lane & 31), acc[ib][j][v]);
+    } else {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int j = 0; j < TN / 16; ++j)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) f(16 * h + 4 * (lane >> 4) + v, j * 16 + (lane & 15), acc[2 * ib + h][j][v]);
+    }
+  };
+  // The same for the pair epilogues, as (row, pair in the wave tile, first
+  // half, second half): column c with c % 64 < 32 pairs with c + 32, pair
+  // index 32 (c / 64) + c % 32.
+  auto for_each_pair = [&](int ib, auto&& f) {
+    if constexpr (MI == 32) {
+#pragma unroll
+      for (int jp = 0; jp < TN / 64; ++jp)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          f(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3), jp * 32 + (lane & 31), acc[ib][2 * jp][v], acc[ib][2 * jp + 1][v]);
+    } else {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int t = 0; t < TN / 64; ++t)
+#pragma unroll
+          for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+              f(16 * h + 4 * (lane >> 4) + v, t * 32 + u * 16 + (lane & 15), acc[2 * ib + h][4 * t + u][v],
+                acc[2 * ib + h][4 * t + u + 2][v]);
+    }
+  };
+#pragma unroll
+  for (int ib = 0; ib < TM / 32; ++ib) {
+    const int brow = rowbase + ib * 32;
     if constexpr (EPI == EPI_RESID) {
       constexpr int GPR = TN / 8, G = 32 * GPR, IT = (G + 63) / 64;
       uint4 rv[IT];
@@ -379,10 +425,7 @@ __device__ __forceinline__ void gemm_epilogue_lds(const GemmParams& P, floatx16_
         rv[it] = *(const uint4*)(P.resid + (size_t)row * P.N + col);
       }
       float* st = (float*)region;
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) st[(8 * (v >> 2) + 4 * lk + (v & 3)) * TN + j * 32 + lr] = acc[i][j][v];
+      for_each_elem(ib, [&](int r, int c, float x) { st[r * TN + c] = x; });
       // a wave's LDS accesses complete in order: the reads below see its writes
 #pragma unroll
       for (int it = 0; it < IT; ++it) {
@@ -406,12 +449,7 @@ __device__ __forceinline__ void gemm_epilogue_lds(const GemmParams& P, floatx16_
     } else if constexpr (EPI == EPI_SWIGLU) {
       constexpr int NP = TN / 2, GPR = NP / 8, G = 32 * GPR;
       bf16_t* st = (bf16_t*)region;
-#pragma unroll
-      for (int jp = 0; jp < FN / 2; ++jp)
-#pragma unroll
-        for (int v = 0; v < 16; ++v)
-          st[(8 * (v >> 2) + 4 * lk + (v & 3)) * NP + jp * 32 + lr] =
-              f32_to_bf16(silu_f(acc[i][2 * jp][v]) * acc[i][2 * jp + 1][v]);
+      for_each_pair(ib, [&](int r, int pp, float g, float u) { st[r * NP + pp] = f32_to_bf16(silu_f(g) * u); });
       const int pbase = colbase >> 1;  // colbase is a multiple of 64
 #pragma unroll
       for (int g0 = 0; g0 < G; g0 += 64) {
@@ -429,14 +467,10 @@ __device__ __forceinline__ void gemm_epilogue_lds(const GemmParams& P, floatx16_
       const int pbase = colbase >> 1;
       const int pb = P.row_pos ? 0 : brow % P.seq_len;  // wave-uniform
       float* st = (float*)region;  // [2][32][NP]: first and second halves of the pairs
-#pragma unroll
-      for (int jp = 0; jp < FN / 2; ++jp)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int r = 8 * (v >> 2) + 4 * lk + (v & 3);
-          st[r * NP + jp * 32 + lr] = acc[i][2 * jp][v];
-          st[32 * NP + r * NP + jp * 32 + lr] = acc[i][2 * jp + 1][v];
-        }
+      for_each_pair(ib, [&](int r, int pp, float x1, float x2) {
+        st[r * NP + pp] = x1;
+        st[32 * NP + r * NP + pp] = x2;
+      });
 #pragma unroll
       for (int b0 = 0; b0 < IT; b0 += BATCH) {
         float4 cs[BATCH][4];  // 8 (cos, sin) entries per group, fetched before use
@@ -499,13 +533,19 @@ __device__ __forceinline__ void gemm_epilogue_lds(const GemmParams& P, floatx16_
   }
 }
 
-template <int EPI, int BM, int BN, int WM, int WN, int STAGES>
+template <int EPI, int BM, int BN, int WM, int WN, int STAGES, int BKT, int MI>
 __global__ void __launch_bounds__(WM * WN * 64)
 gemm_bf16_lds_kernel(GemmParams P) {
-  constexpr int BKT = 64, KK = 4;
+  // MI: MFMA tile, 32 (v_mfma_f32_32x32x16_bf16) or 16 (v_mfma_f32_16x16x32_bf16:
+  // the same work per LDS byte in shorter, lower-power instructions)
+  static_assert(MI == 32 || MI == 16, "MFMA tile");
+  using acc_t = typename std::conditional<MI == 32, floatx16_t, floatx4_t>::type;
+  constexpr int KS = 512 / MI;  // k per MFMA: 16 or 32
+  constexpr int KK = BKT / KS;
+  static_assert(BKT == 32 || BKT == 64, "k-tile depth");
   constexpr int NW = WM * WN;
   constexpr int TM = BM / WM, TN = BN / WN;
-  constexpr int FM = TM / 32, FN = TN / 32, NF = FM + FN, NMF = FM * FN;
+  constexpr int FM = TM / MI, FN = TN / MI, NF = FM + FN, NMF = FM * FN;
   constexpr int CPR = BKT / 8, RPG = 16 / CPR;  // the chunk swizzle described above
   constexpr int AI = BM * CPR / (64 * NW);
   constexpr int BI = BN * CPR / (64 * NW);
@@ -557,21 +597,24 @@ gemm_bf16_lds_kernel(GemmParams P) {
                                        (lds_void_t*)(st + BM * BKT + (wave * BI + j - AI) * 64 * 8), 16, 0, 0);
   };
 
-  floatx16_t acc[FM][FN];
+  acc_t acc[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+      for (int v = 0; v < MI * MI / 64; ++v) acc[i][j][v] = 0.f;
 
-  const int lr = lane & 31, lk = lane >> 5;
+  // an operand lane supplies row lr of its fragment, 16-byte k-chunk lk of the step
+  const int lr = lane % MI, lk = lane / MI;
   int foff[NF];  // element offset of fragment g's row in a stage: A0..A(FM-1), B0..B(FN-1)
 #pragma unroll
   for (int g = 0; g < NF; ++g)
-    foff[g] = g < FM ? (wm * TM + g * 32 + lr) * BKT : BM * BKT + (wn * TN + (g - FM) * 32 + lr) * BKT;
-  const int sw = (lr / RPG) % CPR;  // fragment row bases are multiples of 32
-  auto rd_off = [&](int kt, int kk) -> int { return (kt % STAGES) * STAGE + (((kk * 2 + lk) ^ sw) << 3); };
+    foff[g] = g < FM ? (wm * TM + g * MI + lr) * BKT : BM * BKT + (wn * TN + (g - FM) * MI + lr) * BKT;
+  const int sw = (lr / RPG) % CPR;  // fragment row bases are multiples of 16
+  auto rd_off = [&](int kt, int kk) -> int {
+    return (kt % STAGES) * STAGE + (((kk * (KS / 8) + lk) ^ sw) << 3);
+  };
   bf16x8_t fr[2][NF];
 
   const int nk = P.K / BKT;
@@ -610,7 +653,10 @@ gemm_bf16_lds_kernel(GemmParams P) {
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[cur][i], fr[cur][FM + j], acc[i][j], 0, 0, 0);
+          if constexpr (MI == 32)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[cur][i], fr[cur][FM + j], acc[i][j], 0, 0, 0);
+          else
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fr[cur][i], fr[cur][FM + j], acc[i][j], 0, 0, 0);
           __builtin_amdgcn_sched_barrier(0);
           if (more && m < NF) fr[nxt][m] = *(const bf16x8_t*)(na + foff[m]);
           if (kk == KK - 1 && refill) {
@@ -629,10 +675,10 @@ gemm_bf16_lds_kernel(GemmParams P) {
                                      : (P.npairs % 8) == 0 && (EPI == EPI_SWIGLU || (P.dh % 16) == 0);
   if (fast) {
     barrier_lds();  // every wave is done with the stages
-    gemm_epilogue_lds<EPI, TM, TN, FM, FN>(P, acc, m0, n0, wm, wn, lr, lk, smem + wave * epi_region_bytes<EPI, TN>());
-  } else {
+    gemm_epilogue_lds<EPI, TM, TN, MI>(P, acc, m0, n0, wm, wn, lane, smem + wave * epi_region_bytes<EPI, TN>());
+  } else if constexpr (MI == 32) {
     gemm_epilogue_t<EPI, TM, TN, FM, FN>(P, acc, m0, n0, wm, wn, lr, lk);
-  }
+  }  // (the launch takes MI = 16 only for the shapes of the staged epilogue)
 }
 
 // ---- fp32 path: one thread per (row, logical pair or column) ----------------
@@ -695,26 +741,30 @@ static hipError_t run_bf16(const GemmParams& P, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int EPI, int BM, int BN, int WM, int WN, int STAGES>
+template <int EPI, int BM, int BN, int WM, int WN, int STAGES, int BKT, int MI>
 static hipError_t run_lds_t(const GemmParams& P, hipStream_t s) {
   constexpr int NT = WM * WN * 64;
   const int tiles = ((P.M + BM - 1) / BM) * ((P.n_cnt + BN - 1) / BN);
-  const size_t lds = (size_t)STAGES * (BM + BN) * 64 * sizeof(bf16_t);
+  const size_t lds = (size_t)STAGES * (BM + BN) * BKT * sizeof(bf16_t);
   static bool attr = false;
   if (!attr) {
-    (void)hipFuncSetAttribute((const void*)gemm_bf16_lds_kernel<EPI, BM, BN, WM, WN, STAGES>,
+    (void)hipFuncSetAttribute((const void*)gemm_bf16_lds_kernel<EPI, BM, BN, WM, WN, STAGES, BKT, MI>,
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     attr = true;
   }
-  return launch_ext(gemm_bf16_lds_kernel<EPI, BM, BN, WM, WN, STAGES>, dim3(tiles), dim3(NT), (uint32_t)lds, s,
-                    P);
+  return launch_ext(gemm_bf16_lds_kernel<EPI, BM, BN, WM, WN, STAGES, BKT, MI>, dim3(tiles), dim3(NT),
+                    (uint32_t)lds, s, P);
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES>
+template <int BM, int BN, int WM, int WN, int STAGES, int BKT = 64, int MI = 32>
 static hipError_t run_lds(const GemmParams& P, hipStream_t s) {
-  if (P.epi == EPI_RESID) return run_lds_t<EPI_RESID, BM, BN, WM, WN, STAGES>(P, s);
-  if (P.epi == EPI_SWIGLU) return run_lds_t<EPI_SWIGLU, BM, BN, WM, WN, STAGES>(P, s);
-  return run_lds_t<EPI_QKV_ROPE, BM, BN, WM, WN, STAGES>(P, s);
+  if (P.epi == EPI_RESID) return run_lds_t<EPI_RESID, BM, BN, WM, WN, STAGES, BKT, MI>(P, s);
+  if (P.epi == EPI_SWIGLU) return run_lds_t<EPI_SWIGLU, BM, BN, WM, WN, STAGES, BKT, MI>(P, s);
+  return run_lds_t<EPI_QKV_ROPE, BM, BN, WM, WN, STAGES, BKT, MI>(P, s);
+}
+// the shapes of the LDS-staged epilogue (8 consecutive outputs per lane)
+static bool staged_epilogue_shape(const GemmParams& P) {
+  return P.epi == EPI_RESID ? (P.N % 8) == 0 : (P.npairs % 8) == 0 && (P.epi == EPI_SWIGLU || (P.dh % 16) == 0);
 }
 
 static bool attrs_done = false;
@@ -773,7 +823,14 @@ hipError_t launch_gemm(int dtype, const GemmArgs& g, hipStream_t s) {
     // CUs; when they would take a second, partly empty round, one full
     // round of 256x256 tiles followed by 256x128 tiles for the remaining
     // columns; narrow products (N < 8192) with 128x128 tiles.
-    if (g.M >= 4096) return run_lds<256, 256, 2, 4, 2>(P, s);
+    // The 16x16x32 MFMA (same LDS traffic per flop, lower power, so a higher
+    // clock under load) where the staged epilogue takes the shape: 5-10%
+    // faster at 256x256 and 256x128, no gain at 128x128.
+    const bool mi16 = staged_epilogue_shape(P);
+    auto big = [&](const GemmParams& Q) {
+      return mi16 ? run_lds<256, 256, 2, 4, 2, 64, 16>(Q, s) : run_lds<256, 256, 2, 4, 2>(Q, s);
+    };
+    if (g.M >= 4096) return big(P);
     if (nlog >= 8192) {
       const int mt = (g.M + 255) / 256, nt = (nlog + 255) / 256;
       const int full = 256 / mt;  // 256-column tiles per full round
@@ -783,11 +840,11 @@ hipError_t launch_gemm(int dtype, const GemmArgs& g, hipStream_t s) {
         P1.n_cnt = full * 256;
         P2.n_off = full * 256;
         P2.n_cnt = nlog - full * 256;
-        hipError_t e = run_lds<256, 256, 2, 4, 2>(P1, s);
+        hipError_t e = big(P1);
         if (e != hipSuccess) return e;
-        return run_lds<256, 128, 4, 2, 3>(P2, s);
+        return mi16 ? run_lds<256, 128, 4, 2, 3, 64, 16>(P2, s) : run_lds<256, 128, 4, 2, 3>(P2, s);
       }
-      return run_lds<256, 256, 2, 4, 2>(P, s);
+      return big(P);
     }
     return run_lds<128, 128, 4, 2, 4>(P, s);
   }

@@ -146,7 +146,7 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams& P, int gi, int c
     if (row >= P.M) continue;
     float x1 = tot[v], x2 = partner[v];
     if (epi == EPI_SWIGLU) {
-      ((bf16_t*)P.out)[(size_t)row * P.npairs + p] = f32_to_bf16(x1 / (1.0f + __expf(-x1)) * x2);
+      ((bf16_t*)P.out)[(size_t)row * P.npairs + p] = f32_to_bf16(x1 * __builtin_amdgcn_rcpf(1.0f + __expf(-x1)) * x2);
       continue;
     }
     const int hd = p / hh, ir = p % hh;
