@@ -147,10 +147,11 @@ hipError_t launch_block_summaries(int dtype, const void* K, int b, int n, int Hk
 // one is scored), one exact fp64 FMA chain per (row, block), j ascending,
 // each keeping a register Top-K (best first) and a running LSE.  The lists
 // are ordered by score, then by lower block index (the order of a single
-// ascending scan with strict comparisons), and wave 0 merges the others'
-// lists into its own in wave order: the elementwise better of its list and
-// the reversed other list holds the best K as a bitonic sequence, which a
-// bitonic network sorts.
+// ascending scan with strict comparisons).  Two sorted lists are merged by
+// taking the elementwise better of one and the reverse of the other, which
+// holds the best K as a bitonic sequence that a half-cleaner cascade sorts:
+// a chunk's candidates (sorted by a bitonic network) into a wave's list, and
+// the other waves' lists into wave 0's, in wave order.
 constexpr int SEL_NW = 4;  // waves per workgroup
 
 __device__ __forceinline__ void lds_fence() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
@@ -259,19 +260,6 @@ __global__ void __launch_bounds__(SEL_NW * WAVE) select_kernel(SelectArgs P) {
       return (ca == 0 && a > b) || ((ca == 1 || a == b) && am < bm);
     }
   };
-  auto insert = [&](double cr, int cm) {
-    if (cm == EMPTY || !beats(cr, tr[KMAX - 1], tm[KMAX - 1])) return;
-#pragma unroll
-    for (int i = 0; i < KMAX; ++i) {
-      const bool better = beats(cr, tr[i], tm[i]);
-      const double orr = tr[i];
-      const int om = tm[i];
-      tr[i] = better ? cr : orr;
-      tm[i] = better ? cm : om;
-      cr = better ? orr : cr;
-      cm = better ? om : cm;
-    }
-  };
 
   const T* kbar = (const T*)P.kbar + ((size_t)bi * P.Hkv + g) * (size_t)P.NB * DH;
   const int per = (cmax - mlo + SEL_NW - 1) / SEL_NW;
@@ -321,9 +309,16 @@ __global__ void __launch_bounds__(SEL_NW * WAVE) select_kernel(SelectArgs P) {
         r[mm] = fma(qd[3], k23.y, r[mm]);
       }
     }
+    // the chunk's candidates (ranking key, block; EMPTY where the block is not
+    // a historical block of this row's document)
+    double cr[SEL_MC];
+    int cmi[SEL_MC];
+    bool any = false;
 #pragma unroll
     for (int mm = 0; mm < SEL_MC; ++mm) {
       const int m = m0 + mm;
+      cr[mm] = -DBL_MAX;
+      cmi[mm] = EMPTY;
       if (mm >= mc || m >= ct || m < fb) continue;
       // ranking key: the raw score r, or the noisy score s + noise when noise is given
       const double sv = noise ? r[mm] / den + (double)noise[m] : r[mm] * inv_scale;
@@ -339,7 +334,50 @@ __global__ void __launch_bounds__(SEL_NW * WAVE) select_kernel(SelectArgs P) {
       } else {
         lrun += expf((float)(sv - mrun));
       }
-      insert(rv, m);
+      cr[mm] = rv;
+      cmi[mm] = m;
+      any = any || beats(rv, tr[KMAX - 1], tm[KMAX - 1]);
+    }
+    // Keep the best KMAX of the list and the chunk's candidates: sort the
+    // candidates best first; the better of list slot KMAX-1-i and candidate i
+    // leaves the best KMAX as a bitonic sequence, which a half-cleaner cascade
+    // sorts.  The order is the total order (key descending, block ascending)
+    // that inserting the blocks one by one in ascending order gives.
+    if (__builtin_amdgcn_ballot_w64(any) != 0) {
+      auto cas = [&](double& ra, int& ma, double& rb, int& mb) {  // the better one into (ra, ma)
+        const bool sw = ahead(rb, mb, ra, ma);
+        const double x = ra, y = rb;
+        const int u = ma, v = mb;
+        ra = sw ? y : x;
+        rb = sw ? x : y;
+        ma = sw ? v : u;
+        mb = sw ? u : v;
+      };
+#pragma unroll
+      for (int k = 2; k <= SEL_MC; k <<= 1)
+#pragma unroll
+        for (int j = k >> 1; j > 0; j >>= 1)
+#pragma unroll
+          for (int i = 0; i < SEL_MC; ++i) {
+            const int l = i ^ j;
+            if (l > i) {
+              if ((i & k) == 0) cas(cr[i], cmi[i], cr[l], cmi[l]);
+              else cas(cr[l], cmi[l], cr[i], cmi[i]);
+            }
+          }
+#pragma unroll
+      for (int i = 0; i < SEL_MC && i < KMAX; ++i) {
+        const int q = KMAX - 1 - i;
+        if (ahead(cr[i], cmi[i], tr[q], tm[q])) {
+          tr[q] = cr[i];
+          tm[q] = cmi[i];
+        }
+      }
+#pragma unroll
+      for (int len = KMAX / 2; len >= 1; len >>= 1)
+#pragma unroll
+        for (int i = 0; i < KMAX; ++i)
+          if ((i & len) == 0) cas(tr[i], tm[i], tr[i + len], tm[i + len]);
     }
     lds_fence();  // this chunk's reads are done before it is restaged
   }
