@@ -463,16 +463,18 @@ def hipblaslt_yardstick(w, dev, reps=10, copies=4):
 
 
 def attention_executed_flops(w, sel):
-    """MFMA work the attention kernel executes: every (128-query tile, head)
-    job multiplies whole 64-key tiles, those holding any key one of its
-    queries attends (the selected blocks of any of the tile's queries and
-    the current blocks up to the tile's last query).  sel [b, Hkv, n, K]."""
+    """MFMA work the attention kernel executes: every job (128 rows: 128 / G
+    consecutive positions x the G heads of one kv group) multiplies whole
+    64-key tiles, those holding any key one of its rows attends (the selected
+    blocks of any of the tile's positions and the current blocks up to the
+    tile's last position).  sel [b, Hkv, n, K]."""
     import numpy as np
     b, Hkv, n, K = sel.shape
     B, G, dh = w.block_size, w.n_heads // w.n_kv_heads, w.head_dim
+    qpt = 128 // G
     tiles = 0
-    for q0 in range(0, n, 128):
-        q1 = min(n, q0 + 128)
+    for q0 in range(0, n, qpt):
+        q1 = min(n, q0 + qpt)
         rows = sel[:, :, q0:q1, :].reshape(b, Hkv, -1)
         for bi in range(b):
             for g in range(Hkv):
@@ -483,7 +485,7 @@ def attention_executed_flops(w, sel):
                     keys.update(range(m * B // 64, ((m + 1) * B - 1) // 64 + 1))
                 keys.update(range((q0 // B) * B // 64, (q1 - 1) // 64 + 1))   # current blocks (causal)
                 tiles += len(keys)
-    return 4.0 * dh * 128 * 64 * tiles * G
+    return 4.0 * dh * 128 * 64 * tiles
 
 
 def layer_bench(name, steps=30, warmup=10):

@@ -4,8 +4,9 @@
 // the paper, redesigned for CDNA4 wave64 MFMA), with the gating
 // formulations of Table 1 as flags (outer gate, full scope).
 //
-// bf16 kernel layout: one workgroup = 4 waves = 128 consecutive queries of
-// one (batch, head); each wave owns 32 queries.  Scores are computed
+// bf16 kernel layout: one workgroup = 4 waves = 128 query rows of one (batch,
+// kv group): 128 / G consecutive positions x the group's G heads (the heads of
+// a group share the selection at a position); each wave owns 32 rows.  Scores are computed
 // transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16: lane l then holds
 // query l%32 and 16 of the tile's keys, so the softmax max/sum need only the
 // partner lane l^32.  The exponentiated scores P^T stay in registers and are
@@ -47,7 +48,7 @@ constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 
 template <int DH, int LSB, bool OUTER>
-__device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile, const int h, const int bi,
+__device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile, const int g, const int bi,
                                               const int tlo, const int thi, const int slot) {
   constexpr int KP = DH + 8;    // K tile row pitch (elements)
   // V^T tile: head dimension d starts at (d / 8) * VGS + (d % 8) * VP
@@ -74,11 +75,16 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lk = lane >> 5;
-  const int G = P.H / P.Hkv, g = h / G;
+  // the workgroup's 128 rows: QPT consecutive positions x the G heads of kv
+  // group g (the heads of a group share the selection at a position, so the
+  // key tiles the rows attend are the union over QPT positions, not 128)
+  const int G = P.H / P.Hkv, QPT = 128 / G;
   const int n = P.n, B = P.B;
   const int qrow = wave * 32 + lr;
-  const int t = qtile * 128 + qrow;
-  const bool qvalid = t < n;
+  const int pl = qrow / G, h = g * G + (qrow - pl * G);
+  const int t0 = qtile * QPT;  // first position of the tile
+  const int t = t0 + pl;
+  const bool qvalid = pl < QPT && t < n;
   const int beta = qvalid ? t / B : -1;
   const bool gated = P.mode == SAS_MODE_GATED;
   const bool full = gated && P.full;  // every historical block, gates from the table
@@ -86,13 +92,13 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
   const bool outer = OUTER;  // the launch picks OUTER = GATED with the outer gate
   const int Kn = every ? 0 : P.K;
   const int ntiles = (n + 63) / 64;
-  const int t_hi = min(n, qtile * 128 + 128) - 1;  // last query of the workgroup
+  const int t_hi = min(n, t0 + QPT) - 1;  // last position of the workgroup
   const int last_tile = t_hi / 64;
   const size_t grow = ((size_t)bi * P.Hkv + g) * n;  // first (b, g) row of [b, Hkv, n, ...]
   const int NB = (n + B - 1) / B;
   const int fb = qvalid ? doc_first(P.doc, bi, NB, t, B) : 0;  // first block of the query's document
   // the workgroup's earliest document start (queries are ascending): its first possible key tile
-  const int first_tile = doc_first(P.doc, bi, NB, qtile * 128, B) * B / 64;
+  const int first_tile = doc_first(P.doc, bi, NB, t0, B) * B / 64;
 
   // Q^T as the B operand: lane supplies Q[t][ks*16 + lk*8 + 0..7]
   bf16x8_t qb[DH / 16];
@@ -285,7 +291,7 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
     }
     __builtin_amdgcn_s_setprio(0);
     // causal mask on the diagonal tiles (raw scores of later keys -> -inf)
-    if (k0 + 63 > qtile * 128) {
+    if (k0 + 63 > t0) {
 #pragma unroll
       for (int st = 0; st < 2; ++st)
 #pragma unroll
@@ -396,33 +402,33 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
 // workgroups the longest job bounds the kernel, so a tile whose causal range
 // holds more than `split_tiles` key tiles is cut into up to ATTN_MAX_SPLIT
 // parts of about equal tile counts, merged afterwards by attn_combine_kernel.
-__device__ __forceinline__ int attn_tiles(int n, int qtile) { return (min(n, qtile * 128 + 128) - 1) / 64 + 1; }
-__device__ __forceinline__ int attn_splits(int n, int qtile, int split_tiles) {
+// (a query tile holds QPT = 128 / G positions of every head of one kv group)
+__device__ __forceinline__ int attn_tiles(int n, int qpt, int qtile) { return (min(n, qtile * qpt + qpt) - 1) / 64 + 1; }
+__device__ __forceinline__ int attn_splits(int n, int qpt, int qtile, int split_tiles) {
   if (split_tiles <= 0) return 1;
-  return min(ATTN_MAX_SPLIT, (attn_tiles(n, qtile) + split_tiles - 1) / split_tiles);
+  return min(ATTN_MAX_SPLIT, (attn_tiles(n, qpt, qtile) + split_tiles - 1) / split_tiles);
 }
-// job -> (query tile, head, batch entry, part); the latest query tiles first, a tile's
+// job -> (query tile, kv group, batch entry, part); the latest query tiles first, a tile's
 // parts consecutive; jbase: the job index of the tile's first job
-__device__ __forceinline__ void attn_job_of(const AttnArgs& P, int job, int& qtile, int& h, int& bi, int& part,
+__device__ __forceinline__ void attn_job_of(const AttnArgs& P, int job, int& qtile, int& g, int& bi, int& part,
                                             int& nparts, int& jbase) {
-  const int nqt = (P.n + 127) / 128, per = P.H * P.b;
+  const int qpt = 128 / (P.H / P.Hkv), nqt = (P.n + qpt - 1) / qpt, per = P.Hkv * P.b;
   jbase = 0;
   for (qtile = nqt - 1; qtile > 0; --qtile) {
-    const int cnt = attn_splits(P.n, qtile, P.split_tiles) * per;
+    const int cnt = attn_splits(P.n, qpt, qtile, P.split_tiles) * per;
     if (job < jbase + cnt) break;
     jbase += cnt;
   }
-  nparts = attn_splits(P.n, qtile, P.split_tiles);
+  nparts = attn_splits(P.n, qpt, qtile, P.split_tiles);
   int r = job - jbase;
   part = r % nparts;
   r /= nparts;
-  h = r % P.H;
-  bi = r / P.H;
+  g = r % P.Hkv;
+  bi = r / P.Hkv;
 }
 
 // Work-queue order.  The jobs that read the same keys and values are those
-// of one unit (batch entry, kv head): its query tiles and, with grouped
-// queries, the heads that share the kv head.  Each XCD (the workgroups
+// of one unit (batch entry, kv head): its query tiles.  Each XCD (the workgroups
 // blockIdx % ATTN_XCDS, which the dispatcher places on that die) owns a
 // contiguous share of the units and a counter of its own, so that a unit's
 // jobs run together on one L2.  A unit is split into `unit_parts`
@@ -435,7 +441,7 @@ struct AttnQueuePos {
   int nv, cq, v0;  // units of the share, query-tile slots per unit, first unit
 };
 __device__ __forceinline__ AttnQueuePos attn_share(const AttnArgs& P, int x) {
-  const int nqt = (P.n + 127) / 128, V = P.b * P.Hkv * P.unit_parts;
+  const int qpt = 128 / (P.H / P.Hkv), nqt = (P.n + qpt - 1) / qpt, V = P.b * P.Hkv * P.unit_parts;
   AttnQueuePos s;
   s.v0 = (int)((long long)x * V / ATTN_XCDS);
   s.nv = (int)((long long)(x + 1) * V / ATTN_XCDS) - s.v0;
@@ -443,24 +449,24 @@ __device__ __forceinline__ AttnQueuePos attn_share(const AttnArgs& P, int x) {
   return s;
 }
 // position r of share s -> job; false for the empty slots of a ragged interleave
-__device__ __forceinline__ bool attn_queue_job(const AttnArgs& P, const AttnQueuePos& s, int r, int& qtile, int& h,
+__device__ __forceinline__ bool attn_queue_job(const AttnArgs& P, const AttnQueuePos& s, int r, int& qtile, int& g,
                                                int& bi) {
-  const int G = P.H / P.Hkv, nqt = (P.n + 127) / 128;
-  const int tail = min(P.tail_units, s.nv), nh = s.nv - tail, hpos = nh * s.cq * G;
+  const int qpt = 128 / (P.H / P.Hkv), nqt = (P.n + qpt - 1) / qpt;
+  const int tail = min(P.tail_units, s.nv), nh = s.nv - tail, hpos = nh * s.cq;
   int a, se;
   if (r < hpos) {
-    a = r / (P.unit_group * s.cq * G) * P.unit_group;
+    a = r / (P.unit_group * s.cq) * P.unit_group;
     se = min(P.unit_group, nh - a);
   } else {
     a = nh;
     se = tail;
   }
-  const int rr = r - a * s.cq * G, i = rr / (se * G), r2 = rr - i * se * G;
-  const int vu = s.v0 + a + r2 / G, hg = r2 % G;
+  const int rr = r - a * s.cq, i = rr / se;
+  const int vu = s.v0 + a + (rr - i * se);
   const int part = vu % P.unit_parts, u = vu / P.unit_parts;
   qtile = nqt - 1 - i * P.unit_parts - part;
   bi = u / P.Hkv;
-  h = (u % P.Hkv) * G + hg;
+  g = u % P.Hkv;
   return qtile >= 0;
 }
 
@@ -470,10 +476,10 @@ template <int DH, int LSB, bool OUTER>
 __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P, int njobs) {
   if (!P.queue) {
     const int job = blockIdx.x;
-    int qtile, h, bi, part, nparts, jbase;
-    attn_job_of(P, job, qtile, h, bi, part, nparts, jbase);
-    const int nt = attn_tiles(P.n, qtile), per_part = (nt + nparts - 1) / nparts;
-    attn_bf16_job<DH, LSB, OUTER>(P, qtile, h, bi, part * per_part, nparts > 1 ? (part + 1) * per_part : 1 << 30,
+    int qtile, g, bi, part, nparts, jbase;
+    attn_job_of(P, job, qtile, g, bi, part, nparts, jbase);
+    const int nt = attn_tiles(P.n, 128 / (P.H / P.Hkv), qtile), per_part = (nt + nparts - 1) / nparts;
+    attn_bf16_job<DH, LSB, OUTER>(P, qtile, g, bi, part * per_part, nparts > 1 ? (part + 1) * per_part : 1 << 30,
                                   nparts > 1 ? job : -1);
     return;
   }
@@ -487,7 +493,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P, int njobs
       while (drained < ATTN_XCDS) {
         const int x = (x0 + drained) % ATTN_XCDS;
         const AttnQueuePos sh = attn_share(P, x);
-        const uint32_t npos = (uint32_t)sh.nv * sh.cq * (P.H / P.Hkv);
+        const uint32_t npos = (uint32_t)sh.nv * sh.cq;
         const uint32_t r = npos ? atomicAdd(&P.queue[x], 1u) : npos;
         if (r >= npos) {
           ++drained;
@@ -516,12 +522,13 @@ __global__ void attn_combine_kernel(AttnArgs P) {
   const int t = (int)(r % n);
   r /= n;
   const int h = (int)(r % P.H), bi = (int)(r / P.H);
-  const int qtile = t / 128, nparts = attn_splits(n, qtile, P.split_tiles);
+  const int G = P.H / P.Hkv, qpt = 128 / G, g = h / G;
+  const int qtile = t / qpt, nparts = attn_splits(n, qpt, qtile, P.split_tiles);
   if (nparts <= 1) return;
-  const int nqt = (n + 127) / 128, per = P.H * P.b;
+  const int nqt = (n + qpt - 1) / qpt, per = P.Hkv * P.b;
   int jbase = 0;
-  for (int q = nqt - 1; q > qtile; --q) jbase += attn_splits(n, q, P.split_tiles) * per;
-  const int j0 = jbase + (bi * P.H + h) * nparts, qrow = t - qtile * 128;
+  for (int q = nqt - 1; q > qtile; --q) jbase += attn_splits(n, qpt, q, P.split_tiles) * per;
+  const int j0 = jbase + (bi * P.Hkv + g) * nparts, qrow = (t - qtile * qpt) * G + (h - g * G);
   float mx = -INFINITY;
   for (int p = 0; p < nparts; ++p) mx = fmaxf(mx, P.part_ml[((size_t)(j0 + p) * 128 + qrow) * 2]);
   const float mu = mx == -INFINITY ? 0.f : mx;
@@ -645,7 +652,10 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
                                                                               : attn_bf16_kernel<128, 4, false>)
                          : (lsb == 6 ? attn_bf16_kernel<64, 6, false> : lsb == 5 ? attn_bf16_kernel<64, 5, false>
                                                                              : attn_bf16_kernel<64, 4, false>);
-    const int nqt = cdiv(a.n, 128), ntk = cdiv(a.n, 64), per = a.H * a.b;
+    // query tiles of qpt positions x the G heads of a kv group
+    if (a.Hkv <= 0 || a.H % a.Hkv != 0 || a.H / a.Hkv > 128) return hipErrorInvalidValue;
+    const int qpt = 128 / (a.H / a.Hkv);
+    const int nqt = cdiv(a.n, qpt), ntk = cdiv(a.n, 64), per = a.Hkv * a.b;
     const long long jobs = (long long)nqt * per;
     const int res = resident_workgroups(kern, 256);
     if (res <= 0 || jobs > INT32_MAX) return hipErrorInvalidValue;
@@ -656,7 +666,7 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
     if (jobs < res && a.part_o && a.part_ml && jobs * ATTN_MAX_SPLIT <= a.part_slots) {
       // fewer jobs than resident workgroups: split the long query tiles so that no job
       // walks much more than the average share of key tiles
-      auto tiles = [&](int q) { return std::min(ntk, (std::min(a.n, q * 128 + 128) - 1) / 64 + 1); };
+      auto tiles = [&](int q) { return std::min(ntk, (std::min(a.n, q * qpt + qpt) - 1) / 64 + 1); };
       long long W = 0;
       for (int q = 0; q < nqt; ++q) W += (long long)tiles(q) * per;
       // the smallest part length whose job count still fits the resident workgroups
