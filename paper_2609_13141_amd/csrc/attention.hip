@@ -47,7 +47,7 @@ __global__ void fill_u32_kernel(uint32_t* p, int n, uint32_t v) {
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 
-template <int DH, int LSB, bool OUTER>
+template <int DH, int LSB, bool OUTER, bool SKIP>
 __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile, const int g, const int bi,
                                               const int tlo, const int thi, const int slot) {
   constexpr int KP = DH + 8;    // K tile row pitch (elements)
@@ -254,6 +254,15 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
     }
     const int nkt = next_set(need, kt + 1, tend);
     if (nkt < tend) prefetch(nkt);
+    // SKIP (grouped queries: a wave's 32 rows span only 32 / G positions): a
+    // wave none of whose rows attends a key of the tile skips its products;
+    // it still stages the tiles and meets the barriers
+    bool att_any = !SKIP;
+    if constexpr (SKIP) {
+#pragma unroll
+      for (int sb = 0; sb < NSUB; ++sb) att_any = att_any || offs[sb] != -INFINITY;
+    }
+    if (!SKIP || __builtin_amdgcn_ballot_w64(att_any) != 0) {
 
     // S^T = K Q^T for keys [0,32) and [32,64) of the tile.  The MFMA phases
     // run at a raised wave priority, so that while this wave feeds the
@@ -368,6 +377,7 @@ __device__ __forceinline__ void attn_bf16_job(const AttnArgs& P, const int qtile
       }
     }
     __builtin_amdgcn_s_setprio(0);
+    }
     lds_barrier();
     kt = nkt;
   }
@@ -472,15 +482,15 @@ __device__ __forceinline__ bool attn_queue_job(const AttnArgs& P, const AttnQueu
 
 // One job (query tile or part of it, head, batch entry) per workgroup (grid =
 // job count, no queue), or the per-XCD work queues.
-template <int DH, int LSB, bool OUTER>
+template <int DH, int LSB, bool OUTER, bool SKIP>
 __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P, int njobs) {
   if (!P.queue) {
     const int job = blockIdx.x;
     int qtile, g, bi, part, nparts, jbase;
     attn_job_of(P, job, qtile, g, bi, part, nparts, jbase);
     const int nt = attn_tiles(P.n, 128 / (P.H / P.Hkv), qtile), per_part = (nt + nparts - 1) / nparts;
-    attn_bf16_job<DH, LSB, OUTER>(P, qtile, g, bi, part * per_part, nparts > 1 ? (part + 1) * per_part : 1 << 30,
-                                  nparts > 1 ? job : -1);
+    attn_bf16_job<DH, LSB, OUTER, SKIP>(P, qtile, g, bi, part * per_part,
+                                        nparts > 1 ? (part + 1) * per_part : 1 << 30, nparts > 1 ? job : -1);
     return;
   }
   __shared__ int3 job_s;
@@ -507,7 +517,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(AttnArgs P, int njobs
     __syncthreads();
     const int3 j = job_s;
     if (j.x < 0) break;
-    attn_bf16_job<DH, LSB, OUTER>(P, j.x, j.y, j.z, 0, 1 << 30, -1);
+    attn_bf16_job<DH, LSB, OUTER, SKIP>(P, j.x, j.y, j.z, 0, 1 << 30, -1);
   }
 }
 
@@ -641,17 +651,21 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
     if ((unsigned long long)a.n * a.Hkv * a.dh > 0xffffffffull) return hipErrorInvalidValue;
     const int lsb = a.B >= 64 ? 6 : (a.B == 32 ? 5 : 4);
     const bool outer = a.mode == SAS_MODE_GATED && a.outer;
+    const bool skip = a.Hkv > 0 && a.H > a.Hkv;  // grouped queries
     void (*kern)(AttnArgs, int);
-    if (outer)
-      kern = a.dh == 128 ? (lsb == 6 ? attn_bf16_kernel<128, 6, true> : lsb == 5 ? attn_bf16_kernel<128, 5, true>
-                                                                             : attn_bf16_kernel<128, 4, true>)
-                         : (lsb == 6 ? attn_bf16_kernel<64, 6, true> : lsb == 5 ? attn_bf16_kernel<64, 5, true>
-                                                                            : attn_bf16_kernel<64, 4, true>);
-    else
-      kern = a.dh == 128 ? (lsb == 6 ? attn_bf16_kernel<128, 6, false> : lsb == 5 ? attn_bf16_kernel<128, 5, false>
-                                                                              : attn_bf16_kernel<128, 4, false>)
-                         : (lsb == 6 ? attn_bf16_kernel<64, 6, false> : lsb == 5 ? attn_bf16_kernel<64, 5, false>
-                                                                             : attn_bf16_kernel<64, 4, false>);
+#define ATTN_PICK(DH, LSB)                                                                              \
+  kern = outer ? (skip ? attn_bf16_kernel<DH, LSB, true, true> : attn_bf16_kernel<DH, LSB, true, false>) \
+               : (skip ? attn_bf16_kernel<DH, LSB, false, true> : attn_bf16_kernel<DH, LSB, false, false>)
+    if (a.dh == 128) {
+      if (lsb == 6) ATTN_PICK(128, 6);
+      else if (lsb == 5) ATTN_PICK(128, 5);
+      else ATTN_PICK(128, 4);
+    } else {
+      if (lsb == 6) ATTN_PICK(64, 6);
+      else if (lsb == 5) ATTN_PICK(64, 5);
+      else ATTN_PICK(64, 4);
+    }
+#undef ATTN_PICK
     // query tiles of qpt positions x the G heads of a kv group
     if (a.Hkv <= 0 || a.H % a.Hkv != 0 || a.H / a.Hkv > 128) return hipErrorInvalidValue;
     const int qpt = 128 / (a.H / a.Hkv);
