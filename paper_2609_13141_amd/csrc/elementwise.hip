@@ -21,11 +21,13 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const T* __restrict__ x, c
   const T* xr = x + row * (size_t)d;
   T* o = out + row * (size_t)d;
   const int nch = d / EPC;
-  uint4 v[CPT];
+  // the row and the gains are loaded together: one memory round trip before the reduction
+  uint4 v[CPT], gv[CPT];
 #pragma unroll
   for (int i = 0; i < CPT; ++i) {
     const int c = threadIdx.x + i * 256;
     v[i] = c < nch ? *(const uint4*)(xr + (size_t)c * EPC) : make_uint4(0, 0, 0, 0);
+    gv[i] = c < nch ? *(const uint4*)(gamma + (size_t)c * EPC) : make_uint4(0, 0, 0, 0);
   }
   if constexpr (ROPE) {
     const int half = dh >> 1;
@@ -57,9 +59,8 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const T* __restrict__ x, c
   for (int i = 0; i < CPT; ++i) {
     const int c = threadIdx.x + i * 256;
     if (c >= nch) continue;
-    const uint4 gv = *(const uint4*)(gamma + (size_t)c * EPC);
     const T* e = (const T*)&v[i];
-    const T* ge = (const T*)&gv;
+    const T* ge = (const T*)&gv[i];
     uint4 r;
     T* re = (T*)&r;
 #pragma unroll

@@ -141,11 +141,15 @@ hipError_t launch_block_summaries(int dtype, const void* K, int b, int n, int Hk
 // ---------------------------------------------------------------------------
 // Selection: one workgroup of SEL_NW waves per 64 consecutive query rows of
 // one (batch, group); lane = query row.  The 64 gate queries are staged in
-// LDS once; the waves split the historical blocks into contiguous ranges and
-// walk theirs in ascending order, in chunks of SEL_MC summaries staged in
-// LDS as fp64 (the next chunk is loaded into registers while the current
-// one is scored), one exact fp64 FMA chain per (row, block), j ascending,
-// each keeping a register Top-K (best first) and a running LSE.  The lists
+// LDS once (as fp32, each the rounded gate query); the waves split the
+// historical blocks into contiguous ranges and walk theirs in ascending
+// order, in chunks of SEL_MC = 8 summaries, one exact fp64 FMA chain per
+// (row, block), j ascending.  The summary values reach the rows through DPP
+// row broadcasts: for a 16-dimension group, lane n of every 16-lane row holds
+// summary n % 8 at dimensions 8 (n / 8) .. + 8 (the four rows hold the same
+// values), and each v_fmac_f64 takes its summary operand from one lane of its
+// row, so the wave's 64 chains share one loaded copy without LDS traffic.
+// Each lane keeps a register Top-K (best first) and a running LSE.  The lists
 // are ordered by score, then by lower block index (the order of a single
 // ascending scan with strict comparisons).  Two sorted lists are merged by
 // taking the elementwise better of one and the reverse of the other, which
@@ -154,17 +158,48 @@ hipError_t launch_block_summaries(int dtype, const void* K, int b, int n, int Hk
 // the other waves' lists into wave 0's, in wave order.
 constexpr int SEL_NW = 4;  // waves per workgroup
 
-__device__ __forceinline__ void lds_fence() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// r[mm] += k(lane L + mm of the 16-lane row) * q, mm = 0..7, for the four
+// dimensions whose summary values are k0..k3 and query values q0..q3, in that
+// order (L = 0: summaries of the group's first 8 dimensions, L = 8: its last
+// 8).  v_fmac_f64 with a row_newbcast DPP source: every lane of a row reads
+// the source from one lane of that row.  The s_nop covers the two wait states
+// a DPP read needs after a VALU write of its source.
+#define SEL_F(R, K, Q, N) "v_fmac_f64_dpp %" #R ", %" #K ", %" #Q " row_newbcast:" #N " row_mask:0xf bank_mask:0xf\n\t"
+#define SEL_DIM0(K, Q) \
+  SEL_F(0, K, Q, 0) SEL_F(1, K, Q, 1) SEL_F(2, K, Q, 2) SEL_F(3, K, Q, 3) \
+  SEL_F(4, K, Q, 4) SEL_F(5, K, Q, 5) SEL_F(6, K, Q, 6) SEL_F(7, K, Q, 7)
+#define SEL_DIM8(K, Q) \
+  SEL_F(0, K, Q, 8) SEL_F(1, K, Q, 9) SEL_F(2, K, Q, 10) SEL_F(3, K, Q, 11) \
+  SEL_F(4, K, Q, 12) SEL_F(5, K, Q, 13) SEL_F(6, K, Q, 14) SEL_F(7, K, Q, 15)
+template <int L>
+__device__ __forceinline__ void sel_fma4(double (&r)[8], double k0, double k1, double k2, double k3, double q0,
+                                         double q1, double q2, double q3) {
+  static_assert(L == 0 || L == 8, "lane base 0 or 8");
+  if constexpr (L == 0) {
+    asm("s_nop 1\n\t" SEL_DIM0(8, 12) SEL_DIM0(9, 13) SEL_DIM0(10, 14) SEL_DIM0(11, 15)
+        : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]), "+v"(r[4]), "+v"(r[5]), "+v"(r[6]), "+v"(r[7])
+        : "v"(k0), "v"(k1), "v"(k2), "v"(k3), "v"(q0), "v"(q1), "v"(q2), "v"(q3));
+  } else {
+    asm("s_nop 1\n\t" SEL_DIM8(8, 12) SEL_DIM8(9, 13) SEL_DIM8(10, 14) SEL_DIM8(11, 15)
+        : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]), "+v"(r[4]), "+v"(r[5]), "+v"(r[6]), "+v"(r[7])
+        : "v"(k0), "v"(k1), "v"(k2), "v"(k3), "v"(q0), "v"(q1), "v"(q2), "v"(q3));
+  }
+}
+#undef SEL_DIM8
+#undef SEL_DIM0
+#undef SEL_F
 
 template <typename T, int DH, int KMAX, int SEL_MC, bool NOISY>
 __global__ void __launch_bounds__(SEL_NW * WAVE) select_kernel(SelectArgs P) {
   static_assert((KMAX & (KMAX - 1)) == 0, "the merge network needs a power-of-two list");
-  constexpr int KW_BYTES = SEL_NW * SEL_MC * DH * 8;
+  static_assert(SEL_MC == 8 && DH % 16 == 0, "chunks of 8 summaries, 16-dimension groups");
   constexpr int MG_BYTES = KMAX * WAVE * 12 + WAVE * 12;
-  __shared__ __align__(16) unsigned char pool[KW_BYTES > MG_BYTES ? KW_BYTES : MG_BYTES];
-  __shared__ __align__(16) T qs[WAVE][DH + 8];  // the 64 gate queries
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  double(*kw)[DH] = (double(*)[DH])pool + wave * SEL_MC;  // this wave's staged summaries (exact in fp64)
+  __shared__ __align__(16) unsigned char pool[MG_BYTES];
+  // the 64 gate queries as fp32 (exact: each is a rounded value of T); the
+  // pitch of DH + 4 puts the 16-byte reads of 16 lanes in distinct banks
+  __shared__ __align__(16) float qs[WAVE][DH + 4];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   double* mg_r = (double*)pool;                            // merge: [KMAX][WAVE] keys
   int* mg_m = (int*)(pool + KMAX * WAVE * 8);              // [KMAX][WAVE] blocks
   double* mg_mx = (double*)(pool + KMAX * WAVE * 12);      // [WAVE] running max
@@ -221,7 +256,7 @@ __global__ void __launch_bounds__(SEL_NW * WAVE) select_kernel(SelectArgs P) {
       const int c = tid + i * SEL_NW * WAVE;
       const int r = c / NC, c8 = c % NC;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) qs[r][c8 * 8 + e] = r < rows ? Act<T>::from_f64(acc[i][e]) : Act<T>::from_f32(0.f);
+      for (int e = 0; e < 8; ++e) qs[r][c8 * 8 + e] = r < rows ? Act<T>::to_f32(Act<T>::from_f64(acc[i][e])) : 0.f;
     }
   }
   __syncthreads();
@@ -264,50 +299,38 @@ __global__ void __launch_bounds__(SEL_NW * WAVE) select_kernel(SelectArgs P) {
   const T* kbar = (const T*)P.kbar + ((size_t)bi * P.Hkv + g) * (size_t)P.NB * DH;
   const int per = (cmax - mlo + SEL_NW - 1) / SEL_NW;
   const int mb = mlo + wave * per, me = min(cmax, mb + per);
-  // staging: SEL_MC x DH summary values as 8-value chunks, NCL per lane
-  constexpr int NC = DH / 8, NCH = SEL_MC * NC, NCL = (NCH + WAVE - 1) / WAVE;
-  Vec8<T> nx[NCL];
-  auto fetch = [&](int m0) {
-    const int mc = min(SEL_MC, me - m0);
-#pragma unroll
-    for (int i = 0; i < NCL; ++i) {
-      const int c = min(lane + i * WAVE, NCH - 1);
-      nx[i].load(kbar + (size_t)(m0 + min(c / NC, mc - 1)) * DH + (c % NC) * 8);
-    }
+  // this lane's part of a 16-dimension group jg of the chunk at m0: summary
+  // (lane % 8) of the chunk (the last block for a ragged chunk's missing
+  // ones), dimensions 16 jg + 8 ((lane % 16) / 8) .. + 8
+  const int lsum = lane & 7, lhalf = (lane >> 3) & 1;
+  auto group_ptr = [&](int m0, int jg) {
+    return kbar + (size_t)min(m0 + lsum, me - 1) * DH + jg * 16 + lhalf * 8;
   };
-  if (mb < me) fetch(mb);
+  constexpr int NG = DH / 16;  // dimension groups per summary
+  Vec8<T> kn;  // the next group's values, loaded one group ahead
+  if (mb < me) kn.load(group_ptr(mb, 0));
   for (int m0 = mb; m0 < me; m0 += SEL_MC) {
     const int mc = min(SEL_MC, me - m0);
-#pragma unroll
-    for (int i = 0; i < NCL; ++i) {
-      const int c = lane + i * WAVE;
-      if (NCH % WAVE != 0 && c >= NCH) continue;
-      const int r = c / NC, c8 = c % NC;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) kw[r][c8 * 8 + e] = r < mc ? (double)nx[i].get(e) : 0.0;
-    }
-    lds_fence();
-    if (m0 + SEL_MC < me) fetch(m0 + SEL_MC);  // the next chunk, in flight while this one is scored
     // r[mm] = sum_j q_j kbar[m0+mm]_j: one fp64 FMA chain per block, j ascending
     double r[SEL_MC];
 #pragma unroll
     for (int mm = 0; mm < SEL_MC; ++mm) r[mm] = 0.0;
-    // (a bounded unroll: a full one lets the summary reads of every step be
-    // hoisted, more registers than the wave has)
-#pragma unroll 2
-    for (int j = 0; j < DH; j += 4) {
-      double qd[4];
+    const float* qrow = qs[lane];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) qd[u] = Act<T>::to_f32(qs[lane][j + u]);
+    for (int jg = 0; jg < NG; ++jg) {
+      const Vec8<T> kc = kn;
+      if (jg + 1 < NG) kn.load(group_ptr(m0, jg + 1));
+      else if (m0 + SEL_MC < me) kn.load(group_ptr(m0 + SEL_MC, 0));
+      double kd[8];
 #pragma unroll
-      for (int mm = 0; mm < SEL_MC; ++mm) {
-        const double2 k01 = *(const double2*)&kw[mm][j];  // four dimensions of one summary (broadcast)
-        const double2 k23 = *(const double2*)&kw[mm][j + 2];
-        r[mm] = fma(qd[0], k01.x, r[mm]);
-        r[mm] = fma(qd[1], k01.y, r[mm]);
-        r[mm] = fma(qd[2], k23.x, r[mm]);
-        r[mm] = fma(qd[3], k23.y, r[mm]);
-      }
+      for (int e = 0; e < 8; ++e) kd[e] = (double)kc.get(e);
+      const float4 q0 = *(const float4*)(qrow + jg * 16), q1 = *(const float4*)(qrow + jg * 16 + 4);
+      const float4 q2 = *(const float4*)(qrow + jg * 16 + 8), q3 = *(const float4*)(qrow + jg * 16 + 12);
+      // dimensions 16 jg + 0..7 from lanes 0..7 of the row, then 16 jg + 8..15 from lanes 8..15
+      sel_fma4<0>(r, kd[0], kd[1], kd[2], kd[3], q0.x, q0.y, q0.z, q0.w);
+      sel_fma4<0>(r, kd[4], kd[5], kd[6], kd[7], q1.x, q1.y, q1.z, q1.w);
+      sel_fma4<8>(r, kd[0], kd[1], kd[2], kd[3], q2.x, q2.y, q2.z, q2.w);
+      sel_fma4<8>(r, kd[4], kd[5], kd[6], kd[7], q3.x, q3.y, q3.z, q3.w);
     }
     // the chunk's candidates (ranking key, block; EMPTY where the block is not
     // a historical block of this row's document)
@@ -379,7 +402,6 @@ __global__ void __launch_bounds__(SEL_NW * WAVE) select_kernel(SelectArgs P) {
         for (int i = 0; i < KMAX; ++i)
           if ((i & len) == 0) cas(tr[i], tm[i], tr[i + len], tm[i + len]);
     }
-    lds_fence();  // this chunk's reads are done before it is restaged
   }
   __syncthreads();
   // merge the other waves' lists into wave 0's, in wave order
@@ -504,16 +526,9 @@ __global__ void finish_table_kernel(float* __restrict__ table, const float* __re
 template <typename T, int DH, bool NOISY>
 static void run_select_t(const SelectArgs& a, hipStream_t s) {
   dim3 grid(cdiv(a.n, WAVE), a.Hkv, a.b);
-  // chunks of 4 summaries when no wave has more than 4 blocks to score (short sequences)
-  if (cdiv(a.NB, SEL_NW) <= 4) {
-    if (a.K <= 8) select_kernel<T, DH, 8, 4, NOISY><<<grid, SEL_NW * WAVE, 0, s>>>(a);
-    else if (a.K <= 16) select_kernel<T, DH, 16, 4, NOISY><<<grid, SEL_NW * WAVE, 0, s>>>(a);
-    else select_kernel<T, DH, 32, 4, NOISY><<<grid, SEL_NW * WAVE, 0, s>>>(a);
-  } else {
-    if (a.K <= 8) select_kernel<T, DH, 8, 8, NOISY><<<grid, SEL_NW * WAVE, 0, s>>>(a);
-    else if (a.K <= 16) select_kernel<T, DH, 16, 8, NOISY><<<grid, SEL_NW * WAVE, 0, s>>>(a);
-    else select_kernel<T, DH, 32, 8, NOISY><<<grid, SEL_NW * WAVE, 0, s>>>(a);
-  }
+  if (a.K <= 8) select_kernel<T, DH, 8, 8, NOISY><<<grid, SEL_NW * WAVE, 0, s>>>(a);
+  else if (a.K <= 16) select_kernel<T, DH, 16, 8, NOISY><<<grid, SEL_NW * WAVE, 0, s>>>(a);
+  else select_kernel<T, DH, 32, 8, NOISY><<<grid, SEL_NW * WAVE, 0, s>>>(a);
 }
 
 template <typename T, int DH>
