@@ -169,6 +169,16 @@ __global__ void __launch_bounds__(64) decode_select_kernel(const T* __restrict__
   const int lane = threadIdx.x;
   const int g = blockIdx.x, i = blockIdx.y;
   const int G = c.H / c.Hkv, dh = DH, K = c.K;
+  // this lane's first summary row, loaded before the position is known so
+  // that its latency overlaps the position's and the queries' (a row past the
+  // cache's blocks is clamped and its score is never used)
+  const T* ks = (const T*)c.k_summary + ((size_t)i * c.Hkv + g) * c.max_blocks * dh;
+  Vec8<T> kv0[DH / 8];
+  if (c.max_blocks > 0) {
+    const T* kr = ks + (size_t)min(lane, c.max_blocks - 1) * DH;
+#pragma unroll
+    for (int c8 = 0; c8 < DH / 8; ++c8) kv0[c8].load(kr + c8 * 8);
+  }
   const int p = c.pos[i];
   const int ct = max(0, min(p / c.B, min(c.max_blocks, DSEL_WAVE_MAX_BLOCKS)));
   for (int j = lane; j < dh; j += 64) {
@@ -188,18 +198,21 @@ __global__ void __launch_bounds__(64) decode_select_kernel(const T* __restrict__
     for (int j = lane; j < dh; j += 64) qh[j] = qp[j];
     __syncthreads();
   }
-  const T* ks = (const T*)c.k_summary + ((size_t)i * c.Hkv + g) * c.max_blocks * dh;
-  for (int m = lane; m < ct; m += 64) {
-    const T* kr = ks + (size_t)m * DH;
-    Vec8<T> kv[DH / 8];
-#pragma unroll
-    for (int c8 = 0; c8 < DH / 8; ++c8) kv[c8].load(kr + c8 * 8);
+  auto score = [&](const Vec8<T>(&kv)[DH / 8]) {
     double acc = 0.0;
 #pragma unroll
     for (int c8 = 0; c8 < DH / 8; ++c8)
 #pragma unroll
       for (int e = 0; e < 8; ++e) acc = fma(qh[c8 * 8 + e], (double)kv[c8].get(e), acc);
-    rs[m] = acc;
+    return acc;
+  };
+  if (lane < ct) rs[lane] = score(kv0);
+  for (int m = lane + 64; m < ct; m += 64) {
+    const T* kr = ks + (size_t)m * DH;
+    Vec8<T> kv[DH / 8];
+#pragma unroll
+    for (int c8 = 0; c8 < DH / 8; ++c8) kv[c8].load(kr + c8 * 8);
+    rs[m] = score(kv);
   }
   __syncthreads();
   int32_t* out = sel + ((size_t)i * c.Hkv + g) * K;
@@ -209,8 +222,11 @@ __global__ void __launch_bounds__(64) decode_select_kernel(const T* __restrict__
     bool keep = false;
     if (m < ct) {
       const double r = rs[m];
+      // rank = the blocks ahead of m (a full pass without an early exit, so
+      // that the unrolled LDS reads are issued together)
       int rank = 0;
-      for (int o = 0; o < ct && rank < K; ++o) {
+#pragma unroll 8
+      for (int o = 0; o < ct; ++o) {
         const double ro = rs[o];
         rank += (ro > r || (ro == r && o < m)) ? 1 : 0;
       }

@@ -543,6 +543,7 @@ gemm_bf16_lds_kernel(GemmParams P) {
   constexpr int KS = 512 / MI;  // k per MFMA: 16 or 32
   constexpr int KK = BKT / KS;
   static_assert(BKT == 32 || BKT == 64, "k-tile depth");
+  static_assert(KK % 2 == 0, "the fragment double buffer alternates with the k-step: an even count per k-tile");
   constexpr int NW = WM * WN;
   constexpr int TM = BM / WM, TN = BN / WN;
   constexpr int FM = TM / MI, FN = TN / MI, NF = FM + FN, NMF = FM * FN;
