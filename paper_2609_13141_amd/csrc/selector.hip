@@ -193,17 +193,17 @@ template <typename T, int DH, int KMAX, int SEL_MC, bool NOISY>
 __global__ void __launch_bounds__(SEL_NW * WAVE) select_kernel(SelectArgs P) {
   static_assert((KMAX & (KMAX - 1)) == 0, "the merge network needs a power-of-two list");
   static_assert(SEL_MC == 8 && DH % 16 == 0, "chunks of 8 summaries, 16-dimension groups");
+  // a list exchange region: [KMAX][WAVE] keys, [KMAX][WAVE] blocks, [WAVE]
+  // running max and sum; the second region reuses the query staging when it
+  // is large enough (the queries are dead once every wave has scored)
   constexpr int MG_BYTES = KMAX * WAVE * 12 + WAVE * 12;
-  __shared__ __align__(16) unsigned char pool[MG_BYTES];
+  constexpr bool R1_IN_QS = WAVE * (DH + 4) * 4 >= MG_BYTES;
+  __shared__ __align__(16) unsigned char pool[R1_IN_QS ? MG_BYTES : 2 * MG_BYTES];
   // the 64 gate queries as fp32 (exact: each is a rounded value of T); the
   // pitch of DH + 4 puts the 16-byte reads of 16 lanes in distinct banks
   __shared__ __align__(16) float qs[WAVE][DH + 4];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  double* mg_r = (double*)pool;                            // merge: [KMAX][WAVE] keys
-  int* mg_m = (int*)(pool + KMAX * WAVE * 8);              // [KMAX][WAVE] blocks
-  double* mg_mx = (double*)(pool + KMAX * WAVE * 12);      // [WAVE] running max
-  float* mg_l = (float*)(pool + KMAX * WAVE * 12 + WAVE * 8);  // [WAVE] running sum
   const int g = blockIdx.y, bi = blockIdx.z;
   const int t0 = (gridDim.x - 1 - blockIdx.x) * WAVE;  // the late rows (more blocks to score) first
   const int t = t0 + lane;
@@ -404,56 +404,69 @@ __global__ void __launch_bounds__(SEL_NW * WAVE) select_kernel(SelectArgs P) {
     }
   }
   __syncthreads();
-  // merge the other waves' lists into wave 0's, in wave order
-  for (int w = 1; w < SEL_NW; ++w) {
-    if (wave == w) {
+  // merge the waves' lists as a tree: 1 into 0 and 3 into 2, then 2 into 0.
+  // The lists are ordered by a strict total order, so the best KMAX of the
+  // union do not depend on the merge order.
+  unsigned char* const region[2] = {pool, R1_IN_QS ? (unsigned char*)&qs[0][0] : pool + MG_BYTES};
+  auto put = [&](const unsigned char* base) {  // this wave's list and LSE into a region
+    double* rk = (double*)base;
+    int* rb = (int*)(base + KMAX * WAVE * 8);
 #pragma unroll
-      for (int i = 0; i < KMAX; ++i) {
-        mg_r[i * WAVE + lane] = tr[i];
-        mg_m[i * WAVE + lane] = tm[i];
-      }
-      mg_mx[lane] = mrun;
-      mg_l[lane] = lrun;
+    for (int i = 0; i < KMAX; ++i) {
+      rk[i * WAVE + lane] = tr[i];
+      rb[i * WAVE + lane] = tm[i];
     }
-    __syncthreads();
-    if (wave == 0) {
-      // the better of slot i and the other list's slot KMAX-1-i: the best KMAX
-      // of both, descending then ascending (a bitonic sequence)
+    ((double*)(base + KMAX * WAVE * 12))[lane] = mrun;
+    ((float*)(base + KMAX * WAVE * 12 + WAVE * 8))[lane] = lrun;
+  };
+  auto take = [&](const unsigned char* base) {  // a region's list and LSE into this wave's
+    const double* rk = (const double*)base;
+    const int* rb = (const int*)(base + KMAX * WAVE * 8);
+    // the better of slot i and the other list's slot KMAX-1-i: the best KMAX
+    // of both, descending then ascending (a bitonic sequence)
 #pragma unroll
-      for (int i = 0; i < KMAX; ++i) {
-        const double ob = mg_r[(KMAX - 1 - i) * WAVE + lane];
-        const int om = mg_m[(KMAX - 1 - i) * WAVE + lane];
-        if (ahead(ob, om, tr[i], tm[i])) {
-          tr[i] = ob;
-          tm[i] = om;
+    for (int i = 0; i < KMAX; ++i) {
+      const double ob = rk[(KMAX - 1 - i) * WAVE + lane];
+      const int om = rb[(KMAX - 1 - i) * WAVE + lane];
+      if (ahead(ob, om, tr[i], tm[i])) {
+        tr[i] = ob;
+        tm[i] = om;
+      }
+    }
+    // bitonic sort, best first
+#pragma unroll
+    for (int len = KMAX / 2; len >= 1; len >>= 1)
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i)
+        if ((i & len) == 0) {
+          const int j = i + len;
+          const bool sw = ahead(tr[j], tm[j], tr[i], tm[i]);
+          const double ri = tr[i], rj = tr[j];
+          const int mi = tm[i], mj = tm[j];
+          tr[i] = sw ? rj : ri;
+          tr[j] = sw ? ri : rj;
+          tm[i] = sw ? mj : mi;
+          tm[j] = sw ? mi : mj;
         }
-      }
-      // bitonic sort, best first
-#pragma unroll
-      for (int len = KMAX / 2; len >= 1; len >>= 1)
-#pragma unroll
-        for (int i = 0; i < KMAX; ++i)
-          if ((i & len) == 0) {
-            const int j = i + len;
-            const bool sw = ahead(tr[j], tm[j], tr[i], tm[i]);
-            const double ri = tr[i], rj = tr[j];
-            const int mi = tm[i], mj = tm[j];
-            tr[i] = sw ? rj : ri;
-            tr[j] = sw ? ri : rj;
-            tm[i] = sw ? mj : mi;
-            tm[j] = sw ? mi : mj;
-          }
-      const double om = mg_mx[lane];
-      const float ol = mg_l[lane];
-      if (om > mrun) {
-        lrun = lrun * expf((float)(mrun - om)) + ol;
-        mrun = om;
-      } else if (ol > 0.f) {
-        lrun += ol * expf((float)(om - mrun));
-      }
+    const double om = ((const double*)(base + KMAX * WAVE * 12))[lane];
+    const float ol = ((const float*)(base + KMAX * WAVE * 12 + WAVE * 8))[lane];
+    if (om > mrun) {
+      lrun = lrun * expf((float)(mrun - om)) + ol;
+      mrun = om;
+    } else if (ol > 0.f) {
+      lrun += ol * expf((float)(om - mrun));
     }
-    __syncthreads();
-  }
+  };
+  static_assert(SEL_NW == 4, "a two-level merge tree");
+  if (wave == 1) put(region[0]);
+  if (wave == 3) put(region[1]);
+  __syncthreads();
+  if (wave == 0) take(region[0]);
+  if (wave == 2) take(region[1]);
+  __syncthreads();
+  if (wave == 2) put(region[0]);
+  __syncthreads();
+  if (wave == 0) take(region[0]);
   if (wave != 0 || !valid) return;
   const double lse = (ct > fb) ? mrun + log((double)lrun) : 0.0;
   auto log_gate_of = [&](double key) -> double {  // log g of a block from its ranking key
@@ -480,23 +493,28 @@ __global__ void __launch_bounds__(SEL_NW * WAVE) select_kernel(SelectArgs P) {
     P.tau[row] = tau;
   }
 
-  // order the kept blocks by index (odd-even transposition; empty slots last)
+  // order the kept blocks by index (a bitonic sorting network; empty slots,
+  // the largest index, last)
 #pragma unroll
   for (int i = 0; i < KMAX; ++i)
     if (i >= kk) tm[i] = EMPTY;
 #pragma unroll
-  for (int pass = 0; pass < KMAX; ++pass) {
+  for (int k = 2; k <= KMAX; k <<= 1)
 #pragma unroll
-    for (int i = (pass & 1); i + 1 < KMAX; i += 2) {
-      const bool sw = tm[i] > tm[i + 1];
-      const int a = tm[i], c = tm[i + 1];
-      const double ra = tr[i], rc = tr[i + 1];
-      tm[i] = sw ? c : a;
-      tm[i + 1] = sw ? a : c;
-      tr[i] = sw ? rc : ra;
-      tr[i + 1] = sw ? ra : rc;
-    }
-  }
+    for (int j = k >> 1; j > 0; j >>= 1)
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i) {
+        const int l = i ^ j;
+        if (l > i) {
+          const bool sw = (i & k) == 0 ? tm[i] > tm[l] : tm[i] < tm[l];
+          const int a = tm[i], c = tm[l];
+          const double ra = tr[i], rc = tr[l];
+          tm[i] = sw ? c : a;
+          tm[l] = sw ? a : c;
+          tr[i] = sw ? rc : ra;
+          tr[l] = sw ? ra : rc;
+        }
+      }
   int32_t* sel = P.sel + row * K;
   float* sb = P.sel_bias + row * K;
 #pragma unroll
