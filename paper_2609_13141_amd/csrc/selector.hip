@@ -251,12 +251,16 @@ __global__ void __launch_bounds__(SEL_NW * WAVE) select_kernel(SelectArgs P) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[i][e] += (double)v[i].get(e);
     }
+    // a single row (one head, or the projected query) is already a value of
+    // T, and its rounding the identity: stored as it is
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int c = tid + i * SEL_NW * WAVE;
       const int r = c / NC, c8 = c % NC;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) qs[r][c8 * 8 + e] = r < rows ? Act<T>::to_f32(Act<T>::from_f64(acc[i][e])) : 0.f;
+      for (int e = 0; e < 8; ++e)
+        qs[r][c8 * 8 + e] =
+            r < rows ? (nh == 1 ? (float)acc[i][e] : Act<T>::to_f32(Act<T>::from_f64(acc[i][e]))) : 0.f;
     }
   }
   __syncthreads();
@@ -388,19 +392,31 @@ __global__ void __launch_bounds__(SEL_NW * WAVE) select_kernel(SelectArgs P) {
               else cas(cr[l], cmi[l], cr[i], cmi[i]);
             }
           }
+      static_assert(SEL_MC <= KMAX, "a chunk fits the list");
+      if (!NOISY && m0 == mb) {
+        // the wave's first chunk: the list is empty, so the sorted candidates
+        // are the list (what the merge below would leave; the noisy variant,
+        // at its register limit, takes the merge)
 #pragma unroll
-      for (int i = 0; i < SEL_MC && i < KMAX; ++i) {
-        const int q = KMAX - 1 - i;
-        if (ahead(cr[i], cmi[i], tr[q], tm[q])) {
-          tr[q] = cr[i];
-          tm[q] = cmi[i];
+        for (int i = 0; i < SEL_MC; ++i) {
+          tr[i] = cr[i];
+          tm[i] = cmi[i];
         }
+      } else {
+#pragma unroll
+        for (int i = 0; i < SEL_MC; ++i) {
+          const int q = KMAX - 1 - i;
+          if (ahead(cr[i], cmi[i], tr[q], tm[q])) {
+            tr[q] = cr[i];
+            tm[q] = cmi[i];
+          }
+        }
+#pragma unroll
+        for (int len = KMAX / 2; len >= 1; len >>= 1)
+#pragma unroll
+          for (int i = 0; i < KMAX; ++i)
+            if ((i & len) == 0) cas(tr[i], tm[i], tr[i + len], tm[i + len]);
       }
-#pragma unroll
-      for (int len = KMAX / 2; len >= 1; len >>= 1)
-#pragma unroll
-        for (int i = 0; i < KMAX; ++i)
-          if ((i & len) == 0) cas(tr[i], tm[i], tr[i + len], tm[i + len]);
     }
   }
   __syncthreads();
