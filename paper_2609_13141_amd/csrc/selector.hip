@@ -355,11 +355,14 @@ __global__ void __launch_bounds__(SEL_NW * WAVE) select_kernel(SelectArgs P) {
         if (act == SAS_ACT_SIGMOID) gv = sv >= 0.0 ? -log1p(exp(-sv)) : sv - log1p(exp(sv));
         lgrow[m] = (float)gv;
       }
-      if (sv > mrun) {
-        lrun = lrun * expf((float)(mrun - sv)) + 1.f;
-        mrun = sv;
-      } else {
-        lrun += expf((float)(sv - mrun));
+      // running LSE: one exponential of minus the gap to the running max, the
+      // sum rescaled when sv is the new max (no divergent branch)
+      {
+        const float d = (float)(sv - mrun);
+        const float e = __expf(-fabsf(d));
+        const bool up = d > 0.f;
+        lrun = up ? fmaf(lrun, e, 1.f) : lrun + e;
+        mrun = up ? sv : mrun;
       }
       cr[mm] = rv;
       cmi[mm] = m;
