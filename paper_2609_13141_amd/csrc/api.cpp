@@ -1130,6 +1130,9 @@ sas_status sas_layer_forward(const sas_config* c, int32_t batch, int32_t seq_len
   g.head_dim = c->head_dim;
   g.seq_len = seq_len;
   g.rope = lw.rope;
+  // with a cache, the QKV product writes the K/V pages itself where it can
+  const DecodeArgs da = cache ? decode_args(c, batch, nullptr, cache, w) : DecodeArgs{};
+  g.prefill_cache = (cache && gemm_fills_cache(c->dtype, g)) ? &da : nullptr;
   {
     Timed tm("gemm_qkv", s);
     HIP_TRY(launch_gemm(c->dtype, g, s), "qkv gemm");
@@ -1138,9 +1141,9 @@ sas_status sas_layer_forward(const sas_config* c, int32_t batch, int32_t seq_len
                         st.log_gate, st.tau, lw.att, s, cache != nullptr));
   if (cache) {
     Timed tm("cache_fill", s);
-    const DecodeArgs da = decode_args(c, batch, nullptr, cache, w);
     HIP_TRY(launch_cache_fill(c->dtype, k, v, st.k_summary ? st.k_summary : lw.att.ksum, batch, seq_len,
-                              c->n_kv_heads, c->head_dim, c->block_size, cdiv(seq_len, c->block_size), da, s),
+                              c->n_kv_heads, c->head_dim, c->block_size, cdiv(seq_len, c->block_size), da, s,
+                              g.prefill_cache == nullptr),
             "cache fill");
   }
   GemmArgs og = {};

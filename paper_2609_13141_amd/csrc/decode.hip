@@ -69,8 +69,8 @@ __global__ void summary_copy_kernel(const T* __restrict__ ksum, int b, int Hkv, 
 }
 
 hipError_t launch_cache_fill(int dtype, const void* K, const void* V, const void* ksum, int b, int n, int Hkv,
-                             int dh, int B, int NB, const DecodeArgs& c, hipStream_t s) {
-  const size_t total = (size_t)b * n * Hkv * (dh / 8);
+                             int dh, int B, int NB, const DecodeArgs& c, hipStream_t s, bool kv) {
+  const size_t total = kv ? (size_t)b * n * Hkv * (dh / 8) : 0;
   const int nfull = n / B;
   const size_t stot = (size_t)b * Hkv * nfull * dh;
   if (dtype == SAS_BF16) {

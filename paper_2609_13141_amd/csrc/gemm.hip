@@ -32,6 +32,10 @@ struct GemmParams {
   const int32_t* row_pos;
   int group_m;       // M tiles per group of the tile order (0: M-fastest over all tiles, no XCD remap)
   int n_off, n_cnt;  // gemm_bf16_lds_kernel: logical columns [n_off, n_off + n_cnt) of this launch
+  // prefill cache write of the staged QKV epilogue (NULL k_pages: none)
+  bf16_t* k_pages;
+  bf16_t* v_pages;
+  PageGeom geom;
 };
 
 // Tile of workgroup `bid`.  Workgroups are dispatched round-robin over the 8
@@ -525,8 +529,21 @@ __device__ __forceinline__ void gemm_epilogue_lds(
             }
           }
           dst += (size_t)row * ld;
-          *(uint4*)dst = pack8_bf16(x1);
-          *(uint4*)(dst + hh) = pack8_bf16(x2);
+          const uint4 w1 = pack8_bf16(x1), w2 = pack8_bf16(x2);
+          *(uint4*)dst = w1;
+          *(uint4*)(dst + hh) = w2;
+          if (P.k_pages && hd >= P.H) {
+            // the same K/V values into the paged cache: sequence row / seq_len,
+            // position row % seq_len (positions without a page are skipped)
+            const bool isk = hd < P.H + P.Hkv;
+            const int g = isk ? hd - P.H : hd - P.H - P.Hkv;
+            const long long off = P.geom.offset(row / P.seq_len, g, row % P.seq_len, P.Hkv, P.dh);
+            if (off >= 0) {
+              bf16_t* pg = (isk ? P.k_pages : P.v_pages) + off + ir;
+              *(uint4*)pg = w1;
+              *(uint4*)(pg + hh) = w2;
+            }
+          }
         }
       }
     }
@@ -770,7 +787,15 @@ static bool staged_epilogue_shape(const GemmParams& P) {
 
 static bool attrs_done = false;
 
+bool gemm_fills_cache(int dtype, const GemmArgs& g) {
+  // the staged epilogue of the LDS kernels (every bf16 launch with K % 64 == 0 and the
+  // fast epilogue shape below), with rows at their sequence positions
+  return dtype == SAS_BF16 && g.epi == EPI_QKV_ROPE && g.K % 64 == 0 && !g.row_pos && g.seq_len > 0 &&
+         (g.N / 2) % 8 == 0 && g.head_dim % 16 == 0;
+}
+
 hipError_t launch_gemm(int dtype, const GemmArgs& g, hipStream_t s) {
+  if (g.prefill_cache && !gemm_fills_cache(dtype, g)) return hipErrorInvalidValue;
   if (g.M <= 0) return hipSuccess;
   // pair epilogues: SWIGLU has F pairs, QKV has (H + 2 Hkv) dh / 2 pairs
   const int npairs = g.epi == EPI_SWIGLU ? g.N : (g.epi == EPI_QKV_ROPE ? g.N / 2 : 0);
@@ -815,6 +840,11 @@ hipError_t launch_gemm(int dtype, const GemmArgs& g, hipStream_t s) {
   P.seq_len = g.seq_len;
   P.rope = g.rope;
   P.row_pos = g.row_pos;
+  P.k_pages = g.prefill_cache ? (bf16_t*)g.prefill_cache->k_pages : nullptr;
+  P.v_pages = g.prefill_cache ? (bf16_t*)g.prefill_cache->v_pages : nullptr;
+  P.geom = g.prefill_cache ? PageGeom{g.prefill_cache->block_table, g.prefill_cache->num_pages,
+                                      g.prefill_cache->page_size, g.prefill_cache->max_pages}
+                           : PageGeom{nullptr, 0, 1, 0};
   const long big_tiles = (long)((g.M + 255) / 256) * ((nlog + 255) / 256);
   if (g.epi == EPI_F32OUT) return hipErrorInvalidValue;  // bf16 fp32-output products go through gemv
   if (g.K % 64 == 0) {

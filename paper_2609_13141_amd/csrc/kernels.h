@@ -80,8 +80,15 @@ struct GemmArgs {
   const struct DecodeArgs* append;
   // decode (launch_gemv): the product's weights in the packed decode layout, or NULL
   const void* packed;
+  // prefill (launch_gemm, EPI_QKV_ROPE, row_pos NULL): also write the K/V rows
+  // into the paged cache, row r being position r % seq_len of sequence
+  // r / seq_len (only where gemm_fills_cache holds), or NULL
+  const struct DecodeArgs* prefill_cache;
 };
 hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s);
+// Does launch_gemm write the K/V pages of `a.prefill_cache` itself (the bf16
+// staged QKV epilogue)?  Otherwise the caller fills the cache.
+bool gemm_fills_cache(int dtype, const GemmArgs& a);
 
 // ---- gemv.hip --------------------------------------------------------------
 // The same products for M <= 16 rows (bf16, K % 128 == 0), streaming the
@@ -287,10 +294,12 @@ struct PageGeom {
     return (((long long)page * Hkv + g) * ps + (p % ps)) * dh;
   }
 };
-// Writes K/V of positions 0..n-1 of every sequence into the pages and copies
-// the complete-block summaries into the summary cache.
+// Writes K/V of positions 0..n-1 of every sequence into the pages (unless
+// `kv` is false: the QKV product wrote them) and copies the complete-block
+// summaries into the summary cache.
 hipError_t launch_cache_fill(int dtype, const void* K, const void* V, const void* ksum, int b, int n,
-                             int Hkv, int dh, int B, int NB, const DecodeArgs& c, hipStream_t s);
+                             int Hkv, int dh, int B, int NB, const DecodeArgs& c, hipStream_t s,
+                             bool kv = true);
 // q [b, H, dh], k/v [b, Hkv, dh] of the new tokens -> append + summary.
 hipError_t launch_kv_append(int dtype, const void* k, const void* v, const DecodeArgs& c,
                             void* kplain_scratch, hipStream_t s);
