@@ -153,21 +153,38 @@ def test_decode_wide_blocks_match_oracle(dt, page):
     print(f"  {nd} rows differ from the oracle's own selection, each at a near-tie", flush=True)
 
 
-def test_cache_holds_prefill_keys_values_and_summaries():
-    w = W_(seq_len=70, index=76)
+@pytest.mark.parametrize("dt,d", [("bf16", 256), ("bf16", 224), ("f32", 256)],
+                         ids=["bf16-qkv-epilogue", "bf16-fill-kernel", "f32-fill-kernel"])
+def test_cache_holds_prefill_keys_values_and_summaries(dt, d):
+    # The pages hold the prefill's K/V rows bit for bit, whether the QKV
+    # product's epilogue wrote them (bf16, d % 64 == 0) or the fill kernel did
+    # (d = 224, fp32); a position whose page is unmapped (-1) writes nothing.
+    w = W_(seq_len=70, index=76, dtype=dt, d_model=d)
     x = inputs.embeddings(w)
-    Wd = sas.weights_to_device(inputs.layer_weights(w), "bf16")
+    Wd = sas.weights_to_device(inputs.layer_weights(w), dt)
     cfg = sas.make_config(w, "dense")
     cache = sas.alloc_cache(cfg, w.batch, 80, page_size=8, seed=5)
-    out = sas.layer_forward(cfg, sas.to_device(x, "bf16"), Wd, taps=True, k_summary=True, cache=cache)
+    sentinel = 3.0
+    cache.k_pages.fill_(sentinel)
+    cache.v_pages.fill_(sentinel)
+    bt0 = cache.block_table.cpu().numpy().copy()
+    dropped = [(0, 2), (w.batch - 1, 5)]  # (sequence, page index) left unmapped
+    for bi, pi in dropped:
+        cache.block_table[bi, pi] = -1
+    out = sas.layer_forward(cfg, sas.to_device(x, dt), Wd, taps=True, k_summary=True, cache=cache)
     torch.cuda.synchronize()
     bt = cache.block_table.cpu().numpy()
     kp, vp = cache.k_pages.cpu(), cache.v_pages.cpu()
     for bi in range(w.batch):
         for t in range(w.seq_len):
             page, slot = bt[bi, t // 8], t % 8
-            assert torch.equal(kp[page, :, slot], out["k"][bi, t].cpu())
-            assert torch.equal(vp[page, :, slot], out["v"][bi, t].cpu())
+            if page < 0:
+                continue
+            assert torch.equal(kp[page, :, slot], out["k"][bi, t].cpu()), (bi, t)
+            assert torch.equal(vp[page, :, slot], out["v"][bi, t].cpu()), (bi, t)
+    for bi, pi in dropped:
+        page = bt0[bi, pi]
+        assert bool((kp[page] == sentinel).all()) and bool((vp[page] == sentinel).all()), (bi, pi)
     nfull = w.seq_len // w.block_size
     assert torch.equal(cache.k_summary[:, :, :nfull].cpu(), out["k_summary"][:, :, :nfull].cpu())
 
