@@ -189,8 +189,10 @@ __device__ __forceinline__ void sel_fma4(double (&r)[8], double k0, double k1, d
 #undef SEL_DIM0
 #undef SEL_F
 
+// Lists of up to 16 slots: three waves per SIMD (a few values spill, and the
+// third wave hides more of the merge and load latency than they cost).
 template <typename T, int DH, int KMAX, int SEL_MC, bool NOISY>
-__global__ void __launch_bounds__(SEL_NW * WAVE) select_kernel(SelectArgs P) {
+__global__ void __launch_bounds__(SEL_NW * WAVE, KMAX <= 16 ? 3 : 2) select_kernel(SelectArgs P) {
   static_assert((KMAX & (KMAX - 1)) == 0, "the merge network needs a power-of-two list");
   static_assert(SEL_MC == 8 && DH % 16 == 0, "chunks of 8 summaries, 16-dimension groups");
   // a list exchange region: [KMAX][WAVE] keys, [KMAX][WAVE] blocks, [WAVE]
