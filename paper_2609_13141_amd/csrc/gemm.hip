@@ -834,7 +834,9 @@ hipError_t launch_gemm(int dtype, const GemmArgs& g, hipStream_t s) {
   P.H = g.n_heads;
   P.Hkv = g.n_kv_heads;
   P.dh = g.head_dim;
-  P.group_m = 8;
+  // tile order: groups of 8 M tiles; the long-K residual product (the MLP's
+  // down projection, K > 2N) runs faster with groups of 2 (measured 4-5%)
+  P.group_m = (g.epi == EPI_RESID && g.K > 2 * nlog) ? 2 : 8;
   P.n_off = 0;
   P.n_cnt = nlog;
   P.seq_len = g.seq_len;
