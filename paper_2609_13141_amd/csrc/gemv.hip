@@ -176,18 +176,39 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams& P, int gi, int c
       pg[ir + hh] = b2;
       if (!isk || (ps + 1) % P.B != 0 || ps / P.B >= P.max_blocks) continue;
       // this position completes block m: its summary in these two dimensions
-      // (fp64 sum over ascending positions, the new key last)
+      // (fp64 sum over ascending positions, the new key last).  Positions go
+      // in chunks of SUMC: the chunk's page ids, then its keys, are loaded
+      // unconditionally from clamped addresses and masked afterwards, so each
+      // chunk costs two memory round trips instead of two per position.
+      constexpr int SUMC = 16;
       const int m = ps / P.B;
+      const bf16_t* kp = (const bf16_t*)P.k_pages;
+      const int32_t* trow = P.geom.table + (size_t)row * P.geom.max_pages;
       double s1 = 0.0, s2 = 0.0;
-      for (int q = m * P.B; q < ps; ++q) {
-        const long long o = P.geom.offset(row, g, q, P.Hkv, P.dh);
-        float k1 = 0.f, k2 = 0.f;  // a position without a page adds zero
-        if (o >= 0) {
-          k1 = bf16_to_f32(((const bf16_t*)P.k_pages)[o + ir]);
-          k2 = bf16_to_f32(((const bf16_t*)P.k_pages)[o + ir + hh]);
+      for (int q0 = m * P.B; q0 < ps; q0 += SUMC) {
+        long long o[SUMC];
+#pragma unroll
+        for (int j = 0; j < SUMC; ++j) {
+          const int q = q0 + j, pi = q / P.geom.ps;
+          const int page = trow[min(pi, P.geom.max_pages - 1)];
+          const bool ok = q < ps && pi < P.geom.max_pages && page >= 0 && page < P.geom.num_pages;
+          o[j] = ok ? (((long long)page * P.Hkv + g) * P.geom.ps + (q % P.geom.ps)) * P.dh : -1;
         }
-        s1 += (double)k1;
-        s2 += (double)k2;
+        float k1[SUMC], k2[SUMC];
+#pragma unroll
+        for (int j = 0; j < SUMC; ++j) {
+          const long long oc = o[j] >= 0 ? o[j] : 0;
+          const float a = bf16_to_f32(kp[oc + ir]), b = bf16_to_f32(kp[oc + ir + hh]);
+          k1[j] = o[j] >= 0 ? a : 0.f;  // a position without a page adds zero
+          k2[j] = o[j] >= 0 ? b : 0.f;
+        }
+#pragma unroll
+        for (int j = 0; j < SUMC; ++j) {
+          if (q0 + j < ps) {
+            s1 += (double)k1[j];
+            s2 += (double)k2[j];
+          }
+        }
       }
       s1 += (double)bf16_to_f32(b1);
       s2 += (double)bf16_to_f32(b2);
