@@ -569,29 +569,37 @@ __global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restric
   __syncthreads();
 
   const int ns = s1 - s0;
-  // segment t of the split into S; t >= ns gives an empty segment (count 0,
-  // loads of the pool's start), so that every call issues the same loads
+  // segment t of the split into S.  Every load is issued unconditionally,
+  // also for segments without keys (past the split's end, or past the
+  // position in the current block): loads under a branch, even a uniform
+  // one, make the compiler wait for all loads in flight.  Keys past the count
+  // reload the segment's last key (lines the same instruction reads anyway);
+  // segments without keys and keys without a page reload the workgroup's own
+  // query slice (cached, and different for every workgroup: padding loads of
+  // one shared address from every workgroup crowd a few L2 channels).  ok
+  // masks them all.
+  const T* qpad = q + ((size_t)i * c.H + g * G + min(hc * GMAX, G - 1)) * DH + sl * 8;
   auto load = [&](Seg& S, int t) {
     const bool live = t < ns;
+    const int cnt = live ? sm_count[t] : 0;
+    S.count = cnt;
     const int sg = s0 + (live ? t : 0), chl = (sg >> spb_shift) - ch0;
     const int base = (sg & (spb - 1)) * seg_len;  // the segment's first key within its block
-    S.count = live ? sm_count[t] : 0;
-    // offsets first, then every load unconditionally (keys without a page read
-    // the start of the pool and are masked by ok): loads under divergent
-    // branches make the compiler wait for all loads in flight before each one
     size_t off[IT];
+    bool use[IT];
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
       const int kl = kq + KPI * it;
-      const int a = base + kl;  // key within the block
-      const int page = kl < S.count ? sm_pages[chl * ppb + (a >> pshift)] : -1;
-      S.ok[it] = page >= 0;
-      off[it] = S.ok[it] ? (size_t)page * kvstride + (uint32_t)(((g << pshift) + (a & (ps - 1))) * DH + sl * 8) : 0;
+      const int a = base + max(0, min(kl, cnt - 1));  // key within the block
+      const int page = sm_pages[chl * ppb + (a >> pshift)];
+      use[it] = cnt > 0 && page >= 0;
+      S.ok[it] = kl < cnt && use[it];
+      off[it] = (size_t)(use[it] ? page : 0) * kvstride + (uint32_t)(((g << pshift) + (a & (ps - 1))) * DH + sl * 8);
     }
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
-      S.k[it].load((const T*)c.k_pages + off[it]);
-      S.v[it].load((const T*)c.v_pages + off[it]);
+      S.k[it].load(use[it] ? (const T*)c.k_pages + off[it] : qpad);
+      S.v[it].load(use[it] ? (const T*)c.v_pages + off[it] : qpad);
     }
   };
 
@@ -688,6 +696,8 @@ __global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restric
   // two segments in registers: the next one's loads are in flight while one
   // is computed.  Loads and computes are unconditional (empty segments past
   // the end), so the compiler's waits count exactly the other buffer's loads.
+  // (A third segment in flight, which the registers allow with one head per
+  // workgroup, was slower: 32 -> 37 us at batch 8, 7B shape.)
   Seg sa, sb;
   load(sa, wave);
   for (int t = wave; t < ns; t += 2 * NW) {
