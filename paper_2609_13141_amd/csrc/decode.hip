@@ -485,14 +485,14 @@ template <typename T, int DH>
 struct DecodeSeg {
   static constexpr int NC = DH / 8;                          // lanes per key
   static constexpr int KPI = 64 / NC;                        // keys per load instruction
-  static constexpr int SEG = 8192 / (DH * (int)sizeof(T));   // keys per segment: K and V in 64 VGPRs
+  static constexpr int SEG = 4096 / (DH * (int)sizeof(T));   // keys per segment: K and V in 32 VGPRs
   static constexpr int IT = SEG / KPI;                       // load steps per segment
   Vec8<T> k[IT], v[IT];
   bool ok[IT];
   int count;
 };
 
-constexpr int DSEG_MAX = 33 * 8;   // segments of a split: (K + 1) blocks of at most 8 segments
+constexpr int DSEG_MAX = 33 * 16;  // segments of a split: (K + 1) blocks of at most 16 segments
 constexpr int DPAGE_MAX = 33 * 64;  // page ids of a split: (K + 1) blocks of at most 64 pages
 
 // Sum over groups of NC consecutive lanes (NC = 8 or 16) with DPP moves:
@@ -696,8 +696,9 @@ __global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restric
   // two segments in registers: the next one's loads are in flight while one
   // is computed.  Loads and computes are unconditional (empty segments past
   // the end), so the compiler's waits count exactly the other buffer's loads.
-  // (A third segment in flight, which the registers allow with one head per
-  // workgroup, was slower: 32 -> 37 us at batch 8, 7B shape.)
+  // (Measured at batch 8, 7B shape, per layer step: segments of 16 keys
+  // 30.8 us, of 8 keys 31.4, of 32 keys 31.9; a third segment of 32 keys in
+  // flight 37 us: more bytes in flight per wave make the stream slower.)
   Seg sa, sb;
   load(sa, wave);
   for (int t = wave; t < ns; t += 2 * NW) {
