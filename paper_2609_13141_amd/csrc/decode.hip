@@ -108,10 +108,32 @@ __global__ void kv_append_kernel(const T* __restrict__ k, const T* __restrict__ 
   if ((p + 1) % c.B != 0) return;
   const int m = p / c.B;
   if (m >= c.max_blocks) return;
+  // positions in chunks of SUMC: the chunk's page ids, then its keys, loaded
+  // unconditionally from clamped addresses and masked afterwards (two memory
+  // round trips per chunk instead of two per position); the fp64 sum keeps
+  // the ascending order
+  constexpr int SUMC = 16;
+  const T* kp = (const T*)c.k_pages;
+  const int32_t* trow = c.block_table + (size_t)i * c.max_pages;
   double acc = 0.0;
-  for (int q = m * c.B; q < p; ++q) {
-    const long long o = G.offset(i, g, q, c.Hkv, c.dh);
-    acc += (double)Act<T>::to_f32(o >= 0 ? ((const T*)c.k_pages)[o + j] : Act<T>::from_f32(0.f));
+  for (int q0 = m * c.B; q0 < p; q0 += SUMC) {
+    long long o[SUMC];
+#pragma unroll
+    for (int u = 0; u < SUMC; ++u) {
+      const int q = q0 + u, pi = q / c.page_size;
+      const int page = trow[min(pi, c.max_pages - 1)];
+      const bool ok = q < p && pi < c.max_pages && page >= 0 && page < c.num_pages;
+      o[u] = ok ? (((long long)page * c.Hkv + g) * c.page_size + (q % c.page_size)) * c.dh : -1;
+    }
+    float kq[SUMC];
+#pragma unroll
+    for (int u = 0; u < SUMC; ++u) {
+      const float x = Act<T>::to_f32(kp[(o[u] >= 0 ? o[u] : 0) + j]);
+      kq[u] = o[u] >= 0 ? x : 0.f;  // a position without a page adds zero
+    }
+#pragma unroll
+    for (int u = 0; u < SUMC; ++u)
+      if (q0 + u < p) acc += (double)kq[u];
   }
   acc += (double)Act<T>::to_f32(kv);
   T* dst = kplain ? kplain + ((size_t)i * c.Hkv + g) * c.dh
