@@ -206,7 +206,10 @@ typedef struct {
  *                   block_table[i][p / page_size], slot p % page_size
  *  k_summary        [b, Hkv, max_blocks, dh] selector key summaries of the
  *                   complete SAS blocks (after w_gk)
- *  block_size must be a multiple of page_size. */
+ *  block_size must be a multiple of page_size.  A page id outside
+ *  [0, num_pages) (e.g. -1) marks an unmapped page: writes to its positions
+ *  are dropped, they add zero to their block's summary, and the decode
+ *  attention leaves their keys out (as if the selection had not kept them). */
 typedef struct {
   void* k_pages;
   void* v_pages;

@@ -682,7 +682,7 @@ __global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restric
         acc = S.ok[it] ? acc : 0.f;
         acc = lane_group_sum<NC>(acc);
         if constexpr (BF) acc *= c.sm_scale;
-        sc[it] = kq + KPI * it < S.count ? acc : -INFINITY;
+        sc[it] = S.ok[it] ? acc : -INFINITY;  // keys past the count or without a page take no part
         mx = fmaxf(mx, sc[it]);
       }
       mx = wave_max(mx);
@@ -695,7 +695,7 @@ __global__ void __launch_bounds__(NW * 64) decode_attn_kernel(const T* __restric
       for (int e = 0; e < 8; ++e) o[hg][e] *= scale;
 #pragma unroll
       for (int it = 0; it < IT; ++it) {
-        const float pk = any && kq + KPI * it < S.count ? __expf(sc[it] - mn) : 0.f;
+        const float pk = any && S.ok[it] ? __expf(sc[it] - mn) : 0.f;
         l[hg] += pk;
         // keys without data read arbitrary bytes: their values are zeroed
         // (the probability alone would give 0 x NaN)

@@ -10,7 +10,7 @@ import oracle
 from paper_2609_13141_amd import configs, inputs, sas
 
 from oracle.selector import select
-from helpers import TOL, assert_close, cache_keys, check_decode_selection, f64, spec_of
+from helpers import TOL, assert_close, cache_keys, check_decode_selection, f64, rel_err, spec_of
 
 pytestmark = pytest.mark.gpu
 
@@ -215,3 +215,54 @@ def test_embed_and_lm_head_argmax():
     for r in range(2):
         if gap[r] > 2 * err:
             assert tok[r].item() == otok[r]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_decode_leaves_out_keys_of_unmapped_pages(dt):
+    # A selected block whose pages are unmapped (page id -1) takes no part in
+    # the decode attention: the step equals the oracle's sparse attention with
+    # that block dropped from the selection (the selection itself still keeps
+    # it: the block summaries are not in the pages).
+    w = W_(dtype=dt, index=81)
+    n0, t = 64, 64
+    print(f"\n[case] decode with an unmapped selected block {dt}", flush=True)
+    x = inputs.embeddings(w)
+    Wl = inputs.layer_weights(w)
+    OW = _oracle_W(Wl)
+    Wd = sas.weights_to_device(Wl, dt)
+    xd = sas.to_device(x, dt)
+    cfg_d = sas.make_config(w, "sparse")
+    cache = sas.alloc_cache(cfg_d, w.batch, w.seq_len, page_size=16, seed=9)
+    sas.layer_forward(sas.make_config(w, "dense"), xd[:, :n0].contiguous(), Wd, stats=False, cache=cache)
+    sp = spec_of(w, "sparse")
+    ocache = oracle.DecodeCache(w.batch, w.seq_len, sp)
+    pre = oracle.layer_forward(f64(x[:, :n0]), OW, spec_of(w, "dense"))
+    for bi in range(w.batch):
+        ocache.fill_prefill(bi, pre["K"][bi], pre["V"][bi], pre["k_summary"][bi])
+    _, selo, qo = oracle.decode_step(f64(x[:, t]), np.full(w.batch, t), OW, ocache, sp, taps=True)
+    m_star = int(selo[0, 0, 0])
+    assert m_star >= 0
+    for pi in range(m_star * w.block_size // 16, (m_star + 1) * w.block_size // 16):
+        cache.block_table[0, pi] = -1
+    pos = torch.full((w.batch,), t, dtype=torch.int32, device="cuda")
+    _, sel, tp = sas.decode_step(cfg_d, xd[:, t].contiguous(), pos, Wd, cache, taps=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(sel.cpu().numpy()[0], selo[0])
+
+    def h1_ref(s):  # sequence 0's residual after the attention, for selection s [Hkv, K]
+        O, _, _ = oracle.sas_attention(qo[0][None], ocache.K[0, :t + 1], ocache.V[0, :t + 1], w.block_size,
+                                       "sparse", sp.dtype, sel=s[:, None, :], rows=np.array([t]),
+                                       sm_scale=sp.sm_scale)
+        return oracle.rho(f64(x[0, t]) + O.reshape(-1) @ OW["wo"].T, sp.dtype)
+
+    dropped = selo[0].copy()
+    dropped[dropped == m_star] = -1
+    # fp32 compares the attention's part of the residual (h1 - x, a fiftieth
+    # of h1 here); bf16 compares h1 itself, whose rounding would swamp h1 - x
+    x0 = f64(x[0, t]) if dt == "f32" else 0.0
+    got = tp["h1"][0].float().cpu().numpy().astype(np.float64) - x0
+    e_drop = rel_err(got, h1_ref(dropped) - x0)
+    e_keep = rel_err(got, h1_ref(selo[0]) - x0)
+    print(f"  rel err {e_drop:.2e} against the block left out, {e_keep:.2e} against it kept", flush=True)
+    assert e_drop <= (1e-4 if dt == "f32" else TOL["bf16"])
+    assert e_keep > 3 * e_drop
