@@ -85,20 +85,28 @@ __global__ void __launch_bounds__(256) argmax_stage1(const float* __restrict__ l
   }
 }
 
-__global__ void argmax_stage2(const float* __restrict__ pv, const int32_t* __restrict__ pi, int slices,
-                              int32_t* __restrict__ tokens, int b) {
-  const int row = blockIdx.x * blockDim.x + threadIdx.x;
-  if (row >= b) return;
+// one wave per row: lane l takes slices l, l + 64, ... (the reduction under
+// better_of does not depend on the order: larger value, then lower index)
+__global__ void __launch_bounds__(64) argmax_stage2(const float* __restrict__ pv, const int32_t* __restrict__ pi,
+                                                    int slices, int32_t* __restrict__ tokens) {
+  const size_t row = blockIdx.x;
   float v = -INFINITY;
   int idx = 0x7fffffff;
-  for (int s2 = 0; s2 < slices; ++s2) better_of(v, idx, pv[(size_t)row * slices + s2], pi[(size_t)row * slices + s2]);
-  tokens[row] = idx;
+  for (int s2 = threadIdx.x; s2 < slices; s2 += 64) better_of(v, idx, pv[row * slices + s2], pi[row * slices + s2]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float v2 = __shfl_xor(v, o, 64);
+    const int i2 = __shfl_xor(idx, o, 64);
+    better_of(v, idx, v2, i2);
+  }
+  if (threadIdx.x == 0) tokens[row] = idx;
 }
 
 hipError_t launch_argmax(const float* logits, int b, int V, float* pv, int32_t* pi, int slices, int32_t* tokens,
                          hipStream_t s) {
+  if (b <= 0) return hipSuccess;
   argmax_stage1<<<dim3(slices, b), 256, 0, s>>>(logits, V, slices, pv, pi);
-  argmax_stage2<<<cdiv(b, 64), 64, 0, s>>>(pv, pi, slices, tokens, b);
+  argmax_stage2<<<b, 64, 0, s>>>(pv, pi, slices, tokens);
   return hipGetLastError();
 }
 
