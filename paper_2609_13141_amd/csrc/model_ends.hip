@@ -31,8 +31,19 @@ __global__ void __launch_bounds__(256) embed_kernel(const int32_t* __restrict__ 
     const int slot = part[0] + part[1] + part[2] + part[3];
     if (img && slot < n_img) src = img + ((size_t)bi * n_img + slot) * d;
   }
-  T* dst = x + ((size_t)bi * n + t) * d;
-  for (int j = threadIdx.x; j < d; j += 256) dst[j] = src ? src[j] : Act<T>::from_f32(0.f);
+  // 16-byte chunks (d is a multiple of 8, so rows are 16-byte aligned), up to
+  // four per thread loaded before any is stored
+  uint4* dst = (uint4*)(x + ((size_t)bi * n + t) * d);
+  const uint4* s16 = (const uint4*)src;
+  const int nch = d * (int)sizeof(T) / 16;
+  for (int c0 = threadIdx.x; c0 < nch; c0 += 4 * 256) {
+    uint4 r[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) r[u] = src ? s16[min(c0 + u * 256, nch - 1)] : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (c0 + u * 256 < nch) dst[c0 + u * 256] = r[u];
+  }
 }
 
 hipError_t launch_embed(int dtype, int b, int n, const int32_t* ids, const void* table, int vocab, const void* img,
