@@ -16,9 +16,11 @@
 namespace sas {
 
 // ---------------------------------------------------------------------------
-// Block summaries: thread per (b, g, m, 8-dim chunk); the B keys of the block
-// are read 16 at a time (independent 16-byte loads) and summed per dimension
-// in fp64 in ascending token order.
+// Block summaries: thread per (b, m, g, 8-dim chunk), the chunk fastest and
+// then the KV head, so that a load instruction reads a contiguous stretch of
+// one key row (Hkv * dh values per position); the B keys of the block are
+// read 16 at a time (independent 16-byte loads) and summed per dimension in
+// fp64 in ascending token order.
 template <typename T>
 __global__ void summaries_kernel(const T* __restrict__ K, T* __restrict__ out, int n, int Hkv, int dh,
                                  int B, int NB, size_t total) {
@@ -27,10 +29,10 @@ __global__ void summaries_kernel(const T* __restrict__ K, T* __restrict__ out, i
   const int nc = dh / 8;
   const int c8 = (int)(idx % nc);
   size_t r = idx / nc;
-  const int m = (int)(r % NB);
-  r /= NB;
   const int g = (int)(r % Hkv);
-  const int bi = (int)(r / Hkv);
+  r /= Hkv;
+  const int m = (int)(r % NB);
+  const int bi = (int)(r / NB);
   T* o = out + (((size_t)bi * Hkv + g) * NB + m) * dh + c8 * 8;
   if ((m + 1) * B > n) {  // incomplete block: no summary
 #pragma unroll
