@@ -75,23 +75,37 @@ __global__ void project_kernel(const T* __restrict__ in, const T* __restrict__ W
 }
 
 // Gate query qhat[b, g, t, j] = rho(sum over the group's heads of Q[b, t, h, j]),
-// fp64 sum in ascending head order: thread per (b, g, t, j).
+// fp64 sum in ascending head order: thread per (b, g, t, 8-dim chunk), with
+// 16-byte loads and stores.
 template <typename T>
 __global__ void gate_query_kernel(const T* __restrict__ Q, T* __restrict__ out, int n, int H, int Hkv, int dh,
-                                  size_t total) {
-  size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= total) return;
-  const int j = (int)(idx % dh);
-  size_t r = idx / dh;
+                                  size_t chunks) {
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= chunks) return;
+  const int nc = dh / 8;
+  const int c8 = (int)(idx % nc);
+  size_t r = idx / nc;
   const int t = (int)(r % n);
   r /= n;
   const int g = (int)(r % Hkv);
   const int bi = (int)(r / Hkv);
   const int G = H / Hkv;
-  const T* q = Q + (((size_t)bi * n + t) * H + (size_t)g * G) * dh + j;
-  double acc = 0.0;
-  for (int h = 0; h < G; ++h) acc += (double)Act<T>::to_f32(q[(size_t)h * dh]);
-  out[idx] = Act<T>::from_f64(acc);
+  const T* q = Q + (((size_t)bi * n + t) * H + (size_t)g * G) * dh + c8 * 8;
+  double acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+  for (int h = 0; h < G; ++h) {
+    Vec8<T> v;
+    v.load(q + (size_t)h * dh);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] += (double)v.get(e);
+  }
+  alignas(16) T res[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) res[e] = Act<T>::from_f64(acc[e]);
+  uint4* o = (uint4*)(out + idx * 8);  // [b, Hkv, n, dh]: chunk idx
+#pragma unroll
+  for (int k = 0; k < (int)(8 * sizeof(T) / 16); ++k) o[k] = ((const uint4*)res)[k];
 }
 
 hipError_t launch_gate_query(int dtype, const void* Q, int b, int n, int H, int Hkv, int dh, const void* w_gq,
@@ -99,11 +113,13 @@ hipError_t launch_gate_query(int dtype, const void* Q, int b, int n, int H, int 
   const size_t total = (size_t)b * Hkv * n * dh;
   if (total == 0) return hipSuccess;
   const unsigned grid = (unsigned)((total + 255) / 256);
+  const size_t chunks = total / 8;  // dh is a multiple of 8
+  const unsigned cgrid = (unsigned)((chunks + 255) / 256);
   void* dst = w_gq ? qplain : qhat;
   if (dtype == SAS_BF16)
-    gate_query_kernel<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)Q, (bf16_t*)dst, n, H, Hkv, dh, total);
+    gate_query_kernel<bf16_t><<<cgrid, 256, 0, s>>>((const bf16_t*)Q, (bf16_t*)dst, n, H, Hkv, dh, chunks);
   else
-    gate_query_kernel<float><<<grid, 256, 0, s>>>((const float*)Q, (float*)dst, n, H, Hkv, dh, total);
+    gate_query_kernel<float><<<cgrid, 256, 0, s>>>((const float*)Q, (float*)dst, n, H, Hkv, dh, chunks);
   if (w_gq) {
     if (dtype == SAS_BF16)
       project_kernel<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)qplain, (const bf16_t*)w_gq, (bf16_t*)qhat,
